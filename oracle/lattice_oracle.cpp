@@ -1,0 +1,508 @@
+// Plain, slow CPU oracle for the permutohedral-lattice hot path of LatticeNet
+// (Rosu, Schuett, Quenzel, Behnke, "LatticeNet: Fast Point Cloud
+// Segmentation Using Permutohedral Lattices", arXiv:1912.05905).
+//
+// TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+// CPU-baseline leg of the benchmark may load this library.  It shares no code,
+// header or constant with the GPU path.
+//
+// Design: std::map lattice keyed by integer coordinates, scalar loops,
+// features accumulated in double.  Vertices are numbered in lexicographic
+// key order (std::map order).  The embedding of a point (elevation, rounding,
+// ranking, barycentric weights) is done in float32 with a fixed order of
+// single roundings, because the vertex set it produces is a discontinuous
+// function of that arithmetic; the paper fixes no precision for it.
+//
+// Sources followed:
+//  * Notation: lattice V = (C, X), cloud P = (G, F), I_p, J_v (Notation).
+//  * Lattice: projection of (d+1)Z^{d+1} along 1 onto H_d, coordinates sum
+//    to zero, 2(d+1) neighbours at +-[-1..d..-1] (Permutohedral Lattice).
+//  * Enclosing simplex by rounding: the paper defers to Baek and Adams; the
+//    construction used is the closest-remainder-0-point / rank / sum-fix
+//    method of Adams, Baek and Davis, "Fast High-Dimensional Filtering Using
+//    the Permutohedral Lattice", Eurographics 2010, Sec. 3, restated here
+//    from the mathematics.
+//  * Scale G/sigma (Method), Splat Eq. (splat), Convolve (1-hop, missing
+//    neighbour = 0, Fig. convolve), Slice Eq. (slice), Downsample and
+//    Upsample (Proposed Operations), DeformSlice Eq. (deformSlice) with the
+//    permutation-equivariant offset regressor.
+//
+// Readings of points the paper leaves open (each listed in the design notes):
+//  * Elevation basis and scale: the isometric basis of H_d scaled by
+//    (d+1)*sqrt(2/3), with fixed float32 operation order.
+//  * Rounding ties go to the lower multiple of d+1; equal differentials rank
+//    the lower coordinate index first.
+//  * Simplex vertex k is the remainder-k vertex (consistent enumeration).
+//  * Zero-weight vertices are inserted (|I_p| = d+1 always).
+//  * Splat: sum of b*f, optionally divided by the sum of b (0/0 -> 0).
+//  * Tap order 0 = self, 1..d+1 = +n_j, d+2..2d+2 = -n_j, n_j = (d+1)e_j - 1;
+//    weights laid out W[tap][c_in][c_out].
+//  * Coarse lattices come from the points with positions halved per level.
+//  * Upsample: tap t of fine vertex f reads coarse vertex (f + o_t)/2 only
+//    when that is a lattice point (all coordinates even and the halves
+//    congruent mod d+1); every other tap, the centre included, is ignored.
+//  * DeformSlice: max per channel over all d+1 weighted vertex values (the
+//    vertex itself included), nonlinearity tanh.
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <vector>
+
+namespace {
+
+constexpr int kDim = 3;              // d: dimension of the points
+constexpr int kD1 = kDim + 1;        // d+1: lattice coordinates and simplex vertices
+constexpr int kTaps = 2 * kD1 + 1;   // 1-hop neighbourhood incl. the centre
+constexpr int32_t kCoordLimit = 1 << 20;
+
+enum { OK = 0, EINVAL_ = -1, EUNSUPPORTED = -2, ENOMEM_ = -3, EHASHFULL = -4,
+       EKEYRANGE = -5, ENONFINITE = -6, EDEVICE = -7, ELEVEL = -8 };
+
+using Key = std::array<int32_t, kD1>;
+
+struct Lattice {
+  int64_t m = 0;
+  int level = 0;
+  std::vector<float> y;                 // m x (d+1) elevated positions (float32)
+  std::map<Key, int64_t> index;         // key -> vertex number (lexicographic)
+  std::vector<Key> keys;                // vertex number -> key
+  std::vector<int64_t> idx;             // m x (d+1) simplex vertices of each point
+  std::vector<float> bary;              // m x (d+1) barycentric weights
+  const Lattice* parent = nullptr;      // finer lattice this one was coarsened from
+};
+
+// ---------------------------------------------------------------------------
+// Embedding of one point (float32, every line a single rounding).
+// ---------------------------------------------------------------------------
+
+// Per-axis factor a_j = s / (sigma_j * sqrt((j+1)(j+2))), s = (d+1) sqrt(2/3):
+// scaling by 1/sigma (Method) folded into the isometric basis of H_d.
+// Evaluated in double and rounded once to float32.
+void axis_factors(const float* sigma, float a[kDim]) {
+  const double s = (kDim + 1) * std::sqrt(2.0 / 3.0);
+  for (int j = 0; j < kDim; ++j)
+    a[j] = static_cast<float>(s / (static_cast<double>(sigma[j]) * std::sqrt(static_cast<double>((j + 1) * (j + 2)))));
+}
+
+// y = E (g / sigma) with E's columns orthonormal and orthogonal to 1, so
+// y lies in H_d (coordinates sum to zero).  Column j of E has
+// 1/sqrt((j+1)(j+2)) in rows 0..j and -(j+1)/sqrt((j+1)(j+2)) in row j+1.
+void elevate(const float g[kDim], const float a[kDim], float y[kD1]) {
+  float t[kDim];
+  for (int j = 0; j < kDim; ++j) t[j] = g[j] * a[j];
+  float run = 0.0f;                     // sum of t_j over j >= i
+  for (int i = kDim; i >= 1; --i) {
+    const float it = static_cast<float>(i) * t[i - 1];
+    y[i] = run - it;
+    run = run + t[i - 1];
+  }
+  y[0] = run;
+}
+
+// Enclosing simplex of y: the d+1 vertex keys (vertex k has every coordinate
+// congruent to k mod d+1) and the barycentric weights b_k.
+void enclosing_simplex(const float y[kD1], Key vert[kD1], float b[kD1]) {
+  const float inv = 1.0f / static_cast<float>(kD1);   // exact for d = 3
+  const float step = static_cast<float>(kD1);
+  // nearest point of (d+1)Z per coordinate; a tie goes to the lower one
+  int32_t base[kD1];
+  int32_t total = 0;
+  for (int i = 0; i < kD1; ++i) {
+    const float lo = std::floor(y[i] * inv) * step;
+    const float hi = lo + step;
+    const float up = hi - y[i];
+    const float down = y[i] - lo;
+    base[i] = static_cast<int32_t>(up < down ? hi : lo);
+    total += base[i];
+  }
+  const int32_t excess = total / kD1;  // base lies on H_d iff excess == 0
+  float diff[kD1];
+  for (int i = 0; i < kD1; ++i) diff[i] = y[i] - static_cast<float>(base[i]);
+  // rank: 0 for the largest differential; ties rank the lower index first
+  int rank[kD1];
+  for (int i = 0; i < kD1; ++i) {
+    rank[i] = 0;
+    for (int j = 0; j < kD1; ++j)
+      if (diff[j] > diff[i] || (diff[j] == diff[i] && j < i)) ++rank[i];
+  }
+  // move base onto H_d: shift the |excess| coordinates whose differentials
+  // are most extreme by d+1, which rotates the ranks
+  if (excess > 0) {
+    for (int i = 0; i < kD1; ++i) {
+      if (rank[i] >= kD1 - excess) { base[i] -= kD1; rank[i] += excess - kD1; }
+      else rank[i] += excess;
+    }
+  } else if (excess < 0) {
+    for (int i = 0; i < kD1; ++i) {
+      if (rank[i] < -excess) { base[i] += kD1; rank[i] += kD1 + excess; }
+      else rank[i] += excess;
+    }
+  }
+  // sorted scaled differentials z_0 >= ... >= z_d
+  float z[kD1];
+  for (int i = 0; i < kD1; ++i) z[rank[i]] = (y[i] - static_cast<float>(base[i])) * inv;
+  b[0] = 1.0f - (z[0] - z[kDim]);
+  for (int k = 1; k < kD1; ++k) b[k] = z[kDim - k] - z[kDim - k + 1];
+  // vertex k: base + k*1, minus (d+1) on the k coordinates of smallest
+  // differential (the k highest ranks)
+  for (int k = 0; k < kD1; ++k)
+    for (int i = 0; i < kD1; ++i)
+      vert[k][i] = base[i] + k - (rank[i] > kDim - k ? kD1 : 0);
+}
+
+bool key_in_range(const Key& c) {
+  for (int i = 0; i < kD1; ++i)
+    if (c[i] >= kCoordLimit || c[i] <= -kCoordLimit) return false;
+  return true;
+}
+
+// Offsets of the 1-hop taps: o_0 = 0, o_{1+j} = +n_j, o_{d+2+j} = -n_j,
+// with n_j = (d+1) e_j - 1.
+Key tap_offset(int t) {
+  Key o{};
+  if (t == 0) return o;
+  const int j = (t - 1) % kD1;
+  const int sign = t <= kD1 ? 1 : -1;
+  for (int i = 0; i < kD1; ++i) o[i] = sign * ((i == j ? kD1 : 0) - 1);
+  return o;
+}
+
+// Build the lattice of m points given their elevated positions.
+int build_from_elevated(Lattice* L) {
+  const int64_t m = L->m;
+  std::vector<Key> pv(static_cast<size_t>(m) * kD1);
+  L->bary.assign(static_cast<size_t>(m) * kD1, 0.0f);
+  for (int64_t p = 0; p < m; ++p) {
+    const float* y = &L->y[static_cast<size_t>(p) * kD1];
+    for (int i = 0; i < kD1; ++i) {
+      if (!std::isfinite(y[i])) return ENONFINITE;
+      if (std::fabs(y[i]) >= 2.0f * kCoordLimit) return EKEYRANGE;  // keys would leave the range
+    }
+    enclosing_simplex(y, &pv[static_cast<size_t>(p) * kD1], &L->bary[static_cast<size_t>(p) * kD1]);
+    for (int k = 0; k < kD1; ++k) {
+      const Key& c = pv[static_cast<size_t>(p) * kD1 + k];
+      if (!key_in_range(c)) return EKEYRANGE;
+      L->index.emplace(c, 0);
+    }
+  }
+  int64_t next = 0;
+  L->keys.reserve(L->index.size());
+  for (auto& kv : L->index) { kv.second = next++; L->keys.push_back(kv.first); }
+  L->idx.resize(static_cast<size_t>(m) * kD1);
+  for (size_t e = 0; e < pv.size(); ++e) L->idx[e] = L->index.at(pv[e]);
+  return OK;
+}
+
+int64_t find_vertex(const Lattice* L, const Key& c) {
+  if (!key_in_range(c)) return -1;
+  auto it = L->index.find(c);
+  return it == L->index.end() ? -1 : it->second;
+}
+
+// Neighbour table of a lattice (n x taps); -1 = vertex not allocated.
+std::vector<int64_t> same_level_table(const Lattice* L) {
+  const int64_t n = static_cast<int64_t>(L->keys.size());
+  std::vector<int64_t> nb(static_cast<size_t>(n) * kTaps);
+  for (int64_t v = 0; v < n; ++v)
+    for (int t = 0; t < kTaps; ++t) {
+      Key c = L->keys[v];
+      const Key o = tap_offset(t);
+      for (int i = 0; i < kD1; ++i) c[i] += o[i];
+      nb[static_cast<size_t>(v) * kTaps + t] = find_vertex(L, c);
+    }
+  return nb;
+}
+
+// Downsample: coarse vertex c reads the fine vertices at 2c + o_t (the coarse
+// lattice embedded in the fine one by scaling by 2).
+std::vector<int64_t> down_table(const Lattice* coarse, const Lattice* fine) {
+  const int64_t n = static_cast<int64_t>(coarse->keys.size());
+  std::vector<int64_t> nb(static_cast<size_t>(n) * kTaps);
+  for (int64_t v = 0; v < n; ++v)
+    for (int t = 0; t < kTaps; ++t) {
+      Key c = coarse->keys[v];
+      const Key o = tap_offset(t);
+      for (int i = 0; i < kD1; ++i) c[i] = 2 * c[i] + o[i];
+      nb[static_cast<size_t>(v) * kTaps + t] = find_vertex(fine, c);
+    }
+  return nb;
+}
+
+// Upsample: fine vertex f reads the coarse vertex (f + o_t)/2 when that is a
+// lattice point; fractional neighbours contribute nothing.
+std::vector<int64_t> up_table(const Lattice* fine, const Lattice* coarse) {
+  const int64_t n = static_cast<int64_t>(fine->keys.size());
+  std::vector<int64_t> nb(static_cast<size_t>(n) * kTaps);
+  for (int64_t v = 0; v < n; ++v)
+    for (int t = 0; t < kTaps; ++t) {
+      Key u = fine->keys[v];
+      const Key o = tap_offset(t);
+      bool lattice_point = true;
+      for (int i = 0; i < kD1; ++i) {
+        u[i] += o[i];
+        if (u[i] % 2 != 0) lattice_point = false;
+      }
+      int64_t found = -1;
+      if (lattice_point) {
+        Key h;
+        for (int i = 0; i < kD1; ++i) h[i] = u[i] / 2;
+        const int r0 = ((h[0] % kD1) + kD1) % kD1;
+        for (int i = 1; i < kD1; ++i)
+          if (((h[i] % kD1) + kD1) % kD1 != r0) lattice_point = false;
+        if (lattice_point) found = find_vertex(coarse, h);
+      }
+      nb[static_cast<size_t>(v) * kTaps + t] = found;
+    }
+  return nb;
+}
+
+// Y[v] = bias + sum_t sum_c X[nb[v][t]][c] W[t][c][:], missing taps add 0.
+void conv_with_table(const std::vector<int64_t>& nb, const double* X, int64_t ldx, int cin,
+                     const double* W, const double* bias, int cout, int relu,
+                     const int64_t* rows, int64_t nrows, double* Y, int64_t ldy) {
+  std::vector<double> acc(cout);
+  for (int64_t r = 0; r < nrows; ++r) {
+    const int64_t v = rows ? rows[r] : r;
+    for (int o = 0; o < cout; ++o) acc[o] = bias ? bias[o] : 0.0;
+    for (int t = 0; t < kTaps; ++t) {
+      const int64_t u = nb[static_cast<size_t>(v) * kTaps + t];
+      if (u < 0) continue;
+      for (int c = 0; c < cin; ++c) {
+        const double x = X[u * ldx + c];
+        const double* wrow = W + (static_cast<int64_t>(t) * cin + c) * cout;
+        for (int o = 0; o < cout; ++o) acc[o] += x * wrow[o];
+      }
+    }
+    for (int o = 0; o < cout; ++o) {
+      double val = acc[o];
+      if (relu && val < 0.0) val = 0.0;
+      Y[r * ldy + o] = val;
+    }
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+typedef struct Lattice orc_lattice;
+
+// Per-axis elevation factors (for pins).
+void orc_axis_factors(const float* sigma, float* a) { axis_factors(sigma, a); }
+
+// Elevate m points: pos m x d, sigma d -> y m x (d+1).
+int orc_elevate(const float* pos, int64_t m, const float* sigma, float* y) {
+  if (!pos || !sigma || !y || m < 0) return EINVAL_;
+  float a[kDim];
+  axis_factors(sigma, a);
+  for (int64_t p = 0; p < m; ++p) elevate(pos + p * kDim, a, y + p * kD1);
+  return OK;
+}
+
+// Enclosing simplices of m elevated points: keys m x (d+1) x (d+1), w m x (d+1).
+int orc_simplex(const float* y, int64_t m, int32_t* keys, float* w) {
+  if (!y || !keys || !w || m < 0) return EINVAL_;
+  for (int64_t p = 0; p < m; ++p) {
+    Key vert[kD1];
+    enclosing_simplex(y + p * kD1, vert, w + p * kD1);
+    for (int k = 0; k < kD1; ++k)
+      for (int i = 0; i < kD1; ++i) keys[(p * kD1 + k) * kD1 + i] = vert[k][i];
+  }
+  return OK;
+}
+
+// Lattice of a cloud: positions m x d (float32), sigma d.
+int orc_create(const float* pos, int64_t m, int d, const float* sigma, orc_lattice** out) {
+  if (!out) return EINVAL_;
+  *out = nullptr;
+  if (d != kDim) return EUNSUPPORTED;
+  if (m < 0 || (m > 0 && !pos) || !sigma) return EINVAL_;
+  for (int j = 0; j < kDim; ++j)
+    if (!(sigma[j] > 0.0f) || !std::isfinite(sigma[j])) return EINVAL_;
+  for (int64_t e = 0; e < m * kDim; ++e)
+    if (!std::isfinite(pos[e])) return ENONFINITE;
+  Lattice* L = new Lattice();
+  L->m = m;
+  L->y.resize(static_cast<size_t>(m) * kD1);
+  orc_elevate(pos, m, sigma, L->y.data());
+  const int st = build_from_elevated(L);
+  if (st != OK) { delete L; return st; }
+  *out = L;
+  return OK;
+}
+
+// Next-coarser lattice: the same points with elevated positions halved
+// (equivalently, positions divided by 2).
+int orc_coarsen(const orc_lattice* fine, orc_lattice** out) {
+  if (!fine || !out) return EINVAL_;
+  Lattice* L = new Lattice();
+  L->m = fine->m;
+  L->level = fine->level + 1;
+  L->parent = fine;
+  L->y.resize(fine->y.size());
+  for (size_t e = 0; e < fine->y.size(); ++e) L->y[e] = fine->y[e] * 0.5f;
+  const int st = build_from_elevated(L);
+  if (st != OK) { delete L; return st; }
+  *out = L;
+  return OK;
+}
+
+void orc_destroy(orc_lattice* L) { delete L; }
+int64_t orc_num_vertices(const orc_lattice* L) { return static_cast<int64_t>(L->keys.size()); }
+int64_t orc_num_points(const orc_lattice* L) { return L->m; }
+int orc_level(const orc_lattice* L) { return L->level; }
+
+void orc_export_elevated(const orc_lattice* L, float* y) {
+  std::memcpy(y, L->y.data(), L->y.size() * sizeof(float));
+}
+
+void orc_export_keys(const orc_lattice* L, int32_t* keys) {
+  for (size_t v = 0; v < L->keys.size(); ++v)
+    for (int i = 0; i < kD1; ++i) keys[v * kD1 + i] = L->keys[v][i];
+}
+
+void orc_export_simplices(const orc_lattice* L, int64_t* idx, float* w) {
+  std::memcpy(idx, L->idx.data(), L->idx.size() * sizeof(int64_t));
+  std::memcpy(w, L->bary.data(), L->bary.size() * sizeof(float));
+}
+
+void orc_export_neighbors(const orc_lattice* L, int64_t* nbr) {
+  const auto nb = same_level_table(L);
+  std::memcpy(nbr, nb.data(), nb.size() * sizeof(int64_t));
+}
+
+void orc_export_down_table(const orc_lattice* coarse, int64_t* nbr) {
+  const auto nb = down_table(coarse, coarse->parent);
+  std::memcpy(nbr, nb.data(), nb.size() * sizeof(int64_t));
+}
+
+void orc_export_up_table(const orc_lattice* coarse, int64_t* nbr) {
+  const auto nb = up_table(coarse->parent, coarse);
+  std::memcpy(nbr, nb.data(), nb.size() * sizeof(int64_t));
+}
+
+// Splat, Eq. (splat): x_v = sum_{p in J_v} b_pv f_p; wsum_v = sum b_pv.
+// normalize != 0 divides by wsum (weighted average), 0 where wsum == 0.
+int orc_splat(const orc_lattice* L, const double* F, int C, int normalize, double* X, double* wsum) {
+  if (!L || C <= 0 || (L->m > 0 && !F) || !X) return EINVAL_;
+  const int64_t n = static_cast<int64_t>(L->keys.size());
+  std::vector<double> ws(n, 0.0);
+  std::fill(X, X + n * C, 0.0);
+  for (int64_t p = 0; p < L->m; ++p)
+    for (int k = 0; k < kD1; ++k) {
+      const int64_t v = L->idx[p * kD1 + k];
+      const double b = L->bary[p * kD1 + k];
+      ws[v] += b;
+      for (int c = 0; c < C; ++c) X[v * C + c] += b * F[p * C + c];
+    }
+  if (normalize)
+    for (int64_t v = 0; v < n; ++v)
+      for (int c = 0; c < C; ++c) X[v * C + c] = ws[v] > 0.0 ? X[v * C + c] / ws[v] : 0.0;
+  if (wsum) std::copy(ws.begin(), ws.end(), wsum);
+  return OK;
+}
+
+// Convolution.  dst == src: 1-hop convolution over the 2(d+1)+1 vertices.
+// dst coarsened from src: strided convolution (Downsample).  rows (optional)
+// selects the output vertices computed; Y then holds nrows rows.
+int orc_conv(const orc_lattice* dst, const orc_lattice* src, const double* X, int64_t ldx, int cin,
+             const double* W, const double* bias, int cout, int relu,
+             const int64_t* rows, int64_t nrows, double* Y, int64_t ldy) {
+  if (!dst || !src || !X || !W || !Y || cin <= 0 || cout <= 0) return EINVAL_;
+  std::vector<int64_t> nb;
+  if (dst == src) nb = same_level_table(dst);
+  else if (dst->parent == src) nb = down_table(dst, src);
+  else return ELEVEL;
+  if (!rows) nrows = static_cast<int64_t>(dst->keys.size());
+  conv_with_table(nb, X, ldx, cin, W, bias, cout, relu, rows, nrows, Y, ldy);
+  return OK;
+}
+
+// Upsample (transposed convolution) from coarse to its parent fine lattice.
+int orc_refine(const orc_lattice* fine, const orc_lattice* coarse, const double* X, int64_t ldx, int cin,
+               const double* W, const double* bias, int cout, int relu,
+               const int64_t* rows, int64_t nrows, double* Y, int64_t ldy) {
+  if (!fine || !coarse || !X || !W || !Y || cin <= 0 || cout <= 0) return EINVAL_;
+  if (coarse->parent != fine) return ELEVEL;
+  const auto nb = up_table(fine, coarse);
+  if (!rows) nrows = static_cast<int64_t>(fine->keys.size());
+  conv_with_table(nb, X, ldx, cin, W, bias, cout, relu, rows, nrows, Y, ldy);
+  return OK;
+}
+
+// Slice, Eq. (slice), on explicit simplices: out_p = sum_k w_pk X[idx_pk].
+void orc_slice_raw(const double* X, int64_t ldx, int C, const int64_t* idx, const float* w,
+                   int64_t m, const int64_t* pts, double* out) {
+  for (int64_t r = 0; r < m; ++r) {
+    const int64_t p = pts ? pts[r] : r;
+    for (int c = 0; c < C; ++c) {
+      double acc = 0.0;
+      for (int k = 0; k < kD1; ++k)
+        acc += static_cast<double>(w[p * kD1 + k]) * X[idx[p * kD1 + k] * ldx + c];
+      out[r * C + c] = acc;
+    }
+  }
+}
+
+// DeformSlice, Eq. (deformSlice) with the equivariant offset regressor:
+//   q_k = b_k x_k,  M = max_k q_k (per channel),
+//   db_k = tanh(beta + (q_k - M) . wv),  out = sum_k (b_k + db_k) x_k.
+void orc_deform_slice_raw(const double* X, int64_t ldx, int C, const int64_t* idx, const float* w,
+                          int64_t m, const double* wv, double beta, const int64_t* pts,
+                          double* out, double* delta) {
+  std::vector<double> q(static_cast<size_t>(kD1) * C), mx(C);
+  for (int64_t r = 0; r < m; ++r) {
+    const int64_t p = pts ? pts[r] : r;
+    for (int k = 0; k < kD1; ++k)
+      for (int c = 0; c < C; ++c)
+        q[k * C + c] = static_cast<double>(w[p * kD1 + k]) * X[idx[p * kD1 + k] * ldx + c];
+    for (int c = 0; c < C; ++c) {
+      mx[c] = q[c];
+      for (int k = 1; k < kD1; ++k) mx[c] = std::max(mx[c], q[k * C + c]);
+    }
+    double db[kD1];
+    for (int k = 0; k < kD1; ++k) {
+      double s = beta;
+      for (int c = 0; c < C; ++c) s += (q[k * C + c] - mx[c]) * wv[c];
+      db[k] = std::tanh(s);
+      if (delta) delta[r * kD1 + k] = db[k];
+    }
+    for (int c = 0; c < C; ++c) {
+      double acc = 0.0;
+      for (int k = 0; k < kD1; ++k)
+        acc += (static_cast<double>(w[p * kD1 + k]) + db[k]) * X[idx[p * kD1 + k] * ldx + c];
+      out[r * C + c] = acc;
+    }
+  }
+}
+
+int orc_slice(const orc_lattice* L, const double* X, int64_t ldx, int C,
+              const int64_t* pts, int64_t npts, double* out) {
+  if (!L || !X || !out || C <= 0) return EINVAL_;
+  orc_slice_raw(X, ldx, C, L->idx.data(), L->bary.data(), pts ? npts : L->m, pts, out);
+  return OK;
+}
+
+int orc_deform_slice(const orc_lattice* L, const double* X, int64_t ldx, int C, const double* wv,
+                     double beta, const int64_t* pts, int64_t npts, double* out, double* delta) {
+  if (!L || !X || !out || !wv || C <= 0) return EINVAL_;
+  orc_deform_slice_raw(X, ldx, C, L->idx.data(), L->bary.data(), pts ? npts : L->m, wv, beta,
+                       pts, out, delta);
+  return OK;
+}
+
+// Round to the nearest bfloat16 (8 significant bits), ties to even, in place.
+// Used where the bf16 pipeline stores activations; normal range only.
+void orc_round_bf16(double* x, int64_t n) {
+  for (int64_t e = 0; e < n; ++e) {
+    if (x[e] == 0.0 || !std::isfinite(x[e])) continue;
+    int ex = 0;
+    const double f = std::frexp(x[e], &ex);            // x = f * 2^ex, 0.5 <= |f| < 1
+    x[e] = std::ldexp(std::nearbyint(std::ldexp(f, 8)), ex - 8);
+  }
+}
+
+}  // extern "C"

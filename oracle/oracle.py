@@ -1,0 +1,251 @@
+"""ctypes wrapper of the CPU oracle (test infrastructure only).
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg use
+this module.  It takes numpy arrays on the host; features are float64.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_lib = None
+
+ERRORS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "ENOMEM", -4: "EHASHFULL",
+          -5: "EKEYRANGE", -6: "ENONFINITE", -7: "EDEVICE", -8: "ELEVEL"}
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code):
+        super().__init__(f"oracle returned {ERRORS.get(code, code)}")
+        self.code = code
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        L = C.CDLL(_build.LIB)
+        p, i64, i32, dbl = C.c_void_p, C.c_int64, C.c_int, C.c_double
+        sig = {
+            "orc_axis_factors": (None, [p, p]),
+            "orc_elevate": (i32, [p, i64, p, p]),
+            "orc_simplex": (i32, [p, i64, p, p]),
+            "orc_create": (i32, [p, i64, i32, p, C.POINTER(C.c_void_p)]),
+            "orc_coarsen": (i32, [p, C.POINTER(C.c_void_p)]),
+            "orc_destroy": (None, [p]),
+            "orc_num_vertices": (i64, [p]),
+            "orc_num_points": (i64, [p]),
+            "orc_level": (i32, [p]),
+            "orc_export_elevated": (None, [p, p]),
+            "orc_export_keys": (None, [p, p]),
+            "orc_export_simplices": (None, [p, p, p]),
+            "orc_export_neighbors": (None, [p, p]),
+            "orc_export_down_table": (None, [p, p]),
+            "orc_export_up_table": (None, [p, p]),
+            "orc_splat": (i32, [p, p, i32, i32, p, p]),
+            "orc_conv": (i32, [p, p, p, i64, i32, p, p, i32, i32, p, i64, p, i64]),
+            "orc_refine": (i32, [p, p, p, i64, i32, p, p, i32, i32, p, i64, p, i64]),
+            "orc_slice_raw": (None, [p, i64, i32, p, p, i64, p, p]),
+            "orc_deform_slice_raw": (None, [p, i64, i32, p, p, i64, p, dbl, p, p, p]),
+            "orc_slice": (i32, [p, p, i64, i32, p, i64, p]),
+            "orc_deform_slice": (i32, [p, p, i64, i32, p, dbl, p, i64, p, p]),
+            "orc_round_bf16": (None, [p, i64]),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _check(code):
+    if code != 0:
+        raise OracleError(code)
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def axis_factors(sigma) -> np.ndarray:
+    s = _f32(sigma)
+    a = np.zeros(3, np.float32)
+    lib().orc_axis_factors(_ptr(s), _ptr(a))
+    return a
+
+
+def elevate(pos, sigma) -> np.ndarray:
+    pos, sigma = _f32(pos), _f32(sigma)
+    y = np.zeros((pos.shape[0], 4), np.float32)
+    _check(lib().orc_elevate(_ptr(pos), pos.shape[0], _ptr(sigma), _ptr(y)))
+    return y
+
+
+def simplex(y):
+    """Enclosing simplex of elevated points: keys (m,4,4) int32, w (m,4) f32."""
+    y = _f32(y).reshape(-1, 4)
+    m = y.shape[0]
+    keys = np.zeros((m, 4, 4), np.int32)
+    w = np.zeros((m, 4), np.float32)
+    _check(lib().orc_simplex(_ptr(y), m, _ptr(keys), _ptr(w)))
+    return keys, w
+
+
+def round_bf16(x) -> np.ndarray:
+    a = np.array(x, dtype=np.float64, copy=True, order="C")
+    lib().orc_round_bf16(_ptr(a), a.size)
+    return a
+
+
+class Lattice:
+    """A lattice held by the oracle (std::map numbering = lexicographic keys)."""
+
+    def __init__(self, handle, parent=None):
+        self._h = handle
+        self.parent = parent
+        self.n = int(lib().orc_num_vertices(handle))
+        self.m = int(lib().orc_num_points(handle))
+        self.level = int(lib().orc_level(handle))
+
+    @classmethod
+    def create(cls, pos, sigma, d: int = 3):
+        pos, sigma = _f32(pos).reshape(-1, 3) if d == 3 else _f32(pos), _f32(sigma)
+        h = C.c_void_p()
+        _check(lib().orc_create(_ptr(pos), pos.shape[0], d, _ptr(sigma), C.byref(h)))
+        return cls(h)
+
+    def coarsen(self):
+        h = C.c_void_p()
+        _check(lib().orc_coarsen(self._h, C.byref(h)))
+        return Lattice(h, parent=self)
+
+    def __del__(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.orc_destroy(self._h)
+            self._h = None
+
+    # ---- structure ----
+    def elevated(self):
+        y = np.zeros((self.m, 4), np.float32)
+        lib().orc_export_elevated(self._h, _ptr(y))
+        return y
+
+    def keys(self):
+        k = np.zeros((self.n, 4), np.int32)
+        lib().orc_export_keys(self._h, _ptr(k))
+        return k
+
+    def simplices(self):
+        idx = np.zeros((self.m, 4), np.int64)
+        w = np.zeros((self.m, 4), np.float32)
+        lib().orc_export_simplices(self._h, _ptr(idx), _ptr(w))
+        return idx, w
+
+    def neighbors(self):
+        nb = np.zeros((self.n, 9), np.int64)
+        lib().orc_export_neighbors(self._h, _ptr(nb))
+        return nb
+
+    def down_table(self):
+        """For a coarsened lattice: fine vertex at 2c + o_t (n_coarse x 9)."""
+        nb = np.zeros((self.n, 9), np.int64)
+        lib().orc_export_down_table(self._h, _ptr(nb))
+        return nb
+
+    def up_table(self):
+        """For a coarsened lattice: coarse vertex read by each fine vertex and
+        tap (n_fine x 9)."""
+        nb = np.zeros((self.parent.n, 9), np.int64)
+        lib().orc_export_up_table(self._h, _ptr(nb))
+        return nb
+
+    # ---- ops ----
+    def splat(self, F, normalize=True):
+        F = _f64(F)
+        Cc = F.shape[1]
+        X = np.zeros((self.n, Cc), np.float64)
+        W = np.zeros(self.n, np.float64)
+        _check(lib().orc_splat(self._h, _ptr(F), Cc, int(bool(normalize)), _ptr(X), _ptr(W)))
+        return X, W
+
+    def conv(self, src: "Lattice", X, W, bias=None, relu=False, rows=None):
+        """dst = self.  src is self (1-hop conv) or self.parent (strided)."""
+        X, W = _f64(X), _f64(W)
+        cin, cout = W.shape[1], W.shape[2]
+        assert X.shape[1] == cin
+        b = None if bias is None else _f64(bias)
+        r = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+        nr = self.n if r is None else r.shape[0]
+        Y = np.zeros((nr, cout), np.float64)
+        _check(lib().orc_conv(self._h, src._h, _ptr(X), cin, cin, _ptr(W), _ptr(b), cout,
+                              int(bool(relu)), _ptr(r), nr, _ptr(Y), cout))
+        return Y
+
+    def refine_into(self, coarse: "Lattice", X, W, bias=None, relu=False, rows=None):
+        """Upsample coarse (a coarsening of self) values X to self."""
+        X, W = _f64(X), _f64(W)
+        cin, cout = W.shape[1], W.shape[2]
+        assert X.shape[1] == cin
+        b = None if bias is None else _f64(bias)
+        r = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+        nr = self.n if r is None else r.shape[0]
+        Y = np.zeros((nr, cout), np.float64)
+        _check(lib().orc_refine(self._h, coarse._h, _ptr(X), cin, cin, _ptr(W), _ptr(b), cout,
+                                int(bool(relu)), _ptr(r), nr, _ptr(Y), cout))
+        return Y
+
+    def slice(self, X, pts=None):
+        X = _f64(X)
+        Cc = X.shape[1]
+        p = None if pts is None else np.ascontiguousarray(pts, dtype=np.int64)
+        npt = self.m if p is None else p.shape[0]
+        out = np.zeros((npt, Cc), np.float64)
+        _check(lib().orc_slice(self._h, _ptr(X), Cc, Cc, _ptr(p), npt, _ptr(out)))
+        return out
+
+    def deform_slice(self, X, wv, beta, pts=None):
+        X, wv = _f64(X), _f64(wv)
+        Cc = X.shape[1]
+        p = None if pts is None else np.ascontiguousarray(pts, dtype=np.int64)
+        npt = self.m if p is None else p.shape[0]
+        out = np.zeros((npt, Cc), np.float64)
+        delta = np.zeros((npt, 4), np.float64)
+        _check(lib().orc_deform_slice(self._h, _ptr(X), Cc, Cc, _ptr(wv), float(beta), _ptr(p), npt,
+                                      _ptr(out), _ptr(delta)))
+        return out, delta
+
+
+def slice_raw(X, idx, w):
+    X = _f64(X)
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    w = _f32(w)
+    m, Cc = idx.shape[0], X.shape[1]
+    out = np.zeros((m, Cc), np.float64)
+    lib().orc_slice_raw(_ptr(X), Cc, Cc, _ptr(idx), _ptr(w), m, None, _ptr(out))
+    return out
+
+
+def deform_slice_raw(X, idx, w, wv, beta):
+    X, wv = _f64(X), _f64(wv)
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    w = _f32(w)
+    m, Cc = idx.shape[0], X.shape[1]
+    out = np.zeros((m, Cc), np.float64)
+    delta = np.zeros((m, 4), np.float64)
+    lib().orc_deform_slice_raw(_ptr(X), Cc, Cc, _ptr(idx), _ptr(w), m, _ptr(wv), float(beta), None,
+                               _ptr(out), _ptr(delta))
+    return out, delta

@@ -1,0 +1,359 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test ties one part of the oracle to something other than itself: a
+hand-derived case, a closed form, an invariant stated in the paper, or a
+brute-force construction from the lattice definition (tests/bruteforce.py).
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+from tests import bruteforce as bf
+from workloads import configs, generators as gen
+from workloads.rng import Stream
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _tiny_cloud(seed, m=150, extent=1.0):
+    st = Stream(seed, "tiny")
+    return (extent * st.uniform(3 * m).reshape(m, 3)).astype(np.float32)
+
+
+# ----------------------------------------------------------------------------
+# embedding: hand-derived cases, closed forms, invariants
+# ----------------------------------------------------------------------------
+def test_golden_simplex_cases(oracle_mod):
+    """Hand-derived simplices (tie rules, faces, vertices of each class)."""
+    cases = json.load(open(os.path.join(GOLDEN, "simplex_cases.json")))["cases"]
+    Y = np.array([c["y"] for c in cases], np.float32)
+    keys, w = oracle_mod.simplex(Y)
+    for i, c in enumerate(cases):
+        assert keys[i].tolist() == c["keys"], c["derivation"]
+        assert w[i].tolist() == c["w"], c["derivation"]
+
+
+def test_keys_are_lattice_points_of_each_remainder(oracle_mod):
+    """Every key sums to zero and vertex k has all coordinates = k mod d+1
+    (Permutohedral Lattice section)."""
+    wl = configs.make(1)
+    y = oracle_mod.elevate(wl.positions, wl.sigma)
+    keys, w = oracle_mod.simplex(y)
+    assert (keys.sum(axis=2) == 0).all()
+    for k in range(4):
+        assert (np.mod(keys[:, k, :], 4) == k).all()
+
+
+def test_barycentric_weights_and_reconstruction(oracle_mod):
+    """b >= 0, sum b = 1 up to rounding, and sum_k b_k c_k = y."""
+    for cfg in (1, 2, 4):
+        wl = configs.make(cfg)
+        y = oracle_mod.elevate(wl.positions, wl.sigma)
+        keys, w = oracle_mod.simplex(y)
+        assert (w >= 0).all()
+        assert np.abs(w.astype(np.float64).sum(axis=1) - 1.0).max() <= 4 * np.finfo(np.float32).eps
+        rec = np.einsum("pk,pki->pi", w.astype(np.float64), keys.astype(np.float64))
+        scale = np.abs(y).max(axis=1, keepdims=True) + 1.0
+        assert (np.abs(rec - y) / scale).max() < 2e-6
+
+
+def test_point_on_a_vertex_gets_weight_one(oracle_mod):
+    """A point exactly on a lattice vertex of remainder k: b_k = 1 and
+    vertex k is that point."""
+    pts = bf.lattice_points_in_box(12)
+    keys, w = oracle_mod.simplex(pts.astype(np.float32))
+    rem = np.mod(pts[:, 0], 4)
+    for p in range(pts.shape[0]):
+        k = rem[p]
+        assert w[p, k] == 1.0
+        assert (keys[p, k] == pts[p]).all()
+
+
+def test_simplex_matches_exhaustive_search(oracle_mod):
+    """The rounding construction's simplex is the one an exhaustive search
+    over all Delaunay simplices finds, with the same barycentric weights."""
+    st = Stream(7, "bf-simplex")
+    g = st.uniform_range(3 * 60, -3.0, 3.0).reshape(60, 3).astype(np.float32)
+    y = oracle_mod.elevate(g, np.array([0.7, 0.9, 1.3], np.float32))
+    keys, w = oracle_mod.simplex(y)
+    for p in range(y.shape[0]):
+        cands = bf.candidate_simplices(y[p])
+        assert cands, "no simplex contains the point"
+        ok = False
+        for V, lam in cands:
+            order = np.argsort(np.mod(V[:, 0], 4))
+            if (V[order] == keys[p]).all():
+                assert np.abs(lam[order] - w[p]).max() < 1e-5
+                ok = True
+        assert ok
+
+
+def test_elevation_is_scaled_isometry_onto_hyperplane(oracle_mod):
+    """Elevation maps R^3 isometrically (times s = (d+1) sqrt(2/3)) onto H_d:
+    coordinates sum to 0 and pairwise distances scale by s/sigma."""
+    st = Stream(3, "iso")
+    g = st.uniform_range(3 * 200, -5, 5).reshape(200, 3).astype(np.float32)
+    sigma = np.array([0.5, 0.25, 2.0], np.float32)
+    y = oracle_mod.elevate(g, sigma).astype(np.float64)
+    assert np.abs(y.sum(axis=1)).max() < 1e-4
+    s = 4.0 * np.sqrt(2.0 / 3.0)
+    gs = g.astype(np.float64) / sigma.astype(np.float64)
+    dg = np.linalg.norm(gs[:, None] - gs[None], axis=2) * s
+    dy = np.linalg.norm(y[:, None] - y[None], axis=2)
+    assert np.abs(dg - dy).max() / dg.max() < 1e-6
+
+
+def test_neighbour_shell_of_the_lattice():
+    """The nearest lattice points of the origin are exactly the 2(d+1) vectors
+    +-[-1..d..-1] (Permutohedral Lattice section), at squared norm d(d+1)."""
+    pts = bf.lattice_points_in_box(8)
+    sq = (pts ** 2).sum(axis=1)
+    nonzero = sq > 0
+    nearest = pts[nonzero & (sq == sq[nonzero].min())]
+    assert sq[nonzero].min() == 12
+    assert sorted(map(tuple, nearest)) == sorted(map(tuple, bf.neighbour_vectors()))
+
+
+def test_error_codes(oracle_mod):
+    with pytest.raises(oracle_mod.OracleError) as e:
+        oracle_mod.Lattice.create(np.array([[0, np.nan, 0]], np.float32), np.ones(3, np.float32))
+    assert e.value.code == -6
+    with pytest.raises(oracle_mod.OracleError) as e:
+        oracle_mod.Lattice.create(np.array([[1e7, 0, 0]], np.float32), np.full(3, 0.1, np.float32))
+    assert e.value.code == -5
+    L = oracle_mod.Lattice.create(np.zeros((0, 3), np.float32), np.ones(3, np.float32))
+    assert L.n == 0 and L.m == 0
+
+
+# ----------------------------------------------------------------------------
+# lattice structure
+# ----------------------------------------------------------------------------
+def test_lattice_matches_bruteforce_construction(oracle_mod):
+    """Vertex set, numbering and per-point simplices equal those built from
+    the exhaustive simplex search (points strictly inside simplices)."""
+    pos = _tiny_cloud(11, 120, extent=0.6)
+    sigma = np.full(3, 0.1, np.float32)
+    L = oracle_mod.Lattice.create(pos, sigma)
+    y = L.elevated()
+    keys_b, _, idx_b, w_b = bf.brute_lattice(y)
+    assert (L.keys() == keys_b).all()
+    idx, w = L.simplices()
+    assert (idx == idx_b).all()
+    assert np.abs(w - w_b).max() < 1e-5
+
+
+def test_neighbours_match_pairwise_scan(oracle_mod):
+    for seed in (1, 2):
+        L = oracle_mod.Lattice.create(_tiny_cloud(seed, 200), np.full(3, 0.15, np.float32))
+        assert (L.neighbors() == bf.brute_neighbours(L.keys().astype(np.int64))).all()
+
+
+def test_coarse_level_equals_doubled_sigma(oracle_mod):
+    """Halving positions (Downsample) equals creating with 2*sigma, bitwise."""
+    wl = configs.make(2)
+    L0 = oracle_mod.Lattice.create(wl.positions, wl.sigma)
+    L1 = L0.coarsen()
+    L1b = oracle_mod.Lattice.create(wl.positions, 2 * wl.sigma)
+    assert (L1.keys() == L1b.keys()).all()
+    i1, w1 = L1.simplices()
+    i2, w2 = L1b.simplices()
+    assert (i1 == i2).all() and (w1 == w2).all()
+    assert L1.level == 1 and L1.n < L0.n
+
+
+def test_down_table_by_embedding(oracle_mod):
+    """Coarse vertex c reads the fine vertex at 2c + o_t (pairwise search)."""
+    L0 = oracle_mod.Lattice.create(_tiny_cloud(5, 200), np.full(3, 0.12, np.float32))
+    L1 = L0.coarsen()
+    kf, kc = L0.keys().astype(np.int64), L1.keys().astype(np.int64)
+    offs = bf.tap_offsets()
+    tab = L1.down_table()
+    for v in range(L1.n):
+        for t in range(9):
+            hit = np.nonzero((kf == 2 * kc[v] + offs[t]).all(axis=1))[0]
+            assert tab[v, t] == (hit[0] if hit.size else -1)
+
+
+# ----------------------------------------------------------------------------
+# operators
+# ----------------------------------------------------------------------------
+def test_splat_mass_and_constant(oracle_mod):
+    """Raw splat conserves sum_p f_p (weights sum to 1); the normalised splat
+    of a constant, sliced back, returns the constant."""
+    wl = configs.make(1)
+    L = oracle_mod.Lattice.create(wl.positions, wl.sigma)
+    F = wl.features.astype(np.float64)
+    X, W = L.splat(F, normalize=False)
+    assert np.allclose(X.sum(axis=0), F.sum(axis=0), rtol=1e-6, atol=1e-6)
+    assert abs(W.sum() - wl.m) < 1e-3
+    const = np.full((wl.m, 3), 2.5)
+    Xc, _ = L.splat(const, normalize=True)
+    assert np.abs(L.slice(Xc) - 2.5).max() < 1e-5
+
+
+def test_splat_matches_definition(oracle_mod):
+    pos = _tiny_cloud(12, 100, 0.5)
+    L = oracle_mod.Lattice.create(pos, np.full(3, 0.1, np.float32))
+    keys_b, index, idx_b, w_b = bf.brute_lattice(L.elevated())
+    F = np.random.default_rng(0).normal(size=(100, 5))
+    X = np.zeros((len(keys_b), 5))
+    Wb = np.zeros(len(keys_b))
+    for p in range(100):
+        for k in range(4):
+            X[idx_b[p, k]] += w_b[p, k] * F[p]
+            Wb[idx_b[p, k]] += w_b[p, k]
+    Xo, Wo = L.splat(F, normalize=False)
+    assert np.abs(Xo - X).max() < 1e-5 and np.abs(Wo - Wb).max() < 1e-5
+    Xn, _ = L.splat(F, normalize=True)
+    ref = np.where(Wb[:, None] > 0, X / np.where(Wb > 0, Wb, 1)[:, None], 0)
+    assert np.abs(Xn - ref).max() < 1e-4
+
+
+def test_slice_reproduces_affine_functions(oracle_mod):
+    """With x_v = c_v, slicing returns the elevated position (barycentric
+    interpolation reproduces affine functions)."""
+    wl = configs.make(1)
+    L = oracle_mod.Lattice.create(wl.positions, wl.sigma)
+    out = L.slice(L.keys().astype(np.float64))
+    assert np.abs(out - L.elevated()).max() < 2e-5
+
+
+def test_conv_identity_shift_and_definition(oracle_mod):
+    L = oracle_mod.Lattice.create(_tiny_cloud(21, 200), np.full(3, 0.12, np.float32))
+    keys = L.keys().astype(np.int64)
+    index = {tuple(k): i for i, k in enumerate(keys)}
+    rng = np.random.default_rng(1)
+    X = rng.normal(size=(L.n, 6))
+    W = np.zeros((9, 6, 6))
+    W[0] = np.eye(6)
+    assert np.abs(L.conv(L, X, W) - X).max() == 0
+    offs = bf.tap_offsets()
+    for t in range(1, 9):
+        W = np.zeros((9, 6, 6))
+        W[t] = np.eye(6)
+        Y = L.conv(L, X, W)
+        for v in range(L.n):
+            u = index.get(tuple(keys[v] + offs[t]))
+            assert np.array_equal(Y[v], X[u] if u is not None else np.zeros(6))
+    W = rng.normal(size=(9, 6, 4))
+    b = rng.normal(size=4)
+    ref = bf.brute_conv(keys, index, X, W) + b
+    assert np.abs(L.conv(L, X, W, bias=b) - ref).max() < 1e-12
+    assert np.abs(L.conv(L, X, W, bias=b, relu=True) - np.maximum(ref, 0)).max() < 1e-12
+    rows = np.array([3, 0, L.n - 1])
+    assert np.abs(L.conv(L, X, W, bias=b, rows=rows) - ref[rows]).max() < 1e-12
+
+
+def test_strided_conv_matches_definition(oracle_mod):
+    L0 = oracle_mod.Lattice.create(_tiny_cloud(22, 200), np.full(3, 0.12, np.float32))
+    L1 = L0.coarsen()
+    kf = L0.keys().astype(np.int64)
+    index_f = {tuple(k): i for i, k in enumerate(kf)}
+    rng = np.random.default_rng(2)
+    X = rng.normal(size=(L0.n, 5))
+    W = rng.normal(size=(9, 5, 3))
+    ref = bf.brute_conv(L1.keys().astype(np.int64), index_f, X, W, dst_scale=2)
+    assert np.abs(L1.conv(L0, X, W) - ref).max() < 1e-12
+
+
+def _mirror(t):
+    return 0 if t == 0 else (t + 4 if t <= 4 else t - 4)
+
+
+def test_refine_is_adjoint_of_coarsen(oracle_mod):
+    """Upsample is the transposed convolution of Downsample:
+    <coarsen_W(X), Z> = <X, refine_W'(Z)>, W'[t] = W[mirror t]^T."""
+    for seed, cfg_sigma in ((31, 0.12), (32, 0.07)):
+        L0 = oracle_mod.Lattice.create(_tiny_cloud(seed, 300), np.full(3, cfg_sigma, np.float32))
+        L1 = L0.coarsen()
+        rng = np.random.default_rng(seed)
+        X = rng.normal(size=(L0.n, 4))
+        Z = rng.normal(size=(L1.n, 3))
+        W = rng.normal(size=(9, 4, 3))
+        Wt = np.stack([W[_mirror(t)].T for t in range(9)])
+        lhs = np.sum(L1.conv(L0, X, W) * Z)
+        rhs = np.sum(X * L0.refine_into(L1, Z, Wt))
+        assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs)), (lhs, rhs)
+
+
+def test_refine_support_of_one_coarse_vertex(oracle_mod):
+    """A one-hot coarse vertex c reaches exactly the existing fine vertices
+    2c + o_t, through tap mirror(t)."""
+    L0 = oracle_mod.Lattice.create(_tiny_cloud(33, 300), np.full(3, 0.1, np.float32))
+    L1 = L0.coarsen()
+    kf, kc = L0.keys().astype(np.int64), L1.keys().astype(np.int64)
+    index_f = {tuple(k): i for i, k in enumerate(kf)}
+    offs = bf.tap_offsets()
+    for c in range(0, L1.n, max(1, L1.n // 15)):
+        Z = np.zeros((L1.n, 1))
+        Z[c] = 1.0
+        for t in range(9):
+            W = np.zeros((9, 1, 1))
+            W[_mirror(t)] = 1.0
+            Y = L0.refine_into(L1, Z, W)[:, 0]
+            expect = np.zeros(L0.n)
+            f = index_f.get(tuple(2 * kc[c] + offs[t]))
+            if f is not None:
+                expect[f] = 1.0
+            assert np.array_equal(Y, expect)
+
+
+def test_deform_slice_special_cases_and_equivariance(oracle_mod):
+    wl = configs.make(1)
+    L = oracle_mod.Lattice.create(wl.positions, wl.sigma)
+    rng = np.random.default_rng(3)
+    X = rng.normal(size=(L.n, 8))
+    zero = np.zeros(8)
+    out, delta = L.deform_slice(X, zero, 0.0)
+    assert np.array_equal(out, L.slice(X)) and not delta.any()
+    idx, w = L.simplices()
+    out, delta = L.deform_slice(X, zero, 0.3)
+    ref = L.slice(X) + np.tanh(0.3) * X[idx].sum(axis=1)
+    assert np.abs(out - ref).max() < 1e-12
+    wv = rng.normal(size=8)
+    o1, d1 = oracle_mod.deform_slice_raw(X, idx, w, wv, 0.1)
+    perm = np.array([2, 0, 3, 1])
+    o2, d2 = oracle_mod.deform_slice_raw(X, idx[:, perm], w[:, perm], wv, 0.1)
+    assert np.abs(o1 - o2).max() < 1e-12
+    assert np.abs(d1[:, perm] - d2).max() < 1e-15
+    # offsets by the definition for a few points
+    for p in (0, 17, 4095):
+        q = w[p, :, None].astype(np.float64) * X[idx[p]]
+        dd = np.tanh(0.1 + (q - q.max(axis=0)) @ wv)
+        assert np.abs(dd - d1[p]).max() < 1e-12
+        assert np.abs((w[p] + dd) @ X[idx[p]] - o1[p]).max() < 1e-12
+
+
+def test_end_to_end_bruteforce(oracle_mod):
+    """splat -> conv -> slice on a tiny cloud from brute-force definitions."""
+    pos = _tiny_cloud(41, 150, 0.8)
+    L = oracle_mod.Lattice.create(pos, np.full(3, 0.13, np.float32))
+    keys_b, index, idx_b, w_b = bf.brute_lattice(L.elevated())
+    rng = np.random.default_rng(4)
+    F = rng.normal(size=(150, 4))
+    W = rng.normal(size=(9, 4, 5))
+    X = np.zeros((len(keys_b), 4))
+    Ws = np.zeros(len(keys_b))
+    for p in range(150):
+        for k in range(4):
+            X[idx_b[p, k]] += w_b[p, k] * F[p]
+            Ws[idx_b[p, k]] += w_b[p, k]
+    X = np.where(Ws[:, None] > 0, X / np.where(Ws > 0, Ws, 1)[:, None], 0)
+    Y = bf.brute_conv(keys_b, index, X, W)
+    out = np.einsum("pk,pkc->pc", w_b, Y[idx_b])
+    Xo, _ = L.splat(F)
+    got = L.slice(L.conv(L, Xo, W))
+    assert np.abs(got - out).max() < 1e-4 * (1 + np.abs(out).max())
+
+
+def test_bf16_rounding(oracle_mod):
+    """Round to nearest even at 8 significant bits."""
+    x = np.array([1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -9, -3.14159, 0.0, 1e-3])
+    r = oracle_mod.round_bf16(x)
+    assert r[0] == 1.0 and r[1] == 1.0 and r[2] == 1.0 + 2 ** -6 and r[3] == 1.0
+    bits = gen.to_bf16_bits(x.astype(np.float32))
+    assert np.array_equal(gen.bf16_bits_to_f32(bits).astype(np.float64)[4:], r[4:])

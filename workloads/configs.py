@@ -1,0 +1,193 @@
+"""The five synthetic workloads and the lattice pipelines run on them.
+
+A workload is a seeded cloud plus a list of lattice operations (a small
+pipeline description).  The GPU runner and the oracle runner each interpret
+that list on their own; this module only describes inputs and the order of
+operations, it computes nothing of the method.
+
+Operations (fields in brackets):
+  create        [level=0]                 lattice of the cloud at scale sigma
+  coarsen       [level]                   lattice of the cloud at scale 2^level * sigma
+  splat         [dst, normalize]          point features -> level-0 vertex values
+  conv          [level, src, dst, w, relu]        1-hop convolution on one level
+  conv_down     [level, src, dst, w, relu]        strided convolution level-1 -> level
+  refine        [level, src, dst, w, relu]        transposed convolution level+1 -> level
+  slice         [level, src, out]                 vertex values -> points
+  deform_slice  [level, src, wv, beta, out]       DeformSlice to points
+`src`/`dst` are (buffer, first column, channels); buffers are row-major
+(vertices of their level) x (total channels), so several ops can write
+disjoint column ranges of one buffer (concatenation without a copy).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import generators as gen
+
+TAPS = 9  # 2(d+1)+1 vertices of the 1-hop neighbourhood for d = 3
+
+
+@dataclass
+class Workload:
+    cfg: int
+    name: str
+    seed: int
+    positions: np.ndarray            # m x 3 float32
+    sigma: np.ndarray                # 3 float32
+    dtype: str                       # "f32" or "bf16"
+    features: np.ndarray             # m x C float32 (already bf16-representable when dtype == bf16)
+    weights: dict = field(default_factory=dict)    # name -> float32 array
+    vectors: dict = field(default_factory=dict)    # DeformSlice weight vectors
+    buffers: dict = field(default_factory=dict)    # name -> (level, channels)
+    ops: list = field(default_factory=list)
+    levels: int = 1
+
+    @property
+    def m(self) -> int:
+        return int(self.positions.shape[0])
+
+
+def _round_bf16(x: np.ndarray) -> np.ndarray:
+    return gen.bf16_bits_to_f32(gen.to_bf16_bits(x))
+
+
+def _finish(wl: Workload) -> Workload:
+    if wl.dtype == "bf16":
+        wl.features = _round_bf16(wl.features)
+        wl.weights = {k: _round_bf16(v) for k, v in wl.weights.items()}
+    wl.levels = 1 + max([op["level"] for op in wl.ops if op["op"] == "coarsen"] + [0])
+    return wl
+
+
+def _conv(wl, kind, level, src, dst, relu, seed, std=None):
+    name = f"{kind}{level}_{src[0]}_{dst[0]}_{dst[1]}"
+    wl.weights[name] = gen.conv_weights(seed, name, TAPS, src[2], dst[2], std)
+    wl.ops.append(dict(op=kind, level=level, src=src, dst=dst, w=name, relu=relu))
+
+
+def config1(seed: int = 0, m: int = 4096) -> Workload:
+    """4,096 points uniform in the unit cube, sigma 0.1, 8 features N(0,1);
+    splat -> conv 8->16 (weights N(0, 0.1^2)) -> slice, fp32."""
+    pos = gen.uniform_cube(seed, m)
+    F = gen.normal_matrix(seed, "F", m, 8, 1.0)
+    wl = Workload(1, "uniform-cube", seed, pos, np.full(3, 0.1, np.float32), "f32", F)
+    wl.buffers = {"s0": (0, 8), "c0": (0, 16)}
+    wl.ops = [dict(op="create", level=0), dict(op="splat", dst=("s0", 0, 8), normalize=1)]
+    _conv(wl, "conv", 0, ("s0", 0, 8), ("c0", 0, 16), False, seed, std=0.1)
+    wl.ops.append(dict(op="slice", level=0, src=("c0", 0, 16), out="slice"))
+    return _finish(wl)
+
+
+def config2(seed: int = 1, m: int = 2048) -> Workload:
+    """ShapeNet-sized object (2,048 surface points), sigma 0.05, 32 features;
+    splat -> conv 32->64 -> coarsen (strided conv 64->64) -> conv 64->64 ->
+    slice at the coarse level, fp32."""
+    pos = gen.object_surfaces(seed, m)
+    F = gen.normal_matrix(seed, "F", m, 32, 1.0)
+    wl = Workload(2, "object", seed, pos, np.full(3, 0.05, np.float32), "f32", F)
+    wl.buffers = {"s0": (0, 32), "c0": (0, 64), "d1": (1, 64), "c1": (1, 64)}
+    wl.ops = [dict(op="create", level=0), dict(op="splat", dst=("s0", 0, 32), normalize=1)]
+    _conv(wl, "conv", 0, ("s0", 0, 32), ("c0", 0, 64), True, seed)
+    wl.ops.append(dict(op="coarsen", level=1))
+    _conv(wl, "conv_down", 1, ("c0", 0, 64), ("d1", 0, 64), True, seed)
+    _conv(wl, "conv", 1, ("d1", 0, 64), ("c1", 0, 64), False, seed)
+    wl.ops.append(dict(op="slice", level=1, src=("c1", 0, 64), out="slice"))
+    return _finish(wl)
+
+
+def _room_features(seed, pos, channels, st_name="rgb"):
+    st = gen.Stream(seed, st_name)
+    rgb = st.uniform(3 * pos.shape[0]).reshape(-1, 3)
+    raw = np.concatenate([pos.astype(np.float64), rgb], axis=1)
+    return gen.lifted_features(seed, raw, channels)
+
+
+def _deform_vector(wl, seed, C, name="deform"):
+    wl.vectors[name] = (gen.normal_matrix(seed, "wv:" + name, 1, C, 1.0 / np.sqrt(C))[0], 0.1)
+
+
+def config3(seed: int = 2, m: int = 200_000) -> Workload:
+    """ScanNet-sized room (200k points, 8x8x3 m, 20 boxes, 1 cm noise),
+    xyz+RGB lifted to 64 channels, sigma 0.05 m; splat -> conv 64->64 ->
+    slice and DeformSlice, fp32."""
+    pos = gen.room(seed, m, (8.0, 8.0, 3.0), 20, 0.01)
+    F = _room_features(seed, pos, 64)
+    wl = Workload(3, "indoor-room", seed, pos, np.full(3, 0.05, np.float32), "f32", F)
+    wl.buffers = {"s0": (0, 64), "c0": (0, 64)}
+    wl.ops = [dict(op="create", level=0), dict(op="splat", dst=("s0", 0, 64), normalize=1)]
+    _conv(wl, "conv", 0, ("s0", 0, 64), ("c0", 0, 64), False, seed)
+    _deform_vector(wl, seed, 64)
+    wl.ops.append(dict(op="slice", level=0, src=("c0", 0, 64), out="slice"))
+    wl.ops.append(dict(op="deform_slice", level=0, src=("c0", 0, 64), wv="deform", out="deform"))
+    return _finish(wl)
+
+
+def config4(seed: int = 3, m: int = 120_000) -> Workload:
+    """SemanticKITTI-sized LiDAR scan (120k points), intensity lifted to 64
+    channels, sigma 0.3 m, three lattice levels, fp32:
+      L0 conv 64->64, coarsen 64->128, L1 conv 128->128, coarsen 128->128,
+      L2 conv 128->128, refine 128->128 to L1, refine 128->64 to L0,
+      then slice and DeformSlice of the L0 result."""
+    pos = gen.lidar_scan(seed, m)
+    st = gen.Stream(seed, "intensity")
+    F = gen.lifted_features(seed, st.uniform(m).reshape(m, 1), 64)
+    wl = Workload(4, "lidar-scan", seed, pos, np.full(3, 0.3, np.float32), "f32", F)
+    wl.buffers = {"s0": (0, 64), "e0": (0, 64), "d1": (1, 128), "e1": (1, 128),
+                  "d2": (2, 128), "e2": (2, 128), "u1": (1, 128), "u0": (0, 64)}
+    wl.ops = [dict(op="create", level=0), dict(op="splat", dst=("s0", 0, 64), normalize=1)]
+    _conv(wl, "conv", 0, ("s0", 0, 64), ("e0", 0, 64), True, seed)
+    wl.ops.append(dict(op="coarsen", level=1))
+    _conv(wl, "conv_down", 1, ("e0", 0, 64), ("d1", 0, 128), True, seed)
+    _conv(wl, "conv", 1, ("d1", 0, 128), ("e1", 0, 128), True, seed)
+    wl.ops.append(dict(op="coarsen", level=2))
+    _conv(wl, "conv_down", 2, ("e1", 0, 128), ("d2", 0, 128), True, seed)
+    _conv(wl, "conv", 2, ("d2", 0, 128), ("e2", 0, 128), True, seed)
+    _conv(wl, "refine", 1, ("e2", 0, 128), ("u1", 0, 128), True, seed)
+    _conv(wl, "refine", 0, ("u1", 0, 128), ("u0", 0, 64), False, seed)
+    _deform_vector(wl, seed, 64)
+    wl.ops.append(dict(op="slice", level=0, src=("u0", 0, 64), out="slice"))
+    wl.ops.append(dict(op="deform_slice", level=0, src=("u0", 0, 64), wv="deform", out="deform"))
+    return _finish(wl)
+
+
+def config5(seed: int = 4, m: int = 1_000_000, size=(20.0, 20.0, 3.0), nboxes: int = 125) -> Workload:
+    """Large indoor stack (1M points, 20x20x3 m room, 125 boxes), 64 lifted
+    channels, sigma 0.05 m, a 4-level U-Net of lattice convolutions at
+    64/128/192/256 channels with concatenated skips, bf16 storage and MFMA
+    inputs with fp32 accumulation, DeformSlice to the points."""
+    pos = gen.room(seed, m, size, nboxes, 0.01)
+    F = _room_features(seed, pos, 64)
+    wl = Workload(5, "large-indoor-unet", seed, pos, np.full(3, 0.05, np.float32), "bf16", F)
+    wl.buffers = {"s0": (0, 64), "cat0": (0, 128), "d1": (1, 128), "cat1": (1, 256),
+                  "d2": (2, 192), "cat2": (2, 384), "d3": (3, 256), "e3": (3, 256),
+                  "u2": (2, 192), "u1": (1, 128), "out0": (0, 64)}
+    wl.ops = [dict(op="create", level=0), dict(op="splat", dst=("s0", 0, 64), normalize=1)]
+    _conv(wl, "conv", 0, ("s0", 0, 64), ("cat0", 64, 64), True, seed)
+    wl.ops.append(dict(op="coarsen", level=1))
+    _conv(wl, "conv_down", 1, ("cat0", 64, 64), ("d1", 0, 128), True, seed)
+    _conv(wl, "conv", 1, ("d1", 0, 128), ("cat1", 128, 128), True, seed)
+    wl.ops.append(dict(op="coarsen", level=2))
+    _conv(wl, "conv_down", 2, ("cat1", 128, 128), ("d2", 0, 192), True, seed)
+    _conv(wl, "conv", 2, ("d2", 0, 192), ("cat2", 192, 192), True, seed)
+    wl.ops.append(dict(op="coarsen", level=3))
+    _conv(wl, "conv_down", 3, ("cat2", 192, 192), ("d3", 0, 256), True, seed)
+    _conv(wl, "conv", 3, ("d3", 0, 256), ("e3", 0, 256), True, seed)
+    _conv(wl, "refine", 2, ("e3", 0, 256), ("cat2", 0, 192), True, seed)
+    _conv(wl, "conv", 2, ("cat2", 0, 384), ("u2", 0, 192), True, seed)
+    _conv(wl, "refine", 1, ("u2", 0, 192), ("cat1", 0, 128), True, seed)
+    _conv(wl, "conv", 1, ("cat1", 0, 256), ("u1", 0, 128), True, seed)
+    _conv(wl, "refine", 0, ("u1", 0, 128), ("cat0", 0, 64), True, seed)
+    _conv(wl, "conv", 0, ("cat0", 0, 128), ("out0", 0, 64), False, seed)
+    _deform_vector(wl, seed, 64)
+    wl.ops.append(dict(op="deform_slice", level=0, src=("out0", 0, 64), wv="deform", out="deform"))
+    return _finish(wl)
+
+
+CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
+
+
+def make(cfg: int, seed: int | None = None, **kw) -> Workload:
+    fn = CONFIGS[cfg]
+    return fn(**kw) if seed is None else fn(seed=seed, **kw)
