@@ -1,0 +1,201 @@
+/*
+ * liblattice: the permutohedral-lattice hot path of LatticeNet
+ * (Rosu, Schuett, Quenzel, Behnke, arXiv:1912.05905) on AMD MI355X (gfx950).
+ *
+ * Lattice notation (paper, Notation section): a lattice V = (C, X) has n
+ * vertices with integer coordinates c_v in Z^{d+1} (summing to zero) and
+ * values x_v; a point cloud P = (G, F) has m points with positions g_p in R^d
+ * and features f_p.  I_p is the set of d+1 vertices of the simplex enclosing
+ * p, b_pv the barycentric weight of p at v, J_v the points splatting onto v.
+ * Only d = 3 is supported.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers named *_dev are device pointers owned by the caller; they must
+ *    stay valid until the work enqueued on the given stream has finished.
+ *    Pointers named *_host are read before the call returns.
+ *  - All calls enqueue work on `stream` and return without waiting, except
+ *    lattice_num_vertices (and lattice_create / lattice_coarsen when the
+ *    library has to learn n, which they do with one stream synchronisation).
+ *  - Matrices are row-major.  ld_* arguments are row strides in elements
+ *    (0 = dense, i.e. the number of channels); they let several ops write
+ *    disjoint column ranges of one buffer (channel concatenation).
+ *  - Channel counts: multiples of 4 for LAT_F32 and of 8 for LAT_BF16, and
+ *    ld_* likewise; device pointers 16-byte aligned.
+ *  - Outputs are overwritten, never accumulated into.
+ *  - Vertex numbering is the order in which the device hash claimed vertices
+ *    (not deterministic); compare lattices by sorting their keys.
+ *  - Return value: LAT_OK (0) or a negative LAT_E* status.  Host-detectable
+ *    errors return immediately with nothing enqueued.  Errors found on the
+ *    device (hash full, coordinate range, non-finite positions) are reported
+ *    by the next call that synchronises (lattice_create, lattice_coarsen,
+ *    lattice_num_vertices); the handle is then poisoned and every later call
+ *    on it returns the same status.  lattice_last_error() gives the text of
+ *    the last non-OK status of the calling thread.
+ *  - Handles are not thread-safe; distinct handles are independent.
+ */
+#ifndef LATTICE_H_
+#define LATTICE_H_
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lattice_s* lattice_t;
+
+typedef enum { LAT_F32 = 0, LAT_BF16 = 1 } lat_dtype;
+
+enum {
+  LAT_OK = 0,
+  LAT_EINVAL = -1,        /* bad argument (null pointer, size, alignment, aliasing) */
+  LAT_EUNSUPPORTED = -2,  /* d != 3 or an unsupported dtype / channel count */
+  LAT_ENOMEM = -3,        /* device allocation failed */
+  LAT_EHASHFULL = -4,     /* more distinct vertices than the hash table holds */
+  LAT_EKEYRANGE = -5,     /* a vertex coordinate reaches +-2^20 */
+  LAT_ENONFINITE = -6,    /* a position is NaN or infinite */
+  LAT_EDEVICE = -7,       /* a HIP runtime call failed */
+  LAT_ELEVEL = -8         /* lattices not related as the call requires */
+};
+
+#define LAT_RELU 1         /* flags bit: apply max(0, .) after bias */
+#define LAT_TAPS 9         /* 2(d+1)+1 vertices of the 1-hop neighbourhood */
+
+/* Text of the calling thread's last non-OK status ("" if none). */
+const char* lattice_last_error(void);
+
+/* Static name of a status code ("LAT_EHASHFULL", ...). */
+const char* lattice_status_string(int status);
+
+/*
+ * Build the lattice of a point cloud (Permutohedral Lattice section and
+ * Method: positions scaled as G/sigma, each point embedded in H_d, its
+ * enclosing simplex found by rounding, the d+1 vertices inserted into a
+ * device hash map keyed by their coordinates).
+ *   pos_dev        m x d float32 positions.
+ *   m              number of points, >= 0 (m = 0 gives an empty lattice).
+ *   d              must be 3 (else LAT_EUNSUPPORTED).
+ *   sigma_host     d float32 scale factors, each > 0 and finite.
+ *   capacity_hint  upper bound on the number of vertices used to size the
+ *                  hash table (0: d+1 per point); too small -> LAT_EHASHFULL.
+ *   out            receives the new handle (owned by the caller; release it
+ *                  with lattice_destroy).
+ * The handle keeps the elevated positions (m x 4 float32), every point's
+ * simplex (vertex indices and weights), the vertex keys, the neighbour
+ * table and the per-vertex point lists J_v.
+ */
+int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_host,
+                   int64_t capacity_hint, hipStream_t stream, lattice_t* out);
+
+/*
+ * Coarser lattice for Downsample (Proposed Operations: positions divided by
+ * 2 create the coarse lattice).  The coarse lattice holds the same points
+ * with elevated positions halved, and a table mapping each coarse vertex c
+ * and tap t to the fine vertex at 2c + o_t.  The coarse handle refers to
+ * `fine`, which must outlive it (destroying a parent with live children
+ * returns LAT_ELEVEL).
+ */
+int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, lattice_t* coarse);
+
+/* Release a handle and its device memory (LAT_ELEVEL while it has children). */
+int lattice_destroy(lattice_t L);
+
+/* Number of vertices n / of points m.  Reports deferred device errors. */
+int lattice_num_vertices(lattice_t L, int64_t* n);
+int lattice_num_points(lattice_t L, int64_t* m);
+
+/* Coarsening level of a handle (0 for lattice_create). */
+int lattice_level(lattice_t L, int* level);
+
+/* Vertex coordinates c_v, n x (d+1) int32. */
+int lattice_export_keys(lattice_t L, int32_t* keys_dev, hipStream_t stream);
+
+/* Per point: the d+1 vertex indices of I_p (m x (d+1) int32, vertex k has
+ * every coordinate congruent to k mod d+1) and weights b_pv (m x (d+1)). */
+int lattice_export_simplices(lattice_t L, int32_t* idx_dev, float* w_dev, hipStream_t stream);
+
+/* 1-hop neighbour table, n x 9 int32: column 0 the vertex itself, 1..d+1 the
+ * vertex at c + n_j, d+2..2d+2 at c - n_j, n_j = (d+1)e_j - 1; -1 where the
+ * neighbour is not allocated (Permutohedral Lattice section). */
+int lattice_export_neighbors(lattice_t L, int32_t* nbr_dev, hipStream_t stream);
+
+/*
+ * Splat, Eq. (splat): x_v = sum_{p in J_v} b_pv f_p.
+ *   feat_dev   m x C features (dtype dt), row stride ld_feat.
+ *   normalize  nonzero: divide by sum_{p in J_v} b_pv (the weighted average
+ *              the paper describes), 0 where that sum is 0.
+ *   vals_dev   n x C output (dtype dt, float32 accumulation), row stride ld_vals.
+ *   wsum_dev   optional n float32 sums of weights (may be NULL).
+ */
+int lattice_splat(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat_dtype dt,
+                  int normalize, void* vals_dev, int64_t ld_vals, float* wsum_dev,
+                  hipStream_t stream);
+
+/*
+ * Lattice convolution (Method, Convolving; Downsample):
+ *   out[v] = bias + sum_{t<9} in[nb(v,t)] W[t]^T   (missing neighbours add 0)
+ *   dst == src: 1-hop convolution, nb(v,t) = vertex at c_v + o_t.
+ *   dst = lattice_coarsen(src): strided convolution, nb(v,t) = fine vertex
+ *   at 2 c_v + o_t (the values of the coarse lattice).
+ *   in_dev    n_src x Cin (dtype dt), row stride ld_in.
+ *   W_dev     9 x Cout x Cin (dtype dt): W[t][o][i] multiplies input channel
+ *             i of tap t into output channel o.  Taps: 0 self, 1+j +n_j,
+ *             5+j -n_j.
+ *   bias_dev  optional Cout float32.
+ *   flags     LAT_RELU or 0.
+ *   out_dev   n_dst x Cout (dtype dt, float32 accumulation), row stride
+ *             ld_out; must not overlap in_dev.
+ */
+int lattice_conv(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in, int Cin,
+                 const void* W_dev, const float* bias_dev, int Cout, lat_dtype dt, int flags,
+                 void* out_dev, int64_t ld_out, hipStream_t stream);
+
+/*
+ * Upsample (Proposed Operations): transposed convolution from `coarse`
+ * (= lattice_coarsen(fine)) to `fine`.  Fine vertex f reads, for tap t, the
+ * coarse vertex at (c_f + o_t)/2 when that is a lattice point; taps landing
+ * between coarse vertices contribute nothing.  With W[t] = W_down[mirror t]^T
+ * this is exactly the adjoint of the strided convolution.  Arguments as for
+ * lattice_conv with in_dev n_coarse x Cin and out_dev n_fine x Cout.
+ */
+int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t ld_in, int Cin,
+                   const void* W_dev, const float* bias_dev, int Cout, lat_dtype dt, int flags,
+                   void* out_dev, int64_t ld_out, hipStream_t stream);
+
+/*
+ * Slice, Eq. (slice): out_p = sum_{v in I_p} b_pv x_v.
+ *   vals_dev  n x C (dtype dt), row stride ld_vals.
+ *   out_dev   m x C float32 (dense).
+ */
+int lattice_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
+                  float* out_dev, hipStream_t stream);
+
+/*
+ * DeformSlice, Eq. (deformSlice) with the permutation-equivariant offsets:
+ *   q_k = b_k x_k (k over I_p),  M = max_k q_k per channel,
+ *   db_k = tanh(beta + (q_k - M) . wv),  out_p = sum_k (b_k + db_k) x_k.
+ *   wv_dev     C float32 weight vector, beta the scalar bias.
+ *   out_dev    m x C float32; delta_dev optional m x (d+1) float32 offsets.
+ */
+int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
+                         const float* wv_dev, float beta, float* out_dev, float* delta_dev,
+                         hipStream_t stream);
+
+/*
+ * Timing of the library's kernels with HIP events on the launch stream, for
+ * measurement.  enable != 0 records a start/stop event pair around every
+ * launch of the kernel family `name` ("conv", "splat", "slice", "insert",
+ * ...); lattice_timing_read waits for the recorded events and returns the
+ * number of launches and their summed duration in milliseconds, then clears
+ * the record.
+ */
+int lattice_timing_enable(const char* name, int enable);
+int lattice_timing_read(const char* name, int64_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LATTICE_H_ */

@@ -1,0 +1,678 @@
+// liblattice C ABI: argument validation, handle lifetime, device memory and
+// kernel-family timing.  Every lattice operation is a hand-written kernel in
+// create.hip, splat_slice.hip or conv.hip; this file only orchestrates them.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "lattice_internal.h"
+
+namespace lat {
+int splat_max_channels(bool bf16);
+int deform_max_channels(bool bf16);
+}
+
+using namespace lat;
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const std::string& msg) {
+  g_last_error = std::string(lattice_status_string(status)) + ": " + msg;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(LAT_EDEVICE, std::string(what) + " failed: " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr)                                  \
+  do {                                                 \
+    hipError_t e_ = (expr);                            \
+    if (e_ != hipSuccess) return hip_fail(e_, #expr);  \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// caching device allocator: freed blocks are kept per (device, size class)
+// and handed out again without hipMalloc.  A block released on one stream is
+// reused on another only after that stream has drained.
+// ---------------------------------------------------------------------------
+struct Block {
+  void* ptr;
+  size_t bytes;
+  hipStream_t stream;
+};
+
+class Pool {
+ public:
+  static Pool& get() {
+    static Pool* p = new Pool();   // never destroyed: blocks live until exit
+    return *p;
+  }
+
+  static size_t size_class(size_t bytes) {
+    size_t c = 256;
+    while (c < bytes) c <<= 1;
+    return c;
+  }
+
+  int alloc(size_t bytes, hipStream_t s, void** out) {
+    *out = nullptr;
+    if (bytes == 0) return LAT_OK;
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    const size_t cls = size_class(bytes);
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      auto& lst = free_[{dev, cls}];
+      for (size_t i = 0; i < lst.size(); ++i) {
+        if (lst[i].stream == s) {
+          *out = lst[i].ptr;
+          lst.erase(lst.begin() + static_cast<long>(i));
+          return LAT_OK;
+        }
+      }
+      if (!lst.empty()) {
+        Block b = lst.back();
+        lst.pop_back();
+        HIP_TRY(hipStreamSynchronize(b.stream));
+        *out = b.ptr;
+        return LAT_OK;
+      }
+    }
+    void* p = nullptr;
+    hipError_t e = hipMalloc(&p, cls);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      trim(dev);
+      e = hipMalloc(&p, cls);
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(LAT_ENOMEM, "hipMalloc of " + std::to_string(cls) + " bytes");
+      }
+    }
+    *out = p;
+    return LAT_OK;
+  }
+
+  void release(void* p, size_t bytes, hipStream_t s) {
+    if (!p || bytes == 0) return;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return;
+    std::lock_guard<std::mutex> lk(mu_);
+    free_[{dev, size_class(bytes)}].push_back(Block{p, bytes, s});
+  }
+
+ private:
+  void trim(int dev) {
+    std::lock_guard<std::mutex> lk(mu_);
+    (void)hipDeviceSynchronize();
+    for (auto& kv : free_) {
+      if (kv.first.first != dev) continue;
+      for (auto& b : kv.second) (void)hipFree(b.ptr);
+      kv.second.clear();
+    }
+  }
+
+  std::mutex mu_;
+  std::map<std::pair<int, size_t>, std::vector<Block>> free_;
+};
+
+// ---------------------------------------------------------------------------
+// kernel-family timing with events on the launch stream
+// ---------------------------------------------------------------------------
+struct TimerFamily {
+  std::string name;
+  bool enabled = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> recorded;
+  std::vector<hipEvent_t> spare;
+  hipEvent_t pending = nullptr;
+};
+
+std::mutex g_timer_mu;
+std::vector<TimerFamily>& timer_families() {
+  static auto* v = new std::vector<TimerFamily>();
+  return *v;
+}
+bool g_any_timer = false;
+
+TimerFamily* find_family(const char* name, bool create) {
+  auto& fams = timer_families();
+  for (auto& f : fams)
+    if (f.name == name) return &f;
+  if (!create) return nullptr;
+  fams.push_back(TimerFamily{});
+  fams.back().name = name;
+  return &fams.back();
+}
+
+hipEvent_t take_event(TimerFamily* f) {
+  if (!f->spare.empty()) {
+    hipEvent_t e = f->spare.back();
+    f->spare.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+}  // namespace
+
+namespace lat {
+
+void timer_begin(const char* family, hipStream_t s) {
+  if (!g_any_timer) return;
+  std::lock_guard<std::mutex> lk(g_timer_mu);
+  TimerFamily* f = find_family(family, false);
+  if (!f || !f->enabled) return;
+  f->pending = take_event(f);
+  if (f->pending) (void)hipEventRecord(f->pending, s);
+}
+
+void timer_end(const char* family, hipStream_t s) {
+  if (!g_any_timer) return;
+  std::lock_guard<std::mutex> lk(g_timer_mu);
+  TimerFamily* f = find_family(family, false);
+  if (!f || !f->enabled || !f->pending) return;
+  hipEvent_t stop = take_event(f);
+  if (!stop) return;
+  (void)hipEventRecord(stop, s);
+  f->recorded.emplace_back(f->pending, stop);
+  f->pending = nullptr;
+}
+
+}  // namespace lat
+
+// ---------------------------------------------------------------------------
+// handle
+// ---------------------------------------------------------------------------
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+};
+
+struct lattice_s {
+  int level = 0;
+  int64_t m = 0;
+  int64_t n = 0;
+  int64_t cap = 0;               // hash slots
+  int status = LAT_OK;           // poisoned when != LAT_OK
+  int children = 0;
+  lattice_s* parent = nullptr;
+  hipStream_t stream = nullptr;  // stream the handle's buffers were produced on
+  std::vector<DevBuf> owned;
+
+  float* y = nullptr;            // m x 4 elevated positions
+  int32_t* idx = nullptr;        // m x 4 simplex vertex indices
+  float* w = nullptr;            // m x 4 barycentric weights
+  uint64_t* tkeys = nullptr;     // hash keys (cap)
+  int32_t* tvals = nullptr;      // hash values (cap)
+  uint64_t* vkeys = nullptr;     // n packed vertex keys
+  int32_t* offsets = nullptr;    // n+1 list offsets of J_v
+  int32_t* entries = nullptr;    // 4m entries p*4+k grouped by vertex
+  float* entry_w = nullptr;      // 4m weights of those entries
+  int32_t* nbr = nullptr;        // 9 x n same-level table (tap-major)
+  int32_t* down = nullptr;       // 9 x n table into the parent (coarse levels)
+  int32_t* up = nullptr;         // 9 x n_parent table from the parent into this level
+  bool up_built = false;
+
+  HashView hash() const { return HashView{tkeys, tvals, static_cast<uint64_t>(cap - 1)}; }
+
+  int alloc(size_t bytes, hipStream_t s, void** out) {
+    const int st = Pool::get().alloc(bytes, s, out);
+    if (st == LAT_OK && *out) owned.push_back(DevBuf{*out, bytes});
+    return st;
+  }
+
+  void free_all() {
+    for (auto& b : owned) Pool::get().release(b.p, b.bytes, stream);
+    owned.clear();
+  }
+};
+
+namespace {
+
+struct DeviceCounters {
+  int32_t counter;
+  uint32_t err;
+};
+
+// pinned host landing zone for the per-create readback
+DeviceCounters* host_readback() {
+  thread_local DeviceCounters* h = nullptr;
+  if (!h) {
+    void* p = nullptr;
+    if (hipHostMalloc(&p, sizeof(DeviceCounters) * 2, hipHostMallocDefault) != hipSuccess) return nullptr;
+    h = static_cast<DeviceCounters*>(p);
+  }
+  return h;
+}
+
+int64_t next_pow2(int64_t v) {
+  int64_t c = 1;
+  while (c < v) c <<= 1;
+  return c;
+}
+
+int status_from_err_bits(uint32_t bits) {
+  if (bits & kErrNonFinite) return LAT_ENONFINITE;
+  if (bits & kErrKeyRange) return LAT_EKEYRANGE;
+  if (bits & kErrHashFull) return LAT_EHASHFULL;
+  return LAT_OK;
+}
+
+int check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, what);
+  return LAT_OK;
+}
+
+// Build a lattice for `m` points: either from positions (pos, a[]) or from a
+// parent's elevated positions scaled by 1/2.
+int build_lattice(lattice_s* L, const float* pos, const float a[3], const lattice_s* parent,
+                  int64_t capacity_hint, hipStream_t s) {
+  const int64_t m = L->m;
+  if (m == 0) return LAT_OK;
+  const int64_t refs = 4 * m;
+  if (refs > INT32_MAX) return fail(LAT_EUNSUPPORTED, "more than 2^29 points");
+  const int64_t want = capacity_hint > 0 ? std::min(capacity_hint, refs) : refs;
+  L->cap = next_pow2(std::max<int64_t>(1024, 2 * want));
+  const int64_t nmax = std::min(L->cap, refs);
+  int st;
+  void* p;
+#define ALLOC(field, type, count)                                                 \
+  if ((st = L->alloc(sizeof(type) * static_cast<size_t>(count), s, &p)) != LAT_OK) \
+    return st;                                                                    \
+  L->field = static_cast<type*>(p)
+  ALLOC(y, float, 4 * m);
+  ALLOC(idx, int32_t, refs);
+  ALLOC(w, float, refs);
+  ALLOC(tkeys, uint64_t, L->cap);
+  ALLOC(tvals, int32_t, L->cap);
+  ALLOC(vkeys, uint64_t, nmax);
+#undef ALLOC
+  // scratch for this build only
+  int32_t* count = nullptr;
+  int32_t* slot_rank = nullptr;
+  DeviceCounters* dc = nullptr;
+  void* q;
+  if ((st = Pool::get().alloc(sizeof(int32_t) * nmax, s, &q)) != LAT_OK) return st;
+  count = static_cast<int32_t*>(q);
+  if ((st = Pool::get().alloc(sizeof(int32_t) * refs, s, &q)) != LAT_OK) return st;
+  slot_rank = static_cast<int32_t*>(q);
+  if ((st = Pool::get().alloc(sizeof(DeviceCounters), s, &q)) != LAT_OK) return st;
+  dc = static_cast<DeviceCounters*>(q);
+
+  launch_fill_u64(L->tkeys, kEmptyKey, L->cap, s);
+  launch_fill_u64(reinterpret_cast<uint64_t*>(dc), 0ull, 1, s);
+  launch_insert_points(pos, parent ? parent->y : nullptr, 0.5f, a[0], a[1], a[2], m, L->hash(),
+                       &dc->counter, L->vkeys, count, slot_rank, L->w, L->y, &dc->err, s);
+  if ((st = check_launch("insert")) != LAT_OK) return st;
+  DeviceCounters* h = host_readback();
+  if (!h) return fail(LAT_ENOMEM, "pinned host buffer");
+  HIP_TRY(hipMemcpyAsync(h, dc, sizeof(DeviceCounters), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  const int dev_status = status_from_err_bits(h->err);
+  L->n = h->counter;
+  if (dev_status != LAT_OK) {
+    Pool::get().release(count, sizeof(int32_t) * nmax, s);
+    Pool::get().release(slot_rank, sizeof(int32_t) * refs, s);
+    Pool::get().release(dc, sizeof(DeviceCounters), s);
+    const char* why = dev_status == LAT_EHASHFULL ? "hash table full (raise capacity_hint)"
+                      : dev_status == LAT_EKEYRANGE ? "a vertex coordinate reaches 2^20 (positions / sigma too large)"
+                                                    : "non-finite position";
+    return fail(dev_status, why);
+  }
+  const int64_t n = L->n;
+#define ALLOC(field, type, count)                                                 \
+  if ((st = L->alloc(sizeof(type) * static_cast<size_t>(count), s, &p)) != LAT_OK) \
+    return st;                                                                    \
+  L->field = static_cast<type*>(p)
+  ALLOC(offsets, int32_t, n + 1);
+  ALLOC(entries, int32_t, refs);
+  ALLOC(entry_w, float, refs);
+  ALLOC(nbr, int32_t, kTaps * n);
+#undef ALLOC
+  int32_t* work = nullptr;
+  if ((st = Pool::get().alloc(sizeof(int32_t) * scan_workspace_elems(n), s, &q)) != LAT_OK) return st;
+  work = static_cast<int32_t*>(q);
+
+  launch_resolve(L->hash(), slot_rank, L->idx, count, refs, s);
+  launch_exclusive_scan(count, L->offsets, n, work, s);
+  launch_fill_lists(L->idx, slot_rank, L->w, L->offsets, L->entries, L->entry_w, refs, s);
+  launch_neighbor_table(L->hash(), L->vkeys, n, L->nbr, n, s);
+  if ((st = check_launch("lattice build")) != LAT_OK) return st;
+
+  Pool::get().release(work, sizeof(int32_t) * scan_workspace_elems(n), s);
+  Pool::get().release(count, sizeof(int32_t) * nmax, s);
+  Pool::get().release(slot_rank, sizeof(int32_t) * refs, s);
+  Pool::get().release(dc, sizeof(DeviceCounters), s);
+  return LAT_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_handle(const lattice_s* L) {
+  if (!L) return fail(LAT_EINVAL, "null lattice handle");
+  if (L->status != LAT_OK) return fail(L->status, "lattice handle is poisoned by an earlier error");
+  return LAT_OK;
+}
+
+// channel count / stride / alignment rules of one feature matrix
+int check_matrix(const void* p, int64_t ld, int C, lat_dtype dt, const char* what, bool need_ptr) {
+  const int vec = dt == LAT_BF16 ? 8 : 4;
+  if (need_ptr && !p) return fail(LAT_EINVAL, std::string(what) + " is null");
+  if (C <= 0) return fail(LAT_EINVAL, std::string(what) + ": channel count must be positive");
+  if (C % vec != 0)
+    return fail(LAT_EUNSUPPORTED, std::string(what) + ": channels must be a multiple of " + std::to_string(vec));
+  if (ld < C || ld % vec != 0)
+    return fail(LAT_EINVAL, std::string(what) + ": row stride must be >= channels and a multiple of " +
+                                std::to_string(vec));
+  if (p && !aligned16(p)) return fail(LAT_EINVAL, std::string(what) + " must be 16-byte aligned");
+  return LAT_OK;
+}
+
+int check_dtype(lat_dtype dt) {
+  if (dt != LAT_F32 && dt != LAT_BF16) return fail(LAT_EUNSUPPORTED, "dtype must be LAT_F32 or LAT_BF16");
+  return LAT_OK;
+}
+
+bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + bbytes && y < x + abytes;
+}
+
+int conv_common(const int32_t* table, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
+                int Cin, const void* W, const float* bias, int Cout, lat_dtype dt, int flags,
+                void* out, int64_t ld_out, hipStream_t s) {
+  int st;
+  if ((st = check_dtype(dt)) != LAT_OK) return st;
+  if (ld_in == 0) ld_in = Cin;
+  if (ld_out == 0) ld_out = Cout;
+  if ((st = check_matrix(in, ld_in, Cin, dt, "in", n_in > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(out, ld_out, Cout, dt, "out", n_out > 0)) != LAT_OK) return st;
+  if (!W) return fail(LAT_EINVAL, "W is null");
+  if (!aligned16(W)) return fail(LAT_EINVAL, "W must be 16-byte aligned");
+  if (flags & ~LAT_RELU) return fail(LAT_EINVAL, "unknown flags");
+  const size_t u = dt == LAT_BF16 ? 2 : 4;
+  if (n_in > 0 && n_out > 0 &&
+      overlaps(in, static_cast<size_t>((n_in - 1) * ld_in + Cin) * u, out,
+               static_cast<size_t>((n_out - 1) * ld_out + Cout) * u))
+    return fail(LAT_EINVAL, "in and out overlap");
+  if (n_out == 0) return LAT_OK;
+  launch_conv(table, n_out, n_out, in, ld_in, Cin, W, bias, Cout, dt == LAT_BF16, flags & LAT_RELU, out,
+              ld_out, s);
+  return check_launch("conv");
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// ABI
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char* lattice_last_error(void) { return g_last_error.c_str(); }
+
+const char* lattice_status_string(int status) {
+  switch (status) {
+    case LAT_OK: return "LAT_OK";
+    case LAT_EINVAL: return "LAT_EINVAL";
+    case LAT_EUNSUPPORTED: return "LAT_EUNSUPPORTED";
+    case LAT_ENOMEM: return "LAT_ENOMEM";
+    case LAT_EHASHFULL: return "LAT_EHASHFULL";
+    case LAT_EKEYRANGE: return "LAT_EKEYRANGE";
+    case LAT_ENONFINITE: return "LAT_ENONFINITE";
+    case LAT_EDEVICE: return "LAT_EDEVICE";
+    case LAT_ELEVEL: return "LAT_ELEVEL";
+    default: return "LAT_UNKNOWN";
+  }
+}
+
+int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_host,
+                   int64_t capacity_hint, hipStream_t stream, lattice_t* out) {
+  if (!out) return fail(LAT_EINVAL, "out is null");
+  *out = nullptr;
+  if (d != kDim) return fail(LAT_EUNSUPPORTED, "only d = 3 is supported");
+  if (m < 0) return fail(LAT_EINVAL, "m < 0");
+  if (m > 0 && !pos_dev) return fail(LAT_EINVAL, "pos is null");
+  if (!sigma_host) return fail(LAT_EINVAL, "sigma is null");
+  if (capacity_hint < 0) return fail(LAT_EINVAL, "capacity_hint < 0");
+  for (int j = 0; j < kDim; ++j)
+    if (!(sigma_host[j] > 0.0f) || !std::isfinite(sigma_host[j]))
+      return fail(LAT_EINVAL, "sigma must be positive and finite");
+  // a_j = (d+1) sqrt(2/3) / (sigma_j sqrt((j+1)(j+2))), in double, rounded once
+  float a[kDim];
+  const double sc = (kDim + 1) * std::sqrt(2.0 / 3.0);
+  for (int j = 0; j < kDim; ++j)
+    a[j] = static_cast<float>(sc / (static_cast<double>(sigma_host[j]) *
+                                    std::sqrt(static_cast<double>((j + 1) * (j + 2)))));
+  lattice_s* L = new lattice_s();
+  L->m = m;
+  L->stream = stream;
+  const int st = build_lattice(L, pos_dev, a, nullptr, capacity_hint, stream);
+  if (st != LAT_OK) {
+    L->free_all();
+    delete L;
+    return st;
+  }
+  *out = L;
+  return LAT_OK;
+}
+
+int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, lattice_t* coarse) {
+  if (!coarse) return fail(LAT_EINVAL, "out is null");
+  *coarse = nullptr;
+  int st;
+  if ((st = check_handle(fine)) != LAT_OK) return st;
+  if (capacity_hint < 0) return fail(LAT_EINVAL, "capacity_hint < 0");
+  lattice_s* L = new lattice_s();
+  L->m = fine->m;
+  L->level = fine->level + 1;
+  L->parent = fine;
+  L->stream = stream;
+  const float a[3] = {0.f, 0.f, 0.f};
+  st = build_lattice(L, nullptr, a, fine, capacity_hint, stream);
+  if (st == LAT_OK && L->n > 0) {
+    void* p;
+    st = L->alloc(sizeof(int32_t) * kTaps * L->n, stream, &p);
+    if (st == LAT_OK) {
+      L->down = static_cast<int32_t*>(p);
+      launch_down_table(fine->hash(), L->vkeys, L->n, L->down, L->n, stream);
+      st = check_launch("down table");
+    }
+  }
+  if (st != LAT_OK) {
+    L->free_all();
+    delete L;
+    return st;
+  }
+  fine->children += 1;
+  *coarse = L;
+  return LAT_OK;
+}
+
+int lattice_destroy(lattice_t L) {
+  if (!L) return LAT_OK;
+  if (L->children > 0) return fail(LAT_ELEVEL, "destroy the coarser lattices first");
+  if (L->parent) L->parent->children -= 1;
+  L->free_all();
+  delete L;
+  return LAT_OK;
+}
+
+int lattice_num_vertices(lattice_t L, int64_t* n) {
+  int st;
+  if (!n) return fail(LAT_EINVAL, "n is null");
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  *n = L->n;
+  return LAT_OK;
+}
+
+int lattice_num_points(lattice_t L, int64_t* m) {
+  int st;
+  if (!m) return fail(LAT_EINVAL, "m is null");
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  *m = L->m;
+  return LAT_OK;
+}
+
+int lattice_level(lattice_t L, int* level) {
+  int st;
+  if (!level) return fail(LAT_EINVAL, "level is null");
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  *level = L->level;
+  return LAT_OK;
+}
+
+int lattice_export_keys(lattice_t L, int32_t* keys_dev, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if (L->n > 0 && !keys_dev) return fail(LAT_EINVAL, "keys is null");
+  if (L->n > 0 && !aligned16(keys_dev)) return fail(LAT_EINVAL, "keys must be 16-byte aligned");
+  launch_export_keys(L->vkeys, L->n, keys_dev, stream);
+  return check_launch("export keys");
+}
+
+int lattice_export_simplices(lattice_t L, int32_t* idx_dev, float* w_dev, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if (L->m == 0) return LAT_OK;
+  if (!idx_dev || !w_dev) return fail(LAT_EINVAL, "idx / w is null");
+  HIP_TRY(hipMemcpyAsync(idx_dev, L->idx, sizeof(int32_t) * 4 * L->m, hipMemcpyDeviceToDevice, stream));
+  HIP_TRY(hipMemcpyAsync(w_dev, L->w, sizeof(float) * 4 * L->m, hipMemcpyDeviceToDevice, stream));
+  return LAT_OK;
+}
+
+int lattice_export_neighbors(lattice_t L, int32_t* nbr_dev, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if (L->n == 0) return LAT_OK;
+  if (!nbr_dev) return fail(LAT_EINVAL, "nbr is null");
+  launch_transpose_table(L->nbr, L->n, L->n, nbr_dev, stream);
+  return check_launch("export neighbours");
+}
+
+int lattice_splat(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat_dtype dt,
+                  int normalize, void* vals_dev, int64_t ld_vals, float* wsum_dev, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = check_dtype(dt)) != LAT_OK) return st;
+  if (ld_feat == 0) ld_feat = C;
+  if (ld_vals == 0) ld_vals = C;
+  if ((st = check_matrix(feat_dev, ld_feat, C, dt, "feat", L->m > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(vals_dev, ld_vals, C, dt, "vals", L->n > 0)) != LAT_OK) return st;
+  if (C > splat_max_channels(dt == LAT_BF16))
+    return fail(LAT_EUNSUPPORTED, "splat supports at most " + std::to_string(splat_max_channels(dt == LAT_BF16)) +
+                                      " channels");
+  launch_splat(L->offsets, L->entries, L->entry_w, feat_dev, ld_feat, C, dt == LAT_BF16, normalize != 0,
+               L->n, vals_dev, ld_vals, wsum_dev, stream);
+  return check_launch("splat");
+}
+
+int lattice_conv(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in, int Cin,
+                 const void* W_dev, const float* bias_dev, int Cout, lat_dtype dt, int flags,
+                 void* out_dev, int64_t ld_out, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(dst)) != LAT_OK) return st;
+  if ((st = check_handle(src)) != LAT_OK) return st;
+  const int32_t* table;
+  if (dst == src) table = dst->nbr;
+  else if (dst->parent == src) table = dst->down;
+  else return fail(LAT_ELEVEL, "dst must be src or lattice_coarsen(src)");
+  return conv_common(table, dst->n, src->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt, flags,
+                     out_dev, ld_out, stream);
+}
+
+int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t ld_in, int Cin,
+                   const void* W_dev, const float* bias_dev, int Cout, lat_dtype dt, int flags,
+                   void* out_dev, int64_t ld_out, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(fine)) != LAT_OK) return st;
+  if ((st = check_handle(coarse)) != LAT_OK) return st;
+  if (coarse->parent != fine) return fail(LAT_ELEVEL, "coarse must be lattice_coarsen(fine)");
+  if (!coarse->up_built && fine->n > 0) {
+    void* p;
+    if ((st = coarse->alloc(sizeof(int32_t) * kTaps * fine->n, coarse->stream, &p)) != LAT_OK) return st;
+    coarse->up = static_cast<int32_t*>(p);
+    launch_up_table(coarse->hash(), fine->vkeys, fine->n, coarse->up, fine->n, coarse->stream);
+    if ((st = check_launch("up table")) != LAT_OK) return st;
+    if (stream != coarse->stream) HIP_TRY(hipStreamSynchronize(coarse->stream));
+    coarse->up_built = true;
+  }
+  return conv_common(coarse->up, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
+                     flags, out_dev, ld_out, stream);
+}
+
+int lattice_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
+                  float* out_dev, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = check_dtype(dt)) != LAT_OK) return st;
+  if (ld_vals == 0) ld_vals = C;
+  if ((st = check_matrix(vals_dev, ld_vals, C, dt, "vals", L->n > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(out_dev, C, C, LAT_F32, "out", L->m > 0)) != LAT_OK) return st;
+  launch_slice(L->idx, L->w, L->m, vals_dev, ld_vals, C, dt == LAT_BF16, out_dev, stream);
+  return check_launch("slice");
+}
+
+int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
+                         const float* wv_dev, float beta, float* out_dev, float* delta_dev,
+                         hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = check_dtype(dt)) != LAT_OK) return st;
+  if (ld_vals == 0) ld_vals = C;
+  if ((st = check_matrix(vals_dev, ld_vals, C, dt, "vals", L->n > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(out_dev, C, C, LAT_F32, "out", L->m > 0)) != LAT_OK) return st;
+  if (!wv_dev) return fail(LAT_EINVAL, "wv is null");
+  if (!std::isfinite(beta)) return fail(LAT_EINVAL, "beta must be finite");
+  if (delta_dev && !aligned16(delta_dev)) return fail(LAT_EINVAL, "delta must be 16-byte aligned");
+  if (C > deform_max_channels(dt == LAT_BF16))
+    return fail(LAT_EUNSUPPORTED, "DeformSlice supports at most " +
+                                      std::to_string(deform_max_channels(dt == LAT_BF16)) + " channels");
+  launch_deform_slice(L->idx, L->w, L->m, vals_dev, ld_vals, C, dt == LAT_BF16, wv_dev, beta, out_dev,
+                      delta_dev, stream);
+  return check_launch("deform slice");
+}
+
+int lattice_timing_enable(const char* name, int enable) {
+  if (!name) return fail(LAT_EINVAL, "name is null");
+  std::lock_guard<std::mutex> lk(g_timer_mu);
+  TimerFamily* f = find_family(name, true);
+  f->enabled = enable != 0;
+  g_any_timer = false;
+  for (auto& fam : timer_families()) g_any_timer = g_any_timer || fam.enabled;
+  return LAT_OK;
+}
+
+int lattice_timing_read(const char* name, int64_t* launches, double* total_ms) {
+  if (!name || !launches || !total_ms) return fail(LAT_EINVAL, "null argument");
+  std::lock_guard<std::mutex> lk(g_timer_mu);
+  *launches = 0;
+  *total_ms = 0.0;
+  TimerFamily* f = find_family(name, false);
+  if (!f) return LAT_OK;
+  for (auto& pr : f->recorded) {
+    HIP_TRY(hipEventSynchronize(pr.second));
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, pr.first, pr.second));
+    *total_ms += ms;
+    *launches += 1;
+    f->spare.push_back(pr.first);
+    f->spare.push_back(pr.second);
+  }
+  f->recorded.clear();
+  return LAT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,442 @@
+// Lattice construction on gfx950: point embedding, device hash insert,
+// vertex numbering, per-vertex point lists J_v and the neighbour tables.
+//
+// The embedding (elevation, rounding, ranking, barycentric weights) must
+// produce the vertex set bit for bit, so this file is compiled with float
+// contraction off and every float operation below is one IEEE rounding.
+#pragma clang fp contract(off)
+
+#include "lattice_internal.h"
+
+namespace lat {
+namespace {
+
+constexpr int kBlock = 256;
+
+__global__ void __launch_bounds__(kBlock) k_fill_u64(uint64_t* __restrict__ p, uint64_t v, int64_t n) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int64_t e = i; e < n; e += stride) p[e] = v;
+}
+
+// Insert a key; returns its slot, or -1 when the table is full.  The thread
+// whose compare-and-swap claims an empty slot numbers the vertex.
+__device__ inline int32_t hash_insert(const HashView& h, uint64_t key, int32_t* counter,
+                                      uint64_t* vkeys, int32_t* count, uint32_t* err) {
+  uint64_t slot = hash_key(key) & h.mask;
+  for (uint64_t probe = 0; probe <= h.mask; ++probe) {
+    const uint64_t cur = h.keys[slot];
+    if (cur == key) return static_cast<int32_t>(slot);
+    if (cur == kEmptyKey) {
+      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(&h.keys[slot]),
+                                      static_cast<unsigned long long>(kEmptyKey),
+                                      static_cast<unsigned long long>(key));
+      if (prev == kEmptyKey) {
+        const int32_t v = atomicAdd(counter, 1);
+        h.vals[slot] = v;
+        vkeys[v] = key;
+        count[v] = 0;
+        return static_cast<int32_t>(slot);
+      }
+      if (prev == key) return static_cast<int32_t>(slot);
+    }
+    slot = (slot + 1) & h.mask;
+  }
+  atomicOr(err, kErrHashFull);
+  return -1;
+}
+
+// One thread per point: elevate (or take the parent's elevated position
+// times y_scale), find the enclosing simplex, insert its d+1 vertices.
+//
+// Elevation: y = E (g/sigma) with E's columns orthonormal and orthogonal to
+// 1 (the lattice lives on H_d, coordinates summing to zero), scaled by
+// (d+1) sqrt(2/3); a_j folds 1/sigma_j and the column norm into one factor.
+// Simplex (the rounding construction of Adams, Baek and Davis 2010, which
+// the paper cites for finding the enclosing simplex): round each coordinate
+// to the nearest multiple of d+1 (ties down), rank the differentials
+// (largest first, equal ones by lower index), move the most extreme ones by
+// d+1 until the point lies on H_d, then vertex k adds k to every coordinate
+// and subtracts d+1 from the k highest-ranked ones; the barycentric weights
+// are the gaps between consecutive sorted differentials.
+__global__ void __launch_bounds__(kBlock)
+k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, float y_scale,
+                float a0, float a1, float a2, int64_t m, HashView h, int32_t* counter,
+                uint64_t* vkeys, int32_t* count, int4* __restrict__ slot_out,
+                float4* __restrict__ w_out, float4* __restrict__ y_out, uint32_t* err) {
+  const int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (p >= m) return;
+  float y[kVerts];
+  if (pos != nullptr) {
+    const float g0 = pos[3 * p + 0], g1 = pos[3 * p + 1], g2 = pos[3 * p + 2];
+    if (!isfinite(g0) || !isfinite(g1) || !isfinite(g2)) {
+      atomicOr(err, kErrNonFinite);
+      slot_out[p] = make_int4(-1, -1, -1, -1);
+      w_out[p] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (y_out) y_out[p] = make_float4(0.f, 0.f, 0.f, 0.f);
+      return;
+    }
+    const float t0 = g0 * a0, t1 = g1 * a1, t2 = g2 * a2;
+    float run = 0.0f;
+    const float m3 = 3.0f * t2;
+    y[3] = run - m3;
+    run = run + t2;
+    const float m2 = 2.0f * t1;
+    y[2] = run - m2;
+    run = run + t1;
+    const float m1 = 1.0f * t0;
+    y[1] = run - m1;
+    run = run + t0;
+    y[0] = run;
+  } else {
+    const float4 v = y_in[p];
+    y[0] = v.x * y_scale;
+    y[1] = v.y * y_scale;
+    y[2] = v.z * y_scale;
+    y[3] = v.w * y_scale;
+  }
+  if (y_out) y_out[p] = make_float4(y[0], y[1], y[2], y[3]);
+
+  bool ok = true;
+  for (int i = 0; i < kVerts; ++i)
+    if (!(fabsf(y[i]) < 2.0f * static_cast<float>(kCoordLimit))) ok = false;
+  if (!ok) {
+    atomicOr(err, isfinite(y[0] + y[1] + y[2] + y[3]) ? kErrKeyRange : kErrNonFinite);
+    slot_out[p] = make_int4(-1, -1, -1, -1);
+    w_out[p] = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
+
+  // nearest multiple of d+1 per coordinate, ties to the lower one
+  int32_t base[kVerts];
+  int32_t total = 0;
+#pragma unroll
+  for (int i = 0; i < kVerts; ++i) {
+    const float q = y[i] * 0.25f;
+    const float lo = floorf(q) * 4.0f;
+    const float hi = lo + 4.0f;
+    const float up = hi - y[i];
+    const float down = y[i] - lo;
+    base[i] = static_cast<int32_t>(up < down ? hi : lo);
+    total += base[i];
+  }
+  const int32_t excess = total / kVerts;
+  float diff[kVerts];
+#pragma unroll
+  for (int i = 0; i < kVerts; ++i) diff[i] = y[i] - static_cast<float>(base[i]);
+  int32_t rank[kVerts];
+#pragma unroll
+  for (int i = 0; i < kVerts; ++i) {
+    int32_t r = 0;
+#pragma unroll
+    for (int j = 0; j < kVerts; ++j)
+      r += (diff[j] > diff[i] || (diff[j] == diff[i] && j < i)) ? 1 : 0;
+    rank[i] = r;
+  }
+#pragma unroll
+  for (int i = 0; i < kVerts; ++i) {
+    if (excess > 0) {
+      if (rank[i] >= kVerts - excess) { base[i] -= kVerts; rank[i] += excess - kVerts; }
+      else rank[i] += excess;
+    } else if (excess < 0) {
+      if (rank[i] < -excess) { base[i] += kVerts; rank[i] += kVerts + excess; }
+      else rank[i] += excess;
+    }
+  }
+  // z sorted by rank (z_0 largest), scaled by 1/(d+1)
+  float z[kVerts];
+#pragma unroll
+  for (int i = 0; i < kVerts; ++i) {
+    const float dz = (y[i] - static_cast<float>(base[i])) * 0.25f;
+#pragma unroll
+    for (int r = 0; r < kVerts; ++r)
+      if (rank[i] == r) z[r] = dz;
+  }
+  float b[kVerts];
+  b[0] = 1.0f - (z[0] - z[3]);
+  b[1] = z[2] - z[3];
+  b[2] = z[1] - z[2];
+  b[3] = z[0] - z[1];
+
+  int32_t slots[kVerts];
+#pragma unroll
+  for (int k = 0; k < kVerts; ++k) {
+    int32_t c[kVerts];
+#pragma unroll
+    for (int i = 0; i < kVerts; ++i) c[i] = base[i] + k - (rank[i] > kDim - k ? kVerts : 0);
+    if (!coords_in_range(c[0], c[1], c[2], c[3])) {
+      atomicOr(err, kErrKeyRange);
+      slots[k] = -1;
+      continue;
+    }
+    slots[k] = hash_insert(h, pack_key(c[0], c[1], c[2]), counter, vkeys, count, err);
+  }
+  slot_out[p] = make_int4(slots[0], slots[1], slots[2], slots[3]);
+  w_out[p] = make_float4(b[0], b[1], b[2], b[3]);
+}
+
+// Slot -> vertex index; count points per vertex, remembering each entry's
+// position in its vertex list.
+__global__ void __launch_bounds__(kBlock)
+k_resolve(HashView h, int32_t* __restrict__ slot_rank, int32_t* __restrict__ idx,
+          int32_t* __restrict__ count, int64_t m4) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (e >= m4) return;
+  const int32_t slot = slot_rank[e];
+  if (slot < 0) {
+    idx[e] = -1;
+    slot_rank[e] = -1;
+    return;
+  }
+  const int32_t v = h.vals[slot];
+  idx[e] = v;
+  slot_rank[e] = atomicAdd(&count[v], 1);
+}
+
+// ---- exclusive scan (three passes: tile sums, scan of sums, apply) ----
+constexpr int kScanPer = 8;
+constexpr int kScanTile = kBlock * kScanPer;
+
+__device__ inline int32_t block_exclusive_scan(int32_t v, int32_t* lds, int32_t* total) {
+  const int tid = threadIdx.x;
+  lds[tid] = v;
+  __syncthreads();
+  for (int off = 1; off < kBlock; off <<= 1) {
+    const int32_t add = tid >= off ? lds[tid - off] : 0;
+    __syncthreads();
+    lds[tid] += add;
+    __syncthreads();
+  }
+  const int32_t incl = lds[tid];
+  *total = lds[kBlock - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ void __launch_bounds__(kBlock)
+k_scan_tiles(const int32_t* __restrict__ in, int64_t n, int32_t* __restrict__ sums) {
+  __shared__ int32_t lds[kBlock];
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x * kScanPer;
+  int32_t s = 0;
+  for (int j = 0; j < kScanPer; ++j)
+    if (base + j < n) s += in[base + j];
+  int32_t total;
+  block_exclusive_scan(s, lds, &total);
+  if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ void __launch_bounds__(kBlock)
+k_scan_sums(int32_t* __restrict__ sums, int64_t nt) {
+  __shared__ int32_t lds[kBlock];
+  int32_t carry = 0;
+  for (int64_t start = 0; start < nt; start += kBlock) {
+    const int64_t i = start + threadIdx.x;
+    const int32_t v = i < nt ? sums[i] : 0;
+    int32_t total;
+    const int32_t ex = block_exclusive_scan(v, lds, &total);
+    if (i < nt) sums[i] = carry + ex;
+    carry += total;
+  }
+}
+
+__global__ void __launch_bounds__(kBlock)
+k_scan_apply(const int32_t* __restrict__ in, int64_t n, const int32_t* __restrict__ sums,
+             int32_t* __restrict__ out) {
+  __shared__ int32_t lds[kBlock];
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x * kScanPer;
+  int32_t vals[kScanPer];
+  int32_t s = 0;
+  for (int j = 0; j < kScanPer; ++j) {
+    vals[j] = base + j < n ? in[base + j] : 0;
+    s += vals[j];
+  }
+  int32_t total;
+  int32_t run = block_exclusive_scan(s, lds, &total) + sums[blockIdx.x];
+  for (int j = 0; j < kScanPer; ++j) {
+    if (base + j < n) out[base + j] = run;
+    if (base + j == n - 1) out[n] = run + vals[j];
+    run += vals[j];
+  }
+}
+
+// entries[offsets[v] + rank] = p*(d+1) + k: the points of J_v, per vertex,
+// with their barycentric weights alongside.
+__global__ void __launch_bounds__(kBlock)
+k_fill_lists(const int32_t* __restrict__ idx, const int32_t* __restrict__ rank,
+             const float* __restrict__ w, const int32_t* __restrict__ offsets,
+             int32_t* __restrict__ entries, float* __restrict__ entry_w, int64_t m4) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (e >= m4) return;
+  const int32_t v = idx[e];
+  if (v < 0) return;
+  const int32_t pos = offsets[v] + rank[e];
+  entries[pos] = static_cast<int32_t>(e);
+  entry_w[pos] = w[e];
+}
+
+// nbr[t][v] for taps 1..8 (tap 0 = v): the vertex at c_v + o_t.
+__global__ void __launch_bounds__(kBlock)
+k_neighbor_table(HashView h, const uint64_t* __restrict__ vkeys, int64_t n, int32_t* __restrict__ nbr,
+                 int64_t ldn) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n * kTaps) return;
+  const int t = static_cast<int>(i / n);
+  const int64_t v = i - static_cast<int64_t>(t) * n;
+  if (t == 0) {
+    nbr[v] = static_cast<int32_t>(v);
+    return;
+  }
+  int32_t c[kVerts];
+  unpack_key(vkeys[v], c);
+  for (int j = 0; j < kVerts; ++j) c[j] += tap_offset(t, j);
+  const uint64_t key = key_or_empty(c);
+  nbr[static_cast<int64_t>(t) * ldn + v] = key == kEmptyKey ? -1 : hash_find(h, key);
+}
+
+// Downsample: coarse vertex v reads the fine vertex at 2 c_v + o_t.
+__global__ void __launch_bounds__(kBlock)
+k_down_table(HashView fine, const uint64_t* __restrict__ ckeys, int64_t n, int32_t* __restrict__ nbr,
+             int64_t ldn) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n * kTaps) return;
+  const int t = static_cast<int>(i / n);
+  const int64_t v = i - static_cast<int64_t>(t) * n;
+  int32_t c[kVerts];
+  unpack_key(ckeys[v], c);
+  for (int j = 0; j < kVerts; ++j) c[j] = 2 * c[j] + tap_offset(t, j);
+  const uint64_t key = key_or_empty(c);
+  nbr[static_cast<int64_t>(t) * ldn + v] = key == kEmptyKey ? -1 : hash_find(fine, key);
+}
+
+// Upsample: fine vertex v reads the coarse vertex at (c_v + o_t)/2 when that
+// is a lattice point (even coordinates whose halves agree mod d+1).
+__global__ void __launch_bounds__(kBlock)
+k_up_table(HashView coarse, const uint64_t* __restrict__ fkeys, int64_t n, int32_t* __restrict__ nbr,
+           int64_t ldn) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n * kTaps) return;
+  const int t = static_cast<int>(i / n);
+  const int64_t v = i - static_cast<int64_t>(t) * n;
+  int32_t c[kVerts];
+  unpack_key(fkeys[v], c);
+  bool lattice_point = true;
+  for (int j = 0; j < kVerts; ++j) {
+    const int32_t u = c[j] + tap_offset(t, j);
+    if (u & 1) lattice_point = false;
+    c[j] = u / 2;
+  }
+  for (int j = 1; j < kVerts; ++j)
+    if ((c[j] & 3) != (c[0] & 3)) lattice_point = false;
+  int32_t found = -1;
+  if (lattice_point) {
+    const uint64_t key = key_or_empty(c);
+    if (key != kEmptyKey) found = hash_find(coarse, key);
+  }
+  nbr[static_cast<int64_t>(t) * ldn + v] = found;
+}
+
+__global__ void __launch_bounds__(kBlock)
+k_export_keys(const uint64_t* __restrict__ vkeys, int64_t n, int4* __restrict__ out) {
+  const int64_t v = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (v >= n) return;
+  int32_t c[kVerts];
+  unpack_key(vkeys[v], c);
+  out[v] = make_int4(c[0], c[1], c[2], c[3]);
+}
+
+__global__ void __launch_bounds__(kBlock)
+k_transpose_table(const int32_t* __restrict__ tab, int64_t ld, int64_t n, int32_t* __restrict__ out) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n * kTaps) return;
+  const int64_t v = i / kTaps;
+  const int t = static_cast<int>(i - v * kTaps);
+  out[i] = tab[static_cast<int64_t>(t) * ld + v];
+}
+
+inline unsigned blocks_for(int64_t n) { return static_cast<unsigned>((n + kBlock - 1) / kBlock); }
+
+}  // namespace
+
+void launch_fill_u64(uint64_t* p, uint64_t v, int64_t n, hipStream_t s) {
+  if (n <= 0) return;
+  const int64_t want = (n + kBlock * 4 - 1) / (kBlock * 4);
+  const unsigned grid = static_cast<unsigned>(want < 8192 ? want : 8192);
+  ScopedKernelTimer tm("fill", s);
+  hipLaunchKernelGGL(k_fill_u64, dim3(grid), dim3(kBlock), 0, s, p, v, n);
+}
+
+void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
+                          float a2, int64_t m, HashView h, int32_t* counter, uint64_t* vkeys,
+                          int32_t* count, int32_t* slot_out, float* w_out, float* y_out,
+                          uint32_t* err, hipStream_t s) {
+  if (m <= 0) return;
+  ScopedKernelTimer tm("insert", s);
+  hipLaunchKernelGGL(k_insert_points, dim3(blocks_for(m)), dim3(kBlock), 0, s, pos,
+                     reinterpret_cast<const float4*>(y_in), y_scale, a0, a1, a2, m, h, counter,
+                     vkeys, count, reinterpret_cast<int4*>(slot_out),
+                     reinterpret_cast<float4*>(w_out), reinterpret_cast<float4*>(y_out), err);
+}
+
+void launch_resolve(HashView h, int32_t* slot_rank, int32_t* idx, int32_t* count, int64_t m4,
+                    hipStream_t s) {
+  if (m4 <= 0) return;
+  ScopedKernelTimer tm("resolve", s);
+  hipLaunchKernelGGL(k_resolve, dim3(blocks_for(m4)), dim3(kBlock), 0, s, h, slot_rank, idx, count, m4);
+}
+
+int64_t scan_workspace_elems(int64_t n) { return (n + kScanTile - 1) / kScanTile + 1; }
+
+void launch_exclusive_scan(const int32_t* in, int32_t* out, int64_t n, int32_t* work, hipStream_t s) {
+  if (n <= 0) return;
+  const int64_t nt = (n + kScanTile - 1) / kScanTile;
+  ScopedKernelTimer tm("scan", s);
+  hipLaunchKernelGGL(k_scan_tiles, dim3(static_cast<unsigned>(nt)), dim3(kBlock), 0, s, in, n, work);
+  hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(kBlock), 0, s, work, nt);
+  hipLaunchKernelGGL(k_scan_apply, dim3(static_cast<unsigned>(nt)), dim3(kBlock), 0, s, in, n, work, out);
+}
+
+void launch_fill_lists(const int32_t* idx, const int32_t* rank, const float* w,
+                       const int32_t* offsets, int32_t* entries, float* entry_w, int64_t m4,
+                       hipStream_t s) {
+  if (m4 <= 0) return;
+  ScopedKernelTimer tm("lists", s);
+  hipLaunchKernelGGL(k_fill_lists, dim3(blocks_for(m4)), dim3(kBlock), 0, s, idx, rank, w, offsets,
+                     entries, entry_w, m4);
+}
+
+void launch_neighbor_table(HashView h, const uint64_t* vkeys, int64_t n, int32_t* nbr, int64_t ldn,
+                           hipStream_t s) {
+  if (n <= 0) return;
+  ScopedKernelTimer tm("nbr", s);
+  hipLaunchKernelGGL(k_neighbor_table, dim3(blocks_for(n * kTaps)), dim3(kBlock), 0, s, h, vkeys, n,
+                     nbr, ldn);
+}
+
+void launch_down_table(HashView fine, const uint64_t* coarse_keys, int64_t n_coarse, int32_t* nbr,
+                       int64_t ldn, hipStream_t s) {
+  if (n_coarse <= 0) return;
+  ScopedKernelTimer tm("nbr", s);
+  hipLaunchKernelGGL(k_down_table, dim3(blocks_for(n_coarse * kTaps)), dim3(kBlock), 0, s, fine,
+                     coarse_keys, n_coarse, nbr, ldn);
+}
+
+void launch_up_table(HashView coarse, const uint64_t* fine_keys, int64_t n_fine, int32_t* nbr,
+                     int64_t ldn, hipStream_t s) {
+  if (n_fine <= 0) return;
+  ScopedKernelTimer tm("nbr", s);
+  hipLaunchKernelGGL(k_up_table, dim3(blocks_for(n_fine * kTaps)), dim3(kBlock), 0, s, coarse,
+                     fine_keys, n_fine, nbr, ldn);
+}
+
+void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s) {
+  if (n <= 0) return;
+  hipLaunchKernelGGL(k_export_keys, dim3(blocks_for(n)), dim3(kBlock), 0, s, vkeys, n,
+                     reinterpret_cast<int4*>(out));
+}
+
+void launch_transpose_table(const int32_t* tab, int64_t ld, int64_t n, int32_t* out, hipStream_t s) {
+  if (n <= 0) return;
+  hipLaunchKernelGGL(k_transpose_table, dim3(blocks_for(n * kTaps)), dim3(kBlock), 0, s, tab, ld, n, out);
+}
+
+}  // namespace lat

@@ -1,0 +1,139 @@
+// Internal declarations of liblattice (gfx950).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "lattice.h"
+
+namespace lat {
+
+constexpr int kDim = 3;                 // d
+constexpr int kVerts = kDim + 1;        // d+1 vertices per simplex, coordinates per key
+constexpr int kTaps = 2 * kVerts + 1;   // 1-hop neighbourhood incl. the centre
+constexpr int kCoordBits = 21;
+constexpr int32_t kCoordLimit = 1 << 20;          // |c_i| < 2^20
+constexpr uint64_t kEmptyKey = ~0ull;             // bit 63 set: never a packed key
+
+// error bits raised by kernels into the handle's device flag
+enum : uint32_t { kErrHashFull = 1u, kErrKeyRange = 2u, kErrNonFinite = 4u };
+
+// Packed key: the first d coordinates, each biased by 2^20 into 21 bits
+// (the last coordinate is minus their sum).  Unsigned order of packed keys is
+// the lexicographic order of the coordinates.
+__host__ __device__ inline bool coords_in_range(int32_t c0, int32_t c1, int32_t c2, int32_t c3) {
+  return c0 > -kCoordLimit && c0 < kCoordLimit && c1 > -kCoordLimit && c1 < kCoordLimit &&
+         c2 > -kCoordLimit && c2 < kCoordLimit && c3 > -kCoordLimit && c3 < kCoordLimit;
+}
+
+__host__ __device__ inline uint64_t pack_key(int32_t c0, int32_t c1, int32_t c2) {
+  return (static_cast<uint64_t>(static_cast<uint32_t>(c0 + kCoordLimit)) << (2 * kCoordBits)) |
+         (static_cast<uint64_t>(static_cast<uint32_t>(c1 + kCoordLimit)) << kCoordBits) |
+         static_cast<uint64_t>(static_cast<uint32_t>(c2 + kCoordLimit));
+}
+
+__host__ __device__ inline void unpack_key(uint64_t k, int32_t c[kVerts]) {
+  const uint64_t mask = (1ull << kCoordBits) - 1;
+  c[0] = static_cast<int32_t>((k >> (2 * kCoordBits)) & mask) - kCoordLimit;
+  c[1] = static_cast<int32_t>((k >> kCoordBits) & mask) - kCoordLimit;
+  c[2] = static_cast<int32_t>(k & mask) - kCoordLimit;
+  c[3] = -(c[0] + c[1] + c[2]);
+}
+
+// Slot hash: the murmur3 64-bit finaliser.
+__host__ __device__ inline uint64_t hash_key(uint64_t k) {
+  k ^= k >> 33;
+  k *= 0xff51afd7ed558ccdull;
+  k ^= k >> 33;
+  k *= 0xc4ceb9fe1a85ec53ull;
+  k ^= k >> 33;
+  return k;
+}
+
+// Open-addressing table with linear probing.  keys[slot] is kEmptyKey or a
+// packed key; vals[slot] the vertex index of that key.
+struct HashView {
+  uint64_t* keys;
+  int32_t* vals;
+  uint64_t mask;      // capacity - 1 (capacity a power of two)
+};
+
+// Look up a key; -1 when absent.  The table is not modified concurrently.
+__device__ inline int32_t hash_find(const HashView& h, uint64_t key) {
+  uint64_t slot = hash_key(key) & h.mask;
+  for (uint64_t probe = 0; probe <= h.mask; ++probe) {
+    const uint64_t k = h.keys[slot];
+    if (k == key) return h.vals[slot];
+    if (k == kEmptyKey) return -1;
+    slot = (slot + 1) & h.mask;
+  }
+  return -1;
+}
+
+// Key of lattice point c (d+1 coordinates), or kEmptyKey when c is out of
+// range (such a point can never be a vertex).
+__device__ inline uint64_t key_or_empty(const int32_t c[kVerts]) {
+  return coords_in_range(c[0], c[1], c[2], c[3]) ? pack_key(c[0], c[1], c[2]) : kEmptyKey;
+}
+
+// Tap offsets o_t: 0; +n_j; -n_j with n_j = (d+1) e_j - 1.
+__device__ inline int32_t tap_offset(int t, int i) {
+  if (t == 0) return 0;
+  const int j = (t - 1) & 3;
+  const int32_t v = (i == j ? kVerts : 0) - 1;
+  return t <= kVerts ? v : -v;
+}
+
+// ---------------------------------------------------------------------------
+// host-side pieces shared by the translation units
+// ---------------------------------------------------------------------------
+struct Timer;   // kernel-family event timer (api.hip)
+void timer_begin(const char* family, hipStream_t s);
+void timer_end(const char* family, hipStream_t s);
+
+struct ScopedKernelTimer {
+  const char* fam;
+  hipStream_t s;
+  ScopedKernelTimer(const char* f, hipStream_t st) : fam(f), s(st) { timer_begin(fam, s); }
+  ~ScopedKernelTimer() { timer_end(fam, s); }
+};
+
+// Launchers (each .hip file implements its own kernels' launchers).
+// create.hip
+void launch_fill_u64(uint64_t* p, uint64_t v, int64_t n, hipStream_t s);
+void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
+                          float a2, int64_t m, HashView h, int32_t* counter, uint64_t* vkeys,
+                          int32_t* count, int32_t* slot_out, float* w_out, float* y_out,
+                          uint32_t* err, hipStream_t s);
+void launch_resolve(HashView h, int32_t* slot_rank, int32_t* idx, int32_t* count, int64_t m4,
+                    hipStream_t s);
+int64_t scan_workspace_elems(int64_t n);
+void launch_exclusive_scan(const int32_t* in, int32_t* out, int64_t n, int32_t* work, hipStream_t s);
+void launch_fill_lists(const int32_t* idx, const int32_t* rank, const float* w,
+                       const int32_t* offsets, int32_t* entries, float* entry_w, int64_t m4,
+                       hipStream_t s);
+void launch_neighbor_table(HashView h, const uint64_t* vkeys, int64_t n, int32_t* nbr, int64_t ldn,
+                           hipStream_t s);
+void launch_down_table(HashView fine, const uint64_t* coarse_keys, int64_t n_coarse, int32_t* nbr,
+                       int64_t ldn, hipStream_t s);
+void launch_up_table(HashView coarse, const uint64_t* fine_keys, int64_t n_fine, int32_t* nbr,
+                     int64_t ldn, hipStream_t s);
+void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s);
+void launch_transpose_table(const int32_t* tab, int64_t ld, int64_t n, int32_t* out, hipStream_t s);
+// splat_slice.hip
+void launch_splat(const int32_t* offsets, const int32_t* entries, const float* entry_w, const void* feat,
+                  int64_t ld_feat, int C, int bf16, int normalize, int64_t n, void* vals,
+                  int64_t ld_vals, float* wsum, hipStream_t s);
+void launch_slice(const int32_t* idx, const float* w, int64_t m, const void* vals, int64_t ld_vals,
+                  int C, int bf16, float* out, hipStream_t s);
+void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const void* vals,
+                         int64_t ld_vals, int C, int bf16, const float* wv, float beta, float* out,
+                         float* delta, hipStream_t s);
+// conv.hip
+void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
+                 int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
+                 int64_t ld_out, hipStream_t s);
+
+}  // namespace lat

@@ -1,0 +1,239 @@
+"""Python binding of liblattice (ctypes).
+
+Argument marshalling only: every lattice operation runs in the library's HIP
+kernels.  PyTorch supplies device memory (tensors) and the current HIP
+stream.  The library must be built (``python -m paper_1912_05905_amd.build``);
+importing this module without it raises, there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblattice.so")
+
+LAT_F32, LAT_BF16 = 0, 1
+LAT_RELU = 1
+TAPS = 9
+STATUS = {0: "LAT_OK", -1: "LAT_EINVAL", -2: "LAT_EUNSUPPORTED", -3: "LAT_ENOMEM",
+          -4: "LAT_EHASHFULL", -5: "LAT_EKEYRANGE", -6: "LAT_ENONFINITE", -7: "LAT_EDEVICE",
+          -8: "LAT_ELEVEL"}
+
+_lib = None
+
+# exported entry points and their argument types
+_P, _I64, _I32, _F32 = C.c_void_p, C.c_int64, C.c_int, C.c_float
+SIGNATURES = {
+    "lattice_last_error": (C.c_char_p, []),
+    "lattice_status_string": (C.c_char_p, [_I32]),
+    "lattice_create": (_I32, [_P, _I64, _I32, _P, _I64, _P, C.POINTER(_P)]),
+    "lattice_coarsen": (_I32, [_P, _I64, _P, C.POINTER(_P)]),
+    "lattice_destroy": (_I32, [_P]),
+    "lattice_num_vertices": (_I32, [_P, C.POINTER(_I64)]),
+    "lattice_num_points": (_I32, [_P, C.POINTER(_I64)]),
+    "lattice_level": (_I32, [_P, C.POINTER(_I32)]),
+    "lattice_export_keys": (_I32, [_P, _P, _P]),
+    "lattice_export_simplices": (_I32, [_P, _P, _P, _P]),
+    "lattice_export_neighbors": (_I32, [_P, _P, _P]),
+    "lattice_splat": (_I32, [_P, _P, _I64, _I32, _I32, _I32, _P, _I64, _P, _P]),
+    "lattice_conv": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _I32, _I32, _P, _I64, _P]),
+    "lattice_refine": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _I32, _I32, _P, _I64, _P]),
+    "lattice_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
+    "lattice_deform_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _P]),
+    "lattice_timing_enable": (_I32, [C.c_char_p, _I32]),
+    "lattice_timing_read": (_I32, [C.c_char_p, C.POINTER(_I64), C.POINTER(C.c_double)]),
+}
+
+
+class LatticeError(RuntimeError):
+    def __init__(self, status: int, text: str):
+        super().__init__(text or STATUS.get(status, str(status)))
+        self.status = status
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with python -m paper_1912_05905_amd.build")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise LatticeError(status, lib().lattice_last_error().decode())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return C.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return LAT_F32
+    if t.dtype == torch.bfloat16:
+        return LAT_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _rows(t: torch.Tensor):
+    """(pointer, row stride) of a row-major matrix or a column slice of one."""
+    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError("expected a 2-D tensor with unit column stride")
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    return C.c_void_p(t.data_ptr()), t.stride(0)
+
+
+def timing_enable(family: str, enable: bool = True):
+    _check(lib().lattice_timing_enable(family.encode(), int(enable)))
+
+
+def timing_read(family: str):
+    n = C.c_int64()
+    ms = C.c_double()
+    _check(lib().lattice_timing_read(family.encode(), C.byref(n), C.byref(ms)))
+    return int(n.value), float(ms.value)
+
+
+class Lattice:
+    """A sparse permutohedral lattice owned by liblattice."""
+
+    def __init__(self, handle: C.c_void_p, parent: "Lattice | None" = None):
+        self._h = handle
+        self.parent = parent
+        n, m, lv = C.c_int64(), C.c_int64(), C.c_int()
+        _check(lib().lattice_num_vertices(handle, C.byref(n)))
+        _check(lib().lattice_num_points(handle, C.byref(m)))
+        _check(lib().lattice_level(handle, C.byref(lv)))
+        self.n, self.m, self.level = int(n.value), int(m.value), int(lv.value)
+
+    # ---- construction ----
+    @classmethod
+    def create(cls, pos: torch.Tensor, sigma, capacity_hint: int = 0, stream=None) -> "Lattice":
+        if pos.dtype != torch.float32 or pos.dim() != 2 or not pos.is_contiguous():
+            raise ValueError("positions must be a contiguous m x d float32 tensor")
+        sig = (C.c_float * pos.shape[1])(*[float(s) for s in sigma])
+        h = C.c_void_p()
+        _check(lib().lattice_create(C.c_void_p(pos.data_ptr()), pos.shape[0], pos.shape[1], sig,
+                                    int(capacity_hint), _stream(stream), C.byref(h)))
+        return cls(h)
+
+    def coarsen(self, capacity_hint: int = 0, stream=None) -> "Lattice":
+        h = C.c_void_p()
+        _check(lib().lattice_coarsen(self._h, int(capacity_hint), _stream(stream), C.byref(h)))
+        return Lattice(h, parent=self)
+
+    def destroy(self):
+        if getattr(self, "_h", None):
+            _check(lib().lattice_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            if getattr(self, "_h", None) and _lib is not None:
+                _lib.lattice_destroy(self._h)
+                self._h = None
+        except Exception:
+            pass
+
+    @property
+    def handle(self):
+        return self._h
+
+    # ---- structure export ----
+    def keys(self, stream=None) -> torch.Tensor:
+        k = torch.empty((self.n, 4), dtype=torch.int32, device="cuda")
+        _check(lib().lattice_export_keys(self._h, C.c_void_p(k.data_ptr()), _stream(stream)))
+        return k
+
+    def simplices(self, stream=None):
+        idx = torch.empty((self.m, 4), dtype=torch.int32, device="cuda")
+        w = torch.empty((self.m, 4), dtype=torch.float32, device="cuda")
+        _check(lib().lattice_export_simplices(self._h, C.c_void_p(idx.data_ptr()),
+                                              C.c_void_p(w.data_ptr()), _stream(stream)))
+        return idx, w
+
+    def neighbors(self, stream=None) -> torch.Tensor:
+        nb = torch.empty((self.n, TAPS), dtype=torch.int32, device="cuda")
+        _check(lib().lattice_export_neighbors(self._h, C.c_void_p(nb.data_ptr()), _stream(stream)))
+        return nb
+
+    # ---- operators ----
+    def splat(self, feat: torch.Tensor, normalize: bool = True, out: torch.Tensor | None = None,
+              wsum: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        Cc = feat.shape[1]
+        if out is None:
+            out = torch.empty((self.n, Cc), dtype=feat.dtype, device="cuda")
+        fp, fld = _rows(feat)
+        op, old = _rows(out)
+        _check(lib().lattice_splat(self._h, fp, fld, Cc, _dtype_code(feat), int(bool(normalize)),
+                                   op, old, None if wsum is None else C.c_void_p(wsum.data_ptr()),
+                                   _stream(stream)))
+        return out
+
+    def conv(self, src: "Lattice", x: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = None,
+             relu: bool = False, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """self is the destination lattice: src itself (1-hop) or its parent
+        (strided convolution).  W is taps x Cout x Cin."""
+        cout, cin = W.shape[1], W.shape[2]
+        if out is None:
+            out = torch.empty((self.n, cout), dtype=x.dtype, device="cuda")
+        xp, xld = _rows(x)
+        op, old = _rows(out)
+        if not W.is_contiguous() or W.dtype != x.dtype:
+            raise ValueError("W must be contiguous with the dtype of x")
+        _check(lib().lattice_conv(self._h, src._h, xp, xld, cin, C.c_void_p(W.data_ptr()),
+                                  None if bias is None else C.c_void_p(bias.data_ptr()), cout,
+                                  _dtype_code(x), LAT_RELU if relu else 0, op, old, _stream(stream)))
+        return out
+
+    def refine(self, coarse: "Lattice", x: torch.Tensor, W: torch.Tensor,
+               bias: torch.Tensor | None = None, relu: bool = False, out: torch.Tensor | None = None,
+               stream=None) -> torch.Tensor:
+        """self is the fine lattice; coarse = self.coarsen()."""
+        cout, cin = W.shape[1], W.shape[2]
+        if out is None:
+            out = torch.empty((self.n, cout), dtype=x.dtype, device="cuda")
+        xp, xld = _rows(x)
+        op, old = _rows(out)
+        if not W.is_contiguous() or W.dtype != x.dtype:
+            raise ValueError("W must be contiguous with the dtype of x")
+        _check(lib().lattice_refine(self._h, coarse._h, xp, xld, cin, C.c_void_p(W.data_ptr()),
+                                    None if bias is None else C.c_void_p(bias.data_ptr()), cout,
+                                    _dtype_code(x), LAT_RELU if relu else 0, op, old, _stream(stream)))
+        return out
+
+    def slice(self, x: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        Cc = x.shape[1]
+        if out is None:
+            out = torch.empty((self.m, Cc), dtype=torch.float32, device="cuda")
+        xp, xld = _rows(x)
+        _check(lib().lattice_slice(self._h, xp, xld, Cc, _dtype_code(x), C.c_void_p(out.data_ptr()),
+                                   _stream(stream)))
+        return out
+
+    def deform_slice(self, x: torch.Tensor, wv: torch.Tensor, beta: float,
+                     out: torch.Tensor | None = None, delta: torch.Tensor | None = None,
+                     stream=None) -> torch.Tensor:
+        Cc = x.shape[1]
+        if out is None:
+            out = torch.empty((self.m, Cc), dtype=torch.float32, device="cuda")
+        xp, xld = _rows(x)
+        _check(lib().lattice_deform_slice(self._h, xp, xld, Cc, _dtype_code(x),
+                                          C.c_void_p(wv.data_ptr()), float(beta),
+                                          C.c_void_p(out.data_ptr()),
+                                          None if delta is None else C.c_void_p(delta.data_ptr()),
+                                          _stream(stream)))
+        return out

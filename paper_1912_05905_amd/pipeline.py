@@ -1,0 +1,77 @@
+"""Run a workload's lattice pipeline on the GPU through liblattice.
+
+A workload (see workloads.configs) lists lattice operations; this runner
+executes them in order: lattices are created / coarsened per step, values
+live in device buffers (row-major, vertices of their level x channels), and
+each operation reads / writes a column range of a buffer, which gives channel
+concatenation without copies.  All arithmetic happens in the library's
+kernels; torch only allocates the buffers.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from .lattice import Lattice
+
+
+class GpuPipeline:
+    def __init__(self, wl):
+        self.wl = wl
+        self.dtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+        self.pos = torch.from_numpy(np.ascontiguousarray(wl.positions)).cuda()
+        self.feat = torch.from_numpy(np.ascontiguousarray(wl.features)).cuda().to(self.dtype)
+        # library weight layout: taps x Cout x Cin
+        self.weights = {k: torch.from_numpy(np.ascontiguousarray(np.transpose(w, (0, 2, 1))))
+                        .cuda().to(self.dtype).contiguous() for k, w in wl.weights.items()}
+        self.vectors = {k: (torch.from_numpy(np.ascontiguousarray(v)).cuda(), float(beta))
+                        for k, (v, beta) in wl.vectors.items()}
+        self.sigma = [float(s) for s in wl.sigma]
+
+    def _view(self, bufs, levels, spec):
+        name, c0, cc = spec
+        if name not in bufs:
+            lv, total = self.wl.buffers[name]
+            bufs[name] = torch.empty((levels[lv].n, total), dtype=self.dtype, device="cuda")
+        return bufs[name][:, c0:c0 + cc]
+
+    def step(self, keep=False):
+        """One pass of the pipeline.  Returns (levels, buffers, point outputs)."""
+        levels: dict[int, Lattice] = {}
+        bufs: dict[str, torch.Tensor] = {}
+        outs: dict[str, torch.Tensor] = {}
+        for op in self.wl.ops:
+            kind = op["op"]
+            if kind == "create":
+                levels[0] = Lattice.create(self.pos, self.sigma)
+            elif kind == "coarsen":
+                levels[op["level"]] = levels[op["level"] - 1].coarsen()
+            elif kind == "splat":
+                levels[0].splat(self.feat, normalize=bool(op["normalize"]),
+                                out=self._view(bufs, levels, op["dst"]))
+            elif kind in ("conv", "conv_down", "refine"):
+                lv = op["level"]
+                x = self._view(bufs, levels, op["src"])
+                y = self._view(bufs, levels, op["dst"])
+                W = self.weights[op["w"]]
+                if kind == "conv":
+                    levels[lv].conv(levels[lv], x, W, relu=op["relu"], out=y)
+                elif kind == "conv_down":
+                    levels[lv].conv(levels[lv - 1], x, W, relu=op["relu"], out=y)
+                else:
+                    levels[lv].refine(levels[lv + 1], x, W, relu=op["relu"], out=y)
+            elif kind == "slice":
+                outs[op["out"]] = levels[op["level"]].slice(self._view(bufs, levels, op["src"]))
+            elif kind == "deform_slice":
+                wv, beta = self.vectors[op["wv"]]
+                outs[op["out"]] = levels[op["level"]].deform_slice(
+                    self._view(bufs, levels, op["src"]), wv, beta)
+            else:
+                raise ValueError(f"unknown op {kind}")
+        return levels, bufs, outs
+
+    @staticmethod
+    def release(levels):
+        """Destroy lattices finest-last (children before parents)."""
+        for lv in sorted(levels, reverse=True):
+            levels[lv].destroy()

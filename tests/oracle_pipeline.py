@@ -1,0 +1,65 @@
+"""Run a workload's pipeline on the CPU oracle (test infrastructure).
+
+Mirrors the operation list of workloads.configs with the oracle's functions:
+float64 buffers, and in bf16 workloads every stored activation is rounded to
+bfloat16 where the GPU stores bf16 (splat, convolution outputs).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import oracle as O
+
+
+class OraclePipeline:
+    def __init__(self, wl):
+        self.wl = wl
+        self.bf16 = wl.dtype == "bf16"
+
+    def _store(self, x):
+        return O.round_bf16(x) if self.bf16 else x
+
+    def run(self, stop_after=None):
+        wl = self.wl
+        levels, bufs, outs = {}, {}, {}
+
+        def view_src(spec):
+            name, c0, cc = spec
+            return bufs[name][:, c0:c0 + cc]
+
+        def write(spec, val):
+            name, c0, cc = spec
+            if name not in bufs:
+                lv, total = wl.buffers[name]
+                bufs[name] = np.zeros((levels[lv].n, total))
+            bufs[name][:, c0:c0 + cc] = self._store(val)
+
+        for i, op in enumerate(wl.ops):
+            kind = op["op"]
+            if kind == "create":
+                levels[0] = O.Lattice.create(wl.positions, wl.sigma)
+            elif kind == "coarsen":
+                levels[op["level"]] = levels[op["level"] - 1].coarsen()
+            elif kind == "splat":
+                X, _ = levels[0].splat(wl.features.astype(np.float64), normalize=bool(op["normalize"]))
+                write(op["dst"], X)
+            elif kind in ("conv", "conv_down", "refine"):
+                lv = op["level"]
+                x = np.ascontiguousarray(view_src(op["src"]))
+                W = wl.weights[op["w"]].astype(np.float64)
+                if kind == "conv":
+                    y = levels[lv].conv(levels[lv], x, W, relu=op["relu"])
+                elif kind == "conv_down":
+                    y = levels[lv].conv(levels[lv - 1], x, W, relu=op["relu"])
+                else:
+                    y = levels[lv].refine_into(levels[lv + 1], x, W, relu=op["relu"])
+                write(op["dst"], y)
+            elif kind == "slice":
+                outs[op["out"]] = levels[op["level"]].slice(np.ascontiguousarray(view_src(op["src"])))
+            elif kind == "deform_slice":
+                wv, beta = wl.vectors[op["wv"]]
+                outs[op["out"]], _ = levels[op["level"]].deform_slice(
+                    np.ascontiguousarray(view_src(op["src"])), wv.astype(np.float64), beta)
+            if stop_after is not None and i == stop_after:
+                break
+        return levels, bufs, outs

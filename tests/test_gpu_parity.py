@@ -1,0 +1,364 @@
+"""GPU parity: liblattice (HIP, gfx950) against the CPU oracle.
+
+Structure (vertex keys, per-point simplices and weights, neighbour tables)
+must match bit for bit after ordering vertices by key; features within
+1e-4 (fp32) / 2e-2 (bf16) in the per-tensor relative-plus-RMS bound.
+Every call goes through the C ABI via the ctypes binding.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from tests import parity as P
+from tests.oracle_pipeline import OraclePipeline
+from workloads import configs
+from workloads.rng import Stream
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1912_05905_amd import lattice
+    lattice.lib()
+    return lattice
+
+
+@pytest.fixture(scope="module")
+def O():
+    from oracle import oracle
+    oracle.lib()
+    return oracle
+
+
+def _cloud(seed, m, extent=1.0):
+    st = Stream(seed, "gpu-cloud")
+    return (extent * st.uniform(3 * m).reshape(m, 3)).astype(np.float32)
+
+
+def _dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return t if dtype is None else t.to(dtype)
+
+
+def _host(t):
+    torch.cuda.synchronize()
+    return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+
+def _check_structure(gl, ol):
+    """Keys, simplices and neighbour table bit-exact; returns gpu2orc."""
+    assert gl.n == ol.n and gl.m == ol.m
+    g2o = P.key_permutation(_host(gl.keys()), ol.keys())
+    gidx, gw = gl.simplices()
+    oidx, ow = ol.simplices()
+    assert np.array_equal(P.remap_index(_host(gidx), g2o), oidx), "simplex vertices differ"
+    assert np.array_equal(_host(gw), ow), "barycentric weights differ"
+    gnb = P.rows_in_oracle_order(P.remap_index(_host(gl.neighbors()), g2o), g2o)
+    assert np.array_equal(gnb, ol.neighbors()), "neighbour tables differ"
+    return g2o
+
+
+# ----------------------------------------------------------------------------
+# structure
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("seed,m,sigma", [(0, 1, 0.1), (1, 37, 0.1), (2, 1000, 0.05),
+                                          (3, 4097, 0.1), (4, 20_000, 0.03)])
+def test_create_structure_random(L, O, seed, m, sigma):
+    pos = _cloud(seed, m)
+    gl = L.Lattice.create(_dev(pos), [sigma] * 3)
+    ol = O.Lattice.create(pos, np.full(3, sigma, np.float32))
+    _check_structure(gl, ol)
+
+
+def test_create_structure_adversarial(L, O):
+    """Points on lattice vertices, faces and ties; duplicates; one simplex
+    shared by thousands of points (insert contention)."""
+    a = O.axis_factors(np.ones(3, np.float32)).astype(np.float64)
+    grid = np.stack(np.meshgrid(*[np.arange(-3, 4)] * 3, indexing="ij"), -1).reshape(-1, 3) / a
+    half = grid * 0.5
+    same = np.tile(np.array([[0.123, 0.456, 0.789]]), (5000, 1))
+    pos = np.concatenate([grid, half, same, grid[:50]], 0).astype(np.float32)
+    gl = L.Lattice.create(_dev(pos), [1.0] * 3)
+    ol = O.Lattice.create(pos, np.ones(3, np.float32))
+    _check_structure(gl, ol)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_create_structure_configs(L, O, cfg):
+    wl = configs.make(cfg)
+    gl = L.Lattice.create(_dev(wl.positions), wl.sigma)
+    ol = O.Lattice.create(wl.positions, wl.sigma)
+    _check_structure(gl, ol)
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_coarsen_structure(L, O, cfg):
+    wl = configs.make(cfg)
+    gl = L.Lattice.create(_dev(wl.positions), wl.sigma)
+    ol = O.Lattice.create(wl.positions, wl.sigma)
+    glv, olv = [gl], [ol]
+    for lvl in range(1, 4):
+        glv.append(glv[-1].coarsen())
+        olv.append(olv[-1].coarsen())
+        assert glv[-1].level == lvl
+        _check_structure(glv[-1], olv[-1])
+
+
+def test_empty_cloud(L):
+    gl = L.Lattice.create(torch.zeros((0, 3), device="cuda"), [0.1] * 3)
+    assert gl.n == 0 and gl.m == 0
+    x = gl.splat(torch.zeros((0, 8), device="cuda"))
+    assert x.shape == (0, 8)
+    y = gl.conv(gl, x, torch.zeros((9, 16, 8), device="cuda"))
+    assert y.shape == (0, 16)
+    assert gl.slice(y).shape == (0, 16)
+    c = gl.coarsen()
+    assert c.n == 0
+
+
+# ----------------------------------------------------------------------------
+# errors found on the device
+# ----------------------------------------------------------------------------
+def test_device_errors(L):
+    pos = _cloud(5, 1000)
+    bad = pos.copy()
+    bad[17, 1] = np.nan
+    with pytest.raises(L.LatticeError) as e:
+        L.Lattice.create(_dev(bad), [0.1] * 3)
+    assert e.value.status == -6
+    far = pos.copy()
+    far[3] = [1e6, 0, 0]
+    with pytest.raises(L.LatticeError) as e:
+        L.Lattice.create(_dev(far), [0.1] * 3)
+    assert e.value.status == -5
+    with pytest.raises(L.LatticeError) as e:
+        L.Lattice.create(_dev(_cloud(6, 5000)), [0.01] * 3, capacity_hint=16)
+    assert e.value.status == -4
+    # the library stays usable after device-side errors
+    ok = L.Lattice.create(_dev(pos), [0.1] * 3)
+    assert ok.n > 0
+
+
+def test_host_validation_on_gpu(L):
+    gl = L.Lattice.create(_dev(_cloud(7, 500)), [0.1] * 3)
+    x = torch.zeros((gl.n, 6), device="cuda")
+    with pytest.raises(L.LatticeError) as e:
+        gl.conv(gl, x, torch.zeros((9, 8, 6), device="cuda"))     # Cin % 4 != 0
+    assert e.value.status == -2
+    x = torch.zeros((gl.n, 8), device="cuda")
+    with pytest.raises(L.LatticeError) as e:
+        gl.conv(gl, x, torch.zeros((9, 8, 8), device="cuda"), out=x)   # in == out
+    assert e.value.status == -1
+    other = L.Lattice.create(_dev(_cloud(8, 500)), [0.1] * 3)
+    with pytest.raises(L.LatticeError) as e:
+        gl.conv(other, x, torch.zeros((9, 8, 8), device="cuda"))
+    assert e.value.status == -8
+    c = gl.coarsen()
+    with pytest.raises(L.LatticeError) as e:
+        gl.destroy()                                               # child alive
+    assert e.value.status == -8
+    c.destroy()
+    gl.destroy()
+
+
+# ----------------------------------------------------------------------------
+# operators, one at a time, on the oracle's own inputs
+# ----------------------------------------------------------------------------
+def _pair(L, O, pos, sigma):
+    gl = L.Lattice.create(_dev(pos), [sigma] * 3)
+    ol = O.Lattice.create(pos, np.full(3, sigma, np.float32))
+    g2o = P.key_permutation(_host(gl.keys()), ol.keys())
+    return gl, ol, g2o
+
+
+@pytest.mark.parametrize("C,normalize", [(4, True), (8, True), (36, False), (64, True), (256, True)])
+def test_splat(L, O, C, normalize):
+    pos = _cloud(10 + C, 9000, 0.7)
+    gl, ol, g2o = _pair(L, O, pos, 0.06)
+    F = np.random.default_rng(C).normal(size=(pos.shape[0], C)).astype(np.float32)
+    ws = torch.empty(gl.n, device="cuda")
+    gx = gl.splat(_dev(F), normalize=normalize, wsum=ws)
+    ox, ow = ol.splat(F.astype(np.float64), normalize=normalize)
+    P.assert_close(P.rows_in_oracle_order(_host(gx), g2o), ox, P.TOL_F32, "splat")
+    P.assert_close(P.rows_in_oracle_order(_host(ws), g2o), ow, P.TOL_F32, "wsum")
+
+
+def test_splat_bf16(L, O):
+    pos = _cloud(31, 9000, 0.7)
+    gl, ol, g2o = _pair(L, O, pos, 0.06)
+    F = np.random.default_rng(3).normal(size=(pos.shape[0], 64)).astype(np.float32)
+    Fb = O.round_bf16(F)
+    gx = gl.splat(_dev(Fb.astype(np.float32), torch.bfloat16))
+    ox, _ = ol.splat(Fb)
+    P.assert_close(P.rows_in_oracle_order(_host(gx), g2o), O.round_bf16(ox), P.TOL_BF16, "splat bf16")
+
+
+def _rand_w(rng, cin, cout, std):
+    return (std * rng.normal(size=(9, cin, cout))).astype(np.float32)
+
+
+def _gpu_w(W, dtype=torch.float32):
+    return _dev(np.ascontiguousarray(np.transpose(W, (0, 2, 1))), dtype).contiguous()
+
+
+@pytest.mark.parametrize("cin,cout", [(8, 16), (4, 4), (12, 20), (64, 64), (32, 96), (128, 128),
+                                      (256, 64)])
+def test_conv_fp32(L, O, cin, cout):
+    pos = _cloud(40 + cin, 6000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.07)
+    rng = np.random.default_rng(cin * 1000 + cout)
+    X = rng.normal(size=(ol.n, cin)).astype(np.float32)
+    W = _rand_w(rng, cin, cout, 1.0 / np.sqrt(9 * cin))
+    b = rng.normal(size=cout).astype(np.float32)
+    Xg = np.empty_like(X)
+    Xg[np.arange(ol.n)] = X[g2o]          # GPU row v holds oracle row g2o[v]
+    for relu in (False, True):
+        gy = gl.conv(gl, _dev(Xg), _gpu_w(W), bias=_dev(b), relu=relu)
+        oy = ol.conv(ol, X.astype(np.float64), W.astype(np.float64), bias=b.astype(np.float64), relu=relu)
+        P.assert_close(P.rows_in_oracle_order(_host(gy), g2o), oy, P.TOL_F32, f"conv {cin}->{cout}")
+
+
+@pytest.mark.parametrize("cin,cout", [(64, 64), (8, 24), (128, 192), (384, 192), (256, 256)])
+def test_conv_bf16(L, O, cin, cout):
+    pos = _cloud(50 + cin, 6000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.07)
+    rng = np.random.default_rng(cin + 7 * cout)
+    X = O.round_bf16(rng.normal(size=(ol.n, cin)))
+    W = O.round_bf16(_rand_w(rng, cin, cout, 1.0 / np.sqrt(9 * cin)))
+    Xg = X[g2o].astype(np.float32)
+    gy = gl.conv(gl, _dev(Xg, torch.bfloat16), _gpu_w(W.astype(np.float32), torch.bfloat16), relu=True)
+    oy = O.round_bf16(ol.conv(ol, X, W, relu=True))
+    P.assert_close(P.rows_in_oracle_order(_host(gy), g2o), oy, P.TOL_BF16, f"bf16 conv {cin}->{cout}")
+
+
+def test_conv_column_slices(L, O):
+    """Input and output as column ranges of wider buffers (concatenation)."""
+    pos = _cloud(60, 5000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.07)
+    rng = np.random.default_rng(9)
+    X = rng.normal(size=(ol.n, 32)).astype(np.float32)
+    W = _rand_w(rng, 32, 16, 0.1)
+    big_in = torch.zeros((gl.n, 96), device="cuda")
+    big_in[:, 32:64] = _dev(X[g2o])
+    big_out = torch.full((gl.n, 48), 7.0, device="cuda")
+    gl.conv(gl, big_in[:, 32:64], _gpu_w(W), out=big_out[:, 16:32])
+    oy = ol.conv(ol, X.astype(np.float64), W.astype(np.float64))
+    h = _host(big_out)
+    P.assert_close(P.rows_in_oracle_order(h[:, 16:32], g2o), oy, P.TOL_F32, "sliced conv")
+    assert (h[:, :16] == 7.0).all() and (h[:, 32:] == 7.0).all()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_strided_and_transposed_conv(L, O, dtype):
+    pos = _cloud(70, 8000, 0.8)
+    sigma = 0.05
+    gl = L.Lattice.create(_dev(pos), [sigma] * 3)
+    ol = O.Lattice.create(pos, np.full(3, sigma, np.float32))
+    gc, oc = gl.coarsen(), ol.coarsen()
+    g2o_f = P.key_permutation(_host(gl.keys()), ol.keys())
+    g2o_c = P.key_permutation(_host(gc.keys()), oc.keys())
+    rng = np.random.default_rng(11)
+    bf = dtype == "bf16"
+    tdt = torch.bfloat16 if bf else torch.float32
+    rnd = O.round_bf16 if bf else (lambda a: np.asarray(a, np.float64))
+    tol = P.TOL_BF16 if bf else P.TOL_F32
+    Xf = rnd(rng.normal(size=(ol.n, 64)))
+    Wd = rnd(_rand_w(rng, 64, 128, 1.0 / 24))
+    gy = gc.conv(gl, _dev(Xf[g2o_f].astype(np.float32), tdt), _gpu_w(Wd.astype(np.float32), tdt))
+    oy = rnd(oc.conv(ol, Xf, Wd))
+    P.assert_close(P.rows_in_oracle_order(_host(gy), g2o_c), oy, tol, "strided conv")
+    Xc = rnd(rng.normal(size=(oc.n, 128)))
+    Wu = rnd(_rand_w(rng, 128, 64, 1.0 / 24))
+    gz = gl.refine(gc, _dev(Xc[g2o_c].astype(np.float32), tdt), _gpu_w(Wu.astype(np.float32), tdt), relu=True)
+    oz = rnd(ol.refine_into(oc, Xc, Wu, relu=True))
+    P.assert_close(P.rows_in_oracle_order(_host(gz), g2o_f), oz, tol, "transposed conv")
+
+
+@pytest.mark.parametrize("C,dtype", [(4, "f32"), (16, "f32"), (64, "f32"), (128, "f32"),
+                                     (512, "f32"), (64, "bf16"), (256, "bf16")])
+def test_slice_and_deform_slice(L, O, C, dtype):
+    pos = _cloud(80 + C, 7000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.06)
+    rng = np.random.default_rng(C)
+    bf = dtype == "bf16"
+    tdt = torch.bfloat16 if bf else torch.float32
+    X = rng.normal(size=(ol.n, C))
+    if bf:
+        X = O.round_bf16(X)
+    Xg = _dev(X[g2o].astype(np.float32), tdt)
+    P.assert_close(_host(gl.slice(Xg)), ol.slice(X), P.TOL_F32, "slice")
+    if C <= 256:
+        wv = (rng.normal(size=C) / np.sqrt(C)).astype(np.float32)
+        delta = torch.empty((gl.m, 4), device="cuda")
+        out = gl.deform_slice(Xg, _dev(wv), 0.1, delta=delta)
+        oo, od = ol.deform_slice(X, wv.astype(np.float64), 0.1)
+        P.assert_close(_host(out), oo, P.TOL_F32, "deform slice")
+        P.assert_close(_host(delta), od, P.TOL_F32, "deform offsets")
+
+
+# ----------------------------------------------------------------------------
+# whole pipelines
+# ----------------------------------------------------------------------------
+def rounding_depths(wl):
+    """bf16 storage roundings on the longest path to every written column
+    range and point output (see tests/parity.py)."""
+    cols = {name: np.zeros(total, dtype=np.int64) for name, (_, total) in wl.buffers.items()}
+    depth = {}
+    for op in wl.ops:
+        if "src" in op:
+            name, c0, cc = op["src"]
+            d_in = int(cols[name][c0:c0 + cc].max())
+        else:
+            d_in = 0
+        if "dst" in op:
+            name, c0, cc = op["dst"]
+            cols[name][c0:c0 + cc] = d_in + 1
+            depth[(name, c0, cc)] = d_in + 1
+        if "out" in op:
+            depth[op["out"]] = d_in + 1
+    return depth
+
+
+def _run_both(L, O, wl):
+    from paper_1912_05905_amd.pipeline import GpuPipeline
+    levels, bufs, outs = GpuPipeline(wl).step()
+    olv, obufs, oouts = OraclePipeline(wl).run()
+    bf = wl.dtype == "bf16"
+    tol = P.TOL_BF16 if bf else P.TOL_F32
+    depth = rounding_depths(wl)
+    g2o = {}
+    for lv in sorted(levels):
+        g2o[lv] = _check_structure(levels[lv], olv[lv])
+    for key, d in depth.items():
+        if not isinstance(key, tuple):
+            continue
+        name, c0, cc = key
+        lv = wl.buffers[name][0]
+        got = P.rows_in_oracle_order(_host(bufs[name]), g2o[lv])[:, c0:c0 + cc]
+        P.assert_close(got, obufs[name][:, c0:c0 + cc], tol, f"{name}[{c0}:{c0 + cc}]",
+                       depth=d if bf else 1)
+    for name in outs:
+        P.assert_close(_host(outs[name]), oouts[name], tol, name, depth=depth[name] if bf else 1)
+    return levels
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_pipeline_full_size(L, O, cfg):
+    _run_both(L, O, configs.make(cfg))
+
+
+@pytest.mark.parametrize("seed", [100, 101])
+def test_pipeline_other_seeds(L, O, seed):
+    for cfg in (1, 2):
+        _run_both(L, O, configs.make(cfg, seed=seed))
+
+
+def test_pipeline_config5_reduced(L, O):
+    """The bf16 4-level U-Net on a 30k-point room of the same generator."""
+    _run_both(L, O, configs.config5(m=30_000, size=(4.0, 4.0, 3.0), nboxes=20))
