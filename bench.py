@@ -23,7 +23,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"hbm": 8.0e12, "mfma_f32": 157.3e12, "mfma_bf16": 2.5e15}
-FAMILIES = ["fill", "insert", "resolve", "scan", "lists", "nbr", "splat", "conv", "slice", "deform_slice"]
+FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "conv", "slice", "deform_slice"]
 
 
 def conv_flops(wl, levels):

@@ -220,6 +220,8 @@ struct lattice_s {
   int32_t* offsets = nullptr;    // n+1 list offsets of J_v
   int32_t* entries = nullptr;    // 4m entries p*4+k grouped by vertex
   float* entry_w = nullptr;      // 4m weights of those entries
+  int32_t* chunk_first = nullptr;  // vertex owning list position c * kSplatChunk
+  int64_t total = 0;               // number of list entries (4m)
   int32_t* nbr = nullptr;        // 9 x n same-level table (tap-major)
   int32_t* down = nullptr;       // 9 x n table into the parent (coarse levels)
   int32_t* up = nullptr;         // 9 x n_parent table from the parent into this level
@@ -276,17 +278,28 @@ int check_launch(const char* what) {
   return LAT_OK;
 }
 
-// Build a lattice for `m` points: either from positions (pos, a[]) or from a
-// parent's elevated positions scaled by 1/2.
-int build_lattice(lattice_s* L, const float* pos, const float a[3], const lattice_s* parent,
-                  int64_t capacity_hint, hipStream_t s) {
+// Scratch buffer from the pool, returned when the scope ends.
+struct Scratch {
+  void* p = nullptr;
+  size_t bytes = 0;
+  hipStream_t s = nullptr;
+  ~Scratch() { Pool::get().release(p, bytes, s); }
+  int get(size_t b, hipStream_t st) {
+    bytes = b;
+    s = st;
+    return Pool::get().alloc(b, st, &p);
+  }
+  template <class T> T* as() const { return static_cast<T*>(p); }
+};
+
+// One attempt at building a lattice with a table of `cap` slots.
+// Returns LAT_EHASHFULL (with nothing kept) when the table overflows.
+int build_attempt(lattice_s* L, const float* pos, const float a[3], const lattice_s* parent, int64_t cap,
+                  hipStream_t s) {
   const int64_t m = L->m;
-  if (m == 0) return LAT_OK;
   const int64_t refs = 4 * m;
-  if (refs > INT32_MAX) return fail(LAT_EUNSUPPORTED, "more than 2^29 points");
-  const int64_t want = capacity_hint > 0 ? std::min(capacity_hint, refs) : refs;
-  L->cap = next_pow2(std::max<int64_t>(1024, 2 * want));
-  const int64_t nmax = std::min(L->cap, refs);
+  const int64_t nmax = std::min(cap, refs);
+  L->cap = cap;
   int st;
   void* p;
 #define ALLOC(field, type, count)                                                 \
@@ -296,43 +309,38 @@ int build_lattice(lattice_s* L, const float* pos, const float a[3], const lattic
   ALLOC(y, float, 4 * m);
   ALLOC(idx, int32_t, refs);
   ALLOC(w, float, refs);
-  ALLOC(tkeys, uint64_t, L->cap);
-  ALLOC(tvals, int32_t, L->cap);
+  ALLOC(tkeys, uint64_t, cap);
+  ALLOC(tvals, int32_t, cap);
   ALLOC(vkeys, uint64_t, nmax);
 #undef ALLOC
-  // scratch for this build only
-  int32_t* count = nullptr;
-  int32_t* slot_rank = nullptr;
-  DeviceCounters* dc = nullptr;
-  void* q;
-  if ((st = Pool::get().alloc(sizeof(int32_t) * nmax, s, &q)) != LAT_OK) return st;
-  count = static_cast<int32_t*>(q);
-  if ((st = Pool::get().alloc(sizeof(int32_t) * refs, s, &q)) != LAT_OK) return st;
-  slot_rank = static_cast<int32_t*>(q);
-  if ((st = Pool::get().alloc(sizeof(DeviceCounters), s, &q)) != LAT_OK) return st;
-  dc = static_cast<DeviceCounters*>(q);
+  Scratch slot_count, vslot, slot, rank, dcs;
+  if ((st = slot_count.get(sizeof(int32_t) * cap, s)) != LAT_OK) return st;
+  if ((st = vslot.get(sizeof(int32_t) * nmax, s)) != LAT_OK) return st;
+  if ((st = slot.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
+  if ((st = rank.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
+  if ((st = dcs.get(sizeof(DeviceCounters), s)) != LAT_OK) return st;
+  DeviceCounters* dc = dcs.as<DeviceCounters>();
 
-  launch_fill_u64(L->tkeys, kEmptyKey, L->cap, s);
-  launch_fill_u64(reinterpret_cast<uint64_t*>(dc), 0ull, 1, s);
+  launch_clear_table(L->tkeys, slot_count.as<int32_t>(), cap, reinterpret_cast<uint64_t*>(dc), s);
   launch_insert_points(pos, parent ? parent->y : nullptr, 0.5f, a[0], a[1], a[2], m, L->hash(),
-                       &dc->counter, L->vkeys, count, slot_rank, L->w, L->y, &dc->err, s);
+                       &dc->counter, slot_count.as<int32_t>(), L->vkeys, vslot.as<int32_t>(),
+                       slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->y, &dc->err, s);
   if ((st = check_launch("insert")) != LAT_OK) return st;
   DeviceCounters* h = host_readback();
   if (!h) return fail(LAT_ENOMEM, "pinned host buffer");
   HIP_TRY(hipMemcpyAsync(h, dc, sizeof(DeviceCounters), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   const int dev_status = status_from_err_bits(h->err);
-  L->n = h->counter;
   if (dev_status != LAT_OK) {
-    Pool::get().release(count, sizeof(int32_t) * nmax, s);
-    Pool::get().release(slot_rank, sizeof(int32_t) * refs, s);
-    Pool::get().release(dc, sizeof(DeviceCounters), s);
     const char* why = dev_status == LAT_EHASHFULL ? "hash table full (raise capacity_hint)"
                       : dev_status == LAT_EKEYRANGE ? "a vertex coordinate reaches 2^20 (positions / sigma too large)"
                                                     : "non-finite position";
     return fail(dev_status, why);
   }
-  const int64_t n = L->n;
+  const int64_t n = h->counter;
+  L->n = n;
+  L->total = refs;
+  const int64_t nchunks = (refs + kSplatChunk - 1) / kSplatChunk;
 #define ALLOC(field, type, count)                                                 \
   if ((st = L->alloc(sizeof(type) * static_cast<size_t>(count), s, &p)) != LAT_OK) \
     return st;                                                                    \
@@ -340,23 +348,37 @@ int build_lattice(lattice_s* L, const float* pos, const float a[3], const lattic
   ALLOC(offsets, int32_t, n + 1);
   ALLOC(entries, int32_t, refs);
   ALLOC(entry_w, float, refs);
+  ALLOC(chunk_first, int32_t, nchunks);
   ALLOC(nbr, int32_t, kTaps * n);
 #undef ALLOC
-  int32_t* work = nullptr;
-  if ((st = Pool::get().alloc(sizeof(int32_t) * scan_workspace_elems(n), s, &q)) != LAT_OK) return st;
-  work = static_cast<int32_t*>(q);
-
-  launch_resolve(L->hash(), slot_rank, L->idx, count, refs, s);
-  launch_exclusive_scan(count, L->offsets, n, work, s);
-  launch_fill_lists(L->idx, slot_rank, L->w, L->offsets, L->entries, L->entry_w, refs, s);
+  Scratch work;
+  if ((st = work.get(sizeof(int32_t) * scan_workspace_elems(n), s)) != LAT_OK) return st;
+  launch_count_scan(slot_count.as<int32_t>(), vslot.as<int32_t>(), L->offsets, n, work.as<int32_t>(), s);
+  launch_fill_lists(L->hash(), slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->offsets, L->idx,
+                    L->entries, L->entry_w, L->chunk_first, refs, s);
   launch_neighbor_table(L->hash(), L->vkeys, n, L->nbr, n, s);
-  if ((st = check_launch("lattice build")) != LAT_OK) return st;
+  return check_launch("lattice build");
+}
 
-  Pool::get().release(work, sizeof(int32_t) * scan_workspace_elems(n), s);
-  Pool::get().release(count, sizeof(int32_t) * nmax, s);
-  Pool::get().release(slot_rank, sizeof(int32_t) * refs, s);
-  Pool::get().release(dc, sizeof(DeviceCounters), s);
-  return LAT_OK;
+// Build a lattice for `m` points: from positions (pos, a[]) or from a
+// parent's elevated positions halved.  Coarse levels first try a table sized
+// from the parent's vertex count and fall back to the worst-case size.
+int build_lattice(lattice_s* L, const float* pos, const float a[3], const lattice_s* parent,
+                  int64_t capacity_hint, hipStream_t s) {
+  const int64_t m = L->m;
+  if (m == 0) return LAT_OK;
+  const int64_t refs = 4 * m;
+  if (refs > INT32_MAX) return fail(LAT_EUNSUPPORTED, "more than 2^29 points");
+  const int64_t full = next_pow2(std::max<int64_t>(1024, 2 * refs));
+  int64_t cap = full;
+  if (capacity_hint > 0) cap = next_pow2(std::max<int64_t>(1024, 2 * std::min(capacity_hint, refs)));
+  else if (parent) cap = std::min(full, next_pow2(std::max<int64_t>(1024, 2 * parent->n)));
+  int st = build_attempt(L, pos, a, parent, cap, s);
+  if (st == LAT_EHASHFULL && capacity_hint == 0 && cap < full) {
+    L->free_all();
+    st = build_attempt(L, pos, a, parent, full, s);
+  }
+  return st;
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -574,8 +596,11 @@ int lattice_splat(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat
   if (C > splat_max_channels(dt == LAT_BF16))
     return fail(LAT_EUNSUPPORTED, "splat supports at most " + std::to_string(splat_max_channels(dt == LAT_BF16)) +
                                       " channels");
-  launch_splat(L->offsets, L->entries, L->entry_w, feat_dev, ld_feat, C, dt == LAT_BF16, normalize != 0,
-               L->n, vals_dev, ld_vals, wsum_dev, stream);
+  if (L->n == 0) return LAT_OK;
+  Scratch partials;
+  if ((st = partials.get(sizeof(float) * splat_partial_floats(L->total, C), stream)) != LAT_OK) return st;
+  launch_splat(L->offsets, L->entries, L->entry_w, L->chunk_first, L->n, L->total, feat_dev, ld_feat, C,
+               dt == LAT_BF16, normalize != 0, vals_dev, ld_vals, wsum_dev, partials.as<float>(), stream);
   return check_launch("splat");
 }
 

@@ -4,6 +4,13 @@
 // The embedding (elevation, rounding, ranking, barycentric weights) must
 // produce the vertex set bit for bit, so this file is compiled with float
 // contraction off and every float operation below is one IEEE rounding.
+//
+// Device-scope atomics on this part are resolved beyond the per-XCD L2, so
+// the insert kernel keeps them off the per-reference path: a workgroup first
+// merges its 1024 vertex references in an LDS hash table, then touches the
+// global table once per distinct key, adds its reference count for that key
+// with one atomic, and numbers all vertices it created with one atomic on
+// the vertex counter.
 #pragma clang fp contract(off)
 
 #include "lattice_internal.h"
@@ -12,17 +19,25 @@ namespace lat {
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int kLdsSlots = 2048;             // LDS table: 2x the references of a workgroup
+constexpr int kLdsPerThread = kLdsSlots / kBlock;
 
-__global__ void __launch_bounds__(kBlock) k_fill_u64(uint64_t* __restrict__ p, uint64_t v, int64_t n) {
+__global__ void __launch_bounds__(kBlock)
+k_clear_table(uint64_t* __restrict__ keys, int32_t* __restrict__ counts, int64_t cap,
+              uint64_t* __restrict__ dev_counters) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-  for (int64_t e = i; e < n; e += stride) p[e] = v;
+  for (int64_t e = i; e < cap; e += stride) {
+    keys[e] = kEmptyKey;
+    counts[e] = 0;
+  }
+  if (i == 0) *dev_counters = 0ull;
 }
 
-// Insert a key; returns its slot, or -1 when the table is full.  The thread
-// whose compare-and-swap claims an empty slot numbers the vertex.
-__device__ inline int32_t hash_insert(const HashView& h, uint64_t key, int32_t* counter,
-                                      uint64_t* vkeys, int32_t* count, uint32_t* err) {
+// Global insert of a key; returns its slot (or -1 when the table is full)
+// and whether this call created it.
+__device__ inline int32_t global_insert(const HashView& h, uint64_t key, bool* created, uint32_t* err) {
+  *created = false;
   uint64_t slot = hash_key(key) & h.mask;
   for (uint64_t probe = 0; probe <= h.mask; ++probe) {
     const uint64_t cur = h.keys[slot];
@@ -32,10 +47,7 @@ __device__ inline int32_t hash_insert(const HashView& h, uint64_t key, int32_t* 
                                       static_cast<unsigned long long>(kEmptyKey),
                                       static_cast<unsigned long long>(key));
       if (prev == kEmptyKey) {
-        const int32_t v = atomicAdd(counter, 1);
-        h.vals[slot] = v;
-        vkeys[v] = key;
-        count[v] = 0;
+        *created = true;
         return static_cast<int32_t>(slot);
       }
       if (prev == key) return static_cast<int32_t>(slot);
@@ -46,158 +58,7 @@ __device__ inline int32_t hash_insert(const HashView& h, uint64_t key, int32_t* 
   return -1;
 }
 
-// One thread per point: elevate (or take the parent's elevated position
-// times y_scale), find the enclosing simplex, insert its d+1 vertices.
-//
-// Elevation: y = E (g/sigma) with E's columns orthonormal and orthogonal to
-// 1 (the lattice lives on H_d, coordinates summing to zero), scaled by
-// (d+1) sqrt(2/3); a_j folds 1/sigma_j and the column norm into one factor.
-// Simplex (the rounding construction of Adams, Baek and Davis 2010, which
-// the paper cites for finding the enclosing simplex): round each coordinate
-// to the nearest multiple of d+1 (ties down), rank the differentials
-// (largest first, equal ones by lower index), move the most extreme ones by
-// d+1 until the point lies on H_d, then vertex k adds k to every coordinate
-// and subtracts d+1 from the k highest-ranked ones; the barycentric weights
-// are the gaps between consecutive sorted differentials.
-__global__ void __launch_bounds__(kBlock)
-k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, float y_scale,
-                float a0, float a1, float a2, int64_t m, HashView h, int32_t* counter,
-                uint64_t* vkeys, int32_t* count, int4* __restrict__ slot_out,
-                float4* __restrict__ w_out, float4* __restrict__ y_out, uint32_t* err) {
-  const int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (p >= m) return;
-  float y[kVerts];
-  if (pos != nullptr) {
-    const float g0 = pos[3 * p + 0], g1 = pos[3 * p + 1], g2 = pos[3 * p + 2];
-    if (!isfinite(g0) || !isfinite(g1) || !isfinite(g2)) {
-      atomicOr(err, kErrNonFinite);
-      slot_out[p] = make_int4(-1, -1, -1, -1);
-      w_out[p] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (y_out) y_out[p] = make_float4(0.f, 0.f, 0.f, 0.f);
-      return;
-    }
-    const float t0 = g0 * a0, t1 = g1 * a1, t2 = g2 * a2;
-    float run = 0.0f;
-    const float m3 = 3.0f * t2;
-    y[3] = run - m3;
-    run = run + t2;
-    const float m2 = 2.0f * t1;
-    y[2] = run - m2;
-    run = run + t1;
-    const float m1 = 1.0f * t0;
-    y[1] = run - m1;
-    run = run + t0;
-    y[0] = run;
-  } else {
-    const float4 v = y_in[p];
-    y[0] = v.x * y_scale;
-    y[1] = v.y * y_scale;
-    y[2] = v.z * y_scale;
-    y[3] = v.w * y_scale;
-  }
-  if (y_out) y_out[p] = make_float4(y[0], y[1], y[2], y[3]);
-
-  bool ok = true;
-  for (int i = 0; i < kVerts; ++i)
-    if (!(fabsf(y[i]) < 2.0f * static_cast<float>(kCoordLimit))) ok = false;
-  if (!ok) {
-    atomicOr(err, isfinite(y[0] + y[1] + y[2] + y[3]) ? kErrKeyRange : kErrNonFinite);
-    slot_out[p] = make_int4(-1, -1, -1, -1);
-    w_out[p] = make_float4(0.f, 0.f, 0.f, 0.f);
-    return;
-  }
-
-  // nearest multiple of d+1 per coordinate, ties to the lower one
-  int32_t base[kVerts];
-  int32_t total = 0;
-#pragma unroll
-  for (int i = 0; i < kVerts; ++i) {
-    const float q = y[i] * 0.25f;
-    const float lo = floorf(q) * 4.0f;
-    const float hi = lo + 4.0f;
-    const float up = hi - y[i];
-    const float down = y[i] - lo;
-    base[i] = static_cast<int32_t>(up < down ? hi : lo);
-    total += base[i];
-  }
-  const int32_t excess = total / kVerts;
-  float diff[kVerts];
-#pragma unroll
-  for (int i = 0; i < kVerts; ++i) diff[i] = y[i] - static_cast<float>(base[i]);
-  int32_t rank[kVerts];
-#pragma unroll
-  for (int i = 0; i < kVerts; ++i) {
-    int32_t r = 0;
-#pragma unroll
-    for (int j = 0; j < kVerts; ++j)
-      r += (diff[j] > diff[i] || (diff[j] == diff[i] && j < i)) ? 1 : 0;
-    rank[i] = r;
-  }
-#pragma unroll
-  for (int i = 0; i < kVerts; ++i) {
-    if (excess > 0) {
-      if (rank[i] >= kVerts - excess) { base[i] -= kVerts; rank[i] += excess - kVerts; }
-      else rank[i] += excess;
-    } else if (excess < 0) {
-      if (rank[i] < -excess) { base[i] += kVerts; rank[i] += kVerts + excess; }
-      else rank[i] += excess;
-    }
-  }
-  // z sorted by rank (z_0 largest), scaled by 1/(d+1)
-  float z[kVerts];
-#pragma unroll
-  for (int i = 0; i < kVerts; ++i) {
-    const float dz = (y[i] - static_cast<float>(base[i])) * 0.25f;
-#pragma unroll
-    for (int r = 0; r < kVerts; ++r)
-      if (rank[i] == r) z[r] = dz;
-  }
-  float b[kVerts];
-  b[0] = 1.0f - (z[0] - z[3]);
-  b[1] = z[2] - z[3];
-  b[2] = z[1] - z[2];
-  b[3] = z[0] - z[1];
-
-  int32_t slots[kVerts];
-#pragma unroll
-  for (int k = 0; k < kVerts; ++k) {
-    int32_t c[kVerts];
-#pragma unroll
-    for (int i = 0; i < kVerts; ++i) c[i] = base[i] + k - (rank[i] > kDim - k ? kVerts : 0);
-    if (!coords_in_range(c[0], c[1], c[2], c[3])) {
-      atomicOr(err, kErrKeyRange);
-      slots[k] = -1;
-      continue;
-    }
-    slots[k] = hash_insert(h, pack_key(c[0], c[1], c[2]), counter, vkeys, count, err);
-  }
-  slot_out[p] = make_int4(slots[0], slots[1], slots[2], slots[3]);
-  w_out[p] = make_float4(b[0], b[1], b[2], b[3]);
-}
-
-// Slot -> vertex index; count points per vertex, remembering each entry's
-// position in its vertex list.
-__global__ void __launch_bounds__(kBlock)
-k_resolve(HashView h, int32_t* __restrict__ slot_rank, int32_t* __restrict__ idx,
-          int32_t* __restrict__ count, int64_t m4) {
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (e >= m4) return;
-  const int32_t slot = slot_rank[e];
-  if (slot < 0) {
-    idx[e] = -1;
-    slot_rank[e] = -1;
-    return;
-  }
-  const int32_t v = h.vals[slot];
-  idx[e] = v;
-  slot_rank[e] = atomicAdd(&count[v], 1);
-}
-
-// ---- exclusive scan (three passes: tile sums, scan of sums, apply) ----
-constexpr int kScanPer = 8;
-constexpr int kScanTile = kBlock * kScanPer;
-
-__device__ inline int32_t block_exclusive_scan(int32_t v, int32_t* lds, int32_t* total) {
+__device__ inline int32_t block_exclusive_sum(int32_t v, int32_t* lds, int32_t* total) {
   const int tid = threadIdx.x;
   lds[tid] = v;
   __syncthreads();
@@ -213,15 +74,230 @@ __device__ inline int32_t block_exclusive_scan(int32_t v, int32_t* lds, int32_t*
   return incl - v;
 }
 
+// One thread per point.  Embedding: y = E (g/sigma) with E's columns
+// orthonormal and orthogonal to 1 (the lattice lives on H_d, coordinates
+// summing to zero), scaled by (d+1) sqrt(2/3); a_j folds 1/sigma_j and the
+// column norm into one factor.  Coarse levels take the parent's elevated
+// position times y_scale (1/2).
+// Enclosing simplex (the rounding construction of Adams, Baek and Davis
+// 2010, which the paper cites for finding the simplex): round each
+// coordinate to the nearest multiple of d+1 (ties down), rank the
+// differentials (largest first, equal ones by lower index), move the most
+// extreme ones by d+1 until the point lies on H_d, then vertex k adds k to
+// every coordinate and subtracts d+1 from the k highest-ranked ones; the
+// barycentric weights are the gaps between consecutive sorted differentials.
+//
+// Outputs per point: slot of each vertex in the global table, its rank in
+// that vertex's point list, the weights and the elevated position.  Per new
+// vertex: vals[slot] = vertex number, vkeys / vslot by vertex number.
+// slot_count[slot] ends as the number of references of the vertex.
 __global__ void __launch_bounds__(kBlock)
-k_scan_tiles(const int32_t* __restrict__ in, int64_t n, int32_t* __restrict__ sums) {
+k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, float y_scale,
+                float a0, float a1, float a2, int64_t m, HashView h, int32_t* counter,
+                int32_t* __restrict__ slot_count, uint64_t* __restrict__ vkeys,
+                int32_t* __restrict__ vslot, int4* __restrict__ slot_out, int4* __restrict__ rank_out,
+                float4* __restrict__ w_out, float4* __restrict__ y_out, uint32_t* err) {
+  __shared__ uint64_t lkey[kLdsSlots];
+  __shared__ int32_t lcount[kLdsSlots];
+  __shared__ int32_t lslot[kLdsSlots];
+  __shared__ int32_t lbase[kLdsSlots];
+  __shared__ int32_t scan_buf[kBlock];
+  __shared__ int32_t id_base;
+
+  const int tid = threadIdx.x;
+  for (int j = 0; j < kLdsPerThread; ++j) {
+    lkey[tid + j * kBlock] = kEmptyKey;
+    lcount[tid + j * kBlock] = 0;
+  }
+  __syncthreads();
+
+  const int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + tid;
+  bool live = p < m;
+  float y[kVerts] = {0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    if (pos != nullptr) {
+      const float g0 = pos[3 * p + 0], g1 = pos[3 * p + 1], g2 = pos[3 * p + 2];
+      if (!isfinite(g0) || !isfinite(g1) || !isfinite(g2)) {
+        atomicOr(err, kErrNonFinite);
+        live = false;
+      } else {
+        const float t0 = g0 * a0, t1 = g1 * a1, t2 = g2 * a2;
+        float run = 0.0f;
+        const float m3 = 3.0f * t2;
+        y[3] = run - m3;
+        run = run + t2;
+        const float m2 = 2.0f * t1;
+        y[2] = run - m2;
+        run = run + t1;
+        const float m1 = 1.0f * t0;
+        y[1] = run - m1;
+        run = run + t0;
+        y[0] = run;
+      }
+    } else {
+      const float4 v = y_in[p];
+      y[0] = v.x * y_scale;
+      y[1] = v.y * y_scale;
+      y[2] = v.z * y_scale;
+      y[3] = v.w * y_scale;
+    }
+    if (y_out) y_out[p] = make_float4(y[0], y[1], y[2], y[3]);
+  }
+  if (live) {
+    bool ok = true;
+    for (int i = 0; i < kVerts; ++i)
+      if (!(fabsf(y[i]) < 2.0f * static_cast<float>(kCoordLimit))) ok = false;
+    if (!ok) {
+      atomicOr(err, isfinite(y[0] + y[1] + y[2] + y[3]) ? kErrKeyRange : kErrNonFinite);
+      live = false;
+    }
+  }
+
+  float b[kVerts] = {0.f, 0.f, 0.f, 0.f};
+  uint64_t keys[kVerts] = {kEmptyKey, kEmptyKey, kEmptyKey, kEmptyKey};
+  if (live) {
+    int32_t base[kVerts];
+    int32_t total = 0;
+#pragma unroll
+    for (int i = 0; i < kVerts; ++i) {
+      const float q = y[i] * 0.25f;
+      const float lo = floorf(q) * 4.0f;
+      const float hi = lo + 4.0f;
+      const float up = hi - y[i];
+      const float down = y[i] - lo;
+      base[i] = static_cast<int32_t>(up < down ? hi : lo);
+      total += base[i];
+    }
+    const int32_t excess = total / kVerts;
+    float diff[kVerts];
+#pragma unroll
+    for (int i = 0; i < kVerts; ++i) diff[i] = y[i] - static_cast<float>(base[i]);
+    int32_t rank[kVerts];
+#pragma unroll
+    for (int i = 0; i < kVerts; ++i) {
+      int32_t r = 0;
+#pragma unroll
+      for (int j = 0; j < kVerts; ++j)
+        r += (diff[j] > diff[i] || (diff[j] == diff[i] && j < i)) ? 1 : 0;
+      rank[i] = r;
+    }
+#pragma unroll
+    for (int i = 0; i < kVerts; ++i) {
+      if (excess > 0) {
+        if (rank[i] >= kVerts - excess) { base[i] -= kVerts; rank[i] += excess - kVerts; }
+        else rank[i] += excess;
+      } else if (excess < 0) {
+        if (rank[i] < -excess) { base[i] += kVerts; rank[i] += kVerts + excess; }
+        else rank[i] += excess;
+      }
+    }
+    float z[kVerts];
+#pragma unroll
+    for (int i = 0; i < kVerts; ++i) {
+      const float dz = (y[i] - static_cast<float>(base[i])) * 0.25f;
+#pragma unroll
+      for (int r = 0; r < kVerts; ++r)
+        if (rank[i] == r) z[r] = dz;
+    }
+    b[0] = 1.0f - (z[0] - z[3]);
+    b[1] = z[2] - z[3];
+    b[2] = z[1] - z[2];
+    b[3] = z[0] - z[1];
+#pragma unroll
+    for (int k = 0; k < kVerts; ++k) {
+      int32_t c[kVerts];
+#pragma unroll
+      for (int i = 0; i < kVerts; ++i) c[i] = base[i] + k - (rank[i] > kDim - k ? kVerts : 0);
+      if (coords_in_range(c[0], c[1], c[2], c[3])) keys[k] = pack_key(c[0], c[1], c[2]);
+      else atomicOr(err, kErrKeyRange);
+    }
+  }
+
+  // 1. merge the workgroup's references in LDS
+  int32_t lsl[kVerts], lrank[kVerts];
+#pragma unroll
+  for (int k = 0; k < kVerts; ++k) {
+    lsl[k] = -1;
+    lrank[k] = 0;
+    if (keys[k] == kEmptyKey) continue;
+    uint32_t s = static_cast<uint32_t>(hash_key(keys[k])) & (kLdsSlots - 1);
+    for (int probe = 0; probe < kLdsSlots; ++probe) {
+      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(&lkey[s]),
+                                      static_cast<unsigned long long>(kEmptyKey),
+                                      static_cast<unsigned long long>(keys[k]));
+      if (prev == kEmptyKey || prev == keys[k]) break;
+      s = (s + 1) & (kLdsSlots - 1);
+    }
+    lsl[k] = static_cast<int32_t>(s);
+    lrank[k] = atomicAdd(&lcount[s], 1);
+  }
+  __syncthreads();
+
+  // 2. one global insert and one count update per distinct key
+  uint32_t created_mask = 0;
+  int32_t ncreated = 0;
+  for (int j = 0; j < kLdsPerThread; ++j) {
+    const int s = tid + j * kBlock;
+    const uint64_t key = lkey[s];
+    if (key == kEmptyKey) continue;
+    bool created = false;
+    const int32_t gs = global_insert(h, key, &created, err);
+    lslot[s] = gs;
+    lbase[s] = gs >= 0 ? atomicAdd(&slot_count[gs], lcount[s]) : 0;
+    if (created) {
+      created_mask |= 1u << j;
+      ++ncreated;
+    }
+  }
+  int32_t nblock = 0;
+  int32_t my_first = block_exclusive_sum(ncreated, scan_buf, &nblock);
+  if (tid == 0) id_base = nblock > 0 ? atomicAdd(counter, nblock) : 0;
+  __syncthreads();
+  int32_t id = id_base + my_first;
+  for (int j = 0; j < kLdsPerThread; ++j) {
+    if (!(created_mask & (1u << j))) continue;
+    const int s = tid + j * kBlock;
+    const int32_t gs = lslot[s];
+    h.vals[gs] = id;
+    vkeys[id] = lkey[s];
+    vslot[id] = gs;
+    ++id;
+  }
+  __syncthreads();
+
+  // 3. per reference: global slot and rank in the vertex's point list
+  if (p < m) {
+    int32_t so[kVerts], ro[kVerts];
+#pragma unroll
+    for (int k = 0; k < kVerts; ++k) {
+      so[k] = lsl[k] >= 0 ? lslot[lsl[k]] : -1;
+      ro[k] = lsl[k] >= 0 ? lbase[lsl[k]] + lrank[k] : 0;
+    }
+    slot_out[p] = make_int4(so[0], so[1], so[2], so[3]);
+    rank_out[p] = make_int4(ro[0], ro[1], ro[2], ro[3]);
+    w_out[p] = make_float4(b[0], b[1], b[2], b[3]);
+  }
+}
+
+// ---- exclusive scan of per-vertex counts (tile sums, scan of sums, apply) ----
+constexpr int kScanPer = 8;
+constexpr int kScanTile = kBlock * kScanPer;
+
+// count of vertex i: in[gather[i]] (reference count stored by table slot)
+__device__ inline int32_t vertex_count(const int32_t* in, const int32_t* gather, int64_t i) {
+  return in[gather[i]];
+}
+
+__global__ void __launch_bounds__(kBlock)
+k_scan_tiles(const int32_t* __restrict__ in, const int32_t* __restrict__ gather, int64_t n,
+             int32_t* __restrict__ sums) {
   __shared__ int32_t lds[kBlock];
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x * kScanPer;
   int32_t s = 0;
   for (int j = 0; j < kScanPer; ++j)
-    if (base + j < n) s += in[base + j];
+    if (base + j < n) s += vertex_count(in, gather, base + j);
   int32_t total;
-  block_exclusive_scan(s, lds, &total);
+  block_exclusive_sum(s, lds, &total);
   if (threadIdx.x == 0) sums[blockIdx.x] = total;
 }
 
@@ -233,25 +309,25 @@ k_scan_sums(int32_t* __restrict__ sums, int64_t nt) {
     const int64_t i = start + threadIdx.x;
     const int32_t v = i < nt ? sums[i] : 0;
     int32_t total;
-    const int32_t ex = block_exclusive_scan(v, lds, &total);
+    const int32_t ex = block_exclusive_sum(v, lds, &total);
     if (i < nt) sums[i] = carry + ex;
     carry += total;
   }
 }
 
 __global__ void __launch_bounds__(kBlock)
-k_scan_apply(const int32_t* __restrict__ in, int64_t n, const int32_t* __restrict__ sums,
-             int32_t* __restrict__ out) {
+k_scan_apply(const int32_t* __restrict__ in, const int32_t* __restrict__ gather, int64_t n,
+             const int32_t* __restrict__ sums, int32_t* __restrict__ out) {
   __shared__ int32_t lds[kBlock];
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x * kScanPer;
   int32_t vals[kScanPer];
   int32_t s = 0;
   for (int j = 0; j < kScanPer; ++j) {
-    vals[j] = base + j < n ? in[base + j] : 0;
+    vals[j] = base + j < n ? vertex_count(in, gather, base + j) : 0;
     s += vals[j];
   }
   int32_t total;
-  int32_t run = block_exclusive_scan(s, lds, &total) + sums[blockIdx.x];
+  int32_t run = block_exclusive_sum(s, lds, &total) + sums[blockIdx.x];
   for (int j = 0; j < kScanPer; ++j) {
     if (base + j < n) out[base + j] = run;
     if (base + j == n - 1) out[n] = run + vals[j];
@@ -259,19 +335,27 @@ k_scan_apply(const int32_t* __restrict__ in, int64_t n, const int32_t* __restric
   }
 }
 
-// entries[offsets[v] + rank] = p*(d+1) + k: the points of J_v, per vertex,
-// with their barycentric weights alongside.
+// Per reference e = p*(d+1)+k: vertex index, and its place in J_v:
+// entries[offsets[v] + rank] = e with the weight alongside.  The vertex that
+// owns list position c*E (E = kSplatChunk) is recorded for the chunked splat.
 __global__ void __launch_bounds__(kBlock)
-k_fill_lists(const int32_t* __restrict__ idx, const int32_t* __restrict__ rank,
+k_fill_lists(HashView h, const int32_t* __restrict__ slot, const int32_t* __restrict__ rank,
              const float* __restrict__ w, const int32_t* __restrict__ offsets,
-             int32_t* __restrict__ entries, float* __restrict__ entry_w, int64_t m4) {
+             int32_t* __restrict__ idx, int32_t* __restrict__ entries, float* __restrict__ entry_w,
+             int32_t* __restrict__ chunk_first, int64_t m4) {
   const int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   if (e >= m4) return;
-  const int32_t v = idx[e];
-  if (v < 0) return;
-  const int32_t pos = offsets[v] + rank[e];
-  entries[pos] = static_cast<int32_t>(e);
-  entry_w[pos] = w[e];
+  const int32_t s = slot[e];
+  if (s < 0) {
+    idx[e] = -1;
+    return;
+  }
+  const int32_t v = h.vals[s];
+  idx[e] = v;
+  const int32_t at = offsets[v] + rank[e];
+  entries[at] = static_cast<int32_t>(e);
+  entry_w[at] = w[e];
+  if (at % kSplatChunk == 0) chunk_first[at / kSplatChunk] = v;
 }
 
 // nbr[t][v] for taps 1..8 (tap 0 = v): the vertex at c_v + o_t.
@@ -309,7 +393,9 @@ k_down_table(HashView fine, const uint64_t* __restrict__ ckeys, int64_t n, int32
 }
 
 // Upsample: fine vertex v reads the coarse vertex at (c_v + o_t)/2 when that
-// is a lattice point (even coordinates whose halves agree mod d+1).
+// is a lattice point (even coordinates whose halves agree mod d+1).  The
+// check matters: packed keys omit the last coordinate, so a non-lattice point
+// could otherwise alias a stored key.
 __global__ void __launch_bounds__(kBlock)
 k_up_table(HashView coarse, const uint64_t* __restrict__ fkeys, int64_t n, int32_t* __restrict__ nbr,
            int64_t ldn) {
@@ -357,51 +443,48 @@ inline unsigned blocks_for(int64_t n) { return static_cast<unsigned>((n + kBlock
 
 }  // namespace
 
-void launch_fill_u64(uint64_t* p, uint64_t v, int64_t n, hipStream_t s) {
-  if (n <= 0) return;
-  const int64_t want = (n + kBlock * 4 - 1) / (kBlock * 4);
-  const unsigned grid = static_cast<unsigned>(want < 8192 ? want : 8192);
+void launch_clear_table(uint64_t* keys, int32_t* counts, int64_t cap, uint64_t* dev_counters,
+                        hipStream_t s) {
+  const int64_t want = (cap + kBlock * 4 - 1) / (kBlock * 4);
+  const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : (want < 8192 ? want : 8192));
   ScopedKernelTimer tm("fill", s);
-  hipLaunchKernelGGL(k_fill_u64, dim3(grid), dim3(kBlock), 0, s, p, v, n);
+  hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, s, keys, counts, cap, dev_counters);
 }
 
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
-                          float a2, int64_t m, HashView h, int32_t* counter, uint64_t* vkeys,
-                          int32_t* count, int32_t* slot_out, float* w_out, float* y_out,
-                          uint32_t* err, hipStream_t s) {
+                          float a2, int64_t m, HashView h, int32_t* counter, int32_t* slot_count,
+                          uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
+                          float* w_out, float* y_out, uint32_t* err, hipStream_t s) {
   if (m <= 0) return;
   ScopedKernelTimer tm("insert", s);
   hipLaunchKernelGGL(k_insert_points, dim3(blocks_for(m)), dim3(kBlock), 0, s, pos,
                      reinterpret_cast<const float4*>(y_in), y_scale, a0, a1, a2, m, h, counter,
-                     vkeys, count, reinterpret_cast<int4*>(slot_out),
-                     reinterpret_cast<float4*>(w_out), reinterpret_cast<float4*>(y_out), err);
-}
-
-void launch_resolve(HashView h, int32_t* slot_rank, int32_t* idx, int32_t* count, int64_t m4,
-                    hipStream_t s) {
-  if (m4 <= 0) return;
-  ScopedKernelTimer tm("resolve", s);
-  hipLaunchKernelGGL(k_resolve, dim3(blocks_for(m4)), dim3(kBlock), 0, s, h, slot_rank, idx, count, m4);
+                     slot_count, vkeys, vslot, reinterpret_cast<int4*>(slot_out),
+                     reinterpret_cast<int4*>(rank_out), reinterpret_cast<float4*>(w_out),
+                     reinterpret_cast<float4*>(y_out), err);
 }
 
 int64_t scan_workspace_elems(int64_t n) { return (n + kScanTile - 1) / kScanTile + 1; }
 
-void launch_exclusive_scan(const int32_t* in, int32_t* out, int64_t n, int32_t* work, hipStream_t s) {
+void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, int32_t* offsets, int64_t n,
+                       int32_t* work, hipStream_t s) {
   if (n <= 0) return;
   const int64_t nt = (n + kScanTile - 1) / kScanTile;
   ScopedKernelTimer tm("scan", s);
-  hipLaunchKernelGGL(k_scan_tiles, dim3(static_cast<unsigned>(nt)), dim3(kBlock), 0, s, in, n, work);
+  hipLaunchKernelGGL(k_scan_tiles, dim3(static_cast<unsigned>(nt)), dim3(kBlock), 0, s, slot_count,
+                     vslot, n, work);
   hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(kBlock), 0, s, work, nt);
-  hipLaunchKernelGGL(k_scan_apply, dim3(static_cast<unsigned>(nt)), dim3(kBlock), 0, s, in, n, work, out);
+  hipLaunchKernelGGL(k_scan_apply, dim3(static_cast<unsigned>(nt)), dim3(kBlock), 0, s, slot_count,
+                     vslot, n, work, offsets);
 }
 
-void launch_fill_lists(const int32_t* idx, const int32_t* rank, const float* w,
-                       const int32_t* offsets, int32_t* entries, float* entry_w, int64_t m4,
-                       hipStream_t s) {
+void launch_fill_lists(HashView h, const int32_t* slot, const int32_t* rank, const float* w,
+                       const int32_t* offsets, int32_t* idx, int32_t* entries, float* entry_w,
+                       int32_t* chunk_first, int64_t m4, hipStream_t s) {
   if (m4 <= 0) return;
   ScopedKernelTimer tm("lists", s);
-  hipLaunchKernelGGL(k_fill_lists, dim3(blocks_for(m4)), dim3(kBlock), 0, s, idx, rank, w, offsets,
-                     entries, entry_w, m4);
+  hipLaunchKernelGGL(k_fill_lists, dim3(blocks_for(m4)), dim3(kBlock), 0, s, h, slot, rank, w, offsets,
+                     idx, entries, entry_w, chunk_first, m4);
 }
 
 void launch_neighbor_table(HashView h, const uint64_t* vkeys, int64_t n, int32_t* nbr, int64_t ldn,

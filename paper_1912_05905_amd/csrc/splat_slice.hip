@@ -50,67 +50,178 @@ template <> struct Chunk<true> {
   }
 };
 
-// Splat (Eq. splat) as a gather over J_v: one lane group per vertex reads
-// the vertex's (point, weight) list and accumulates b * f in fp32.  Lane i of
-// the group fetches list entry s+i; the group then walks the batch with
-// shuffles, so LPR feature rows are in flight at once.  No float atomics.
-template <bool BF16, int LPR>
-__global__ void __launch_bounds__(kBlock)
-k_splat(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
-        const float* __restrict__ entry_w, const void* __restrict__ feat, int64_t ld_feat, int C,
-        int normalize, int64_t n, void* __restrict__ vals, int64_t ld_vals, float* __restrict__ wsum) {
+// Splat (Eq. splat) as a gather over the point lists J_v, which are stored
+// back to back (entries grouped by vertex).  The entry array is cut into
+// chunks of kSplatChunk entries and each chunk goes to one lane group, so
+// the work is balanced however skewed the vertex degrees are (a LiDAR vertex
+// next to the sensor can hold thousands of points).  A vertex whose list lies
+// inside one chunk is finished there; a vertex cut by chunk boundaries leaves
+// a partial sum per chunk (head: the vertex continues from the previous
+// chunk; tail: it starts here and continues), which k_splat_finish adds in
+// chunk order.  No float atomics; the summation order is fixed.
+template <bool BF16, int LPR, int Q>
+__device__ inline void splat_store(int32_t v, const float (&acc)[Q][Chunk<BF16>::N], float ws, int lane,
+                                   int nchunk, int normalize, void* vals, int64_t ld_vals, float* wsum) {
   using Ch = Chunk<BF16>;
-  constexpr int kMaxChunks = 4;                  // up to 4*LPR chunks per row
-  const int lane = threadIdx.x & (LPR - 1);
-  const int64_t v = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
-  const bool live = v < n;
-  const int nchunk = C / Ch::N;
-  float acc[kMaxChunks][Ch::N];
-#pragma unroll
-  for (int q = 0; q < kMaxChunks; ++q)
-#pragma unroll
-    for (int e = 0; e < Ch::N; ++e) acc[q][e] = 0.f;
-  float ws = 0.f;
-  const int32_t beg = live ? offsets[v] : 0;
-  const int32_t end = live ? offsets[v + 1] : 0;
-  for (int32_t s = beg; s < end; s += LPR) {
-    const int cnt = min(LPR, end - s);
-    int32_t my_e = 0;
-    float my_w = 0.f;
-    if (lane < cnt) {
-      my_e = entries[s + lane];
-      my_w = entry_w[s + lane];
-    }
-    for (int j = 0; j < cnt; ++j) {
-      const int32_t e = __shfl(my_e, j, LPR);
-      const float wt = __shfl(my_w, j, LPR);
-      const int64_t p = e >> 2;
-      ws += wt;
-#pragma unroll
-      for (int q = 0; q < kMaxChunks; ++q) {
-        const int ch = lane + q * LPR;
-        if (ch < nchunk) {
-          Ch f;
-          f.load(feat, p * ld_feat + static_cast<int64_t>(ch) * Ch::N);
-#pragma unroll
-          for (int i = 0; i < Ch::N; ++i) acc[q][i] += wt * f.v[i];
-        }
-      }
-    }
-  }
-  if (!live) return;
   const float scale = normalize ? (ws > 0.f ? 1.0f / ws : 0.f) : 1.0f;
 #pragma unroll
-  for (int q = 0; q < kMaxChunks; ++q) {
+  for (int q = 0; q < Q; ++q) {
     const int ch = lane + q * LPR;
     if (ch < nchunk) {
       Ch o;
 #pragma unroll
-      for (int i = 0; i < Ch::N; ++i) o.v[i] = normalize ? acc[q][i] * scale : acc[q][i];
-      o.store(vals, v * ld_vals + static_cast<int64_t>(ch) * Ch::N);
+      for (int i = 0; i < Ch::N; ++i) o.v[i] = acc[q][i] * scale;
+      o.store(vals, static_cast<int64_t>(v) * ld_vals + static_cast<int64_t>(ch) * Ch::N);
     }
   }
   if (wsum && lane == 0) wsum[v] = ws;
+}
+
+template <bool BF16, int LPR, int Q>
+__device__ inline void splat_partial(float* part, float* part_w, int64_t c, int slot,
+                                     const float (&acc)[Q][Chunk<BF16>::N], float ws, int lane, int C) {
+  using Ch = Chunk<BF16>;
+  const int nchunk = C / Ch::N;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int ch = lane + q * LPR;
+    if (ch < nchunk) {
+      float* dst = part + c * C + static_cast<int64_t>(ch) * Ch::N;
+#pragma unroll
+      for (int i = 0; i < Ch::N; i += 4)
+        *reinterpret_cast<float4*>(dst + i) = make_float4(acc[q][i], acc[q][i + 1], acc[q][i + 2], acc[q][i + 3]);
+    }
+  }
+  if (lane == 0) part_w[2 * c + slot] = ws;
+}
+
+template <bool BF16, int LPR, int Q, int B>
+__global__ void __launch_bounds__(kBlock)
+k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
+               const float* __restrict__ entry_w, const int32_t* __restrict__ chunk_first,
+               int64_t n, int64_t total, const void* __restrict__ feat, int64_t ld_feat, int C, int normalize,
+               void* __restrict__ vals, int64_t ld_vals, float* __restrict__ wsum,
+               float* __restrict__ part_head, float* __restrict__ part_tail, float* __restrict__ part_w) {
+  using Ch = Chunk<BF16>;
+  const int lane = threadIdx.x & (LPR - 1);
+  const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
+  const int64_t s0 = c * kSplatChunk;
+  if (s0 >= total) return;
+  const int64_t s1 = min(s0 + static_cast<int64_t>(kSplatChunk), total);
+  const int nchunk = C / Ch::N;
+  int32_t v = chunk_first[c];
+  // window of list ends for the next LPR vertices
+  int32_t v_win = v;
+  int32_t win = offsets[min(static_cast<int64_t>(v) + 1 + lane, n)];
+  int32_t vb = offsets[v];
+  int32_t ve = __shfl(win, 0, LPR);
+  float acc[Q][Ch::N];
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
+  float ws = 0.f;
+  for (int64_t s = s0; s < s1; s += B) {
+    int32_t e[B];
+    float wt[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const bool in = s + j < s1;
+      e[j] = in ? entries[s + j] : 0;
+      wt[j] = in ? entry_w[s + j] : 0.f;
+    }
+    Ch f[B][Q];
+#pragma unroll
+    for (int j = 0; j < B; ++j)
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int ch = lane + q * LPR;
+        if (s + j < s1 && ch < nchunk)
+          f[j][q].load(feat, static_cast<int64_t>(e[j] >> 2) * ld_feat + static_cast<int64_t>(ch) * Ch::N);
+        else
+#pragma unroll
+          for (int i = 0; i < Ch::N; ++i) f[j][q].v[i] = 0.f;
+      }
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      if (s + j >= s1) break;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int i = 0; i < Ch::N; ++i) acc[q][i] += wt[j] * f[j][q].v[i];
+      ws += wt[j];
+      const int64_t nxt = s + j + 1;
+      if (nxt == ve || nxt == s1) {
+        if (vb >= s0 && ve <= s1)
+          splat_store<BF16, LPR, Q>(v, acc, ws, lane, nchunk, normalize, vals, ld_vals, wsum);
+        else if (vb < s0)
+          splat_partial<BF16, LPR, Q>(part_head, part_w, c, 0, acc, ws, lane, C);
+        else
+          splat_partial<BF16, LPR, Q>(part_tail, part_w, c, 1, acc, ws, lane, C);
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+#pragma unroll
+          for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
+        ws = 0.f;
+        if (nxt == ve && nxt < s1) {
+          v += 1;
+          vb = ve;
+          if (v - v_win >= LPR) {
+            v_win = v;
+            win = offsets[min(static_cast<int64_t>(v) + 1 + lane, n)];
+          }
+          ve = __shfl(win, v - v_win, LPR);
+        }
+      }
+    }
+  }
+}
+
+// Vertices cut by chunk boundaries: the chunk in which a vertex's list starts
+// adds its tail partial and the head partials of the following chunks.
+template <bool BF16, int LPR, int Q>
+__global__ void __launch_bounds__(kBlock)
+k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ chunk_first,
+               int64_t nchunks, int C, int normalize, void* __restrict__ vals, int64_t ld_vals,
+               float* __restrict__ wsum, const float* __restrict__ part_head,
+               const float* __restrict__ part_tail, const float* __restrict__ part_w) {
+  using Ch = Chunk<BF16>;
+  const int lane = threadIdx.x & (LPR - 1);
+  const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
+  if (c + 1 >= nchunks) return;
+  const int64_t s0 = c * kSplatChunk, s1 = s0 + kSplatChunk;
+  const int32_t v = chunk_first[c + 1];
+  const int32_t vb = offsets[v];
+  if (!(vb < s1 && vb >= s0)) return;
+  const int32_t ve = offsets[v + 1];
+  const int64_t last = (static_cast<int64_t>(ve) - 1) / kSplatChunk;
+  const int nchunk = C / Ch::N;
+  float acc[Q][Ch::N];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int ch = lane + q * LPR;
+#pragma unroll
+    for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
+    if (ch < nchunk) {
+      const float* src = part_tail + c * C + static_cast<int64_t>(ch) * Ch::N;
+#pragma unroll
+      for (int i = 0; i < Ch::N; ++i) acc[q][i] = src[i];
+    }
+  }
+  float ws = part_w[2 * c + 1];
+  for (int64_t c2 = c + 1; c2 <= last; ++c2) {
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int ch = lane + q * LPR;
+      if (ch < nchunk) {
+        const float* src = part_head + c2 * C + static_cast<int64_t>(ch) * Ch::N;
+#pragma unroll
+        for (int i = 0; i < Ch::N; ++i) acc[q][i] += src[i];
+      }
+    }
+    ws += part_w[2 * c2];
+  }
+  splat_store<BF16, LPR, Q>(v, acc, ws, lane, nchunk, normalize, vals, ld_vals, wsum);
 }
 
 // Slice (Eq. slice): out_p = sum_k b_pk x_{idx_pk}; one lane group per point.
@@ -241,20 +352,29 @@ inline unsigned grid_for(int64_t rows, int lpr) {
   return static_cast<unsigned>((rows * lpr + kBlock - 1) / kBlock);
 }
 
+template <bool BF16, int LPR, int Q>
+void splat_launch(const int32_t* off, const int32_t* ent, const float* ew, const int32_t* cf, int64_t n, int64_t total,
+                  const void* feat, int64_t ldf, int C, int norm, void* vals, int64_t ldv, float* wsum,
+                  float* ph, float* pt, float* pw, hipStream_t s) {
+  constexpr int B = (BF16 ? 8 : 16) / Q;
+  const int64_t nchunks = (total + kSplatChunk - 1) / kSplatChunk;
+  const dim3 g(grid_for(nchunks, LPR)), b(kBlock);
+  hipLaunchKernelGGL((k_splat_chunks<BF16, LPR, Q, B>), g, b, 0, s, off, ent, ew, cf, n, total, feat, ldf, C,
+                     norm, vals, ldv, wsum, ph, pt, pw);
+  if (nchunks > 1)
+    hipLaunchKernelGGL((k_splat_finish<BF16, LPR, Q>), g, b, 0, s, off, cf, nchunks, C, norm, vals, ldv,
+                       wsum, ph, pt, pw);
+}
+
 template <bool BF16>
-void splat_dispatch(int lpr, const int32_t* off, const int32_t* ent, const float* ew, const void* feat,
-                    int64_t ldf, int C, int norm, int64_t n, void* vals, int64_t ldv, float* wsum,
-                    hipStream_t s) {
-  const dim3 g(grid_for(n, lpr)), b(kBlock);
-  switch (lpr) {
-    case 1: hipLaunchKernelGGL((k_splat<BF16, 1>), g, b, 0, s, off, ent, ew, feat, ldf, C, norm, n, vals, ldv, wsum); break;
-    case 2: hipLaunchKernelGGL((k_splat<BF16, 2>), g, b, 0, s, off, ent, ew, feat, ldf, C, norm, n, vals, ldv, wsum); break;
-    case 4: hipLaunchKernelGGL((k_splat<BF16, 4>), g, b, 0, s, off, ent, ew, feat, ldf, C, norm, n, vals, ldv, wsum); break;
-    case 8: hipLaunchKernelGGL((k_splat<BF16, 8>), g, b, 0, s, off, ent, ew, feat, ldf, C, norm, n, vals, ldv, wsum); break;
-    case 16: hipLaunchKernelGGL((k_splat<BF16, 16>), g, b, 0, s, off, ent, ew, feat, ldf, C, norm, n, vals, ldv, wsum); break;
-    case 32: hipLaunchKernelGGL((k_splat<BF16, 32>), g, b, 0, s, off, ent, ew, feat, ldf, C, norm, n, vals, ldv, wsum); break;
-    default: hipLaunchKernelGGL((k_splat<BF16, 64>), g, b, 0, s, off, ent, ew, feat, ldf, C, norm, n, vals, ldv, wsum); break;
-  }
+void splat_dispatch(int lpr, int q, const int32_t* off, const int32_t* ent, const float* ew,
+                    const int32_t* cf, int64_t n, int64_t total, const void* feat, int64_t ldf, int C, int norm,
+                    void* vals, int64_t ldv, float* wsum, float* ph, float* pt, float* pw, hipStream_t s) {
+#define SPLAT_CASE(L, QQ) \
+  if (lpr == L && q == QQ) return splat_launch<BF16, L, QQ>(off, ent, ew, cf, n, total, feat, ldf, C, norm, vals, ldv, wsum, ph, pt, pw, s);
+  SPLAT_CASE(1, 1) SPLAT_CASE(2, 1) SPLAT_CASE(4, 1) SPLAT_CASE(8, 1) SPLAT_CASE(16, 1)
+  SPLAT_CASE(32, 1) SPLAT_CASE(64, 1) SPLAT_CASE(64, 2) SPLAT_CASE(64, 4)
+#undef SPLAT_CASE
 }
 
 template <bool BF16>
@@ -300,14 +420,26 @@ void deform_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, con
 int splat_max_channels(bool bf16) { return (bf16 ? 8 : 4) * 64 * 4; }
 int deform_max_channels(bool bf16) { return (bf16 ? 8 : 4) * 64 * 2; }
 
-void launch_splat(const int32_t* offsets, const int32_t* entries, const float* entry_w, const void* feat,
-                  int64_t ld_feat, int C, int bf16, int normalize, int64_t n, void* vals,
-                  int64_t ld_vals, float* wsum, hipStream_t s) {
-  if (n <= 0) return;
+int64_t splat_partial_floats(int64_t total, int C) {
+  const int64_t nchunks = (total + kSplatChunk - 1) / kSplatChunk;
+  return nchunks * (2 * static_cast<int64_t>(C) + 2);
+}
+
+void launch_splat(const int32_t* offsets, const int32_t* entries, const float* entry_w,
+                  const int32_t* chunk_first, int64_t n, int64_t total, const void* feat, int64_t ld_feat, int C,
+                  int bf16, int normalize, void* vals, int64_t ld_vals, float* wsum, float* partials,
+                  hipStream_t s) {
+  if (total <= 0) return;
+  const int chunks = C / (bf16 ? 8 : 4);
   const int lpr = lanes_per_row(C, bf16 != 0);
+  const int q = chunks <= lpr ? 1 : (chunks <= 2 * lpr ? 2 : 4);
+  const int64_t nchunks = (total + kSplatChunk - 1) / kSplatChunk;
+  float* ph = partials;
+  float* pt = partials + nchunks * C;
+  float* pw = partials + 2 * nchunks * C;
   ScopedKernelTimer tm("splat", s);
-  if (bf16) splat_dispatch<true>(lpr, offsets, entries, entry_w, feat, ld_feat, C, normalize, n, vals, ld_vals, wsum, s);
-  else splat_dispatch<false>(lpr, offsets, entries, entry_w, feat, ld_feat, C, normalize, n, vals, ld_vals, wsum, s);
+  if (bf16) splat_dispatch<true>(lpr, q, offsets, entries, entry_w, chunk_first, n, total, feat, ld_feat, C, normalize, vals, ld_vals, wsum, ph, pt, pw, s);
+  else splat_dispatch<false>(lpr, q, offsets, entries, entry_w, chunk_first, n, total, feat, ld_feat, C, normalize, vals, ld_vals, wsum, ph, pt, pw, s);
 }
 
 void launch_slice(const int32_t* idx, const float* w, int64_t m, const void* vals, int64_t ld_vals,
