@@ -20,6 +20,8 @@
 // Any assignment of K indices to (lane group, element) works as long as A
 // and B use the same one; the accumulator layout is fixed by the hardware:
 // lane l holds rows 4*(l/16) + r, r = 0..3, of column l%16.
+#include <type_traits>
+
 #include "lattice_internal.h"
 
 namespace lat {
@@ -175,24 +177,229 @@ void conv_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in,
                      ld_in, Cin, W, bias, Cout, relu, out, ld_out);
 }
 
+// ---------------------------------------------------------------------------
+// LDS-staged pipeline.  A stage is one tap and KC channels.  The whole
+// workgroup gathers the stage's A tile (BM neighbour rows, KC channels) and
+// B tile (BN weight rows, KC channels) into LDS with 16-byte loads, 8 or 16
+// lanes per row segment; the next stage's global loads are issued before the
+// current stage is multiplied, so their latency hides behind the MFMAs.  Rows
+// of the LDS tiles are padded by 16 bytes so that the 16 rows read by one
+// MFMA fragment fall in different banks.  Workgroups are numbered so that
+// each XCD gets a contiguous range of row tiles: neighbouring rows (the
+// gather's halo) then stay in that XCD's L2.
+// ---------------------------------------------------------------------------
+template <bool BF16, int BM, int BN, int WM, int WN, int KCB>
+struct LdsConv {
+  static constexpr int U = BF16 ? 2 : 4;            // bytes per element
+  static constexpr int EPC = 16 / U;                // elements per 16-byte chunk
+  static constexpr int KC = KCB / U;                // channels per stage
+  static constexpr int CPR = KCB / 16;              // chunks per row per stage
+  static constexpr int LDR = KC + EPC;              // padded LDS row (elements)
+  static constexpr int RM = BM / (16 * WM);
+  static constexpr int RN = BN / (16 * WN);
+  static constexpr int KS = BF16 ? 32 : 16;         // channels per MFMA step
+  static constexpr int EPL = BF16 ? 8 : 4;          // elements per lane per MFMA step
+  static constexpr int A_PER_T = BM * CPR / kBlock; // A chunks copied per thread
+  static constexpr int B_PER_T = (BN * CPR + kBlock - 1) / kBlock;
+  static constexpr int A_BYTES = BM * LDR * U;
+  static constexpr int B_BYTES = BN * LDR * U;
+  static constexpr int LDS_BYTES = 2 * (A_BYTES + B_BYTES) + kTaps * BM * 4;
+  static_assert(WM * WN == kWaves, "four waves");
+  static_assert(RM >= 1 && RN >= 1, "wave tile");
+  static_assert(A_PER_T >= 1 && BM * CPR % kBlock == 0, "A copy split");
+};
+
+template <bool BF16, int BM, int BN, int WM, int WN, int KCB>
+__global__ void __launch_bounds__(kBlock)
+k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const void* __restrict__ in,
+           int64_t ld_in, int Cin, const void* __restrict__ W, const float* __restrict__ bias, int Cout,
+           int relu, void* __restrict__ out, int64_t ld_out, unsigned row_tiles) {
+  using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
+  using E = typename std::conditional<BF16, uint16_t, float>::type;
+  extern __shared__ __align__(16) unsigned char smem[];
+  E* As = reinterpret_cast<E*>(smem);
+  E* Bs = reinterpret_cast<E*>(smem + 2 * P::A_BYTES);
+  int32_t* nbt = reinterpret_cast<int32_t*>(smem + 2 * (P::A_BYTES + P::B_BYTES));
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int li = lane & 15;
+  const int lg = lane >> 4;
+  // XCD-aware tile order: workgroup b runs on XCD b % 8; give each XCD a
+  // contiguous range of row tiles.
+  const unsigned b = blockIdx.x;
+  const unsigned per_xcd = (row_tiles + 7) / 8;
+  const unsigned tile = (b % 8) * per_xcd + b / 8;
+  if (tile >= row_tiles) return;
+  const int64_t row0 = static_cast<int64_t>(tile) * BM;
+  const int col0 = blockIdx.y * BN;
+  const int wm = wave % WM, wn = wave / WM;
+
+  for (int i = tid; i < kTaps * BM; i += kBlock) {
+    const int t = i / BM, r = i - t * BM;
+    nbt[i] = row0 + r < n_out ? nbr[t * ldn + row0 + r] : -1;
+  }
+  __syncthreads();
+
+  const int kc_steps = (Cin + P::KC - 1) / P::KC;
+  const int stages = kTaps * kc_steps;
+
+  // global -> register copies of one stage
+  using V = uint4;
+  V ra[P::A_PER_T], rb[P::B_PER_T];
+  auto fetch = [&](int st) {
+    const int t = st / kc_steps;
+    const int kc = (st - t * kc_steps) * P::KC;
+#pragma unroll
+    for (int j = 0; j < P::A_PER_T; ++j) {
+      const int q = tid + j * kBlock;
+      const int r = q / P::CPR, cc = q % P::CPR;
+      const int ch = kc + cc * P::EPC;
+      const int32_t nb = nbt[t * BM + r];
+      ra[j] = (nb >= 0 && ch < Cin)
+                  ? *reinterpret_cast<const V*>(static_cast<const E*>(in) + static_cast<int64_t>(nb) * ld_in + ch)
+                  : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int j = 0; j < P::B_PER_T; ++j) {
+      const int q = tid + j * kBlock;
+      const int r = q / P::CPR, cc = q % P::CPR;
+      const int ch = kc + cc * P::EPC;
+      const int col = col0 + r;
+      rb[j] = (q < BN * P::CPR && col < Cout && ch < Cin)
+                  ? *reinterpret_cast<const V*>(static_cast<const E*>(W) +
+                                                (static_cast<int64_t>(t) * Cout + col) * Cin + ch)
+                  : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto stash = [&](int buf) {
+    E* a = As + buf * (BM * P::LDR);
+    E* bb = Bs + buf * (BN * P::LDR);
+#pragma unroll
+    for (int j = 0; j < P::A_PER_T; ++j) {
+      const int q = tid + j * kBlock;
+      const int r = q / P::CPR, cc = q % P::CPR;
+      *reinterpret_cast<V*>(a + r * P::LDR + cc * P::EPC) = ra[j];
+    }
+#pragma unroll
+    for (int j = 0; j < P::B_PER_T; ++j) {
+      const int q = tid + j * kBlock;
+      if (q < BN * P::CPR) {
+        const int r = q / P::CPR, cc = q % P::CPR;
+        *reinterpret_cast<V*>(bb + r * P::LDR + cc * P::EPC) = rb[j];
+      }
+    }
+  };
+
+  f32x4 acc[P::RM][P::RN];
+#pragma unroll
+  for (int a = 0; a < P::RM; ++a)
+#pragma unroll
+    for (int c = 0; c < P::RN; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int st = 0; st < stages; ++st) {
+    const int buf = st & 1;
+    if (st + 1 < stages) fetch(st + 1);
+    const E* a = As + buf * (BM * P::LDR) + (wm * P::RM * 16 + li) * P::LDR + lg * P::EPL;
+    const E* bb = Bs + buf * (BN * P::LDR) + (wn * P::RN * 16 + li) * P::LDR + lg * P::EPL;
+#pragma unroll
+    for (int k = 0; k < P::KC; k += P::KS) {
+      Frag<BF16> fa[P::RM], fb[P::RN];
+#pragma unroll
+      for (int i = 0; i < P::RM; ++i) fa[i].load(a, i * 16 * P::LDR + k);
+#pragma unroll
+      for (int j = 0; j < P::RN; ++j) fb[j].load(bb, j * 16 * P::LDR + k);
+      if constexpr (BF16) {
+#pragma unroll
+        for (int i = 0; i < P::RM; ++i)
+#pragma unroll
+          for (int j = 0; j < P::RN; ++j) mma(acc[i][j], fa[i], fb[j]);
+      } else {
+        // interleave independent accumulators between dependent MFMAs
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int i = 0; i < P::RM; ++i)
+#pragma unroll
+            for (int j = 0; j < P::RN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i].v[e], fb[j].v[e], acc[i][j], 0, 0, 0);
+      }
+    }
+    if (st + 1 < stages) stash(buf ^ 1);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int j = 0; j < P::RN; ++j) {
+    const int col = col0 + (wn * P::RN + j) * 16 + li;
+    if (col >= Cout) continue;
+    const float bv = bias ? bias[col] : 0.f;
+#pragma unroll
+    for (int i = 0; i < P::RM; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = row0 + (wm * P::RM + i) * 16 + lg * 4 + r;
+        if (row >= n_out) continue;
+        float v = acc[i][j][r] + bv;
+        if (relu) v = fmaxf(v, 0.f);
+        if constexpr (BF16)
+          static_cast<uint16_t*>(out)[row * ld_out + col] = f32_to_bf16(v);
+        else
+          static_cast<float*>(out)[row * ld_out + col] = v;
+      }
+  }
+}
+
+template <bool BF16, int BM, int BN, int WM, int WN, int KCB>
+void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
+                     int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
+                     int64_t ld_out, hipStream_t s) {
+  using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
+  static bool lds_limit_set = false;
+  if (!lds_limit_set) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_lds<BF16, BM, BN, WM, WN, KCB>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, P::LDS_BYTES);
+    lds_limit_set = true;
+  }
+  const int64_t tiles = (n_out + BM - 1) / BM;
+  const unsigned per_xcd = static_cast<unsigned>((tiles + 7) / 8);
+  const dim3 grid(per_xcd * 8, static_cast<unsigned>((Cout + BN - 1) / BN));
+  hipLaunchKernelGGL((k_conv_lds<BF16, BM, BN, WM, WN, KCB>), grid, dim3(kBlock), P::LDS_BYTES, s, nbr, ldn,
+                     n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, static_cast<unsigned>(tiles));
+}
+
 int64_t blocks_of(int64_t n_out, int Cout, int rows, int cols) {
   return ((n_out + rows - 1) / rows) * ((Cout + cols - 1) / cols);
 }
 
 // Tile choice: the largest tile that still gives every CU a couple of
-// workgroups; small lattice levels fall back to 16-row wave tiles.
+// workgroups; small lattice levels fall back to narrower tiles.
 template <bool BF16>
 void conv_dispatch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                    int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
                    int64_t ld_out, hipStream_t s) {
   constexpr int64_t kWant = 512;
-  if (Cout > 32 && blocks_of(n_out, Cout, 128, 64) >= kWant)
-    return conv_launch<BF16, 2, 4, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-  if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= kWant)
-    return conv_launch<BF16, 1, 4, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-  if (Cout > 16)
-    return conv_launch<BF16, 1, 2, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-  return conv_launch<BF16, 1, 1, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+  if (Cout <= 16)
+    return conv_launch<BF16, 1, 1, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+  if constexpr (BF16) {
+    if (Cout > 64 && blocks_of(n_out, Cout, 128, 128) >= kWant)
+      return conv_lds_launch<true, 128, 128, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+    if (Cout > 32 && blocks_of(n_out, Cout, 128, 64) >= kWant)
+      return conv_lds_launch<true, 128, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+    if (Cout > 32)
+      return conv_lds_launch<true, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+    return conv_lds_launch<true, 64, 32, 4, 1, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+  } else {
+    if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= kWant)
+      return conv_lds_launch<false, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+    if (Cout > 32)
+      return conv_lds_launch<false, 32, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+    return conv_lds_launch<false, 32, 32, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+  }
 }
 
 }  // namespace
