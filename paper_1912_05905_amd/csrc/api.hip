@@ -200,11 +200,22 @@ struct DevBuf {
   size_t bytes = 0;
 };
 
+struct DeviceCounters {
+  int32_t counter;
+  uint32_t err;
+};
+
 struct lattice_s {
   int level = 0;
   int64_t m = 0;
-  int64_t n = 0;
+  int64_t n = 0;                 // valid once counts_known
+  int64_t nmax = 0;              // host-side bound on n (buffer sizes)
   int64_t cap = 0;               // hash slots
+  bool counts_known = true;      // n and the device error flag have been read back
+  DeviceCounters* dc = nullptr;  // device counters (vertex count, error bits)
+  DeviceCounters* host_dc = nullptr;  // pinned landing slot of their readback
+  hipEvent_t counts_ready = nullptr;  // recorded after the readback
+  int chunk = 64;                // list entries per splat work item
   int status = LAT_OK;           // poisoned when != LAT_OK
   int children = 0;
   lattice_s* parent = nullptr;
@@ -222,10 +233,11 @@ struct lattice_s {
   float* entry_w = nullptr;      // 4m weights of those entries
   int32_t* chunk_first = nullptr;  // vertex owning list position c * kSplatChunk
   int64_t total = 0;               // number of list entries (4m)
-  int32_t* nbr = nullptr;        // 9 x n same-level table (tap-major)
-  int32_t* down = nullptr;       // 9 x n table into the parent (coarse levels)
+  int32_t* nbr = nullptr;        // 9 x nmax same-level table (tap-major, ld nmax)
+  int32_t* down = nullptr;       // 9 x nmax table into the parent (coarse levels, ld nmax)
   int32_t* up = nullptr;         // 9 x n_parent table from the parent into this level
   bool up_built = false;
+  int64_t retry_cap = 0;          // coarse levels: table size of a rebuild after overflow
 
   HashView hash() const { return HashView{tkeys, tvals, static_cast<uint64_t>(cap - 1)}; }
 
@@ -236,6 +248,7 @@ struct lattice_s {
   }
 
   void free_all() {
+    if (!counts_known && counts_ready) (void)hipEventSynchronize(counts_ready);
     for (auto& b : owned) Pool::get().release(b.p, b.bytes, stream);
     owned.clear();
   }
@@ -243,21 +256,53 @@ struct lattice_s {
 
 namespace {
 
-struct DeviceCounters {
-  int32_t counter;
-  uint32_t err;
-};
-
-// pinned host landing zone for the per-create readback
-DeviceCounters* host_readback() {
-  thread_local DeviceCounters* h = nullptr;
-  if (!h) {
-    void* p = nullptr;
-    if (hipHostMalloc(&p, sizeof(DeviceCounters) * 2, hipHostMallocDefault) != hipSuccess) return nullptr;
-    h = static_cast<DeviceCounters*>(p);
+// Pinned host slots for the counter readbacks and a pool of events; both are
+// recycled when handles are destroyed.
+class HostSlots {
+ public:
+  static HostSlots& get() {
+    static HostSlots* h = new HostSlots();
+    return *h;
   }
-  return h;
-}
+  DeviceCounters* take() {
+    std::lock_guard<std::mutex> lk(mu_);
+    if (free_.empty()) {
+      void* p = nullptr;
+      constexpr int kSlab = 256;
+      if (hipHostMalloc(&p, sizeof(DeviceCounters) * kSlab, hipHostMallocDefault) != hipSuccess) return nullptr;
+      for (int i = 0; i < kSlab; ++i) free_.push_back(static_cast<DeviceCounters*>(p) + i);
+    }
+    DeviceCounters* d = free_.back();
+    free_.pop_back();
+    return d;
+  }
+  void give(DeviceCounters* d) {
+    if (!d) return;
+    std::lock_guard<std::mutex> lk(mu_);
+    free_.push_back(d);
+  }
+  hipEvent_t take_event() {
+    std::lock_guard<std::mutex> lk(mu_);
+    if (!events_.empty()) {
+      hipEvent_t e = events_.back();
+      events_.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+    return e;
+  }
+  void give_event(hipEvent_t e) {
+    if (!e) return;
+    std::lock_guard<std::mutex> lk(mu_);
+    events_.push_back(e);
+  }
+
+ private:
+  std::mutex mu_;
+  std::vector<DeviceCounters*> free_;
+  std::vector<hipEvent_t> events_;
+};
 
 int64_t next_pow2(int64_t v) {
   int64_t c = 1;
@@ -292,14 +337,20 @@ struct Scratch {
   template <class T> T* as() const { return static_cast<T*>(p); }
 };
 
-// One attempt at building a lattice with a table of `cap` slots.
-// Returns LAT_EHASHFULL (with nothing kept) when the table overflows.
-int build_attempt(lattice_s* L, const float* pos, const float a[3], const lattice_s* parent, int64_t cap,
+// Enqueue the construction of a lattice with a table of `cap` slots:
+// clear, insert, readback of the vertex count and error bits (asynchronous,
+// with an event), then the scan, the vertex lists and the neighbour table,
+// which take the vertex count from device memory.  Nothing waits here.
+int enqueue_build(lattice_s* L, const float* pos, const float a[3], const lattice_s* parent, int64_t cap,
                   hipStream_t s) {
   const int64_t m = L->m;
   const int64_t refs = 4 * m;
   const int64_t nmax = std::min(cap, refs);
   L->cap = cap;
+  L->nmax = nmax;
+  L->total = refs;
+  L->chunk = refs >= 64 * 32768 ? 64 : (refs >= 32 * 32768 ? 32 : 16);
+  const int64_t nchunks = (refs + L->chunk - 1) / L->chunk;
   int st;
   void* p;
 #define ALLOC(field, type, count)                                                 \
@@ -312,79 +363,100 @@ int build_attempt(lattice_s* L, const float* pos, const float a[3], const lattic
   ALLOC(tkeys, uint64_t, cap);
   ALLOC(tvals, int32_t, cap);
   ALLOC(vkeys, uint64_t, nmax);
+  ALLOC(dc, DeviceCounters, 1);
+  ALLOC(offsets, int32_t, nmax + 1);
+  ALLOC(entries, int32_t, refs);
+  ALLOC(entry_w, float, refs);
+  ALLOC(chunk_first, int32_t, nchunks);
+  ALLOC(nbr, int32_t, kTaps * nmax);
 #undef ALLOC
-  Scratch slot_count, vslot, slot, rank, dcs;
+  Scratch slot_count, vslot, slot, rank, work;
   if ((st = slot_count.get(sizeof(int32_t) * cap, s)) != LAT_OK) return st;
   if ((st = vslot.get(sizeof(int32_t) * nmax, s)) != LAT_OK) return st;
   if ((st = slot.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
   if ((st = rank.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
-  if ((st = dcs.get(sizeof(DeviceCounters), s)) != LAT_OK) return st;
-  DeviceCounters* dc = dcs.as<DeviceCounters>();
+  if ((st = work.get(sizeof(int32_t) * scan_workspace_elems(), s)) != LAT_OK) return st;
+  if (!L->host_dc && !(L->host_dc = HostSlots::get().take())) return fail(LAT_ENOMEM, "pinned host slot");
+  if (!L->counts_ready && !(L->counts_ready = HostSlots::get().take_event()))
+    return fail(LAT_EDEVICE, "event creation failed");
 
-  launch_clear_table(L->tkeys, slot_count.as<int32_t>(), cap, reinterpret_cast<uint64_t*>(dc), s);
+  launch_clear_table(L->tkeys, slot_count.as<int32_t>(), cap, reinterpret_cast<uint64_t*>(L->dc), s);
   launch_insert_points(pos, parent ? parent->y : nullptr, 0.5f, a[0], a[1], a[2], m, L->hash(),
-                       &dc->counter, slot_count.as<int32_t>(), L->vkeys, vslot.as<int32_t>(),
-                       slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->y, &dc->err, s);
-  if ((st = check_launch("insert")) != LAT_OK) return st;
-  DeviceCounters* h = host_readback();
-  if (!h) return fail(LAT_ENOMEM, "pinned host buffer");
-  HIP_TRY(hipMemcpyAsync(h, dc, sizeof(DeviceCounters), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
-  const int dev_status = status_from_err_bits(h->err);
+                       &L->dc->counter, slot_count.as<int32_t>(), L->vkeys, vslot.as<int32_t>(),
+                       slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->y, &L->dc->err, s);
+  HIP_TRY(hipMemcpyAsync(L->host_dc, L->dc, sizeof(DeviceCounters), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipEventRecord(L->counts_ready, s));
+  L->counts_known = false;
+  const int32_t* n_dev = &L->dc->counter;
+  launch_count_scan(slot_count.as<int32_t>(), vslot.as<int32_t>(), n_dev, L->offsets, work.as<int32_t>(), s);
+  launch_fill_lists(L->hash(), slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->offsets, L->idx,
+                    L->entries, L->entry_w, L->chunk_first, L->chunk, refs, s);
+  launch_neighbor_table(L->hash(), L->vkeys, n_dev, nmax, L->nbr, nmax, s);
+  if (parent) {
+    if ((st = L->alloc(sizeof(int32_t) * kTaps * nmax, s, &p)) != LAT_OK) return st;
+    L->down = static_cast<int32_t*>(p);
+    launch_down_table(parent->hash(), L->vkeys, n_dev, nmax, L->down, nmax, s);
+  }
+  return check_launch("lattice build");
+}
+
+// Table size for a build: the caller's hint, or 2x the worst case (d+1
+// vertices per point); coarse levels start from 2x the parent's vertex count
+// when it is known and are rebuilt at the worst case should that overflow.
+int64_t initial_capacity(const lattice_s* L, const lattice_s* parent, int64_t capacity_hint) {
+  const int64_t refs = 4 * L->m;
+  const int64_t full = next_pow2(std::max<int64_t>(1024, 2 * refs));
+  if (capacity_hint > 0) return next_pow2(std::max<int64_t>(1024, 2 * std::min(capacity_hint, refs)));
+  if (parent && parent->counts_known) return std::min(full, next_pow2(std::max<int64_t>(1024, 2 * parent->n)));
+  return full;
+}
+
+// Wait for a handle's counter readback; report device-side errors.
+int ensure_counts(lattice_s* L) {
+  if (L->counts_known) return L->status;
+  HIP_TRY(hipEventSynchronize(L->counts_ready));
+  L->counts_known = true;
+  L->n = L->host_dc->counter;
+  const int dev_status = status_from_err_bits(L->host_dc->err);
+  if (dev_status == LAT_EHASHFULL && L->parent && L->retry_cap > L->cap) {
+    // coarse level with a table sized from the parent: rebuild at full size
+    const int64_t cap = L->retry_cap;
+    L->retry_cap = 0;
+    L->free_all();
+    const float a[3] = {0.f, 0.f, 0.f};
+    int st = enqueue_build(L, nullptr, a, L->parent, cap, L->stream);
+    if (st != LAT_OK) { L->status = st; return st; }
+    return ensure_counts(L);
+  }
   if (dev_status != LAT_OK) {
     const char* why = dev_status == LAT_EHASHFULL ? "hash table full (raise capacity_hint)"
                       : dev_status == LAT_EKEYRANGE ? "a vertex coordinate reaches 2^20 (positions / sigma too large)"
                                                     : "non-finite position";
+    L->status = dev_status;
     return fail(dev_status, why);
   }
-  const int64_t n = h->counter;
-  L->n = n;
-  L->total = refs;
-  const int64_t nchunks = (refs + kSplatChunk - 1) / kSplatChunk;
-#define ALLOC(field, type, count)                                                 \
-  if ((st = L->alloc(sizeof(type) * static_cast<size_t>(count), s, &p)) != LAT_OK) \
-    return st;                                                                    \
-  L->field = static_cast<type*>(p)
-  ALLOC(offsets, int32_t, n + 1);
-  ALLOC(entries, int32_t, refs);
-  ALLOC(entry_w, float, refs);
-  ALLOC(chunk_first, int32_t, nchunks);
-  ALLOC(nbr, int32_t, kTaps * n);
-#undef ALLOC
-  Scratch work;
-  if ((st = work.get(sizeof(int32_t) * scan_workspace_elems(n), s)) != LAT_OK) return st;
-  launch_count_scan(slot_count.as<int32_t>(), vslot.as<int32_t>(), L->offsets, n, work.as<int32_t>(), s);
-  launch_fill_lists(L->hash(), slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->offsets, L->idx,
-                    L->entries, L->entry_w, L->chunk_first, refs, s);
-  launch_neighbor_table(L->hash(), L->vkeys, n, L->nbr, n, s);
-  return check_launch("lattice build");
+  return LAT_OK;
 }
 
-// Build a lattice for `m` points: from positions (pos, a[]) or from a
-// parent's elevated positions halved.  Coarse levels first try a table sized
-// from the parent's vertex count and fall back to the worst-case size.
 int build_lattice(lattice_s* L, const float* pos, const float a[3], const lattice_s* parent,
                   int64_t capacity_hint, hipStream_t s) {
   const int64_t m = L->m;
   if (m == 0) return LAT_OK;
-  const int64_t refs = 4 * m;
-  if (refs > INT32_MAX) return fail(LAT_EUNSUPPORTED, "more than 2^29 points");
-  const int64_t full = next_pow2(std::max<int64_t>(1024, 2 * refs));
-  int64_t cap = full;
-  if (capacity_hint > 0) cap = next_pow2(std::max<int64_t>(1024, 2 * std::min(capacity_hint, refs)));
-  else if (parent) cap = std::min(full, next_pow2(std::max<int64_t>(1024, 2 * parent->n)));
-  int st = build_attempt(L, pos, a, parent, cap, s);
-  if (st == LAT_EHASHFULL && capacity_hint == 0 && cap < full) {
-    L->free_all();
-    st = build_attempt(L, pos, a, parent, full, s);
-  }
-  return st;
+  if (4 * m > INT32_MAX) return fail(LAT_EUNSUPPORTED, "more than 2^29 points");
+  const int64_t cap = initial_capacity(L, parent, capacity_hint);
+  L->retry_cap = (parent && capacity_hint == 0) ? next_pow2(std::max<int64_t>(1024, 8 * m)) : 0;
+  return enqueue_build(L, pos, a, parent, cap, s);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-int check_handle(const lattice_s* L) {
+// A usable handle: not null, its vertex count read back, no device error.
+int check_handle(lattice_s* L) {
   if (!L) return fail(LAT_EINVAL, "null lattice handle");
+  if (L->status == LAT_OK) {
+    const int st = ensure_counts(L);
+    if (st != LAT_OK) return st;
+  }
   if (L->status != LAT_OK) return fail(L->status, "lattice handle is poisoned by an earlier error");
   return LAT_OK;
 }
@@ -413,7 +485,7 @@ bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
   return x < y + bbytes && y < x + abytes;
 }
 
-int conv_common(const int32_t* table, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
+int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                 int Cin, const void* W, const float* bias, int Cout, lat_dtype dt, int flags,
                 void* out, int64_t ld_out, hipStream_t s) {
   int st;
@@ -431,7 +503,7 @@ int conv_common(const int32_t* table, int64_t n_out, int64_t n_in, const void* i
                static_cast<size_t>((n_out - 1) * ld_out + Cout) * u))
     return fail(LAT_EINVAL, "in and out overlap");
   if (n_out == 0) return LAT_OK;
-  launch_conv(table, n_out, n_out, in, ld_in, Cin, W, bias, Cout, dt == LAT_BF16, flags & LAT_RELU, out,
+  launch_conv(table, ldn, n_out, in, ld_in, Cin, W, bias, Cout, dt == LAT_BF16, flags & LAT_RELU, out,
               ld_out, s);
   return check_launch("conv");
 }
@@ -484,6 +556,8 @@ int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_ho
   const int st = build_lattice(L, pos_dev, a, nullptr, capacity_hint, stream);
   if (st != LAT_OK) {
     L->free_all();
+    HostSlots::get().give(L->host_dc);
+    HostSlots::get().give_event(L->counts_ready);
     delete L;
     return st;
   }
@@ -504,17 +578,10 @@ int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, l
   L->stream = stream;
   const float a[3] = {0.f, 0.f, 0.f};
   st = build_lattice(L, nullptr, a, fine, capacity_hint, stream);
-  if (st == LAT_OK && L->n > 0) {
-    void* p;
-    st = L->alloc(sizeof(int32_t) * kTaps * L->n, stream, &p);
-    if (st == LAT_OK) {
-      L->down = static_cast<int32_t*>(p);
-      launch_down_table(fine->hash(), L->vkeys, L->n, L->down, L->n, stream);
-      st = check_launch("down table");
-    }
-  }
   if (st != LAT_OK) {
     L->free_all();
+    HostSlots::get().give(L->host_dc);
+    HostSlots::get().give_event(L->counts_ready);
     delete L;
     return st;
   }
@@ -528,6 +595,8 @@ int lattice_destroy(lattice_t L) {
   if (L->children > 0) return fail(LAT_ELEVEL, "destroy the coarser lattices first");
   if (L->parent) L->parent->children -= 1;
   L->free_all();
+  HostSlots::get().give(L->host_dc);
+  HostSlots::get().give_event(L->counts_ready);
   delete L;
   return LAT_OK;
 }
@@ -580,7 +649,7 @@ int lattice_export_neighbors(lattice_t L, int32_t* nbr_dev, hipStream_t stream) 
   if ((st = check_handle(L)) != LAT_OK) return st;
   if (L->n == 0) return LAT_OK;
   if (!nbr_dev) return fail(LAT_EINVAL, "nbr is null");
-  launch_transpose_table(L->nbr, L->n, L->n, nbr_dev, stream);
+  launch_transpose_table(L->nbr, L->nmax, L->n, nbr_dev, stream);
   return check_launch("export neighbours");
 }
 
@@ -598,8 +667,8 @@ int lattice_splat(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat
                                       " channels");
   if (L->n == 0) return LAT_OK;
   Scratch partials;
-  if ((st = partials.get(sizeof(float) * splat_partial_floats(L->total, C), stream)) != LAT_OK) return st;
-  launch_splat(L->offsets, L->entries, L->entry_w, L->chunk_first, L->n, L->total, feat_dev, ld_feat, C,
+  if ((st = partials.get(sizeof(float) * splat_partial_floats(L->total, L->chunk, C), stream)) != LAT_OK) return st;
+  launch_splat(L->offsets, L->entries, L->entry_w, L->chunk_first, L->chunk, L->nmax, L->total, feat_dev, ld_feat, C,
                dt == LAT_BF16, normalize != 0, vals_dev, ld_vals, wsum_dev, partials.as<float>(), stream);
   return check_launch("splat");
 }
@@ -614,7 +683,7 @@ int lattice_conv(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in
   if (dst == src) table = dst->nbr;
   else if (dst->parent == src) table = dst->down;
   else return fail(LAT_ELEVEL, "dst must be src or lattice_coarsen(src)");
-  return conv_common(table, dst->n, src->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt, flags,
+  return conv_common(table, dst->nmax, dst->n, src->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt, flags,
                      out_dev, ld_out, stream);
 }
 
@@ -634,7 +703,7 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
     if (stream != coarse->stream) HIP_TRY(hipStreamSynchronize(coarse->stream));
     coarse->up_built = true;
   }
-  return conv_common(coarse->up, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
+  return conv_common(coarse->up, fine->n, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
                      flags, out_dev, ld_out, stream);
 }
 

@@ -58,20 +58,28 @@ __device__ inline int32_t global_insert(const HashView& h, uint64_t key, bool* c
   return -1;
 }
 
-__device__ inline int32_t block_exclusive_sum(int32_t v, int32_t* lds, int32_t* total) {
-  const int tid = threadIdx.x;
-  lds[tid] = v;
-  __syncthreads();
-  for (int off = 1; off < kBlock; off <<= 1) {
-    const int32_t add = tid >= off ? lds[tid - off] : 0;
-    __syncthreads();
-    lds[tid] += add;
-    __syncthreads();
+// Exclusive prefix sum over the workgroup (wave shuffles, then the four
+// wave totals through LDS); *total receives the workgroup sum.
+__device__ inline int32_t block_exclusive_sum(int32_t v, int32_t* lds4, int32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int32_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int32_t y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
   }
-  const int32_t incl = lds[tid];
-  *total = lds[kBlock - 1];
+  if (lane == 63) lds4[wave] = x;
   __syncthreads();
-  return incl - v;
+  int32_t before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / 64; ++w) {
+    const int32_t sw = lds4[w];
+    if (w < wave) before += sw;
+    tot += sw;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + x - v;
 }
 
 // One thread per point.  Embedding: y = E (g/sigma) with E's columns
@@ -101,7 +109,8 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
   __shared__ int32_t lcount[kLdsSlots];
   __shared__ int32_t lslot[kLdsSlots];
   __shared__ int32_t lbase[kLdsSlots];
-  __shared__ int32_t scan_buf[kBlock];
+  __shared__ int32_t ulist[kBlock * kVerts];
+  __shared__ int32_t scan_buf[kBlock / 64];
   __shared__ int32_t id_base;
 
   const int tid = threadIdx.x;
@@ -233,33 +242,41 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
   }
   __syncthreads();
 
-  // 2. one global insert and one count update per distinct key
+  // 2. compact the distinct keys, then one global insert and one count
+  //    update per distinct key, spread over all threads
+  int32_t occupied = 0;
+  for (int j = 0; j < kLdsPerThread; ++j) occupied += lkey[tid + j * kBlock] != kEmptyKey ? 1 : 0;
+  int32_t nunique = 0;
+  int32_t at = block_exclusive_sum(occupied, scan_buf, &nunique);
+  for (int j = 0; j < kLdsPerThread; ++j) {
+    const int sl = tid + j * kBlock;
+    if (lkey[sl] != kEmptyKey) ulist[at++] = sl;
+  }
+  __syncthreads();
   uint32_t created_mask = 0;
   int32_t ncreated = 0;
-  for (int j = 0; j < kLdsPerThread; ++j) {
-    const int s = tid + j * kBlock;
-    const uint64_t key = lkey[s];
-    if (key == kEmptyKey) continue;
+  for (int u = tid, j = 0; u < nunique; u += kBlock, ++j) {
+    const int sl = ulist[u];
     bool created = false;
-    const int32_t gs = global_insert(h, key, &created, err);
-    lslot[s] = gs;
-    lbase[s] = gs >= 0 ? atomicAdd(&slot_count[gs], lcount[s]) : 0;
+    const int32_t gs = global_insert(h, lkey[sl], &created, err);
+    lslot[sl] = gs;
+    lbase[sl] = gs >= 0 ? atomicAdd(&slot_count[gs], lcount[sl]) : 0;
     if (created) {
       created_mask |= 1u << j;
       ++ncreated;
     }
   }
   int32_t nblock = 0;
-  int32_t my_first = block_exclusive_sum(ncreated, scan_buf, &nblock);
+  const int32_t my_first = block_exclusive_sum(ncreated, scan_buf, &nblock);
   if (tid == 0) id_base = nblock > 0 ? atomicAdd(counter, nblock) : 0;
   __syncthreads();
   int32_t id = id_base + my_first;
-  for (int j = 0; j < kLdsPerThread; ++j) {
+  for (int u = tid, j = 0; u < nunique; u += kBlock, ++j) {
     if (!(created_mask & (1u << j))) continue;
-    const int s = tid + j * kBlock;
-    const int32_t gs = lslot[s];
+    const int sl = ulist[u];
+    const int32_t gs = lslot[sl];
     h.vals[gs] = id;
-    vkeys[id] = lkey[s];
+    vkeys[id] = lkey[sl];
     vslot[id] = gs;
     ++id;
   }
@@ -279,70 +296,70 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
   }
 }
 
-// ---- exclusive scan of per-vertex counts (tile sums, scan of sums, apply) ----
+// ---- exclusive scan of per-vertex counts over a device-side n ----
+// kScanBlocks workgroups each own a contiguous range of vertices: the first
+// kernel sums each range, the second adds the sums of the earlier ranges and
+// scans its own range.  The count of vertex v is slot_count[vslot[v]].
+constexpr int kScanBlocks = 256;
 constexpr int kScanPer = 8;
-constexpr int kScanTile = kBlock * kScanPer;
-
-// count of vertex i: in[gather[i]] (reference count stored by table slot)
-__device__ inline int32_t vertex_count(const int32_t* in, const int32_t* gather, int64_t i) {
-  return in[gather[i]];
-}
 
 __global__ void __launch_bounds__(kBlock)
-k_scan_tiles(const int32_t* __restrict__ in, const int32_t* __restrict__ gather, int64_t n,
-             int32_t* __restrict__ sums) {
-  __shared__ int32_t lds[kBlock];
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x * kScanPer;
+k_scan_partials(const int32_t* __restrict__ slot_count, const int32_t* __restrict__ vslot,
+                const int32_t* __restrict__ n_dev, int32_t* __restrict__ sums) {
+  __shared__ int32_t lds4[kBlock / 64];
+  const int64_t n = *n_dev;
+  const int64_t per = (n + kScanBlocks - 1) / kScanBlocks;
+  const int64_t beg = blockIdx.x * per, end = min(beg + per, n);
   int32_t s = 0;
-  for (int j = 0; j < kScanPer; ++j)
-    if (base + j < n) s += vertex_count(in, gather, base + j);
+  for (int64_t i = beg + threadIdx.x; i < end; i += kBlock) s += slot_count[vslot[i]];
   int32_t total;
-  block_exclusive_sum(s, lds, &total);
+  block_exclusive_sum(s, lds4, &total);
   if (threadIdx.x == 0) sums[blockIdx.x] = total;
 }
 
 __global__ void __launch_bounds__(kBlock)
-k_scan_sums(int32_t* __restrict__ sums, int64_t nt) {
-  __shared__ int32_t lds[kBlock];
-  int32_t carry = 0;
-  for (int64_t start = 0; start < nt; start += kBlock) {
-    const int64_t i = start + threadIdx.x;
-    const int32_t v = i < nt ? sums[i] : 0;
-    int32_t total;
-    const int32_t ex = block_exclusive_sum(v, lds, &total);
-    if (i < nt) sums[i] = carry + ex;
-    carry += total;
+k_scan_ranges(const int32_t* __restrict__ slot_count, const int32_t* __restrict__ vslot,
+              const int32_t* __restrict__ n_dev, const int32_t* __restrict__ sums,
+              int32_t* __restrict__ offsets) {
+  __shared__ int32_t lds4[kBlock / 64];
+  const int64_t n = *n_dev;
+  const int64_t per = (n + kScanBlocks - 1) / kScanBlocks;
+  const int64_t beg = blockIdx.x * per, end = min(beg + per, n);
+  int32_t before = 0;
+  for (int b = threadIdx.x; b < static_cast<int>(blockIdx.x); b += kBlock) before += sums[b];
+  int32_t tmp;
+  block_exclusive_sum(before, lds4, &tmp);
+  int32_t carry = tmp;                       // sum of all earlier ranges
+  for (int64_t t0 = beg; t0 < end; t0 += kBlock * kScanPer) {
+    const int64_t base = t0 + threadIdx.x * kScanPer;
+    int32_t v[kScanPer];
+    int32_t loc = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+      v[j] = base + j < end ? slot_count[vslot[base + j]] : 0;
+      loc += v[j];
+    }
+    int32_t tile_total;
+    int32_t run = carry + block_exclusive_sum(loc, lds4, &tile_total);
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+      if (base + j < end) offsets[base + j] = run;
+      run += v[j];
+    }
+    carry += tile_total;
   }
-}
-
-__global__ void __launch_bounds__(kBlock)
-k_scan_apply(const int32_t* __restrict__ in, const int32_t* __restrict__ gather, int64_t n,
-             const int32_t* __restrict__ sums, int32_t* __restrict__ out) {
-  __shared__ int32_t lds[kBlock];
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x * kScanPer;
-  int32_t vals[kScanPer];
-  int32_t s = 0;
-  for (int j = 0; j < kScanPer; ++j) {
-    vals[j] = base + j < n ? vertex_count(in, gather, base + j) : 0;
-    s += vals[j];
-  }
-  int32_t total;
-  int32_t run = block_exclusive_sum(s, lds, &total) + sums[blockIdx.x];
-  for (int j = 0; j < kScanPer; ++j) {
-    if (base + j < n) out[base + j] = run;
-    if (base + j == n - 1) out[n] = run + vals[j];
-    run += vals[j];
-  }
+  if (end == n && beg < end && threadIdx.x == 0) offsets[n] = carry;
+  if (n == 0 && blockIdx.x == 0 && threadIdx.x == 0) offsets[0] = 0;
 }
 
 // Per reference e = p*(d+1)+k: vertex index, and its place in J_v:
 // entries[offsets[v] + rank] = e with the weight alongside.  The vertex that
-// owns list position c*E (E = kSplatChunk) is recorded for the chunked splat.
+// owns list position c*E (E = chunk) is recorded for the chunked splat.
 __global__ void __launch_bounds__(kBlock)
 k_fill_lists(HashView h, const int32_t* __restrict__ slot, const int32_t* __restrict__ rank,
              const float* __restrict__ w, const int32_t* __restrict__ offsets,
              int32_t* __restrict__ idx, int32_t* __restrict__ entries, float* __restrict__ entry_w,
-             int32_t* __restrict__ chunk_first, int64_t m4) {
+             int32_t* __restrict__ chunk_first, int chunk, int64_t m4) {
   const int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   if (e >= m4) return;
   const int32_t s = slot[e];
@@ -355,41 +372,45 @@ k_fill_lists(HashView h, const int32_t* __restrict__ slot, const int32_t* __rest
   const int32_t at = offsets[v] + rank[e];
   entries[at] = static_cast<int32_t>(e);
   entry_w[at] = w[e];
-  if (at % kSplatChunk == 0) chunk_first[at / kSplatChunk] = v;
+  if (at % chunk == 0) chunk_first[at / chunk] = v;
 }
 
 // nbr[t][v] for taps 1..8 (tap 0 = v): the vertex at c_v + o_t.
 __global__ void __launch_bounds__(kBlock)
-k_neighbor_table(HashView h, const uint64_t* __restrict__ vkeys, int64_t n, int32_t* __restrict__ nbr,
-                 int64_t ldn) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (i >= n * kTaps) return;
-  const int t = static_cast<int>(i / n);
-  const int64_t v = i - static_cast<int64_t>(t) * n;
-  if (t == 0) {
-    nbr[v] = static_cast<int32_t>(v);
-    return;
+k_neighbor_table(HashView h, const uint64_t* __restrict__ vkeys, const int32_t* __restrict__ n_dev,
+                 int32_t* __restrict__ nbr, int64_t ldn) {
+  const int64_t n = *n_dev;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n * kTaps;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int t = static_cast<int>(i / n);
+    const int64_t v = i - static_cast<int64_t>(t) * n;
+    if (t == 0) {
+      nbr[v] = static_cast<int32_t>(v);
+      continue;
+    }
+    int32_t c[kVerts];
+    unpack_key(vkeys[v], c);
+    for (int j = 0; j < kVerts; ++j) c[j] += tap_offset(t, j);
+    const uint64_t key = key_or_empty(c);
+    nbr[static_cast<int64_t>(t) * ldn + v] = key == kEmptyKey ? -1 : hash_find(h, key);
   }
-  int32_t c[kVerts];
-  unpack_key(vkeys[v], c);
-  for (int j = 0; j < kVerts; ++j) c[j] += tap_offset(t, j);
-  const uint64_t key = key_or_empty(c);
-  nbr[static_cast<int64_t>(t) * ldn + v] = key == kEmptyKey ? -1 : hash_find(h, key);
 }
 
 // Downsample: coarse vertex v reads the fine vertex at 2 c_v + o_t.
 __global__ void __launch_bounds__(kBlock)
-k_down_table(HashView fine, const uint64_t* __restrict__ ckeys, int64_t n, int32_t* __restrict__ nbr,
-             int64_t ldn) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (i >= n * kTaps) return;
-  const int t = static_cast<int>(i / n);
-  const int64_t v = i - static_cast<int64_t>(t) * n;
-  int32_t c[kVerts];
-  unpack_key(ckeys[v], c);
-  for (int j = 0; j < kVerts; ++j) c[j] = 2 * c[j] + tap_offset(t, j);
-  const uint64_t key = key_or_empty(c);
-  nbr[static_cast<int64_t>(t) * ldn + v] = key == kEmptyKey ? -1 : hash_find(fine, key);
+k_down_table(HashView fine, const uint64_t* __restrict__ ckeys, const int32_t* __restrict__ n_dev,
+             int32_t* __restrict__ nbr, int64_t ldn) {
+  const int64_t n = *n_dev;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n * kTaps;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int t = static_cast<int>(i / n);
+    const int64_t v = i - static_cast<int64_t>(t) * n;
+    int32_t c[kVerts];
+    unpack_key(ckeys[v], c);
+    for (int j = 0; j < kVerts; ++j) c[j] = 2 * c[j] + tap_offset(t, j);
+    const uint64_t key = key_or_empty(c);
+    nbr[static_cast<int64_t>(t) * ldn + v] = key == kEmptyKey ? -1 : hash_find(fine, key);
+  }
 }
 
 // Upsample: fine vertex v reads the coarse vertex at (c_v + o_t)/2 when that
@@ -464,43 +485,45 @@ void launch_insert_points(const float* pos, const float* y_in, float y_scale, fl
                      reinterpret_cast<float4*>(y_out), err);
 }
 
-int64_t scan_workspace_elems(int64_t n) { return (n + kScanTile - 1) / kScanTile + 1; }
+int64_t scan_workspace_elems() { return kScanBlocks; }
 
-void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, int32_t* offsets, int64_t n,
-                       int32_t* work, hipStream_t s) {
-  if (n <= 0) return;
-  const int64_t nt = (n + kScanTile - 1) / kScanTile;
+void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, const int32_t* n_dev,
+                       int32_t* offsets, int32_t* work, hipStream_t s) {
   ScopedKernelTimer tm("scan", s);
-  hipLaunchKernelGGL(k_scan_tiles, dim3(static_cast<unsigned>(nt)), dim3(kBlock), 0, s, slot_count,
-                     vslot, n, work);
-  hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(kBlock), 0, s, work, nt);
-  hipLaunchKernelGGL(k_scan_apply, dim3(static_cast<unsigned>(nt)), dim3(kBlock), 0, s, slot_count,
-                     vslot, n, work, offsets);
+  hipLaunchKernelGGL(k_scan_partials, dim3(kScanBlocks), dim3(kBlock), 0, s, slot_count, vslot, n_dev, work);
+  hipLaunchKernelGGL(k_scan_ranges, dim3(kScanBlocks), dim3(kBlock), 0, s, slot_count, vslot, n_dev, work,
+                     offsets);
 }
 
 void launch_fill_lists(HashView h, const int32_t* slot, const int32_t* rank, const float* w,
                        const int32_t* offsets, int32_t* idx, int32_t* entries, float* entry_w,
-                       int32_t* chunk_first, int64_t m4, hipStream_t s) {
+                       int32_t* chunk_first, int chunk, int64_t m4, hipStream_t s) {
   if (m4 <= 0) return;
   ScopedKernelTimer tm("lists", s);
   hipLaunchKernelGGL(k_fill_lists, dim3(blocks_for(m4)), dim3(kBlock), 0, s, h, slot, rank, w, offsets,
-                     idx, entries, entry_w, chunk_first, m4);
+                     idx, entries, entry_w, chunk_first, chunk, m4);
 }
 
-void launch_neighbor_table(HashView h, const uint64_t* vkeys, int64_t n, int32_t* nbr, int64_t ldn,
-                           hipStream_t s) {
-  if (n <= 0) return;
+// grid for a grid-stride pass over up to `work` items
+inline unsigned stride_grid(int64_t work) {
+  const int64_t b = (work + kBlock - 1) / kBlock;
+  return static_cast<unsigned>(b < 1 ? 1 : (b < 4096 ? b : 4096));
+}
+
+void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_dev, int64_t n_max,
+                           int32_t* nbr, int64_t ldn, hipStream_t s) {
+  if (n_max <= 0) return;
   ScopedKernelTimer tm("nbr", s);
-  hipLaunchKernelGGL(k_neighbor_table, dim3(blocks_for(n * kTaps)), dim3(kBlock), 0, s, h, vkeys, n,
+  hipLaunchKernelGGL(k_neighbor_table, dim3(stride_grid(n_max * kTaps)), dim3(kBlock), 0, s, h, vkeys, n_dev,
                      nbr, ldn);
 }
 
-void launch_down_table(HashView fine, const uint64_t* coarse_keys, int64_t n_coarse, int32_t* nbr,
-                       int64_t ldn, hipStream_t s) {
-  if (n_coarse <= 0) return;
+void launch_down_table(HashView fine, const uint64_t* coarse_keys, const int32_t* n_dev, int64_t n_max,
+                       int32_t* nbr, int64_t ldn, hipStream_t s) {
+  if (n_max <= 0) return;
   ScopedKernelTimer tm("nbr", s);
-  hipLaunchKernelGGL(k_down_table, dim3(blocks_for(n_coarse * kTaps)), dim3(kBlock), 0, s, fine,
-                     coarse_keys, n_coarse, nbr, ldn);
+  hipLaunchKernelGGL(k_down_table, dim3(stride_grid(n_max * kTaps)), dim3(kBlock), 0, s, fine, coarse_keys,
+                     n_dev, nbr, ldn);
 }
 
 void launch_up_table(HashView coarse, const uint64_t* fine_keys, int64_t n_fine, int32_t* nbr,

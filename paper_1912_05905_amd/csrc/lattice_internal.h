@@ -16,7 +16,6 @@ constexpr int kTaps = 2 * kVerts + 1;   // 1-hop neighbourhood incl. the centre
 constexpr int kCoordBits = 21;
 constexpr int32_t kCoordLimit = 1 << 20;          // |c_i| < 2^20
 constexpr uint64_t kEmptyKey = ~0ull;             // bit 63 set: never a packed key
-constexpr int kSplatChunk = 64;                   // list entries per splat work item
 
 // error bits raised by kernels into the handle's device flag
 enum : uint32_t { kErrHashFull = 1u, kErrKeyRange = 2u, kErrNonFinite = 4u };
@@ -109,26 +108,26 @@ void launch_insert_points(const float* pos, const float* y_in, float y_scale, fl
                           float a2, int64_t m, HashView h, int32_t* counter, int32_t* slot_count,
                           uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
                           float* w_out, float* y_out, uint32_t* err, hipStream_t s);
-int64_t scan_workspace_elems(int64_t n);
-void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, int32_t* offsets, int64_t n,
-                       int32_t* work, hipStream_t s);
+int64_t scan_workspace_elems();
+void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, const int32_t* n_dev,
+                       int32_t* offsets, int32_t* work, hipStream_t s);
 void launch_fill_lists(HashView h, const int32_t* slot, const int32_t* rank, const float* w,
                        const int32_t* offsets, int32_t* idx, int32_t* entries, float* entry_w,
-                       int32_t* chunk_first, int64_t m4, hipStream_t s);
-void launch_neighbor_table(HashView h, const uint64_t* vkeys, int64_t n, int32_t* nbr, int64_t ldn,
-                           hipStream_t s);
-void launch_down_table(HashView fine, const uint64_t* coarse_keys, int64_t n_coarse, int32_t* nbr,
-                       int64_t ldn, hipStream_t s);
+                       int32_t* chunk_first, int chunk, int64_t m4, hipStream_t s);
+void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_dev, int64_t n_max,
+                           int32_t* nbr, int64_t ldn, hipStream_t s);
+void launch_down_table(HashView fine, const uint64_t* coarse_keys, const int32_t* n_dev, int64_t n_max,
+                       int32_t* nbr, int64_t ldn, hipStream_t s);
 void launch_up_table(HashView coarse, const uint64_t* fine_keys, int64_t n_fine, int32_t* nbr,
                      int64_t ldn, hipStream_t s);
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s);
 void launch_transpose_table(const int32_t* tab, int64_t ld, int64_t n, int32_t* out, hipStream_t s);
 // splat_slice.hip
-int64_t splat_partial_floats(int64_t total, int C);
+int64_t splat_partial_floats(int64_t total, int chunk, int C);
 void launch_splat(const int32_t* offsets, const int32_t* entries, const float* entry_w,
-                  const int32_t* chunk_first, int64_t n, int64_t total, const void* feat,
-                  int64_t ld_feat, int C, int bf16, int normalize, void* vals, int64_t ld_vals,
-                  float* wsum, float* partials, hipStream_t s);
+                  const int32_t* chunk_first, int chunk, int64_t n_max, int64_t total,
+                  const void* feat, int64_t ld_feat, int C, int bf16, int normalize, void* vals,
+                  int64_t ld_vals, float* wsum, float* partials, hipStream_t s);
 void launch_slice(const int32_t* idx, const float* w, int64_t m, const void* vals, int64_t ld_vals,
                   int C, int bf16, float* out, hipStream_t s);
 void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const void* vals,

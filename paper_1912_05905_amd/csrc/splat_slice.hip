@@ -52,7 +52,7 @@ template <> struct Chunk<true> {
 
 // Splat (Eq. splat) as a gather over the point lists J_v, which are stored
 // back to back (entries grouped by vertex).  The entry array is cut into
-// chunks of kSplatChunk entries and each chunk goes to one lane group, so
+// chunks of `chunk` entries and each chunk goes to one lane group, so
 // the work is balanced however skewed the vertex degrees are (a LiDAR vertex
 // next to the sensor can hold thousands of points).  A vertex whose list lies
 // inside one chunk is finished there; a vertex cut by chunk boundaries leaves
@@ -98,16 +98,16 @@ __device__ inline void splat_partial(float* part, float* part_w, int64_t c, int 
 template <bool BF16, int LPR, int Q, int B>
 __global__ void __launch_bounds__(kBlock)
 k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
-               const float* __restrict__ entry_w, const int32_t* __restrict__ chunk_first,
+               const float* __restrict__ entry_w, const int32_t* __restrict__ chunk_first, int chunk,
                int64_t n, int64_t total, const void* __restrict__ feat, int64_t ld_feat, int C, int normalize,
                void* __restrict__ vals, int64_t ld_vals, float* __restrict__ wsum,
                float* __restrict__ part_head, float* __restrict__ part_tail, float* __restrict__ part_w) {
   using Ch = Chunk<BF16>;
   const int lane = threadIdx.x & (LPR - 1);
   const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
-  const int64_t s0 = c * kSplatChunk;
+  const int64_t s0 = c * chunk;
   if (s0 >= total) return;
-  const int64_t s1 = min(s0 + static_cast<int64_t>(kSplatChunk), total);
+  const int64_t s1 = min(s0 + static_cast<int64_t>(chunk), total);
   const int nchunk = C / Ch::N;
   int32_t v = chunk_first[c];
   // window of list ends for the next LPR vertices
@@ -181,7 +181,7 @@ k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
 // adds its tail partial and the head partials of the following chunks.
 template <bool BF16, int LPR, int Q>
 __global__ void __launch_bounds__(kBlock)
-k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ chunk_first,
+k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ chunk_first, int chunk,
                int64_t nchunks, int C, int normalize, void* __restrict__ vals, int64_t ld_vals,
                float* __restrict__ wsum, const float* __restrict__ part_head,
                const float* __restrict__ part_tail, const float* __restrict__ part_w) {
@@ -189,12 +189,12 @@ k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
   const int lane = threadIdx.x & (LPR - 1);
   const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
   if (c + 1 >= nchunks) return;
-  const int64_t s0 = c * kSplatChunk, s1 = s0 + kSplatChunk;
+  const int64_t s0 = c * chunk, s1 = s0 + chunk;
   const int32_t v = chunk_first[c + 1];
   const int32_t vb = offsets[v];
   if (!(vb < s1 && vb >= s0)) return;
   const int32_t ve = offsets[v + 1];
-  const int64_t last = (static_cast<int64_t>(ve) - 1) / kSplatChunk;
+  const int64_t last = (static_cast<int64_t>(ve) - 1) / chunk;
   const int nchunk = C / Ch::N;
   float acc[Q][Ch::N];
 #pragma unroll
@@ -209,6 +209,7 @@ k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
     }
   }
   float ws = part_w[2 * c + 1];
+#pragma unroll 4
   for (int64_t c2 = c + 1; c2 <= last; ++c2) {
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
@@ -353,25 +354,25 @@ inline unsigned grid_for(int64_t rows, int lpr) {
 }
 
 template <bool BF16, int LPR, int Q>
-void splat_launch(const int32_t* off, const int32_t* ent, const float* ew, const int32_t* cf, int64_t n, int64_t total,
+void splat_launch(const int32_t* off, const int32_t* ent, const float* ew, const int32_t* cf, int chunk, int64_t n, int64_t total,
                   const void* feat, int64_t ldf, int C, int norm, void* vals, int64_t ldv, float* wsum,
                   float* ph, float* pt, float* pw, hipStream_t s) {
   constexpr int B = (BF16 ? 8 : 16) / Q;
-  const int64_t nchunks = (total + kSplatChunk - 1) / kSplatChunk;
+  const int64_t nchunks = (total + chunk - 1) / chunk;
   const dim3 g(grid_for(nchunks, LPR)), b(kBlock);
-  hipLaunchKernelGGL((k_splat_chunks<BF16, LPR, Q, B>), g, b, 0, s, off, ent, ew, cf, n, total, feat, ldf, C,
+  hipLaunchKernelGGL((k_splat_chunks<BF16, LPR, Q, B>), g, b, 0, s, off, ent, ew, cf, chunk, n, total, feat, ldf, C,
                      norm, vals, ldv, wsum, ph, pt, pw);
   if (nchunks > 1)
-    hipLaunchKernelGGL((k_splat_finish<BF16, LPR, Q>), g, b, 0, s, off, cf, nchunks, C, norm, vals, ldv,
+    hipLaunchKernelGGL((k_splat_finish<BF16, LPR, Q>), g, b, 0, s, off, cf, chunk, nchunks, C, norm, vals, ldv,
                        wsum, ph, pt, pw);
 }
 
 template <bool BF16>
 void splat_dispatch(int lpr, int q, const int32_t* off, const int32_t* ent, const float* ew,
-                    const int32_t* cf, int64_t n, int64_t total, const void* feat, int64_t ldf, int C, int norm,
+                    const int32_t* cf, int chunk, int64_t n, int64_t total, const void* feat, int64_t ldf, int C, int norm,
                     void* vals, int64_t ldv, float* wsum, float* ph, float* pt, float* pw, hipStream_t s) {
 #define SPLAT_CASE(L, QQ) \
-  if (lpr == L && q == QQ) return splat_launch<BF16, L, QQ>(off, ent, ew, cf, n, total, feat, ldf, C, norm, vals, ldv, wsum, ph, pt, pw, s);
+  if (lpr == L && q == QQ) return splat_launch<BF16, L, QQ>(off, ent, ew, cf, chunk, n, total, feat, ldf, C, norm, vals, ldv, wsum, ph, pt, pw, s);
   SPLAT_CASE(1, 1) SPLAT_CASE(2, 1) SPLAT_CASE(4, 1) SPLAT_CASE(8, 1) SPLAT_CASE(16, 1)
   SPLAT_CASE(32, 1) SPLAT_CASE(64, 1) SPLAT_CASE(64, 2) SPLAT_CASE(64, 4)
 #undef SPLAT_CASE
@@ -420,26 +421,26 @@ void deform_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, con
 int splat_max_channels(bool bf16) { return (bf16 ? 8 : 4) * 64 * 4; }
 int deform_max_channels(bool bf16) { return (bf16 ? 8 : 4) * 64 * 2; }
 
-int64_t splat_partial_floats(int64_t total, int C) {
-  const int64_t nchunks = (total + kSplatChunk - 1) / kSplatChunk;
+int64_t splat_partial_floats(int64_t total, int chunk, int C) {
+  const int64_t nchunks = (total + chunk - 1) / chunk;
   return nchunks * (2 * static_cast<int64_t>(C) + 2);
 }
 
 void launch_splat(const int32_t* offsets, const int32_t* entries, const float* entry_w,
-                  const int32_t* chunk_first, int64_t n, int64_t total, const void* feat, int64_t ld_feat, int C,
+                  const int32_t* chunk_first, int chunk, int64_t n, int64_t total, const void* feat, int64_t ld_feat, int C,
                   int bf16, int normalize, void* vals, int64_t ld_vals, float* wsum, float* partials,
                   hipStream_t s) {
   if (total <= 0) return;
   const int chunks = C / (bf16 ? 8 : 4);
   const int lpr = lanes_per_row(C, bf16 != 0);
   const int q = chunks <= lpr ? 1 : (chunks <= 2 * lpr ? 2 : 4);
-  const int64_t nchunks = (total + kSplatChunk - 1) / kSplatChunk;
+  const int64_t nchunks = (total + chunk - 1) / chunk;
   float* ph = partials;
   float* pt = partials + nchunks * C;
   float* pw = partials + 2 * nchunks * C;
   ScopedKernelTimer tm("splat", s);
-  if (bf16) splat_dispatch<true>(lpr, q, offsets, entries, entry_w, chunk_first, n, total, feat, ld_feat, C, normalize, vals, ld_vals, wsum, ph, pt, pw, s);
-  else splat_dispatch<false>(lpr, q, offsets, entries, entry_w, chunk_first, n, total, feat, ld_feat, C, normalize, vals, ld_vals, wsum, ph, pt, pw, s);
+  if (bf16) splat_dispatch<true>(lpr, q, offsets, entries, entry_w, chunk_first, chunk, n, total, feat, ld_feat, C, normalize, vals, ld_vals, wsum, ph, pt, pw, s);
+  else splat_dispatch<false>(lpr, q, offsets, entries, entry_w, chunk_first, chunk, n, total, feat, ld_feat, C, normalize, vals, ld_vals, wsum, ph, pt, pw, s);
 }
 
 void launch_slice(const int32_t* idx, const float* w, int64_t m, const void* vals, int64_t ld_vals,
