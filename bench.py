@@ -24,6 +24,102 @@ sys.path.insert(0, ROOT)
 
 PEAK = {"hbm": 8.0e12, "mfma_f32": 157.3e12, "mfma_bf16": 2.5e15}
 FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "conv", "slice", "deform_slice"]
+# kernel symbol fragments of each family (rocprofv3 kernel names)
+FAMILY_KERNELS = {
+    "fill": ["k_clear_table"], "insert": ["k_insert_points"], "scan": ["k_scan_partials", "k_scan_ranges"],
+    "lists": ["k_fill_lists"], "nbr": ["k_neighbor_table", "k_down_table", "k_up_table"],
+    "splat": ["k_splat_chunks", "k_splat_finish"], "conv": ["k_conv"], "slice": ["k_slice<"],
+    "deform_slice": ["k_deform_slice"],
+}
+CSRC = os.path.join(ROOT, "paper_1912_05905_amd", "csrc")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def kernel_source_hash() -> str:
+    """Hash of the HIP sources: measured traffic is reported only while the
+    kernels are the ones the counters were taken on."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as fh:
+            h.update(name.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def family_of(kernel_name: str):
+    for fam, frags in FAMILY_KERNELS.items():
+        if any(f in kernel_name for f in frags):
+            return fam
+    return None
+
+
+def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mb, steps, warmup, key):
+    """Per-family HBM bytes per step from rocprofv3 --pmc FETCH_SIZE and
+    WRITE_SIZE runs of this benchmark, each counter scaled by what it reads
+    for a device-to-device copy of copy_mb MiB.  Appends the result to
+    profiles/traffic.json under `key`."""
+    import csv
+    import glob
+
+    def counter_rows(d):
+        files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        rows = []
+        for f in files:
+            rows += list(csv.DictReader(open(f)))
+        return rows
+
+    def per_kernel(rows, counter):
+        out = {}
+        for r in rows:
+            if r.get("Counter_Name") != counter:
+                continue
+            out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return out
+
+    def copy_value(d, counter):
+        vals = per_kernel(counter_rows(d), counter)
+        best = max(vals.items(), key=lambda kv: max(kv[1]))
+        return max(best[1])
+
+    nbytes = copy_mb * 2 ** 20
+    scale_f = nbytes / copy_value(copy_fetch_dir, "FETCH_SIZE")
+    scale_w = nbytes / copy_value(copy_write_dir, "WRITE_SIZE")
+    fams = {}
+    for d, counter, scale, field in ((fetch_dir, "FETCH_SIZE", scale_f, "fetch_bytes"),
+                                      (write_dir, "WRITE_SIZE", scale_w, "write_bytes")):
+        for name, vals in per_kernel(counter_rows(d), counter).items():
+            fam = family_of(name)
+            if fam is None:
+                continue
+            ent = fams.setdefault(fam, {"fetch_bytes": 0.0, "write_bytes": 0.0, "dispatches": 0})
+            ent[field] += sum(vals) * scale
+            if counter == "FETCH_SIZE":
+                ent["dispatches"] += len(vals)
+    runs = warmup + 1 + steps     # warmup, instrumented and timed steps of the profiled bench run
+    for ent in fams.values():
+        ent["fetch_bytes_per_step"] = ent.pop("fetch_bytes") / runs
+        ent["write_bytes_per_step"] = ent.pop("write_bytes") / runs
+        ent["dispatches_per_step"] = ent.pop("dispatches") / runs
+    data = json.load(open(TRAFFIC_FILE)) if os.path.exists(TRAFFIC_FILE) else {}
+    data[key] = {"kernel_source_hash": kernel_source_hash(), "fetch_scale": scale_f, "write_scale": scale_w,
+                 "copy_mib": copy_mb, "families": fams}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(data, fh, indent=1, sort_keys=True)
+    print(json.dumps(data[key], indent=1))
+
+
+def measured_traffic(key, family):
+    """HBM bytes per step of a family from profiles/traffic.json, or None when
+    absent or taken on different kernel sources."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    ent = json.load(open(TRAFFIC_FILE)).get(key)
+    if not ent or ent.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    fam = ent["families"].get(family)
+    if not fam:
+        return None
+    return fam["fetch_bytes_per_step"] + fam["write_bytes_per_step"]
 
 
 def conv_flops(wl, levels):
@@ -69,7 +165,24 @@ def main():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--report", default=None, help="write a per-family timing report (JSON) here")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run device-to-device copies of MIB MiB (PMC scale calibration)")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="summarise rocprofv3 --pmc runs into profiles/traffic.json")
+    ap.add_argument("--copy-mib", type=int, default=256)
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, args.copy_mib, args.steps, args.warmup, f"config{args.config}")
+        return
+    if args.calibrate_copy:
+        import torch
+        src = torch.ones(args.calibrate_copy * 2 ** 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"copied {args.calibrate_copy} MiB x3", flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
@@ -133,12 +246,18 @@ def main():
         achieved = flops / (dom_ms_step * 1e-3)
         roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
                 "frac": achieved / peak, "traffic": None}
+        t = measured_traffic(f"config{wl.cfg}", dominant)
+        if t is not None:
+            roof["traffic"] = t / max(launches / args.steps, 1)
     else:
         b = bytes_by_fam.get(dominant)
         achieved = (b / (dom_ms_step * 1e-3)) if b else None
         roof = {"bound": "hbm", "achieved": None if achieved is None else achieved / 1e9,
                 "peak": PEAK["hbm"] / 1e9, "unit": "GB/s",
                 "frac": None if achieved is None else achieved / PEAK["hbm"], "traffic": None}
+        t = measured_traffic(f"config{wl.cfg}", dominant)
+        if t is not None:
+            roof["traffic"] = t / max(launches / args.steps, 1)
     roof["kernel"] = dominant
     roof["launches_per_step"] = launches / args.steps
     roof["ms_per_step"] = dom_ms_step

@@ -16,6 +16,20 @@ __device__ inline uint16_t f32_to_bf16(float f) {
   return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
+// Row / chunk index of a lane group with XCD-contiguous workgroup order:
+// workgroup b runs on XCD b % 8, so consecutive work items (which share
+// feature or vertex rows) are given to workgroups of the same XCD and meet in
+// its L2.  Launches use xcd_grid() workgroups.
+template <int LPR>
+__device__ inline int64_t xcd_item(unsigned nblocks_logical) {
+  const unsigned b = blockIdx.x;
+  const unsigned per = (nblocks_logical + 7) / 8;
+  const int64_t logical = static_cast<int64_t>(b % 8) * per + b / 8;
+  return (logical * kBlock + threadIdx.x) / LPR;
+}
+
+inline unsigned xcd_grid(unsigned nblocks_logical) { return ((nblocks_logical + 7) / 8) * 8; }
+
 // A 16-byte chunk of a row as 8 floats (bf16) or 4 floats (fp32).
 template <bool BF16> struct Chunk;
 template <> struct Chunk<false> {
@@ -101,10 +115,11 @@ k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
                const float* __restrict__ entry_w, const int32_t* __restrict__ chunk_first, int chunk,
                int64_t n, int64_t total, const void* __restrict__ feat, int64_t ld_feat, int C, int normalize,
                void* __restrict__ vals, int64_t ld_vals, float* __restrict__ wsum,
-               float* __restrict__ part_head, float* __restrict__ part_tail, float* __restrict__ part_w) {
+               float* __restrict__ part_head, float* __restrict__ part_tail, float* __restrict__ part_w,
+               unsigned nblk) {
   using Ch = Chunk<BF16>;
   const int lane = threadIdx.x & (LPR - 1);
-  const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
+  const int64_t c = xcd_item<LPR>(nblk);
   const int64_t s0 = c * chunk;
   if (s0 >= total) return;
   const int64_t s1 = min(s0 + static_cast<int64_t>(chunk), total);
@@ -209,7 +224,7 @@ k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
     }
   }
   float ws = part_w[2 * c + 1];
-#pragma unroll 4
+#pragma unroll 16
   for (int64_t c2 = c + 1; c2 <= last; ++c2) {
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
@@ -229,10 +244,10 @@ k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
 template <bool BF16, int LPR>
 __global__ void __launch_bounds__(kBlock)
 k_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64_t m,
-        const void* __restrict__ vals, int64_t ld_vals, int C, float* __restrict__ out) {
+        const void* __restrict__ vals, int64_t ld_vals, int C, float* __restrict__ out, unsigned nblk) {
   using Ch = Chunk<BF16>;
   const int lane = threadIdx.x & (LPR - 1);
-  const int64_t p = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
+  const int64_t p = xcd_item<LPR>(nblk);
   if (p >= m) return;
   const int4 iv = idx[p];
   const float4 wv = w[p];
@@ -266,10 +281,10 @@ template <bool BF16, int LPR, int CPL>
 __global__ void __launch_bounds__(kBlock)
 k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64_t m,
                const void* __restrict__ vals, int64_t ld_vals, int C, const float* __restrict__ wvec,
-               float beta, float* __restrict__ out, float4* __restrict__ delta) {
+               float beta, float* __restrict__ out, float4* __restrict__ delta, unsigned nblk) {
   using Ch = Chunk<BF16>;
   const int lane = threadIdx.x & (LPR - 1);
-  const int64_t p = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
+  const int64_t p = xcd_item<LPR>(nblk);
   const bool live = p < m;
   const int nchunk = C / Ch::N;
   int4 iv = make_int4(-1, -1, -1, -1);
@@ -359,9 +374,10 @@ void splat_launch(const int32_t* off, const int32_t* ent, const float* ew, const
                   float* ph, float* pt, float* pw, hipStream_t s) {
   constexpr int B = (BF16 ? 8 : 16) / Q;
   const int64_t nchunks = (total + chunk - 1) / chunk;
-  const dim3 g(grid_for(nchunks, LPR)), b(kBlock);
-  hipLaunchKernelGGL((k_splat_chunks<BF16, LPR, Q, B>), g, b, 0, s, off, ent, ew, cf, chunk, n, total, feat, ldf, C,
-                     norm, vals, ldv, wsum, ph, pt, pw);
+  const unsigned nblk = grid_for(nchunks, LPR);
+  const dim3 g(nblk), b(kBlock);
+  hipLaunchKernelGGL((k_splat_chunks<BF16, LPR, Q, B>), dim3(xcd_grid(nblk)), b, 0, s, off, ent, ew, cf, chunk, n,
+                     total, feat, ldf, C, norm, vals, ldv, wsum, ph, pt, pw, nblk);
   if (nchunks > 1)
     hipLaunchKernelGGL((k_splat_finish<BF16, LPR, Q>), g, b, 0, s, off, cf, chunk, nchunks, C, norm, vals, ldv,
                        wsum, ph, pt, pw);
@@ -381,17 +397,18 @@ void splat_dispatch(int lpr, int q, const int32_t* off, const int32_t* ent, cons
 template <bool BF16>
 void slice_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, const void* vals,
                     int64_t ldv, int C, float* out, hipStream_t s) {
-  const dim3 g(grid_for(m, lpr)), b(kBlock);
+  const unsigned nblk = grid_for(m, lpr);
+  const dim3 g(xcd_grid(nblk)), b(kBlock);
   const int4* i4 = reinterpret_cast<const int4*>(idx);
   const float4* w4 = reinterpret_cast<const float4*>(w);
   switch (lpr) {
-    case 1: hipLaunchKernelGGL((k_slice<BF16, 1>), g, b, 0, s, i4, w4, m, vals, ldv, C, out); break;
-    case 2: hipLaunchKernelGGL((k_slice<BF16, 2>), g, b, 0, s, i4, w4, m, vals, ldv, C, out); break;
-    case 4: hipLaunchKernelGGL((k_slice<BF16, 4>), g, b, 0, s, i4, w4, m, vals, ldv, C, out); break;
-    case 8: hipLaunchKernelGGL((k_slice<BF16, 8>), g, b, 0, s, i4, w4, m, vals, ldv, C, out); break;
-    case 16: hipLaunchKernelGGL((k_slice<BF16, 16>), g, b, 0, s, i4, w4, m, vals, ldv, C, out); break;
-    case 32: hipLaunchKernelGGL((k_slice<BF16, 32>), g, b, 0, s, i4, w4, m, vals, ldv, C, out); break;
-    default: hipLaunchKernelGGL((k_slice<BF16, 64>), g, b, 0, s, i4, w4, m, vals, ldv, C, out); break;
+    case 1: hipLaunchKernelGGL((k_slice<BF16, 1>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 2: hipLaunchKernelGGL((k_slice<BF16, 2>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 4: hipLaunchKernelGGL((k_slice<BF16, 4>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 8: hipLaunchKernelGGL((k_slice<BF16, 8>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 16: hipLaunchKernelGGL((k_slice<BF16, 16>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 32: hipLaunchKernelGGL((k_slice<BF16, 32>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    default: hipLaunchKernelGGL((k_slice<BF16, 64>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
   }
 }
 
@@ -399,18 +416,19 @@ template <bool BF16, int CPL>
 void deform_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, const void* vals,
                      int64_t ldv, int C, const float* wv, float beta, float* out, float* delta,
                      hipStream_t s) {
-  const dim3 g(grid_for(m, lpr)), b(kBlock);
+  const unsigned nblk = grid_for(m, lpr);
+  const dim3 g(xcd_grid(nblk)), b(kBlock);
   const int4* i4 = reinterpret_cast<const int4*>(idx);
   const float4* w4 = reinterpret_cast<const float4*>(w);
   float4* d4 = reinterpret_cast<float4*>(delta);
   switch (lpr) {
-    case 1: hipLaunchKernelGGL((k_deform_slice<BF16, 1, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4); break;
-    case 2: hipLaunchKernelGGL((k_deform_slice<BF16, 2, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4); break;
-    case 4: hipLaunchKernelGGL((k_deform_slice<BF16, 4, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4); break;
-    case 8: hipLaunchKernelGGL((k_deform_slice<BF16, 8, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4); break;
-    case 16: hipLaunchKernelGGL((k_deform_slice<BF16, 16, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4); break;
-    case 32: hipLaunchKernelGGL((k_deform_slice<BF16, 32, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4); break;
-    default: hipLaunchKernelGGL((k_deform_slice<BF16, 64, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4); break;
+    case 1: hipLaunchKernelGGL((k_deform_slice<BF16, 1, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 2: hipLaunchKernelGGL((k_deform_slice<BF16, 2, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 4: hipLaunchKernelGGL((k_deform_slice<BF16, 4, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 8: hipLaunchKernelGGL((k_deform_slice<BF16, 8, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 16: hipLaunchKernelGGL((k_deform_slice<BF16, 16, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 32: hipLaunchKernelGGL((k_deform_slice<BF16, 32, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    default: hipLaunchKernelGGL((k_deform_slice<BF16, 64, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
   }
 }
 
