@@ -101,7 +101,10 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mb,
         ent["write_bytes_per_step"] = ent.pop("write_bytes") / runs
         ent["dispatches_per_step"] = ent.pop("dispatches") / runs
     data = json.load(open(TRAFFIC_FILE)) if os.path.exists(TRAFFIC_FILE) else {}
-    data[key] = {"kernel_source_hash": kernel_source_hash(), "fetch_scale": scale_f, "write_scale": scale_w,
+    stamp = os.path.join(fetch_dir, "source_hash.txt")
+    if not os.path.exists(stamp):
+        raise SystemExit(f"{stamp} missing: write it with bench.py --source-hash when the counters are taken")
+    data[key] = {"kernel_source_hash": open(stamp).read().strip(), "fetch_scale": scale_f, "write_scale": scale_w,
                  "copy_mib": copy_mb, "families": fams}
     with open(TRAFFIC_FILE, "w") as fh:
         json.dump(data, fh, indent=1, sort_keys=True)
@@ -170,7 +173,11 @@ def main():
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="summarise rocprofv3 --pmc runs into profiles/traffic.json")
     ap.add_argument("--copy-mib", type=int, default=256)
+    ap.add_argument("--source-hash", action="store_true", help="print the hash of the HIP sources and exit")
     args = ap.parse_args()
+    if args.source_hash:
+        print(kernel_source_hash())
+        return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.copy_mib, args.steps, args.warmup, f"config{args.config}")
         return

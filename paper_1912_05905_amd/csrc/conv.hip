@@ -247,8 +247,9 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
 
   // global -> register copies of one stage
   using V = uint4;
-  V ra[P::A_PER_T], rb[P::B_PER_T];
-  auto fetch = [&](int st) {
+  V ra[2][P::A_PER_T], rb[2][P::B_PER_T];
+  auto fetch = [&](auto set_c, int st) {
+    constexpr int set = decltype(set_c)::value;
     const int t = st / kc_steps;
     const int kc = (st - t * kc_steps) * P::KC;
 #pragma unroll
@@ -257,7 +258,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
       const int r = q / P::CPR, cc = q % P::CPR;
       const int ch = kc + cc * P::EPC;
       const int32_t nb = nbt[t * BM + r];
-      ra[j] = (nb >= 0 && ch < Cin)
+      ra[set][j] = (nb >= 0 && ch < Cin)
                   ? *reinterpret_cast<const V*>(static_cast<const E*>(in) + static_cast<int64_t>(nb) * ld_in + ch)
                   : make_uint4(0u, 0u, 0u, 0u);
     }
@@ -267,27 +268,28 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
       const int r = q / P::CPR, cc = q % P::CPR;
       const int ch = kc + cc * P::EPC;
       const int col = col0 + r;
-      rb[j] = (q < BN * P::CPR && col < Cout && ch < Cin)
+      rb[set][j] = (q < BN * P::CPR && col < Cout && ch < Cin)
                   ? *reinterpret_cast<const V*>(static_cast<const E*>(W) +
                                                 (static_cast<int64_t>(t) * Cout + col) * Cin + ch)
                   : make_uint4(0u, 0u, 0u, 0u);
     }
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](auto set_c, int buf) {
+    constexpr int set = decltype(set_c)::value;
     E* a = As + buf * (BM * P::LDR);
     E* bb = Bs + buf * (BN * P::LDR);
 #pragma unroll
     for (int j = 0; j < P::A_PER_T; ++j) {
       const int q = tid + j * kBlock;
       const int r = q / P::CPR, cc = q % P::CPR;
-      *reinterpret_cast<V*>(a + r * P::LDR + cc * P::EPC) = ra[j];
+      *reinterpret_cast<V*>(a + r * P::LDR + cc * P::EPC) = ra[set][j];
     }
 #pragma unroll
     for (int j = 0; j < P::B_PER_T; ++j) {
       const int q = tid + j * kBlock;
       if (q < BN * P::CPR) {
         const int r = q / P::CPR, cc = q % P::CPR;
-        *reinterpret_cast<V*>(bb + r * P::LDR + cc * P::EPC) = rb[j];
+        *reinterpret_cast<V*>(bb + r * P::LDR + cc * P::EPC) = rb[set][j];
       }
     }
   };
@@ -298,14 +300,20 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
 #pragma unroll
     for (int c = 0; c < P::RN; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  fetch(0);
-  stash(0);
+  // Two stages of global loads in flight: while stage st is multiplied,
+  // stage st+1 waits in registers set (st+1)&1 (loaded one iteration ago) and
+  // stage st+2 is being loaded into the other set.
+  fetch(std::integral_constant<int, 0>{}, 0);
+  if (stages > 1) fetch(std::integral_constant<int, 1>{}, 1);
+  stash(std::integral_constant<int, 0>{}, 0);
   __syncthreads();
-  for (int st = 0; st < stages; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < stages) fetch(st + 1);
-    const E* a = As + buf * (BM * P::LDR) + (wm * P::RM * 16 + li) * P::LDR + lg * P::EPL;
-    const E* bb = Bs + buf * (BN * P::LDR) + (wn * P::RN * 16 + li) * P::LDR + lg * P::EPL;
+  // one pipeline step; SET = st & 1 is a compile-time constant so that the
+  // register sets stay in registers
+  auto step = [&](auto set_c, int st) {
+    constexpr int SET = decltype(set_c)::value;
+    constexpr int OTHER = SET ^ 1;
+    const E* a = As + SET * (BM * P::LDR) + (wm * P::RM * 16 + li) * P::LDR + lg * P::EPL;
+    const E* bb = Bs + SET * (BN * P::LDR) + (wn * P::RN * 16 + li) * P::LDR + lg * P::EPL;
 #pragma unroll
     for (int k = 0; k < P::KC; k += P::KS) {
       Frag<BF16> fa[P::RM], fb[P::RN];
@@ -329,8 +337,13 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
               acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i].v[e], fb[j].v[e], acc[i][j], 0, 0, 0);
       }
     }
-    if (st + 1 < stages) stash(buf ^ 1);
+    if (st + 1 < stages) stash(std::integral_constant<int, OTHER>{}, OTHER);
+    if (st + 2 < stages) fetch(std::integral_constant<int, SET>{}, st + 2);
     __syncthreads();
+  };
+  for (int st = 0; st < stages; st += 2) {
+    step(std::integral_constant<int, 0>{}, st);
+    if (st + 1 < stages) step(std::integral_constant<int, 1>{}, st + 1);
   }
 
 #pragma unroll
@@ -376,29 +389,26 @@ int64_t blocks_of(int64_t n_out, int Cout, int rows, int cols) {
   return ((n_out + rows - 1) / rows) * ((Cout + cols - 1) / cols);
 }
 
-// Tile choice: the largest tile that still gives every CU a couple of
-// workgroups; small lattice levels fall back to narrower tiles.
+// Tile choice, from a sweep of every tile shape over the lattices of the
+// LiDAR scan (fp32) and the 1M-point room (bf16) on MI355X: small tiles with
+// deep pipelines win because the gathered A operand, not the matrix cores,
+// sets the pace; wide-output fp32 layers on large levels prefer 32 x 64.
 template <bool BF16>
 void conv_dispatch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                    int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
                    int64_t ld_out, hipStream_t s) {
-  constexpr int64_t kWant = 512;
   if (Cout <= 16)
     return conv_launch<BF16, 1, 1, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
   if constexpr (BF16) {
-    if (Cout > 64 && blocks_of(n_out, Cout, 128, 128) >= kWant)
-      return conv_lds_launch<true, 128, 128, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-    if (Cout > 32 && blocks_of(n_out, Cout, 128, 64) >= kWant)
-      return conv_lds_launch<true, 128, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-    if (Cout > 32)
+    if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= 256)
       return conv_lds_launch<true, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-    return conv_lds_launch<true, 64, 32, 4, 1, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+    return conv_lds_launch<true, 32, 32, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
   } else {
-    if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= kWant)
+    if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= 2048)
       return conv_lds_launch<false, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-    if (Cout > 32)
+    if (Cout > 64 && blocks_of(n_out, Cout, 32, 64) >= 1024)
       return conv_lds_launch<false, 32, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-    return conv_lds_launch<false, 32, 32, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+    return conv_lds_launch<false, 32, 32, 2, 2, 256>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
   }
 }
 

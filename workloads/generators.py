@@ -116,8 +116,9 @@ def room(seed: int, m: int, size=(8.0, 8.0, 3.0), nboxes: int = 20,
     """An indoor room: floor, four walls and `nboxes` boxes standing on the
     floor, sampled area-weighted, plus isotropic Gaussian noise (metres).
 
-    Points come out surface by surface (floor, walls, boxes), in random order
-    within each surface, the way a scan assembled from fragments does."""
+    Points come out in the order a volumetric reconstruction emits its mesh
+    vertices: block by block (0.5 m blocks in Morton order), in random order
+    inside a block."""
     st = Stream(seed, "room")
     sx, sy, sz = size
     surfaces = [
@@ -139,7 +140,19 @@ def room(seed: int, m: int, size=(8.0, 8.0, 3.0), nboxes: int = 20,
     parts = [_sample_faces(st, int(k), s) for s, k in zip(surfaces, counts) if k > 0]
     p = np.concatenate(parts, axis=0)
     p = p + noise * st.normal(3 * m).reshape(m, 3)
+    p = p[st.permutation(m)]
+    p = p[np.argsort(_morton_blocks(p, 0.5), kind="stable")]
     return p.astype(np.float32)
+
+
+def _morton_blocks(p: np.ndarray, block: float) -> np.ndarray:
+    """Morton (Z-order) code of the block each point falls in."""
+    q = np.floor((p - p.min(axis=0)) / block).astype(np.uint64)
+    code = np.zeros(p.shape[0], dtype=np.uint64)
+    for bit in range(16):
+        for axis in range(3):
+            code |= ((q[:, axis] >> np.uint64(bit)) & np.uint64(1)) << np.uint64(3 * bit + axis)
+    return code
 
 
 def _ray_box(orig, dirs, lo, hi):
