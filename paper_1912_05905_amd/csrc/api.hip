@@ -225,8 +225,7 @@ struct lattice_s {
   float* y = nullptr;            // m x 4 elevated positions
   int32_t* idx = nullptr;        // m x 4 simplex vertex indices
   float* w = nullptr;            // m x 4 barycentric weights
-  uint64_t* tkeys = nullptr;     // hash keys (cap)
-  int32_t* tvals = nullptr;      // hash values (cap)
+  HashEntry* table = nullptr;    // hash table (cap entries of key + vertex number)
   uint64_t* vkeys = nullptr;     // n packed vertex keys
   int32_t* offsets = nullptr;    // n+1 list offsets of J_v
   int32_t* entries = nullptr;    // 4m entries p*4+k grouped by vertex
@@ -239,7 +238,7 @@ struct lattice_s {
   bool up_built = false;
   int64_t retry_cap = 0;          // coarse levels: table size of a rebuild after overflow
 
-  HashView hash() const { return HashView{tkeys, tvals, static_cast<uint64_t>(cap - 1)}; }
+  HashView hash() const { return HashView{table, static_cast<uint64_t>(cap - 1)}; }
 
   int alloc(size_t bytes, hipStream_t s, void** out) {
     const int st = Pool::get().alloc(bytes, s, out);
@@ -341,8 +340,8 @@ struct Scratch {
 // clear, insert, readback of the vertex count and error bits (asynchronous,
 // with an event), then the scan, the vertex lists and the neighbour table,
 // which take the vertex count from device memory.  Nothing waits here.
-int enqueue_build(lattice_s* L, const float* pos, const float a[3], const lattice_s* parent, int64_t cap,
-                  hipStream_t s) {
+int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_scale, const float a[3],
+                  const lattice_s* parent, int64_t cap, hipStream_t s) {
   const int64_t m = L->m;
   const int64_t refs = 4 * m;
   const int64_t nmax = std::min(cap, refs);
@@ -360,8 +359,7 @@ int enqueue_build(lattice_s* L, const float* pos, const float a[3], const lattic
   ALLOC(y, float, 4 * m);
   ALLOC(idx, int32_t, refs);
   ALLOC(w, float, refs);
-  ALLOC(tkeys, uint64_t, cap);
-  ALLOC(tvals, int32_t, cap);
+  ALLOC(table, HashEntry, cap);
   ALLOC(vkeys, uint64_t, nmax);
   ALLOC(dc, DeviceCounters, 1);
   ALLOC(offsets, int32_t, nmax + 1);
@@ -380,8 +378,8 @@ int enqueue_build(lattice_s* L, const float* pos, const float a[3], const lattic
   if (!L->counts_ready && !(L->counts_ready = HostSlots::get().take_event()))
     return fail(LAT_EDEVICE, "event creation failed");
 
-  launch_clear_table(L->tkeys, slot_count.as<int32_t>(), cap, reinterpret_cast<uint64_t*>(L->dc), s);
-  launch_insert_points(pos, parent ? parent->y : nullptr, 0.5f, a[0], a[1], a[2], m, L->hash(),
+  launch_clear_table(L->table, slot_count.as<int32_t>(), cap, reinterpret_cast<uint64_t*>(L->dc), s);
+  launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], m, L->hash(),
                        &L->dc->counter, slot_count.as<int32_t>(), L->vkeys, vslot.as<int32_t>(),
                        slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->y, &L->dc->err, s);
   HIP_TRY(hipMemcpyAsync(L->host_dc, L->dc, sizeof(DeviceCounters), hipMemcpyDeviceToHost, s));
@@ -400,14 +398,17 @@ int enqueue_build(lattice_s* L, const float* pos, const float a[3], const lattic
   return check_launch("lattice build");
 }
 
-// Table size for a build: the caller's hint, or 2x the worst case (d+1
-// vertices per point); coarse levels start from 2x the parent's vertex count
-// when it is known and are rebuilt at the worst case should that overflow.
+// Table size for a build: the caller's hint, else 2 slots per point for
+// the first level (surface clouds have at most about one vertex per point)
+// and 2 per parent vertex for coarse levels.  A table that overflows is
+// rebuilt at the worst-case size (2 slots per vertex reference) from the
+// handle's own elevated positions, so no caller buffer is needed again.
 int64_t initial_capacity(const lattice_s* L, const lattice_s* parent, int64_t capacity_hint) {
   const int64_t refs = 4 * L->m;
   const int64_t full = next_pow2(std::max<int64_t>(1024, 2 * refs));
   if (capacity_hint > 0) return next_pow2(std::max<int64_t>(1024, 2 * std::min(capacity_hint, refs)));
   if (parent && parent->counts_known) return std::min(full, next_pow2(std::max<int64_t>(1024, 2 * parent->n)));
+  if (!parent) return std::min(full, next_pow2(std::max<int64_t>(1024, 2 * L->m)));
   return full;
 }
 
@@ -418,13 +419,24 @@ int ensure_counts(lattice_s* L) {
   L->counts_known = true;
   L->n = L->host_dc->counter;
   const int dev_status = status_from_err_bits(L->host_dc->err);
-  if (dev_status == LAT_EHASHFULL && L->parent && L->retry_cap > L->cap) {
-    // coarse level with a table sized from the parent: rebuild at full size
+  if (dev_status == LAT_EHASHFULL && L->retry_cap > L->cap) {
+    // table sized from an estimate overflowed: rebuild at the worst case
     const int64_t cap = L->retry_cap;
     L->retry_cap = 0;
+    DevBuf old_y{};
+    if (!L->parent) {
+      for (size_t i = 0; i < L->owned.size(); ++i)
+        if (L->owned[i].p == L->y) {
+          old_y = L->owned[i];
+          L->owned.erase(L->owned.begin() + static_cast<long>(i));
+          break;
+        }
+    }
     L->free_all();
     const float a[3] = {0.f, 0.f, 0.f};
-    int st = enqueue_build(L, nullptr, a, L->parent, cap, L->stream);
+    const float* src = L->parent ? L->parent->y : static_cast<const float*>(old_y.p);
+    int st = enqueue_build(L, nullptr, src, L->parent ? 0.5f : 1.0f, a, L->parent, cap, L->stream);
+    Pool::get().release(old_y.p, old_y.bytes, L->stream);
     if (st != LAT_OK) { L->status = st; return st; }
     return ensure_counts(L);
   }
@@ -444,8 +456,8 @@ int build_lattice(lattice_s* L, const float* pos, const float a[3], const lattic
   if (m == 0) return LAT_OK;
   if (4 * m > INT32_MAX) return fail(LAT_EUNSUPPORTED, "more than 2^29 points");
   const int64_t cap = initial_capacity(L, parent, capacity_hint);
-  L->retry_cap = (parent && capacity_hint == 0) ? next_pow2(std::max<int64_t>(1024, 8 * m)) : 0;
-  return enqueue_build(L, pos, a, parent, cap, s);
+  L->retry_cap = capacity_hint == 0 ? next_pow2(std::max<int64_t>(1024, 8 * m)) : 0;
+  return enqueue_build(L, pos, parent ? parent->y : nullptr, 0.5f, a, parent, cap, s);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }

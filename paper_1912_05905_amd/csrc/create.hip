@@ -23,12 +23,12 @@ constexpr int kLdsSlots = 2048;             // LDS table: 2x the references of a
 constexpr int kLdsPerThread = kLdsSlots / kBlock;
 
 __global__ void __launch_bounds__(kBlock)
-k_clear_table(uint64_t* __restrict__ keys, int32_t* __restrict__ counts, int64_t cap,
+k_clear_table(HashEntry* __restrict__ entries, int32_t* __restrict__ counts, int64_t cap,
               uint64_t* __restrict__ dev_counters) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
   for (int64_t e = i; e < cap; e += stride) {
-    keys[e] = kEmptyKey;
+    *reinterpret_cast<uint4*>(&entries[e]) = make_uint4(0xffffffffu, 0xffffffffu, 0u, 0u);
     counts[e] = 0;
   }
   if (i == 0) *dev_counters = 0ull;
@@ -40,10 +40,10 @@ __device__ inline int32_t global_insert(const HashView& h, uint64_t key, bool* c
   *created = false;
   uint64_t slot = hash_key(key) & h.mask;
   for (uint64_t probe = 0; probe <= h.mask; ++probe) {
-    const uint64_t cur = h.keys[slot];
+    const uint64_t cur = h.e[slot].key;
     if (cur == key) return static_cast<int32_t>(slot);
     if (cur == kEmptyKey) {
-      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(&h.keys[slot]),
+      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(&h.e[slot].key),
                                       static_cast<unsigned long long>(kEmptyKey),
                                       static_cast<unsigned long long>(key));
       if (prev == kEmptyKey) {
@@ -275,7 +275,7 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
     if (!(created_mask & (1u << j))) continue;
     const int sl = ulist[u];
     const int32_t gs = lslot[sl];
-    h.vals[gs] = id;
+    h.e[gs].val = id;
     vkeys[id] = lkey[sl];
     vslot[id] = gs;
     ++id;
@@ -367,7 +367,7 @@ k_fill_lists(HashView h, const int32_t* __restrict__ slot, const int32_t* __rest
     idx[e] = -1;
     return;
   }
-  const int32_t v = h.vals[s];
+  const int32_t v = h.e[s].val;
   idx[e] = v;
   const int32_t at = offsets[v] + rank[e];
   entries[at] = static_cast<int32_t>(e);
@@ -464,7 +464,7 @@ inline unsigned blocks_for(int64_t n) { return static_cast<unsigned>((n + kBlock
 
 }  // namespace
 
-void launch_clear_table(uint64_t* keys, int32_t* counts, int64_t cap, uint64_t* dev_counters,
+void launch_clear_table(HashEntry* keys, int32_t* counts, int64_t cap, uint64_t* dev_counters,
                         hipStream_t s) {
   const int64_t want = (cap + kBlock * 4 - 1) / (kBlock * 4);
   const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : (want < 8192 ? want : 8192));

@@ -52,11 +52,17 @@ __host__ __device__ inline uint64_t hash_key(uint64_t k) {
   return k;
 }
 
-// Open-addressing table with linear probing.  keys[slot] is kEmptyKey or a
-// packed key; vals[slot] the vertex index of that key.
+// Open-addressing table with linear probing.  A slot is 16 bytes: the
+// packed key (kEmptyKey when free) and the vertex number, so a probe reads
+// one aligned 16-byte entry.
+struct alignas(16) HashEntry {
+  uint64_t key;
+  int32_t val;
+  int32_t pad;
+};
+
 struct HashView {
-  uint64_t* keys;
-  int32_t* vals;
+  HashEntry* e;
   uint64_t mask;      // capacity - 1 (capacity a power of two)
 };
 
@@ -64,8 +70,9 @@ struct HashView {
 __device__ inline int32_t hash_find(const HashView& h, uint64_t key) {
   uint64_t slot = hash_key(key) & h.mask;
   for (uint64_t probe = 0; probe <= h.mask; ++probe) {
-    const uint64_t k = h.keys[slot];
-    if (k == key) return h.vals[slot];
+    const uint4 ent = *reinterpret_cast<const uint4*>(&h.e[slot]);
+    const uint64_t k = (static_cast<uint64_t>(ent.y) << 32) | ent.x;
+    if (k == key) return static_cast<int32_t>(ent.z);
     if (k == kEmptyKey) return -1;
     slot = (slot + 1) & h.mask;
   }
@@ -102,7 +109,7 @@ struct ScopedKernelTimer {
 
 // Launchers (each .hip file implements its own kernels' launchers).
 // create.hip
-void launch_clear_table(uint64_t* keys, int32_t* counts, int64_t cap, uint64_t* dev_counters,
+void launch_clear_table(HashEntry* entries, int32_t* counts, int64_t cap, uint64_t* dev_counters,
                         hipStream_t s);
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
                           float a2, int64_t m, HashView h, int32_t* counter, int32_t* slot_count,
