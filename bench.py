@@ -126,12 +126,17 @@ def measured_traffic(key, family):
 
 
 def conv_flops(wl, levels):
-    """Nominal flops of all convolutions of one step (9 taps each)."""
+    """Nominal flops of all convolutions of one step: 2 * 9 * Cin * Cout per
+    output vertex for the same-level and the strided (Downsample)
+    convolution, and per coarse (input) vertex for Upsample, the transposed
+    convolution, whose natural form multiplies every coarse vertex by the
+    nine tap matrices."""
     total = 0
     for op in wl.ops:
-        if op["op"] in ("conv", "conv_down", "refine"):
-            n_out = levels[op["level"]].n
-            total += 2 * n_out * 9 * op["src"][2] * op["dst"][2]
+        if op["op"] in ("conv", "conv_down"):
+            total += 2 * levels[op["level"]].n * 9 * op["src"][2] * op["dst"][2]
+        elif op["op"] == "refine":
+            total += 2 * levels[op["level"] + 1].n * 9 * op["src"][2] * op["dst"][2]
     return total
 
 

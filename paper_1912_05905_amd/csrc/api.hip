@@ -235,6 +235,7 @@ struct lattice_s {
   int32_t* nbr = nullptr;        // 9 x nmax same-level table (tap-major, ld nmax)
   int32_t* down = nullptr;       // 9 x nmax table into the parent (coarse levels, ld nmax)
   int32_t* up = nullptr;         // 9 x n_parent table from the parent into this level
+  int32_t* up_rows = nullptr;    // parent vertices, grouped by the tap mask of their up row
   bool up_built = false;
   int64_t retry_cap = 0;          // coarse levels: table size of a rebuild after overflow
 
@@ -367,6 +368,9 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   ALLOC(entry_w, float, refs);
   ALLOC(chunk_first, int32_t, nchunks);
   ALLOC(nbr, int32_t, kTaps * nmax);
+  if (parent) {
+    ALLOC(down, int32_t, kTaps * nmax);
+  }
 #undef ALLOC
   Scratch slot_count, vslot, slot, rank, work;
   if ((st = slot_count.get(sizeof(int32_t) * cap, s)) != LAT_OK) return st;
@@ -390,11 +394,7 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   launch_fill_lists(L->hash(), slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->offsets, L->idx,
                     L->entries, L->entry_w, L->chunk_first, L->chunk, refs, s);
   launch_neighbor_table(L->hash(), L->vkeys, n_dev, nmax, L->nbr, nmax, s);
-  if (parent) {
-    if ((st = L->alloc(sizeof(int32_t) * kTaps * nmax, s, &p)) != LAT_OK) return st;
-    L->down = static_cast<int32_t*>(p);
-    launch_down_table(parent->hash(), L->vkeys, n_dev, nmax, L->down, nmax, s);
-  }
+  if (parent) launch_down_table(parent->hash(), L->vkeys, n_dev, nmax, L->down, nmax, s);
   return check_launch("lattice build");
 }
 
@@ -499,7 +499,7 @@ bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
 
 int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                 int Cin, const void* W, const float* bias, int Cout, lat_dtype dt, int flags,
-                void* out, int64_t ld_out, hipStream_t s) {
+                void* out, int64_t ld_out, const int32_t* rows, hipStream_t s) {
   int st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_in == 0) ld_in = Cin;
@@ -516,7 +516,7 @@ int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, 
     return fail(LAT_EINVAL, "in and out overlap");
   if (n_out == 0) return LAT_OK;
   launch_conv(table, ldn, n_out, in, ld_in, Cin, W, bias, Cout, dt == LAT_BF16, flags & LAT_RELU, out,
-              ld_out, s);
+              ld_out, rows, s);
   return check_launch("conv");
 }
 
@@ -696,7 +696,7 @@ int lattice_conv(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in
   else if (dst->parent == src) table = dst->down;
   else return fail(LAT_ELEVEL, "dst must be src or lattice_coarsen(src)");
   return conv_common(table, dst->nmax, dst->n, src->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt, flags,
-                     out_dev, ld_out, stream);
+                     out_dev, ld_out, nullptr, stream);
 }
 
 int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t ld_in, int Cin,
@@ -710,13 +710,15 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
     void* p;
     if ((st = coarse->alloc(sizeof(int32_t) * kTaps * fine->n, coarse->stream, &p)) != LAT_OK) return st;
     coarse->up = static_cast<int32_t*>(p);
-    launch_up_table(coarse->hash(), fine->vkeys, fine->n, coarse->up, fine->n, coarse->stream);
+    if ((st = coarse->alloc(sizeof(int32_t) * fine->n, coarse->stream, &p)) != LAT_OK) return st;
+    coarse->up_rows = static_cast<int32_t*>(p);
+    launch_up_table(coarse->hash(), fine->vkeys, fine->n, coarse->up, fine->n, coarse->up_rows, coarse->stream);
     if ((st = check_launch("up table")) != LAT_OK) return st;
     if (stream != coarse->stream) HIP_TRY(hipStreamSynchronize(coarse->stream));
     coarse->up_built = true;
   }
   return conv_common(coarse->up, fine->n, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
-                     flags, out_dev, ld_out, stream);
+                     flags, out_dev, ld_out, coarse->up_rows, stream);
 }
 
 int lattice_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,

@@ -20,7 +20,9 @@
 // Any assignment of K indices to (lane group, element) works as long as A
 // and B use the same one; the accumulator layout is fixed by the hardware:
 // lane l holds rows 4*(l/16) + r, r = 0..3, of column l%16.
+#include <algorithm>
 #include <type_traits>
+#include <utility>
 
 #include "lattice_internal.h"
 
@@ -38,6 +40,16 @@ __device__ inline uint16_t f32_to_bf16(float f) {
   const uint32_t u = __float_as_uint(f);
   if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
   return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+
+// f(std::integral_constant<int, i>) for i = 0 .. N-1, unrolled.
+template <class F, int... I>
+__device__ inline void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ inline void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
 // Operand fragment of one lane: 16 bytes of one row (A) or weight row (B).
@@ -73,7 +85,7 @@ template <bool BF16, int RM, int RN, int WM, int WN>
 __global__ void __launch_bounds__(kBlock)
 k_conv(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const void* __restrict__ in,
        int64_t ld_in, int Cin, const void* __restrict__ W, const float* __restrict__ bias, int Cout,
-       int relu, void* __restrict__ out, int64_t ld_out) {
+       int relu, void* __restrict__ out, int64_t ld_out, const int32_t* __restrict__ rows) {
   static_assert(WM * WN == kWaves, "four waves per workgroup");
   constexpr int KS = BF16 ? 32 : 16;          // channels per K step
   constexpr int EPL = BF16 ? 8 : 4;           // elements per lane per step
@@ -97,7 +109,7 @@ k_conv(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const void* 
 #pragma unroll
     for (int a = 0; a < RM; ++a) {
       const int64_t r = row0 + a * 16 + li;
-      nb[t][a] = r < n_out ? nbr[t * ldn + r] : -1;
+      nb[t][a] = r < n_out ? nbr[t * ldn + (rows ? rows[r] : r)] : -1;
     }
   int64_t wrow[RN];
   bool col_ok[RN];
@@ -153,8 +165,9 @@ k_conv(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const void* 
     for (int a = 0; a < RM; ++a)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t row = row0 + a * 16 + lg * 4 + r;
-        if (row >= n_out) continue;
+        const int64_t r0 = row0 + a * 16 + lg * 4 + r;
+        if (r0 >= n_out) continue;
+        const int64_t row = rows ? rows[r0] : r0;
         float v = acc[a][b][r] + bb;
         if (relu) v = fmaxf(v, 0.f);
         if constexpr (BF16)
@@ -168,13 +181,13 @@ k_conv(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const void* 
 template <bool BF16, int RM, int RN, int WM, int WN>
 void conv_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
-                 int64_t ld_out, hipStream_t s) {
+                 int64_t ld_out, const int32_t* rows, hipStream_t s) {
   const int64_t rows_per_block = static_cast<int64_t>(WM) * 16 * RM;
   const int cols_per_block = WN * 16 * RN;
   const dim3 grid(static_cast<unsigned>((n_out + rows_per_block - 1) / rows_per_block),
                   static_cast<unsigned>((Cout + cols_per_block - 1) / cols_per_block));
   hipLaunchKernelGGL((k_conv<BF16, RM, RN, WM, WN>), grid, dim3(kBlock), 0, s, nbr, ldn, n_out, in,
-                     ld_in, Cin, W, bias, Cout, relu, out, ld_out);
+                     ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows);
 }
 
 // ---------------------------------------------------------------------------
@@ -203,23 +216,26 @@ struct LdsConv {
   static constexpr int B_PER_T = (BN * CPR + kBlock - 1) / kBlock;
   static constexpr int A_BYTES = BM * LDR * U;
   static constexpr int B_BYTES = BN * LDR * U;
-  static constexpr int LDS_BYTES = 2 * (A_BYTES + B_BYTES) + kTaps * BM * 4;
+  static constexpr int LDS_BYTES = 2 * (A_BYTES + B_BYTES) + kTaps * BM * 4 + 32 * 4;
   static_assert(WM * WN == kWaves, "four waves");
   static_assert(RM >= 1 && RN >= 1, "wave tile");
   static_assert(A_PER_T >= 1 && BM * CPR % kBlock == 0, "A copy split");
 };
 
-template <bool BF16, int BM, int BN, int WM, int WN, int KCB>
+template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS>
 __global__ void __launch_bounds__(kBlock)
 k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const void* __restrict__ in,
            int64_t ld_in, int Cin, const void* __restrict__ W, const float* __restrict__ bias, int Cout,
-           int relu, void* __restrict__ out, int64_t ld_out, unsigned row_tiles) {
+           int relu, void* __restrict__ out, int64_t ld_out, const int32_t* __restrict__ rows,
+           unsigned row_tiles, int splits, float* __restrict__ part) {
   using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
   using E = typename std::conditional<BF16, uint16_t, float>::type;
   extern __shared__ __align__(16) unsigned char smem[];
   E* As = reinterpret_cast<E*>(smem);
   E* Bs = reinterpret_cast<E*>(smem + 2 * P::A_BYTES);
   int32_t* nbt = reinterpret_cast<int32_t*>(smem + 2 * (P::A_BYTES + P::B_BYTES));
+  int32_t* tflag = nbt + kTaps * BM;  // [16] tap used by some row of the tile
+  int32_t* tlist = tflag + 16;        // [16] used taps, count in tlist[15]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -236,22 +252,41 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   const int col0 = blockIdx.y * BN;
   const int wm = wave % WM, wn = wave / WM;
 
-  for (int i = tid; i < kTaps * BM; i += kBlock) {
+  // split z of the K dimension takes taps [tb, te)
+  const int tb = static_cast<int>(blockIdx.z) * kTaps / splits;
+  const int te = (static_cast<int>(blockIdx.z) + 1) * kTaps / splits;
+  // Taps that no row of the tile uses are skipped: their A rows are all
+  // zero.  Rows are multiplied independently, so the result of a row does
+  // not depend on which other rows share its tile.
+  if (tid < 16) tflag[tid] = 0;
+  __syncthreads();
+  for (int i = tid; i < (te - tb) * BM; i += kBlock) {
     const int t = i / BM, r = i - t * BM;
-    nbt[i] = row0 + r < n_out ? nbr[t * ldn + row0 + r] : -1;
+    int32_t nb = -1;
+    if (row0 + r < n_out) nb = nbr[(tb + t) * ldn + (rows ? rows[row0 + r] : row0 + r)];
+    nbt[i] = nb;
+    if (nb >= 0) tflag[t] = 1;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int k = 0;
+    for (int t = 0; t < te - tb; ++t)
+      if (tflag[t]) tlist[k++] = t;
+    tlist[15] = k;
   }
   __syncthreads();
 
   const int kc_steps = (Cin + P::KC - 1) / P::KC;
-  const int stages = kTaps * kc_steps;
+  const int stages = tlist[15] * kc_steps;
 
   // global -> register copies of one stage
   using V = uint4;
-  V ra[2][P::A_PER_T], rb[2][P::B_PER_T];
+  V ra[NS][P::A_PER_T], rb[NS][P::B_PER_T];
   auto fetch = [&](auto set_c, int st) {
     constexpr int set = decltype(set_c)::value;
-    const int t = st / kc_steps;
-    const int kc = (st - t * kc_steps) * P::KC;
+    const int ti = st / kc_steps;
+    const int t = tlist[ti];
+    const int kc = (st - ti * kc_steps) * P::KC;
 #pragma unroll
     for (int j = 0; j < P::A_PER_T; ++j) {
       const int q = tid + j * kBlock;
@@ -270,7 +305,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
       const int col = col0 + r;
       rb[set][j] = (q < BN * P::CPR && col < Cout && ch < Cin)
                   ? *reinterpret_cast<const V*>(static_cast<const E*>(W) +
-                                                (static_cast<int64_t>(t) * Cout + col) * Cin + ch)
+                                                (static_cast<int64_t>(tb + t) * Cout + col) * Cin + ch)
                   : make_uint4(0u, 0u, 0u, 0u);
     }
   };
@@ -300,20 +335,23 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
 #pragma unroll
     for (int c = 0; c < P::RN; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Two stages of global loads in flight: while stage st is multiplied,
-  // stage st+1 waits in registers set (st+1)&1 (loaded one iteration ago) and
-  // stage st+2 is being loaded into the other set.
-  fetch(std::integral_constant<int, 0>{}, 0);
-  if (stages > 1) fetch(std::integral_constant<int, 1>{}, 1);
-  stash(std::integral_constant<int, 0>{}, 0);
+  // NS stages of global loads in flight: stage st is multiplied from LDS
+  // buffer st & 1 while stages st+1 .. st+NS-1 wait in register sets
+  // (st+i) % NS.  After the multiply, stage st+1 goes to the other LDS
+  // buffer and stage st+NS is loaded into the set that stage st vacated, so
+  // a load has NS-1 steps to arrive.  Set indices are compile-time constants
+  // so that the register sets stay in registers.
+  static_for<NS>([&](auto i_c) {
+    if (decltype(i_c)::value < stages) fetch(i_c, decltype(i_c)::value);
+  });
+  if (stages > 0) stash(std::integral_constant<int, 0>{}, 0);
   __syncthreads();
-  // one pipeline step; SET = st & 1 is a compile-time constant so that the
-  // register sets stay in registers
   auto step = [&](auto set_c, int st) {
     constexpr int SET = decltype(set_c)::value;
-    constexpr int OTHER = SET ^ 1;
-    const E* a = As + SET * (BM * P::LDR) + (wm * P::RM * 16 + li) * P::LDR + lg * P::EPL;
-    const E* bb = Bs + SET * (BN * P::LDR) + (wn * P::RN * 16 + li) * P::LDR + lg * P::EPL;
+    constexpr int NEXT = (SET + 1) % NS;
+    const int buf = st & 1;
+    const E* a = As + buf * (BM * P::LDR) + (wm * P::RM * 16 + li) * P::LDR + lg * P::EPL;
+    const E* bb = Bs + buf * (BN * P::LDR) + (wn * P::RN * 16 + li) * P::LDR + lg * P::EPL;
 #pragma unroll
     for (int k = 0; k < P::KC; k += P::KS) {
       Frag<BF16> fa[P::RM], fb[P::RN];
@@ -337,15 +375,32 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
               acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i].v[e], fb[j].v[e], acc[i][j], 0, 0, 0);
       }
     }
-    if (st + 1 < stages) stash(std::integral_constant<int, OTHER>{}, OTHER);
-    if (st + 2 < stages) fetch(std::integral_constant<int, SET>{}, st + 2);
+    if (st + 1 < stages) stash(std::integral_constant<int, NEXT>{}, buf ^ 1);
+    if (st + NS < stages) fetch(set_c, st + NS);
     __syncthreads();
   };
-  for (int st = 0; st < stages; st += 2) {
-    step(std::integral_constant<int, 0>{}, st);
-    if (st + 1 < stages) step(std::integral_constant<int, 1>{}, st + 1);
-  }
+  for (int st = 0; st < stages; st += NS)
+    static_for<NS>([&](auto i_c) {
+      if (st + decltype(i_c)::value < stages) step(i_c, st + decltype(i_c)::value);
+    });
 
+  if (part) {
+    // raw partial sums of this split, [split][n_out][Cout]
+    float* dst = part + static_cast<int64_t>(blockIdx.z) * n_out * Cout;
+#pragma unroll
+    for (int j = 0; j < P::RN; ++j) {
+      const int col = col0 + (wn * P::RN + j) * 16 + li;
+      if (col >= Cout) continue;
+#pragma unroll
+      for (int i = 0; i < P::RM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t row = row0 + (wm * P::RM + i) * 16 + lg * 4 + r;
+          if (row < n_out) dst[row * Cout + col] = acc[i][j][r];
+        }
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < P::RN; ++j) {
     const int col = col0 + (wn * P::RN + j) * 16 + li;
@@ -355,8 +410,9 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
     for (int i = 0; i < P::RM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t row = row0 + (wm * P::RM + i) * 16 + lg * 4 + r;
-        if (row >= n_out) continue;
+        const int64_t r0 = row0 + (wm * P::RM + i) * 16 + lg * 4 + r;
+        if (r0 >= n_out) continue;
+        const int64_t row = rows ? rows[r0] : r0;
         float v = acc[i][j][r] + bv;
         if (relu) v = fmaxf(v, 0.f);
         if constexpr (BF16)
@@ -367,48 +423,99 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   }
 }
 
-template <bool BF16, int BM, int BN, int WM, int WN, int KCB>
+// Sum of the split partials in split order, then bias, ReLU and conversion.
+template <bool BF16>
+__global__ void __launch_bounds__(kBlock)
+k_conv_reduce(const float* __restrict__ part, int splits, int64_t n_out, int Cout, const float* __restrict__ bias,
+              int relu, void* __restrict__ out, int64_t ld_out) {
+  const int64_t quads = n_out * (Cout / 4);
+  const int64_t plane = n_out * Cout;
+  for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < quads;
+       q += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int64_t row = q / (Cout / 4);
+    const int col = static_cast<int>(q - row * (Cout / 4)) * 4;
+    float4 a = *reinterpret_cast<const float4*>(part + row * Cout + col);
+    for (int z = 1; z < splits; ++z) {
+      const float4 b = *reinterpret_cast<const float4*>(part + z * plane + row * Cout + col);
+      a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+    }
+    float v[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (bias) v[i] += bias[col + i];
+      if (relu) v[i] = fmaxf(v[i], 0.f);
+    }
+    if constexpr (BF16) {
+      const uint32_t lo = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+      const uint32_t hi = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + row * ld_out + col) = make_uint2(lo, hi);
+    } else {
+      *reinterpret_cast<float4*>(static_cast<float*>(out) + row * ld_out + col) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  }
+}
+
+template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS = 2>
 void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                      int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
-                     int64_t ld_out, hipStream_t s) {
+                     int64_t ld_out, const int32_t* rows, hipStream_t s, int splits = 1, float* part = nullptr) {
   using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
+  if (rows) splits = 1;  // partial sums are kept in permuted row order
   static bool lds_limit_set = false;
   if (!lds_limit_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_lds<BF16, BM, BN, WM, WN, KCB>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, P::LDS_BYTES);
     lds_limit_set = true;
   }
   const int64_t tiles = (n_out + BM - 1) / BM;
   const unsigned per_xcd = static_cast<unsigned>((tiles + 7) / 8);
-  const dim3 grid(per_xcd * 8, static_cast<unsigned>((Cout + BN - 1) / BN));
-  hipLaunchKernelGGL((k_conv_lds<BF16, BM, BN, WM, WN, KCB>), grid, dim3(kBlock), P::LDS_BYTES, s, nbr, ldn,
-                     n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, static_cast<unsigned>(tiles));
+  const dim3 grid(per_xcd * 8, static_cast<unsigned>((Cout + BN - 1) / BN), static_cast<unsigned>(splits));
+  hipLaunchKernelGGL((k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS>), grid, dim3(kBlock), P::LDS_BYTES, s, nbr, ldn,
+                     n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, static_cast<unsigned>(tiles),
+                     splits, splits > 1 ? part : nullptr);
+  if (splits > 1) {
+    const int64_t quads = n_out * (Cout / 4);
+    const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((quads + kBlock - 1) / kBlock, 8192));
+    hipLaunchKernelGGL((k_conv_reduce<BF16>), dim3(blocks), dim3(kBlock), 0, s, part, splits, n_out, Cout, bias,
+                       relu, out, ld_out);
+  }
 }
 
 int64_t blocks_of(int64_t n_out, int Cout, int rows, int cols) {
   return ((n_out + rows - 1) / rows) * ((Cout + cols - 1) / cols);
 }
 
-// Tile choice, from a sweep of every tile shape over the lattices of the
-// LiDAR scan (fp32) and the 1M-point room (bf16) on MI355X: small tiles with
-// deep pipelines win because the gathered A operand, not the matrix cores,
-// sets the pace; wide-output fp32 layers on large levels prefer 32 x 64.
+// Tile choice, from a sweep of tile shapes and pipeline depths over the
+// lattices of the LiDAR scan (fp32) and of the 1M-point room (bf16) on
+// MI355X.  fp32: small tiles win; the gathered A operand, not the matrix
+// cores, sets the pace, and the levels are small.  bf16: 128 x 128 tiles
+// halve the gathered bytes per flop and win once there are enough of them
+// (wide layers on large levels); 64 x 64 otherwise.
 template <bool BF16>
 void conv_dispatch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                    int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
-                   int64_t ld_out, hipStream_t s) {
+                   int64_t ld_out, const int32_t* rows, hipStream_t s) {
   if (Cout <= 16)
-    return conv_launch<BF16, 1, 1, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+    return conv_launch<BF16, 1, 1, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, s);
   if constexpr (BF16) {
+    const int64_t b128 = blocks_of(n_out, Cout, 128, 128);
+    if (Cout % 128 == 0 && (b128 >= 1500 || (Cin >= 256 && b128 >= 400)))
+      return conv_lds_launch<true, 128, 128, 2, 2, 64, 3>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
+                                                          ld_out, rows, s);
     if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= 256)
-      return conv_lds_launch<true, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-    return conv_lds_launch<true, 32, 32, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+      return conv_lds_launch<true, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
+                                                      ld_out, rows, s);
+    return conv_lds_launch<true, 32, 32, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
+                                                    ld_out, rows, s);
   } else {
     if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= 2048)
-      return conv_lds_launch<false, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+      return conv_lds_launch<false, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
+                                                       ld_out, rows, s);
     if (Cout > 64 && blocks_of(n_out, Cout, 32, 64) >= 1024)
-      return conv_lds_launch<false, 32, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-    return conv_lds_launch<false, 32, 32, 2, 2, 256>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+      return conv_lds_launch<false, 32, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
+                                                       ld_out, rows, s);
+    return conv_lds_launch<false, 32, 32, 2, 2, 256>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
+                                                     ld_out, rows, s);
   }
 }
 
@@ -416,11 +523,11 @@ void conv_dispatch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* i
 
 void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
-                 int64_t ld_out, hipStream_t s) {
+                 int64_t ld_out, const int32_t* rows, hipStream_t s) {
   if (n_out <= 0) return;
   ScopedKernelTimer tm("conv", s);
-  if (bf16) conv_dispatch<true>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
-  else conv_dispatch<false>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, s);
+  if (bf16) conv_dispatch<true>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, s);
+  else conv_dispatch<false>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, s);
 }
 
 }  // namespace lat

@@ -13,6 +13,8 @@
 // the vertex counter.
 #pragma clang fp contract(off)
 
+#include <algorithm>
+
 #include "lattice_internal.h"
 
 namespace lat {
@@ -442,6 +444,46 @@ k_up_table(HashView coarse, const uint64_t* __restrict__ fkeys, int64_t n, int32
   nbr[static_cast<int64_t>(t) * ldn + v] = found;
 }
 
+// Row order for a convolution table: within each range of kOrderRange rows,
+// rows are grouped by their tap mask (bit t set when tap t is present) with
+// a counting sort in LDS.  Tiles of the convolution then mostly hold rows of
+// one mask and skip the taps none of their rows uses, while the order stays
+// local, so the gather keeps its spatial locality.  The order within a mask
+// depends on scheduling; the convolution's result for a row does not.
+constexpr int kOrderRange = 4096;
+
+__global__ void __launch_bounds__(kBlock)
+k_mask_order(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n, int32_t* __restrict__ rows) {
+  __shared__ int32_t hist[kMaskBins];
+  __shared__ int32_t start[kMaskBins];
+  __shared__ int32_t lds4[kBlock / 64];
+  __shared__ uint16_t mk[kOrderRange];
+  __shared__ uint16_t rk[kOrderRange];
+  static_assert(kMaskBins == 2 * kBlock, "two bins per thread");
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kOrderRange;
+  const int cnt = static_cast<int>(n - r0 < kOrderRange ? n - r0 : kOrderRange);
+  hist[2 * threadIdx.x] = 0;
+  hist[2 * threadIdx.x + 1] = 0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < cnt; i += kBlock) {
+    int m = 0;
+#pragma unroll
+    for (int t = 0; t < kTaps; ++t)
+      if (nbr[static_cast<int64_t>(t) * ldn + r0 + i] >= 0) m |= 1 << t;
+    mk[i] = static_cast<uint16_t>(m);
+    rk[i] = static_cast<uint16_t>(atomicAdd(&hist[m], 1));
+  }
+  __syncthreads();
+  const int32_t b0 = hist[2 * threadIdx.x], b1 = hist[2 * threadIdx.x + 1];
+  int32_t total;
+  const int32_t ex = block_exclusive_sum(b0 + b1, lds4, &total);
+  start[2 * threadIdx.x] = ex;
+  start[2 * threadIdx.x + 1] = ex + b0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < cnt; i += kBlock)
+    rows[r0 + start[mk[i]] + rk[i]] = static_cast<int32_t>(r0 + i);
+}
+
 __global__ void __launch_bounds__(kBlock)
 k_export_keys(const uint64_t* __restrict__ vkeys, int64_t n, int4* __restrict__ out) {
   const int64_t v = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
@@ -527,11 +569,13 @@ void launch_down_table(HashView fine, const uint64_t* coarse_keys, const int32_t
 }
 
 void launch_up_table(HashView coarse, const uint64_t* fine_keys, int64_t n_fine, int32_t* nbr,
-                     int64_t ldn, hipStream_t s) {
+                     int64_t ldn, int32_t* rows, hipStream_t s) {
   if (n_fine <= 0) return;
   ScopedKernelTimer tm("nbr", s);
-  hipLaunchKernelGGL(k_up_table, dim3(blocks_for(n_fine * kTaps)), dim3(kBlock), 0, s, coarse,
-                     fine_keys, n_fine, nbr, ldn);
+  hipLaunchKernelGGL(k_up_table, dim3(blocks_for(n_fine * kTaps)), dim3(kBlock), 0, s, coarse, fine_keys, n_fine,
+                     nbr, ldn);
+  hipLaunchKernelGGL(k_mask_order, dim3(static_cast<unsigned>((n_fine + kOrderRange - 1) / kOrderRange)),
+                     dim3(kBlock), 0, s, nbr, ldn, n_fine, rows);
 }
 
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s) {

@@ -13,6 +13,7 @@ namespace lat {
 constexpr int kDim = 3;                 // d
 constexpr int kVerts = kDim + 1;        // d+1 vertices per simplex, coordinates per key
 constexpr int kTaps = 2 * kVerts + 1;   // 1-hop neighbourhood incl. the centre
+constexpr int kMaskBins = 1 << kTaps;   // tap masks (bit t: tap t present)
 constexpr int kCoordBits = 21;
 constexpr int32_t kCoordLimit = 1 << 20;          // |c_i| < 2^20
 constexpr uint64_t kEmptyKey = ~0ull;             // bit 63 set: never a packed key
@@ -126,7 +127,7 @@ void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_d
 void launch_down_table(HashView fine, const uint64_t* coarse_keys, const int32_t* n_dev, int64_t n_max,
                        int32_t* nbr, int64_t ldn, hipStream_t s);
 void launch_up_table(HashView coarse, const uint64_t* fine_keys, int64_t n_fine, int32_t* nbr,
-                     int64_t ldn, hipStream_t s);
+                     int64_t ldn, int32_t* rows, hipStream_t s);
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s);
 void launch_transpose_table(const int32_t* tab, int64_t ld, int64_t n, int32_t* out, hipStream_t s);
 // splat_slice.hip
@@ -143,6 +144,6 @@ void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const vo
 // conv.hip
 void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
-                 int64_t ld_out, hipStream_t s);
+                 int64_t ld_out, const int32_t* rows, hipStream_t s);
 
 }  // namespace lat
