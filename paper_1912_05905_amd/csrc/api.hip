@@ -234,9 +234,8 @@ struct lattice_s {
   int64_t total = 0;               // number of list entries (4m)
   int32_t* nbr = nullptr;        // 9 x nmax same-level table (tap-major, ld nmax)
   int32_t* down = nullptr;       // 9 x nmax table into the parent (coarse levels, ld nmax)
-  int32_t* up = nullptr;         // 9 x n_parent table from the parent into this level
+  int32_t* up = nullptr;         // 9 x parent->nmax table from the parent into this level
   int32_t* up_rows = nullptr;    // parent vertices, grouped by the tap mask of their up row
-  bool up_built = false;
   int64_t retry_cap = 0;          // coarse levels: table size of a rebuild after overflow
 
   HashView hash() const { return HashView{table, static_cast<uint64_t>(cap - 1)}; }
@@ -370,6 +369,8 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   ALLOC(nbr, int32_t, kTaps * nmax);
   if (parent) {
     ALLOC(down, int32_t, kTaps * nmax);
+    ALLOC(up, int32_t, kTaps * parent->nmax);
+    ALLOC(up_rows, int32_t, parent->nmax);
   }
 #undef ALLOC
   Scratch slot_count, vslot, slot, rank, work;
@@ -393,8 +394,11 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   launch_count_scan(slot_count.as<int32_t>(), vslot.as<int32_t>(), n_dev, L->offsets, work.as<int32_t>(), s);
   launch_fill_lists(L->hash(), slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->offsets, L->idx,
                     L->entries, L->entry_w, L->chunk_first, L->chunk, refs, s);
-  launch_neighbor_table(L->hash(), L->vkeys, n_dev, nmax, L->nbr, nmax, s);
-  if (parent) launch_down_table(parent->hash(), L->vkeys, n_dev, nmax, L->down, nmax, s);
+  if (parent)
+    launch_coarse_tables(L->hash(), parent->hash(), L->vkeys, parent->vkeys, n_dev, &parent->dc->counter, nmax,
+                         parent->nmax, L->nbr, L->down, L->up, L->up_rows, s);
+  else
+    launch_neighbor_table(L->hash(), L->vkeys, n_dev, nmax, L->nbr, nmax, s);
   return check_launch("lattice build");
 }
 
@@ -706,18 +710,7 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
   if ((st = check_handle(fine)) != LAT_OK) return st;
   if ((st = check_handle(coarse)) != LAT_OK) return st;
   if (coarse->parent != fine) return fail(LAT_ELEVEL, "coarse must be lattice_coarsen(fine)");
-  if (!coarse->up_built && fine->n > 0) {
-    void* p;
-    if ((st = coarse->alloc(sizeof(int32_t) * kTaps * fine->n, coarse->stream, &p)) != LAT_OK) return st;
-    coarse->up = static_cast<int32_t*>(p);
-    if ((st = coarse->alloc(sizeof(int32_t) * fine->n, coarse->stream, &p)) != LAT_OK) return st;
-    coarse->up_rows = static_cast<int32_t*>(p);
-    launch_up_table(coarse->hash(), fine->vkeys, fine->n, coarse->up, fine->n, coarse->up_rows, coarse->stream);
-    if ((st = check_launch("up table")) != LAT_OK) return st;
-    if (stream != coarse->stream) HIP_TRY(hipStreamSynchronize(coarse->stream));
-    coarse->up_built = true;
-  }
-  return conv_common(coarse->up, fine->n, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
+  return conv_common(coarse->up, fine->nmax, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
                      flags, out_dev, ld_out, coarse->up_rows, stream);
 }
 

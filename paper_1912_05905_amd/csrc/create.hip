@@ -378,56 +378,33 @@ k_fill_lists(HashView h, const int32_t* __restrict__ slot, const int32_t* __rest
 }
 
 // nbr[t][v] for taps 1..8 (tap 0 = v): the vertex at c_v + o_t.
-__global__ void __launch_bounds__(kBlock)
-k_neighbor_table(HashView h, const uint64_t* __restrict__ vkeys, const int32_t* __restrict__ n_dev,
-                 int32_t* __restrict__ nbr, int64_t ldn) {
-  const int64_t n = *n_dev;
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n * kTaps;
-       i += static_cast<int64_t>(gridDim.x) * kBlock) {
-    const int t = static_cast<int>(i / n);
-    const int64_t v = i - static_cast<int64_t>(t) * n;
-    if (t == 0) {
-      nbr[v] = static_cast<int32_t>(v);
-      continue;
-    }
-    int32_t c[kVerts];
-    unpack_key(vkeys[v], c);
-    for (int j = 0; j < kVerts; ++j) c[j] += tap_offset(t, j);
-    const uint64_t key = key_or_empty(c);
-    nbr[static_cast<int64_t>(t) * ldn + v] = key == kEmptyKey ? -1 : hash_find(h, key);
-  }
-}
-
-// Downsample: coarse vertex v reads the fine vertex at 2 c_v + o_t.
-__global__ void __launch_bounds__(kBlock)
-k_down_table(HashView fine, const uint64_t* __restrict__ ckeys, const int32_t* __restrict__ n_dev,
-             int32_t* __restrict__ nbr, int64_t ldn) {
-  const int64_t n = *n_dev;
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n * kTaps;
-       i += static_cast<int64_t>(gridDim.x) * kBlock) {
-    const int t = static_cast<int>(i / n);
-    const int64_t v = i - static_cast<int64_t>(t) * n;
-    int32_t c[kVerts];
-    unpack_key(ckeys[v], c);
-    for (int j = 0; j < kVerts; ++j) c[j] = 2 * c[j] + tap_offset(t, j);
-    const uint64_t key = key_or_empty(c);
-    nbr[static_cast<int64_t>(t) * ldn + v] = key == kEmptyKey ? -1 : hash_find(fine, key);
-  }
-}
-
-// Upsample: fine vertex v reads the coarse vertex at (c_v + o_t)/2 when that
-// is a lattice point (even coordinates whose halves agree mod d+1).  The
-// check matters: packed keys omit the last coordinate, so a non-lattice point
-// could otherwise alias a stored key.
-__global__ void __launch_bounds__(kBlock)
-k_up_table(HashView coarse, const uint64_t* __restrict__ fkeys, int64_t n, int32_t* __restrict__ nbr,
-           int64_t ldn) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (i >= n * kTaps) return;
-  const int t = static_cast<int>(i / n);
-  const int64_t v = i - static_cast<int64_t>(t) * n;
+// Entries of the convolution tables (tap t of the vertex with packed key
+// `key`; -1 where the target vertex does not exist):
+//   same level: the vertex at c_v + o_t (tap 0: the vertex itself);
+//   Downsample (coarse vertex into the fine level): the vertex at 2 c_v + o_t;
+//   Upsample (fine vertex into the coarse level): the vertex at
+//   (c_v + o_t)/2 when that is a lattice point, i.e. even coordinates whose
+//   halves agree mod d+1.  The check matters: packed keys omit the last
+//   coordinate, so a non-lattice point could otherwise alias a stored key.
+__device__ inline int32_t same_level_entry(const HashView& h, uint64_t key, int t) {
   int32_t c[kVerts];
-  unpack_key(fkeys[v], c);
+  unpack_key(key, c);
+  for (int j = 0; j < kVerts; ++j) c[j] += tap_offset(t, j);
+  const uint64_t k = key_or_empty(c);
+  return k == kEmptyKey ? -1 : hash_find(h, k);
+}
+
+__device__ inline int32_t down_entry(const HashView& fine, uint64_t key, int t) {
+  int32_t c[kVerts];
+  unpack_key(key, c);
+  for (int j = 0; j < kVerts; ++j) c[j] = 2 * c[j] + tap_offset(t, j);
+  const uint64_t k = key_or_empty(c);
+  return k == kEmptyKey ? -1 : hash_find(fine, k);
+}
+
+__device__ inline int32_t up_entry(const HashView& coarse, uint64_t key, int t) {
+  int32_t c[kVerts];
+  unpack_key(key, c);
   bool lattice_point = true;
   for (int j = 0; j < kVerts; ++j) {
     const int32_t u = c[j] + tap_offset(t, j);
@@ -436,12 +413,53 @@ k_up_table(HashView coarse, const uint64_t* __restrict__ fkeys, int64_t n, int32
   }
   for (int j = 1; j < kVerts; ++j)
     if ((c[j] & 3) != (c[0] & 3)) lattice_point = false;
-  int32_t found = -1;
-  if (lattice_point) {
-    const uint64_t key = key_or_empty(c);
-    if (key != kEmptyKey) found = hash_find(coarse, key);
+  if (!lattice_point) return -1;
+  const uint64_t k = key_or_empty(c);
+  return k == kEmptyKey ? -1 : hash_find(coarse, k);
+}
+
+// Same-level table of the finest level, tap-major (nbr[t * ldn + v]).
+__global__ void __launch_bounds__(kBlock)
+k_neighbor_table(HashView h, const uint64_t* __restrict__ vkeys, const int32_t* __restrict__ n_dev,
+                 int32_t* __restrict__ nbr, int64_t ldn) {
+  const int64_t n = *n_dev;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n * kTaps;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int t = static_cast<int>(i / n);
+    const int64_t v = i - static_cast<int64_t>(t) * n;
+    nbr[static_cast<int64_t>(t) * ldn + v] = t == 0 ? static_cast<int32_t>(v) : same_level_entry(h, vkeys[v], t);
   }
-  nbr[static_cast<int64_t>(t) * ldn + v] = found;
+}
+
+// The three tables of a coarse level in one launch: its same-level table
+// and its Downsample table (9 entries per coarse vertex) and the Upsample
+// table from it into the fine level (9 entries per fine vertex).  Both
+// vertex counts come from device memory.
+__global__ void __launch_bounds__(kBlock)
+k_coarse_tables(HashView hc, HashView hf, const uint64_t* __restrict__ ckeys, const uint64_t* __restrict__ fkeys,
+                const int32_t* __restrict__ nc_dev, const int32_t* __restrict__ nf_dev, int32_t* __restrict__ nbr,
+                int32_t* __restrict__ down, int64_t ldc, int32_t* __restrict__ up, int64_t ldf) {
+  const int64_t nc = *nc_dev, nf = *nf_dev;
+  const int64_t per_c = nc * kTaps;
+  const int64_t total = 2 * per_c + nf * kTaps;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < total;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    if (i < per_c) {
+      const int t = static_cast<int>(i / nc);
+      const int64_t v = i - static_cast<int64_t>(t) * nc;
+      nbr[static_cast<int64_t>(t) * ldc + v] = t == 0 ? static_cast<int32_t>(v) : same_level_entry(hc, ckeys[v], t);
+    } else if (i < 2 * per_c) {
+      const int64_t k = i - per_c;
+      const int t = static_cast<int>(k / nc);
+      const int64_t v = k - static_cast<int64_t>(t) * nc;
+      down[static_cast<int64_t>(t) * ldc + v] = down_entry(hf, ckeys[v], t);
+    } else {
+      const int64_t k = i - 2 * per_c;
+      const int t = static_cast<int>(k / nf);
+      const int64_t v = k - static_cast<int64_t>(t) * nf;
+      up[static_cast<int64_t>(t) * ldf + v] = up_entry(hc, fkeys[v], t);
+    }
+  }
 }
 
 // Row order for a convolution table: within each range of kOrderRange rows,
@@ -453,25 +471,43 @@ k_up_table(HashView coarse, const uint64_t* __restrict__ fkeys, int64_t n, int32
 constexpr int kOrderRange = 4096;
 
 __global__ void __launch_bounds__(kBlock)
-k_mask_order(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n, int32_t* __restrict__ rows) {
+k_mask_order(const int32_t* __restrict__ nbr, int64_t ldn, const int32_t* __restrict__ n_dev,
+             int32_t* __restrict__ rows) {
   __shared__ int32_t hist[kMaskBins];
   __shared__ int32_t start[kMaskBins];
   __shared__ int32_t lds4[kBlock / 64];
   __shared__ uint16_t mk[kOrderRange];
   __shared__ uint16_t rk[kOrderRange];
   static_assert(kMaskBins == 2 * kBlock, "two bins per thread");
+  constexpr int kBatch = 4;  // rows per thread whose table entries are loaded together
+  static_assert(kOrderRange % (kBatch * kBlock) == 0, "whole batches");
+  const int64_t n = *n_dev;
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kOrderRange;
+  if (r0 >= n) return;
   const int cnt = static_cast<int>(n - r0 < kOrderRange ? n - r0 : kOrderRange);
   hist[2 * threadIdx.x] = 0;
   hist[2 * threadIdx.x + 1] = 0;
   __syncthreads();
-  for (int i = threadIdx.x; i < cnt; i += kBlock) {
-    int m = 0;
+  for (int i0 = 0; i0 < cnt; i0 += kBatch * kBlock) {
+    int m[kBatch];
 #pragma unroll
-    for (int t = 0; t < kTaps; ++t)
-      if (nbr[static_cast<int64_t>(t) * ldn + r0 + i] >= 0) m |= 1 << t;
-    mk[i] = static_cast<uint16_t>(m);
-    rk[i] = static_cast<uint16_t>(atomicAdd(&hist[m], 1));
+    for (int b = 0; b < kBatch; ++b) {
+      const int i = i0 + b * kBlock + threadIdx.x;
+      m[b] = 0;
+      if (i < cnt) {
+#pragma unroll
+        for (int t = 0; t < kTaps; ++t)
+          if (nbr[static_cast<int64_t>(t) * ldn + r0 + i] >= 0) m[b] |= 1 << t;
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int i = i0 + b * kBlock + threadIdx.x;
+      if (i < cnt) {
+        mk[i] = static_cast<uint16_t>(m[b]);
+        rk[i] = static_cast<uint16_t>(atomicAdd(&hist[m[b]], 1));
+      }
+    }
   }
   __syncthreads();
   const int32_t b0 = hist[2 * threadIdx.x], b1 = hist[2 * threadIdx.x + 1];
@@ -560,22 +596,15 @@ void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_d
                      nbr, ldn);
 }
 
-void launch_down_table(HashView fine, const uint64_t* coarse_keys, const int32_t* n_dev, int64_t n_max,
-                       int32_t* nbr, int64_t ldn, hipStream_t s) {
-  if (n_max <= 0) return;
+void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse_keys, const uint64_t* fine_keys,
+                          const int32_t* nc_dev, const int32_t* nf_dev, int64_t nc_max, int64_t nf_max, int32_t* nbr,
+                          int32_t* down, int32_t* up, int32_t* up_rows, hipStream_t s) {
+  if (nc_max <= 0 || nf_max <= 0) return;
   ScopedKernelTimer tm("nbr", s);
-  hipLaunchKernelGGL(k_down_table, dim3(stride_grid(n_max * kTaps)), dim3(kBlock), 0, s, fine, coarse_keys,
-                     n_dev, nbr, ldn);
-}
-
-void launch_up_table(HashView coarse, const uint64_t* fine_keys, int64_t n_fine, int32_t* nbr,
-                     int64_t ldn, int32_t* rows, hipStream_t s) {
-  if (n_fine <= 0) return;
-  ScopedKernelTimer tm("nbr", s);
-  hipLaunchKernelGGL(k_up_table, dim3(blocks_for(n_fine * kTaps)), dim3(kBlock), 0, s, coarse, fine_keys, n_fine,
-                     nbr, ldn);
-  hipLaunchKernelGGL(k_mask_order, dim3(static_cast<unsigned>((n_fine + kOrderRange - 1) / kOrderRange)),
-                     dim3(kBlock), 0, s, nbr, ldn, n_fine, rows);
+  hipLaunchKernelGGL(k_coarse_tables, dim3(stride_grid((2 * nc_max + nf_max) * kTaps)), dim3(kBlock), 0, s, coarse,
+                     fine, coarse_keys, fine_keys, nc_dev, nf_dev, nbr, down, nc_max, up, nf_max);
+  hipLaunchKernelGGL(k_mask_order, dim3(static_cast<unsigned>((nf_max + kOrderRange - 1) / kOrderRange)),
+                     dim3(kBlock), 0, s, up, nf_max, nf_dev, up_rows);
 }
 
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s) {
