@@ -2,6 +2,7 @@
 // kernel-family timing.  Every lattice operation is a hand-written kernel in
 // create.hip, splat_slice.hip or conv.hip; this file only orchestrates them.
 #include <cmath>
+#include <cstddef>
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -201,7 +202,17 @@ struct DevBuf {
 };
 
 struct DeviceCounters {
-  int32_t counter;
+  int32_t counter;  // vertex count; with `done`, one 64-bit word updated atomically
+  uint32_t done;    // workgroups of the insert kernel past their vertex claims
+  uint32_t err;     // error bits
+  uint32_t pad;
+};
+static_assert(offsetof(DeviceCounters, done) == 4, "count and done share one aligned 64-bit word");
+
+// Pinned host landing slot, written by the last workgroup of the insert
+// kernel: [0] vertex count, [1] error bits.
+struct HostCounts {
+  int32_t n;
   uint32_t err;
 };
 
@@ -213,7 +224,7 @@ struct lattice_s {
   int64_t cap = 0;               // hash slots
   bool counts_known = true;      // n and the device error flag have been read back
   DeviceCounters* dc = nullptr;  // device counters (vertex count, error bits)
-  DeviceCounters* host_dc = nullptr;  // pinned landing slot of their readback
+  HostCounts* host_dc = nullptr;  // pinned landing slot of their readback
   hipEvent_t counts_ready = nullptr;  // recorded after the readback
   int chunk = 64;                // list entries per splat work item
   int status = LAT_OK;           // poisoned when != LAT_OK
@@ -263,19 +274,19 @@ class HostSlots {
     static HostSlots* h = new HostSlots();
     return *h;
   }
-  DeviceCounters* take() {
+  HostCounts* take() {
     std::lock_guard<std::mutex> lk(mu_);
     if (free_.empty()) {
       void* p = nullptr;
       constexpr int kSlab = 256;
-      if (hipHostMalloc(&p, sizeof(DeviceCounters) * kSlab, hipHostMallocDefault) != hipSuccess) return nullptr;
-      for (int i = 0; i < kSlab; ++i) free_.push_back(static_cast<DeviceCounters*>(p) + i);
+      if (hipHostMalloc(&p, sizeof(HostCounts) * kSlab, hipHostMallocDefault) != hipSuccess) return nullptr;
+      for (int i = 0; i < kSlab; ++i) free_.push_back(static_cast<HostCounts*>(p) + i);
     }
-    DeviceCounters* d = free_.back();
+    HostCounts* d = free_.back();
     free_.pop_back();
     return d;
   }
-  void give(DeviceCounters* d) {
+  void give(HostCounts* d) {
     if (!d) return;
     std::lock_guard<std::mutex> lk(mu_);
     free_.push_back(d);
@@ -299,7 +310,7 @@ class HostSlots {
 
  private:
   std::mutex mu_;
-  std::vector<DeviceCounters*> free_;
+  std::vector<HostCounts*> free_;
   std::vector<hipEvent_t> events_;
 };
 
@@ -337,9 +348,10 @@ struct Scratch {
 };
 
 // Enqueue the construction of a lattice with a table of `cap` slots:
-// clear, insert, readback of the vertex count and error bits (asynchronous,
-// with an event), then the scan, the vertex lists and the neighbour table,
-// which take the vertex count from device memory.  Nothing waits here.
+// clear, insert (whose last workgroup writes the vertex count and the error
+// bits into the pinned host slot; an event marks its completion), then the
+// scan, the vertex lists and the tables, which take the vertex count from
+// device memory.  Nothing waits here.
 int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_scale, const float a[3],
                   const lattice_s* parent, int64_t cap, hipStream_t s) {
   const int64_t m = L->m;
@@ -378,20 +390,21 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   if ((st = vslot.get(sizeof(int32_t) * nmax, s)) != LAT_OK) return st;
   if ((st = slot.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
   if ((st = rank.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
-  if ((st = work.get(sizeof(int32_t) * scan_workspace_elems(), s)) != LAT_OK) return st;
+  if ((st = work.get(scan_workspace_bytes(), s)) != LAT_OK) return st;
   if (!L->host_dc && !(L->host_dc = HostSlots::get().take())) return fail(LAT_ENOMEM, "pinned host slot");
   if (!L->counts_ready && !(L->counts_ready = HostSlots::get().take_event()))
     return fail(LAT_EDEVICE, "event creation failed");
 
-  launch_clear_table(L->table, slot_count.as<int32_t>(), cap, reinterpret_cast<uint64_t*>(L->dc), s);
+  int32_t* host_counts = nullptr;  // device view of the pinned landing slot
+  HIP_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&host_counts), L->host_dc, 0));
+  launch_clear_table(L->table, slot_count.as<int32_t>(), cap, L->dc, work.p, s);
   launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], m, L->hash(),
                        &L->dc->counter, slot_count.as<int32_t>(), L->vkeys, vslot.as<int32_t>(),
-                       slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->y, &L->dc->err, s);
-  HIP_TRY(hipMemcpyAsync(L->host_dc, L->dc, sizeof(DeviceCounters), hipMemcpyDeviceToHost, s));
+                       slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->y, &L->dc->err, host_counts, s);
   HIP_TRY(hipEventRecord(L->counts_ready, s));
   L->counts_known = false;
   const int32_t* n_dev = &L->dc->counter;
-  launch_count_scan(slot_count.as<int32_t>(), vslot.as<int32_t>(), n_dev, L->offsets, work.as<int32_t>(), s);
+  launch_count_scan(slot_count.as<int32_t>(), vslot.as<int32_t>(), n_dev, L->offsets, work.p, s);
   launch_fill_lists(L->hash(), slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->offsets, L->idx,
                     L->entries, L->entry_w, L->chunk_first, L->chunk, refs, s);
   if (parent)
@@ -421,7 +434,7 @@ int ensure_counts(lattice_s* L) {
   if (L->counts_known) return L->status;
   HIP_TRY(hipEventSynchronize(L->counts_ready));
   L->counts_known = true;
-  L->n = L->host_dc->counter;
+  L->n = L->host_dc->n;
   const int dev_status = status_from_err_bits(L->host_dc->err);
   if (dev_status == LAT_EHASHFULL && L->retry_cap > L->cap) {
     // table sized from an estimate overflowed: rebuild at the worst case

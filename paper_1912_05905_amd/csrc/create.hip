@@ -24,16 +24,28 @@ constexpr int kBlock = 256;
 constexpr int kLdsSlots = 2048;             // LDS table: 2x the references of a workgroup
 constexpr int kLdsPerThread = kLdsSlots / kBlock;
 
+// ---- exclusive scan of per-vertex counts over a device-side n ----
+// kScanBlocks workgroups each own a contiguous range of vertices (the count
+// of vertex v is slot_count[vslot[v]]).  Single pass: a workgroup publishes
+// the sum of its range in scan_status, adds the published sums of the
+// earlier ranges and scans its own range.
+constexpr int kScanBlocks = 256;
+constexpr uint64_t kScanReady = 1ull << 32;  // flag of a published range sum
+constexpr int kScanPer = 8;                   // consecutive vertices per thread in a scan tile
+
+// Empty hash table and zero reference counts; zero device counters and scan
+// status words for the build that follows.
 __global__ void __launch_bounds__(kBlock)
 k_clear_table(HashEntry* __restrict__ entries, int32_t* __restrict__ counts, int64_t cap,
-              uint64_t* __restrict__ dev_counters) {
+              uint4* __restrict__ dev_counters, uint64_t* __restrict__ scan_status) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
   for (int64_t e = i; e < cap; e += stride) {
     *reinterpret_cast<uint4*>(&entries[e]) = make_uint4(0xffffffffu, 0xffffffffu, 0u, 0u);
     counts[e] = 0;
   }
-  if (i == 0) *dev_counters = 0ull;
+  if (i == 0) *dev_counters = make_uint4(0u, 0u, 0u, 0u);
+  if (i < kScanBlocks) scan_status[i] = 0ull;
 }
 
 // Global insert of a key; returns its slot (or -1 when the table is full)
@@ -106,7 +118,8 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
                 float a0, float a1, float a2, int64_t m, HashView h, int32_t* counter,
                 int32_t* __restrict__ slot_count, uint64_t* __restrict__ vkeys,
                 int32_t* __restrict__ vslot, int4* __restrict__ slot_out, int4* __restrict__ rank_out,
-                float4* __restrict__ w_out, float4* __restrict__ y_out, uint32_t* err) {
+                float4* __restrict__ w_out, float4* __restrict__ y_out, uint32_t* err,
+                int32_t* __restrict__ host_counts) {
   __shared__ uint64_t lkey[kLdsSlots];
   __shared__ int32_t lcount[kLdsSlots];
   __shared__ int32_t lslot[kLdsSlots];
@@ -270,7 +283,23 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
   }
   int32_t nblock = 0;
   const int32_t my_first = block_exclusive_sum(ncreated, scan_buf, &nblock);
-  if (tid == 0) id_base = nblock > 0 ? atomicAdd(counter, nblock) : 0;
+  // One 64-bit atomic per workgroup claims the numbers of its new vertices
+  // (low word: the vertex count) and counts the workgroup as finished with
+  // its inserts (high word); the last one copies the count and the error
+  // bits into pinned host memory (read by the host after an event).  Error
+  // bits are set with atomics before this point in every workgroup.
+  if (tid == 0) {
+    const unsigned long long old =
+        __hip_atomic_fetch_add(reinterpret_cast<unsigned long long*>(counter),
+                               (1ull << 32) | static_cast<uint32_t>(nblock), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+    id_base = static_cast<int32_t>(old & 0xffffffffull);
+    if ((old >> 32) == gridDim.x - 1) {
+      host_counts[0] = id_base + nblock;
+      host_counts[1] = static_cast<int32_t>(__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      __threadfence_system();
+    }
+  }
   __syncthreads();
   int32_t id = id_base + my_first;
   for (int u = tid, j = 0; u < nunique; u += kBlock, ++j) {
@@ -296,57 +325,60 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
     rank_out[p] = make_int4(ro[0], ro[1], ro[2], ro[3]);
     w_out[p] = make_float4(b[0], b[1], b[2], b[3]);
   }
+
 }
 
-// ---- exclusive scan of per-vertex counts over a device-side n ----
-// kScanBlocks workgroups each own a contiguous range of vertices: the first
-// kernel sums each range, the second adds the sums of the earlier ranges and
-// scans its own range.  The count of vertex v is slot_count[vslot[v]].
-constexpr int kScanBlocks = 256;
-constexpr int kScanPer = 8;
-
 __global__ void __launch_bounds__(kBlock)
-k_scan_partials(const int32_t* __restrict__ slot_count, const int32_t* __restrict__ vslot,
-                const int32_t* __restrict__ n_dev, int32_t* __restrict__ sums) {
+k_scan(const int32_t* __restrict__ slot_count, const int32_t* __restrict__ vslot, const int32_t* __restrict__ n_dev,
+       uint64_t* __restrict__ status, int32_t* __restrict__ offsets) {
+  static_assert(kScanBlocks <= kBlock, "one earlier range per thread");
   __shared__ int32_t lds4[kBlock / 64];
   const int64_t n = *n_dev;
   const int64_t per = (n + kScanBlocks - 1) / kScanBlocks;
   const int64_t beg = blockIdx.x * per, end = min(beg + per, n);
   int32_t s = 0;
   for (int64_t i = beg + threadIdx.x; i < end; i += kBlock) s += slot_count[vslot[i]];
-  int32_t total;
-  block_exclusive_sum(s, lds4, &total);
-  if (threadIdx.x == 0) sums[blockIdx.x] = total;
-}
-
-__global__ void __launch_bounds__(kBlock)
-k_scan_ranges(const int32_t* __restrict__ slot_count, const int32_t* __restrict__ vslot,
-              const int32_t* __restrict__ n_dev, const int32_t* __restrict__ sums,
-              int32_t* __restrict__ offsets) {
-  __shared__ int32_t lds4[kBlock / 64];
-  const int64_t n = *n_dev;
-  const int64_t per = (n + kScanBlocks - 1) / kScanBlocks;
-  const int64_t beg = blockIdx.x * per, end = min(beg + per, n);
+  int32_t agg;
+  block_exclusive_sum(s, lds4, &agg);
+  // the status word carries the sum itself, so relaxed atomics suffice
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&status[blockIdx.x], kScanReady | static_cast<uint32_t>(agg), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  // thread j < blockIdx.x takes the sum of range j: published, or, should it
+  // not appear within a bounded wait, summed here from the counts themselves
   int32_t before = 0;
-  for (int b = threadIdx.x; b < static_cast<int>(blockIdx.x); b += kBlock) before += sums[b];
-  int32_t tmp;
-  block_exclusive_sum(before, lds4, &tmp);
-  int32_t carry = tmp;                       // sum of all earlier ranges
+  const int j = threadIdx.x;
+  if (j < static_cast<int>(blockIdx.x)) {
+    uint64_t st = 0;
+    for (int spin = 0; spin < 100000; ++spin) {
+      st = __hip_atomic_load(&status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (st & kScanReady) break;
+      __builtin_amdgcn_s_sleep(2);
+    }
+    if (st & kScanReady) {
+      before = static_cast<int32_t>(static_cast<uint32_t>(st));
+    } else {
+      const int64_t b2 = j * per, e2 = min(b2 + per, n);
+      for (int64_t i = b2; i < e2; ++i) before += slot_count[vslot[i]];
+    }
+  }
+  int32_t carry;
+  block_exclusive_sum(before, lds4, &carry);  // carry = sum of all earlier ranges
   for (int64_t t0 = beg; t0 < end; t0 += kBlock * kScanPer) {
     const int64_t base = t0 + threadIdx.x * kScanPer;
     int32_t v[kScanPer];
     int32_t loc = 0;
 #pragma unroll
-    for (int j = 0; j < kScanPer; ++j) {
-      v[j] = base + j < end ? slot_count[vslot[base + j]] : 0;
-      loc += v[j];
+    for (int q = 0; q < kScanPer; ++q) {
+      v[q] = base + q < end ? slot_count[vslot[base + q]] : 0;
+      loc += v[q];
     }
     int32_t tile_total;
     int32_t run = carry + block_exclusive_sum(loc, lds4, &tile_total);
 #pragma unroll
-    for (int j = 0; j < kScanPer; ++j) {
-      if (base + j < end) offsets[base + j] = run;
-      run += v[j];
+    for (int q = 0; q < kScanPer; ++q) {
+      if (base + q < end) offsets[base + q] = run;
+      run += v[q];
     }
     carry += tile_total;
   }
@@ -542,35 +574,35 @@ inline unsigned blocks_for(int64_t n) { return static_cast<unsigned>((n + kBlock
 
 }  // namespace
 
-void launch_clear_table(HashEntry* keys, int32_t* counts, int64_t cap, uint64_t* dev_counters,
+void launch_clear_table(HashEntry* keys, int32_t* counts, int64_t cap, void* dev_counters, void* scan_work,
                         hipStream_t s) {
   const int64_t want = (cap + kBlock * 4 - 1) / (kBlock * 4);
   const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : (want < 8192 ? want : 8192));
   ScopedKernelTimer tm("fill", s);
-  hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, s, keys, counts, cap, dev_counters);
+  hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, s, keys, counts, cap,
+                     static_cast<uint4*>(dev_counters), static_cast<uint64_t*>(scan_work));
 }
 
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
                           float a2, int64_t m, HashView h, int32_t* counter, int32_t* slot_count,
                           uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
-                          float* w_out, float* y_out, uint32_t* err, hipStream_t s) {
+                          float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, hipStream_t s) {
   if (m <= 0) return;
   ScopedKernelTimer tm("insert", s);
   hipLaunchKernelGGL(k_insert_points, dim3(blocks_for(m)), dim3(kBlock), 0, s, pos,
                      reinterpret_cast<const float4*>(y_in), y_scale, a0, a1, a2, m, h, counter,
                      slot_count, vkeys, vslot, reinterpret_cast<int4*>(slot_out),
                      reinterpret_cast<int4*>(rank_out), reinterpret_cast<float4*>(w_out),
-                     reinterpret_cast<float4*>(y_out), err);
+                     reinterpret_cast<float4*>(y_out), err, host_counts);
 }
 
-int64_t scan_workspace_elems() { return kScanBlocks; }
+int64_t scan_workspace_bytes() { return kScanBlocks * sizeof(uint64_t); }
 
 void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, const int32_t* n_dev,
-                       int32_t* offsets, int32_t* work, hipStream_t s) {
+                       int32_t* offsets, void* work, hipStream_t s) {
   ScopedKernelTimer tm("scan", s);
-  hipLaunchKernelGGL(k_scan_partials, dim3(kScanBlocks), dim3(kBlock), 0, s, slot_count, vslot, n_dev, work);
-  hipLaunchKernelGGL(k_scan_ranges, dim3(kScanBlocks), dim3(kBlock), 0, s, slot_count, vslot, n_dev, work,
-                     offsets);
+  hipLaunchKernelGGL(k_scan, dim3(kScanBlocks), dim3(kBlock), 0, s, slot_count, vslot, n_dev,
+                     static_cast<uint64_t*>(work), offsets);
 }
 
 void launch_fill_lists(HashView h, const int32_t* slot, const int32_t* rank, const float* w,

@@ -110,15 +110,15 @@ struct ScopedKernelTimer {
 
 // Launchers (each .hip file implements its own kernels' launchers).
 // create.hip
-void launch_clear_table(HashEntry* entries, int32_t* counts, int64_t cap, uint64_t* dev_counters,
+void launch_clear_table(HashEntry* entries, int32_t* counts, int64_t cap, void* dev_counters, void* scan_work,
                         hipStream_t s);
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
                           float a2, int64_t m, HashView h, int32_t* counter, int32_t* slot_count,
                           uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
-                          float* w_out, float* y_out, uint32_t* err, hipStream_t s);
-int64_t scan_workspace_elems();
+                          float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, hipStream_t s);
+int64_t scan_workspace_bytes();
 void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, const int32_t* n_dev,
-                       int32_t* offsets, int32_t* work, hipStream_t s);
+                       int32_t* offsets, void* work, hipStream_t s);
 void launch_fill_lists(HashView h, const int32_t* slot, const int32_t* rank, const float* w,
                        const int32_t* offsets, int32_t* idx, int32_t* entries, float* entry_w,
                        int32_t* chunk_first, int chunk, int64_t m4, hipStream_t s);
