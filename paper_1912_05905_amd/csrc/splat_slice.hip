@@ -66,13 +66,18 @@ template <> struct Chunk<true> {
 
 // Splat (Eq. splat) as a gather over the point lists J_v, which are stored
 // back to back (entries grouped by vertex).  The entry array is cut into
-// chunks of `chunk` entries and each chunk goes to one lane group, so
-// the work is balanced however skewed the vertex degrees are (a LiDAR vertex
-// next to the sensor can hold thousands of points).  A vertex whose list lies
-// inside one chunk is finished there; a vertex cut by chunk boundaries leaves
-// a partial sum per chunk (head: the vertex continues from the previous
-// chunk; tail: it starts here and continues), which k_splat_finish adds in
-// chunk order.  No float atomics; the summation order is fixed.
+// chunks of `chunk` entries and each chunk goes to one lane group, so the
+// work is balanced however skewed the vertex degrees are (a LiDAR vertex next
+// to the sensor can hold thousands of points).  A vertex whose list lies
+// inside one chunk is finished there.  A vertex cut by chunk boundaries
+// leaves pieces: a head piece in a chunk it continues into, a tail piece in
+// the chunk where it starts.  The G = kBlock/LPR consecutive chunks of a
+// workgroup (its span) put their pieces in LDS and the workgroup joins them
+// in chunk order: a vertex that starts and ends in the span is finished
+// there; the piece of the vertex the span starts inside and the piece of the
+// vertex that runs past its end go to global memory as the span's head and
+// tail partials, which k_splat_finish adds in span order.  No float
+// atomics; the summation order is fixed.
 template <bool BF16, int LPR, int Q>
 __device__ inline void splat_store(int32_t v, const float (&acc)[Q][Chunk<BF16>::N], float ws, int lane,
                                    int nchunk, int normalize, void* vals, int64_t ld_vals, float* wsum) {
@@ -91,6 +96,7 @@ __device__ inline void splat_store(int32_t v, const float (&acc)[Q][Chunk<BF16>:
   if (wsum && lane == 0) wsum[v] = ws;
 }
 
+// row c of a C-wide partial array (global or LDS) and its weight
 template <bool BF16, int LPR, int Q>
 __device__ inline void splat_partial(float* part, float* part_w, int64_t c, int slot,
                                      const float (&acc)[Q][Chunk<BF16>::N], float ws, int lane, int C) {
@@ -109,6 +115,34 @@ __device__ inline void splat_partial(float* part, float* part_w, int64_t c, int 
   if (lane == 0) part_w[2 * c + slot] = ws;
 }
 
+template <bool BF16, int LPR, int Q>
+__device__ inline void splat_add(float (&acc)[Q][Chunk<BF16>::N], const float* part, int64_t c, int lane, int C) {
+  using Ch = Chunk<BF16>;
+  const int nchunk = C / Ch::N;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int ch = lane + q * LPR;
+    if (ch < nchunk) {
+      const float* src = part + c * C + static_cast<int64_t>(ch) * Ch::N;
+#pragma unroll
+      for (int i = 0; i < Ch::N; i += 4) {
+        const float4 x = *reinterpret_cast<const float4*>(src + i);
+        acc[q][i] += x.x;
+        acc[q][i + 1] += x.y;
+        acc[q][i + 2] += x.z;
+        acc[q][i + 3] += x.w;
+      }
+    }
+  }
+}
+
+// LDS of k_splat_chunks: head and tail pieces of the G chunks, their weights
+// and flags.
+inline size_t splat_lds_bytes(int lpr, int C) {
+  const int G = 256 / lpr;
+  return sizeof(float) * (2 * static_cast<size_t>(G) * C + 2 * G) + sizeof(int32_t) * G;
+}
+
 template <bool BF16, int LPR, int Q, int B>
 __global__ void __launch_bounds__(kBlock)
 k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
@@ -118,123 +152,166 @@ k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
                float* __restrict__ part_head, float* __restrict__ part_tail, float* __restrict__ part_w,
                unsigned nblk) {
   using Ch = Chunk<BF16>;
+  constexpr int G = kBlock / LPR;
+  extern __shared__ __align__(16) float sm[];
+  float* sh_head = sm;                 // [G][C]
+  float* sh_tail = sm + G * C;         // [G][C]
+  float* sh_w = sm + 2 * G * C;        // [G][2]
+  int32_t* sh_flag = reinterpret_cast<int32_t*>(sh_w + 2 * G);  // bit 0 head piece, bit 1 tail piece
   const int lane = threadIdx.x & (LPR - 1);
-  const int64_t c = xcd_item<LPR>(nblk);
+  const int g = threadIdx.x / LPR;
+  // XCD-contiguous span order (see xcd_item)
+  const unsigned b = blockIdx.x;
+  const int64_t span = static_cast<int64_t>(b % 8) * ((nblk + 7) / 8) + b / 8;
+  const int64_t c0 = span * G;
+  if (c0 * chunk >= total) return;     // whole workgroup
+  const int64_t c = c0 + g;
   const int64_t s0 = c * chunk;
-  if (s0 >= total) return;
   const int64_t s1 = min(s0 + static_cast<int64_t>(chunk), total);
+  const int64_t span_end = min((c0 + G) * static_cast<int64_t>(chunk), total);
   const int nchunk = C / Ch::N;
-  int32_t v = chunk_first[c];
-  // window of list ends for the next LPR vertices
-  int32_t v_win = v;
-  int32_t win = offsets[min(static_cast<int64_t>(v) + 1 + lane, n)];
-  int32_t vb = offsets[v];
-  int32_t ve = __shfl(win, 0, LPR);
+  if (lane == 0) sh_flag[g] = 0;
+  int32_t tail_v = -1, tail_ve = 0;    // vertex of this chunk's tail piece
+  int32_t head_ve = 0;                 // end of the vertex the chunk starts inside
+  if (s0 < total) {
+    int32_t v = chunk_first[c];
+    // window of list ends for the next LPR vertices
+    int32_t v_win = v;
+    int32_t win = offsets[min(static_cast<int64_t>(v) + 1 + lane, n)];
+    int32_t vb = offsets[v];
+    int32_t ve = __shfl(win, 0, LPR);
+    head_ve = ve;
+    float acc[Q][Ch::N];
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+#pragma unroll
+      for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
+    float ws = 0.f;
+    for (int64_t s = s0; s < s1; s += B) {
+      int32_t e[B];
+      float wt[B];
+#pragma unroll
+      for (int j = 0; j < B; ++j) {
+        const bool in = s + j < s1;
+        e[j] = in ? entries[s + j] : 0;
+        wt[j] = in ? entry_w[s + j] : 0.f;
+      }
+      Ch f[B][Q];
+#pragma unroll
+      for (int j = 0; j < B; ++j)
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const int ch = lane + q * LPR;
+          if (s + j < s1 && ch < nchunk)
+            f[j][q].load(feat, static_cast<int64_t>(e[j] >> 2) * ld_feat + static_cast<int64_t>(ch) * Ch::N);
+          else
+#pragma unroll
+            for (int i = 0; i < Ch::N; ++i) f[j][q].v[i] = 0.f;
+        }
+#pragma unroll
+      for (int j = 0; j < B; ++j) {
+        if (s + j >= s1) break;
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+#pragma unroll
+          for (int i = 0; i < Ch::N; ++i) acc[q][i] += wt[j] * f[j][q].v[i];
+        ws += wt[j];
+        const int64_t nxt = s + j + 1;
+        if (nxt == ve || nxt == s1) {
+          if (vb >= s0 && ve <= s1) {
+            splat_store<BF16, LPR, Q>(v, acc, ws, lane, nchunk, normalize, vals, ld_vals, wsum);
+          } else if (vb < s0) {
+            splat_partial<BF16, LPR, Q>(sh_head, sh_w, g, 0, acc, ws, lane, C);
+            if (lane == 0) sh_flag[g] |= 1;
+          } else {
+            splat_partial<BF16, LPR, Q>(sh_tail, sh_w, g, 1, acc, ws, lane, C);
+            if (lane == 0) sh_flag[g] |= 2;
+            tail_v = v;
+            tail_ve = ve;
+          }
+#pragma unroll
+          for (int q = 0; q < Q; ++q)
+#pragma unroll
+            for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
+          ws = 0.f;
+          if (nxt == ve && nxt < s1) {
+            v += 1;
+            vb = ve;
+            if (v - v_win >= LPR) {
+              v_win = v;
+              win = offsets[min(static_cast<int64_t>(v) + 1 + lane, n)];
+            }
+            ve = __shfl(win, v - v_win, LPR);
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // join the pieces of the span in chunk order
+  float acc[Q][Ch::N];
+  if (tail_v >= 0) {
+    // vertex starting in chunk g: its tail piece, then the head pieces of the
+    // following chunks it runs into
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+#pragma unroll
+      for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
+    splat_add<BF16, LPR, Q>(acc, sh_tail, g, lane, C);
+    float ws = sh_w[2 * g + 1];
+    for (int g2 = g + 1; g2 < G && (c0 + g2) * chunk < tail_ve; ++g2) {
+      splat_add<BF16, LPR, Q>(acc, sh_head, g2, lane, C);
+      ws += sh_w[2 * g2];
+    }
+    if (tail_ve <= span_end)
+      splat_store<BF16, LPR, Q>(tail_v, acc, ws, lane, nchunk, normalize, vals, ld_vals, wsum);
+    else
+      splat_partial<BF16, LPR, Q>(part_tail, part_w, span, 1, acc, ws, lane, C);
+  }
+  if (g == 0 && (sh_flag[0] & 1)) {
+    // the vertex the span starts inside: head pieces of the chunks it covers
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+#pragma unroll
+      for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
+    float ws = 0.f;
+    for (int g2 = 0; g2 < G && (c0 + g2) * chunk < head_ve; ++g2) {
+      splat_add<BF16, LPR, Q>(acc, sh_head, g2, lane, C);
+      ws += sh_w[2 * g2];
+    }
+    splat_partial<BF16, LPR, Q>(part_head, part_w, span, 0, acc, ws, lane, C);
+  }
+}
+
+// Vertices cut by span boundaries: the span in which a vertex's list starts
+// adds its tail partial and the head partials of the following spans.
+template <bool BF16, int LPR, int Q>
+__global__ void __launch_bounds__(kBlock)
+k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ chunk_first, int64_t span_len,
+               int chunks_per_span, int64_t nspans, int C, int normalize, void* __restrict__ vals, int64_t ld_vals,
+               float* __restrict__ wsum, const float* __restrict__ part_head, const float* __restrict__ part_tail,
+               const float* __restrict__ part_w) {
+  using Ch = Chunk<BF16>;
+  const int lane = threadIdx.x & (LPR - 1);
+  const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
+  if (c + 1 >= nspans) return;
+  const int64_t s0 = c * span_len, s1 = s0 + span_len;
+  const int32_t v = chunk_first[(c + 1) * chunks_per_span];
+  const int32_t vb = offsets[v];
+  if (!(vb < s1 && vb >= s0)) return;
+  const int32_t ve = offsets[v + 1];
+  const int64_t last = (static_cast<int64_t>(ve) - 1) / span_len;
+  const int nchunk = C / Ch::N;
   float acc[Q][Ch::N];
 #pragma unroll
   for (int q = 0; q < Q; ++q)
 #pragma unroll
     for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
-  float ws = 0.f;
-  for (int64_t s = s0; s < s1; s += B) {
-    int32_t e[B];
-    float wt[B];
-#pragma unroll
-    for (int j = 0; j < B; ++j) {
-      const bool in = s + j < s1;
-      e[j] = in ? entries[s + j] : 0;
-      wt[j] = in ? entry_w[s + j] : 0.f;
-    }
-    Ch f[B][Q];
-#pragma unroll
-    for (int j = 0; j < B; ++j)
-#pragma unroll
-      for (int q = 0; q < Q; ++q) {
-        const int ch = lane + q * LPR;
-        if (s + j < s1 && ch < nchunk)
-          f[j][q].load(feat, static_cast<int64_t>(e[j] >> 2) * ld_feat + static_cast<int64_t>(ch) * Ch::N);
-        else
-#pragma unroll
-          for (int i = 0; i < Ch::N; ++i) f[j][q].v[i] = 0.f;
-      }
-#pragma unroll
-    for (int j = 0; j < B; ++j) {
-      if (s + j >= s1) break;
-#pragma unroll
-      for (int q = 0; q < Q; ++q)
-#pragma unroll
-        for (int i = 0; i < Ch::N; ++i) acc[q][i] += wt[j] * f[j][q].v[i];
-      ws += wt[j];
-      const int64_t nxt = s + j + 1;
-      if (nxt == ve || nxt == s1) {
-        if (vb >= s0 && ve <= s1)
-          splat_store<BF16, LPR, Q>(v, acc, ws, lane, nchunk, normalize, vals, ld_vals, wsum);
-        else if (vb < s0)
-          splat_partial<BF16, LPR, Q>(part_head, part_w, c, 0, acc, ws, lane, C);
-        else
-          splat_partial<BF16, LPR, Q>(part_tail, part_w, c, 1, acc, ws, lane, C);
-#pragma unroll
-        for (int q = 0; q < Q; ++q)
-#pragma unroll
-          for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
-        ws = 0.f;
-        if (nxt == ve && nxt < s1) {
-          v += 1;
-          vb = ve;
-          if (v - v_win >= LPR) {
-            v_win = v;
-            win = offsets[min(static_cast<int64_t>(v) + 1 + lane, n)];
-          }
-          ve = __shfl(win, v - v_win, LPR);
-        }
-      }
-    }
-  }
-}
-
-// Vertices cut by chunk boundaries: the chunk in which a vertex's list starts
-// adds its tail partial and the head partials of the following chunks.
-template <bool BF16, int LPR, int Q>
-__global__ void __launch_bounds__(kBlock)
-k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ chunk_first, int chunk,
-               int64_t nchunks, int C, int normalize, void* __restrict__ vals, int64_t ld_vals,
-               float* __restrict__ wsum, const float* __restrict__ part_head,
-               const float* __restrict__ part_tail, const float* __restrict__ part_w) {
-  using Ch = Chunk<BF16>;
-  const int lane = threadIdx.x & (LPR - 1);
-  const int64_t c = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / LPR;
-  if (c + 1 >= nchunks) return;
-  const int64_t s0 = c * chunk, s1 = s0 + chunk;
-  const int32_t v = chunk_first[c + 1];
-  const int32_t vb = offsets[v];
-  if (!(vb < s1 && vb >= s0)) return;
-  const int32_t ve = offsets[v + 1];
-  const int64_t last = (static_cast<int64_t>(ve) - 1) / chunk;
-  const int nchunk = C / Ch::N;
-  float acc[Q][Ch::N];
-#pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int ch = lane + q * LPR;
-#pragma unroll
-    for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
-    if (ch < nchunk) {
-      const float* src = part_tail + c * C + static_cast<int64_t>(ch) * Ch::N;
-#pragma unroll
-      for (int i = 0; i < Ch::N; ++i) acc[q][i] = src[i];
-    }
-  }
+  splat_add<BF16, LPR, Q>(acc, part_tail, c, lane, C);
   float ws = part_w[2 * c + 1];
-#pragma unroll 16
+#pragma unroll 8
   for (int64_t c2 = c + 1; c2 <= last; ++c2) {
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int ch = lane + q * LPR;
-      if (ch < nchunk) {
-        const float* src = part_head + c2 * C + static_cast<int64_t>(ch) * Ch::N;
-#pragma unroll
-        for (int i = 0; i < Ch::N; ++i) acc[q][i] += src[i];
-      }
-    }
+    splat_add<BF16, LPR, Q>(acc, part_head, c2, lane, C);
     ws += part_w[2 * c2];
   }
   splat_store<BF16, LPR, Q>(v, acc, ws, lane, nchunk, normalize, vals, ld_vals, wsum);
@@ -373,14 +450,23 @@ void splat_launch(const int32_t* off, const int32_t* ent, const float* ew, const
                   const void* feat, int64_t ldf, int C, int norm, void* vals, int64_t ldv, float* wsum,
                   float* ph, float* pt, float* pw, hipStream_t s) {
   constexpr int B = (BF16 ? 8 : 16) / Q;
-  const int64_t nchunks = (total + chunk - 1) / chunk;
-  const unsigned nblk = grid_for(nchunks, LPR);
-  const dim3 g(nblk), b(kBlock);
-  hipLaunchKernelGGL((k_splat_chunks<BF16, LPR, Q, B>), dim3(xcd_grid(nblk)), b, 0, s, off, ent, ew, cf, chunk, n,
-                     total, feat, ldf, C, norm, vals, ldv, wsum, ph, pt, pw, nblk);
-  if (nchunks > 1)
-    hipLaunchKernelGGL((k_splat_finish<BF16, LPR, Q>), g, b, 0, s, off, cf, chunk, nchunks, C, norm, vals, ldv,
-                       wsum, ph, pt, pw);
+  constexpr int G = kBlock / LPR;
+  const int64_t span_len = static_cast<int64_t>(G) * chunk;
+  const int64_t nspans = (total + span_len - 1) / span_len;
+  const unsigned nblk = static_cast<unsigned>(nspans);
+  const size_t lds = splat_lds_bytes(LPR, C);
+  static bool lds_limit_set = false;
+  if (!lds_limit_set) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_splat_chunks<BF16, LPR, Q, B>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              static_cast<int>(splat_lds_bytes(LPR, LPR * Q * Chunk<BF16>::N)));
+    lds_limit_set = true;
+  }
+  hipLaunchKernelGGL((k_splat_chunks<BF16, LPR, Q, B>), dim3(xcd_grid(nblk)), dim3(kBlock), lds, s, off, ent, ew, cf,
+                     chunk, n, total, feat, ldf, C, norm, vals, ldv, wsum, ph, pt, pw, nblk);
+  if (nspans > 1)
+    hipLaunchKernelGGL((k_splat_finish<BF16, LPR, Q>), dim3(grid_for(nspans, LPR)), dim3(kBlock), 0, s, off, cf,
+                       span_len, G, nspans, C, norm, vals, ldv, wsum, ph, pt, pw);
 }
 
 template <bool BF16>
@@ -439,9 +525,13 @@ void deform_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, con
 int splat_max_channels(bool bf16) { return (bf16 ? 8 : 4) * 64 * 4; }
 int deform_max_channels(bool bf16) { return (bf16 ? 8 : 4) * 64 * 2; }
 
+// Partials of k_splat_chunks: a head and a tail row of C floats and two
+// weights per span of kBlock/LPR chunks (sized for the smallest span, LPR =
+// 64, whatever the channel count).
 int64_t splat_partial_floats(int64_t total, int chunk, int C) {
-  const int64_t nchunks = (total + chunk - 1) / chunk;
-  return nchunks * (2 * static_cast<int64_t>(C) + 2);
+  const int64_t span_len = static_cast<int64_t>(kBlock / 64) * chunk;
+  const int64_t nspans = (total + span_len - 1) / span_len;
+  return nspans * (2 * static_cast<int64_t>(C) + 2);
 }
 
 void launch_splat(const int32_t* offsets, const int32_t* entries, const float* entry_w,
@@ -452,10 +542,11 @@ void launch_splat(const int32_t* offsets, const int32_t* entries, const float* e
   const int chunks = C / (bf16 ? 8 : 4);
   const int lpr = lanes_per_row(C, bf16 != 0);
   const int q = chunks <= lpr ? 1 : (chunks <= 2 * lpr ? 2 : 4);
-  const int64_t nchunks = (total + chunk - 1) / chunk;
+  const int64_t span_len = static_cast<int64_t>(kBlock / lpr) * chunk;
+  const int64_t nspans = (total + span_len - 1) / span_len;
   float* ph = partials;
-  float* pt = partials + nchunks * C;
-  float* pw = partials + 2 * nchunks * C;
+  float* pt = partials + nspans * C;
+  float* pw = partials + 2 * nspans * C;
   ScopedKernelTimer tm("splat", s);
   if (bf16) splat_dispatch<true>(lpr, q, offsets, entries, entry_w, chunk_first, chunk, n, total, feat, ld_feat, C, normalize, vals, ld_vals, wsum, ph, pt, pw, s);
   else splat_dispatch<false>(lpr, q, offsets, entries, entry_w, chunk_first, chunk, n, total, feat, ld_feat, C, normalize, vals, ld_vals, wsum, ph, pt, pw, s);

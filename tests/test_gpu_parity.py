@@ -189,6 +189,30 @@ def test_splat(L, O, C, normalize):
     P.assert_close(P.rows_in_oracle_order(_host(ws), g2o), ow, P.TOL_F32, "wsum")
 
 
+@pytest.mark.parametrize("C,dtype", [(4, "f32"), (36, "f32"), (64, "f32"), (256, "f32"), (64, "bf16"),
+                                     (512, "bf16")])
+def test_splat_skewed(L, O, C, dtype):
+    """Vertex lists far longer than a workgroup span (a 6000-point clump
+    inside one simplex), next to short ones and a ragged end."""
+    rng = np.random.default_rng(C)
+    clump = (np.array([0.31, 0.42, 0.53]) + 1e-4 * rng.random((6000, 3))).astype(np.float32)
+    spread = rng.random((3001, 3)).astype(np.float32)
+    pos = np.concatenate([spread[:1500], clump, spread[1500:]]).astype(np.float32)
+    gl, ol, g2o = _pair(L, O, pos, 0.05)
+    F = rng.normal(size=(pos.shape[0], C)).astype(np.float32)
+    if dtype == "bf16":
+        F = O.round_bf16(F).astype(np.float32)
+        gx = gl.splat(_dev(F, torch.bfloat16))
+        ox, _ = ol.splat(F.astype(np.float64))
+        P.assert_close(P.rows_in_oracle_order(_host(gx), g2o), O.round_bf16(ox), P.TOL_BF16, "skewed splat bf16")
+    else:
+        ws = torch.empty(gl.n, device="cuda")
+        gx = gl.splat(_dev(F), wsum=ws)
+        ox, ow = ol.splat(F.astype(np.float64))
+        P.assert_close(P.rows_in_oracle_order(_host(gx), g2o), ox, P.TOL_F32, "skewed splat")
+        P.assert_close(P.rows_in_oracle_order(_host(ws), g2o), ow, P.TOL_F32, "skewed wsum")
+
+
 def test_splat_bf16(L, O):
     pos = _cloud(31, 9000, 0.7)
     gl, ol, g2o = _pair(L, O, pos, 0.06)
