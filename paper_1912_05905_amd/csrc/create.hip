@@ -502,54 +502,65 @@ k_coarse_tables(HashView hc, HashView hf, const uint64_t* __restrict__ ckeys, co
 // depends on scheduling; the convolution's result for a row does not.
 constexpr int kOrderRange = 4096;
 
-__global__ void __launch_bounds__(kBlock)
+constexpr int kOrderThreads = 1024;
+
+__global__ void __launch_bounds__(kOrderThreads)
 k_mask_order(const int32_t* __restrict__ nbr, int64_t ldn, const int32_t* __restrict__ n_dev,
              int32_t* __restrict__ rows) {
   __shared__ int32_t hist[kMaskBins];
-  __shared__ int32_t start[kMaskBins];
-  __shared__ int32_t lds4[kBlock / 64];
+  __shared__ int32_t wave_sum[kMaskBins / 64];
   __shared__ uint16_t mk[kOrderRange];
   __shared__ uint16_t rk[kOrderRange];
-  static_assert(kMaskBins == 2 * kBlock, "two bins per thread");
-  constexpr int kBatch = 4;  // rows per thread whose table entries are loaded together
-  static_assert(kOrderRange % (kBatch * kBlock) == 0, "whole batches");
+  constexpr int kPer = kOrderRange / kOrderThreads;  // rows per thread, loaded together
+  static_assert(kMaskBins <= kOrderThreads, "one bin per thread");
+  const int tid = threadIdx.x;
   const int64_t n = *n_dev;
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kOrderRange;
   if (r0 >= n) return;
   const int cnt = static_cast<int>(n - r0 < kOrderRange ? n - r0 : kOrderRange);
-  hist[2 * threadIdx.x] = 0;
-  hist[2 * threadIdx.x + 1] = 0;
+  if (tid < kMaskBins) hist[tid] = 0;
   __syncthreads();
-  for (int i0 = 0; i0 < cnt; i0 += kBatch * kBlock) {
-    int m[kBatch];
+  int m[kPer];
 #pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int i = i0 + b * kBlock + threadIdx.x;
-      m[b] = 0;
-      if (i < cnt) {
+  for (int b = 0; b < kPer; ++b) {
+    const int i = b * kOrderThreads + tid;
+    m[b] = 0;
+    if (i < cnt) {
 #pragma unroll
-        for (int t = 0; t < kTaps; ++t)
-          if (nbr[static_cast<int64_t>(t) * ldn + r0 + i] >= 0) m[b] |= 1 << t;
-      }
+      for (int t = 0; t < kTaps; ++t)
+        if (nbr[static_cast<int64_t>(t) * ldn + r0 + i] >= 0) m[b] |= 1 << t;
     }
+  }
 #pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int i = i0 + b * kBlock + threadIdx.x;
-      if (i < cnt) {
-        mk[i] = static_cast<uint16_t>(m[b]);
-        rk[i] = static_cast<uint16_t>(atomicAdd(&hist[m[b]], 1));
-      }
+  for (int b = 0; b < kPer; ++b) {
+    const int i = b * kOrderThreads + tid;
+    if (i < cnt) {
+      mk[i] = static_cast<uint16_t>(m[b]);
+      rk[i] = static_cast<uint16_t>(atomicAdd(&hist[m[b]], 1));
     }
   }
   __syncthreads();
-  const int32_t b0 = hist[2 * threadIdx.x], b1 = hist[2 * threadIdx.x + 1];
-  int32_t total;
-  const int32_t ex = block_exclusive_sum(b0 + b1, lds4, &total);
-  start[2 * threadIdx.x] = ex;
-  start[2 * threadIdx.x + 1] = ex + b0;
+  // exclusive scan of the 512 bins, one per thread of the first 512
+  const int lane = tid & 63, wave = tid >> 6;
+  int32_t x = tid < kMaskBins ? hist[tid] : 0;
+  const int32_t own = x;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int32_t y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  if (tid < kMaskBins && lane == 63) wave_sum[wave] = x;
   __syncthreads();
-  for (int i = threadIdx.x; i < cnt; i += kBlock)
-    rows[r0 + start[mk[i]] + rk[i]] = static_cast<int32_t>(r0 + i);
+  int32_t before = 0;
+  for (int w = 0; w < wave && w < kMaskBins / 64; ++w) before += wave_sum[w];
+  __syncthreads();
+  if (tid < kMaskBins) hist[tid] = before + x - own;  // now the start of each mask
+  __syncthreads();
+#pragma unroll
+  for (int b = 0; b < kPer; ++b) {
+    const int i = b * kOrderThreads + tid;
+    if (i < cnt) rows[r0 + hist[mk[i]] + rk[i]] = static_cast<int32_t>(r0 + i);
+  }
 }
 
 __global__ void __launch_bounds__(kBlock)
@@ -636,7 +647,7 @@ void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse
   hipLaunchKernelGGL(k_coarse_tables, dim3(stride_grid((2 * nc_max + nf_max) * kTaps)), dim3(kBlock), 0, s, coarse,
                      fine, coarse_keys, fine_keys, nc_dev, nf_dev, nbr, down, nc_max, up, nf_max);
   hipLaunchKernelGGL(k_mask_order, dim3(static_cast<unsigned>((nf_max + kOrderRange - 1) / kOrderRange)),
-                     dim3(kBlock), 0, s, up, nf_max, nf_dev, up_rows);
+                     dim3(kOrderThreads), 0, s, up, nf_max, nf_dev, up_rows);
 }
 
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s) {

@@ -113,11 +113,21 @@ class Lattice:
     def __init__(self, handle: C.c_void_p, parent: "Lattice | None" = None):
         self._h = handle
         self.parent = parent
-        n, m, lv = C.c_int64(), C.c_int64(), C.c_int()
-        _check(lib().lattice_num_vertices(handle, C.byref(n)))
+        self._n = None
+        m, lv = C.c_int64(), C.c_int()
         _check(lib().lattice_num_points(handle, C.byref(m)))
         _check(lib().lattice_level(handle, C.byref(lv)))
-        self.n, self.m, self.level = int(n.value), int(m.value), int(lv.value)
+        self.m, self.level = int(m.value), int(lv.value)
+
+    @property
+    def n(self) -> int:
+        """Vertex count; the first read waits for the lattice's build to
+        report it (and raises a device-side build error)."""
+        if self._n is None:
+            n = C.c_int64()
+            _check(lib().lattice_num_vertices(self._h, C.byref(n)))
+            self._n = int(n.value)
+        return self._n
 
     # ---- construction ----
     @classmethod

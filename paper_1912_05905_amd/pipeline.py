@@ -27,25 +27,44 @@ class GpuPipeline:
         self.vectors = {k: (torch.from_numpy(np.ascontiguousarray(v)).cuda(), float(beta))
                         for k, (v, beta) in wl.vectors.items()}
         self.sigma = [float(s) for s in wl.sigma]
+        self._store: dict[str, torch.Tensor] = {}
 
     def _view(self, bufs, levels, spec):
         name, c0, cc = spec
         if name not in bufs:
             lv, total = self.wl.buffers[name]
-            bufs[name] = torch.empty((levels[lv].n, total), dtype=self.dtype, device="cuda")
+            n = levels[lv].n
+            # device buffers are kept across steps (same stream, so a step's
+            # kernels finish with a buffer before the next step's reuse it)
+            store = self._store.get(name)
+            if store is None or store.shape[0] < n:
+                store = torch.empty((n, total), dtype=self.dtype, device="cuda")
+                self._store[name] = store
+            bufs[name] = store[:n]
         return bufs[name][:, c0:c0 + cc]
 
     def step(self, keep=False):
-        """One pass of the pipeline.  Returns (levels, buffers, point outputs)."""
+        """One pass of the pipeline.  Returns (levels, buffers, point outputs).
+
+        The lattice hierarchy (create, coarsen) is issued first: a coarse
+        level depends only on the positions, and issuing every build before
+        the feature operations keeps the device busy while the host waits
+        for vertex counts.  With keep=True the buffers are fresh tensors
+        that later steps do not overwrite."""
         levels: dict[int, Lattice] = {}
         bufs: dict[str, torch.Tensor] = {}
         outs: dict[str, torch.Tensor] = {}
+        if keep:
+            self._store = {}
+        for op in self.wl.ops:
+            if op["op"] == "create":
+                levels[0] = Lattice.create(self.pos, self.sigma)
+            elif op["op"] == "coarsen":
+                levels[op["level"]] = levels[op["level"] - 1].coarsen()
         for op in self.wl.ops:
             kind = op["op"]
-            if kind == "create":
-                levels[0] = Lattice.create(self.pos, self.sigma)
-            elif kind == "coarsen":
-                levels[op["level"]] = levels[op["level"] - 1].coarsen()
+            if kind in ("create", "coarsen"):
+                continue
             elif kind == "splat":
                 levels[0].splat(self.feat, normalize=bool(op["normalize"]),
                                 out=self._view(bufs, levels, op["dst"]))
@@ -68,6 +87,8 @@ class GpuPipeline:
                     self._view(bufs, levels, op["src"]), wv, beta)
             else:
                 raise ValueError(f"unknown op {kind}")
+        if keep:
+            self._store = {}
         return levels, bufs, outs
 
     @staticmethod
