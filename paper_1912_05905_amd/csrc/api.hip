@@ -532,7 +532,7 @@ int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, 
                static_cast<size_t>((n_out - 1) * ld_out + Cout) * u))
     return fail(LAT_EINVAL, "in and out overlap");
   if (n_out == 0) return LAT_OK;
-  launch_conv(table, ldn, n_out, in, ld_in, Cin, W, bias, Cout, dt == LAT_BF16, flags & LAT_RELU, out,
+  launch_conv(table, ldn, n_out, n_in, in, ld_in, Cin, W, bias, Cout, dt == LAT_BF16, flags & LAT_RELU, out,
               ld_out, rows, s);
   return check_launch("conv");
 }

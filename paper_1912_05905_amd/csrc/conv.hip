@@ -36,6 +36,13 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kWaves = 4;
 constexpr int kBlock = 64 * kWaves;
 
+// Buffer resource word 3 for raw (untyped) buffer loads on CDNA, and an
+// offset beyond any buffer the kernels build (at most kMaxBufferBytes), for
+// which a buffer load returns zeros without a memory access.
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kOutOfRange = static_cast<int>(0x80000000u);
+constexpr int64_t kMaxBufferBytes = (int64_t{1} << 31) - 64;
+
 __device__ inline uint16_t f32_to_bf16(float f) {
   const uint32_t u = __float_as_uint(f);
   if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
@@ -222,12 +229,12 @@ struct LdsConv {
   static_assert(A_PER_T >= 1 && BM * CPR % kBlock == 0, "A copy split");
 };
 
-template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS>
+template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS, bool BUF, int SCHED>
 __global__ void __launch_bounds__(kBlock)
 k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const void* __restrict__ in,
            int64_t ld_in, int Cin, const void* __restrict__ W, const float* __restrict__ bias, int Cout,
            int relu, void* __restrict__ out, int64_t ld_out, const int32_t* __restrict__ rows,
-           unsigned row_tiles, int splits, float* __restrict__ part) {
+           unsigned row_tiles, int splits, float* __restrict__ part, uint32_t in_bytes, uint32_t w_bytes) {
   using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
   using E = typename std::conditional<BF16, uint16_t, float>::type;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -279,13 +286,34 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   const int kc_steps = (Cin + P::KC - 1) / P::KC;
   const int stages = tlist[15] * kc_steps;
 
-  // global -> register copies of one stage
+  // global -> register copies of one stage.  Every load is issued, also for
+  // a missing neighbour, a channel past Cin or a stage past the last: with
+  // buffer loads (BUF) such a load gets an offset beyond the buffer and
+  // reads zeros without touching memory; otherwise it reads a valid address
+  // and the value is replaced by zeros.  With no load skipped, the number of
+  // loads in flight is known, and the wait before a stage is copied to LDS
+  // covers that stage's loads only, not the ones issued after it.
   using V = uint4;
   V ra[NS][P::A_PER_T], rb[NS][P::B_PER_T];
+  // (unused without BUF, where the byte counts are 0)
+  const __amdgpu_buffer_rsrc_t rin =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(in), 0, static_cast<int>(in_bytes), kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rw =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(W), 0, static_cast<int>(w_bytes), kRsrcWord3);
+  auto load16 = [&](const __amdgpu_buffer_rsrc_t& rs, const void* base, int64_t elem, bool ok) -> V {
+    if constexpr (BUF) {
+      const int off = ok ? static_cast<int>(elem * static_cast<int64_t>(sizeof(E))) : kOutOfRange;
+      return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+    } else {
+      const V x = *reinterpret_cast<const V*>(static_cast<const E*>(base) + (ok ? elem : 0));
+      return ok ? x : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
   auto fetch = [&](auto set_c, int st) {
     constexpr int set = decltype(set_c)::value;
-    const int ti = st / kc_steps;
-    const int t = tlist[ti];
+    const bool live = st < stages;
+    const int ti = min(st / kc_steps, 15);
+    const int t = live ? tlist[ti] : 0;
     const int kc = (st - ti * kc_steps) * P::KC;
 #pragma unroll
     for (int j = 0; j < P::A_PER_T; ++j) {
@@ -293,9 +321,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
       const int r = q / P::CPR, cc = q % P::CPR;
       const int ch = kc + cc * P::EPC;
       const int32_t nb = nbt[t * BM + r];
-      ra[set][j] = (nb >= 0 && ch < Cin)
-                  ? *reinterpret_cast<const V*>(static_cast<const E*>(in) + static_cast<int64_t>(nb) * ld_in + ch)
-                  : make_uint4(0u, 0u, 0u, 0u);
+      ra[set][j] = load16(rin, in, static_cast<int64_t>(nb) * ld_in + ch, live && nb >= 0 && ch < Cin);
     }
 #pragma unroll
     for (int j = 0; j < P::B_PER_T; ++j) {
@@ -303,10 +329,8 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
       const int r = q / P::CPR, cc = q % P::CPR;
       const int ch = kc + cc * P::EPC;
       const int col = col0 + r;
-      rb[set][j] = (q < BN * P::CPR && col < Cout && ch < Cin)
-                  ? *reinterpret_cast<const V*>(static_cast<const E*>(W) +
-                                                (static_cast<int64_t>(tb + t) * Cout + col) * Cin + ch)
-                  : make_uint4(0u, 0u, 0u, 0u);
+      rb[set][j] = load16(rw, W, (static_cast<int64_t>(tb + t) * Cout + col) * Cin + ch,
+                          live && q < BN * P::CPR && col < Cout && ch < Cin);
     }
   };
   auto stash = [&](auto set_c, int buf) {
@@ -341,29 +365,40 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   // buffer and stage st+NS is loaded into the set that stage st vacated, so
   // a load has NS-1 steps to arrive.  Set indices are compile-time constants
   // so that the register sets stay in registers.
-  static_for<NS>([&](auto i_c) {
-    if (decltype(i_c)::value < stages) fetch(i_c, decltype(i_c)::value);
-  });
-  if (stages > 0) stash(std::integral_constant<int, 0>{}, 0);
+  static_for<NS>([&](auto i_c) { fetch(i_c, decltype(i_c)::value); });
+  stash(std::integral_constant<int, 0>{}, 0);
   __syncthreads();
+  // One pipeline step: stage st is multiplied from LDS buffer st & 1; stage
+  // st+1 goes from its register set to the other buffer and stage st+NS is
+  // loaded into the set stage st vacated.  With SCHED 1 the copy and the
+  // loads come first, so that they overlap the multiply.  All fragments of
+  // the stage are read from LDS before the first MFMA.
   auto step = [&](auto set_c, int st) {
     constexpr int SET = decltype(set_c)::value;
     constexpr int NEXT = (SET + 1) % NS;
     const int buf = st & 1;
+    if constexpr (SCHED == 1) {
+      stash(std::integral_constant<int, NEXT>{}, buf ^ 1);
+      fetch(set_c, st + NS);
+    }
     const E* a = As + buf * (BM * P::LDR) + (wm * P::RM * 16 + li) * P::LDR + lg * P::EPL;
     const E* bb = Bs + buf * (BN * P::LDR) + (wn * P::RN * 16 + li) * P::LDR + lg * P::EPL;
+    constexpr int NK = P::KC / P::KS;
+    Frag<BF16> fa[NK][P::RM], fb[NK][P::RN];
 #pragma unroll
-    for (int k = 0; k < P::KC; k += P::KS) {
-      Frag<BF16> fa[P::RM], fb[P::RN];
+    for (int k = 0; k < NK; ++k) {
 #pragma unroll
-      for (int i = 0; i < P::RM; ++i) fa[i].load(a, i * 16 * P::LDR + k);
+      for (int i = 0; i < P::RM; ++i) fa[k][i].load(a, i * 16 * P::LDR + k * P::KS);
 #pragma unroll
-      for (int j = 0; j < P::RN; ++j) fb[j].load(bb, j * 16 * P::LDR + k);
+      for (int j = 0; j < P::RN; ++j) fb[k][j].load(bb, j * 16 * P::LDR + k * P::KS);
+    }
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
       if constexpr (BF16) {
 #pragma unroll
         for (int i = 0; i < P::RM; ++i)
 #pragma unroll
-          for (int j = 0; j < P::RN; ++j) mma(acc[i][j], fa[i], fb[j]);
+          for (int j = 0; j < P::RN; ++j) mma(acc[i][j], fa[k][i], fb[k][j]);
       } else {
         // interleave independent accumulators between dependent MFMAs
 #pragma unroll
@@ -372,17 +407,23 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
           for (int i = 0; i < P::RM; ++i)
 #pragma unroll
             for (int j = 0; j < P::RN; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i].v[e], fb[j].v[e], acc[i][j], 0, 0, 0);
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[k][i].v[e], fb[k][j].v[e], acc[i][j], 0, 0, 0);
       }
     }
-    if (st + 1 < stages) stash(std::integral_constant<int, NEXT>{}, buf ^ 1);
-    if (st + NS < stages) fetch(set_c, st + NS);
+    if constexpr (SCHED == 0) {
+      // unconditional: past the last stage these copy and load zeros
+      stash(std::integral_constant<int, NEXT>{}, buf ^ 1);
+      fetch(set_c, st + NS);
+    }
     __syncthreads();
   };
-  for (int st = 0; st < stages; st += NS)
-    static_for<NS>([&](auto i_c) {
-      if (st + decltype(i_c)::value < stages) step(i_c, st + decltype(i_c)::value);
-    });
+  // whole groups of NS steps without branches, then the remaining steps
+  int st = 0;
+  for (; st + NS <= stages; st += NS)
+    static_for<NS>([&](auto i_c) { step(i_c, st + decltype(i_c)::value); });
+  static_for<NS>([&](auto i_c) {
+    if (st + decltype(i_c)::value < stages) step(i_c, st + decltype(i_c)::value);
+  });
 
   if (part) {
     // raw partial sums of this split, [split][n_out][Cout]
@@ -455,24 +496,32 @@ k_conv_reduce(const float* __restrict__ part, int splits, int64_t n_out, int Cou
   }
 }
 
-template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS = 2>
+// Byte extents of the gathered operands, for the buffer resources.
+struct ConvExtent {
+  int64_t in_bytes, w_bytes;
+  bool buffer_ok() const { return in_bytes <= kMaxBufferBytes && w_bytes <= kMaxBufferBytes; }
+};
+
+template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS = 2, bool BUF = true, int SCHED = 0>
 void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                      int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
-                     int64_t ld_out, const int32_t* rows, hipStream_t s, int splits = 1, float* part = nullptr) {
+                     int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s, int splits = 1,
+                     float* part = nullptr) {
   using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
   if (rows) splits = 1;  // partial sums are kept in permuted row order
   static bool lds_limit_set = false;
   if (!lds_limit_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, P::LDS_BYTES);
     lds_limit_set = true;
   }
   const int64_t tiles = (n_out + BM - 1) / BM;
   const unsigned per_xcd = static_cast<unsigned>((tiles + 7) / 8);
   const dim3 grid(per_xcd * 8, static_cast<unsigned>((Cout + BN - 1) / BN), static_cast<unsigned>(splits));
-  hipLaunchKernelGGL((k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS>), grid, dim3(kBlock), P::LDS_BYTES, s, nbr, ldn,
-                     n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, static_cast<unsigned>(tiles),
-                     splits, splits > 1 ? part : nullptr);
+  hipLaunchKernelGGL((k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED>), grid, dim3(kBlock), P::LDS_BYTES, s, nbr,
+                     ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows,
+                     static_cast<unsigned>(tiles), splits, splits > 1 ? part : nullptr,
+                     static_cast<uint32_t>(BUF ? ext.in_bytes : 0), static_cast<uint32_t>(BUF ? ext.w_bytes : 0));
   if (splits > 1) {
     const int64_t quads = n_out * (Cout / 4);
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((quads + kBlock - 1) / kBlock, 8192));
@@ -485,49 +534,58 @@ int64_t blocks_of(int64_t n_out, int Cout, int rows, int cols) {
   return ((n_out + rows - 1) / rows) * ((Cout + cols - 1) / cols);
 }
 
-// Tile choice, from a sweep of tile shapes and pipeline depths over the
-// lattices of the LiDAR scan (fp32) and of the 1M-point room (bf16) on
-// MI355X.  fp32: small tiles win; the gathered A operand, not the matrix
-// cores, sets the pace, and the levels are small.  bf16: 128 x 128 tiles
-// halve the gathered bytes per flop and win once there are enough of them
-// (wide layers on large levels); 64 x 64 otherwise.
+// Tile choice, from a sweep of tile shapes, pipeline depths and step
+// schedules over the lattices of the LiDAR scan (fp32) and of the 1M-point
+// room (bf16) on MI355X.  fp32: small tiles win; the levels are small and a
+// stage costs several times its MFMA time.  bf16: 128 x 128 tiles halve the
+// gathered bytes per flop and win once there are enough of them (wide
+// layers, large levels); 64 x 64 otherwise.
 template <bool BF16>
 void conv_dispatch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                    int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
-                   int64_t ld_out, const int32_t* rows, hipStream_t s) {
+                   int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s) {
   if (Cout <= 16)
     return conv_launch<BF16, 1, 1, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, s);
+  if (!ext.buffer_ok())  // operands beyond the reach of a buffer resource
+    return conv_lds_launch<BF16, 64, 64, 2, 2, 128, 2, false>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu,
+                                                               out, ld_out, rows, ext, s);
   if constexpr (BF16) {
     const int64_t b128 = blocks_of(n_out, Cout, 128, 128);
-    if (Cout % 128 == 0 && (b128 >= 1500 || (Cin >= 256 && b128 >= 400)))
-      return conv_lds_launch<true, 128, 128, 2, 2, 64, 3>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
-                                                          ld_out, rows, s);
-    if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= 256)
-      return conv_lds_launch<true, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
-                                                      ld_out, rows, s);
+    const int64_t b64 = blocks_of(n_out, Cout, 64, 64);
+    if (Cout >= 128 && (b128 >= 1500 || (Cin >= 256 && Cout % 128 == 0)))
+      return conv_lds_launch<true, 128, 128, 2, 2, 64, 3, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
+                                                                   relu, out, ld_out, rows, ext, s);
+    if (Cout > 32 && b64 >= 8192)
+      return conv_lds_launch<true, 64, 64, 2, 2, 128, 3, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
+                                                                  relu, out, ld_out, rows, ext, s);
+    if (Cout > 32 && b64 >= 256)
+      return conv_lds_launch<true, 64, 64, 2, 2, 128, 2, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
+                                                                  relu, out, ld_out, rows, ext, s);
     return conv_lds_launch<true, 32, 32, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
-                                                    ld_out, rows, s);
+                                                    ld_out, rows, ext, s);
   } else {
     if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= 2048)
-      return conv_lds_launch<false, 64, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
-                                                       ld_out, rows, s);
+      return conv_lds_launch<false, 64, 64, 2, 2, 128, 3, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
+                                                                   relu, out, ld_out, rows, ext, s);
     if (Cout > 64 && blocks_of(n_out, Cout, 32, 64) >= 1024)
-      return conv_lds_launch<false, 32, 64, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
-                                                       ld_out, rows, s);
-    return conv_lds_launch<false, 32, 32, 2, 2, 256>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
-                                                     ld_out, rows, s);
+      return conv_lds_launch<false, 32, 64, 2, 2, 128, 3, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
+                                                                   relu, out, ld_out, rows, ext, s);
+    return conv_lds_launch<false, 32, 32, 2, 2, 256, 2, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
+                                                                 relu, out, ld_out, rows, ext, s);
   }
 }
 
 }  // namespace
 
-void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
+void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
                  int64_t ld_out, const int32_t* rows, hipStream_t s) {
   if (n_out <= 0) return;
   ScopedKernelTimer tm("conv", s);
-  if (bf16) conv_dispatch<true>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, s);
-  else conv_dispatch<false>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, s);
+  const int64_t u = bf16 ? 2 : 4;
+  const ConvExtent ext{n_in > 0 ? ((n_in - 1) * ld_in + Cin) * u : 0, int64_t{kTaps} * Cout * Cin * u};
+  if (bf16) conv_dispatch<true>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s);
+  else conv_dispatch<false>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s);
 }
 
 }  // namespace lat

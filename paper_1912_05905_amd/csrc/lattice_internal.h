@@ -141,7 +141,7 @@ void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const vo
                          int64_t ld_vals, int C, int bf16, const float* wv, float beta, float* out,
                          float* delta, hipStream_t s);
 // conv.hip
-void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
+void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
                  int64_t ld_out, const int32_t* rows, hipStream_t s);
 

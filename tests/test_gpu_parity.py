@@ -248,6 +248,25 @@ def test_conv_fp32(L, O, cin, cout):
         P.assert_close(P.rows_in_oracle_order(_host(gy), g2o), oy, P.TOL_F32, f"conv {cin}->{cout}")
 
 
+def test_conv_input_beyond_buffer_reach(L, O):
+    """An input whose rows span more than 2 GiB (a wide row stride) takes the
+    convolution path without buffer resources."""
+    pos = _cloud(77, 3000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.07)
+    cin = cout = 64
+    ld = ((2**31 // (4 * max(ol.n - 1, 1)) + 64) // 8) * 8
+    assert (ol.n - 1) * ld * 4 > 2**31
+    rng = np.random.default_rng(77)
+    X = rng.normal(size=(ol.n, cin)).astype(np.float32)
+    W = _rand_w(rng, cin, cout, 1.0 / np.sqrt(9 * cin))
+    big = torch.empty((ol.n, ld), dtype=torch.float32, device="cuda")
+    big[:, :cin] = _dev(X[g2o])
+    gy = gl.conv(gl, big[:, :cin], _gpu_w(W), relu=True)
+    del big
+    oy = ol.conv(ol, X.astype(np.float64), W.astype(np.float64), relu=True)
+    P.assert_close(P.rows_in_oracle_order(_host(gy), g2o), oy, P.TOL_F32, "conv, 2 GiB input")
+
+
 @pytest.mark.parametrize("cin,cout", [(64, 64), (8, 24), (128, 192), (384, 192), (256, 256)])
 def test_conv_bf16(L, O, cin, cout):
     pos = _cloud(50 + cin, 6000, 0.8)
