@@ -26,8 +26,8 @@ PEAK = {"hbm": 8.0e12, "mfma_f32": 157.3e12, "mfma_bf16": 2.5e15}
 FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "conv", "slice", "deform_slice"]
 # kernel symbol fragments of each family (rocprofv3 kernel names)
 FAMILY_KERNELS = {
-    "fill": ["k_clear_table"], "insert": ["k_insert_points"], "scan": ["k_scan_partials", "k_scan_ranges"],
-    "lists": ["k_fill_lists"], "nbr": ["k_neighbor_table", "k_down_table", "k_up_table"],
+    "fill": ["k_clear_table"], "insert": ["k_insert_points"], "scan": ["k_scan("],
+    "lists": ["k_fill_lists"], "nbr": ["k_neighbor_table", "k_coarse_tables", "k_mask_order"],
     "splat": ["k_splat_chunks", "k_splat_finish"], "conv": ["k_conv"], "slice": ["k_slice<"],
     "deform_slice": ["k_deform_slice"],
 }
