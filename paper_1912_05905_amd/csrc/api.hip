@@ -5,6 +5,7 @@
 #include <cstddef>
 #include <cstdio>
 #include <cstring>
+#include <deque>
 #include <map>
 #include <mutex>
 #include <string>
@@ -135,12 +136,11 @@ struct TimerFamily {
   bool enabled = false;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> recorded;
   std::vector<hipEvent_t> spare;
-  hipEvent_t pending = nullptr;
 };
 
 std::mutex g_timer_mu;
-std::vector<TimerFamily>& timer_families() {
-  static auto* v = new std::vector<TimerFamily>();
+std::deque<TimerFamily>& timer_families() {
+  static auto* v = new std::deque<TimerFamily>();  // stable element addresses
   return *v;
 }
 bool g_any_timer = false;
@@ -161,8 +161,10 @@ hipEvent_t take_event(TimerFamily* f) {
     f->spare.pop_back();
     return e;
   }
+  // timing events: no system-scope fence when they complete (only device
+  // timestamps are read from them)
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
@@ -170,25 +172,30 @@ hipEvent_t take_event(TimerFamily* f) {
 
 namespace lat {
 
-void timer_begin(const char* family, hipStream_t s) {
+thread_local TimerFamily* t_active = nullptr;  // family of the live ScopedKernelTimer
+
+void timer_begin(const char* family) {
+  t_active = nullptr;
   if (!g_any_timer) return;
   std::lock_guard<std::mutex> lk(g_timer_mu);
   TimerFamily* f = find_family(family, false);
-  if (!f || !f->enabled) return;
-  f->pending = take_event(f);
-  if (f->pending) (void)hipEventRecord(f->pending, s);
+  if (f && f->enabled) t_active = f;
 }
 
-void timer_end(const char* family, hipStream_t s) {
-  if (!g_any_timer) return;
+void timer_end() { t_active = nullptr; }
+
+bool timer_take_events(hipEvent_t* start, hipEvent_t* stop) {
+  if (!t_active) return false;
   std::lock_guard<std::mutex> lk(g_timer_mu);
-  TimerFamily* f = find_family(family, false);
-  if (!f || !f->enabled || !f->pending) return;
-  hipEvent_t stop = take_event(f);
-  if (!stop) return;
-  (void)hipEventRecord(stop, s);
-  f->recorded.emplace_back(f->pending, stop);
-  f->pending = nullptr;
+  hipEvent_t a = take_event(t_active), b = a ? take_event(t_active) : nullptr;
+  if (!a || !b) {
+    if (a) t_active->spare.push_back(a);
+    return false;
+  }
+  t_active->recorded.emplace_back(a, b);
+  *start = a;
+  *stop = b;
+  return true;
 }
 
 }  // namespace lat

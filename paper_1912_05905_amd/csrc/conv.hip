@@ -193,7 +193,7 @@ void conv_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in,
   const int cols_per_block = WN * 16 * RN;
   const dim3 grid(static_cast<unsigned>((n_out + rows_per_block - 1) / rows_per_block),
                   static_cast<unsigned>((Cout + cols_per_block - 1) / cols_per_block));
-  hipLaunchKernelGGL((k_conv<BF16, RM, RN, WM, WN>), grid, dim3(kBlock), 0, s, nbr, ldn, n_out, in,
+  launch((k_conv<BF16, RM, RN, WM, WN>), grid, dim3(kBlock), 0, s, nbr, ldn, n_out, in,
                      ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows);
 }
 
@@ -518,14 +518,14 @@ void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void*
   const int64_t tiles = (n_out + BM - 1) / BM;
   const unsigned per_xcd = static_cast<unsigned>((tiles + 7) / 8);
   const dim3 grid(per_xcd * 8, static_cast<unsigned>((Cout + BN - 1) / BN), static_cast<unsigned>(splits));
-  hipLaunchKernelGGL((k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED>), grid, dim3(kBlock), P::LDS_BYTES, s, nbr,
+  launch((k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED>), grid, dim3(kBlock), P::LDS_BYTES, s, nbr,
                      ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows,
                      static_cast<unsigned>(tiles), splits, splits > 1 ? part : nullptr,
                      static_cast<uint32_t>(BUF ? ext.in_bytes : 0), static_cast<uint32_t>(BUF ? ext.w_bytes : 0));
   if (splits > 1) {
     const int64_t quads = n_out * (Cout / 4);
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((quads + kBlock - 1) / kBlock, 8192));
-    hipLaunchKernelGGL((k_conv_reduce<BF16>), dim3(blocks), dim3(kBlock), 0, s, part, splits, n_out, Cout, bias,
+    launch((k_conv_reduce<BF16>), dim3(blocks), dim3(kBlock), 0, s, part, splits, n_out, Cout, bias,
                        relu, out, ld_out);
   }
 }

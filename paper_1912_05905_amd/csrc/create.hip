@@ -590,7 +590,7 @@ void launch_clear_table(HashEntry* keys, int32_t* counts, int64_t cap, void* dev
   const int64_t want = (cap + kBlock * 4 - 1) / (kBlock * 4);
   const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : (want < 8192 ? want : 8192));
   ScopedKernelTimer tm("fill", s);
-  hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, s, keys, counts, cap,
+  launch(k_clear_table, dim3(grid), dim3(kBlock), 0, s, keys, counts, cap,
                      static_cast<uint4*>(dev_counters), static_cast<uint64_t*>(scan_work));
 }
 
@@ -600,7 +600,7 @@ void launch_insert_points(const float* pos, const float* y_in, float y_scale, fl
                           float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, hipStream_t s) {
   if (m <= 0) return;
   ScopedKernelTimer tm("insert", s);
-  hipLaunchKernelGGL(k_insert_points, dim3(blocks_for(m)), dim3(kBlock), 0, s, pos,
+  launch(k_insert_points, dim3(blocks_for(m)), dim3(kBlock), 0, s, pos,
                      reinterpret_cast<const float4*>(y_in), y_scale, a0, a1, a2, m, h, counter,
                      slot_count, vkeys, vslot, reinterpret_cast<int4*>(slot_out),
                      reinterpret_cast<int4*>(rank_out), reinterpret_cast<float4*>(w_out),
@@ -612,7 +612,7 @@ int64_t scan_workspace_bytes() { return kScanBlocks * sizeof(uint64_t); }
 void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, const int32_t* n_dev,
                        int32_t* offsets, void* work, hipStream_t s) {
   ScopedKernelTimer tm("scan", s);
-  hipLaunchKernelGGL(k_scan, dim3(kScanBlocks), dim3(kBlock), 0, s, slot_count, vslot, n_dev,
+  launch(k_scan, dim3(kScanBlocks), dim3(kBlock), 0, s, slot_count, vslot, n_dev,
                      static_cast<uint64_t*>(work), offsets);
 }
 
@@ -621,7 +621,7 @@ void launch_fill_lists(HashView h, const int32_t* slot, const int32_t* rank, con
                        int32_t* chunk_first, int chunk, int64_t m4, hipStream_t s) {
   if (m4 <= 0) return;
   ScopedKernelTimer tm("lists", s);
-  hipLaunchKernelGGL(k_fill_lists, dim3(blocks_for(m4)), dim3(kBlock), 0, s, h, slot, rank, w, offsets,
+  launch(k_fill_lists, dim3(blocks_for(m4)), dim3(kBlock), 0, s, h, slot, rank, w, offsets,
                      idx, entries, entry_w, chunk_first, chunk, m4);
 }
 
@@ -635,7 +635,7 @@ void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_d
                            int32_t* nbr, int64_t ldn, hipStream_t s) {
   if (n_max <= 0) return;
   ScopedKernelTimer tm("nbr", s);
-  hipLaunchKernelGGL(k_neighbor_table, dim3(stride_grid(n_max * kTaps)), dim3(kBlock), 0, s, h, vkeys, n_dev,
+  launch(k_neighbor_table, dim3(stride_grid(n_max * kTaps)), dim3(kBlock), 0, s, h, vkeys, n_dev,
                      nbr, ldn);
 }
 
@@ -644,21 +644,21 @@ void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse
                           int32_t* down, int32_t* up, int32_t* up_rows, hipStream_t s) {
   if (nc_max <= 0 || nf_max <= 0) return;
   ScopedKernelTimer tm("nbr", s);
-  hipLaunchKernelGGL(k_coarse_tables, dim3(stride_grid((2 * nc_max + nf_max) * kTaps)), dim3(kBlock), 0, s, coarse,
+  launch(k_coarse_tables, dim3(stride_grid((2 * nc_max + nf_max) * kTaps)), dim3(kBlock), 0, s, coarse,
                      fine, coarse_keys, fine_keys, nc_dev, nf_dev, nbr, down, nc_max, up, nf_max);
-  hipLaunchKernelGGL(k_mask_order, dim3(static_cast<unsigned>((nf_max + kOrderRange - 1) / kOrderRange)),
+  launch(k_mask_order, dim3(static_cast<unsigned>((nf_max + kOrderRange - 1) / kOrderRange)),
                      dim3(kOrderThreads), 0, s, up, nf_max, nf_dev, up_rows);
 }
 
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s) {
   if (n <= 0) return;
-  hipLaunchKernelGGL(k_export_keys, dim3(blocks_for(n)), dim3(kBlock), 0, s, vkeys, n,
+  launch(k_export_keys, dim3(blocks_for(n)), dim3(kBlock), 0, s, vkeys, n,
                      reinterpret_cast<int4*>(out));
 }
 
 void launch_transpose_table(const int32_t* tab, int64_t ld, int64_t n, int32_t* out, hipStream_t s) {
   if (n <= 0) return;
-  hipLaunchKernelGGL(k_transpose_table, dim3(blocks_for(n * kTaps)), dim3(kBlock), 0, s, tab, ld, n, out);
+  launch(k_transpose_table, dim3(blocks_for(n * kTaps)), dim3(kBlock), 0, s, tab, ld, n, out);
 }
 
 }  // namespace lat

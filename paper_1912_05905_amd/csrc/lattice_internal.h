@@ -1,6 +1,7 @@
 // Internal declarations of liblattice (gfx950).  Not part of the public ABI.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -98,15 +99,28 @@ __device__ inline int32_t tap_offset(int t, int i) {
 // host-side pieces shared by the translation units
 // ---------------------------------------------------------------------------
 struct Timer;   // kernel-family event timer (api.hip)
-void timer_begin(const char* family, hipStream_t s);
-void timer_end(const char* family, hipStream_t s);
+// Kernel-family timing: while a ScopedKernelTimer of an enabled family is
+// alive on this thread, every launch() gets a start and a stop event that
+// the dispatch itself updates (hipExtLaunchKernel), so the family's time is
+// the sum of its kernels' execution times, without marker packets between
+// kernels.
+void timer_begin(const char* family);
+void timer_end();
+bool timer_take_events(hipEvent_t* start, hipEvent_t* stop);
 
 struct ScopedKernelTimer {
-  const char* fam;
-  hipStream_t s;
-  ScopedKernelTimer(const char* f, hipStream_t st) : fam(f), s(st) { timer_begin(fam, s); }
-  ~ScopedKernelTimer() { timer_end(fam, s); }
+  ScopedKernelTimer(const char* f, hipStream_t) { timer_begin(f); }
+  ~ScopedKernelTimer() { timer_end(); }
 };
+
+template <typename K, typename... Args>
+inline void launch(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  const bool timed = timer_take_events(&e0, &e1);
+  if (timed) (void)hipEventRecord(e0, s);
+  hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+  if (timed) (void)hipEventRecord(e1, s);
+}
 
 // Launchers (each .hip file implements its own kernels' launchers).
 // create.hip

@@ -462,10 +462,10 @@ void splat_launch(const int32_t* off, const int32_t* ent, const float* ew, const
                               static_cast<int>(splat_lds_bytes(LPR, LPR * Q * Chunk<BF16>::N)));
     lds_limit_set = true;
   }
-  hipLaunchKernelGGL((k_splat_chunks<BF16, LPR, Q, B>), dim3(xcd_grid(nblk)), dim3(kBlock), lds, s, off, ent, ew, cf,
+  launch((k_splat_chunks<BF16, LPR, Q, B>), dim3(xcd_grid(nblk)), dim3(kBlock), lds, s, off, ent, ew, cf,
                      chunk, n, total, feat, ldf, C, norm, vals, ldv, wsum, ph, pt, pw, nblk);
   if (nspans > 1)
-    hipLaunchKernelGGL((k_splat_finish<BF16, LPR, Q>), dim3(grid_for(nspans, LPR)), dim3(kBlock), 0, s, off, cf,
+    launch((k_splat_finish<BF16, LPR, Q>), dim3(grid_for(nspans, LPR)), dim3(kBlock), 0, s, off, cf,
                        span_len, G, nspans, C, norm, vals, ldv, wsum, ph, pt, pw);
 }
 
@@ -488,13 +488,13 @@ void slice_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, cons
   const int4* i4 = reinterpret_cast<const int4*>(idx);
   const float4* w4 = reinterpret_cast<const float4*>(w);
   switch (lpr) {
-    case 1: hipLaunchKernelGGL((k_slice<BF16, 1>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
-    case 2: hipLaunchKernelGGL((k_slice<BF16, 2>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
-    case 4: hipLaunchKernelGGL((k_slice<BF16, 4>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
-    case 8: hipLaunchKernelGGL((k_slice<BF16, 8>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
-    case 16: hipLaunchKernelGGL((k_slice<BF16, 16>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
-    case 32: hipLaunchKernelGGL((k_slice<BF16, 32>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
-    default: hipLaunchKernelGGL((k_slice<BF16, 64>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 1: launch((k_slice<BF16, 1>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 2: launch((k_slice<BF16, 2>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 4: launch((k_slice<BF16, 4>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 8: launch((k_slice<BF16, 8>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 16: launch((k_slice<BF16, 16>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    case 32: launch((k_slice<BF16, 32>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
+    default: launch((k_slice<BF16, 64>), g, b, 0, s, i4, w4, m, vals, ldv, C, out, nblk); break;
   }
 }
 
@@ -508,13 +508,13 @@ void deform_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, con
   const float4* w4 = reinterpret_cast<const float4*>(w);
   float4* d4 = reinterpret_cast<float4*>(delta);
   switch (lpr) {
-    case 1: hipLaunchKernelGGL((k_deform_slice<BF16, 1, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 2: hipLaunchKernelGGL((k_deform_slice<BF16, 2, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 4: hipLaunchKernelGGL((k_deform_slice<BF16, 4, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 8: hipLaunchKernelGGL((k_deform_slice<BF16, 8, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 16: hipLaunchKernelGGL((k_deform_slice<BF16, 16, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 32: hipLaunchKernelGGL((k_deform_slice<BF16, 32, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    default: hipLaunchKernelGGL((k_deform_slice<BF16, 64, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 1: launch((k_deform_slice<BF16, 1, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 2: launch((k_deform_slice<BF16, 2, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 4: launch((k_deform_slice<BF16, 4, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 8: launch((k_deform_slice<BF16, 8, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 16: launch((k_deform_slice<BF16, 16, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 32: launch((k_deform_slice<BF16, 32, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    default: launch((k_deform_slice<BF16, 64, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
   }
 }
 
