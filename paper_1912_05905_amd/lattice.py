@@ -74,9 +74,18 @@ def _check(status: int):
         raise LatticeError(status, lib().lattice_last_error().decode())
 
 
+# the raw handle of the current stream without building a torch Stream
+# object (which costs microseconds per call)
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_raw_device = getattr(torch._C, "_cuda_getDevice", None)
+
+
 def _stream(stream=None):
-    s = torch.cuda.current_stream() if stream is None else stream
-    return C.c_void_p(s.cuda_stream)
+    if stream is not None:
+        return C.c_void_p(stream.cuda_stream)
+    if _raw_stream is not None and _raw_device is not None:
+        return C.c_void_p(_raw_stream(_raw_device()))
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
 def _dtype_code(t: torch.Tensor) -> int:
