@@ -43,6 +43,10 @@
 //    congruent mod d+1); every other tap, the centre included, is ignored.
 //  * DeformSlice: max per channel over all d+1 weighted vertex values (the
 //    vertex itself included), nonlinearity tanh.
+//  * Distribute + PointNet: coordinates are the raw positions g_p minus the
+//    unweighted mean over J_v; three 1x1 layers with ReLU before the second
+//    and the third (none on the raw rows), then the per-vertex maximum;
+//    GroupNorm is not part of this operator.
 #include <algorithm>
 #include <array>
 #include <cmath>
@@ -491,6 +495,56 @@ int orc_deform_slice(const orc_lattice* L, const double* X, int64_t ldx, int C, 
   if (!L || !X || !out || !wv || C <= 0) return EINVAL_;
   orc_deform_slice_raw(X, ldx, C, L->idx.data(), L->bary.data(), pts ? npts : L->m, wv, beta,
                        pts, out, delta);
+  return OK;
+}
+
+// Distribute + PointNet (Proposed Operations, Eq. (distribute), and the
+// PointNet block of the architecture figure).  For every vertex v and every
+// point p of J_v (the points whose simplex contains v) the distributed row is
+// [g_p - mu_v ; f_p], mu_v the mean position of the points of J_v.  Each row
+// goes through three 1x1 layers, h1 = W1 r + b1, h2 = W2 relu(h1) + b2,
+// h3 = W3 relu(h2) + b3 (W_i laid out [out][in]), and x_v is the per-channel
+// maximum of h3 over J_v.  G is m x d positions, F m x Cf features; X gets
+// n x C3.  Plain loops in double, following the definition vertex by vertex.
+int orc_distribute_pointnet(const orc_lattice* L, const double* G, const double* F, int cf,
+                            const double* W1, const double* b1, int c1, const double* W2,
+                            const double* b2, int c2, const double* W3, const double* b3, int c3,
+                            double* X) {
+  if (!L || !X || cf < 0 || c1 <= 0 || c2 <= 0 || c3 <= 0 || !W1 || !W2 || !W3) return EINVAL_;
+  if (L->m > 0 && (!G || (cf > 0 && !F))) return EINVAL_;
+  const int64_t n = static_cast<int64_t>(L->keys.size());
+  // J_v: the points whose simplex has v among its d+1 vertices
+  std::vector<std::vector<int64_t>> J(n);
+  for (int64_t p = 0; p < L->m; ++p)
+    for (int k = 0; k < kD1; ++k) J[L->idx[p * kD1 + k]].push_back(p);
+  const int cin = kDim + cf;
+  std::vector<double> r(cin), h1(c1), h2(c2), h3(c3);
+  for (int64_t v = 0; v < n; ++v) {
+    double mu[kDim] = {0.0, 0.0, 0.0};
+    for (int64_t p : J[v])
+      for (int j = 0; j < kDim; ++j) mu[j] += G[p * kDim + j];
+    for (int j = 0; j < kDim; ++j) mu[j] /= static_cast<double>(J[v].size());
+    for (int c = 0; c < c3; ++c) X[v * c3 + c] = -INFINITY;
+    for (int64_t p : J[v]) {
+      for (int j = 0; j < kDim; ++j) r[j] = G[p * kDim + j] - mu[j];
+      for (int c = 0; c < cf; ++c) r[kDim + c] = F[p * cf + c];
+      for (int o = 0; o < c1; ++o) {
+        double a = b1 ? b1[o] : 0.0;
+        for (int i = 0; i < cin; ++i) a += W1[o * cin + i] * r[i];
+        h1[o] = a;
+      }
+      for (int o = 0; o < c2; ++o) {
+        double a = b2 ? b2[o] : 0.0;
+        for (int i = 0; i < c1; ++i) a += W2[o * c1 + i] * std::max(h1[i], 0.0);
+        h2[o] = a;
+      }
+      for (int o = 0; o < c3; ++o) {
+        double a = b3 ? b3[o] : 0.0;
+        for (int i = 0; i < c2; ++i) a += W3[o * c2 + i] * std::max(h2[i], 0.0);
+        X[v * c3 + o] = std::max(X[v * c3 + o], a);
+      }
+    }
+  }
   return OK;
 }
 

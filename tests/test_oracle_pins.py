@@ -357,3 +357,116 @@ def test_bf16_rounding(oracle_mod):
     assert r[0] == 1.0 and r[1] == 1.0 and r[2] == 1.0 + 2 ** -6 and r[3] == 1.0
     bits = gen.to_bf16_bits(x.astype(np.float32))
     assert np.array_equal(gen.bf16_bits_to_f32(bits).astype(np.float64)[4:], r[4:])
+
+
+# ---------------------------------------------------------------------------
+# Distribute + PointNet (Proposed Operations, Eq. (distribute))
+# ---------------------------------------------------------------------------
+def _point_sets(ol):
+    """J_v from the exported simplices: the points whose simplex holds v."""
+    idx, _ = ol.simplices()
+    J = [[] for _ in range(ol.n)]
+    for p in range(idx.shape[0]):
+        for k in range(4):
+            J[idx[p, k]].append(p)
+    return J
+
+
+def _selector(rows, cols, pick, sign=1.0):
+    W = np.zeros((rows, cols))
+    for o, i in enumerate(pick):
+        W[o, i] = sign
+    return W
+
+
+def test_distribute_invariances(oracle_mod):
+    """Translating the cloud leaves g_p - mu_v unchanged; the operator does
+    not depend on the order of the points."""
+    O = oracle_mod
+    G = _tiny_cloud(91, m=300)
+    st = Stream(91, "dist-f")
+    F = st.normal(300 * 5).reshape(300, 5)
+    layers = [(st.normal(16 * 8).reshape(16, 8), st.normal(16)), (st.normal(32 * 16).reshape(32, 16), st.normal(32)),
+              (st.normal(64 * 32).reshape(64, 32), st.normal(64))]
+    ol = O.Lattice.create(G, np.full(3, 0.15, np.float32))
+    X = ol.distribute_pointnet(G.astype(np.float64), F, layers)
+    shift = np.array([0.25, -0.5, 0.125])       # exact in float; lattice rebuilt from the shifted cloud
+    Gs = (G.astype(np.float64) + shift)
+    # same lattice (built from G), shifted coordinates: mu shifts with them
+    Xs = ol.distribute_pointnet(Gs, F, layers)
+    np.testing.assert_allclose(Xs, X, rtol=1e-12, atol=1e-11)
+    perm = st.permutation(300)
+    olp = O.Lattice.create(G[perm], np.full(3, 0.15, np.float32))
+    assert np.array_equal(olp.keys(), ol.keys())    # vertices numbered by key: same rows
+    Xp = olp.distribute_pointnet(G[perm].astype(np.float64), F[perm], layers)
+    np.testing.assert_allclose(Xp, X, rtol=1e-12, atol=1e-12)
+
+
+def test_distribute_coordinates_mean_and_max(oracle_mod):
+    """With selector weights and a bias that keeps every ReLU open, x_v is
+    max_p (g_p - mu_v) + B per coordinate; with negated selectors it is
+    B - min_p (g_p - mu_v).  Checked against the point sets of the exported
+    simplices."""
+    O = oracle_mod
+    G = _tiny_cloud(92, m=400).astype(np.float64)
+    ol = O.Lattice.create(G.astype(np.float32), np.full(3, 0.12, np.float32))
+    J = _point_sets(ol)
+    B = 100.0
+    for sign in (1.0, -1.0):
+        layers = [(_selector(16, 3, [0, 1, 2], sign), np.full(16, B)),
+                  (_selector(32, 16, [0, 1, 2]), None), (_selector(64, 32, [0, 1, 2]), None)]
+        X = ol.distribute_pointnet(G, None, layers)
+        for v in range(ol.n):
+            pts = G[J[v]]
+            d = sign * (pts - pts.mean(axis=0))
+            np.testing.assert_allclose(X[v, :3], d.max(axis=0) + B, rtol=0, atol=1e-9)
+        assert np.all(X[:, 3:] == 0.0)
+
+
+def test_distribute_relu_placement(oracle_mod):
+    """Feature selectors with zero biases: h1 = f (may be negative), ReLU
+    before the second and third layers only, none after the last: x_v =
+    relu(max f) with identity layers, -relu(min f) with a negated last layer."""
+    O = oracle_mod
+    G = _tiny_cloud(93, m=300).astype(np.float64)
+    st = Stream(93, "dist-relu")
+    F = st.normal(300 * 4).reshape(300, 4)
+    ol = O.Lattice.create(G.astype(np.float32), np.full(3, 0.15, np.float32))
+    J = _point_sets(ol)
+    pick = [3, 4, 5, 6]                          # the feature inputs follow the 3 coordinates
+    for sign in (1.0, -1.0):
+        layers = [(_selector(16, 7, pick), None), (_selector(32, 16, [0, 1, 2, 3]), None),
+                  (_selector(64, 32, [0, 1, 2, 3], sign), None)]
+        X = ol.distribute_pointnet(G, F, layers)
+        for v in range(ol.n):
+            f = F[J[v]]
+            want = np.maximum(f.max(axis=0), 0.0) if sign > 0 else -np.maximum(f.min(axis=0), 0.0)
+            np.testing.assert_allclose(X[v, :4], want, rtol=0, atol=1e-12)
+
+
+def test_distribute_each_relu_matters(oracle_mod):
+    """Constructions in which each ReLU changes the result:
+    W1 = I, W2 = -I, W3 = I            -> 0 (the ReLU before layer 3 clips -relu(f));
+    W1 = I, W2 = I, b2 = -c, W3 = I     -> relu(relu(max f) - c);
+    W1 = -I, W2 = I, W3 = I             -> relu(-min f) (no ReLU on the raw rows)."""
+    O = oracle_mod
+    G = _tiny_cloud(94, m=300).astype(np.float64)
+    st = Stream(94, "dist-relu2")
+    F = st.normal(300 * 4).reshape(300, 4)
+    ol = O.Lattice.create(G.astype(np.float32), np.full(3, 0.15, np.float32))
+    J = _point_sets(ol)
+    feat = [3, 4, 5, 6]
+    four = [0, 1, 2, 3]
+    c = 0.5
+    cases = [
+        ([(_selector(16, 7, feat), None), (_selector(32, 16, four, -1.0), None), (_selector(64, 32, four), None)],
+         lambda f: np.zeros(4)),
+        ([(_selector(16, 7, feat), None), (_selector(32, 16, four), np.full(32, -c)), (_selector(64, 32, four), None)],
+         lambda f: np.maximum(np.maximum(f.max(axis=0), 0.0) - c, 0.0)),
+        ([(_selector(16, 7, feat, -1.0), None), (_selector(32, 16, four), None), (_selector(64, 32, four), None)],
+         lambda f: np.maximum(-f.min(axis=0), 0.0)),
+    ]
+    for layers, want in cases:
+        X = ol.distribute_pointnet(G, F, layers)
+        for v in range(ol.n):
+            np.testing.assert_allclose(X[v, :4], want(F[J[v]]), rtol=0, atol=1e-12)
