@@ -23,12 +23,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"hbm": 8.0e12, "mfma_f32": 157.3e12, "mfma_bf16": 2.5e15}
-FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "conv", "slice", "deform_slice"]
+FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "distribute", "conv", "slice", "deform_slice"]
 # kernel symbol fragments of each family (rocprofv3 kernel names)
 FAMILY_KERNELS = {
     "fill": ["k_clear_table"], "insert": ["k_insert_points"], "scan": ["k_scan("],
     "lists": ["k_fill_lists"], "nbr": ["k_neighbor_table", "k_coarse_tables", "k_mask_order"],
-    "splat": ["k_splat_chunks", "k_splat_finish"], "conv": ["k_conv"], "slice": ["k_slice<"],
+    "splat": ["k_splat_chunks", "k_splat_finish"], "distribute": ["k_dist_"], "conv": ["k_conv"],
+    "slice": ["k_slice<"],
     "deform_slice": ["k_deform_slice"],
 }
 CSRC = os.path.join(ROOT, "paper_1912_05905_amd", "csrc")
@@ -140,13 +141,29 @@ def conv_flops(wl, levels):
     return total
 
 
+def distribute_flops(wl):
+    """Flops of the Distribute + PointNet layers of one step: each of the 4m
+    (point, vertex) rows goes through the three 1x1 layers."""
+    total = 0
+    for op in wl.ops:
+        if op["op"] == "distribute":
+            k = 3 + wl.features.shape[1]
+            for name in op["layers"]:
+                W, _ = wl.mlp[name]
+                total += 2 * 4 * wl.m * W.shape[0] * k
+                k = W.shape[0]
+    return total
+
+
 def algorithmic_bytes(wl, levels, family):
     """Bytes a kernel family must move per step (each input read once, each
     output written once), for the HBM-bound families."""
     u = 2 if wl.dtype == "bf16" else 4
     m = wl.m
     if family == "splat":
-        C = next(op["dst"][2] for op in wl.ops if op["op"] == "splat")
+        C = next((op["dst"][2] for op in wl.ops if op["op"] == "splat"), None)
+        if C is None:
+            return None
         n = levels[0].n
         # features m*C*u, lists 4m*(4 entry + 4 weight), offsets, output n*C*u
         return m * C * u + 4 * m * 8 + (n + 1) * 4 + n * C * u
@@ -253,9 +270,10 @@ def main():
     value = wl.m / (ms_per_step * 1e-3)
     dom_ms_step = dom_ms / args.steps
     dtype = "bf16" if wl.dtype == "bf16" else "f32"
-    if dominant == "conv":
+    mfma_flops = {"conv": flops, "distribute": distribute_flops(wl)}
+    if dominant in mfma_flops:
         peak = PEAK["mfma_bf16"] if dtype == "bf16" else PEAK["mfma_f32"]
-        achieved = flops / (dom_ms_step * 1e-3)
+        achieved = mfma_flops[dominant] / (dom_ms_step * 1e-3)
         roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
                 "frac": achieved / peak, "traffic": None}
         t = measured_traffic(f"config{wl.cfg}", dominant)
@@ -291,7 +309,8 @@ def main():
         "dtype": dtype, "data": "synthetic",
         "config": {"workload": f"config{wl.cfg}:{wl.name}", "points": wl.m,
                    "sigma": float(wl.sigma[0]), "vertices_per_level": [ns[k] for k in sorted(ns)],
-                   "conv_gflop_per_step": flops / 1e9},
+                   "conv_gflop_per_step": flops / 1e9,
+                   "distribute_gflop_per_step": mfma_flops["distribute"] / 1e9},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -165,6 +165,29 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
                    void* out_dev, int64_t ld_out, hipStream_t stream);
 
 /*
+ * Distribute + PointNet (Proposed Operations, Eq. (distribute); PointNet
+ * block of the architecture figure).  For every vertex v the rows
+ * r_p = [g_p - mu_v ; f_p], p in J_v, mu_v the mean of g_p over J_v, pass
+ * through three 1x1 layers and the per-channel maximum over J_v:
+ *   x_v = max_{p in J_v} W3 relu(W2 relu(W1 r_p + b1) + b2) + b3.
+ * No activation is applied to the raw rows; GroupNorm is not part of this
+ * operator.  float32 only (the mean is formed in float64).
+ *   pos_dev   m x d float32, the positions the lattice was built from.
+ *   feat_dev  m x Cf float32, row stride ld_feat (0 = Cf); may be NULL when
+ *             Cf = 0.  0 <= Cf <= 60.
+ *   W1_dev    C1 x (d + Cf) float32, [out][in]: inputs 0..d-1 are the
+ *             coordinates, d.. the features.  W2_dev C2 x C1, W3_dev C3 x C2.
+ *   b*_dev    optional C1 / C2 / C3 float32 biases (NULL = 0).
+ *   C1, C2, C3  multiples of 16, at most 64 (the paper uses 16, 32, 64).
+ *   out_dev   n x C3 float32, row stride ld_out (0 = C3).
+ * Uses a work space of O(n + 4m / 64 * C3) from the library's pool.
+ */
+int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* feat_dev, int64_t ld_feat,
+                                int Cf, const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
+                                const float* b2_dev, int C2, const float* W3_dev, const float* b3_dev, int C3,
+                                float* out_dev, int64_t ld_out, hipStream_t stream);
+
+/*
  * Slice, Eq. (slice): out_p = sum_{v in I_p} b_pv x_v.
  *   vals_dev  n x C (dtype dt), row stride ld_vals.
  *   out_dev   m x C float32 (dense).

@@ -23,6 +23,7 @@ SOURCES = {
     "create.hip": ["-ffp-contract=off"],
     "splat_slice.hip": [],
     "conv.hip": [],
+    "distribute.hip": [],
     "api.hip": [],
 }
 

@@ -734,6 +734,34 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
                      flags, out_dev, ld_out, coarse->up_rows, stream);
 }
 
+int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* feat_dev, int64_t ld_feat,
+                                int Cf, const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
+                                const float* b2_dev, int C2, const float* W3_dev, const float* b3_dev, int C3,
+                                float* out_dev, int64_t ld_out, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if (Cf < 0 || Cf > distribute_max_features())
+    return fail(LAT_EUNSUPPORTED, "Cf must be in [0, " + std::to_string(distribute_max_features()) + "]");
+  for (int c : {C1, C2, C3})
+    if (c <= 0 || c % 16 != 0 || c > 64) return fail(LAT_EUNSUPPORTED, "C1, C2, C3 must be 16, 32, 48 or 64");
+  if (ld_feat == 0) ld_feat = Cf;
+  if (ld_out == 0) ld_out = C3;
+  if (ld_feat < Cf) return fail(LAT_EINVAL, "ld_feat < Cf");
+  if (ld_out < C3) return fail(LAT_EINVAL, "ld_out < C3");
+  if (!W1_dev || !W2_dev || !W3_dev) return fail(LAT_EINVAL, "weights are null");
+  if (L->m > 0 && !pos_dev) return fail(LAT_EINVAL, "pos is null");
+  if (L->m > 0 && Cf > 0 && !feat_dev) return fail(LAT_EINVAL, "feat is null");
+  if (L->n > 0 && !out_dev) return fail(LAT_EINVAL, "out is null");
+  if (L->n == 0) return LAT_OK;
+  Scratch mu, work;
+  if ((st = mu.get(sizeof(double) * 4 * static_cast<size_t>(L->n), stream)) != LAT_OK) return st;
+  if ((st = work.get(static_cast<size_t>(distribute_workspace_bytes(L->total, C3)), stream)) != LAT_OK) return st;
+  launch_distribute(L->offsets, L->entries, L->chunk_first, L->chunk, L->n, L->total, pos_dev, feat_dev, ld_feat, Cf,
+                    W1_dev, b1_dev, C1, W2_dev, b2_dev, C2, W3_dev, b3_dev, C3, out_dev, ld_out, mu.as<double>(),
+                    work.p, stream);
+  return check_launch("distribute");
+}
+
 int lattice_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
                   float* out_dev, hipStream_t stream) {
   int st;

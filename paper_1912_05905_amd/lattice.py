@@ -43,6 +43,8 @@ SIGNATURES = {
     "lattice_refine": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _I32, _I32, _P, _I64, _P]),
     "lattice_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
     "lattice_deform_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _P]),
+    "lattice_distribute_pointnet": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _P, _P, _I32, _P, _P, _I32,
+                                           _P, _I64, _P]),
     "lattice_timing_enable": (_I32, [C.c_char_p, _I32]),
     "lattice_timing_read": (_I32, [C.c_char_p, C.POINTER(_I64), C.POINTER(C.c_double)]),
 }
@@ -241,6 +243,27 @@ class Lattice:
         xp, xld = _rows(x)
         _check(lib().lattice_slice(self._h, xp, xld, Cc, _dtype_code(x), C.c_void_p(out.data_ptr()),
                                    _stream(stream)))
+        return out
+
+    def distribute_pointnet(self, pos: torch.Tensor, feat: torch.Tensor | None, layers,
+                            out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """Distribute + PointNet; layers = [(W1, b1), (W2, b2), (W3, b3)] with
+        W_i float32 [out][in] device tensors and optional biases."""
+        (W1, b1), (W2, b2), (W3, b3) = layers
+        c1, c2, c3 = W1.shape[0], W2.shape[0], W3.shape[0]
+        for W in (W1, W2, W3):
+            if W.dtype != torch.float32 or not W.is_contiguous():
+                raise ValueError("weights must be contiguous float32")
+        if pos.dtype != torch.float32 or not pos.is_contiguous():
+            raise ValueError("positions must be a contiguous m x d float32 tensor")
+        cf = 0 if feat is None else feat.shape[1]
+        fp, fld = (None, 0) if feat is None else _rows(feat)
+        if out is None:
+            out = torch.empty((self.n, c3), dtype=torch.float32, device="cuda")
+        op, old = _rows(out)
+        ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
+        _check(lib().lattice_distribute_pointnet(self._h, ptr(pos), fp, fld, cf, ptr(W1), ptr(b1), c1, ptr(W2),
+                                                 ptr(b2), c2, ptr(W3), ptr(b3), c3, op, old, _stream(stream)))
         return out
 
     def deform_slice(self, x: torch.Tensor, wv: torch.Tensor, beta: float,

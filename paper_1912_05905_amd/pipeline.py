@@ -26,6 +26,9 @@ class GpuPipeline:
                         .cuda().to(self.dtype).contiguous() for k, w in wl.weights.items()}
         self.vectors = {k: (torch.from_numpy(np.ascontiguousarray(v)).cuda(), float(beta))
                         for k, (v, beta) in wl.vectors.items()}
+        self.mlp = {k: (torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32)).cuda(),
+                        torch.from_numpy(np.ascontiguousarray(b, dtype=np.float32)).cuda())
+                    for k, (W, b) in wl.mlp.items()}
         self.sigma = [float(s) for s in wl.sigma]
         self._store: dict[str, torch.Tensor] = {}
 
@@ -79,6 +82,9 @@ class GpuPipeline:
                     levels[lv].conv(levels[lv - 1], x, W, relu=op["relu"], out=y)
                 else:
                     levels[lv].refine(levels[lv + 1], x, W, relu=op["relu"], out=y)
+            elif kind == "distribute":
+                levels[op["level"]].distribute_pointnet(self.pos, self.feat, [self.mlp[n] for n in op["layers"]],
+                                                        out=self._view(bufs, levels, op["dst"]))
             elif kind == "slice":
                 outs[op["out"]] = levels[op["level"]].slice(self._view(bufs, levels, op["src"]))
             elif kind == "deform_slice":

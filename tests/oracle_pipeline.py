@@ -54,6 +54,10 @@ class OraclePipeline:
                 else:
                     y = levels[lv].refine_into(levels[lv + 1], x, W, relu=op["relu"])
                 write(op["dst"], y)
+            elif kind == "distribute":
+                layers = [tuple(a.astype(np.float64) for a in wl.mlp[n]) for n in op["layers"]]
+                write(op["dst"], levels[op["level"]].distribute_pointnet(
+                    wl.positions.astype(np.float64), wl.features.astype(np.float64), layers))
             elif kind == "slice":
                 outs[op["out"]] = levels[op["level"]].slice(np.ascontiguousarray(view_src(op["src"])))
             elif kind == "deform_slice":

@@ -31,7 +31,7 @@ def test_header_declares_the_boundary():
     for need in ("lattice_create", "lattice_splat", "lattice_conv", "lattice_coarsen",
                  "lattice_refine", "lattice_slice", "lattice_deform_slice", "lattice_destroy",
                  "lattice_num_vertices", "lattice_export_keys", "lattice_export_neighbors",
-                 "lattice_export_simplices"):
+                 "lattice_export_simplices", "lattice_distribute_pointnet"):
         assert need in names
 
 
@@ -70,6 +70,8 @@ def test_host_validation_without_gpu(lib):
     assert lib.lattice_refine(None, None, None, 0, 8, None, None, 8, 0, 0, None, 0, None) == -1
     assert lib.lattice_slice(None, None, 0, 8, 0, None, None) == -1
     assert lib.lattice_deform_slice(None, None, 0, 8, 0, None, 0.0, None, None, None) == -1
+    assert lib.lattice_distribute_pointnet(None, None, None, 0, 4, None, None, 16, None, None, 32, None, None, 64,
+                                           None, 0, None) == -1
     assert lib.lattice_coarsen(None, 0, None, C.byref(out)) == -1
 
 

@@ -391,7 +391,7 @@ def _run_both(L, O, wl):
     return levels
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 6])
 def test_pipeline_full_size(L, O, cfg):
     _run_both(L, O, configs.make(cfg))
 
@@ -405,3 +405,75 @@ def test_pipeline_other_seeds(L, O, seed):
 def test_pipeline_config5_reduced(L, O):
     """The bf16 4-level U-Net on a 30k-point room of the same generator."""
     _run_both(L, O, configs.config5(m=30_000, size=(4.0, 4.0, 3.0), nboxes=20))
+
+
+# ----------------------------------------------------------------------------
+# Distribute + PointNet
+# ----------------------------------------------------------------------------
+def _pointnet_layers(rng, cin, widths):
+    layers, k = [], cin
+    for w in widths:
+        layers.append(((rng.normal(size=(w, k)) / np.sqrt(k)).astype(np.float32),
+                       (0.1 * rng.normal(size=w)).astype(np.float32)))
+        k = w
+    return layers
+
+
+def _distribute_pair(L, O, gl, ol, g2o, pos, F, widths, seed):
+    rng = np.random.default_rng(seed)
+    cf = 0 if F is None else F.shape[1]
+    layers = _pointnet_layers(rng, 3 + cf, widths)
+    dev_layers = [(_dev(W), _dev(b)) for W, b in layers]
+    gy = gl.distribute_pointnet(_dev(pos), None if F is None else _dev(F), dev_layers)
+    oy = ol.distribute_pointnet(pos.astype(np.float64), None if F is None else F.astype(np.float64),
+                                [(W.astype(np.float64), b.astype(np.float64)) for W, b in layers])
+    return P.rows_in_oracle_order(_host(gy), g2o), oy
+
+
+@pytest.mark.parametrize("cf,widths", [(4, (16, 32, 64)), (0, (16, 32, 64)), (13, (32, 32, 48)),
+                                        (60, (64, 64, 64)), (3, (16, 16, 16))])
+def test_distribute_pointnet(L, O, cf, widths):
+    pos = _cloud(200 + cf, 9000, 0.7)
+    gl, ol, g2o = _pair(L, O, pos, 0.06)
+    F = None if cf == 0 else np.random.default_rng(cf).normal(size=(pos.shape[0], cf)).astype(np.float32)
+    g, o = _distribute_pair(L, O, gl, ol, g2o, pos, F, widths, cf)
+    P.assert_close(g, o, P.TOL_F32, f"distribute cf={cf} {widths}")
+
+
+def test_distribute_pointnet_skewed_and_far(L, O):
+    """Lists far longer than the spans of both passes (a 6000-point clump in
+    one simplex), and a cloud 40 m from the origin, where g - mu is a small
+    difference of large coordinates."""
+    rng = np.random.default_rng(5)
+    clump = (np.array([0.31, 0.42, 0.53]) + 1e-4 * rng.random((6000, 3))).astype(np.float32)
+    spread = rng.random((3001, 3)).astype(np.float32)
+    for shift, sigma in ((0.0, 0.05), (40.0, 0.3)):
+        pos = (np.concatenate([spread[:1500], clump, spread[1500:]]) * (8.0 if shift else 1.0) + shift).astype(np.float32)
+        gl, ol, g2o = _pair(L, O, pos, sigma)
+        F = rng.normal(size=(pos.shape[0], 4)).astype(np.float32)
+        g, o = _distribute_pair(L, O, gl, ol, g2o, pos, F, (16, 32, 64), 11)
+        P.assert_close(g, o, P.TOL_F32, f"distribute shift={shift}")
+
+
+def test_distribute_pointnet_coarse_and_tiny(L, O):
+    pos = _cloud(207, 5000, 0.8)
+    gl = L.Lattice.create(_dev(pos), [0.05] * 3)
+    ol = O.Lattice.create(pos, np.full(3, 0.05, np.float32))
+    gc, oc = gl.coarsen(), ol.coarsen()
+    g2o = P.key_permutation(_host(gc.keys()), oc.keys())
+    F = np.random.default_rng(2).normal(size=(pos.shape[0], 4)).astype(np.float32)
+    g, o = _distribute_pair(L, O, gc, oc, g2o, pos, F, (16, 32, 64), 3)
+    P.assert_close(g, o, P.TOL_F32, "distribute on a coarse level")
+    gc.destroy()
+    gl.destroy()
+    for m in (1, 37):
+        pos = _cloud(300 + m, m, 0.5)
+        gl, ol, g2o = _pair(L, O, pos, 0.1)
+        F = np.random.default_rng(m).normal(size=(m, 4)).astype(np.float32)
+        g, o = _distribute_pair(L, O, gl, ol, g2o, pos, F, (16, 32, 64), m)
+        P.assert_close(g, o, P.TOL_F32, f"distribute m={m}")
+    gl = L.Lattice.create(torch.zeros((0, 3), device="cuda"), [0.1] * 3)
+    assert gl.distribute_pointnet(torch.zeros((0, 3), device="cuda"), None,
+                                  [(torch.zeros((16, 3), device="cuda"), None),
+                                   (torch.zeros((32, 16), device="cuda"), None),
+                                   (torch.zeros((64, 32), device="cuda"), None)]).shape == (0, 64)

@@ -14,6 +14,9 @@ Operations (fields in brackets):
   refine        [level, src, dst, w, relu]        transposed convolution level+1 -> level
   slice         [level, src, out]                 vertex values -> points
   deform_slice  [level, src, wv, beta, out]       DeformSlice to points
+  distribute    [level, dst, layers]              Distribute + PointNet of the point
+                                                  positions and features (layers: names
+                                                  of (W [out][in], b) pairs in `mlp`)
 `src`/`dst` are (buffer, first column, channels); buffers are row-major
 (vertices of their level) x (total channels), so several ops can write
 disjoint column ranges of one buffer (concatenation without a copy).
@@ -40,6 +43,7 @@ class Workload:
     features: np.ndarray             # m x C float32 (already bf16-representable when dtype == bf16)
     weights: dict = field(default_factory=dict)    # name -> float32 array
     vectors: dict = field(default_factory=dict)    # DeformSlice weight vectors
+    mlp: dict = field(default_factory=dict)        # name -> (W [out][in], b) of 1x1 layers
     buffers: dict = field(default_factory=dict)    # name -> (level, channels)
     ops: list = field(default_factory=list)
     levels: int = 1
@@ -185,7 +189,33 @@ def config5(seed: int = 4, m: int = 1_000_000, size=(20.0, 20.0, 3.0), nboxes: i
     return _finish(wl)
 
 
-CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
+def config6(seed: int = 3, m: int = 120_000) -> Workload:
+    """The LiDAR scan of config 4 entering the network the paper's way:
+    Distribute + PointNet of the positions and 4 raw point features
+    (intensity U[0,1] and a random unit vector) through 1x1 layers
+    16/32/64, then a 1-hop convolution 64->64 and slice, fp32."""
+    pos = gen.lidar_scan(seed, m)
+    st = gen.Stream(seed, "raw-features")
+    inten = st.uniform(m).reshape(m, 1)
+    u = st.normal(3 * m).reshape(m, 3)
+    u /= np.linalg.norm(u, axis=1, keepdims=True)
+    F = np.concatenate([inten, u], axis=1).astype(np.float32)
+    wl = Workload(6, "lidar-distribute", seed, pos, np.full(3, 0.3, np.float32), "f32", F)
+    wl.buffers = {"p0": (0, 64), "e0": (0, 64)}
+    k = 3 + F.shape[1]
+    for i, c in enumerate((16, 32, 64)):
+        W = gen.normal_matrix(seed, f"pointnet{i}", c, k, 1.0 / np.sqrt(k))
+        b = gen.normal_matrix(seed, f"pointnet{i}:bias", 1, c, 0.1)[0]
+        wl.mlp[f"pointnet{i}"] = (W, b)
+        k = c
+    wl.ops = [dict(op="create", level=0),
+              dict(op="distribute", level=0, dst=("p0", 0, 64), layers=["pointnet0", "pointnet1", "pointnet2"])]
+    _conv(wl, "conv", 0, ("p0", 0, 64), ("e0", 0, 64), True, seed)
+    wl.ops.append(dict(op="slice", level=0, src=("e0", 0, 64), out="slice"))
+    return _finish(wl)
+
+
+CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5, 6: config6}
 
 
 def make(cfg: int, seed: int | None = None, **kw) -> Workload:
