@@ -11,6 +11,8 @@
 // fp64 (positions can be tens of metres from the origin while g - mu is a
 // fraction of sigma) and g - mu is rounded to fp32 once; the three 1x1
 // layers run on v_mfma_f32_16x16x4_f32, 16 list entries per wave.
+#include <algorithm>
+
 #include "lattice_internal.h"
 
 namespace lat {
@@ -139,23 +141,28 @@ k_dist_mean_finish(const int32_t* __restrict__ offsets, const int32_t* __restric
 // workgroup's output rows (64 x C3).
 struct MlpLds {
   int k1, c1, c2, c3;
-  int ldx, ldh, ldo;
+  int ldx, ldh, ldo, ld1, ld2, ld3;
   size_t w1, w2, w3, b, x, h1, h2, o, win, rows, end;
   __host__ __device__ MlpLds(int K1, int C1, int C2, int C3) : k1(K1), c1(C1), c2(C2), c3(C3) {
+    // every row pitch is odd, so the 4 k rows read by one MFMA operand load
+    // fall in different LDS banks
     ldx = K1 + 1;
-    ldh = kMaxC + 1;
+    ldh = (C1 > C2 ? C1 : C2) + 1;
     ldo = C3 + 1;
+    ld1 = C1 + 1;
+    ld2 = C2 + 1;
+    ld3 = C3 + 1;
     w1 = 0;
-    w2 = w1 + static_cast<size_t>(K1) * C1;
-    w3 = w2 + static_cast<size_t>(C1) * C2;
-    b = w3 + static_cast<size_t>(C2) * C3;
+    w2 = w1 + static_cast<size_t>(K1) * ld1;
+    w3 = w2 + static_cast<size_t>(C1) * ld2;
+    b = w3 + static_cast<size_t>(C2) * ld3;
     x = b + C1 + C2 + C3;
     h1 = x + 4 * 16 * static_cast<size_t>(ldx);
     h2 = h1 + 4 * 16 * static_cast<size_t>(ldh);
     o = h2 + 4 * 16 * static_cast<size_t>(ldh);
     win = o + kMlpSpan * static_cast<size_t>(ldo);   // int32 from here on
-    rows = win + kMlpSpan + 2;                         // per entry: point, window index
-    end = rows + 2 * kMlpSpan;
+    rows = win + kMlpSpan + 2;                         // per entry: point, window index, end code
+    end = rows + 3 * kMlpSpan;
   }
   __host__ __device__ size_t bytes() const { return end * 4; }
 };
@@ -170,6 +177,8 @@ __device__ inline f32x4 tile_mma(const float* A, int lda, const float* B, int ld
   return acc;
 }
 
+// Persistent: a workgroup stages the weights once and takes spans
+// blockIdx.x, blockIdx.x + gridDim.x, ...
 __global__ void __launch_bounds__(kBlock)
 k_dist_mlp(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
            const int32_t* __restrict__ chunk_first, int chunk, int64_t n, int64_t total,
@@ -177,7 +186,7 @@ k_dist_mlp(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entr
            const double4* __restrict__ mu, const float* __restrict__ W1, const float* __restrict__ b1,
            const float* __restrict__ W2, const float* __restrict__ b2, const float* __restrict__ W3,
            const float* __restrict__ b3, int K1, int C1, int C2, int C3, float* __restrict__ out,
-           int64_t ld_out, float* __restrict__ part_head, float* __restrict__ part_tail) {
+           int64_t ld_out, float* __restrict__ part_head, float* __restrict__ part_tail, int64_t nspans) {
   extern __shared__ __align__(16) float sm[];
   const MlpLds lay(K1, C1, C2, C3);
   float* w1 = sm + lay.w1;
@@ -187,12 +196,9 @@ k_dist_mlp(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entr
   int32_t* win = reinterpret_cast<int32_t*>(sm + lay.win);
   int32_t* rp = reinterpret_cast<int32_t*>(sm + lay.rows);   // point of each entry
   int32_t* rv = rp + kMlpSpan;                                // window index of its vertex
+  int32_t* rc = rv + kMlpSpan;                                // end code: -1, or 4 * window index + kind
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int li = lane & 15, lg = lane >> 4;
-  const int64_t span = blockIdx.x;
-  const int64_t s0 = span * kMlpSpan;
-  const int64_t s1 = min(s0 + kMlpSpan, total);
-  const int32_t v0 = chunk_first[s0 / chunk];
   constexpr int W = kMlpSpan + 2;
 
   // weights, transposed to [k][n]; input k of the first layer: 0..2 the
@@ -201,15 +207,15 @@ k_dist_mlp(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entr
   for (int i = t; i < K1 * C1; i += kBlock) {
     const int k = i / C1, o = i - k * C1;
     const int src = k < 3 ? k : (k == 3 ? -1 : (k - 4 < cf ? k - 1 : -1));
-    w1[i] = src >= 0 ? W1[o * cin + src] : 0.f;
+    w1[k * lay.ld1 + o] = src >= 0 ? W1[o * cin + src] : 0.f;
   }
   for (int i = t; i < C1 * C2; i += kBlock) {
     const int k = i / C2, o = i - k * C2;
-    w2[i] = W2[o * C1 + k];
+    w2[k * lay.ld2 + o] = W2[o * C1 + k];
   }
   for (int i = t; i < C2 * C3; i += kBlock) {
     const int k = i / C3, o = i - k * C3;
-    w3[i] = W3[o * C2 + k];
+    w3[k * lay.ld3 + o] = W3[o * C2 + k];
   }
   for (int i = t; i < C1 + C2 + C3; i += kBlock) {
     float v = 0.f;
@@ -218,69 +224,92 @@ k_dist_mlp(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entr
     else v = b3 ? b3[i - C1 - C2] : 0.f;
     bs[i] = v;
   }
-  load_window(offsets, n, v0, W, win);
-  __syncthreads();
-  if (t < kMlpSpan) {
-    const int64_t s = s0 + t;
-    rp[t] = s < s1 ? entries[s] >> 2 : -1;
-    rv[t] = s < s1 ? window_vertex(win, W, s) : 0;
-  }
-  __syncthreads();
-
-  // input rows of this wave's 16 entries: [g - mu (fp64, rounded once), 0, f]
   float* X = sm + lay.x + wave * 16 * lay.ldx;
-  for (int i = lane; i < 16 * K1; i += 64) {
-    const int r = i / K1, k = i - r * K1;
-    const int e = wave * 16 + r;
-    const int32_t p = rp[e];
-    float v = 0.f;
-    if (p >= 0) {
-      if (k < 3) {
-        const double4 m = mu[v0 + rv[e]];
-        const double mk = k == 0 ? m.x : (k == 1 ? m.y : m.z);
-        v = static_cast<float>(static_cast<double>(pos[3 * static_cast<int64_t>(p) + k]) - mk);
-      } else if (k >= 4 && k - 4 < cf) {
-        v = feat[static_cast<int64_t>(p) * ld_feat + (k - 4)];
-      }
-    }
-    X[r * lay.ldx + k] = v;
-  }
-  __syncthreads();
   float* H1 = sm + lay.h1 + wave * 16 * lay.ldh;
   float* H2 = sm + lay.h2 + wave * 16 * lay.ldh;
   float* O = sm + lay.o;
-  // layer 1, ReLU applied when the rows are read by layer 2
-  for (int n0 = 0; n0 < C1; n0 += 16) {
-    const f32x4 a = tile_mma(X, lay.ldx, w1, C1, K1, n0, lane);
-    for (int r = 0; r < 4; ++r) H1[(4 * lg + r) * lay.ldh + n0 + li] = fmaxf(a[r] + bs[n0 + li], 0.f);
-  }
-  __syncthreads();
-  for (int n0 = 0; n0 < C2; n0 += 16) {
-    const f32x4 a = tile_mma(H1, lay.ldh, w2, C2, C1, n0, lane);
-    for (int r = 0; r < 4; ++r) H2[(4 * lg + r) * lay.ldh + n0 + li] = fmaxf(a[r] + bs[C1 + n0 + li], 0.f);
-  }
-  __syncthreads();
-  for (int n0 = 0; n0 < C3; n0 += 16) {
-    const f32x4 a = tile_mma(H2, lay.ldh, w3, C3, C2, n0, lane);
-    for (int r = 0; r < 4; ++r)
-      O[(wave * 16 + 4 * lg + r) * lay.ldo + n0 + li] = a[r] + bs[C1 + C2 + n0 + li];
-  }
-  __syncthreads();
 
-  // per-channel maximum over each vertex's rows in the span
-  if (t >= C3) return;
-  const int rows = static_cast<int>(s1 - s0);
-  float m = -INFINITY;
-  for (int e = 0; e < rows; ++e) {
-    m = fmaxf(m, O[e * lay.ldo + t]);
-    const int vi = rv[e];
-    const int64_t s = s0 + e;
-    const int64_t vb = win[vi], ve = win[vi + 1];
-    if (s + 1 != min(ve, s1)) continue;       // the vertex's piece goes on
-    if (vb >= s0 && ve <= s1) out[static_cast<int64_t>(v0 + vi) * ld_out + t] = m;
-    else if (vb < s0) part_head[span * C3 + t] = m;
-    else part_tail[span * C3 + t] = m;
-    m = -INFINITY;
+  for (int64_t span = blockIdx.x; span < nspans; span += gridDim.x) {
+    const int64_t s0 = span * kMlpSpan;
+    const int64_t s1 = min(s0 + kMlpSpan, total);
+    const int32_t v0 = chunk_first[s0 / chunk];
+    __syncthreads();   // the previous span is done with the LDS rows
+    load_window(offsets, n, v0, W, win);
+    __syncthreads();
+    if (t < kMlpSpan) {
+      const int64_t s = s0 + t;
+      int32_t p = -1, vi = 0, code = -1;
+      if (s < s1) {
+        p = entries[s] >> 2;
+        vi = window_vertex(win, W, s);
+        const int64_t vb = win[vi], ve = win[vi + 1];
+        if (s + 1 == min(ve, s1)) code = 4 * vi + ((vb >= s0 && ve <= s1) ? 0 : (vb < s0 ? 1 : 2));
+      }
+      rp[t] = p;
+      rv[t] = vi;
+      rc[t] = code;
+    }
+    __syncthreads();
+
+    // input rows of this wave's 16 entries: [g - mu (fp64, rounded once), 0, f]
+    for (int i = lane; i < 16 * K1; i += 64) {
+      const int r = i / K1, k = i - r * K1;
+      const int e = wave * 16 + r;
+      const int32_t p = rp[e];
+      float v = 0.f;
+      if (p >= 0) {
+        if (k < 3) {
+          const double4 m = mu[v0 + rv[e]];
+          const double mk = k == 0 ? m.x : (k == 1 ? m.y : m.z);
+          v = static_cast<float>(static_cast<double>(pos[3 * static_cast<int64_t>(p) + k]) - mk);
+        } else if (k >= 4 && k - 4 < cf) {
+          v = feat[static_cast<int64_t>(p) * ld_feat + (k - 4)];
+        }
+      }
+      X[r * lay.ldx + k] = v;
+    }
+    // X, H1 and H2 are this wave's own rows: LDS accesses of one wave take
+    // effect in order, so a wave-level fence (no workgroup barrier) orders
+    // each layer's writes before the next layer's reads
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // layer 1, ReLU applied when the rows are read by layer 2
+    for (int n0 = 0; n0 < C1; n0 += 16) {
+      const f32x4 a = tile_mma(X, lay.ldx, w1, lay.ld1, K1, n0, lane);
+      for (int r = 0; r < 4; ++r) H1[(4 * lg + r) * lay.ldh + n0 + li] = fmaxf(a[r] + bs[n0 + li], 0.f);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int n0 = 0; n0 < C2; n0 += 16) {
+      const f32x4 a = tile_mma(H1, lay.ldh, w2, lay.ld2, C1, n0, lane);
+      for (int r = 0; r < 4; ++r) H2[(4 * lg + r) * lay.ldh + n0 + li] = fmaxf(a[r] + bs[C1 + n0 + li], 0.f);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int n0 = 0; n0 < C3; n0 += 16) {
+      const f32x4 a = tile_mma(H2, lay.ldh, w3, lay.ld3, C2, n0, lane);
+      for (int r = 0; r < 4; ++r)
+        O[(wave * 16 + 4 * lg + r) * lay.ldo + n0 + li] = a[r] + bs[C1 + C2 + n0 + li];
+    }
+    __syncthreads();
+
+    // per-channel maximum over each vertex's rows in the span; the end codes
+    // mark the last row of every vertex's piece
+    if (t < C3) {
+      const int rows = static_cast<int>(s1 - s0);
+      float m = -INFINITY;
+#pragma unroll 8
+      for (int e = 0; e < rows; ++e) {
+        m = fmaxf(m, O[e * lay.ldo + t]);
+        const int32_t code = rc[e];
+        if (code < 0) continue;
+        const int kind = code & 3, vi = code >> 2;
+        if (kind == 0) out[static_cast<int64_t>(v0 + vi) * ld_out + t] = m;
+        else if (kind == 1) part_head[span * C3 + t] = m;
+        else part_tail[span * C3 + t] = m;
+        m = -INFINITY;
+      }
+    }
   }
 }
 
@@ -342,9 +371,10 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
                               static_cast<int>(worst.bytes()));
     lds_limit_set = true;
   }
-  launch(k_dist_mlp, dim3(static_cast<unsigned>(mlp_spans)), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s,
-         offsets, entries, chunk_first, chunk, n, total, pos, feat, ld_feat, cf, static_cast<const double4*>(mu4), W1,
-         b1, W2, b2, W3, b3, K1, C1, C2, C3, out, ld_out, ph, pt);
+  const unsigned grid = static_cast<unsigned>(std::min<int64_t>(mlp_spans, 2048));
+  launch(k_dist_mlp, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s, offsets, entries, chunk_first,
+         chunk, n, total, pos, feat, ld_feat, cf, static_cast<const double4*>(mu4), W1, b1, W2, b2, W3, b3, K1, C1, C2,
+         C3, out, ld_out, ph, pt, mlp_spans);
   if (mlp_spans > 1) {
     const int64_t threads = mlp_spans * C3;
     launch(k_dist_max_finish, dim3(static_cast<unsigned>((threads + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
