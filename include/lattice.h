@@ -180,7 +180,7 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
  *   b*_dev    optional C1 / C2 / C3 float32 biases (NULL = 0).
  *   C1, C2, C3  multiples of 16, at most 64 (the paper uses 16, 32, 64).
  *   out_dev   n x C3 float32, row stride ld_out (0 = C3).
- * Uses a work space of O(n + 4m / 64 * C3) from the library's pool.
+ * Uses a work space of O(n + 4m / 256) from the library's pool.
  */
 int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* feat_dev, int64_t ld_feat,
                                 int Cf, const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,

@@ -3,14 +3,15 @@
 //   x_v = max_{p in J_v} W3 relu(W2 relu(W1 [g_p - mu_v ; f_p] + b1) + b2) + b3,
 //   mu_v = mean of g_p over J_v.
 // J_v are the vertex lists built with the lattice (entries grouped by vertex).
-// Both per-vertex reductions (the mean and the maximum) run over spans of
-// consecutive list entries, so the work is balanced however skewed the list
-// lengths are: a vertex inside a span is finished there; the vertex a span
-// starts inside and the vertex that runs past its end leave a head and a tail
-// partial, which a finishing pass joins in span order.  The mean is summed in
-// fp64 (positions can be tens of metres from the origin while g - mu is a
-// fraction of sigma) and g - mu is rounded to fp32 once; the three 1x1
-// layers run on v_mfma_f32_16x16x4_f32, 16 list entries per wave.
+// The mean runs over spans of 256 consecutive list entries, so the work is
+// balanced however skewed the list lengths are: a vertex inside a span is
+// finished there; the vertex a span starts inside and the vertex that runs
+// past its end leave a head and a tail partial, which a finishing pass joins
+// in span order.  The mean is summed in fp64 (positions can be tens of
+// metres from the origin while g - mu is a fraction of sigma) and g - mu is
+// rounded to fp32 once.  The three 1x1 layers run on
+// v_mfma_f32_16x16x4_f32 with the activations held in registers; each wave
+// takes an equal range of list entries and reduces the maximum across lanes.
 #include <algorithm>
 
 #include "lattice_internal.h"
@@ -20,7 +21,6 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kMeanSpan = kBlock;  // list entries per workgroup of the mean pass
-constexpr int kMlpSpan = 64;       // list entries per workgroup of the MLP pass (16 per wave)
 constexpr int kMaxC = 64;          // widest 1x1 layer
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -53,7 +53,7 @@ __global__ void __launch_bounds__(kBlock)
 k_dist_mean(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
             const int32_t* __restrict__ chunk_first, int chunk, int64_t n, int64_t total,
             const float* __restrict__ pos, double4* __restrict__ mu, double4* __restrict__ part_head,
-            double4* __restrict__ part_tail) {
+            double4* __restrict__ part_tail, int64_t R, float* __restrict__ out, int64_t ld_out, int C3) {
   constexpr int W = kMeanSpan + 2;
   __shared__ int32_t win[W];
   __shared__ double sx[2][kBlock], sy[2][kBlock], sz[2][kBlock];
@@ -101,6 +101,12 @@ k_dist_mean(const int32_t* __restrict__ offsets, const int32_t* __restrict__ ent
   if (!live) return;
   const int64_t vb = win[vi], ve = win[vi + 1];
   if (s + 1 != min(ve, s1)) return;            // not the last entry of its piece
+  if (vb >= s0 && (ve - 1) / R != vb / R) {
+    // the list is cut by a range boundary of the MLP pass, whose maximum
+    // over it is then taken atomically into this row
+    float* o = out + static_cast<int64_t>(v0 + vi) * ld_out;
+    for (int c = 0; c < C3; ++c) o[c] = -INFINITY;
+  }
   const double4 sum = make_double4(sx[cur][t], sy[cur][t], sz[cur][t], 0.0);
   if (vb >= s0 && ve <= s1) {
     const double inv = 1.0 / static_cast<double>(ve - vb);
@@ -136,251 +142,348 @@ k_dist_mean_finish(const int32_t* __restrict__ offsets, const int32_t* __restric
 }
 
 // ---- the three 1x1 layers and the maximum over J_v ----
-// LDS: weights as [k][n] (n contiguous) for the B operand, per-wave input
-// rows X (16 x K1), per-wave hidden rows H (16 x max(C1, C2)) twice, and the
-// workgroup's output rows (64 x C3).
+// A wave owns the list entries [r0, r0 + R) and walks them 64 at a time (one
+// entry per lane for the gathers), then 16 at a time through the layers.
+// The activations stay in registers: with A = weights (16 outputs x 4
+// inputs) and B = activations transposed (4 inputs x 16 entries),
+// v_mfma_f32_16x16x4_f32 leaves in lane (entry i, group g) the outputs
+// 4g..4g+3 of entry i, which is the B operand of the next layer once that
+// layer takes its inputs in the order (block b, register r): input
+// 16b + 4g + r in lane group g.  The weights sit in LDS in that fragment
+// order, one 64-float run per k step, so every A read is one conflict-free
+// ds_read_b32.  The maximum over J_v is a segmented scan across the 16
+// entry lanes (lists are contiguous and sorted by vertex); the segment
+// still open at the end of 16 entries is carried into the next 16.  A list
+// cut by a range boundary is finished with an order-independent atomic
+// maximum on a row the mean pass set to -inf; every other list is stored.
+constexpr int kWaves = kBlock / 64;
+constexpr int kMaxBlocks = kMaxC / 16;
+constexpr int kMaxK1Steps = kMaxC / 4;
+
 struct MlpLds {
-  int k1, c1, c2, c3;
-  int ldx, ldh, ldo, ld1, ld2, ld3;
-  size_t w1, w2, w3, b, x, h1, h2, o, win, rows, end;
-  __host__ __device__ MlpLds(int K1, int C1, int C2, int C3) : k1(K1), c1(C1), c2(C2), c3(C3) {
-    // every row pitch is odd, so the 4 k rows read by one MFMA operand load
-    // fall in different LDS banks
-    ldx = K1 + 1;
-    ldh = (C1 > C2 ? C1 : C2) + 1;
-    ldo = C3 + 1;
-    ld1 = C1 + 1;
-    ld2 = C2 + 1;
-    ld3 = C3 + 1;
-    w1 = 0;
-    w2 = w1 + static_cast<size_t>(K1) * ld1;
-    w3 = w2 + static_cast<size_t>(C1) * ld2;
-    b = w3 + static_cast<size_t>(C2) * ld3;
-    x = b + C1 + C2 + C3;
-    h1 = x + 4 * 16 * static_cast<size_t>(ldx);
-    h2 = h1 + 4 * 16 * static_cast<size_t>(ldh);
-    o = h2 + 4 * 16 * static_cast<size_t>(ldh);
-    win = o + kMlpSpan * static_cast<size_t>(ldo);   // int32 from here on
-    rows = win + kMlpSpan + 2;                         // per entry: point, window index, end code
-    end = rows + 3 * kMlpSpan;
+  size_t a1, a2, a3, b, x, end;   // in floats
+  __host__ __device__ MlpLds(int ks1, int nb1, int nb2, int nb3) {
+    a1 = 0;
+    a2 = a1 + static_cast<size_t>(nb1) * ks1 * 64;
+    a3 = a2 + static_cast<size_t>(nb2) * nb1 * 4 * 64;
+    b = a3 + static_cast<size_t>(nb3) * nb2 * 4 * 64;
+    x = b + 16 * static_cast<size_t>(nb1 + nb2 + nb3);
+    end = x + static_cast<size_t>(kWaves) * 4 * ks1 * 64;   // per wave: 4 groups of 16 entries x ks1 k steps
   }
   __host__ __device__ size_t bytes() const { return end * 4; }
 };
 
-// One 16 x 16 output tile of a wave: sum over k of A[16 x K] (LDS, row
-// pitch lda) times B[K x N] (LDS, [k][n], pitch ldb) for columns n0..n0+15.
-__device__ inline f32x4 tile_mma(const float* A, int lda, const float* B, int ldb, int K, int n0, int lane) {
-  const int li = lane & 15, lg = lane >> 4;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int k0 = 0; k0 < K; k0 += 4)
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A[li * lda + k0 + lg], B[(k0 + lg) * ldb + n0 + li], acc, 0, 0, 0);
-  return acc;
+__device__ inline f32x4 mfma4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-// Persistent: a workgroup stages the weights once and takes spans
-// blockIdx.x, blockIdx.x + gridDim.x, ...
-__global__ void __launch_bounds__(kBlock)
-k_dist_mlp(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
-           const int32_t* __restrict__ chunk_first, int chunk, int64_t n, int64_t total,
+// value of the lane D places lower in the same row of 16 lanes (row_shr:D);
+// lanes without a source keep their own value
+template <int D>
+__device__ inline float from_lower(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v),
+                                                                0x110 + D, 0xf, 0xf, false));
+}
+template <int D>
+__device__ inline int from_lower(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, 0x110 + D, 0xf, 0xf, false);
+}
+// value of the next lane in the same row of 16 lanes (row_shl:1)
+__device__ inline int from_next(int v) { return __builtin_amdgcn_update_dpp(v, v, 0x101, 0xf, 0xf, false); }
+
+// max into *a for any mix of signs: non-negative floats order like their bit
+// patterns as signed integers, negative ones inversely as unsigned integers
+__device__ inline void atomic_max_f32(float* a, float x) {
+  const unsigned u = __float_as_uint(x);
+  if (u >> 31) atomicMin(reinterpret_cast<unsigned*>(a), u);
+  else atomicMax(reinterpret_cast<int*>(a), static_cast<int>(u));
+}
+
+// The 4 lanes of one entry row hold its outputs (lane group g: columns
+// 16 nb + 4 g + r); write the first c3 of them as the result of vertex v.
+template <int NB>
+__device__ inline void emit_row(float* __restrict__ out, int64_t ld_out, int32_t v, bool shared, const f32x4* val,
+                                int c3, int lg) {
+  float* o = out + static_cast<int64_t>(v) * ld_out;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int c = 16 * nb + 4 * lg + r;
+      if (c >= c3) continue;
+      if (shared) atomic_max_f32(o + c, val[nb][r]);
+      else o[c] = val[nb][r];
+    }
+}
+
+// dst[q] = f(q) for q < count, BATCH independent loads in flight per thread
+template <int BATCH, class F>
+__device__ inline void stage(float* dst, int count, F f) {
+  for (int q0 = threadIdx.x; q0 < count; q0 += BATCH * kBlock) {
+    float v[BATCH];
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int q = q0 + j * kBlock;
+      v[j] = q < count ? f(q) : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int q = q0 + j * kBlock;
+      if (q < count) dst[q] = v[j];
+    }
+  }
+}
+
+// NB1..NB3: blocks of 16 outputs per layer, KS1: k steps of the first layer
+// (0 = the runtime ks1); layers narrower than the instance run zero-padded
+// (zero weights and biases: the padded hidden units are relu(0) = 0 and the
+// padded outputs are not written).  WPE: waves per SIMD the register
+// allocation must allow.
+template <int NB1, int NB2, int NB3, int KS1, int WPE>
+__global__ void __launch_bounds__(kBlock, WPE)
+k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx, int64_t total, int64_t R,
            const float* __restrict__ pos, const float* __restrict__ feat, int64_t ld_feat, int cf,
            const double4* __restrict__ mu, const float* __restrict__ W1, const float* __restrict__ b1,
            const float* __restrict__ W2, const float* __restrict__ b2, const float* __restrict__ W3,
-           const float* __restrict__ b3, int K1, int C1, int C2, int C3, float* __restrict__ out,
-           int64_t ld_out, float* __restrict__ part_head, float* __restrict__ part_tail, int64_t nspans) {
+           const float* __restrict__ b3, int ks1_rt, int c1, int c2, int c3, float* __restrict__ out,
+           int64_t ld_out) {
   extern __shared__ __align__(16) float sm[];
-  const MlpLds lay(K1, C1, C2, C3);
-  float* w1 = sm + lay.w1;
-  float* w2 = sm + lay.w2;
-  float* w3 = sm + lay.w3;
-  float* bs = sm + lay.b;
-  int32_t* win = reinterpret_cast<int32_t*>(sm + lay.win);
-  int32_t* rp = reinterpret_cast<int32_t*>(sm + lay.rows);   // point of each entry
-  int32_t* rv = rp + kMlpSpan;                                // window index of its vertex
-  int32_t* rc = rv + kMlpSpan;                                // end code: -1, or 4 * window index + kind
+  const int ks1 = KS1 > 0 ? KS1 : ks1_rt;
+  const MlpLds lay(ks1, NB1, NB2, NB3);
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int li = lane & 15, lg = lane >> 4;
-  constexpr int W = kMlpSpan + 2;
 
-  // weights, transposed to [k][n]; input k of the first layer: 0..2 the
-  // coordinates, 3 a zero pad, 4.. the features
+  // weight fragments: run (nb, k step) holds, for lane (i, g), the weight of
+  // output 16 nb + i and the k step's input for lane group g
   const int cin = 3 + cf;
-  for (int i = t; i < K1 * C1; i += kBlock) {
-    const int k = i / C1, o = i - k * C1;
+  stage<8>(sm + lay.a1, NB1 * ks1 * 64, [&](int q) {
+    const int run = q >> 6, L = q & 63;
+    const int nb = run / ks1, ks = run - nb * ks1;
+    const int o = 16 * nb + (L & 15);
+    const int k = 4 * ks + (L >> 4);   // 0..2 coordinates, 3 a zero pad, 4.. features
     const int src = k < 3 ? k : (k == 3 ? -1 : (k - 4 < cf ? k - 1 : -1));
-    w1[k * lay.ld1 + o] = src >= 0 ? W1[o * cin + src] : 0.f;
-  }
-  for (int i = t; i < C1 * C2; i += kBlock) {
-    const int k = i / C2, o = i - k * C2;
-    w2[k * lay.ld2 + o] = W2[o * C1 + k];
-  }
-  for (int i = t; i < C2 * C3; i += kBlock) {
-    const int k = i / C3, o = i - k * C3;
-    w3[k * lay.ld3 + o] = W3[o * C2 + k];
-  }
-  for (int i = t; i < C1 + C2 + C3; i += kBlock) {
-    float v = 0.f;
-    if (i < C1) v = b1 ? b1[i] : 0.f;
-    else if (i < C1 + C2) v = b2 ? b2[i - C1] : 0.f;
-    else v = b3 ? b3[i - C1 - C2] : 0.f;
-    bs[i] = v;
-  }
-  float* X = sm + lay.x + wave * 16 * lay.ldx;
-  float* H1 = sm + lay.h1 + wave * 16 * lay.ldh;
-  float* H2 = sm + lay.h2 + wave * 16 * lay.ldh;
-  float* O = sm + lay.o;
+    return (o < c1 && src >= 0) ? W1[o * cin + src] : 0.f;
+  });
+  // layers 2 and 3: the 4 k steps (kb, r = 0..3) of input block kb are
+  // consecutive per lane, one ds_read_b128 per (nb, kb)
+  stage<8>(sm + lay.a2, NB2 * NB1 * 4 * 64, [&](int q) {
+    const int r = q & 3, L = (q >> 2) & 63, run = q >> 8;
+    const int nb = run / NB1, kb = run - nb * NB1;
+    const int o = 16 * nb + (L & 15), k = 16 * kb + 4 * (L >> 4) + r;
+    return (o < c2 && k < c1) ? W2[o * c1 + k] : 0.f;
+  });
+  stage<8>(sm + lay.a3, NB3 * NB2 * 4 * 64, [&](int q) {
+    const int r = q & 3, L = (q >> 2) & 63, run = q >> 8;
+    const int nb = run / NB2, kb = run - nb * NB2;
+    const int o = 16 * nb + (L & 15), k = 16 * kb + 4 * (L >> 4) + r;
+    return (o < c3 && k < c2) ? W3[o * c2 + k] : 0.f;
+  });
+  stage<2>(sm + lay.b, 16 * (NB1 + NB2 + NB3), [&](int i) {
+    if (i < 16 * NB1) return (i < c1 && b1) ? b1[i] : 0.f;
+    i -= 16 * NB1;
+    if (i < 16 * NB2) return (i < c2 && b2) ? b2[i] : 0.f;
+    i -= 16 * NB2;
+    return (i < c3 && b3) ? b3[i] : 0.f;
+  });
+  __syncthreads();
 
-  for (int64_t span = blockIdx.x; span < nspans; span += gridDim.x) {
-    const int64_t s0 = span * kMlpSpan;
-    const int64_t s1 = min(s0 + kMlpSpan, total);
-    const int32_t v0 = chunk_first[s0 / chunk];
-    __syncthreads();   // the previous span is done with the LDS rows
-    load_window(offsets, n, v0, W, win);
-    __syncthreads();
-    if (t < kMlpSpan) {
-      const int64_t s = s0 + t;
-      int32_t p = -1, vi = 0, code = -1;
-      if (s < s1) {
-        p = entries[s] >> 2;
-        vi = window_vertex(win, W, s);
-        const int64_t vb = win[vi], ve = win[vi + 1];
-        if (s + 1 == min(ve, s1)) code = 4 * vi + ((vb >= s0 && ve <= s1) ? 0 : (vb < s0 ? 1 : 2));
+  const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kWaves + wave) * R;
+  if (r0 >= total) return;
+  const int64_t r1 = min(r0 + R, total);
+  // the vertices whose lists run past the range's two ends
+  const int32_t key_before = r0 > 0 ? idx[entries[r0 - 1]] : -1;
+  const int32_t key_after = r1 < total ? idx[entries[r1]] : -1;
+  const float* A1 = sm + lay.a1 + lane;
+  const f32x4* A2 = reinterpret_cast<const f32x4*>(sm + lay.a2) + lane;
+  const f32x4* A3 = reinterpret_cast<const f32x4*>(sm + lay.a3) + lane;
+  const float* bias = sm + lay.b + 4 * lg;
+  float* X = sm + lay.x + static_cast<size_t>(wave) * 4 * ks1 * 64;
+
+  int32_t ckey = -1;   // vertex of the segment carried from the previous 16 entries
+  f32x4 carry[NB3];
+#pragma unroll
+  for (int nb = 0; nb < NB3; ++nb) carry[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int64_t base = r0; base < r1; base += 64) {
+    // rows [g - mu (fp64, rounded once), 0, f] of 64 entries, one per lane,
+    // stored as B fragments: group lane/16, k step k/4, slot 16 (k%4) + lane%16
+    const int64_t s = base + lane;
+    int32_t v = -1;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // the last group's reads of X come first
+    {
+      float* xs = X + (lane >> 4) * ks1 * 64 + (lane & 15);
+      if (s < r1) {
+        const int32_t e = entries[s];
+        v = idx[e];
+        const int64_t p = e >> 2;
+        const double4 m = mu[v];
+        xs[0] = static_cast<float>(static_cast<double>(pos[3 * p]) - m.x);
+        xs[16] = static_cast<float>(static_cast<double>(pos[3 * p + 1]) - m.y);
+        xs[32] = static_cast<float>(static_cast<double>(pos[3 * p + 2]) - m.z);
+        xs[48] = 0.f;
+        for (int k = 4; k < 4 * ks1; ++k)
+          xs[(k >> 2) * 64 + (k & 3) * 16] = k - 4 < cf ? feat[p * ld_feat + (k - 4)] : 0.f;
+      } else {
+        for (int k = 0; k < 4 * ks1; ++k) xs[(k >> 2) * 64 + (k & 3) * 16] = 0.f;
       }
-      rp[t] = p;
-      rv[t] = vi;
-      rc[t] = code;
     }
-    __syncthreads();
+    // a wave's LDS accesses take effect in order; the fence keeps the
+    // compiler from moving the reads above the writes
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    // input rows of this wave's 16 entries: [g - mu (fp64, rounded once), 0, f]
-    for (int i = lane; i < 16 * K1; i += 64) {
-      const int r = i / K1, k = i - r * K1;
-      const int e = wave * 16 + r;
-      const int32_t p = rp[e];
-      float v = 0.f;
-      if (p >= 0) {
-        if (k < 3) {
-          const double4 m = mu[v0 + rv[e]];
-          const double mk = k == 0 ? m.x : (k == 1 ? m.y : m.z);
-          v = static_cast<float>(static_cast<double>(pos[3 * static_cast<int64_t>(p) + k]) - mk);
-        } else if (k >= 4 && k - 4 < cf) {
-          v = feat[static_cast<int64_t>(p) * ld_feat + (k - 4)];
+    const int groups = static_cast<int>(min<int64_t>(4, (r1 - base + 15) / 16));
+    for (int grp = 0; grp < groups; ++grp) {
+      // weights and biases are read from LDS again for every 16 entries
+      // (this compiler barrier stops them from being hoisted into registers
+      // for the whole loop, which would halve the resident waves)
+      __asm__ volatile("" ::: "memory");
+      const int32_t key = __shfl(v, 16 * grp + li);   // vertex of entry row li (-1 past the range)
+      f32x4 h1[NB1], h2[NB2], o3[NB3];
+#pragma unroll
+      for (int nb = 0; nb < NB1; ++nb) h1[nb] = *reinterpret_cast<const f32x4*>(bias + 16 * nb);
+      const float* xg = X + grp * ks1 * 64 + lane;
+#pragma unroll
+      for (int ks = 0; ks < (KS1 > 0 ? KS1 : 1); ++ks) {
+        // KS1 = 0: the loop below runs the runtime count instead
+        if (KS1 == 0) break;
+        const float x = xg[ks * 64];
+#pragma unroll
+        for (int nb = 0; nb < NB1; ++nb) h1[nb] = mfma4(A1[(nb * ks1 + ks) * 64], x, h1[nb]);
+      }
+      if (KS1 == 0)
+        for (int ks = 0; ks < ks1; ++ks) {
+          const float x = xg[ks * 64];
+#pragma unroll
+          for (int nb = 0; nb < NB1; ++nb) h1[nb] = mfma4(A1[(nb * ks1 + ks) * 64], x, h1[nb]);
+        }
+#pragma unroll
+      for (int nb = 0; nb < NB2; ++nb) h2[nb] = *reinterpret_cast<const f32x4*>(bias + 16 * NB1 + 16 * nb);
+#pragma unroll
+      for (int kb = 0; kb < NB1; ++kb) {
+        f32x4 w[NB2];
+#pragma unroll
+        for (int nb = 0; nb < NB2; ++nb) w[nb] = A2[(nb * NB1 + kb) * 64];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float x = fmaxf(h1[kb][r], 0.f);
+#pragma unroll
+          for (int nb = 0; nb < NB2; ++nb) h2[nb] = mfma4(w[nb][r], x, h2[nb]);
         }
       }
-      X[r * lay.ldx + k] = v;
-    }
-    // X, H1 and H2 are this wave's own rows: LDS accesses of one wave take
-    // effect in order, so a wave-level fence (no workgroup barrier) orders
-    // each layer's writes before the next layer's reads
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // layer 1, ReLU applied when the rows are read by layer 2
-    for (int n0 = 0; n0 < C1; n0 += 16) {
-      const f32x4 a = tile_mma(X, lay.ldx, w1, lay.ld1, K1, n0, lane);
-      for (int r = 0; r < 4; ++r) H1[(4 * lg + r) * lay.ldh + n0 + li] = fmaxf(a[r] + bs[n0 + li], 0.f);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    for (int n0 = 0; n0 < C2; n0 += 16) {
-      const f32x4 a = tile_mma(H1, lay.ldh, w2, lay.ld2, C1, n0, lane);
-      for (int r = 0; r < 4; ++r) H2[(4 * lg + r) * lay.ldh + n0 + li] = fmaxf(a[r] + bs[C1 + n0 + li], 0.f);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    for (int n0 = 0; n0 < C3; n0 += 16) {
-      const f32x4 a = tile_mma(H2, lay.ldh, w3, lay.ld3, C2, n0, lane);
-      for (int r = 0; r < 4; ++r)
-        O[(wave * 16 + 4 * lg + r) * lay.ldo + n0 + li] = a[r] + bs[C1 + C2 + n0 + li];
-    }
-    __syncthreads();
-
-    // per-channel maximum over each vertex's rows in the span; the end codes
-    // mark the last row of every vertex's piece
-    if (t < C3) {
-      const int rows = static_cast<int>(s1 - s0);
-      float m = -INFINITY;
-#pragma unroll 8
-      for (int e = 0; e < rows; ++e) {
-        m = fmaxf(m, O[e * lay.ldo + t]);
-        const int32_t code = rc[e];
-        if (code < 0) continue;
-        const int kind = code & 3, vi = code >> 2;
-        if (kind == 0) out[static_cast<int64_t>(v0 + vi) * ld_out + t] = m;
-        else if (kind == 1) part_head[span * C3 + t] = m;
-        else part_tail[span * C3 + t] = m;
-        m = -INFINITY;
+#pragma unroll
+      for (int nb = 0; nb < NB3; ++nb)
+        o3[nb] = *reinterpret_cast<const f32x4*>(bias + 16 * (NB1 + NB2) + 16 * nb);
+#pragma unroll
+      for (int kb = 0; kb < NB2; ++kb) {
+        f32x4 w[NB3];
+#pragma unroll
+        for (int nb = 0; nb < NB3; ++nb) w[nb] = A3[(nb * NB2 + kb) * 64];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float x = fmaxf(h2[kb][r], 0.f);
+#pragma unroll
+          for (int nb = 0; nb < NB3; ++nb) o3[nb] = mfma4(w[nb][r], x, o3[nb]);
+        }
       }
+
+      // segmented inclusive max over the 16 entry rows (Hillis-Steele; rows
+      // of one vertex are contiguous)
+#define DIST_SCAN_STEP(D)                                       \
+  {                                                             \
+    const int kd = from_lower<D>(key);                          \
+    const bool take = li >= (D) && kd == key;                   \
+    _Pragma("unroll") for (int nb = 0; nb < NB3; ++nb)          \
+      _Pragma("unroll") for (int r = 0; r < 4; ++r) {           \
+        const float o = from_lower<D>(o3[nb][r]);               \
+        o3[nb][r] = take ? fmaxf(o3[nb][r], o) : o3[nb][r];     \
+      }                                                         \
+  }
+      DIST_SCAN_STEP(1)
+      DIST_SCAN_STEP(2)
+      DIST_SCAN_STEP(4)
+      DIST_SCAN_STEP(8)
+#undef DIST_SCAN_STEP
+
+      // the carried segment: joins the leading rows of its vertex, or ended
+      // with the previous 16 entries
+      if (ckey >= 0) {
+        const int32_t k0 = __shfl(key, 0);
+        if (key == ckey) {
+#pragma unroll
+          for (int nb = 0; nb < NB3; ++nb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) o3[nb][r] = fmaxf(o3[nb][r], carry[nb][r]);
+        }
+        if (k0 != ckey && li == 0) emit_row<NB3>(out, ld_out, ckey, ckey == key_before || ckey == key_after, carry, c3, lg);
+      }
+      // segments that end inside these 16 rows; row 15's segment is carried
+      const int32_t nk = from_next(key);
+      if (li < 15 && key >= 0 && nk != key)
+        emit_row<NB3>(out, ld_out, key, key == key_before || key == key_after, o3, c3, lg);
+      ckey = __shfl(key, 15);
+#pragma unroll
+      for (int nb = 0; nb < NB3; ++nb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) carry[nb][r] = __shfl(o3[nb][r], 16 * lg + 15);
     }
   }
-}
-
-__global__ void __launch_bounds__(kBlock)
-k_dist_max_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ chunk_first, int chunk,
-                  int64_t nspans, int C3, float* __restrict__ out, int64_t ld_out,
-                  const float* __restrict__ part_head, const float* __restrict__ part_tail) {
-  const int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  const int64_t c = g / C3;
-  const int ch = static_cast<int>(g - c * C3);
-  if (c + 1 >= nspans) return;
-  const int64_t s0 = c * kMlpSpan, s1 = s0 + kMlpSpan;
-  const int32_t v = chunk_first[s1 / chunk];
-  const int64_t vb = offsets[v];
-  if (!(vb >= s0 && vb < s1)) return;
-  const int64_t ve = offsets[v + 1];
-  const int64_t last = (ve - 1) / kMlpSpan;
-  float m = part_tail[c * C3 + ch];
-  for (int64_t c2 = c + 1; c2 <= last; ++c2) m = fmaxf(m, part_head[c2 * C3 + ch]);
-  out[static_cast<int64_t>(v) * ld_out + ch] = m;
+  if (ckey >= 0 && li == 0) emit_row<NB3>(out, ld_out, ckey, ckey == key_before || ckey == key_after, carry, c3, lg);
 }
 
 }  // namespace
 
 int64_t distribute_workspace_bytes(int64_t total, int C3) {
+  (void)C3;
   const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
-  const int64_t mlp_spans = (total + kMlpSpan - 1) / kMlpSpan;
-  return 2 * mean_spans * static_cast<int64_t>(sizeof(double4)) + 2 * mlp_spans * C3 * 4;
+  return 2 * mean_spans * static_cast<int64_t>(sizeof(double4));
 }
 
 int distribute_max_features() { return kMaxC - 4; }
 
-void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* chunk_first, int chunk,
-                       int64_t n, int64_t total, const float* pos, const float* feat, int64_t ld_feat, int cf,
-                       const float* W1, const float* b1, int C1, const float* W2, const float* b2, int C2,
-                       const float* W3, const float* b3, int C3, float* out, int64_t ld_out, double* mu,
-                       void* work, hipStream_t s) {
+// Entries per wave of the MLP pass: a multiple of 64, about 4 resident waves
+// per SIMD (1024 SIMDs) over the whole list.
+int64_t distribute_range(int64_t total) {
+  const int64_t groups = (total + 63) / 64;
+  constexpr int64_t kTargetWaves = 4096;
+  return 64 * ((groups + kTargetWaves - 1) / kTargetWaves);
+}
+
+void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* idx,
+                       const int32_t* chunk_first, int chunk, int64_t n, int64_t total, const float* pos,
+                       const float* feat, int64_t ld_feat, int cf, const float* W1, const float* b1, int C1,
+                       const float* W2, const float* b2, int C2, const float* W3, const float* b3, int C3, float* out,
+                       int64_t ld_out, double* mu, void* work, hipStream_t s) {
   if (total <= 0 || n <= 0) return;
   ScopedKernelTimer tm("distribute", s);
   const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
-  const int64_t mlp_spans = (total + kMlpSpan - 1) / kMlpSpan;
+  const int64_t R = distribute_range(total);
   double4* mh = static_cast<double4*>(work);
   double4* mt = mh + mean_spans;
-  float* ph = reinterpret_cast<float*>(mt + mean_spans);
-  float* pt = ph + mlp_spans * C3;
   double4* mu4 = reinterpret_cast<double4*>(mu);
   launch(k_dist_mean, dim3(static_cast<unsigned>(mean_spans)), dim3(kBlock), 0, s, offsets, entries, chunk_first,
-         chunk, n, total, pos, mu4, mh, mt);
+         chunk, n, total, pos, mu4, mh, mt, R, out, ld_out, C3);
   if (mean_spans > 1)
     launch(k_dist_mean_finish, dim3(static_cast<unsigned>((mean_spans + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
            offsets, chunk_first, chunk, mean_spans, mu4, static_cast<const double4*>(mh),
            static_cast<const double4*>(mt));
-  const int K1 = ((3 + cf) + 1 + 3) / 4 * 4;   // coordinates, a zero pad, features; multiple of 4
-  const MlpLds lay(K1, C1, C2, C3);
+  const int ks1 = (4 + cf + 3) / 4;   // coordinates, a zero pad, features, in k steps of 4
+  // the paper's 16-32-64 block (up to 4 raw features) has its own instance;
+  // every other shape runs zero-padded to 64-64-64
+  const bool paper = C1 == 16 && C2 == 32 && C3 == 64 && ks1 <= 2;
+  auto kernel = paper ? k_dist_mlp<1, 2, 4, 2, 4> : k_dist_mlp<kMaxBlocks, kMaxBlocks, kMaxBlocks, 0, 1>;
+  const MlpLds lay = paper ? MlpLds(2, 1, 2, 4) : MlpLds(ks1, kMaxBlocks, kMaxBlocks, kMaxBlocks);
   static bool lds_limit_set = false;
   if (!lds_limit_set) {
-    const MlpLds worst(kMaxC, kMaxC, kMaxC, kMaxC);
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_dist_mlp), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              static_cast<int>(worst.bytes()));
+    const MlpLds worst(kMaxK1Steps, kMaxBlocks, kMaxBlocks, kMaxBlocks);
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_dist_mlp<kMaxBlocks, kMaxBlocks, kMaxBlocks, 0, 1>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(worst.bytes()));
     lds_limit_set = true;
   }
-  const unsigned grid = static_cast<unsigned>(std::min<int64_t>(mlp_spans, 2048));
-  launch(k_dist_mlp, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s, offsets, entries, chunk_first,
-         chunk, n, total, pos, feat, ld_feat, cf, static_cast<const double4*>(mu4), W1, b1, W2, b2, W3, b3, K1, C1, C2,
-         C3, out, ld_out, ph, pt, mlp_spans);
-  if (mlp_spans > 1) {
-    const int64_t threads = mlp_spans * C3;
-    launch(k_dist_max_finish, dim3(static_cast<unsigned>((threads + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
-           offsets, chunk_first, chunk, mlp_spans, C3, out, ld_out, static_cast<const float*>(ph),
-           static_cast<const float*>(pt));
-  }
+  const int64_t waves = (total + R - 1) / R;
+  const unsigned grid = static_cast<unsigned>((waves + kWaves - 1) / kWaves);
+  launch(kernel, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s, entries, idx, total, R, pos, feat,
+         ld_feat, cf, static_cast<const double4*>(mu4), W1, b1, W2, b2, W3, b3, ks1, C1, C2, C3, out, ld_out);
 }
 
 }  // namespace lat
