@@ -160,15 +160,18 @@ constexpr int kWaves = kBlock / 64;
 constexpr int kMaxBlocks = kMaxC / 16;
 constexpr int kMaxK1Steps = kMaxC / 4;
 
+constexpr int kTilePitch = 64 + 4;   // row pitch of a wave's 16 x 64 output tile
+
 struct MlpLds {
-  size_t a1, a2, a3, b, x, end;   // in floats
+  size_t a1, a2, a3, b, x, o, end;   // in floats
   __host__ __device__ MlpLds(int ks1, int nb1, int nb2, int nb3) {
     a1 = 0;
     a2 = a1 + static_cast<size_t>(nb1) * ks1 * 64;
     a3 = a2 + static_cast<size_t>(nb2) * nb1 * 4 * 64;
     b = a3 + static_cast<size_t>(nb3) * nb2 * 4 * 64;
     x = b + 16 * static_cast<size_t>(nb1 + nb2 + nb3);
-    end = x + static_cast<size_t>(kWaves) * 4 * ks1 * 64;   // per wave: 4 groups of 16 entries x ks1 k steps
+    o = x + static_cast<size_t>(kWaves) * 4 * ks1 * 64;   // per wave: 4 groups of 16 entries x ks1 k steps
+    end = o + static_cast<size_t>(kWaves) * 16 * kTilePitch;
   }
   __host__ __device__ size_t bytes() const { return end * 4; }
 };
@@ -176,20 +179,6 @@ struct MlpLds {
 __device__ inline f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
-
-// value of the lane D places lower in the same row of 16 lanes (row_shr:D);
-// lanes without a source keep their own value
-template <int D>
-__device__ inline float from_lower(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v),
-                                                                0x110 + D, 0xf, 0xf, false));
-}
-template <int D>
-__device__ inline int from_lower(int v) {
-  return __builtin_amdgcn_update_dpp(v, v, 0x110 + D, 0xf, 0xf, false);
-}
-// value of the next lane in the same row of 16 lanes (row_shl:1)
-__device__ inline int from_next(int v) { return __builtin_amdgcn_update_dpp(v, v, 0x101, 0xf, 0xf, false); }
 
 // max into *a for any mix of signs: non-negative floats order like their bit
 // patterns as signed integers, negative ones inversely as unsigned integers
@@ -199,21 +188,13 @@ __device__ inline void atomic_max_f32(float* a, float x) {
   else atomicMax(reinterpret_cast<int*>(a), static_cast<int>(u));
 }
 
-// The 4 lanes of one entry row hold its outputs (lane group g: columns
-// 16 nb + 4 g + r); write the first c3 of them as the result of vertex v.
-template <int NB>
-__device__ inline void emit_row(float* __restrict__ out, int64_t ld_out, int32_t v, bool shared, const f32x4* val,
-                                int c3, int lg) {
-  float* o = out + static_cast<int64_t>(v) * ld_out;
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int c = 16 * nb + 4 * lg + r;
-      if (c >= c3) continue;
-      if (shared) atomic_max_f32(o + c, val[nb][r]);
-      else o[c] = val[nb][r];
-    }
+// Lane c holds output channel c of vertex v's maximum.
+__device__ inline void emit_col(float* __restrict__ out, int64_t ld_out, int32_t v, bool shared, float m, int c3,
+                                int lane) {
+  if (lane >= c3) return;
+  float* o = out + static_cast<int64_t>(v) * ld_out + lane;
+  if (shared) atomic_max_f32(o, m);
+  else *o = m;
 }
 
 // dst[q] = f(q) for q < count, BATCH independent loads in flight per thread
@@ -299,10 +280,9 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
   const float* bias = sm + lay.b + 4 * lg;
   float* X = sm + lay.x + static_cast<size_t>(wave) * 4 * ks1 * 64;
 
-  int32_t ckey = -1;   // vertex of the segment carried from the previous 16 entries
-  f32x4 carry[NB3];
-#pragma unroll
-  for (int nb = 0; nb < NB3; ++nb) carry[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float* T = sm + lay.o + static_cast<size_t>(wave) * 16 * kTilePitch;
+  int32_t ckey = -1;   // vertex whose maximum is open (wave-uniform)
+  float cmax = 0.f;    // its running maximum, channel `lane`
 
   for (int64_t base = r0; base < r1; base += 64) {
     // rows [g - mu (fp64, rounded once), 0, f] of 64 entries, one per lane,
@@ -338,7 +318,6 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
       // (this compiler barrier stops them from being hoisted into registers
       // for the whole loop, which would halve the resident waves)
       __asm__ volatile("" ::: "memory");
-      const int32_t key = __shfl(v, 16 * grp + li);   // vertex of entry row li (-1 past the range)
       f32x4 h1[NB1], h2[NB2], o3[NB3];
 #pragma unroll
       for (int nb = 0; nb < NB1; ++nb) h1[nb] = *reinterpret_cast<const f32x4*>(bias + 16 * nb);
@@ -387,48 +366,30 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
         }
       }
 
-      // segmented inclusive max over the 16 entry rows (Hillis-Steele; rows
-      // of one vertex are contiguous)
-#define DIST_SCAN_STEP(D)                                       \
-  {                                                             \
-    const int kd = from_lower<D>(key);                          \
-    const bool take = li >= (D) && kd == key;                   \
-    _Pragma("unroll") for (int nb = 0; nb < NB3; ++nb)          \
-      _Pragma("unroll") for (int r = 0; r < 4; ++r) {           \
-        const float o = from_lower<D>(o3[nb][r]);               \
-        o3[nb][r] = take ? fmaxf(o3[nb][r], o) : o3[nb][r];     \
-      }                                                         \
-  }
-      DIST_SCAN_STEP(1)
-      DIST_SCAN_STEP(2)
-      DIST_SCAN_STEP(4)
-      DIST_SCAN_STEP(8)
-#undef DIST_SCAN_STEP
-
-      // the carried segment: joins the leading rows of its vertex, or ended
-      // with the previous 16 entries
-      if (ckey >= 0) {
-        const int32_t k0 = __shfl(key, 0);
-        if (key == ckey) {
+      // the 16 x 64 outputs go through LDS; lane c then walks channel c
+      // down the 16 rows.  Rows of one vertex are contiguous, so a change of
+      // vertex (a wave-uniform test) closes the open maximum.
 #pragma unroll
-          for (int nb = 0; nb < NB3; ++nb)
+      for (int nb = 0; nb < NB3; ++nb) *reinterpret_cast<f32x4*>(T + li * kTilePitch + 16 * nb + 4 * lg) = o3[nb];
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-            for (int r = 0; r < 4; ++r) o3[nb][r] = fmaxf(o3[nb][r], carry[nb][r]);
+      for (int i = 0; i < 16; ++i) {
+        const int32_t key = __builtin_amdgcn_readlane(v, 16 * grp + i);
+        if (key < 0) break;   // past the range
+        const float x = T[i * kTilePitch + lane];
+        if (key != ckey) {
+          if (ckey >= 0) emit_col(out, ld_out, ckey, ckey == key_before || ckey == key_after, cmax, c3, lane);
+          ckey = key;
+          cmax = x;
+        } else {
+          cmax = fmaxf(cmax, x);
         }
-        if (k0 != ckey && li == 0) emit_row<NB3>(out, ld_out, ckey, ckey == key_before || ckey == key_after, carry, c3, lg);
       }
-      // segments that end inside these 16 rows; row 15's segment is carried
-      const int32_t nk = from_next(key);
-      if (li < 15 && key >= 0 && nk != key)
-        emit_row<NB3>(out, ld_out, key, key == key_before || key == key_after, o3, c3, lg);
-      ckey = __shfl(key, 15);
-#pragma unroll
-      for (int nb = 0; nb < NB3; ++nb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) carry[nb][r] = __shfl(o3[nb][r], 16 * lg + 15);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // the walk's reads come before the next tile's writes
     }
   }
-  if (ckey >= 0 && li == 0) emit_row<NB3>(out, ld_out, ckey, ckey == key_before || ckey == key_after, carry, c3, lg);
+  if (ckey >= 0) emit_col(out, ld_out, ckey, ckey == key_before || ckey == key_after, cmax, c3, lane);
 }
 
 }  // namespace
