@@ -160,7 +160,8 @@ constexpr int kWaves = kBlock / 64;
 constexpr int kMaxBlocks = kMaxC / 16;
 constexpr int kMaxK1Steps = kMaxC / 4;
 
-constexpr int kTilePitch = 64 + 4;   // row pitch of a wave's 16 x 64 output tile
+constexpr int kTilePitch = 64 + 4;
+constexpr int kMlpRange = 128;       // list entries per wave of the MLP pass   // row pitch of a wave's 16 x 64 output tile
 
 struct MlpLds {
   size_t a1, a2, a3, b, x, o, end;   // in floats
@@ -215,83 +216,176 @@ __device__ inline void stage(float* dst, int count, F f) {
   }
 }
 
-// NB1..NB3: blocks of 16 outputs per layer, KS1: k steps of the first layer
-// (0 = the runtime ks1); layers narrower than the instance run zero-padded
-// (zero weights and biases: the padded hidden units are relu(0) = 0 and the
-// padded outputs are not written).  WPE: waves per SIMD the register
-// allocation must allow.
+// Fixed-count variant of stage(): the values are loaded into registers by
+// load() and written to LDS by store(), so that other loads can be issued
+// in between.
+template <int COUNT>
+struct Staged {
+  static constexpr int N = (COUNT + kBlock - 1) / kBlock;
+  float v[N];
+  template <class F>
+  __device__ void load(F f) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      const int q = threadIdx.x + j * kBlock;
+      v[j] = q < COUNT ? f(q) : 0.f;
+    }
+  }
+  __device__ void store(float* dst) const {
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      const int q = threadIdx.x + j * kBlock;
+      if (q < COUNT) dst[q] = v[j];
+    }
+  }
+};
+
+// NB1..NB3: blocks of 16 outputs per layer; KS1: k steps of the first layer,
+// or 0 for the runtime ks1.  Layers narrower than the instance run
+// zero-padded (zero weights and biases: the padded hidden units are
+// relu(0) = 0 and the padded outputs are not written).  With KS1 > 0 the
+// whole range's gathers and the weights are loaded into registers before
+// the workgroup's first barrier, so their latencies overlap; with KS1 = 0
+// (any feature count) the rows are gathered into LDS 64 at a time.  WPE:
+// waves per SIMD the register allocation must allow.
 template <int NB1, int NB2, int NB3, int KS1, int WPE>
 __global__ void __launch_bounds__(kBlock, WPE)
-k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx, int64_t total, int64_t R,
+k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx, int64_t total,
            const float* __restrict__ pos, const float* __restrict__ feat, int64_t ld_feat, int cf,
            const double4* __restrict__ mu, const float* __restrict__ W1, const float* __restrict__ b1,
            const float* __restrict__ W2, const float* __restrict__ b2, const float* __restrict__ W3,
            const float* __restrict__ b3, int ks1_rt, int c1, int c2, int c3, float* __restrict__ out,
            int64_t ld_out) {
+  constexpr bool kPre = KS1 > 0;
+  constexpr int kPer = kMlpRange / 64;   // groups of 64 entries per wave
   extern __shared__ __align__(16) float sm[];
-  const int ks1 = KS1 > 0 ? KS1 : ks1_rt;
+  const int ks1 = kPre ? KS1 : ks1_rt;
   const MlpLds lay(ks1, NB1, NB2, NB3);
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int li = lane & 15, lg = lane >> 4;
+  const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kWaves + wave) * kMlpRange;
+  const bool active = r0 < total;
+  const int64_t r1 = active ? min(r0 + kMlpRange, total) : r0;
 
   // weight fragments: run (nb, k step) holds, for lane (i, g), the weight of
   // output 16 nb + i and the k step's input for lane group g
   const int cin = 3 + cf;
-  stage<8>(sm + lay.a1, NB1 * ks1 * 64, [&](int q) {
+  auto w1_at = [&](int q) {
     const int run = q >> 6, L = q & 63;
     const int nb = run / ks1, ks = run - nb * ks1;
     const int o = 16 * nb + (L & 15);
     const int k = 4 * ks + (L >> 4);   // 0..2 coordinates, 3 a zero pad, 4.. features
     const int src = k < 3 ? k : (k == 3 ? -1 : (k - 4 < cf ? k - 1 : -1));
     return (o < c1 && src >= 0) ? W1[o * cin + src] : 0.f;
-  });
+  };
   // layers 2 and 3: the 4 k steps (kb, r = 0..3) of input block kb are
   // consecutive per lane, one ds_read_b128 per (nb, kb)
-  stage<8>(sm + lay.a2, NB2 * NB1 * 4 * 64, [&](int q) {
+  auto w2_at = [&](int q) {
     const int r = q & 3, L = (q >> 2) & 63, run = q >> 8;
     const int nb = run / NB1, kb = run - nb * NB1;
     const int o = 16 * nb + (L & 15), k = 16 * kb + 4 * (L >> 4) + r;
     return (o < c2 && k < c1) ? W2[o * c1 + k] : 0.f;
-  });
-  stage<8>(sm + lay.a3, NB3 * NB2 * 4 * 64, [&](int q) {
+  };
+  auto w3_at = [&](int q) {
     const int r = q & 3, L = (q >> 2) & 63, run = q >> 8;
     const int nb = run / NB2, kb = run - nb * NB2;
     const int o = 16 * nb + (L & 15), k = 16 * kb + 4 * (L >> 4) + r;
     return (o < c3 && k < c2) ? W3[o * c2 + k] : 0.f;
-  });
-  stage<2>(sm + lay.b, 16 * (NB1 + NB2 + NB3), [&](int i) {
+  };
+  auto b_at = [&](int i) {
     if (i < 16 * NB1) return (i < c1 && b1) ? b1[i] : 0.f;
     i -= 16 * NB1;
     if (i < 16 * NB2) return (i < c2 && b2) ? b2[i] : 0.f;
     i -= 16 * NB2;
     return (i < c3 && b3) ? b3[i] : 0.f;
-  });
-  __syncthreads();
+  };
 
-  const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kWaves + wave) * R;
-  if (r0 >= total) return;
-  const int64_t r1 = min(r0 + R, total);
-  // the vertices whose lists run past the range's two ends
-  const int32_t key_before = r0 > 0 ? idx[entries[r0 - 1]] : -1;
-  const int32_t key_after = r1 < total ? idx[entries[r1]] : -1;
+  // per lane: vertex and input row [g - mu (fp64, rounded once), 0, f] of
+  // entry r0 + 64 j + lane (registers only when kPre)
+  constexpr int kRow = kPre ? 4 * KS1 : 1;
+  int32_t vtx[kPer];
+  float xr[kPre ? kPer : 1][kRow];
+  int32_t key_before = -1, key_after = -1;   // the vertices whose lists run past the range's two ends
+  if constexpr (kPre) {
+    Staged<NB1 * KS1 * 64> s1;
+    Staged<NB2 * NB1 * 4 * 64> s2;
+    Staged<NB3 * NB2 * 4 * 64> s3;
+    Staged<16 * (NB1 + NB2 + NB3)> sb;
+    s1.load(w1_at);
+    s2.load(w2_at);
+    s3.load(w3_at);
+    sb.load(b_at);
+    int32_t ent[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int64_t s = r0 + 64 * j + lane;
+      ent[j] = s < r1 ? entries[s] : -1;
+    }
+    const int32_t eb = (active && r0 > 0) ? entries[r0 - 1] : -1;
+    const int32_t ea = (active && r1 < total) ? entries[r1] : -1;
+    float g[kPer][3];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      vtx[j] = ent[j] >= 0 ? idx[ent[j]] : -1;
+      const int64_t p = ent[j] >= 0 ? ent[j] >> 2 : 0;
+#pragma unroll
+      for (int c = 0; c < 3; ++c) g[j][c] = ent[j] >= 0 ? pos[3 * p + c] : 0.f;
+      xr[j][3] = 0.f;
+#pragma unroll
+      for (int f = 0; f < kRow - 4; ++f) xr[j][4 + f] = (ent[j] >= 0 && f < cf) ? feat[p * ld_feat + f] : 0.f;
+    }
+    key_before = eb >= 0 ? idx[eb] : -1;
+    key_after = ea >= 0 ? idx[ea] : -1;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      double4 m = make_double4(0.0, 0.0, 0.0, 0.0);
+      if (vtx[j] >= 0) m = mu[vtx[j]];
+      xr[j][0] = static_cast<float>(static_cast<double>(g[j][0]) - m.x);
+      xr[j][1] = static_cast<float>(static_cast<double>(g[j][1]) - m.y);
+      xr[j][2] = static_cast<float>(static_cast<double>(g[j][2]) - m.z);
+    }
+    s1.store(sm + lay.a1);
+    s2.store(sm + lay.a2);
+    s3.store(sm + lay.a3);
+    sb.store(sm + lay.b);
+  } else {
+    stage<8>(sm + lay.a1, NB1 * ks1 * 64, w1_at);
+    stage<8>(sm + lay.a2, NB2 * NB1 * 4 * 64, w2_at);
+    stage<8>(sm + lay.a3, NB3 * NB2 * 4 * 64, w3_at);
+    stage<2>(sm + lay.b, 16 * (NB1 + NB2 + NB3), b_at);
+    if (active) {
+      key_before = r0 > 0 ? idx[entries[r0 - 1]] : -1;
+      key_after = r1 < total ? idx[entries[r1]] : -1;
+    }
+  }
+  __syncthreads();
+  if (!active) return;
+
   const float* A1 = sm + lay.a1 + lane;
   const f32x4* A2 = reinterpret_cast<const f32x4*>(sm + lay.a2) + lane;
   const f32x4* A3 = reinterpret_cast<const f32x4*>(sm + lay.a3) + lane;
   const float* bias = sm + lay.b + 4 * lg;
   float* X = sm + lay.x + static_cast<size_t>(wave) * 4 * ks1 * 64;
-
   float* T = sm + lay.o + static_cast<size_t>(wave) * 16 * kTilePitch;
   int32_t ckey = -1;   // vertex whose maximum is open (wave-uniform)
   float cmax = 0.f;    // its running maximum, channel `lane`
 
-  for (int64_t base = r0; base < r1; base += 64) {
-    // rows [g - mu (fp64, rounded once), 0, f] of 64 entries, one per lane,
-    // stored as B fragments: group lane/16, k step k/4, slot 16 (k%4) + lane%16
-    const int64_t s = base + lane;
-    int32_t v = -1;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int64_t base = r0 + 64 * j;
+    if (base >= r1) break;
+    // the 64 rows as B fragments: group lane/16, k step k/4, slot
+    // 16 (k%4) + lane%16
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // the last group's reads of X come first
-    {
-      float* xs = X + (lane >> 4) * ks1 * 64 + (lane & 15);
+    float* xs = X + (lane >> 4) * ks1 * 64 + (lane & 15);
+    int32_t v;
+    if constexpr (kPre) {
+      v = vtx[j];
+#pragma unroll
+      for (int k = 0; k < kRow; ++k) xs[(k >> 2) * 64 + (k & 3) * 16] = xr[j][k];
+    } else {
+      const int64_t s = base + lane;
+      v = -1;
       if (s < r1) {
         const int32_t e = entries[s];
         v = idx[e];
@@ -316,26 +410,26 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
     for (int grp = 0; grp < groups; ++grp) {
       // weights and biases are read from LDS again for every 16 entries
       // (this compiler barrier stops them from being hoisted into registers
-      // for the whole loop, which would halve the resident waves)
+      // for the whole loop, which would cut the resident waves)
       __asm__ volatile("" ::: "memory");
       f32x4 h1[NB1], h2[NB2], o3[NB3];
 #pragma unroll
       for (int nb = 0; nb < NB1; ++nb) h1[nb] = *reinterpret_cast<const f32x4*>(bias + 16 * nb);
       const float* xg = X + grp * ks1 * 64 + lane;
+      if constexpr (kPre) {
 #pragma unroll
-      for (int ks = 0; ks < (KS1 > 0 ? KS1 : 1); ++ks) {
-        // KS1 = 0: the loop below runs the runtime count instead
-        if (KS1 == 0) break;
-        const float x = xg[ks * 64];
+        for (int ks = 0; ks < KS1; ++ks) {
+          const float x = xg[ks * 64];
 #pragma unroll
-        for (int nb = 0; nb < NB1; ++nb) h1[nb] = mfma4(A1[(nb * ks1 + ks) * 64], x, h1[nb]);
-      }
-      if (KS1 == 0)
+          for (int nb = 0; nb < NB1; ++nb) h1[nb] = mfma4(A1[(nb * KS1 + ks) * 64], x, h1[nb]);
+        }
+      } else {
         for (int ks = 0; ks < ks1; ++ks) {
           const float x = xg[ks * 64];
 #pragma unroll
           for (int nb = 0; nb < NB1; ++nb) h1[nb] = mfma4(A1[(nb * ks1 + ks) * 64], x, h1[nb]);
         }
+      }
 #pragma unroll
       for (int nb = 0; nb < NB2; ++nb) h2[nb] = *reinterpret_cast<const f32x4*>(bias + 16 * NB1 + 16 * nb);
 #pragma unroll
@@ -367,20 +461,25 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
       }
 
       // the 16 x 64 outputs go through LDS; lane c then walks channel c
-      // down the 16 rows.  Rows of one vertex are contiguous, so a change of
-      // vertex (a wave-uniform test) closes the open maximum.
+      // down the 16 rows.  Rows of one vertex are contiguous, so a row whose
+      // vertex differs from the row before (bit i of the wave-uniform mask
+      // `starts`) closes the open maximum.  Rows past the range carry
+      // vertex -1, which is never written.
 #pragma unroll
       for (int nb = 0; nb < NB3; ++nb) *reinterpret_cast<f32x4*>(T + li * kTilePitch + 16 * nb + 4 * lg) = o3[nb];
+      // (both shuffles run on all lanes: a lane masked off would read as 0)
+      const int32_t krow = __shfl(v, 16 * grp + li);
+      const int32_t kup = __shfl(v, (16 * grp + li + 63) & 63);
+      const int32_t kprev = li > 0 ? kup : ckey;
+      const uint32_t starts = static_cast<uint32_t>(__ballot(krow != kprev)) & 0xffffu;
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int32_t key = __builtin_amdgcn_readlane(v, 16 * grp + i);
-        if (key < 0) break;   // past the range
         const float x = T[i * kTilePitch + lane];
-        if (key != ckey) {
+        if ((starts >> i) & 1u) {
           if (ckey >= 0) emit_col(out, ld_out, ckey, ckey == key_before || ckey == key_after, cmax, c3, lane);
-          ckey = key;
+          ckey = __builtin_amdgcn_readlane(v, 16 * grp + i);
           cmax = x;
         } else {
           cmax = fmaxf(cmax, x);
@@ -392,6 +491,7 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
   if (ckey >= 0) emit_col(out, ld_out, ckey, ckey == key_before || ckey == key_after, cmax, c3, lane);
 }
 
+
 }  // namespace
 
 int64_t distribute_workspace_bytes(int64_t total, int C3) {
@@ -402,14 +502,6 @@ int64_t distribute_workspace_bytes(int64_t total, int C3) {
 
 int distribute_max_features() { return kMaxC - 4; }
 
-// Entries per wave of the MLP pass: a multiple of 64, about 4 resident waves
-// per SIMD (1024 SIMDs) over the whole list.
-int64_t distribute_range(int64_t total) {
-  const int64_t groups = (total + 63) / 64;
-  constexpr int64_t kTargetWaves = 4096;
-  return 64 * ((groups + kTargetWaves - 1) / kTargetWaves);
-}
-
 void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* idx,
                        const int32_t* chunk_first, int chunk, int64_t n, int64_t total, const float* pos,
                        const float* feat, int64_t ld_feat, int cf, const float* W1, const float* b1, int C1,
@@ -418,12 +510,11 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
   if (total <= 0 || n <= 0) return;
   ScopedKernelTimer tm("distribute", s);
   const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
-  const int64_t R = distribute_range(total);
   double4* mh = static_cast<double4*>(work);
   double4* mt = mh + mean_spans;
   double4* mu4 = reinterpret_cast<double4*>(mu);
   launch(k_dist_mean, dim3(static_cast<unsigned>(mean_spans)), dim3(kBlock), 0, s, offsets, entries, chunk_first,
-         chunk, n, total, pos, mu4, mh, mt, R, out, ld_out, C3);
+         chunk, n, total, pos, mu4, mh, mt, static_cast<int64_t>(kMlpRange), out, ld_out, C3);
   if (mean_spans > 1)
     launch(k_dist_mean_finish, dim3(static_cast<unsigned>((mean_spans + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
            offsets, chunk_first, chunk, mean_spans, mu4, static_cast<const double4*>(mh),
@@ -441,9 +532,9 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(worst.bytes()));
     lds_limit_set = true;
   }
-  const int64_t waves = (total + R - 1) / R;
+  const int64_t waves = (total + kMlpRange - 1) / kMlpRange;
   const unsigned grid = static_cast<unsigned>((waves + kWaves - 1) / kWaves);
-  launch(kernel, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s, entries, idx, total, R, pos, feat,
+  launch(kernel, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s, entries, idx, total, pos, feat,
          ld_feat, cf, static_cast<const double4*>(mu4), W1, b1, W2, b2, W3, b3, ks1, C1, C2, C3, out, ld_out);
 }
 
