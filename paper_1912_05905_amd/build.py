@@ -2,7 +2,9 @@
 
 Every source is compiled for gfx950 only, with packed-FP32 instructions
 disabled.  The lattice-construction unit is compiled without float
-contraction: its vertex set depends on every float rounding.
+contraction: its vertex set depends on every float rounding.  The
+Distribute unit assumes no NaN inputs, so its maxima and ReLUs compile to
+single v_max instructions (no canonicalisation).
 """
 from __future__ import annotations
 
@@ -23,7 +25,7 @@ SOURCES = {
     "create.hip": ["-ffp-contract=off"],
     "splat_slice.hip": [],
     "conv.hip": [],
-    "distribute.hip": [],
+    "distribute.hip": ["-fno-honor-nans"],
     "api.hip": [],
 }
 

@@ -756,7 +756,7 @@ int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* 
   Scratch mu, work;
   if ((st = mu.get(sizeof(double) * 4 * static_cast<size_t>(L->n), stream)) != LAT_OK) return st;
   if ((st = work.get(static_cast<size_t>(distribute_workspace_bytes(L->total, C3)), stream)) != LAT_OK) return st;
-  launch_distribute(L->offsets, L->entries, L->idx, L->chunk_first, L->chunk, L->n, L->total, pos_dev, feat_dev, ld_feat, Cf,
+  launch_distribute(L->offsets, L->entries, L->chunk_first, L->chunk, L->n, L->total, pos_dev, feat_dev, ld_feat, Cf,
                     W1_dev, b1_dev, C1, W2_dev, b2_dev, C2, W3_dev, b3_dev, C3, out_dev, ld_out, mu.as<double>(),
                     work.p, stream);
   return check_launch("distribute");

@@ -53,7 +53,8 @@ __global__ void __launch_bounds__(kBlock)
 k_dist_mean(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
             const int32_t* __restrict__ chunk_first, int chunk, int64_t n, int64_t total,
             const float* __restrict__ pos, double4* __restrict__ mu, double4* __restrict__ part_head,
-            double4* __restrict__ part_tail, int64_t R, float* __restrict__ out, int64_t ld_out, int C3) {
+            double4* __restrict__ part_tail, int32_t* __restrict__ entry_vertex, int64_t R,
+            float* __restrict__ out, int64_t ld_out, int C3) {
   constexpr int W = kMeanSpan + 2;
   __shared__ int32_t win[W];
   __shared__ double sx[2][kBlock], sy[2][kBlock], sz[2][kBlock];
@@ -71,6 +72,7 @@ k_dist_mean(const int32_t* __restrict__ offsets, const int32_t* __restrict__ ent
   double x = 0.0, y = 0.0, z = 0.0;
   if (live) {
     vi = window_vertex(win, W, s);
+    entry_vertex[s] = v0 + vi;
     const int64_t p = entries[s] >> 2;
     x = pos[3 * p];
     y = pos[3 * p + 1];
@@ -250,7 +252,7 @@ struct Staged {
 // waves per SIMD the register allocation must allow.
 template <int NB1, int NB2, int NB3, int KS1, int WPE>
 __global__ void __launch_bounds__(kBlock, WPE)
-k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx, int64_t total,
+k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entry_vertex, int64_t total,
            const float* __restrict__ pos, const float* __restrict__ feat, int64_t ld_feat, int cf,
            const double4* __restrict__ mu, const float* __restrict__ W1, const float* __restrict__ b1,
            const float* __restrict__ W2, const float* __restrict__ b2, const float* __restrict__ W3,
@@ -320,13 +322,13 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
     for (int j = 0; j < kPer; ++j) {
       const int64_t s = r0 + 64 * j + lane;
       ent[j] = s < r1 ? entries[s] : -1;
+      vtx[j] = s < r1 ? entry_vertex[s] : -1;
     }
-    const int32_t eb = (active && r0 > 0) ? entries[r0 - 1] : -1;
-    const int32_t ea = (active && r1 < total) ? entries[r1] : -1;
+    key_before = (active && r0 > 0) ? entry_vertex[r0 - 1] : -1;
+    key_after = (active && r1 < total) ? entry_vertex[r1] : -1;
     float g[kPer][3];
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
-      vtx[j] = ent[j] >= 0 ? idx[ent[j]] : -1;
       const int64_t p = ent[j] >= 0 ? ent[j] >> 2 : 0;
 #pragma unroll
       for (int c = 0; c < 3; ++c) g[j][c] = ent[j] >= 0 ? pos[3 * p + c] : 0.f;
@@ -334,8 +336,6 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
 #pragma unroll
       for (int f = 0; f < kRow - 4; ++f) xr[j][4 + f] = (ent[j] >= 0 && f < cf) ? feat[p * ld_feat + f] : 0.f;
     }
-    key_before = eb >= 0 ? idx[eb] : -1;
-    key_after = ea >= 0 ? idx[ea] : -1;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       double4 m = make_double4(0.0, 0.0, 0.0, 0.0);
@@ -354,8 +354,8 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
     stage<8>(sm + lay.a3, NB3 * NB2 * 4 * 64, w3_at);
     stage<2>(sm + lay.b, 16 * (NB1 + NB2 + NB3), b_at);
     if (active) {
-      key_before = r0 > 0 ? idx[entries[r0 - 1]] : -1;
-      key_after = r1 < total ? idx[entries[r1]] : -1;
+      key_before = r0 > 0 ? entry_vertex[r0 - 1] : -1;
+      key_after = r1 < total ? entry_vertex[r1] : -1;
     }
   }
   __syncthreads();
@@ -388,7 +388,7 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
       v = -1;
       if (s < r1) {
         const int32_t e = entries[s];
-        v = idx[e];
+        v = entry_vertex[s];
         const int64_t p = e >> 2;
         const double4 m = mu[v];
         xs[0] = static_cast<float>(static_cast<double>(pos[3 * p]) - m.x);
@@ -497,24 +497,25 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ idx,
 int64_t distribute_workspace_bytes(int64_t total, int C3) {
   (void)C3;
   const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
-  return 2 * mean_spans * static_cast<int64_t>(sizeof(double4));
+  return 2 * mean_spans * static_cast<int64_t>(sizeof(double4)) + 4 * total;
 }
 
 int distribute_max_features() { return kMaxC - 4; }
 
-void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* idx,
-                       const int32_t* chunk_first, int chunk, int64_t n, int64_t total, const float* pos,
-                       const float* feat, int64_t ld_feat, int cf, const float* W1, const float* b1, int C1,
-                       const float* W2, const float* b2, int C2, const float* W3, const float* b3, int C3, float* out,
-                       int64_t ld_out, double* mu, void* work, hipStream_t s) {
+void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* chunk_first, int chunk,
+                       int64_t n, int64_t total, const float* pos, const float* feat, int64_t ld_feat, int cf,
+                       const float* W1, const float* b1, int C1, const float* W2, const float* b2, int C2,
+                       const float* W3, const float* b3, int C3, float* out, int64_t ld_out, double* mu, void* work,
+                       hipStream_t s) {
   if (total <= 0 || n <= 0) return;
   ScopedKernelTimer tm("distribute", s);
   const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
   double4* mh = static_cast<double4*>(work);
   double4* mt = mh + mean_spans;
+  int32_t* ev = reinterpret_cast<int32_t*>(mt + mean_spans);   // vertex of every list entry
   double4* mu4 = reinterpret_cast<double4*>(mu);
   launch(k_dist_mean, dim3(static_cast<unsigned>(mean_spans)), dim3(kBlock), 0, s, offsets, entries, chunk_first,
-         chunk, n, total, pos, mu4, mh, mt, static_cast<int64_t>(kMlpRange), out, ld_out, C3);
+         chunk, n, total, pos, mu4, mh, mt, ev, static_cast<int64_t>(kMlpRange), out, ld_out, C3);
   if (mean_spans > 1)
     launch(k_dist_mean_finish, dim3(static_cast<unsigned>((mean_spans + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
            offsets, chunk_first, chunk, mean_spans, mu4, static_cast<const double4*>(mh),
@@ -534,8 +535,8 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
   }
   const int64_t waves = (total + kMlpRange - 1) / kMlpRange;
   const unsigned grid = static_cast<unsigned>((waves + kWaves - 1) / kWaves);
-  launch(kernel, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s, entries, idx, total, pos, feat,
-         ld_feat, cf, static_cast<const double4*>(mu4), W1, b1, W2, b2, W3, b3, ks1, C1, C2, C3, out, ld_out);
+  launch(kernel, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s, entries,
+         static_cast<const int32_t*>(ev), total, pos, feat, ld_feat, cf, static_cast<const double4*>(mu4), W1, b1, W2, b2, W3, b3, ks1, C1, C2, C3, out, ld_out);
 }
 
 }  // namespace lat

@@ -157,11 +157,11 @@ void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const vo
 // distribute.hip
 int64_t distribute_workspace_bytes(int64_t total, int C3);
 int distribute_max_features();
-void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* idx,
-                       const int32_t* chunk_first, int chunk, int64_t n, int64_t total, const float* pos,
-                       const float* feat, int64_t ld_feat, int cf, const float* W1, const float* b1, int C1,
-                       const float* W2, const float* b2, int C2, const float* W3, const float* b3, int C3, float* out,
-                       int64_t ld_out, double* mu, void* work, hipStream_t s);
+void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* chunk_first, int chunk,
+                       int64_t n, int64_t total, const float* pos, const float* feat, int64_t ld_feat, int cf,
+                       const float* W1, const float* b1, int C1, const float* W2, const float* b2, int C2,
+                       const float* W3, const float* b3, int C3, float* out, int64_t ld_out, double* mu, void* work,
+                       hipStream_t s);
 // conv.hip
 void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
