@@ -47,6 +47,9 @@
 //    unweighted mean over J_v; three 1x1 layers with ReLU before the second
 //    and the third (none on the raw rows), then the per-vertex maximum;
 //    GroupNorm is not part of this operator.
+//  * Backward passes: gradients of the forward operators above; the ReLU's
+//    derivative is 0 at 0 and DeformSlice's maximum passes its gradient to
+//    the first maximal vertex.
 #include <algorithm>
 #include <array>
 #include <cmath>
@@ -543,6 +546,152 @@ int orc_distribute_pointnet(const orc_lattice* L, const double* G, const double*
         for (int i = 0; i < c2; ++i) a += W3[o * c2 + i] * std::max(h2[i], 0.0);
         X[v * c3 + o] = std::max(X[v * c3 + o], a);
       }
+    }
+  }
+  return OK;
+}
+
+// ---------------------------------------------------------------------------
+// Backward passes (Implementation: the lattice operators have forward and
+// backward passes on the GPU).  Each is the gradient of its forward operator
+// for a scalar loss L with dL/d(output) given; for the linear operators that
+// is the adjoint.  Written from the definitions, point by point / vertex by
+// vertex.
+// ---------------------------------------------------------------------------
+
+// Splat backward: dF_p = sum_{v in I_p} b_pv dX_v, each term divided by
+// wsum_v = sum_{q in J_v} b_qv when the forward normalised (0 where wsum_v is
+// 0, as in the forward).
+int orc_splat_backward(const orc_lattice* L, const double* dX, int C, int normalize, double* dF) {
+  if (!L || C <= 0 || !dX || (L->m > 0 && !dF)) return EINVAL_;
+  const int64_t n = static_cast<int64_t>(L->keys.size());
+  std::vector<double> ws(n, 0.0);
+  for (int64_t p = 0; p < L->m; ++p)
+    for (int k = 0; k < kD1; ++k) ws[L->idx[p * kD1 + k]] += L->bary[p * kD1 + k];
+  for (int64_t p = 0; p < L->m; ++p)
+    for (int c = 0; c < C; ++c) {
+      double acc = 0.0;
+      for (int k = 0; k < kD1; ++k) {
+        const int64_t v = L->idx[p * kD1 + k];
+        double coef = L->bary[p * kD1 + k];
+        if (normalize) coef = ws[v] > 0.0 ? coef / ws[v] : 0.0;
+        acc += coef * dX[v * C + c];
+      }
+      dF[p * C + c] = acc;
+    }
+  return OK;
+}
+
+// Slice backward: dX_v = sum over the pairs (p, k) with I_p[k] = v of
+// b_pk dOut_p.
+int orc_slice_backward(const orc_lattice* L, const double* dOut, int C, double* dX) {
+  if (!L || C <= 0 || !dX || (L->m > 0 && !dOut)) return EINVAL_;
+  const int64_t n = static_cast<int64_t>(L->keys.size());
+  std::fill(dX, dX + n * C, 0.0);
+  for (int64_t p = 0; p < L->m; ++p)
+    for (int k = 0; k < kD1; ++k) {
+      const int64_t v = L->idx[p * kD1 + k];
+      const double b = L->bary[p * kD1 + k];
+      for (int c = 0; c < C; ++c) dX[v * C + c] += b * dOut[p * C + c];
+    }
+  return OK;
+}
+
+// Convolution backward for the three forms: dst == src (1-hop), dst coarsened
+// from src (strided), src coarsened from dst (Upsample into dst).  The
+// forward was Y_v = act(bias + sum_t X[nb(v,t)] W[t]) with W[t] laid out
+// [c_in][c_out]; with G = dY, masked by Y > 0 when act is the ReLU (the
+// derivative taken as 0 at 0):
+//   dX[nb(v,t)] += W[t] G_v,  dW[t] += X[nb(v,t)]^T G_v,  dbias += G_v.
+// Any of dX, dW, dbias may be null.  dX is n_src x cin, dW taps x cin x cout.
+int orc_conv_backward(const orc_lattice* dst, const orc_lattice* src, const double* X, int cin,
+                      const double* W, int cout, int relu, const double* Y, const double* dY,
+                      double* dX, double* dW, double* dbias) {
+  if (!dst || !src || !dY || cin <= 0 || cout <= 0 || (relu && !Y)) return EINVAL_;
+  if ((dX && !W) || (dW && !X)) return EINVAL_;
+  std::vector<int64_t> nb;
+  if (dst == src) nb = same_level_table(dst);
+  else if (dst->parent == src) nb = down_table(dst, src);
+  else if (src->parent == dst) nb = up_table(dst, src);
+  else return ELEVEL;
+  const int64_t n_out = static_cast<int64_t>(dst->keys.size());
+  const int64_t n_in = static_cast<int64_t>(src->keys.size());
+  if (dX) std::fill(dX, dX + n_in * cin, 0.0);
+  if (dW) std::fill(dW, dW + static_cast<int64_t>(kTaps) * cin * cout, 0.0);
+  if (dbias) std::fill(dbias, dbias + cout, 0.0);
+  std::vector<double> g(cout);
+  for (int64_t v = 0; v < n_out; ++v) {
+    for (int o = 0; o < cout; ++o) {
+      g[o] = dY[v * cout + o];
+      if (relu && !(Y[v * cout + o] > 0.0)) g[o] = 0.0;
+      if (dbias) dbias[o] += g[o];
+    }
+    for (int t = 0; t < kTaps; ++t) {
+      const int64_t u = nb[static_cast<size_t>(v) * kTaps + t];
+      if (u < 0) continue;
+      for (int c = 0; c < cin; ++c) {
+        const int64_t wrow = (static_cast<int64_t>(t) * cin + c) * cout;
+        if (dX) {
+          double a = 0.0;
+          for (int o = 0; o < cout; ++o) a += W[wrow + o] * g[o];
+          dX[u * cin + c] += a;
+        }
+        if (dW)
+          for (int o = 0; o < cout; ++o) dW[wrow + o] += X[u * cin + c] * g[o];
+      }
+    }
+  }
+  return OK;
+}
+
+// DeformSlice backward.  Forward per point p (vertex k of its simplex, value
+// x_k = X[I_p[k]], weight b_k):
+//   q_k = b_k x_k,  M = max_k q_k per channel (first maximal k on ties),
+//   s_k = beta + (q_k - M) . wv,  db_k = tanh(s_k),  out = sum_k (b_k + db_k) x_k.
+// With g = dOut_p, a_k = g . x_k and e_k = a_k (1 - db_k^2) = dL/ds_k:
+//   dx_k += (b_k + db_k) g + e_k b_k wv - [k = argmax_c] (sum_j e_j) b_k wv_c,
+//   dwv  += sum_k e_k (q_k - M),   dbeta += sum_k e_k.
+int orc_deform_slice_backward(const orc_lattice* L, const double* X, int C, const double* wv, double beta,
+                              const double* dOut, double* dX, double* dwv, double* dbeta) {
+  if (!L || !X || !wv || C <= 0 || !dX || !dwv || !dbeta || (L->m > 0 && !dOut)) return EINVAL_;
+  const int64_t n = static_cast<int64_t>(L->keys.size());
+  std::fill(dX, dX + n * C, 0.0);
+  std::fill(dwv, dwv + C, 0.0);
+  *dbeta = 0.0;
+  std::vector<double> q(static_cast<size_t>(kD1) * C), mx(C);
+  std::vector<int> am(C);
+  for (int64_t p = 0; p < L->m; ++p) {
+    const int64_t* I = &L->idx[p * kD1];
+    const float* b = &L->bary[p * kD1];
+    for (int k = 0; k < kD1; ++k)
+      for (int c = 0; c < C; ++c) q[k * C + c] = static_cast<double>(b[k]) * X[I[k] * C + c];
+    for (int c = 0; c < C; ++c) {
+      am[c] = 0;
+      for (int k = 1; k < kD1; ++k)
+        if (q[k * C + c] > q[am[c] * C + c]) am[c] = k;
+      mx[c] = q[am[c] * C + c];
+    }
+    const double* g = dOut + p * C;
+    double db[kD1], e[kD1], esum = 0.0;
+    for (int k = 0; k < kD1; ++k) {
+      double sk = beta, ak = 0.0;
+      for (int c = 0; c < C; ++c) {
+        sk += (q[k * C + c] - mx[c]) * wv[c];
+        ak += g[c] * X[I[k] * C + c];
+      }
+      db[k] = std::tanh(sk);
+      e[k] = ak * (1.0 - db[k] * db[k]);
+      esum += e[k];
+    }
+    for (int k = 0; k < kD1; ++k)
+      for (int c = 0; c < C; ++c) {
+        double d = (static_cast<double>(b[k]) + db[k]) * g[c] + e[k] * b[k] * wv[c];
+        if (am[c] == k) d -= esum * b[k] * wv[c];
+        dX[I[k] * C + c] += d;
+      }
+    for (int k = 0; k < kD1; ++k) {
+      for (int c = 0; c < C; ++c) dwv[c] += e[k] * (q[k * C + c] - mx[c]);
+      *dbeta += e[k];
     }
   }
   return OK;

@@ -56,6 +56,10 @@ def lib():
             "orc_deform_slice": (i32, [p, p, i64, i32, p, dbl, p, i64, p, p]),
             "orc_round_bf16": (None, [p, i64]),
             "orc_distribute_pointnet": (i32, [p, p, p, i32, p, p, i32, p, p, i32, p, p, i32, p]),
+            "orc_splat_backward": (i32, [p, p, i32, i32, p]),
+            "orc_slice_backward": (i32, [p, p, i32, p]),
+            "orc_conv_backward": (i32, [p, p, p, i32, p, i32, i32, p, p, p, p, p]),
+            "orc_deform_slice_backward": (i32, [p, p, i32, p, dbl, p, p, p, p]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -223,6 +227,49 @@ class Lattice:
         _check(lib().orc_refine(self._h, coarse._h, _ptr(X), cin, cin, _ptr(W), _ptr(b), cout,
                                 int(bool(relu)), _ptr(r), nr, _ptr(Y), cout))
         return Y
+
+    # ---- backward ----
+    def splat_backward(self, dX, normalize=True):
+        """dL/dF of splat for dL/dX = dX (n x C)."""
+        dX = _f64(dX)
+        Cc = dX.shape[1]
+        dF = np.zeros((self.m, Cc), np.float64)
+        _check(lib().orc_splat_backward(self._h, _ptr(dX), Cc, int(bool(normalize)), _ptr(dF)))
+        return dF
+
+    def slice_backward(self, dOut):
+        """dL/dX of slice for dL/dout = dOut (m x C)."""
+        dOut = _f64(dOut)
+        Cc = dOut.shape[1]
+        dX = np.zeros((self.n, Cc), np.float64)
+        _check(lib().orc_slice_backward(self._h, _ptr(dOut), Cc, _ptr(dX)))
+        return dX
+
+    def conv_backward(self, src: "Lattice", X, W, dY, relu=False, Y=None):
+        """Gradients of Y = act(conv(src -> self)(X, W) + bias) for dL/dY = dY:
+        (dX, dW, dbias).  src is self, self.parent (strided) or a coarsening
+        of self (Upsample into self).  W laid out [tap][c_in][c_out]."""
+        X, W, dY = _f64(X), _f64(W), _f64(dY)
+        cin, cout = W.shape[1], W.shape[2]
+        Yc = None if Y is None else _f64(Y)
+        dX = np.zeros((src.n, cin), np.float64)
+        dW = np.zeros(W.shape, np.float64)
+        db = np.zeros(cout, np.float64)
+        _check(lib().orc_conv_backward(self._h, src._h, _ptr(X), cin, _ptr(W), cout, int(bool(relu)), _ptr(Yc),
+                                       _ptr(dY), _ptr(dX), _ptr(dW), _ptr(db)))
+        return dX, dW, db
+
+    def deform_slice_backward(self, X, wv, beta, dOut):
+        """Gradients of deform_slice(X, wv, beta) for dL/dout = dOut:
+        (dX, dwv, dbeta)."""
+        X, wv, dOut = _f64(X), _f64(wv), _f64(dOut)
+        Cc = X.shape[1]
+        dX = np.zeros((self.n, Cc), np.float64)
+        dwv = np.zeros(Cc, np.float64)
+        dbeta = np.zeros(1, np.float64)
+        _check(lib().orc_deform_slice_backward(self._h, _ptr(X), Cc, _ptr(wv), float(beta), _ptr(dOut), _ptr(dX),
+                                               _ptr(dwv), _ptr(dbeta)))
+        return dX, dwv, float(dbeta[0])
 
     def slice(self, X, pts=None):
         X = _f64(X)

@@ -470,3 +470,120 @@ def test_distribute_each_relu_matters(oracle_mod):
         X = ol.distribute_pointnet(G, F, layers)
         for v in range(ol.n):
             np.testing.assert_allclose(X[v, :4], want(F[J[v]]), rtol=0, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# backward passes: adjoint identities against the forward operators, and
+# central finite differences where the forward is not linear
+# ----------------------------------------------------------------------------
+def _dot(a, b):
+    return float(np.sum(np.asarray(a, np.float64) * np.asarray(b, np.float64)))
+
+
+def test_splat_and_slice_backward_are_adjoints(oracle_mod):
+    """<splat(F), G> = <F, splat^T(G)> for the raw and the normalised splat,
+    and <slice(X), H> = <X, slice^T(H)>."""
+    for seed in (41, 42):
+        L = oracle_mod.Lattice.create(_tiny_cloud(seed, 250), np.full(3, 0.1, np.float32))
+        rng = np.random.default_rng(seed)
+        F = rng.normal(size=(L.m, 5))
+        G = rng.normal(size=(L.n, 5))
+        for norm in (False, True):
+            X, _ = L.splat(F, normalize=norm)
+            lhs, rhs = _dot(X, G), _dot(F, L.splat_backward(G, normalize=norm))
+            assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs)), (norm, lhs, rhs)
+        X = rng.normal(size=(L.n, 3))
+        H = rng.normal(size=(L.m, 3))
+        lhs, rhs = _dot(L.slice(X), H), _dot(X, L.slice_backward(H))
+        assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs)), (lhs, rhs)
+
+
+def _conv_forms(oracle_mod, seed):
+    L0 = oracle_mod.Lattice.create(_tiny_cloud(seed, 300), np.full(3, 0.11, np.float32))
+    L1 = L0.coarsen()
+    return [("same", L0, L0, lambda X, W, b, r: L0.conv(L0, X, W, bias=b, relu=r)),
+            ("strided", L1, L0, lambda X, W, b, r: L1.conv(L0, X, W, bias=b, relu=r)),
+            ("upsample", L0, L1, lambda X, W, b, r: L0.refine_into(L1, X, W, bias=b, relu=r))]
+
+
+def test_conv_backward_linear_part(oracle_mod):
+    """Without the ReLU: dX is the adjoint, <conv(X), G> = <X, dX>; the
+    forward is linear in W and in the bias, so <dW, E> = <G, conv_E(X)> and
+    <dbias, e> = <G, 1 e^T> hold exactly, for the 1-hop, strided and Upsample
+    forms."""
+    for seed in (43, 44):
+        rng = np.random.default_rng(seed)
+        for name, dst, src, fwd in _conv_forms(oracle_mod, seed):
+            X = rng.normal(size=(src.n, 4))
+            W = rng.normal(size=(9, 4, 3))
+            G = rng.normal(size=(dst.n, 3))
+            dX, dW, db = dst.conv_backward(src, X, W, G)
+            Y = fwd(X, W, None, False)
+            assert abs(_dot(Y, G) - _dot(X, dX)) <= 1e-12 * max(1.0, abs(_dot(Y, G))), name
+            E = rng.normal(size=W.shape)
+            lhs, rhs = _dot(dW, E), _dot(G, fwd(X, E, None, False))
+            assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs)), name
+            e = rng.normal(size=3)
+            lhs, rhs = _dot(db, e), _dot(G, np.ones((dst.n, 1)) * e)
+            assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs)), name
+
+
+def test_conv_backward_relu_finite_differences(oracle_mod):
+    """With the ReLU, L = <relu(conv(X) + b), G> is piecewise linear; central
+    differences in random directions of X, W and b match the gradients."""
+    h = 1e-6
+    rng = np.random.default_rng(45)
+    for name, dst, src, fwd in _conv_forms(oracle_mod, 45):
+        X = rng.normal(size=(src.n, 4))
+        W = rng.normal(size=(9, 4, 5))
+        b = rng.normal(size=5) * 0.5
+        G = rng.normal(size=(dst.n, 5))
+        Y = fwd(X, W, b, True)
+        assert (Y == 0).mean() > 0.2, "the ReLU should clip a good share"
+        dX, dW, db = dst.conv_backward(src, X, W, G, relu=True, Y=Y)
+        loss = lambda X_, W_, b_: _dot(fwd(X_, W_, b_, True), G)
+        for _ in range(2):
+            D = rng.normal(size=X.shape)
+            fd = (loss(X + h * D, W, b) - loss(X - h * D, W, b)) / (2 * h)
+            assert abs(fd - _dot(dX, D)) <= 1e-6 * max(1.0, abs(fd)), (name, fd, _dot(dX, D))
+            E = rng.normal(size=W.shape)
+            fd = (loss(X, W + h * E, b) - loss(X, W - h * E, b)) / (2 * h)
+            assert abs(fd - _dot(dW, E)) <= 1e-6 * max(1.0, abs(fd)), name
+            e = rng.normal(size=5)
+            fd = (loss(X, W, b + h * e) - loss(X, W, b - h * e)) / (2 * h)
+            assert abs(fd - _dot(db, e)) <= 1e-6 * max(1.0, abs(fd)), name
+
+
+def test_deform_slice_backward_finite_differences(oracle_mod):
+    """L = <deform_slice(X, w, beta), G>: central differences in random
+    directions of X and w, and in beta, match the gradients, and so do
+    single coordinates of dX at the vertex holding a channel's maximum."""
+    h = 1e-6
+    for seed, C in ((46, 6), (47, 16)):
+        L = oracle_mod.Lattice.create(_tiny_cloud(seed, 200, 0.6), np.full(3, 0.1, np.float32))
+        rng = np.random.default_rng(seed)
+        X = rng.normal(size=(L.n, C))
+        wv = rng.normal(size=C) * 0.5
+        beta = 0.2
+        G = rng.normal(size=(L.m, C))
+        dX, dwv, dbeta = L.deform_slice_backward(X, wv, beta, G)
+        loss = lambda X_, w_, b_: _dot(L.deform_slice(X_, w_, b_)[0], G)
+        for _ in range(3):
+            D = rng.normal(size=X.shape)
+            fd = (loss(X + h * D, wv, beta) - loss(X - h * D, wv, beta)) / (2 * h)
+            assert abs(fd - _dot(dX, D)) <= 1e-6 * max(1.0, abs(fd)), (fd, _dot(dX, D))
+            d = rng.normal(size=C)
+            fd = (loss(X, wv + h * d, beta) - loss(X, wv - h * d, beta)) / (2 * h)
+            assert abs(fd - _dot(dwv, d)) <= 1e-6 * max(1.0, abs(fd)), (fd, _dot(dwv, d))
+        fd = (loss(X, wv, beta + h) - loss(X, wv, beta - h)) / (2 * h)
+        assert abs(fd - dbeta) <= 1e-6 * max(1.0, abs(fd)), (fd, dbeta)
+        # single coordinates of dX, among them the vertex holding a maximum
+        idx, w = L.simplices()
+        for p in (0, 5, L.m - 1):
+            q = w[p, :, None].astype(np.float64) * X[idx[p]]
+            k = int(np.argmax(q[:, 0]))
+            v = idx[p, k]
+            D = np.zeros_like(X)
+            D[v, 0] = 1.0
+            fd = (loss(X + h * D, wv, beta) - loss(X - h * D, wv, beta)) / (2 * h)
+            assert abs(fd - dX[v, 0]) <= 1e-6 * max(1.0, abs(fd)), (p, fd, dX[v, 0])
