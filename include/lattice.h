@@ -207,6 +207,55 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
                          hipStream_t stream);
 
 /*
+ * Backward passes (Implementation: the lattice operators have forward and
+ * backward passes on the GPU).  Each returns the gradient of a scalar loss
+ * with respect to the forward's inputs, given its gradient with respect to
+ * the forward's output.  float32 only.  Output buffers are overwritten (not
+ * accumulated into).
+ */
+
+/*
+ * Splat backward: dF_p = sum_{v in I_p} b_pv dX_v (Eq. (splat) transposed);
+ * with normalize != 0 each term is divided by wsum_v = sum_{q in J_v} b_qv
+ * (0 where wsum_v = 0), the gradient of the normalised splat.
+ *   dX_dev  n x C float32, row stride ld_dX (0 = C).  C a multiple of 4.
+ *   dF_dev  m x C float32, row stride C.
+ */
+int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int C, int normalize, float* dF_dev,
+                           hipStream_t stream);
+
+/*
+ * Slice backward: dX_v = sum_{p in J_v} b_pv dOut_p (Eq. (slice)
+ * transposed), computed as a splat over the vertex lists.
+ *   dOut_dev  m x C float32, row stride ld_dOut (0 = C).
+ *   dX_dev    n x C float32, row stride ld_dX (0 = C).  C <= 256.
+ */
+int lattice_slice_backward(lattice_t L, const float* dOut_dev, int64_t ld_dOut, int C, float* dX_dev, int64_t ld_dX,
+                           hipStream_t stream);
+
+/*
+ * Convolution backward for Y = act(conv(X, W) + bias) as computed by
+ * lattice_conv(dst, src) (1-hop or strided) or lattice_refine(dst, src)
+ * (Upsample: src = lattice_coarsen(dst)); the form follows from dst and src.
+ *   X_dev     n_src x Cin forward input (needed for dW), row stride ld_X.
+ *   W_dev     9 x Cout x Cin forward weights (needed for dX).
+ *   flags     LAT_RELU if the forward applied the ReLU; then Y_dev (n_dst x
+ *             Cout, row stride ld_Y) is the forward output and dY is masked
+ *             by Y > 0 (the derivative is taken as 0 at 0).
+ *   dY_dev    n_dst x Cout gradient of the output, row stride ld_dY.
+ *   dX_dev    n_src x Cin, row stride ld_dX, or NULL: the convolution of the
+ *             masked dY with W'[t] = W[mirror t]^T over the adjoint table;
+ *             must not overlap dY.
+ *   dW_dev    9 x Cout x Cin, or NULL: dW[t] = sum_v dY_v^T X[nb(v,t)].
+ *   dbias_dev Cout, or NULL: sum_v dY_v.
+ * Row strides of 0 mean dense.  Cin, Cout multiples of 4.  Uses work space
+ * from the library's pool; the sums over vertices run in a fixed order.
+ */
+int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int64_t ld_X, int Cin, const float* W_dev,
+                          int Cout, int flags, const float* Y_dev, int64_t ld_Y, const float* dY_dev, int64_t ld_dY,
+                          float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream);
+
+/*
  * Timing of the library's kernels with HIP events on the launch stream, for
  * measurement.  enable != 0 records a start/stop event pair around every
  * launch of the kernel family `name` ("conv", "splat", "slice", "insert",

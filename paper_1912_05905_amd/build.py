@@ -26,6 +26,7 @@ SOURCES = {
     "splat_slice.hip": [],
     "conv.hip": [],
     "distribute.hip": ["-fno-honor-nans"],
+    "backward.hip": [],
     "api.hip": [],
 }
 

@@ -174,7 +174,10 @@ namespace lat {
 
 thread_local TimerFamily* t_active = nullptr;  // family of the live ScopedKernelTimer
 
+thread_local int t_depth = 0;  // nesting of live ScopedKernelTimers; the outermost names the family
+
 void timer_begin(const char* family) {
+  if (t_depth++ > 0) return;
   t_active = nullptr;
   if (!g_any_timer) return;
   std::lock_guard<std::mutex> lk(g_timer_mu);
@@ -182,7 +185,9 @@ void timer_begin(const char* family) {
   if (f && f->enabled) t_active = f;
 }
 
-void timer_end() { t_active = nullptr; }
+void timer_end() {
+  if (--t_depth == 0) t_active = nullptr;
+}
 
 bool timer_take_events(hipEvent_t* start, hipEvent_t* stop) {
   if (!t_active) return false;
@@ -792,6 +797,125 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
   launch_deform_slice(L->idx, L->w, L->m, vals_dev, ld_vals, C, dt == LAT_BF16, wv_dev, beta, out_dev,
                       delta_dev, stream);
   return check_launch("deform slice");
+}
+
+// ---- backward passes ----
+
+int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int C, int normalize, float* dF_dev,
+                           hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if (ld_dX == 0) ld_dX = C;
+  if ((st = check_matrix(dX_dev, ld_dX, C, LAT_F32, "dX", L->n > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(dF_dev, C, C, LAT_F32, "dF", L->m > 0)) != LAT_OK) return st;
+  if (L->m == 0) return LAT_OK;
+  ScopedKernelTimer tm("splat_bwd", stream);
+  const float* src = dX_dev;
+  int64_t ld = ld_dX;
+  Scratch scaled;
+  if (normalize) {
+    if ((st = scaled.get(sizeof(float) * static_cast<size_t>(L->n) * C, stream)) != LAT_OK) return st;
+    launch_scale_by_weight_sum(L->offsets, L->entry_w, L->n, dX_dev, ld_dX, C, scaled.as<float>(), C, stream);
+    src = scaled.as<float>();
+    ld = C;
+  }
+  launch_slice(L->idx, L->w, L->m, src, ld, C, false, dF_dev, stream);
+  return check_launch("splat backward");
+}
+
+int lattice_slice_backward(lattice_t L, const float* dOut_dev, int64_t ld_dOut, int C, float* dX_dev, int64_t ld_dX,
+                           hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if (ld_dOut == 0) ld_dOut = C;
+  if (ld_dX == 0) ld_dX = C;
+  if ((st = check_matrix(dOut_dev, ld_dOut, C, LAT_F32, "dOut", L->m > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(dX_dev, ld_dX, C, LAT_F32, "dX", L->n > 0)) != LAT_OK) return st;
+  if (C > splat_max_channels(false))
+    return fail(LAT_EUNSUPPORTED, "slice backward supports at most " + std::to_string(splat_max_channels(false)) +
+                                      " channels");
+  if (L->n == 0) return LAT_OK;
+  ScopedKernelTimer tm("slice_bwd", stream);
+  Scratch partials;
+  if ((st = partials.get(sizeof(float) * splat_partial_floats(L->total, L->chunk, C), stream)) != LAT_OK) return st;
+  launch_splat(L->offsets, L->entries, L->entry_w, L->chunk_first, L->chunk, L->nmax, L->total, dOut_dev, ld_dOut, C,
+               false, false, dX_dev, ld_dX, nullptr, partials.as<float>(), stream);
+  return check_launch("slice backward");
+}
+
+int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int64_t ld_X, int Cin, const float* W_dev,
+                          int Cout, int flags, const float* Y_dev, int64_t ld_Y, const float* dY_dev, int64_t ld_dY,
+                          float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(dst)) != LAT_OK) return st;
+  if ((st = check_handle(src)) != LAT_OK) return st;
+  // the forward's table (dst rows, src values) and the adjoint's (src rows,
+  // dst values)
+  const int32_t *fwd, *adj, *adj_rows = nullptr;
+  int64_t fwd_ld, adj_ld;
+  if (dst == src) {
+    fwd = adj = dst->nbr;
+    fwd_ld = adj_ld = dst->nmax;
+  } else if (dst->parent == src) {            // strided: adjoint is the Upsample into src
+    fwd = dst->down;
+    fwd_ld = dst->nmax;
+    adj = dst->up;
+    adj_ld = src->nmax;
+    adj_rows = dst->up_rows;
+  } else if (src->parent == dst) {            // Upsample into dst: adjoint is the strided conv
+    fwd = src->up;
+    fwd_ld = dst->nmax;
+    adj = src->down;
+    adj_ld = src->nmax;
+  } else {
+    return fail(LAT_ELEVEL, "dst and src must be one lattice, or one a coarsening of the other");
+  }
+  if (flags & ~LAT_RELU) return fail(LAT_EINVAL, "unknown flags");
+  const bool relu = (flags & LAT_RELU) != 0;
+  if (ld_dY == 0) ld_dY = Cout;
+  if (ld_Y == 0) ld_Y = Cout;
+  if (ld_X == 0) ld_X = Cin;
+  if (ld_dX == 0) ld_dX = Cin;
+  const int64_t n_out = dst->n, n_in = src->n;
+  if ((st = check_matrix(dY_dev, ld_dY, Cout, LAT_F32, "dY", n_out > 0)) != LAT_OK) return st;
+  if (relu && (st = check_matrix(Y_dev, ld_Y, Cout, LAT_F32, "Y", n_out > 0)) != LAT_OK) return st;
+  if (dX_dev) {
+    if ((st = check_matrix(dX_dev, ld_dX, Cin, LAT_F32, "dX", false)) != LAT_OK) return st;
+    if (!W_dev) return fail(LAT_EINVAL, "W is null");
+    if (!aligned16(W_dev)) return fail(LAT_EINVAL, "W must be 16-byte aligned");
+    if (n_in > 0 && n_out > 0 &&
+        overlaps(dX_dev, sizeof(float) * static_cast<size_t>((n_in - 1) * ld_dX + Cin), dY_dev,
+                 sizeof(float) * static_cast<size_t>((n_out - 1) * ld_dY + Cout)))
+      return fail(LAT_EINVAL, "dX and dY overlap");
+  }
+  if (dW_dev || dbias_dev) {
+    if ((st = check_matrix(X_dev, ld_X, Cin, LAT_F32, "X", dW_dev != nullptr && n_in > 0)) != LAT_OK) return st;
+    if (dW_dev && !aligned16(dW_dev)) return fail(LAT_EINVAL, "dW must be 16-byte aligned");
+  }
+  if (!dX_dev && !dW_dev && !dbias_dev) return LAT_OK;
+  ScopedKernelTimer tm("conv_bwd", stream);
+  const float* G = dY_dev;
+  int64_t ld_G = ld_dY;
+  Scratch masked, wt, partials;
+  if (relu && n_out > 0) {
+    if ((st = masked.get(sizeof(float) * static_cast<size_t>(n_out) * Cout, stream)) != LAT_OK) return st;
+    launch_relu_mask(dY_dev, ld_dY, Y_dev, ld_Y, Cout, n_out, masked.as<float>(), Cout, stream);
+    G = masked.as<float>();
+    ld_G = Cout;
+  }
+  if (dX_dev && n_in > 0) {
+    if ((st = wt.get(sizeof(float) * 9 * static_cast<size_t>(Cin) * Cout, stream)) != LAT_OK) return st;
+    launch_adjoint_weights(W_dev, Cout, Cin, wt.as<float>(), stream);
+    launch_conv(adj, adj_ld, n_in, n_out, G, ld_G, Cout, wt.as<float>(), nullptr, Cin, false, false, dX_dev, ld_dX,
+                adj_rows, stream);
+  }
+  if (dW_dev || dbias_dev) {
+    const int64_t pf = wgrad_partial_floats(n_out, Cout, Cin);
+    if (pf > 0 && (st = partials.get(sizeof(float) * static_cast<size_t>(pf), stream)) != LAT_OK) return st;
+    launch_conv_wgrad(fwd, fwd_ld, n_out, X_dev, ld_X, Cin, G, ld_G, Cout, dW_dev, dbias_dev, partials.as<float>(),
+                      stream);
+  }
+  return check_launch("conv backward");
 }
 
 int lattice_timing_enable(const char* name, int enable) {

@@ -1,0 +1,260 @@
+// Backward passes of the lattice operators on gfx950 (Implementation: the
+// lattice operators have forward and backward passes on the GPU).  Every
+// gradient is that of its forward operator for a scalar loss with
+// dL/d(output) given; the linear operators' gradients are their adjoints:
+//   splat  -> a slice of dL/dx (each vertex row scaled by 1 / sum_{J_v} b
+//             when the forward normalised);
+//   slice  -> a (raw) splat of dL/df over the lists J_v;
+//   conv   -> dX: the convolution of dL/dY with W'[t] = W[mirror t]^T over
+//             the adjoint table (1-hop: the same table; strided: the
+//             Upsample table; Upsample: the Downsample table), on the
+//             forward's MFMA kernel;
+//             dW[t] = sum_v dL/dY_v^T X[nb(v,t)], dbias = sum_v dL/dY_v: a
+//             gathered GEMM that reduces over vertices (k_conv_wgrad, split
+//             over vertex chunks, partials added in chunk order).
+// A ReLU in the forward masks dL/dY with Y > 0 first (derivative 0 at 0).
+#include <algorithm>
+
+#include "lattice_internal.h"
+
+namespace lat {
+namespace {
+
+constexpr int kBlock = 256;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---- splat backward with normalisation: rows of dL/dx divided by the
+// vertex weight sums ----
+// One group of 16 lanes per vertex: the lanes sum entry_w over J_v, then
+// scale the vertex's row (0 where the sum is 0, as in the forward).
+constexpr int kScaleLanes = 16;
+
+__global__ void __launch_bounds__(kBlock)
+k_scale_by_weight_sum(const int32_t* __restrict__ offsets, const float* __restrict__ entry_w, int64_t n,
+                      const float* __restrict__ in, int64_t ld_in, int C, float* __restrict__ out, int64_t ld_out) {
+  const int lane = threadIdx.x & (kScaleLanes - 1);
+  const int64_t v = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / kScaleLanes;
+  if (v >= n) return;   // a whole lane group
+  const int32_t b = offsets[v], e = offsets[v + 1];
+  float ws = 0.f;
+  for (int32_t j = b + lane; j < e; j += kScaleLanes) ws += entry_w[j];
+#pragma unroll
+  for (int o = kScaleLanes / 2; o > 0; o >>= 1) ws += __shfl_xor(ws, o, kScaleLanes);
+  const float scale = ws > 0.f ? 1.0f / ws : 0.f;
+  for (int c = 4 * lane; c < C; c += 4 * kScaleLanes) {
+    const float4 x = *reinterpret_cast<const float4*>(in + v * ld_in + c);
+    *reinterpret_cast<float4*>(out + v * ld_out + c) = make_float4(x.x * scale, x.y * scale, x.z * scale, x.w * scale);
+  }
+}
+
+// ---- convolution backward ----
+// G = dY masked by Y > 0 (the forward's ReLU), 4 channels per thread.
+__global__ void __launch_bounds__(kBlock)
+k_relu_mask(const float* __restrict__ dY, int64_t ld_dy, const float* __restrict__ Y, int64_t ld_y, int C,
+            int64_t n, float* __restrict__ G, int64_t ld_g) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int c4 = C / 4;
+  const int64_t v = q / c4;
+  if (v >= n) return;
+  const int c = 4 * static_cast<int>(q - v * c4);
+  const float4 d = *reinterpret_cast<const float4*>(dY + v * ld_dy + c);
+  const float4 y = *reinterpret_cast<const float4*>(Y + v * ld_y + c);
+  *reinterpret_cast<float4*>(G + v * ld_g + c) =
+      make_float4(y.x > 0.f ? d.x : 0.f, y.y > 0.f ? d.y : 0.f, y.z > 0.f ? d.z : 0.f, y.w > 0.f ? d.w : 0.f);
+}
+
+// Taps 0 = self, 1..4 = +n_j, 5..8 = -n_j: the mirror of a tap negates its
+// offset.
+__device__ inline int mirror_tap(int t) { return t == 0 ? 0 : (t <= 4 ? t + 4 : t - 4); }
+
+// Wt[t][i][o] = W[mirror t][o][i]: the weights of the adjoint convolution
+// (W laid out [tap][Cout][Cin]).
+__global__ void __launch_bounds__(kBlock)
+k_adjoint_weights(const float* __restrict__ W, int Cout, int Cin, float* __restrict__ Wt) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int64_t per = static_cast<int64_t>(Cout) * Cin;
+  if (q >= 9 * per) return;
+  const int t = static_cast<int>(q / per);
+  const int64_t r = q - t * per;
+  const int i = static_cast<int>(r / Cout), o = static_cast<int>(r - static_cast<int64_t>(i) * Cout);
+  Wt[q] = W[(mirror_tap(t) * per) + static_cast<int64_t>(o) * Cin + i];
+}
+
+// dW[t][o][i] = sum_v G[v][o] X[nb(v,t)][i] as a GEMM with the vertices as
+// the reduction dimension: A = G^T (Cout x K), B = the gathered rows
+// (K x Cin).  A workgroup owns one tap, one 64 x 64 tile of (o, i) and one
+// chunk of V vertices; it stages 32 vertices at a time (G rows and gathered
+// X rows, a missing neighbour reads as zeros) in double-buffered LDS, each
+// wave multiplying a 32 x 32 sub-tile on v_mfma_f32_16x16x4_f32.  Partials
+// go to part[chunk][tap][o][i]; the workgroups of tap 0 and the first i
+// tile also sum the G columns (the bias gradient).
+constexpr int kWgTile = 64;
+constexpr int kWgStage = 32;
+constexpr int kWgPitch = kWgTile + 4;
+
+__global__ void __launch_bounds__(kBlock)
+k_conv_wgrad(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, int64_t V, const float* __restrict__ X,
+             int64_t ld_x, int Cin, const float* __restrict__ G, int64_t ld_g, int Cout, int tiles_i,
+             float* __restrict__ part, float* __restrict__ part_b) {
+  __shared__ __align__(16) float Gs[2][kWgStage][kWgPitch];
+  __shared__ __align__(16) float Xs[2][kWgStage][kWgPitch];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int li = lane & 15, lg = lane >> 4;
+  const int64_t chunk = blockIdx.x;
+  const int tap = blockIdx.y;
+  const int ti = static_cast<int>(blockIdx.z) % tiles_i, to = static_cast<int>(blockIdx.z) / tiles_i;
+  const int o0 = to * kWgTile, i0 = ti * kWgTile;
+  const int64_t v_begin = chunk * V, v_end = min(v_begin + V, n_out);
+  const int wo = (wave >> 1) * 32, wi = (wave & 1) * 32;
+  const bool do_bias = part_b != nullptr && tap == 0 && ti == 0;
+  const int lr = t >> 4, lc = 4 * (t & 15);   // rows lr and lr + 16, columns lc..lc+3 of a stage
+  const int32_t* tab = nbr + static_cast<int64_t>(tap) * ldn;
+
+  float4 ga[2], xa[2];
+  auto load = [&](int64_t vb) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t v = vb + lr + 16 * h;
+      float4 g = make_float4(0.f, 0.f, 0.f, 0.f), x = g;
+      if (v < v_end) {
+        if (o0 + lc < Cout) g = *reinterpret_cast<const float4*>(G + v * ld_g + o0 + lc);
+        const int32_t u = tab[v];
+        if (u >= 0 && i0 + lc < Cin) x = *reinterpret_cast<const float4*>(X + static_cast<int64_t>(u) * ld_x + i0 + lc);
+      }
+      ga[h] = g;
+      xa[h] = x;
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      *reinterpret_cast<float4*>(&Gs[buf][lr + 16 * h][lc]) = ga[h];
+      *reinterpret_cast<float4*>(&Xs[buf][lr + 16 * h][lc]) = xa[h];
+    }
+  };
+
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float bsum = 0.f;
+
+  load(v_begin);
+  store(0);
+  __syncthreads();
+  int buf = 0;
+  for (int64_t vb = v_begin; vb < v_end; vb += kWgStage) {
+    const bool more = vb + kWgStage < v_end;
+    if (more) load(vb + kWgStage);
+#pragma unroll
+    for (int ks = 0; ks < kWgStage / 4; ++ks) {
+      float a[2], b[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        a[h] = Gs[buf][4 * ks + lg][wo + 16 * h + li];
+        b[h] = Xs[buf][4 * ks + lg][wi + 16 * h + li];
+      }
+#pragma unroll
+      for (int ao = 0; ao < 2; ++ao)
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi) acc[ao][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ao], b[bi], acc[ao][bi], 0, 0, 0);
+    }
+    if (do_bias && t < kWgTile)
+#pragma unroll 8
+      for (int r = 0; r < kWgStage; ++r) bsum += Gs[buf][r][t];
+    if (more) store(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+
+  // lane (i, g) of block (ao, bi) holds o = 16 ao + 4 g + r, i = 16 bi + i
+  float* P = part + (chunk * 9 + tap) * static_cast<int64_t>(Cout) * Cin;
+#pragma unroll
+  for (int ao = 0; ao < 2; ++ao)
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int o = o0 + wo + 16 * ao + 4 * lg + r, i = i0 + wi + 16 * bi + li;
+        if (o < Cout && i < Cin) P[static_cast<int64_t>(o) * Cin + i] = acc[ao][bi][r];
+      }
+  if (do_bias && t < kWgTile && o0 + t < Cout) part_b[chunk * Cout + o0 + t] = bsum;
+}
+
+// dW = sum over chunks of the partials, dbias likewise; fixed order.
+__global__ void __launch_bounds__(kBlock)
+k_wgrad_reduce(const float* __restrict__ part, const float* __restrict__ part_b, int64_t chunks, int64_t count,
+               int Cout, float* __restrict__ dW, float* __restrict__ dbias) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (q < count) {
+    if (!dW) return;
+    float a = 0.f;
+    for (int64_t c = 0; c < chunks; ++c) a += part[c * count + q];
+    dW[q] = a;
+  } else if (q < count + Cout && dbias) {
+    const int64_t o = q - count;
+    float a = 0.f;
+    for (int64_t c = 0; c < chunks; ++c) a += part_b[c * Cout + o];
+    dbias[o] = a;
+  }
+}
+
+inline unsigned blocks_for(int64_t threads) { return static_cast<unsigned>((threads + kBlock - 1) / kBlock); }
+
+// Vertex chunks of the weight gradient: enough workgroups to fill the chip
+// (about 1536 over taps and tiles), chunks a multiple of the stage.
+void wgrad_chunks(int64_t n_out, int tiles, int64_t* chunks, int64_t* V) {
+  int64_t want = std::max<int64_t>(1, 1536 / (9 * static_cast<int64_t>(tiles)));
+  want = std::min<int64_t>(want, (n_out + kWgStage - 1) / kWgStage);
+  int64_t v = (n_out + want - 1) / want;
+  v = (v + kWgStage - 1) / kWgStage * kWgStage;
+  *V = v;
+  *chunks = (n_out + v - 1) / v;
+}
+
+}  // namespace
+
+void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, int64_t n, const float* in,
+                                int64_t ld_in, int C, float* out, int64_t ld_out, hipStream_t s) {
+  if (n <= 0) return;
+  launch(k_scale_by_weight_sum, dim3(blocks_for(n * kScaleLanes)), dim3(kBlock), 0, s, offsets, entry_w, n, in, ld_in,
+         C, out, ld_out);
+}
+
+void launch_relu_mask(const float* dY, int64_t ld_dy, const float* Y, int64_t ld_y, int C, int64_t n, float* G,
+                      int64_t ld_g, hipStream_t s) {
+  if (n <= 0) return;
+  launch(k_relu_mask, dim3(blocks_for(n * (C / 4))), dim3(kBlock), 0, s, dY, ld_dy, Y, ld_y, C, n, G, ld_g);
+}
+
+void launch_adjoint_weights(const float* W, int Cout, int Cin, float* Wt, hipStream_t s) {
+  launch(k_adjoint_weights, dim3(blocks_for(9LL * Cout * Cin)), dim3(kBlock), 0, s, W, Cout, Cin, Wt);
+}
+
+int64_t wgrad_partial_floats(int64_t n_out, int Cout, int Cin) {
+  if (n_out <= 0) return 0;
+  const int tiles = ((Cout + kWgTile - 1) / kWgTile) * ((Cin + kWgTile - 1) / kWgTile);
+  int64_t chunks, V;
+  wgrad_chunks(n_out, tiles, &chunks, &V);
+  return chunks * (9LL * Cout * Cin + Cout);
+}
+
+void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const float* X, int64_t ld_x, int Cin,
+                       const float* G, int64_t ld_g, int Cout, float* dW, float* dbias, float* partials,
+                       hipStream_t s) {
+  const int tiles_o = (Cout + kWgTile - 1) / kWgTile, tiles_i = (Cin + kWgTile - 1) / kWgTile;
+  const int64_t count = 9LL * Cout * Cin;
+  int64_t chunks = 0, V = 0;
+  if (n_out > 0) wgrad_chunks(n_out, tiles_o * tiles_i, &chunks, &V);
+  float* part = partials;
+  float* part_b = dbias ? partials + chunks * count : nullptr;
+  if (chunks > 0)
+    launch(k_conv_wgrad, dim3(static_cast<unsigned>(chunks), 9, static_cast<unsigned>(tiles_o * tiles_i)),
+           dim3(kBlock), 0, s, nbr, ldn, n_out, V, X, ld_x, Cin, G, ld_g, Cout, tiles_i, part, part_b);
+  // with no output vertex (chunks = 0) the sums below are zero
+  launch(k_wgrad_reduce, dim3(blocks_for(count + Cout)), dim3(kBlock), 0, s, static_cast<const float*>(part),
+         static_cast<const float*>(part_b), chunks, count, Cout, dW, dbias);
+}
+
+}  // namespace lat

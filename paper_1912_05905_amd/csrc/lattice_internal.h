@@ -100,10 +100,11 @@ __device__ inline int32_t tap_offset(int t, int i) {
 // ---------------------------------------------------------------------------
 struct Timer;   // kernel-family event timer (api.hip)
 // Kernel-family timing: while a ScopedKernelTimer of an enabled family is
-// alive on this thread, every launch() gets a start and a stop event that
-// the dispatch itself updates (hipExtLaunchKernel), so the family's time is
-// the sum of its kernels' execution times, without marker packets between
-// kernels.
+// alive on this thread, every launch() is bracketed by a start and a stop
+// event (created without the system-scope fence), so the family's time is
+// the sum of its kernels' execution times.  Scopes nest; the outermost one
+// names the family (a backward operator that reuses a forward kernel is
+// timed as the backward operator).
 void timer_begin(const char* family);
 void timer_end();
 bool timer_take_events(hipEvent_t* start, hipEvent_t* stop);
@@ -161,6 +162,16 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
                        int64_t n, int64_t total, const float* pos, const float* feat, int64_t ld_feat, int cf,
                        const float* W1, const float* b1, int C1, const float* W2, const float* b2, int C2,
                        const float* W3, const float* b3, int C3, float* out, int64_t ld_out, double* mu, void* work,
+                       hipStream_t s);
+// backward.hip
+void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, int64_t n, const float* in,
+                                int64_t ld_in, int C, float* out, int64_t ld_out, hipStream_t s);
+void launch_relu_mask(const float* dY, int64_t ld_dy, const float* Y, int64_t ld_y, int C, int64_t n, float* G,
+                      int64_t ld_g, hipStream_t s);
+void launch_adjoint_weights(const float* W, int Cout, int Cin, float* Wt, hipStream_t s);
+int64_t wgrad_partial_floats(int64_t n_out, int Cout, int Cin);
+void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const float* X, int64_t ld_x, int Cin,
+                       const float* G, int64_t ld_g, int Cout, float* dW, float* dbias, float* partials,
                        hipStream_t s);
 // conv.hip
 void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,

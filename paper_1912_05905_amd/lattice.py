@@ -45,6 +45,10 @@ SIGNATURES = {
     "lattice_deform_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _P]),
     "lattice_distribute_pointnet": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _P, _P, _I32, _P, _P, _I32,
                                            _P, _I64, _P]),
+    "lattice_splat_backward": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
+    "lattice_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _I64, _P]),
+    "lattice_conv_backward": (_I32, [_P, _P, _P, _I64, _I32, _P, _I32, _I32, _P, _I64, _P, _I64, _P, _I64, _P, _P,
+                                     _P]),
     "lattice_timing_enable": (_I32, [C.c_char_p, _I32]),
     "lattice_timing_read": (_I32, [C.c_char_p, C.POINTER(_I64), C.POINTER(C.c_double)]),
 }
@@ -265,6 +269,50 @@ class Lattice:
         _check(lib().lattice_distribute_pointnet(self._h, ptr(pos), fp, fld, cf, ptr(W1), ptr(b1), c1, ptr(W2),
                                                  ptr(b2), c2, ptr(W3), ptr(b3), c3, op, old, _stream(stream)))
         return out
+
+    # ---- backward passes (float32) ----
+    def splat_backward(self, dx: torch.Tensor, normalize: bool = True, out: torch.Tensor | None = None,
+                       stream=None) -> torch.Tensor:
+        """Gradient of splat(feat, normalize) with respect to feat, for
+        dL/dvalues = dx (n x C); returns m x C."""
+        Cc = dx.shape[1]
+        if out is None:
+            out = torch.empty((self.m, Cc), dtype=torch.float32, device="cuda")
+        xp, xld = _rows(dx)
+        _check(lib().lattice_splat_backward(self._h, xp, xld, Cc, int(bool(normalize)), C.c_void_p(out.data_ptr()),
+                                            _stream(stream)))
+        return out
+
+    def slice_backward(self, dout: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """Gradient of slice(x) with respect to x, for dL/dout = dout (m x C);
+        returns n x C."""
+        Cc = dout.shape[1]
+        if out is None:
+            out = torch.empty((self.n, Cc), dtype=torch.float32, device="cuda")
+        gp, gld = _rows(dout)
+        op, old = _rows(out)
+        _check(lib().lattice_slice_backward(self._h, gp, gld, Cc, op, old, _stream(stream)))
+        return out
+
+    def conv_backward(self, src: "Lattice", x: torch.Tensor | None, W: torch.Tensor | None, dy: torch.Tensor,
+                      relu: bool = False, y: torch.Tensor | None = None, want_dx: bool = True,
+                      want_dw: bool = True, want_dbias: bool = True, stream=None):
+        """Gradients of the convolution self <- src (1-hop, strided, or
+        Upsample when src = self.coarsen()) for dL/dY = dy: (dx, dW, dbias),
+        None where not asked for.  W is taps x Cout x Cin."""
+        cout = dy.shape[1]
+        cin = W.shape[2] if W is not None else x.shape[1]
+        dx = torch.empty((src.n, cin), dtype=torch.float32, device="cuda") if want_dx else None
+        dW = torch.empty((9, cout, cin), dtype=torch.float32, device="cuda") if want_dw else None
+        db = torch.empty((cout,), dtype=torch.float32, device="cuda") if want_dbias else None
+        xp, xld = _rows(x) if x is not None else (None, 0)
+        yp, yld = _rows(y) if y is not None else (None, 0)
+        gp, gld = _rows(dy)
+        dp, dld = _rows(dx) if dx is not None else (None, 0)
+        ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
+        _check(lib().lattice_conv_backward(self._h, src._h, xp, xld, cin, ptr(W), cout, LAT_RELU if relu else 0,
+                                           yp, yld, gp, gld, dp, dld, ptr(dW), ptr(db), _stream(stream)))
+        return dx, dW, db
 
     def deform_slice(self, x: torch.Tensor, wv: torch.Tensor, beta: float,
                      out: torch.Tensor | None = None, delta: torch.Tensor | None = None,

@@ -31,7 +31,8 @@ def test_header_declares_the_boundary():
     for need in ("lattice_create", "lattice_splat", "lattice_conv", "lattice_coarsen",
                  "lattice_refine", "lattice_slice", "lattice_deform_slice", "lattice_destroy",
                  "lattice_num_vertices", "lattice_export_keys", "lattice_export_neighbors",
-                 "lattice_export_simplices", "lattice_distribute_pointnet"):
+                 "lattice_export_simplices", "lattice_distribute_pointnet", "lattice_splat_backward",
+                 "lattice_slice_backward", "lattice_conv_backward"):
         assert need in names
 
 
@@ -73,6 +74,10 @@ def test_host_validation_without_gpu(lib):
     assert lib.lattice_distribute_pointnet(None, None, None, 0, 4, None, None, 16, None, None, 32, None, None, 64,
                                            None, 0, None) == -1
     assert lib.lattice_coarsen(None, 0, None, C.byref(out)) == -1
+    assert lib.lattice_splat_backward(None, None, 0, 8, 1, None, None) == -1
+    assert lib.lattice_slice_backward(None, None, 0, 8, None, 0, None) == -1
+    assert lib.lattice_conv_backward(None, None, None, 0, 8, None, 8, 0, None, 0, None, 0, None, 0, None, None,
+                                     None) == -1
 
 
 def test_timing_interface_without_events(lib):

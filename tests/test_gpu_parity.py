@@ -477,3 +477,112 @@ def test_distribute_pointnet_coarse_and_tiny(L, O):
                                   [(torch.zeros((16, 3), device="cuda"), None),
                                    (torch.zeros((32, 16), device="cuda"), None),
                                    (torch.zeros((64, 32), device="cuda"), None)]).shape == (0, 64)
+
+
+# ----------------------------------------------------------------------------
+# backward passes, against the oracle's gradients
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("C,normalize", [(4, True), (36, False), (64, True), (256, False)])
+def test_splat_and_slice_backward(L, O, C, normalize):
+    pos = _cloud(500 + C, 9000, 0.7)
+    gl, ol, g2o = _pair(L, O, pos, 0.06)
+    rng = np.random.default_rng(C)
+    dX = rng.normal(size=(ol.n, C)).astype(np.float32)
+    gf = gl.splat_backward(_dev(dX[g2o]), normalize=normalize)
+    of = ol.splat_backward(dX.astype(np.float64), normalize=normalize)
+    P.assert_close(_host(gf), of, P.TOL_F32, f"splat backward C={C}")
+    dO = rng.normal(size=(pos.shape[0], C)).astype(np.float32)
+    gx = gl.slice_backward(_dev(dO))
+    ox = ol.slice_backward(dO.astype(np.float64))
+    P.assert_close(P.rows_in_oracle_order(_host(gx), g2o), ox, P.TOL_F32, f"slice backward C={C}")
+
+
+def test_slice_backward_skewed(L, O):
+    """A 6000-point clump: vertex lists far longer than a workgroup span."""
+    rng = np.random.default_rng(9)
+    clump = (np.array([0.31, 0.42, 0.53]) + 1e-4 * rng.random((6000, 3))).astype(np.float32)
+    spread = rng.random((3001, 3)).astype(np.float32)
+    pos = np.concatenate([spread[:1500], clump, spread[1500:]]).astype(np.float32)
+    gl, ol, g2o = _pair(L, O, pos, 0.05)
+    dO = rng.normal(size=(pos.shape[0], 64)).astype(np.float32)
+    gx = gl.slice_backward(_dev(dO))
+    ox = ol.slice_backward(dO.astype(np.float64))
+    P.assert_close(P.rows_in_oracle_order(_host(gx), g2o), ox, P.TOL_F32, "skewed slice backward")
+    dX = rng.normal(size=(ol.n, 64)).astype(np.float32)
+    gf = gl.splat_backward(_dev(dX[g2o]), normalize=True)
+    P.assert_close(_host(gf), ol.splat_backward(dX.astype(np.float64), normalize=True), P.TOL_F32,
+                   "skewed splat backward")
+
+
+def _conv_backward_pair(L, O, form, seed, m, sigma, cin, cout, relu):
+    pos = _cloud(seed, m, 0.8)
+    gl = L.Lattice.create(_dev(pos), [sigma] * 3)
+    ol = O.Lattice.create(pos, np.full(3, sigma, np.float32))
+    g2o_f = P.key_permutation(_host(gl.keys()), ol.keys())
+    if form == "same":
+        (gd, gs, od, os_, g2o_d, g2o_s) = (gl, gl, ol, ol, g2o_f, g2o_f)
+        keep = ()
+    else:
+        gc, oc = gl.coarsen(), ol.coarsen()
+        g2o_c = P.key_permutation(_host(gc.keys()), oc.keys())
+        keep = (gc,)
+        if form == "strided":
+            (gd, gs, od, os_, g2o_d, g2o_s) = (gc, gl, oc, ol, g2o_c, g2o_f)
+        else:
+            (gd, gs, od, os_, g2o_d, g2o_s) = (gl, gc, ol, oc, g2o_f, g2o_c)
+    rng = np.random.default_rng(seed)
+    X = rng.normal(size=(os_.n, cin)).astype(np.float32)
+    W = _rand_w(rng, cin, cout, 1.0 / np.sqrt(9 * cin))
+    b = (0.3 * rng.normal(size=cout)).astype(np.float32)
+    dY = rng.normal(size=(od.n, cout)).astype(np.float32)
+    if form == "upsample":
+        Y = od.refine_into(os_, X.astype(np.float64), W.astype(np.float64), bias=b.astype(np.float64), relu=relu)
+    else:
+        Y = od.conv(os_, X.astype(np.float64), W.astype(np.float64), bias=b.astype(np.float64), relu=relu)
+    odx, odw, odb = od.conv_backward(os_, X.astype(np.float64), W.astype(np.float64), dY.astype(np.float64),
+                                     relu=relu, Y=Y if relu else None)
+    gdx, gdw, gdb = gd.conv_backward(gs, _dev(X[g2o_s]), _gpu_w(W), _dev(dY[g2o_d]), relu=relu,
+                                     y=_dev(Y[g2o_d].astype(np.float32)) if relu else None)
+    what = f"{form} {cin}->{cout} relu={relu}"
+    P.assert_close(P.rows_in_oracle_order(_host(gdx), g2o_s), odx, P.TOL_F32, "dX " + what)
+    P.assert_close(np.transpose(_host(gdw), (0, 2, 1)), odw, P.TOL_F32, "dW " + what)
+    P.assert_close(_host(gdb), odb, P.TOL_F32, "dbias " + what)
+    del keep
+
+
+@pytest.mark.parametrize("cin,cout", [(8, 16), (12, 20), (64, 64), (32, 96), (128, 128), (256, 64)])
+def test_conv_backward_same_level(L, O, cin, cout):
+    for relu in (False, True):
+        _conv_backward_pair(L, O, "same", 600 + cin, 6000, 0.07, cin, cout, relu)
+
+
+@pytest.mark.parametrize("form", ["strided", "upsample"])
+def test_conv_backward_across_levels(L, O, form):
+    for cin, cout, relu in ((64, 128, True), (128, 64, False), (20, 36, True)):
+        _conv_backward_pair(L, O, form, 700 + cin, 8000, 0.05, cin, cout, relu)
+
+
+def test_conv_backward_partial_outputs_and_tiny(L, O):
+    """Only some gradients asked for; a one-point cloud."""
+    pos = _cloud(801, 3000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.08)
+    rng = np.random.default_rng(801)
+    X = rng.normal(size=(ol.n, 16)).astype(np.float32)
+    W = _rand_w(rng, 16, 8, 0.1)
+    dY = rng.normal(size=(ol.n, 8)).astype(np.float32)
+    odx, odw, odb = ol.conv_backward(ol, X.astype(np.float64), W.astype(np.float64), dY.astype(np.float64))
+    gdx, gdw, gdb = gl.conv_backward(gl, None, _gpu_w(W), _dev(dY[g2o]), want_dw=False, want_dbias=False)
+    assert gdw is None and gdb is None
+    P.assert_close(P.rows_in_oracle_order(_host(gdx), g2o), odx, P.TOL_F32, "dX only")
+    gdx, gdw, gdb = gl.conv_backward(gl, _dev(X[g2o]), None, _dev(dY[g2o]), want_dx=False)
+    P.assert_close(np.transpose(_host(gdw), (0, 2, 1)), odw, P.TOL_F32, "dW only")
+    P.assert_close(_host(gdb), odb, P.TOL_F32, "dbias only")
+    pos1 = _cloud(802, 1, 0.5)
+    g1, o1, g2o1 = _pair(L, O, pos1, 0.1)
+    X1 = rng.normal(size=(o1.n, 8)).astype(np.float32)
+    W1 = _rand_w(rng, 8, 8, 0.3)
+    dY1 = rng.normal(size=(o1.n, 8)).astype(np.float32)
+    odx, odw, odb = o1.conv_backward(o1, X1.astype(np.float64), W1.astype(np.float64), dY1.astype(np.float64))
+    gdx, gdw, gdb = g1.conv_backward(g1, _dev(X1[g2o1]), _gpu_w(W1), _dev(dY1[g2o1]))
+    P.assert_close(P.rows_in_oracle_order(_host(gdx), g2o1), odx, P.TOL_F32, "tiny dX")
+    P.assert_close(np.transpose(_host(gdw), (0, 2, 1)), odw, P.TOL_F32, "tiny dW")
