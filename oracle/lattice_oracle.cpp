@@ -49,7 +49,7 @@
 //    GroupNorm is not part of this operator.
 //  * Backward passes: gradients of the forward operators above; the ReLU's
 //    derivative is 0 at 0 and DeformSlice's maximum passes its gradient to
-//    the first maximal vertex.
+//    the first maximal vertex, maximal among the float32 products b_k x_k.
 #include <algorithm>
 #include <array>
 #include <cmath>
@@ -646,7 +646,7 @@ int orc_conv_backward(const orc_lattice* dst, const orc_lattice* src, const doub
 
 // DeformSlice backward.  Forward per point p (vertex k of its simplex, value
 // x_k = X[I_p[k]], weight b_k):
-//   q_k = b_k x_k,  M = max_k q_k per channel (first maximal k on ties),
+//   q_k = b_k x_k,  M = max_k q_k per channel (at the first k maximal in float32),
 //   s_k = beta + (q_k - M) . wv,  db_k = tanh(s_k),  out = sum_k (b_k + db_k) x_k.
 // With g = dOut_p, a_k = g . x_k and e_k = a_k (1 - db_k^2) = dL/ds_k:
 //   dx_k += (b_k + db_k) g + e_k b_k wv - [k = argmax_c] (sum_j e_j) b_k wv_c,
@@ -665,10 +665,19 @@ int orc_deform_slice_backward(const orc_lattice* L, const double* X, int C, cons
     const float* b = &L->bary[p * kD1];
     for (int k = 0; k < kD1; ++k)
       for (int c = 0; c < C; ++c) q[k * C + c] = static_cast<double>(b[k]) * X[I[k] * C + c];
+    // the vertex that receives the maximum's gradient is decided on the
+    // float32 products b_k x_k (the GPU's precision): a discrete choice taken
+    // by floating point must be taken the same way on both sides
     for (int c = 0; c < C; ++c) {
       am[c] = 0;
-      for (int k = 1; k < kD1; ++k)
-        if (q[k * C + c] > q[am[c] * C + c]) am[c] = k;
+      float best = static_cast<float>(b[0]) * static_cast<float>(X[I[0] * C + c]);
+      for (int k = 1; k < kD1; ++k) {
+        const float qk = static_cast<float>(b[k]) * static_cast<float>(X[I[k] * C + c]);
+        if (qk > best) {
+          best = qk;
+          am[c] = k;
+        }
+      }
       mx[c] = q[am[c] * C + c];
     }
     const double* g = dOut + p * C;
