@@ -256,6 +256,23 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
                           float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream);
 
 /*
+ * DeformSlice backward (Eq. (deformSlice) with the equivariant offset
+ * regressor) for out_p = sum_k (b_pk + db_pk) x_k, db_pk = tanh(beta +
+ * (b_pk x_k - max_j b_pj x_j) . wv), given dOut = dL/dout:
+ *   dvals  n x C (row stride ld_dvals): dL/dx for every vertex, gathered
+ *          over the vertex lists (deterministic order);
+ *   dwv    C floats: dL/dwv;  dbeta  1 float: dL/dbeta.
+ * The maximum passes its gradient to the first vertex slot whose float32
+ * product b_pk x_k is maximal.  vals, wv, beta are the forward's inputs (n x
+ * C float32, row stride ld_vals); dOut is m x C (row stride ld_dOut).  Row
+ * strides of 0 mean dense; C a multiple of 4, at most 512; dvals must not
+ * overlap vals.  Uses work space of O(m (64 + C)) bytes from the pool.
+ */
+int lattice_deform_slice_backward(lattice_t L, const float* vals_dev, int64_t ld_vals, int C, const float* wv_dev,
+                                  float beta, const float* dOut_dev, int64_t ld_dOut, float* dvals_dev,
+                                  int64_t ld_dvals, float* dwv_dev, float* dbeta_dev, hipStream_t stream);
+
+/*
  * Timing of the library's kernels with HIP events on the launch stream, for
  * measurement.  enable != 0 records a start/stop event pair around every
  * launch of the kernel family `name` ("conv", "splat", "slice", "insert",

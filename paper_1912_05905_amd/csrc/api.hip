@@ -918,6 +918,36 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
   return check_launch("conv backward");
 }
 
+int lattice_deform_slice_backward(lattice_t L, const float* vals_dev, int64_t ld_vals, int C, const float* wv_dev,
+                                  float beta, const float* dOut_dev, int64_t ld_dOut, float* dvals_dev,
+                                  int64_t ld_dvals, float* dwv_dev, float* dbeta_dev, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if (ld_vals == 0) ld_vals = C;
+  if (ld_dOut == 0) ld_dOut = C;
+  if (ld_dvals == 0) ld_dvals = C;
+  if ((st = check_matrix(vals_dev, ld_vals, C, LAT_F32, "vals", L->n > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(dOut_dev, ld_dOut, C, LAT_F32, "dOut", L->m > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(dvals_dev, ld_dvals, C, LAT_F32, "dvals", L->n > 0)) != LAT_OK) return st;
+  if (!wv_dev || !dwv_dev || !dbeta_dev) return fail(LAT_EINVAL, "wv, dwv and dbeta must not be null");
+  if (!std::isfinite(beta)) return fail(LAT_EINVAL, "beta must be finite");
+  if (C > deform_max_channels(false))
+    return fail(LAT_EUNSUPPORTED, "DeformSlice backward supports at most " +
+                                      std::to_string(deform_max_channels(false)) + " channels");
+  if (L->n > 0 &&
+      overlaps(dvals_dev, sizeof(float) * static_cast<size_t>((L->n - 1) * ld_dvals + C), vals_dev,
+               sizeof(float) * static_cast<size_t>((L->n - 1) * ld_vals + C)))
+    return fail(LAT_EINVAL, "dvals and vals overlap");
+  Scratch work;
+  if ((st = work.get(static_cast<size_t>(deform_backward_workspace_bytes(L->m, C, L->total, L->chunk)), stream)) !=
+      LAT_OK)
+    return st;
+  launch_deform_slice_backward(L->idx, L->w, L->m, L->offsets, L->entries, L->chunk_first, L->chunk, L->nmax,
+                               L->total, vals_dev, ld_vals, C, wv_dev, beta, dOut_dev, ld_dOut, dvals_dev, ld_dvals,
+                               dwv_dev, dbeta_dev, work.p, stream);
+  return check_launch("deform slice backward");
+}
+
 int lattice_timing_enable(const char* name, int enable) {
   if (!name) return fail(LAT_EINVAL, "name is null");
   std::lock_guard<std::mutex> lk(g_timer_mu);

@@ -2,12 +2,15 @@
 // HBM bandwidth: a row of C channels is handled by a group of LPR lanes
 // (LPR a power of two), each lane moving 16 bytes (4 fp32 or 8 bf16 channels)
 // per access so that a row is one contiguous, fully used transaction.
+#include <algorithm>
+
 #include "lattice_internal.h"
 
 namespace lat {
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int64_t kDeformBwdGrid = 1024;   // workgroups of the DeformSlice backward's per-point pass
 
 // float -> bfloat16, round to nearest even (NaN stays NaN).
 __device__ inline uint16_t f32_to_bf16(float f) {
@@ -136,6 +139,97 @@ __device__ inline void splat_add(float (&acc)[Q][Chunk<BF16>::N], const float* p
   }
 }
 
+// What a list entry e = 4p + k adds to its vertex's row.  The splat adds
+// w_e f_p (and w_e to the weight sum).
+template <bool BF16, int LPR, int Q, int B>
+struct WeightedRows {
+  using Ch = Chunk<BF16>;
+  const float* entry_w;
+  const void* feat;
+  int64_t ld_feat;
+  struct Batch {
+    float wt[B];
+    Ch f[B][Q];
+  };
+  __device__ inline void init(int, int) {}
+  __device__ inline void load(Batch& bt, int j, int64_t s, int32_t e, bool in, int lane, int nchunk) const {
+    bt.wt[j] = in ? entry_w[s] : 0.f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int ch = lane + q * LPR;
+      if (in && ch < nchunk)
+        bt.f[j][q].load(feat, static_cast<int64_t>(e >> 2) * ld_feat + static_cast<int64_t>(ch) * Ch::N);
+      else
+#pragma unroll
+        for (int i = 0; i < Ch::N; ++i) bt.f[j][q].v[i] = 0.f;
+    }
+  }
+  __device__ inline float add(const Batch& bt, int j, float (&acc)[Q][Ch::N]) const {
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+#pragma unroll
+      for (int i = 0; i < Ch::N; ++i) acc[q][i] += bt.wt[j] * bt.f[j][q].v[i];
+    return bt.wt[j];
+  }
+};
+
+// DeformSlice backward, what entry e = (p, k) adds to dL/dx of its vertex:
+//   alpha_e g_p + wv * (beta_e - [argmax_c(p) = k] gamma_e)
+// with coef[e] = (alpha_e, beta_e, gamma_e, 0) and am[p][c] the vertex slot
+// holding channel c's maximum (fp32 only).
+template <int LPR, int Q, int B>
+struct DeformGradRows {
+  using Ch = Chunk<false>;
+  const float* g;
+  int64_t ld_g;
+  const float4* coef;
+  const uint8_t* am;
+  const float* wv;
+  int C;
+  float wvc[Q][4];
+  struct Batch {
+    float4 cf[B];
+    int k[B];
+    Ch f[B][Q];
+    uint32_t m[B][Q];
+  };
+  __device__ inline void init(int lane, int nchunk) {
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int ch = lane + q * LPR;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) wvc[q][i] = ch < nchunk ? wv[4 * ch + i] : 0.f;
+    }
+  }
+  __device__ inline void load(Batch& bt, int j, int64_t, int32_t e, bool in, int lane, int nchunk) const {
+    bt.cf[j] = in ? coef[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+    bt.k[j] = e & 3;
+    const int64_t p = e >> 2;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int ch = lane + q * LPR;
+      if (in && ch < nchunk) {
+        bt.f[j][q].load(g, p * ld_g + 4 * ch);
+        bt.m[j][q] = *reinterpret_cast<const uint32_t*>(am + p * C + 4 * ch);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) bt.f[j][q].v[i] = 0.f;
+        bt.m[j][q] = 0xffffffffu;
+      }
+    }
+  }
+  __device__ inline float add(const Batch& bt, int j, float (&acc)[Q][4]) const {
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool mx = ((bt.m[j][q] >> (8 * i)) & 0xffu) == static_cast<uint32_t>(bt.k[j]);
+        acc[q][i] += bt.cf[j].x * bt.f[j][q].v[i] + wvc[q][i] * (bt.cf[j].y - (mx ? bt.cf[j].z : 0.f));
+      }
+    return 0.f;
+  }
+};
+
 // LDS of k_splat_chunks: head and tail pieces of the G chunks, their weights
 // and flags.
 inline size_t splat_lds_bytes(int lpr, int C) {
@@ -143,11 +237,10 @@ inline size_t splat_lds_bytes(int lpr, int C) {
   return sizeof(float) * (2 * static_cast<size_t>(G) * C + 2 * G) + sizeof(int32_t) * G;
 }
 
-template <bool BF16, int LPR, int Q, int B>
+template <bool BF16, int LPR, int Q, int B, class Rows>
 __global__ void __launch_bounds__(kBlock)
-k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
-               const float* __restrict__ entry_w, const int32_t* __restrict__ chunk_first, int chunk,
-               int64_t n, int64_t total, const void* __restrict__ feat, int64_t ld_feat, int C, int normalize,
+k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries, Rows rows,
+               const int32_t* __restrict__ chunk_first, int chunk, int64_t n, int64_t total, int C, int normalize,
                void* __restrict__ vals, int64_t ld_vals, float* __restrict__ wsum,
                float* __restrict__ part_head, float* __restrict__ part_tail, float* __restrict__ part_w,
                unsigned nblk) {
@@ -170,6 +263,7 @@ k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
   const int64_t s1 = min(s0 + static_cast<int64_t>(chunk), total);
   const int64_t span_end = min((c0 + G) * static_cast<int64_t>(chunk), total);
   const int nchunk = C / Ch::N;
+  rows.init(lane, nchunk);
   if (lane == 0) sh_flag[g] = 0;
   int32_t tail_v = -1, tail_ve = 0;    // vertex of this chunk's tail piece
   int32_t head_ve = 0;                 // end of the vertex the chunk starts inside
@@ -189,33 +283,15 @@ k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
     float ws = 0.f;
     for (int64_t s = s0; s < s1; s += B) {
       int32_t e[B];
-      float wt[B];
 #pragma unroll
-      for (int j = 0; j < B; ++j) {
-        const bool in = s + j < s1;
-        e[j] = in ? entries[s + j] : 0;
-        wt[j] = in ? entry_w[s + j] : 0.f;
-      }
-      Ch f[B][Q];
+      for (int j = 0; j < B; ++j) e[j] = s + j < s1 ? entries[s + j] : 0;
+      typename Rows::Batch bt;
 #pragma unroll
-      for (int j = 0; j < B; ++j)
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-          const int ch = lane + q * LPR;
-          if (s + j < s1 && ch < nchunk)
-            f[j][q].load(feat, static_cast<int64_t>(e[j] >> 2) * ld_feat + static_cast<int64_t>(ch) * Ch::N);
-          else
-#pragma unroll
-            for (int i = 0; i < Ch::N; ++i) f[j][q].v[i] = 0.f;
-        }
+      for (int j = 0; j < B; ++j) rows.load(bt, j, s + j, e[j], s + j < s1, lane, nchunk);
 #pragma unroll
       for (int j = 0; j < B; ++j) {
         if (s + j >= s1) break;
-#pragma unroll
-        for (int q = 0; q < Q; ++q)
-#pragma unroll
-          for (int i = 0; i < Ch::N; ++i) acc[q][i] += wt[j] * f[j][q].v[i];
-        ws += wt[j];
+        ws += rows.add(bt, j, acc);
         const int64_t nxt = s + j + 1;
         if (nxt == ve || nxt == s1) {
           if (vb >= s0 && ve <= s1) {
@@ -434,6 +510,155 @@ k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64
 }
 
 // lanes per row: enough 16-byte chunks to cover C, at most 64 (a wavefront)
+// DeformSlice backward, per point (C channels over LPR lanes, CPL 16-byte
+// chunks per lane, as in the forward), with g = dL/dout_p:
+//   q_k = b_k x_k; am_c = the first slot k whose float32 q_k is maximal,
+//   M_c = q_{am_c}; s_k = beta + (q_k - M) . wv; db_k = tanh(s_k);
+//   a_k = g . x_k; e_k = a_k (1 - db_k^2) (= dL/ds_k).
+// It writes coef[4p + k] = (b_k + db_k, e_k b_k, (sum_j e_j) b_k, 0) and
+// am[p][c] for the gather over J_v, and adds sum_k e_k (q_k - M) (dL/dwv) and
+// sum_k e_k (dL/dbeta) into per-workgroup partials: the workgroups stride
+// over the points, sum in registers, then over their lane groups in a fixed
+// order.
+template <int LPR, int CPL>
+__global__ void __launch_bounds__(kBlock)
+k_deform_bwd_point(const int4* __restrict__ idx, const float4* __restrict__ w, int64_t m,
+                   const float* __restrict__ vals, int64_t ld_vals, int C, const float* __restrict__ wvec, float beta,
+                   const float* __restrict__ dout, int64_t ld_dout, float4* __restrict__ coef,
+                   uint8_t* __restrict__ am, float* __restrict__ part_wv, float* __restrict__ part_beta) {
+  constexpr int G = kBlock / LPR;
+  __shared__ float red[kBlock * CPL * 4];   // [group][channel], G * C <= this
+  __shared__ float red_b[G];
+  const int lane = threadIdx.x & (LPR - 1), grp = threadIdx.x / LPR;
+  const int nchunk = C / 4;
+  float wacc[CPL][4];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) wacc[q][i] = 0.f;
+  float bacc = 0.f;
+  const int64_t groups = (m + G - 1) / G;
+  for (int64_t it = blockIdx.x; it < groups; it += gridDim.x) {
+    const int64_t p = it * G + grp;
+    const bool live = p < m;
+    int4 iv = make_int4(0, 0, 0, 0);
+    float4 wq = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (live) { iv = idx[p]; wq = w[p]; }
+    const int32_t vi[4] = {iv.x, iv.y, iv.z, iv.w};
+    const float bw[4] = {wq.x, wq.y, wq.z, wq.w};
+    float x[CPL][4][4], gv[CPL][4], mx[CPL][4];
+    float sp[4] = {0.f, 0.f, 0.f, 0.f}, ap[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      const int ch = lane + q * LPR;
+      const bool on = live && ch < nchunk;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (on) v = *reinterpret_cast<const float4*>(vals + static_cast<int64_t>(vi[k]) * ld_vals + 4 * ch);
+        x[q][k][0] = v.x; x[q][k][1] = v.y; x[q][k][2] = v.z; x[q][k][3] = v.w;
+      }
+      float4 gg = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (on) gg = *reinterpret_cast<const float4*>(dout + p * ld_dout + 4 * ch);
+      gv[q][0] = gg.x; gv[q][1] = gg.y; gv[q][2] = gg.z; gv[q][3] = gg.w;
+      uint32_t word = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float wc = on ? wvec[4 * ch + i] : 0.f;
+        float qk[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) qk[k] = bw[k] * x[q][k][i];
+        float best = qk[0];
+        uint32_t a = 0;
+#pragma unroll
+        for (int k = 1; k < 4; ++k)
+          if (qk[k] > best) {
+            best = qk[k];
+            a = static_cast<uint32_t>(k);
+          }
+        mx[q][i] = best;
+        word |= a << (8 * i);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          sp[k] += (qk[k] - best) * wc;
+          ap[k] += gv[q][i] * x[q][k][i];
+        }
+      }
+      if (on) *reinterpret_cast<uint32_t*>(am + p * C + 4 * ch) = word;
+    }
+#pragma unroll
+    for (int off = LPR / 2; off > 0; off >>= 1)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        sp[k] += __shfl_xor(sp[k], off, LPR);
+        ap[k] += __shfl_xor(ap[k], off, LPR);
+      }
+    float e[4], esum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float db = tanhf(beta + sp[k]);
+      e[k] = ap[k] * (1.f - db * db);
+      esum += e[k];
+      sp[k] = db;
+    }
+    if (!live) continue;
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) coef[4 * p + k] = make_float4(bw[k] + sp[k], e[k] * bw[k], esum * bw[k], 0.f);
+      bacc += esum;
+    }
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float a = 0.f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) a += e[k] * (bw[k] * x[q][k][i] - mx[q][i]);
+        wacc[q][i] += a;
+      }
+  }
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
+    const int ch = lane + q * LPR;
+    if (ch < nchunk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[grp * C + 4 * ch + i] = wacc[q][i];
+  }
+  if (lane == 0) red_b[grp] = bacc;
+  __syncthreads();
+  for (int c = threadIdx.x; c < C; c += kBlock) {
+    float a = 0.f;
+    for (int g2 = 0; g2 < G; ++g2) a += red[g2 * C + c];
+    part_wv[static_cast<int64_t>(blockIdx.x) * C + c] = a;
+  }
+  if (threadIdx.x == 0) {
+    float a = 0.f;
+    for (int g2 = 0; g2 < G; ++g2) a += red_b[g2];
+    part_beta[blockIdx.x] = a;
+  }
+}
+
+// dL/dwv[c] (workgroup c < C) and dL/dbeta (workgroup C): the per-workgroup
+// partials added by a fixed tree.
+__global__ void __launch_bounds__(kBlock)
+k_deform_bwd_reduce(const float* __restrict__ part_wv, const float* __restrict__ part_beta, int64_t nparts, int C,
+                    float* __restrict__ dwv, float* __restrict__ dbeta) {
+  __shared__ float sh[kBlock];
+  const int c = blockIdx.x;
+  float a = 0.f;
+  for (int64_t b = threadIdx.x; b < nparts; b += kBlock) a += c < C ? part_wv[b * C + c] : part_beta[b];
+  sh[threadIdx.x] = a;
+  __syncthreads();
+  for (int off = kBlock / 2; off > 0; off >>= 1) {
+    if (static_cast<int>(threadIdx.x) < off) sh[threadIdx.x] += sh[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    if (c < C) dwv[c] = sh[0];
+    else *dbeta = sh[0];
+  }
+}
+
 inline int lanes_per_row(int C, bool bf16) {
   const int chunks = C / (bf16 ? 8 : 4);
   int l = 1;
@@ -455,15 +680,17 @@ void splat_launch(const int32_t* off, const int32_t* ent, const float* ew, const
   const int64_t nspans = (total + span_len - 1) / span_len;
   const unsigned nblk = static_cast<unsigned>(nspans);
   const size_t lds = splat_lds_bytes(LPR, C);
+  using Rows = WeightedRows<BF16, LPR, Q, B>;
   static bool lds_limit_set = false;
   if (!lds_limit_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_splat_chunks<BF16, LPR, Q, B>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_splat_chunks<BF16, LPR, Q, B, Rows>),
                               hipFuncAttributeMaxDynamicSharedMemorySize,
                               static_cast<int>(splat_lds_bytes(LPR, LPR * Q * Chunk<BF16>::N)));
     lds_limit_set = true;
   }
-  launch((k_splat_chunks<BF16, LPR, Q, B>), dim3(xcd_grid(nblk)), dim3(kBlock), lds, s, off, ent, ew, cf,
-                     chunk, n, total, feat, ldf, C, norm, vals, ldv, wsum, ph, pt, pw, nblk);
+  const Rows rows{ew, feat, ldf};
+  launch((k_splat_chunks<BF16, LPR, Q, B, Rows>), dim3(xcd_grid(nblk)), dim3(kBlock), lds, s, off, ent, rows, cf,
+         chunk, n, total, C, norm, vals, ldv, wsum, ph, pt, pw, nblk);
   if (nspans > 1)
     launch((k_splat_finish<BF16, LPR, Q>), dim3(grid_for(nspans, LPR)), dim3(kBlock), 0, s, off, cf,
                        span_len, G, nspans, C, norm, vals, ldv, wsum, ph, pt, pw);
@@ -478,6 +705,57 @@ void splat_dispatch(int lpr, int q, const int32_t* off, const int32_t* ent, cons
   SPLAT_CASE(1, 1) SPLAT_CASE(2, 1) SPLAT_CASE(4, 1) SPLAT_CASE(8, 1) SPLAT_CASE(16, 1)
   SPLAT_CASE(32, 1) SPLAT_CASE(64, 1) SPLAT_CASE(64, 2) SPLAT_CASE(64, 4)
 #undef SPLAT_CASE
+}
+
+template <int LPR, int Q>
+void deform_grad_gather(const int32_t* off, const int32_t* ent, const int32_t* cf, int chunk, int64_t n,
+                        int64_t total, const float* g, int64_t ldg, const float4* coef, const uint8_t* am,
+                        const float* wv, int C, float* dx, int64_t ldx, float* ph, float* pt, float* pw,
+                        hipStream_t s) {
+  constexpr int B = 8 / Q;
+  constexpr int G = kBlock / LPR;
+  using Rows = DeformGradRows<LPR, Q, B>;
+  const int64_t span_len = static_cast<int64_t>(G) * chunk;
+  const int64_t nspans = (total + span_len - 1) / span_len;
+  const unsigned nblk = static_cast<unsigned>(nspans);
+  const size_t lds = splat_lds_bytes(LPR, C);
+  static bool lds_limit_set = false;
+  if (!lds_limit_set) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_splat_chunks<false, LPR, Q, B, Rows>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              static_cast<int>(splat_lds_bytes(LPR, LPR * Q * 4)));
+    lds_limit_set = true;
+  }
+  Rows rows{g, ldg, coef, am, wv, C, {}};
+  launch((k_splat_chunks<false, LPR, Q, B, Rows>), dim3(xcd_grid(nblk)), dim3(kBlock), lds, s, off, ent, rows, cf,
+         chunk, n, total, C, 0, static_cast<void*>(dx), ldx, static_cast<float*>(nullptr), ph, pt, pw, nblk);
+  if (nspans > 1)
+    launch((k_splat_finish<false, LPR, Q>), dim3(grid_for(nspans, LPR)), dim3(kBlock), 0, s, off, cf, span_len, G,
+           nspans, C, 0, static_cast<void*>(dx), ldx, static_cast<float*>(nullptr), static_cast<const float*>(ph),
+           static_cast<const float*>(pt), static_cast<const float*>(pw));
+}
+
+void deform_grad_dispatch(int lpr, int q, const int32_t* off, const int32_t* ent, const int32_t* cf, int chunk,
+                          int64_t n, int64_t total, const float* g, int64_t ldg, const float4* coef,
+                          const uint8_t* am, const float* wv, int C, float* dx, int64_t ldx, float* ph, float* pt,
+                          float* pw, hipStream_t s) {
+#define DGRAD_CASE(L, QQ) \
+  if (lpr == L && q == QQ) return deform_grad_gather<L, QQ>(off, ent, cf, chunk, n, total, g, ldg, coef, am, wv, C, dx, ldx, ph, pt, pw, s);
+  DGRAD_CASE(1, 1) DGRAD_CASE(2, 1) DGRAD_CASE(4, 1) DGRAD_CASE(8, 1) DGRAD_CASE(16, 1)
+  DGRAD_CASE(32, 1) DGRAD_CASE(64, 1) DGRAD_CASE(64, 2)
+#undef DGRAD_CASE
+}
+
+template <int CPL>
+void deform_bwd_point_dispatch(int lpr, unsigned grid, const int32_t* idx, const float* w, int64_t m,
+                               const float* vals, int64_t ldv, int C, const float* wv, float beta, const float* dout,
+                               int64_t ldo, float4* coef, uint8_t* am, float* pwv, float* pb, hipStream_t s) {
+  const int4* i4 = reinterpret_cast<const int4*>(idx);
+  const float4* w4 = reinterpret_cast<const float4*>(w);
+#define DPT_CASE(L) \
+  if (lpr == L) return launch((k_deform_bwd_point<L, CPL>), dim3(grid), dim3(kBlock), 0, s, i4, w4, m, vals, ldv, C, wv, beta, dout, ldo, coef, am, pwv, pb);
+  DPT_CASE(1) DPT_CASE(2) DPT_CASE(4) DPT_CASE(8) DPT_CASE(16) DPT_CASE(32) DPT_CASE(64)
+#undef DPT_CASE
 }
 
 template <bool BF16>
@@ -559,6 +837,53 @@ void launch_slice(const int32_t* idx, const float* w, int64_t m, const void* val
   ScopedKernelTimer tm("slice", s);
   if (bf16) slice_dispatch<true>(lpr, idx, w, m, vals, ld_vals, C, out, s);
   else slice_dispatch<false>(lpr, idx, w, m, vals, ld_vals, C, out, s);
+}
+
+// Work space of launch_deform_slice_backward, in bytes.
+int64_t deform_backward_workspace_bytes(int64_t m, int C, int64_t total, int chunk) {
+  return 16 * 4 * m + m * C + 4 * (kDeformBwdGrid * (static_cast<int64_t>(C) + 1)) +
+         4 * splat_partial_floats(total, chunk, C) + 64;
+}
+
+void launch_deform_slice_backward(const int32_t* idx, const float* w, int64_t m, const int32_t* offsets,
+                                  const int32_t* entries, const int32_t* chunk_first, int chunk, int64_t n,
+                                  int64_t total, const float* vals, int64_t ld_vals, int C, const float* wv,
+                                  float beta, const float* dout, int64_t ld_dout, float* dvals, int64_t ld_dvals,
+                                  float* dwv, float* dbeta, void* work, hipStream_t s) {
+  ScopedKernelTimer tm("deform_bwd", s);
+  if (m <= 0 || n <= 0) {
+    // no point: dL/dwv and dL/dbeta are empty sums
+    launch(k_deform_bwd_reduce, dim3(static_cast<unsigned>(C + 1)), dim3(kBlock), 0, s,
+           static_cast<const float*>(nullptr), static_cast<const float*>(nullptr), static_cast<int64_t>(0), C, dwv,
+           dbeta);
+    return;
+  }
+  char* wp = static_cast<char*>(work);
+  float4* coef = reinterpret_cast<float4*>(wp);
+  wp += 16 * 4 * m;
+  float* pwv = reinterpret_cast<float*>(wp);
+  wp += 4 * kDeformBwdGrid * static_cast<int64_t>(C);
+  float* pb = reinterpret_cast<float*>(wp);
+  wp += 4 * kDeformBwdGrid;
+  float* parts = reinterpret_cast<float*>(wp);
+  wp += 4 * splat_partial_floats(total, chunk, C);
+  uint8_t* am = reinterpret_cast<uint8_t*>(wp);
+  const int lpr = lanes_per_row(C, false);
+  const int chunks = C / 4;
+  const int G = kBlock / lpr;
+  const int64_t groups = (m + G - 1) / G;
+  const unsigned grid = static_cast<unsigned>(std::min<int64_t>(groups, kDeformBwdGrid));
+  if (chunks > lpr)
+    deform_bwd_point_dispatch<2>(lpr, grid, idx, w, m, vals, ld_vals, C, wv, beta, dout, ld_dout, coef, am, pwv, pb, s);
+  else
+    deform_bwd_point_dispatch<1>(lpr, grid, idx, w, m, vals, ld_vals, C, wv, beta, dout, ld_dout, coef, am, pwv, pb, s);
+  launch(k_deform_bwd_reduce, dim3(static_cast<unsigned>(C + 1)), dim3(kBlock), 0, s, static_cast<const float*>(pwv),
+         static_cast<const float*>(pb), static_cast<int64_t>(grid), C, dwv, dbeta);
+  const int q = chunks <= lpr ? 1 : 2;
+  const int64_t span_len = static_cast<int64_t>(kBlock / lpr) * chunk;
+  const int64_t nspans = (total + span_len - 1) / span_len;
+  deform_grad_dispatch(lpr, q, offsets, entries, chunk_first, chunk, n, total, dout, ld_dout, coef, am, wv, C, dvals,
+                       ld_dvals, parts, parts + nspans * C, parts + 2 * nspans * C, s);
 }
 
 void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const void* vals,

@@ -49,6 +49,7 @@ SIGNATURES = {
     "lattice_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _I64, _P]),
     "lattice_conv_backward": (_I32, [_P, _P, _P, _I64, _I32, _P, _I32, _I32, _P, _I64, _P, _I64, _P, _I64, _P, _P,
                                      _P]),
+    "lattice_deform_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _F32, _P, _I64, _P, _I64, _P, _P, _P]),
     "lattice_timing_enable": (_I32, [C.c_char_p, _I32]),
     "lattice_timing_read": (_I32, [C.c_char_p, C.POINTER(_I64), C.POINTER(C.c_double)]),
 }
@@ -313,6 +314,22 @@ class Lattice:
         _check(lib().lattice_conv_backward(self._h, src._h, xp, xld, cin, ptr(W), cout, LAT_RELU if relu else 0,
                                            yp, yld, gp, gld, dp, dld, ptr(dW), ptr(db), _stream(stream)))
         return dx, dW, db
+
+    def deform_slice_backward(self, x: torch.Tensor, wv: torch.Tensor, beta: float, dout: torch.Tensor,
+                              stream=None):
+        """Gradients of deform_slice(x, wv, beta) for dL/dout = dout:
+        (dx n x C, dwv C, dbeta scalar tensor)."""
+        Cc = x.shape[1]
+        dx = torch.empty((self.n, Cc), dtype=torch.float32, device="cuda")
+        dwv = torch.empty((Cc,), dtype=torch.float32, device="cuda")
+        dbeta = torch.empty((1,), dtype=torch.float32, device="cuda")
+        xp, xld = _rows(x)
+        gp, gld = _rows(dout)
+        dp, dld = _rows(dx)
+        _check(lib().lattice_deform_slice_backward(self._h, xp, xld, Cc, C.c_void_p(wv.data_ptr()), float(beta), gp, gld,
+                                                   dp, dld, C.c_void_p(dwv.data_ptr()), C.c_void_p(dbeta.data_ptr()),
+                                                   _stream(stream)))
+        return dx, dwv, dbeta
 
     def deform_slice(self, x: torch.Tensor, wv: torch.Tensor, beta: float,
                      out: torch.Tensor | None = None, delta: torch.Tensor | None = None,

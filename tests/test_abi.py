@@ -32,7 +32,7 @@ def test_header_declares_the_boundary():
                  "lattice_refine", "lattice_slice", "lattice_deform_slice", "lattice_destroy",
                  "lattice_num_vertices", "lattice_export_keys", "lattice_export_neighbors",
                  "lattice_export_simplices", "lattice_distribute_pointnet", "lattice_splat_backward",
-                 "lattice_slice_backward", "lattice_conv_backward"):
+                 "lattice_slice_backward", "lattice_conv_backward", "lattice_deform_slice_backward"):
         assert need in names
 
 
@@ -78,6 +78,7 @@ def test_host_validation_without_gpu(lib):
     assert lib.lattice_slice_backward(None, None, 0, 8, None, 0, None) == -1
     assert lib.lattice_conv_backward(None, None, None, 0, 8, None, 8, 0, None, 0, None, 0, None, 0, None, None,
                                      None) == -1
+    assert lib.lattice_deform_slice_backward(None, None, 0, 8, None, 0.0, None, 0, None, 0, None, None, None) == -1
 
 
 def test_timing_interface_without_events(lib):

@@ -586,3 +586,39 @@ def test_conv_backward_partial_outputs_and_tiny(L, O):
     gdx, gdw, gdb = g1.conv_backward(g1, _dev(X1[g2o1]), _gpu_w(W1), _dev(dY1[g2o1]))
     P.assert_close(P.rows_in_oracle_order(_host(gdx), g2o1), odx, P.TOL_F32, "tiny dX")
     P.assert_close(np.transpose(_host(gdw), (0, 2, 1)), odw, P.TOL_F32, "tiny dW")
+
+
+def _deform_backward_pair(L, O, gl, ol, g2o, C, seed):
+    rng = np.random.default_rng(seed)
+    X = rng.normal(size=(ol.n, C)).astype(np.float32)
+    wv = (rng.normal(size=C) / np.sqrt(C)).astype(np.float32)
+    beta = 0.15
+    dO = rng.normal(size=(ol.m, C)).astype(np.float32)
+    odx, odw, odb = ol.deform_slice_backward(X.astype(np.float64), wv.astype(np.float64), beta, dO.astype(np.float64))
+    gdx, gdw, gdb = gl.deform_slice_backward(_dev(X[g2o]), _dev(wv), beta, _dev(dO))
+    P.assert_close(P.rows_in_oracle_order(_host(gdx), g2o), odx, P.TOL_F32, f"DeformSlice dX C={C}")
+    P.assert_close(_host(gdw), odw, P.TOL_F32, f"DeformSlice dwv C={C}")
+    P.assert_close(_host(gdb), np.array([odb]), P.TOL_F32, f"DeformSlice dbeta C={C}")
+
+
+@pytest.mark.parametrize("C", [4, 16, 64, 128, 512])
+def test_deform_slice_backward(L, O, C):
+    pos = _cloud(900 + C, 7000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.06)
+    _deform_backward_pair(L, O, gl, ol, g2o, C, C)
+
+
+def test_deform_slice_backward_skewed_tiny_empty(L, O):
+    rng = np.random.default_rng(5)
+    clump = (np.array([0.31, 0.42, 0.53]) + 1e-4 * rng.random((6000, 3))).astype(np.float32)
+    spread = rng.random((3001, 3)).astype(np.float32)
+    pos = np.concatenate([spread[:1500], clump, spread[1500:]]).astype(np.float32)
+    gl, ol, g2o = _pair(L, O, pos, 0.05)
+    _deform_backward_pair(L, O, gl, ol, g2o, 64, 6)
+    for m in (1, 37):
+        gl, ol, g2o = _pair(L, O, _cloud(950 + m, m, 0.5), 0.1)
+        _deform_backward_pair(L, O, gl, ol, g2o, 32, m)
+    ge = L.Lattice.create(torch.zeros((0, 3), device="cuda"), [0.1] * 3)
+    dx, dwv, dbeta = ge.deform_slice_backward(torch.zeros((0, 8), device="cuda"), torch.ones(8, device="cuda"), 0.1,
+                                              torch.zeros((0, 8), device="cuda"))
+    assert dx.shape == (0, 8) and not _host(dwv).any() and _host(dbeta)[0] == 0.0
