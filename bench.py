@@ -23,11 +23,19 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"hbm": 8.0e12, "mfma_f32": 157.3e12, "mfma_bf16": 2.5e15}
-FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "distribute", "conv", "slice", "deform_slice"]
-# kernel symbol fragments of each family (rocprofv3 kernel names)
+FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "distribute", "conv", "slice", "deform_slice",
+            "deform_bwd", "conv_bwd", "splat_bwd", "slice_bwd"]
+# kernel symbol fragments of each family (rocprofv3 kernel names; first match
+# wins).  Backward operators that reuse a forward kernel (the adjoint
+# convolution on k_conv_lds, splat and slice as each other's adjoints, the
+# finishing pass of the DeformSlice gradient gather) are only separable by
+# the event timing, which names the outermost operator.
 FAMILY_KERNELS = {
     "fill": ["k_clear_table"], "insert": ["k_insert_points"], "scan": ["k_scan("],
     "lists": ["k_fill_lists"], "nbr": ["k_neighbor_table", "k_coarse_tables", "k_mask_order"],
+    "deform_bwd": ["k_deform_bwd", "DeformGradRows"],
+    "conv_bwd": ["k_conv_wgrad", "k_wgrad_reduce", "k_relu_mask", "k_adjoint_weights"],
+    "splat_bwd": ["k_scale_by_weight_sum"],
     "splat": ["k_splat_chunks", "k_splat_finish"], "distribute": ["k_dist_"], "conv": ["k_conv"],
     "slice": ["k_slice<"],
     "deform_slice": ["k_deform_slice"],
@@ -141,6 +149,19 @@ def conv_flops(wl, levels):
     return total
 
 
+def conv_bwd_flops(wl, levels):
+    """Nominal flops of the convolution gradients of one step: dX and dW
+    each cost what the forward convolution costs (counted as in
+    conv_flops)."""
+    total = 0
+    for op in wl.ops:
+        if op["op"] == "conv_bwd":
+            cin, cout = op["x"][2], op["y"][2]
+            lv = op["level"] + 1 if op["kind"] == "refine" else op["level"]
+            total += 2 * 2 * levels[lv].n * 9 * cin * cout
+    return total
+
+
 def distribute_flops(wl):
     """Flops of the Distribute + PointNet layers of one step: each of the 4m
     (point, vertex) rows goes through the three 1x1 layers."""
@@ -250,6 +271,7 @@ def main():
         lattice.timing_enable(f, False)
     ns = {lv: levels[lv].n for lv in levels}
     flops = conv_flops(wl, levels)
+    bwd_flops = conv_bwd_flops(wl, levels)
     bytes_by_fam = {f: algorithmic_bytes(wl, levels, f) for f in FAMILIES}
     GpuPipeline.release(levels)
     dominant = max(fam_ms, key=lambda f: fam_ms[f][1])
@@ -270,7 +292,7 @@ def main():
     value = wl.m / (ms_per_step * 1e-3)
     dom_ms_step = dom_ms / args.steps
     dtype = "bf16" if wl.dtype == "bf16" else "f32"
-    mfma_flops = {"conv": flops, "distribute": distribute_flops(wl)}
+    mfma_flops = {"conv": flops, "distribute": distribute_flops(wl), "conv_bwd": bwd_flops}
     if dominant in mfma_flops:
         peak = PEAK["mfma_bf16"] if dtype == "bf16" else PEAK["mfma_f32"]
         achieved = mfma_flops[dominant] / (dom_ms_step * 1e-3)
@@ -310,7 +332,8 @@ def main():
         "config": {"workload": f"config{wl.cfg}:{wl.name}", "points": wl.m,
                    "sigma": float(wl.sigma[0]), "vertices_per_level": [ns[k] for k in sorted(ns)],
                    "conv_gflop_per_step": flops / 1e9,
-                   "distribute_gflop_per_step": mfma_flops["distribute"] / 1e9},
+                   "distribute_gflop_per_step": mfma_flops["distribute"] / 1e9,
+                   "conv_bwd_gflop_per_step": bwd_flops / 1e9},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -297,13 +297,15 @@ class Lattice:
 
     def conv_backward(self, src: "Lattice", x: torch.Tensor | None, W: torch.Tensor | None, dy: torch.Tensor,
                       relu: bool = False, y: torch.Tensor | None = None, want_dx: bool = True,
-                      want_dw: bool = True, want_dbias: bool = True, stream=None):
+                      want_dw: bool = True, want_dbias: bool = True, dx_out: torch.Tensor | None = None,
+                      stream=None):
         """Gradients of the convolution self <- src (1-hop, strided, or
         Upsample when src = self.coarsen()) for dL/dY = dy: (dx, dW, dbias),
         None where not asked for.  W is taps x Cout x Cin."""
         cout = dy.shape[1]
         cin = W.shape[2] if W is not None else x.shape[1]
-        dx = torch.empty((src.n, cin), dtype=torch.float32, device="cuda") if want_dx else None
+        dx = dx_out if dx_out is not None else (
+            torch.empty((src.n, cin), dtype=torch.float32, device="cuda") if want_dx else None)
         dW = torch.empty((9, cout, cin), dtype=torch.float32, device="cuda") if want_dw else None
         db = torch.empty((cout,), dtype=torch.float32, device="cuda") if want_dbias else None
         xp, xld = _rows(x) if x is not None else (None, 0)
@@ -316,11 +318,11 @@ class Lattice:
         return dx, dW, db
 
     def deform_slice_backward(self, x: torch.Tensor, wv: torch.Tensor, beta: float, dout: torch.Tensor,
-                              stream=None):
+                              dx_out: torch.Tensor | None = None, stream=None):
         """Gradients of deform_slice(x, wv, beta) for dL/dout = dout:
         (dx n x C, dwv C, dbeta scalar tensor)."""
         Cc = x.shape[1]
-        dx = torch.empty((self.n, Cc), dtype=torch.float32, device="cuda")
+        dx = dx_out if dx_out is not None else torch.empty((self.n, Cc), dtype=torch.float32, device="cuda")
         dwv = torch.empty((Cc,), dtype=torch.float32, device="cuda")
         dbeta = torch.empty((1,), dtype=torch.float32, device="cuda")
         xp, xld = _rows(x)

@@ -29,6 +29,7 @@ class GpuPipeline:
         self.mlp = {k: (torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32)).cuda(),
                         torch.from_numpy(np.ascontiguousarray(b, dtype=np.float32)).cuda())
                     for k, (W, b) in wl.mlp.items()}
+        self.grads = {k: torch.from_numpy(np.ascontiguousarray(g)).cuda() for k, g in wl.grads.items()}
         self.sigma = [float(s) for s in wl.sigma]
         self._store: dict[str, torch.Tensor] = {}
 
@@ -91,6 +92,25 @@ class GpuPipeline:
                 wv, beta = self.vectors[op["wv"]]
                 outs[op["out"]] = levels[op["level"]].deform_slice(
                     self._view(bufs, levels, op["src"]), wv, beta)
+            elif kind == "deform_slice_bwd":
+                wv, beta = self.vectors[op["wv"]]
+                _, dwv, dbeta = levels[op["level"]].deform_slice_backward(
+                    self._view(bufs, levels, op["x"]), wv, beta, self.grads[op["grad"]],
+                    dx_out=self._view(bufs, levels, op["dst"]))
+                outs[op["out"]], outs["dbeta:" + op["wv"]] = dwv, dbeta
+            elif kind == "conv_bwd":
+                lv = op["level"]
+                dst = levels[lv]
+                src = {"conv": lv, "conv_down": lv - 1, "refine": lv + 1}[op["kind"]]
+                _, dW, db = dst.conv_backward(levels[src], self._view(bufs, levels, op["x"]), self.weights[op["w"]],
+                                              self._view(bufs, levels, op["src"]), relu=op["relu"],
+                                              y=self._view(bufs, levels, op["y"]) if op["relu"] else None,
+                                              dx_out=self._view(bufs, levels, op["dst"]))
+                outs[op["out"]] = dW.transpose(1, 2)          # taps x Cin x Cout, the workload's layout
+                outs["db:" + op["w"]] = db
+            elif kind == "splat_bwd":
+                outs[op["out"]] = levels[0].splat_backward(self._view(bufs, levels, op["src"]),
+                                                           normalize=bool(op["normalize"]))
             else:
                 raise ValueError(f"unknown op {kind}")
         if keep:

@@ -64,6 +64,25 @@ class OraclePipeline:
                 wv, beta = wl.vectors[op["wv"]]
                 outs[op["out"]], _ = levels[op["level"]].deform_slice(
                     np.ascontiguousarray(view_src(op["src"])), wv.astype(np.float64), beta)
+            elif kind == "deform_slice_bwd":
+                wv, beta = wl.vectors[op["wv"]]
+                dx, dwv, dbeta = levels[op["level"]].deform_slice_backward(
+                    np.ascontiguousarray(view_src(op["x"])), wv.astype(np.float64), beta,
+                    wl.grads[op["grad"]].astype(np.float64))
+                write(op["dst"], dx)
+                outs[op["out"]], outs["dbeta:" + op["wv"]] = dwv, np.array([dbeta])
+            elif kind == "conv_bwd":
+                lv = op["level"]
+                src = {"conv": lv, "conv_down": lv - 1, "refine": lv + 1}[op["kind"]]
+                dx, dW, db = levels[lv].conv_backward(
+                    levels[src], np.ascontiguousarray(view_src(op["x"])), wl.weights[op["w"]].astype(np.float64),
+                    np.ascontiguousarray(view_src(op["src"])), relu=op["relu"],
+                    Y=np.ascontiguousarray(view_src(op["y"])) if op["relu"] else None)
+                write(op["dst"], dx)
+                outs[op["out"]], outs["db:" + op["w"]] = dW, db
+            elif kind == "splat_bwd":
+                outs[op["out"]] = levels[0].splat_backward(np.ascontiguousarray(view_src(op["src"])),
+                                                           normalize=bool(op["normalize"]))
             if stop_after is not None and i == stop_after:
                 break
         return levels, bufs, outs

@@ -44,6 +44,7 @@ class Workload:
     weights: dict = field(default_factory=dict)    # name -> float32 array
     vectors: dict = field(default_factory=dict)    # DeformSlice weight vectors
     mlp: dict = field(default_factory=dict)        # name -> (W [out][in], b) of 1x1 layers
+    grads: dict = field(default_factory=dict)      # point output -> dL/d(output), m x C float32
     buffers: dict = field(default_factory=dict)    # name -> (level, channels)
     ops: list = field(default_factory=list)
     levels: int = 1
@@ -215,7 +216,49 @@ def config6(seed: int = 3, m: int = 120_000) -> Workload:
     return _finish(wl)
 
 
-CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5, 6: config6}
+def _backward(wl, loss_out):
+    """Append the backward pass of wl's forward ops for a loss whose gradient
+    with respect to the point output `loss_out` is wl.grads[loss_out]: the
+    ops in reverse order, each turning the gradient of its output buffer
+    into that of its input buffer ("g" + name) and of its parameters."""
+    fwd = list(wl.ops)
+    for name, (lv, total) in list(wl.buffers.items()):
+        wl.buffers["g" + name] = (lv, total)
+    for op in reversed(fwd):
+        kind = op["op"]
+        if kind == "deform_slice" and op["out"] == loss_out:
+            name, c0, cc = op["src"]
+            wl.ops.append(dict(op="deform_slice_bwd", level=op["level"], x=op["src"], wv=op["wv"], grad=loss_out,
+                               dst=("g" + name, c0, cc), out="dwv:" + op["wv"]))
+        elif kind in ("conv", "conv_down", "refine"):
+            (sn, s0, sc), (dn, d0, dc) = op["src"], op["dst"]
+            wl.ops.append(dict(op="conv_bwd", kind=kind, level=op["level"], x=op["src"], y=op["dst"], w=op["w"],
+                               relu=op["relu"], src=("g" + dn, d0, dc), dst=("g" + sn, s0, sc), out="dW:" + op["w"]))
+        elif kind == "splat":
+            name, c0, cc = op["dst"]
+            wl.ops.append(dict(op="splat_bwd", normalize=op["normalize"], src=("g" + name, c0, cc), out="dfeat"))
+        elif kind in ("create", "coarsen"):
+            continue
+        else:
+            raise ValueError(f"no backward for {kind}")
+
+
+def config7(seed: int = 3, m: int = 120_000) -> Workload:
+    """A training step on the LiDAR scan of config 4: its forward network
+    ending in DeformSlice (no plain slice), then the backward pass of every
+    operator for a loss gradient dL/d(DeformSlice output) ~ N(0, 1): dL/dx
+    through DeformSlice, the two Upsamples, the three convolutions and the
+    two strided convolutions down to the splat, dL/dW and dL/dbias of every
+    convolution, dL/dwv and dL/dbeta of DeformSlice and dL/dfeatures."""
+    wl = config4(seed, m)
+    wl.cfg, wl.name = 7, "lidar-train-step"
+    wl.ops = [op for op in wl.ops if op["op"] != "slice"]
+    wl.grads["deform"] = gen.Stream(seed, "loss-grad").normal(wl.m * 64).reshape(wl.m, 64).astype(np.float32)
+    _backward(wl, "deform")
+    return wl
+
+
+CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5, 6: config6, 7: config7}
 
 
 def make(cfg: int, seed: int | None = None, **kw) -> Workload:
