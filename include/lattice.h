@@ -218,11 +218,14 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
  * Splat backward: dF_p = sum_{v in I_p} b_pv dX_v (Eq. (splat) transposed);
  * with normalize != 0 each term is divided by wsum_v = sum_{q in J_v} b_qv
  * (0 where wsum_v = 0), the gradient of the normalised splat.
- *   dX_dev  n x C float32, row stride ld_dX (0 = C).  C a multiple of 4.
- *   dF_dev  m x C float32, row stride C.
+ *   dX_dev    n x C float32, row stride ld_dX (0 = C).  C a multiple of 4.
+ *   wsum_dev  optional n float32: the weight sums the forward lattice_splat
+ *             returned; NULL = summed again over the lists.  Only read when
+ *             normalize != 0.
+ *   dF_dev    m x C float32, row stride C.
  */
-int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int C, int normalize, float* dF_dev,
-                           hipStream_t stream);
+int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int C, int normalize,
+                           const float* wsum_dev, float* dF_dev, hipStream_t stream);
 
 /*
  * Slice backward: dX_v = sum_{p in J_v} b_pv dOut_p (Eq. (slice)
@@ -247,7 +250,7 @@ int lattice_slice_backward(lattice_t L, const float* dOut_dev, int64_t ld_dOut, 
  *             masked dY with W'[t] = W[mirror t]^T over the adjoint table;
  *             must not overlap dY.
  *   dW_dev    9 x Cout x Cin, or NULL: dW[t] = sum_v dY_v^T X[nb(v,t)].
- *   dbias_dev Cout, or NULL: sum_v dY_v.
+ *   dbias_dev Cout (16-byte aligned), or NULL: sum_v dY_v.
  * Row strides of 0 mean dense.  Cin, Cout multiples of 4.  Uses work space
  * from the library's pool; the sums over vertices run in a fixed order.
  */

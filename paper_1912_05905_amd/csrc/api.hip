@@ -801,8 +801,8 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
 
 // ---- backward passes ----
 
-int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int C, int normalize, float* dF_dev,
-                           hipStream_t stream) {
+int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int C, int normalize,
+                           const float* wsum_dev, float* dF_dev, hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
   if (ld_dX == 0) ld_dX = C;
@@ -815,7 +815,8 @@ int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int 
   Scratch scaled;
   if (normalize) {
     if ((st = scaled.get(sizeof(float) * static_cast<size_t>(L->n) * C, stream)) != LAT_OK) return st;
-    launch_scale_by_weight_sum(L->offsets, L->entry_w, L->n, dX_dev, ld_dX, C, scaled.as<float>(), C, stream);
+    launch_scale_by_weight_sum(L->offsets, L->entry_w, wsum_dev, L->n, dX_dev, ld_dX, C, scaled.as<float>(), C,
+                               stream);
     src = scaled.as<float>();
     ld = C;
   }
@@ -891,21 +892,23 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
   if (dW_dev || dbias_dev) {
     if ((st = check_matrix(X_dev, ld_X, Cin, LAT_F32, "X", dW_dev != nullptr && n_in > 0)) != LAT_OK) return st;
     if (dW_dev && !aligned16(dW_dev)) return fail(LAT_EINVAL, "dW must be 16-byte aligned");
+    if (dbias_dev && !aligned16(dbias_dev)) return fail(LAT_EINVAL, "dbias must be 16-byte aligned");
   }
   if (!dX_dev && !dW_dev && !dbias_dev) return LAT_OK;
   ScopedKernelTimer tm("conv_bwd", stream);
   const float* G = dY_dev;
   int64_t ld_G = ld_dY;
   Scratch masked, wt, partials;
-  if (relu && n_out > 0) {
-    if ((st = masked.get(sizeof(float) * static_cast<size_t>(n_out) * Cout, stream)) != LAT_OK) return st;
-    launch_relu_mask(dY_dev, ld_dY, Y_dev, ld_Y, Cout, n_out, masked.as<float>(), Cout, stream);
+  const bool need_mask = relu && n_out > 0, need_wt = dX_dev && n_in > 0;
+  if (need_mask && (st = masked.get(sizeof(float) * static_cast<size_t>(n_out) * Cout, stream)) != LAT_OK) return st;
+  if (need_wt && (st = wt.get(sizeof(float) * 9 * static_cast<size_t>(Cin) * Cout, stream)) != LAT_OK) return st;
+  launch_conv_bwd_prep(dY_dev, ld_dY, Y_dev, ld_Y, n_out, need_mask ? masked.as<float>() : nullptr, Cout, W_dev, Cout,
+                       Cin, need_wt ? wt.as<float>() : nullptr, stream);
+  if (need_mask) {
     G = masked.as<float>();
     ld_G = Cout;
   }
-  if (dX_dev && n_in > 0) {
-    if ((st = wt.get(sizeof(float) * 9 * static_cast<size_t>(Cin) * Cout, stream)) != LAT_OK) return st;
-    launch_adjoint_weights(W_dev, Cout, Cin, wt.as<float>(), stream);
+  if (need_wt) {
     launch_conv(adj, adj_ld, n_in, n_out, G, ld_G, Cout, wt.as<float>(), nullptr, Cin, false, false, dX_dev, ld_dX,
                 adj_rows, stream);
   }

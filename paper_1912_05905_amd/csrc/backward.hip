@@ -25,21 +25,28 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // ---- splat backward with normalisation: rows of dL/dx divided by the
 // vertex weight sums ----
-// One group of 16 lanes per vertex: the lanes sum entry_w over J_v, then
-// scale the vertex's row (0 where the sum is 0, as in the forward).
+// One group of 16 lanes per vertex: the weight sum comes from the forward
+// (wsum) or is summed over J_v by the lanes; the vertex's row is then
+// scaled (0 where the sum is 0, as in the forward).
 constexpr int kScaleLanes = 16;
 
 __global__ void __launch_bounds__(kBlock)
-k_scale_by_weight_sum(const int32_t* __restrict__ offsets, const float* __restrict__ entry_w, int64_t n,
-                      const float* __restrict__ in, int64_t ld_in, int C, float* __restrict__ out, int64_t ld_out) {
+k_scale_by_weight_sum(const int32_t* __restrict__ offsets, const float* __restrict__ entry_w,
+                      const float* __restrict__ wsum, int64_t n, const float* __restrict__ in, int64_t ld_in, int C,
+                      float* __restrict__ out, int64_t ld_out) {
   const int lane = threadIdx.x & (kScaleLanes - 1);
   const int64_t v = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / kScaleLanes;
   if (v >= n) return;   // a whole lane group
-  const int32_t b = offsets[v], e = offsets[v + 1];
   float ws = 0.f;
-  for (int32_t j = b + lane; j < e; j += kScaleLanes) ws += entry_w[j];
+  if (wsum) {
+    ws = wsum[v];
+  } else {
+    const int32_t b = offsets[v], e = offsets[v + 1];
+#pragma unroll 8
+    for (int32_t j = b + lane; j < e; j += kScaleLanes) ws += entry_w[j];
 #pragma unroll
-  for (int o = kScaleLanes / 2; o > 0; o >>= 1) ws += __shfl_xor(ws, o, kScaleLanes);
+    for (int o = kScaleLanes / 2; o > 0; o >>= 1) ws += __shfl_xor(ws, o, kScaleLanes);
+  }
   const float scale = ws > 0.f ? 1.0f / ws : 0.f;
   for (int c = 4 * lane; c < C; c += 4 * kScaleLanes) {
     const float4 x = *reinterpret_cast<const float4*>(in + v * ld_in + c);
@@ -48,30 +55,32 @@ k_scale_by_weight_sum(const int32_t* __restrict__ offsets, const float* __restri
 }
 
 // ---- convolution backward ----
-// G = dY masked by Y > 0 (the forward's ReLU), 4 channels per thread.
-__global__ void __launch_bounds__(kBlock)
-k_relu_mask(const float* __restrict__ dY, int64_t ld_dy, const float* __restrict__ Y, int64_t ld_y, int C,
-            int64_t n, float* __restrict__ G, int64_t ld_g) {
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  const int c4 = C / 4;
-  const int64_t v = q / c4;
-  if (v >= n) return;
-  const int c = 4 * static_cast<int>(q - v * c4);
-  const float4 d = *reinterpret_cast<const float4*>(dY + v * ld_dy + c);
-  const float4 y = *reinterpret_cast<const float4*>(Y + v * ld_y + c);
-  *reinterpret_cast<float4*>(G + v * ld_g + c) =
-      make_float4(y.x > 0.f ? d.x : 0.f, y.y > 0.f ? d.y : 0.f, y.z > 0.f ? d.z : 0.f, y.w > 0.f ? d.w : 0.f);
-}
-
 // Taps 0 = self, 1..4 = +n_j, 5..8 = -n_j: the mirror of a tap negates its
 // offset.
 __device__ inline int mirror_tap(int t) { return t == 0 ? 0 : (t <= 4 ? t + 4 : t - 4); }
 
-// Wt[t][i][o] = W[mirror t][o][i]: the weights of the adjoint convolution
-// (W laid out [tap][Cout][Cin]).
+// The two preparations of the convolution backward in one launch: the first
+// mask_blocks workgroups write G = dY masked by Y > 0 (the forward's ReLU; 4
+// channels per thread), the rest write the adjoint convolution's weights
+// Wt[t][i][o] = W[mirror t][o][i] (W laid out [tap][Cout][Cin]).  Either
+// part may be empty.
 __global__ void __launch_bounds__(kBlock)
-k_adjoint_weights(const float* __restrict__ W, int Cout, int Cin, float* __restrict__ Wt) {
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+k_conv_bwd_prep(const float* __restrict__ dY, int64_t ld_dy, const float* __restrict__ Y, int64_t ld_y, int64_t n,
+                float* __restrict__ G, int64_t ld_g, unsigned mask_blocks, const float* __restrict__ W, int Cout,
+                int Cin, float* __restrict__ Wt) {
+  if (blockIdx.x < mask_blocks) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const int c4 = Cout / 4;
+    const int64_t v = q / c4;
+    if (v >= n) return;
+    const int c = 4 * static_cast<int>(q - v * c4);
+    const float4 d = *reinterpret_cast<const float4*>(dY + v * ld_dy + c);
+    const float4 y = *reinterpret_cast<const float4*>(Y + v * ld_y + c);
+    *reinterpret_cast<float4*>(G + v * ld_g + c) =
+        make_float4(y.x > 0.f ? d.x : 0.f, y.y > 0.f ? d.y : 0.f, y.z > 0.f ? d.z : 0.f, y.w > 0.f ? d.w : 0.f);
+    return;
+  }
+  const int64_t q = static_cast<int64_t>(blockIdx.x - mask_blocks) * kBlock + threadIdx.x;
   const int64_t per = static_cast<int64_t>(Cout) * Cin;
   if (q >= 9 * per) return;
   const int t = static_cast<int>(q / per);
@@ -182,30 +191,46 @@ k_conv_wgrad(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, int64_
   if (do_bias && t < kWgTile && o0 + t < Cout) part_b[chunk * Cout + o0 + t] = bsum;
 }
 
-// dW = sum over chunks of the partials, dbias likewise; fixed order.
+// dW = sum over chunks of the partials, dbias likewise; fixed order.  A
+// thread sums 4 consecutive entries (count and Cout are multiples of 4).
 __global__ void __launch_bounds__(kBlock)
 k_wgrad_reduce(const float* __restrict__ part, const float* __restrict__ part_b, int64_t chunks, int64_t count,
                int Cout, float* __restrict__ dW, float* __restrict__ dbias) {
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int64_t q = 4 * (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x);
+  const float* src;
+  int64_t stride;
+  float* dst;
   if (q < count) {
-    if (!dW) return;
-    float a = 0.f;
-    for (int64_t c = 0; c < chunks; ++c) a += part[c * count + q];
-    dW[q] = a;
-  } else if (q < count + Cout && dbias) {
-    const int64_t o = q - count;
-    float a = 0.f;
-    for (int64_t c = 0; c < chunks; ++c) a += part_b[c * Cout + o];
-    dbias[o] = a;
+    src = part + q;
+    stride = count;
+    dst = dW ? dW + q : nullptr;
+  } else if (q < count + Cout) {
+    src = part_b + (q - count);
+    stride = Cout;
+    dst = dbias ? dbias + (q - count) : nullptr;
+  } else {
+    return;
   }
+  if (!dst) return;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+  for (int64_t c = 0; c < chunks; ++c) {
+    const float4 x = *reinterpret_cast<const float4*>(src + c * stride);
+    a.x += x.x;
+    a.y += x.y;
+    a.z += x.z;
+    a.w += x.w;
+  }
+  *reinterpret_cast<float4*>(dst) = a;
 }
 
 inline unsigned blocks_for(int64_t threads) { return static_cast<unsigned>((threads + kBlock - 1) / kBlock); }
 
-// Vertex chunks of the weight gradient: enough workgroups to fill the chip
-// (about 1536 over taps and tiles), chunks a multiple of the stage.
+// Vertex chunks of the weight gradient: about two workgroups per compute
+// unit over taps and tiles (more chunks would only grow the partials the
+// reduction reads), chunks a multiple of the stage.
 void wgrad_chunks(int64_t n_out, int tiles, int64_t* chunks, int64_t* V) {
-  int64_t want = std::max<int64_t>(1, 1536 / (9 * static_cast<int64_t>(tiles)));
+  int64_t want = std::max<int64_t>(1, 512 / (9 * static_cast<int64_t>(tiles)));
   want = std::min<int64_t>(want, (n_out + kWgStage - 1) / kWgStage);
   int64_t v = (n_out + want - 1) / want;
   v = (v + kWgStage - 1) / kWgStage * kWgStage;
@@ -215,21 +240,19 @@ void wgrad_chunks(int64_t n_out, int tiles, int64_t* chunks, int64_t* V) {
 
 }  // namespace
 
-void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, int64_t n, const float* in,
-                                int64_t ld_in, int C, float* out, int64_t ld_out, hipStream_t s) {
+void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, const float* wsum, int64_t n,
+                                const float* in, int64_t ld_in, int C, float* out, int64_t ld_out, hipStream_t s) {
   if (n <= 0) return;
-  launch(k_scale_by_weight_sum, dim3(blocks_for(n * kScaleLanes)), dim3(kBlock), 0, s, offsets, entry_w, n, in, ld_in,
-         C, out, ld_out);
+  launch(k_scale_by_weight_sum, dim3(blocks_for(n * kScaleLanes)), dim3(kBlock), 0, s, offsets, entry_w, wsum, n, in,
+         ld_in, C, out, ld_out);
 }
 
-void launch_relu_mask(const float* dY, int64_t ld_dy, const float* Y, int64_t ld_y, int C, int64_t n, float* G,
-                      int64_t ld_g, hipStream_t s) {
-  if (n <= 0) return;
-  launch(k_relu_mask, dim3(blocks_for(n * (C / 4))), dim3(kBlock), 0, s, dY, ld_dy, Y, ld_y, C, n, G, ld_g);
-}
-
-void launch_adjoint_weights(const float* W, int Cout, int Cin, float* Wt, hipStream_t s) {
-  launch(k_adjoint_weights, dim3(blocks_for(9LL * Cout * Cin)), dim3(kBlock), 0, s, W, Cout, Cin, Wt);
+void launch_conv_bwd_prep(const float* dY, int64_t ld_dy, const float* Y, int64_t ld_y, int64_t n, float* G,
+                          int64_t ld_g, const float* W, int Cout, int Cin, float* Wt, hipStream_t s) {
+  const unsigned mb = (G && n > 0) ? blocks_for(n * (Cout / 4)) : 0;
+  const unsigned wb = Wt ? blocks_for(9LL * Cout * Cin) : 0;
+  if (mb + wb == 0) return;
+  launch(k_conv_bwd_prep, dim3(mb + wb), dim3(kBlock), 0, s, dY, ld_dy, Y, ld_y, n, G, ld_g, mb, W, Cout, Cin, Wt);
 }
 
 int64_t wgrad_partial_floats(int64_t n_out, int Cout, int Cin) {
@@ -253,7 +276,7 @@ void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const flo
     launch(k_conv_wgrad, dim3(static_cast<unsigned>(chunks), 9, static_cast<unsigned>(tiles_o * tiles_i)),
            dim3(kBlock), 0, s, nbr, ldn, n_out, V, X, ld_x, Cin, G, ld_g, Cout, tiles_i, part, part_b);
   // with no output vertex (chunks = 0) the sums below are zero
-  launch(k_wgrad_reduce, dim3(blocks_for(count + Cout)), dim3(kBlock), 0, s, static_cast<const float*>(part),
+  launch(k_wgrad_reduce, dim3(blocks_for((count + Cout) / 4)), dim3(kBlock), 0, s, static_cast<const float*>(part),
          static_cast<const float*>(part_b), chunks, count, Cout, dW, dbias);
 }
 

@@ -45,7 +45,7 @@ SIGNATURES = {
     "lattice_deform_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _P]),
     "lattice_distribute_pointnet": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _P, _P, _I32, _P, _P, _I32,
                                            _P, _I64, _P]),
-    "lattice_splat_backward": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
+    "lattice_splat_backward": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "lattice_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _I64, _P]),
     "lattice_conv_backward": (_I32, [_P, _P, _P, _I64, _I32, _P, _I32, _I32, _P, _I64, _P, _I64, _P, _I64, _P, _P,
                                      _P]),
@@ -273,15 +273,17 @@ class Lattice:
 
     # ---- backward passes (float32) ----
     def splat_backward(self, dx: torch.Tensor, normalize: bool = True, out: torch.Tensor | None = None,
-                       stream=None) -> torch.Tensor:
+                       wsum: torch.Tensor | None = None, stream=None) -> torch.Tensor:
         """Gradient of splat(feat, normalize) with respect to feat, for
-        dL/dvalues = dx (n x C); returns m x C."""
+        dL/dvalues = dx (n x C); returns m x C.  wsum: the weight sums the
+        forward splat returned (optional)."""
         Cc = dx.shape[1]
         if out is None:
             out = torch.empty((self.m, Cc), dtype=torch.float32, device="cuda")
         xp, xld = _rows(dx)
-        _check(lib().lattice_splat_backward(self._h, xp, xld, Cc, int(bool(normalize)), C.c_void_p(out.data_ptr()),
-                                            _stream(stream)))
+        _check(lib().lattice_splat_backward(self._h, xp, xld, Cc, int(bool(normalize)),
+                                            None if wsum is None else C.c_void_p(wsum.data_ptr()),
+                                            C.c_void_p(out.data_ptr()), _stream(stream)))
         return out
 
     def slice_backward(self, dout: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

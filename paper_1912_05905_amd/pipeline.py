@@ -32,6 +32,7 @@ class GpuPipeline:
         self.grads = {k: torch.from_numpy(np.ascontiguousarray(g)).cuda() for k, g in wl.grads.items()}
         self.sigma = [float(s) for s in wl.sigma]
         self._store: dict[str, torch.Tensor] = {}
+        self._wsum: torch.Tensor | None = None
 
     def _view(self, bufs, levels, spec):
         name, c0, cc = spec
@@ -70,8 +71,11 @@ class GpuPipeline:
             if kind in ("create", "coarsen"):
                 continue
             elif kind == "splat":
+                # the weight sums are kept for a backward pass
+                if self._wsum is None or self._wsum.shape[0] < levels[0].n:
+                    self._wsum = torch.empty(levels[0].n, dtype=torch.float32, device="cuda")
                 levels[0].splat(self.feat, normalize=bool(op["normalize"]),
-                                out=self._view(bufs, levels, op["dst"]))
+                                out=self._view(bufs, levels, op["dst"]), wsum=self._wsum[:levels[0].n])
             elif kind in ("conv", "conv_down", "refine"):
                 lv = op["level"]
                 x = self._view(bufs, levels, op["src"])
@@ -110,7 +114,8 @@ class GpuPipeline:
                 outs["db:" + op["w"]] = db
             elif kind == "splat_bwd":
                 outs[op["out"]] = levels[0].splat_backward(self._view(bufs, levels, op["src"]),
-                                                           normalize=bool(op["normalize"]))
+                                                           normalize=bool(op["normalize"]),
+                                                           wsum=self._wsum[:levels[0].n])
             else:
                 raise ValueError(f"unknown op {kind}")
         if keep:

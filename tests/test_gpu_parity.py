@@ -491,6 +491,12 @@ def test_splat_and_slice_backward(L, O, C, normalize):
     gf = gl.splat_backward(_dev(dX[g2o]), normalize=normalize)
     of = ol.splat_backward(dX.astype(np.float64), normalize=normalize)
     P.assert_close(_host(gf), of, P.TOL_F32, f"splat backward C={C}")
+    if normalize:
+        # with the forward's weight sums instead of a pass over the lists
+        ws = torch.empty(gl.n, device="cuda")
+        gl.splat(_dev(np.zeros((pos.shape[0], 4), np.float32)), wsum=ws)
+        gf = gl.splat_backward(_dev(dX[g2o]), normalize=True, wsum=ws)
+        P.assert_close(_host(gf), of, P.TOL_F32, f"splat backward with wsum C={C}")
     dO = rng.normal(size=(pos.shape[0], C)).astype(np.float32)
     gx = gl.slice_backward(_dev(dO))
     ox = ol.slice_backward(dO.astype(np.float64))
