@@ -47,6 +47,8 @@
 //    unweighted mean over J_v; three 1x1 layers with ReLU before the second
 //    and the third (none on the raw rows), then the per-vertex maximum;
 //    GroupNorm is not part of this operator.
+//  * Group Normalization: statistics over all vertices of the lattice and the
+//    group's channels, biased variance, eps inside the square root.
 //  * Backward passes: gradients of the forward operators above; the ReLU's
 //    derivative is 0 at 0 and DeformSlice's maximum passes its gradient to
 //    the first maximal vertex, maximal among the float32 products b_k x_k.
@@ -702,6 +704,38 @@ int orc_deform_slice_backward(const orc_lattice* L, const double* X, int C, cons
       for (int c = 0; c < C; ++c) dwv[c] += e[k] * (q[k * C + c] - mx[c]);
       *dbeta += e[k];
     }
+  }
+  return OK;
+}
+
+// Group Normalization (Implementation: every convolution is pre-activated
+// by Group Normalization with 32 groups and a ReLU; Wu and He, "Group
+// Normalization", ECCV 2018), over the vertices of one lattice: channel c
+// belongs to group c / (C / groups); each group's mean and (biased)
+// variance are taken over all n rows and its channels; then
+//   Y[v][c] = (X[v][c] - mean_g) / sqrt(var_g + eps) * gamma_c + beta_c,
+// followed by max(., 0) when relu != 0.  gamma / beta null mean 1 / 0.
+int orc_groupnorm(const double* X, int64_t n, int C, int64_t ldx, int groups, const double* gamma,
+                  const double* beta, double eps, int relu, double* Y, int64_t ldy) {
+  if (!X || !Y || n < 0 || C <= 0 || groups <= 0 || C % groups != 0 || !(eps >= 0.0)) return EINVAL_;
+  const int per = C / groups;
+  for (int g = 0; g < groups; ++g) {
+    double mean = 0.0;
+    for (int64_t v = 0; v < n; ++v)
+      for (int c = g * per; c < (g + 1) * per; ++c) mean += X[v * ldx + c];
+    const double cnt = static_cast<double>(n) * per;
+    mean = cnt > 0 ? mean / cnt : 0.0;
+    double var = 0.0;
+    for (int64_t v = 0; v < n; ++v)
+      for (int c = g * per; c < (g + 1) * per; ++c) var += (X[v * ldx + c] - mean) * (X[v * ldx + c] - mean);
+    var = cnt > 0 ? var / cnt : 0.0;
+    const double inv = 1.0 / std::sqrt(var + eps);
+    for (int64_t v = 0; v < n; ++v)
+      for (int c = g * per; c < (g + 1) * per; ++c) {
+        double y = (X[v * ldx + c] - mean) * inv * (gamma ? gamma[c] : 1.0) + (beta ? beta[c] : 0.0);
+        if (relu && y < 0.0) y = 0.0;
+        Y[v * ldy + c] = y;
+      }
   }
   return OK;
 }

@@ -57,6 +57,7 @@ def lib():
             "orc_round_bf16": (None, [p, i64]),
             "orc_distribute_pointnet": (i32, [p, p, p, i32, p, p, i32, p, p, i32, p, p, i32, p]),
             "orc_splat_backward": (i32, [p, p, i32, i32, p]),
+            "orc_groupnorm": (i32, [p, i64, i32, i64, i32, p, p, dbl, i32, p, i64]),
             "orc_slice_backward": (i32, [p, p, i32, p]),
             "orc_conv_backward": (i32, [p, p, p, i32, p, i32, i32, p, p, p, p, p]),
             "orc_deform_slice_backward": (i32, [p, p, i32, p, dbl, p, p, p, p]),
@@ -290,6 +291,18 @@ class Lattice:
         _check(lib().orc_deform_slice(self._h, _ptr(X), Cc, Cc, _ptr(wv), float(beta), _ptr(p), npt,
                                       _ptr(out), _ptr(delta)))
         return out, delta
+
+
+def groupnorm(X, groups, gamma=None, beta=None, eps=1e-5, relu=False):
+    """Group Normalization over the rows of X (n x C), optional ReLU."""
+    X = _f64(X)
+    n, Cc = X.shape
+    g = None if gamma is None else _f64(gamma)
+    b = None if beta is None else _f64(beta)
+    Y = np.zeros_like(X)
+    _check(lib().orc_groupnorm(_ptr(X), n, Cc, Cc, int(groups), _ptr(g), _ptr(b), float(eps), int(bool(relu)),
+                               _ptr(Y), Cc))
+    return Y
 
 
 def slice_raw(X, idx, w):

@@ -587,3 +587,40 @@ def test_deform_slice_backward_finite_differences(oracle_mod):
             D[v, 0] = 1.0
             fd = (loss(X + h * D, wv, beta) - loss(X - h * D, wv, beta)) / (2 * h)
             assert abs(fd - dX[v, 0]) <= 1e-6 * max(1.0, abs(fd)), (p, fd, dX[v, 0])
+
+
+# ----------------------------------------------------------------------------
+# Group Normalization (pre-activation of the convolutions)
+# ----------------------------------------------------------------------------
+def test_groupnorm_worked_cases(oracle_mod):
+    cases = json.load(open(os.path.join(GOLDEN, "groupnorm_cases.json")))["cases"]
+    for c in cases:
+        Y = oracle_mod.groupnorm(np.array(c["X"], np.float64), c["groups"], c.get("gamma"), c.get("beta"),
+                                 c["eps"], c["relu"])
+        assert np.abs(Y - np.array(c["Y"])).max() < 1e-12, c["derivation"]
+
+
+def test_groupnorm_invariants(oracle_mod):
+    """Each group of the normalised output has mean 0 and variance
+    var / (var + eps); the output does not change when a group is scaled by
+    a positive factor and shifted (eps -> 0); gamma and beta act per channel
+    after the normalisation; groups = C normalises every channel alone."""
+    rng = np.random.default_rng(7)
+    X = rng.normal(size=(500, 64)) * rng.uniform(0.5, 3.0, size=64) + rng.normal(size=64) * 4
+    for G in (32, 8, 1, 64):
+        Y = oracle_mod.groupnorm(X, G, eps=1e-5)
+        per = 64 // G
+        for g in range(G):
+            blk, yb = X[:, g * per:(g + 1) * per], Y[:, g * per:(g + 1) * per]
+            assert abs(yb.mean()) < 1e-12
+            v = blk.var()
+            assert abs(yb.var() - v / (v + 1e-5)) < 1e-12
+    Y0 = oracle_mod.groupnorm(X, 32, eps=1e-12)
+    a = np.repeat(rng.uniform(0.2, 5.0, size=32), 2)
+    b = np.repeat(rng.normal(size=32) * 10, 2)
+    assert np.abs(oracle_mod.groupnorm(X * a + b, 32, eps=1e-12) - Y0).max() < 1e-8
+    gam, bet = rng.normal(size=64), rng.normal(size=64)
+    Yab = oracle_mod.groupnorm(X, 32, gam, bet, eps=1e-5)
+    assert np.abs(Yab - (oracle_mod.groupnorm(X, 32, eps=1e-5) * gam + bet)).max() < 1e-12
+    Yr = oracle_mod.groupnorm(X, 32, gam, bet, eps=1e-5, relu=True)
+    assert np.array_equal(Yr, np.maximum(Yab, 0.0))
