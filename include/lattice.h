@@ -165,6 +165,31 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
                    void* out_dev, int64_t ld_out, hipStream_t stream);
 
 /*
+ * Pre-activated convolutions (Implementation: every convolution is
+ * pre-activated by Group Normalization with 32 groups and a ReLU):
+ *   out = conv(relu(GN(in))) for lattice_conv_preact (1-hop or strided, as
+ *   lattice_conv) and lattice_refine_preact (Upsample, as lattice_refine).
+ * GN: channel c of in belongs to group c / (Cin / groups); mean and biased
+ * variance of a group over all rows of the input lattice and its channels
+ * (summed in float64 in a fixed order); each value becomes
+ * (x - mean) / sqrt(var + eps) * gamma_c + beta_c, then max(., 0).  The
+ * normalisation is applied inside the convolution to the gathered values of
+ * neighbours that exist (a missing neighbour still contributes 0); the
+ * normalised input is never stored.
+ *   groups     divides Cin (the paper uses 32); gamma_dev / beta_dev
+ *              optional Cin float32 (NULL = 1 / 0); eps > 0.
+ *   Other arguments as for lattice_conv / lattice_refine.  Cin <= 1024.
+ */
+int lattice_conv_preact(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in, int Cin, int groups,
+                        const float* gamma_dev, const float* beta_dev, float eps, const void* W_dev,
+                        const float* bias_dev, int Cout, lat_dtype dt, int flags, void* out_dev, int64_t ld_out,
+                        hipStream_t stream);
+int lattice_refine_preact(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t ld_in, int Cin, int groups,
+                          const float* gamma_dev, const float* beta_dev, float eps, const void* W_dev,
+                          const float* bias_dev, int Cout, lat_dtype dt, int flags, void* out_dev, int64_t ld_out,
+                          hipStream_t stream);
+
+/*
  * Distribute + PointNet (Proposed Operations, Eq. (distribute); PointNet
  * block of the architecture figure).  For every vertex v the rows
  * r_p = [g_p - mu_v ; f_p], p in J_v, mu_v the mean of g_p over J_v, pass

@@ -27,6 +27,7 @@ SOURCES = {
     "conv.hip": [],
     "distribute.hip": ["-fno-honor-nans"],
     "backward.hip": [],
+    "norm.hip": [],
     "api.hip": [],
 }
 

@@ -526,9 +526,18 @@ bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
   return x < y + bbytes && y < x + abytes;
 }
 
+// Pre-activation of a convolution's input: Group Normalization over the
+// input lattice's vertices, then a ReLU.
+struct GnArgs {
+  int groups;
+  const float* gamma;
+  const float* beta;
+  float eps;
+};
+
 int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                 int Cin, const void* W, const float* bias, int Cout, lat_dtype dt, int flags,
-                void* out, int64_t ld_out, const int32_t* rows, hipStream_t s) {
+                void* out, int64_t ld_out, const int32_t* rows, hipStream_t s, const GnArgs* gn = nullptr) {
   int st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_in == 0) ld_in = Cin;
@@ -543,9 +552,25 @@ int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, 
       overlaps(in, static_cast<size_t>((n_in - 1) * ld_in + Cin) * u, out,
                static_cast<size_t>((n_out - 1) * ld_out + Cout) * u))
     return fail(LAT_EINVAL, "in and out overlap");
+  if (gn) {
+    if (gn->groups <= 0 || Cin % gn->groups != 0) return fail(LAT_EINVAL, "groups must divide Cin");
+    if (!(gn->eps > 0.f) || !std::isfinite(gn->eps)) return fail(LAT_EINVAL, "eps must be positive and finite");
+    if (Cin > conv_max_pre_channels() || Cin > gn_max_channels())
+      return fail(LAT_EUNSUPPORTED, "pre-activated convolutions take at most " +
+                                        std::to_string(std::min(conv_max_pre_channels(), gn_max_channels())) +
+                                        " input channels");
+  }
   if (n_out == 0) return LAT_OK;
+  Scratch pre, work;
+  if (gn) {
+    // the statistics of the input lattice's rows, then the convolution
+    if ((st = pre.get(sizeof(float) * 2 * static_cast<size_t>(Cin), s)) != LAT_OK) return st;
+    if ((st = work.get(static_cast<size_t>(gn_workspace_bytes(n_in, Cin)), s)) != LAT_OK) return st;
+    launch_gn_affine(in, ld_in, Cin, dt == LAT_BF16, n_in, gn->groups, gn->gamma, gn->beta, gn->eps,
+                     pre.as<float>(), work.p, s);
+  }
   launch_conv(table, ldn, n_out, n_in, in, ld_in, Cin, W, bias, Cout, dt == LAT_BF16, flags & LAT_RELU, out,
-              ld_out, rows, s);
+              ld_out, rows, s, gn ? pre.as<float>() : nullptr);
   return check_launch("conv");
 }
 
@@ -737,6 +762,35 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
   if (coarse->parent != fine) return fail(LAT_ELEVEL, "coarse must be lattice_coarsen(fine)");
   return conv_common(coarse->up, fine->nmax, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
                      flags, out_dev, ld_out, coarse->up_rows, stream);
+}
+
+int lattice_conv_preact(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in, int Cin, int groups,
+                        const float* gamma_dev, const float* beta_dev, float eps, const void* W_dev,
+                        const float* bias_dev, int Cout, lat_dtype dt, int flags, void* out_dev, int64_t ld_out,
+                        hipStream_t stream) {
+  int st;
+  if ((st = check_handle(dst)) != LAT_OK) return st;
+  if ((st = check_handle(src)) != LAT_OK) return st;
+  const int32_t* table;
+  if (dst == src) table = dst->nbr;
+  else if (dst->parent == src) table = dst->down;
+  else return fail(LAT_ELEVEL, "dst must be src or lattice_coarsen(src)");
+  const GnArgs gn{groups, gamma_dev, beta_dev, eps};
+  return conv_common(table, dst->nmax, dst->n, src->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt, flags,
+                     out_dev, ld_out, nullptr, stream, &gn);
+}
+
+int lattice_refine_preact(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t ld_in, int Cin, int groups,
+                          const float* gamma_dev, const float* beta_dev, float eps, const void* W_dev,
+                          const float* bias_dev, int Cout, lat_dtype dt, int flags, void* out_dev, int64_t ld_out,
+                          hipStream_t stream) {
+  int st;
+  if ((st = check_handle(fine)) != LAT_OK) return st;
+  if ((st = check_handle(coarse)) != LAT_OK) return st;
+  if (coarse->parent != fine) return fail(LAT_ELEVEL, "coarse must be lattice_coarsen(fine)");
+  const GnArgs gn{groups, gamma_dev, beta_dev, eps};
+  return conv_common(coarse->up, fine->nmax, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
+                     flags, out_dev, ld_out, coarse->up_rows, stream, &gn);
 }
 
 int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* feat_dev, int64_t ld_feat,

@@ -40,6 +40,7 @@ constexpr int kBlock = 64 * kWaves;
 // offset beyond any buffer the kernels build (at most kMaxBufferBytes), for
 // which a buffer load returns zeros without a memory access.
 constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kMaxPreChannels = 1024;   // widest input of a pre-activated convolution
 constexpr int kOutOfRange = static_cast<int>(0x80000000u);
 constexpr int64_t kMaxBufferBytes = (int64_t{1} << 31) - 64;
 
@@ -229,12 +230,17 @@ struct LdsConv {
   static_assert(A_PER_T >= 1 && BM * CPR % kBlock == 0, "A copy split");
 };
 
-template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS, bool BUF, int SCHED>
+// PRE: the pre-activation of the input (Group Normalization folded into a
+// per-channel scale and shift, then a ReLU) is applied to every gathered
+// input value of a neighbour that exists, as the stage is copied to LDS;
+// pre holds Cin scales then Cin shifts.
+template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS, bool BUF, int SCHED, bool PRE>
 __global__ void __launch_bounds__(kBlock)
 k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const void* __restrict__ in,
            int64_t ld_in, int Cin, const void* __restrict__ W, const float* __restrict__ bias, int Cout,
            int relu, void* __restrict__ out, int64_t ld_out, const int32_t* __restrict__ rows,
-           unsigned row_tiles, int splits, float* __restrict__ part, uint32_t in_bytes, uint32_t w_bytes) {
+           unsigned row_tiles, int splits, float* __restrict__ part, uint32_t in_bytes, uint32_t w_bytes,
+           const float* __restrict__ pre) {
   using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
   using E = typename std::conditional<BF16, uint16_t, float>::type;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -243,6 +249,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   int32_t* nbt = reinterpret_cast<int32_t*>(smem + 2 * (P::A_BYTES + P::B_BYTES));
   int32_t* tflag = nbt + kTaps * BM;  // [16] tap used by some row of the tile
   int32_t* tlist = tflag + 16;        // [16] used taps, count in tlist[15]
+  float* pre_s = reinterpret_cast<float*>(smem + P::LDS_BYTES);   // PRE: [Cin] scales, [Cin] shifts
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -266,6 +273,8 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   // zero.  Rows are multiplied independently, so the result of a row does
   // not depend on which other rows share its tile.
   if (tid < 16) tflag[tid] = 0;
+  if constexpr (PRE)
+    for (int i = tid; i < 2 * Cin; i += kBlock) pre_s[i] = pre[i];
   __syncthreads();
   for (int i = tid; i < (te - tb) * BM; i += kBlock) {
     const int t = i / BM, r = i - t * BM;
@@ -333,15 +342,43 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
                           live && q < BN * P::CPR && col < Cout && ch < Cin);
     }
   };
-  auto stash = [&](auto set_c, int buf) {
+  // stage st's copy from its register set to LDS buffer buf
+  auto stash = [&](auto set_c, int buf, int st) {
     constexpr int set = decltype(set_c)::value;
     E* a = As + buf * (BM * P::LDR);
     E* bb = Bs + buf * (BN * P::LDR);
+    int t = 0, kc = 0;
+    if constexpr (PRE) {
+      const int ti = min(st / kc_steps, 15);
+      t = st < stages ? tlist[ti] : 0;
+      kc = (st - ti * kc_steps) * P::KC;
+    }
 #pragma unroll
     for (int j = 0; j < P::A_PER_T; ++j) {
       const int q = tid + j * kBlock;
       const int r = q / P::CPR, cc = q % P::CPR;
-      *reinterpret_cast<V*>(a + r * P::LDR + cc * P::EPC) = ra[set][j];
+      V v = ra[set][j];
+      if constexpr (PRE) {
+        const int ch = kc + cc * P::EPC;
+        if (st < stages && nbt[t * BM + r] >= 0 && ch < Cin) {
+          uint32_t w[4] = {v.x, v.y, v.z, v.w};
+          if constexpr (BF16) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float lo = fmaxf(fmaf(__uint_as_float(w[i] << 16), pre_s[ch + 2 * i], pre_s[Cin + ch + 2 * i]), 0.f);
+              const float hi = fmaxf(fmaf(__uint_as_float(w[i] & 0xffff0000u), pre_s[ch + 2 * i + 1],
+                                          pre_s[Cin + ch + 2 * i + 1]), 0.f);
+              w[i] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              w[i] = __float_as_uint(fmaxf(fmaf(__uint_as_float(w[i]), pre_s[ch + i], pre_s[Cin + ch + i]), 0.f));
+          }
+          v = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+      }
+      *reinterpret_cast<V*>(a + r * P::LDR + cc * P::EPC) = v;
     }
 #pragma unroll
     for (int j = 0; j < P::B_PER_T; ++j) {
@@ -366,7 +403,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   // a load has NS-1 steps to arrive.  Set indices are compile-time constants
   // so that the register sets stay in registers.
   static_for<NS>([&](auto i_c) { fetch(i_c, decltype(i_c)::value); });
-  stash(std::integral_constant<int, 0>{}, 0);
+  stash(std::integral_constant<int, 0>{}, 0, 0);
   __syncthreads();
   // One pipeline step: stage st is multiplied from LDS buffer st & 1; stage
   // st+1 goes from its register set to the other buffer and stage st+NS is
@@ -378,7 +415,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
     constexpr int NEXT = (SET + 1) % NS;
     const int buf = st & 1;
     if constexpr (SCHED == 1) {
-      stash(std::integral_constant<int, NEXT>{}, buf ^ 1);
+      stash(std::integral_constant<int, NEXT>{}, buf ^ 1, st + 1);
       fetch(set_c, st + NS);
     }
     const E* a = As + buf * (BM * P::LDR) + (wm * P::RM * 16 + li) * P::LDR + lg * P::EPL;
@@ -412,7 +449,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
     }
     if constexpr (SCHED == 0) {
       // unconditional: past the last stage these copy and load zeros
-      stash(std::integral_constant<int, NEXT>{}, buf ^ 1);
+      stash(std::integral_constant<int, NEXT>{}, buf ^ 1, st + 1);
       fetch(set_c, st + NS);
     }
     __syncthreads();
@@ -502,26 +539,29 @@ struct ConvExtent {
   bool buffer_ok() const { return in_bytes <= kMaxBufferBytes && w_bytes <= kMaxBufferBytes; }
 };
 
-template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS = 2, bool BUF = true, int SCHED = 0>
+template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS = 2, bool BUF = true, int SCHED = 0,
+          bool PRE = false>
 void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                      int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
-                     int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s, int splits = 1,
-                     float* part = nullptr) {
+                     int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s, const float* pre = nullptr,
+                     int splits = 1, float* part = nullptr) {
   using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
   if (rows) splits = 1;  // partial sums are kept in permuted row order
+  const int lds = P::LDS_BYTES + (PRE ? 8 * Cin : 0);
   static bool lds_limit_set = false;
   if (!lds_limit_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, P::LDS_BYTES);
+    (void)hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED, PRE>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, P::LDS_BYTES + (PRE ? 8 * kMaxPreChannels : 0));
     lds_limit_set = true;
   }
   const int64_t tiles = (n_out + BM - 1) / BM;
   const unsigned per_xcd = static_cast<unsigned>((tiles + 7) / 8);
   const dim3 grid(per_xcd * 8, static_cast<unsigned>((Cout + BN - 1) / BN), static_cast<unsigned>(splits));
-  launch((k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED>), grid, dim3(kBlock), P::LDS_BYTES, s, nbr,
-                     ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows,
-                     static_cast<unsigned>(tiles), splits, splits > 1 ? part : nullptr,
-                     static_cast<uint32_t>(BUF ? ext.in_bytes : 0), static_cast<uint32_t>(BUF ? ext.w_bytes : 0));
+  launch((k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED, PRE>), grid, dim3(kBlock), static_cast<uint32_t>(lds),
+         s, nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, static_cast<unsigned>(tiles),
+         splits, splits > 1 ? part : nullptr, static_cast<uint32_t>(BUF ? ext.in_bytes : 0),
+         static_cast<uint32_t>(BUF ? ext.w_bytes : 0), pre);
   if (splits > 1) {
     const int64_t quads = n_out * (Cout / 4);
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((quads + kBlock - 1) / kBlock, 8192));
@@ -540,52 +580,62 @@ int64_t blocks_of(int64_t n_out, int Cout, int rows, int cols) {
 // stage costs several times its MFMA time.  bf16: 128 x 128 tiles halve the
 // gathered bytes per flop and win once there are enough of them (wide
 // layers, large levels); 64 x 64 otherwise.
-template <bool BF16>
+// PRE (the pre-activated convolution) uses the same tiles, apart from the
+// register kernel for narrow outputs, which has no pre-activation.
+template <bool BF16, bool PRE>
 void conv_dispatch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                    int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
-                   int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s) {
-  if (Cout <= 16)
+                   int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s, const float* pre) {
+  if (!PRE && Cout <= 16)
     return conv_launch<BF16, 1, 1, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, s);
   if (!ext.buffer_ok())  // operands beyond the reach of a buffer resource
-    return conv_lds_launch<BF16, 64, 64, 2, 2, 128, 2, false>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu,
-                                                               out, ld_out, rows, ext, s);
+    return conv_lds_launch<BF16, 64, 64, 2, 2, 128, 2, false, 0, PRE>(
+        nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
   if constexpr (BF16) {
     const int64_t b128 = blocks_of(n_out, Cout, 128, 128);
     const int64_t b64 = blocks_of(n_out, Cout, 64, 64);
     if (Cout >= 128 && (b128 >= 1500 || (Cin >= 256 && Cout % 128 == 0)))
-      return conv_lds_launch<true, 128, 128, 2, 2, 64, 3, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
-                                                                   relu, out, ld_out, rows, ext, s);
+      return conv_lds_launch<true, 128, 128, 2, 2, 64, 3, true, 1, PRE>(
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
     if (Cout > 32 && b64 >= 8192)
-      return conv_lds_launch<true, 64, 64, 2, 2, 128, 3, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
-                                                                  relu, out, ld_out, rows, ext, s);
+      return conv_lds_launch<true, 64, 64, 2, 2, 128, 3, true, 1, PRE>(
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
     if (Cout > 32 && b64 >= 256)
-      return conv_lds_launch<true, 64, 64, 2, 2, 128, 2, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
-                                                                  relu, out, ld_out, rows, ext, s);
-    return conv_lds_launch<true, 32, 32, 2, 2, 128>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out,
-                                                    ld_out, rows, ext, s);
+      return conv_lds_launch<true, 64, 64, 2, 2, 128, 2, true, 1, PRE>(
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+    return conv_lds_launch<true, 32, 32, 2, 2, 128, 2, true, 0, PRE>(
+        nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
   } else {
     if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= 2048)
-      return conv_lds_launch<false, 64, 64, 2, 2, 128, 3, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
-                                                                   relu, out, ld_out, rows, ext, s);
+      return conv_lds_launch<false, 64, 64, 2, 2, 128, 3, true, 1, PRE>(
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
     if (Cout > 64 && blocks_of(n_out, Cout, 32, 64) >= 1024)
-      return conv_lds_launch<false, 32, 64, 2, 2, 128, 3, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
-                                                                   relu, out, ld_out, rows, ext, s);
-    return conv_lds_launch<false, 32, 32, 2, 2, 256, 2, true, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
-                                                                 relu, out, ld_out, rows, ext, s);
+      return conv_lds_launch<false, 32, 64, 2, 2, 128, 3, true, 1, PRE>(
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+    return conv_lds_launch<false, 32, 32, 2, 2, 256, 2, true, 1, PRE>(
+        nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
   }
 }
 
 }  // namespace
 
+int conv_max_pre_channels() { return kMaxPreChannels; }
+
 void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
-                 int64_t ld_out, const int32_t* rows, hipStream_t s) {
+                 int64_t ld_out, const int32_t* rows, hipStream_t s, const float* pre) {
   if (n_out <= 0) return;
   ScopedKernelTimer tm("conv", s);
   const int64_t u = bf16 ? 2 : 4;
   const ConvExtent ext{n_in > 0 ? ((n_in - 1) * ld_in + Cin) * u : 0, int64_t{kTaps} * Cout * Cin * u};
-  if (bf16) conv_dispatch<true>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s);
-  else conv_dispatch<false>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s);
+  auto go = [&](auto bf_c, auto pre_c) {
+    conv_dispatch<decltype(bf_c)::value, decltype(pre_c)::value>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
+                                                                  relu, out, ld_out, rows, ext, s, pre);
+  };
+  using T = std::true_type;
+  using F = std::false_type;
+  if (pre) bf16 ? go(T{}, T{}) : go(F{}, T{});
+  else bf16 ? go(T{}, F{}) : go(F{}, F{});
 }
 
 }  // namespace lat

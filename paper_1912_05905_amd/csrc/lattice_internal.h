@@ -179,8 +179,16 @@ void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const flo
                        const float* G, int64_t ld_g, int Cout, float* dW, float* dbias, float* partials,
                        hipStream_t s);
 // conv.hip
+// pre: optional Cin scales then Cin shifts of the pre-activation (applied,
+// with a ReLU, to the gathered input values of existing neighbours)
 void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
-                 int64_t ld_out, const int32_t* rows, hipStream_t s);
+                 int64_t ld_out, const int32_t* rows, hipStream_t s, const float* pre = nullptr);
+int conv_max_pre_channels();
+// norm.hip
+int gn_max_channels();
+int64_t gn_workspace_bytes(int64_t n, int C);
+void launch_gn_affine(const void* x, int64_t ld, int C, int bf16, int64_t n, int groups, const float* gamma,
+                      const float* beta, float eps, float* pre, void* work, hipStream_t s);
 
 }  // namespace lat

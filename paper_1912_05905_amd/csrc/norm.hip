@@ -1,0 +1,134 @@
+// Group Normalization statistics for the pre-activated convolutions
+// (Implementation: every convolution is pre-activated by Group Normalization
+// with 32 groups and a ReLU).  Over the n vertices of a lattice and the
+// channels of each group: mean and biased variance, summed in fp64 in a fixed
+// order (per-workgroup partials, then one pass over the partials).  The
+// result is the per-channel affine map the convolution applies to every
+// gathered input value before its ReLU:
+//   scale_c = gamma_c / sqrt(var_g + eps),  shift_c = beta_c - mean_g scale_c.
+#include <algorithm>
+
+#include "lattice_internal.h"
+
+namespace lat {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kGnMaxParts = 512;
+
+// Workgroup w sums rows [w * rows_per, (w + 1) * rows_per): thread t takes
+// channels 4 (t % quads) .. + 3 of rows t / quads, t / quads + slots, ...
+template <bool BF16>
+__global__ void __launch_bounds__(kBlock)
+k_gn_partial(const void* __restrict__ x, int64_t ld, int C, int64_t n, int64_t rows_per,
+             double* __restrict__ part) {
+  __shared__ double sh[2][kBlock][4];
+  const int t = threadIdx.x;
+  const int quads = C / 4;
+  const int slots = kBlock / quads;
+  const int q = t % quads, slot = t / quads;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per;
+  const int64_t r1 = min(r0 + rows_per, n);
+  double s[4] = {0.0, 0.0, 0.0, 0.0}, ss[4] = {0.0, 0.0, 0.0, 0.0};
+  if (slot < slots) {
+    for (int64_t v = r0 + slot; v < r1; v += slots) {
+      float f[4];
+      if constexpr (BF16) {
+        const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(x) + v * ld + 4 * q);
+        f[0] = __uint_as_float(u.x << 16);
+        f[1] = __uint_as_float(u.x & 0xffff0000u);
+        f[2] = __uint_as_float(u.y << 16);
+        f[3] = __uint_as_float(u.y & 0xffff0000u);
+      } else {
+        const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(x) + v * ld + 4 * q);
+        f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        s[i] += f[i];
+        ss[i] += static_cast<double>(f[i]) * f[i];
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    sh[0][t][i] = s[i];
+    sh[1][t][i] = ss[i];
+  }
+  __syncthreads();
+  // thread q < quads: its 4 channels summed over the slots in order
+  if (t < quads) {
+    double a[4] = {0.0, 0.0, 0.0, 0.0}, b[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int sl = 0; sl < slots; ++sl)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] += sh[0][sl * quads + t][i];
+        b[i] += sh[1][sl * quads + t][i];
+      }
+    double* p = part + static_cast<int64_t>(blockIdx.x) * 2 * C;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      p[4 * t + i] = a[i];
+      p[C + 4 * t + i] = b[i];
+    }
+  }
+}
+
+// One thread per group: the partials in workgroup order, then the group's
+// channels; writes scale (pre[0..C)) and shift (pre[C..2C)).
+__global__ void __launch_bounds__(kBlock)
+k_gn_finalize(const double* __restrict__ part, int nparts, int C, int groups, int64_t n,
+              const float* __restrict__ gamma, const float* __restrict__ beta, float eps, float* __restrict__ pre) {
+  const int g = static_cast<int>(blockIdx.x) * kBlock + threadIdx.x;
+  if (g >= groups) return;
+  const int per = C / groups;
+  double s = 0.0, ss = 0.0;
+  for (int w = 0; w < nparts; ++w)
+    for (int c = g * per; c < (g + 1) * per; ++c) {
+      s += part[static_cast<int64_t>(w) * 2 * C + c];
+      ss += part[static_cast<int64_t>(w) * 2 * C + C + c];
+    }
+  const double cnt = static_cast<double>(n) * per;
+  const double mean = cnt > 0 ? s / cnt : 0.0;
+  const double var = cnt > 0 ? max(ss / cnt - mean * mean, 0.0) : 0.0;
+  const double inv = 1.0 / sqrt(var + static_cast<double>(eps));
+  for (int c = g * per; c < (g + 1) * per; ++c) {
+    const double sc = (gamma ? gamma[c] : 1.0) * inv;
+    pre[c] = static_cast<float>(sc);
+    pre[C + c] = static_cast<float>((beta ? beta[c] : 0.0) - mean * sc);
+  }
+}
+
+void gn_parts(int64_t n, int C, int64_t* nparts, int64_t* rows_per) {
+  const int slots = kBlock / (C / 4);
+  int64_t rp = std::max<int64_t>(slots, (n + kGnMaxParts - 1) / kGnMaxParts);
+  rp = (rp + slots - 1) / slots * slots;
+  *rows_per = rp;
+  *nparts = std::max<int64_t>(1, (n + rp - 1) / rp);
+}
+
+}  // namespace
+
+int gn_max_channels() { return 4 * kBlock; }
+
+int64_t gn_workspace_bytes(int64_t n, int C) {
+  int64_t np, rp;
+  gn_parts(n, C, &np, &rp);
+  return np * 2 * C * static_cast<int64_t>(sizeof(double));
+}
+
+void launch_gn_affine(const void* x, int64_t ld, int C, int bf16, int64_t n, int groups, const float* gamma,
+                      const float* beta, float eps, float* pre, void* work, hipStream_t s) {
+  ScopedKernelTimer tm("groupnorm", s);
+  int64_t np, rp;
+  gn_parts(n, C, &np, &rp);
+  double* part = static_cast<double*>(work);
+  if (n > 0) {
+    if (bf16) launch(k_gn_partial<true>, dim3(static_cast<unsigned>(np)), dim3(kBlock), 0, s, x, ld, C, n, rp, part);
+    else launch(k_gn_partial<false>, dim3(static_cast<unsigned>(np)), dim3(kBlock), 0, s, x, ld, C, n, rp, part);
+  }
+  launch(k_gn_finalize, dim3(static_cast<unsigned>((groups + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
+         static_cast<const double*>(part), n > 0 ? static_cast<int>(np) : 0, C, groups, n, gamma, beta, eps, pre);
+}
+
+}  // namespace lat

@@ -43,6 +43,10 @@ SIGNATURES = {
     "lattice_refine": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _I32, _I32, _P, _I64, _P]),
     "lattice_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
     "lattice_deform_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _P]),
+    "lattice_conv_preact": (_I32, [_P, _P, _P, _I64, _I32, _I32, _P, _P, _F32, _P, _P, _I32, _I32, _I32, _P, _I64,
+                                   _P]),
+    "lattice_refine_preact": (_I32, [_P, _P, _P, _I64, _I32, _I32, _P, _P, _F32, _P, _P, _I32, _I32, _I32, _P,
+                                     _I64, _P]),
     "lattice_distribute_pointnet": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _P, _P, _I32, _P, _P, _I32,
                                            _P, _I64, _P]),
     "lattice_splat_backward": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P, _P]),
@@ -239,6 +243,25 @@ class Lattice:
         _check(lib().lattice_refine(self._h, coarse._h, xp, xld, cin, C.c_void_p(W.data_ptr()),
                                     None if bias is None else C.c_void_p(bias.data_ptr()), cout,
                                     _dtype_code(x), LAT_RELU if relu else 0, op, old, _stream(stream)))
+        return out
+
+    def conv_preact(self, src: "Lattice", x: torch.Tensor, W: torch.Tensor, groups: int = 32,
+                    gamma: torch.Tensor | None = None, beta: torch.Tensor | None = None, eps: float = 1e-5,
+                    bias: torch.Tensor | None = None, relu: bool = False, out: torch.Tensor | None = None,
+                    refine: bool = False, stream=None) -> torch.Tensor:
+        """conv(relu(GroupNorm(x))): self is the destination; src as for conv
+        (refine=False) or the coarse lattice of an Upsample (refine=True)."""
+        cout, cin = W.shape[1], W.shape[2]
+        if out is None:
+            out = torch.empty((self.n, cout), dtype=x.dtype, device="cuda")
+        xp, xld = _rows(x)
+        op, old = _rows(out)
+        if not W.is_contiguous() or W.dtype != x.dtype:
+            raise ValueError("W must be contiguous with the dtype of x")
+        ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
+        fn = lib().lattice_refine_preact if refine else lib().lattice_conv_preact
+        _check(fn(self._h, src._h, xp, xld, cin, int(groups), ptr(gamma), ptr(beta), float(eps), ptr(W), ptr(bias),
+                  cout, _dtype_code(x), LAT_RELU if relu else 0, op, old, _stream(stream)))
         return out
 
     def slice(self, x: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

@@ -698,3 +698,56 @@ def test_train_step_full_size(L, O):
             of = olv[0].splat_backward(G.astype(np.float64), normalize=bool(op["normalize"]))
             P.assert_close(_host(gf), of, P.TOL_F32, "replay splat backward")
     GpuPipeline.release(levels)
+
+
+# ----------------------------------------------------------------------------
+# pre-activated convolutions: conv(relu(GroupNorm(x)))
+# ----------------------------------------------------------------------------
+def _preact_case(L, O, gd, gs, od, os_, g2o_d, g2o_s, form, cin, cout, groups, seed, dtype="f32", affine=True,
+                 offset=0.0):
+    rng = np.random.default_rng(seed)
+    bf = dtype == "bf16"
+    tdt = torch.bfloat16 if bf else torch.float32
+    rnd = O.round_bf16 if bf else (lambda a: np.asarray(a, np.float64))
+    X = rnd(offset + rng.normal(size=(os_.n, cin)) * rng.uniform(0.5, 2.0, size=cin))
+    W = rnd(_rand_w(rng, cin, cout, 1.0 / np.sqrt(9 * cin)))
+    gam = rng.uniform(0.5, 1.5, size=cin).astype(np.float32) if affine else None
+    bet = (0.2 * rng.normal(size=cin)).astype(np.float32) if affine else None
+    b = rng.normal(size=cout).astype(np.float32)
+    A = O.groupnorm(X, groups, gam, bet, eps=1e-5, relu=True)
+    if bf:
+        A = O.round_bf16(A)
+    if form == "upsample":
+        oy = od.refine_into(os_, A, W, bias=b.astype(np.float64))
+    else:
+        oy = od.conv(os_, A, W, bias=b.astype(np.float64))
+    gy = gd.conv_preact(gs, _dev(X[g2o_s].astype(np.float32), tdt), _gpu_w(W.astype(np.float32), tdt), groups=groups,
+                        gamma=None if gam is None else _dev(gam), beta=None if bet is None else _dev(bet), eps=1e-5,
+                        bias=_dev(b), refine=form == "upsample")
+    tol = P.TOL_BF16 if bf else P.TOL_F32
+    P.assert_close(P.rows_in_oracle_order(_host(gy), g2o_d), rnd(oy), tol,
+                   f"preact {form} {cin}->{cout} G={groups} {dtype}", depth=2 if bf else 1)
+
+
+@pytest.mark.parametrize("cin,cout,groups", [(64, 64, 32), (12, 20, 4), (128, 128, 32), (32, 96, 1), (64, 16, 64),
+                                             (256, 64, 32)])
+def test_conv_preact_same_level(L, O, cin, cout, groups):
+    pos = _cloud(1000 + cin, 6000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.07)
+    _preact_case(L, O, gl, gl, ol, ol, g2o, g2o, "same", cin, cout, groups, cin + cout)
+    _preact_case(L, O, gl, gl, ol, ol, g2o, g2o, "same", cin, cout, groups, cin + cout + 1, affine=False,
+                 offset=300.0)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_conv_preact_across_levels(L, O, dtype):
+    pos = _cloud(1100, 8000, 0.8)
+    gl = L.Lattice.create(_dev(pos), [0.05] * 3)
+    ol = O.Lattice.create(pos, np.full(3, 0.05, np.float32))
+    gc, oc = gl.coarsen(), ol.coarsen()
+    g2o_f = P.key_permutation(_host(gl.keys()), ol.keys())
+    g2o_c = P.key_permutation(_host(gc.keys()), oc.keys())
+    _preact_case(L, O, gc, gl, oc, ol, g2o_c, g2o_f, "strided", 64, 128, 32, 5, dtype)
+    _preact_case(L, O, gl, gc, ol, oc, g2o_f, g2o_c, "upsample", 128, 64, 32, 6, dtype)
+    if dtype == "bf16":
+        _preact_case(L, O, gl, gl, ol, ol, g2o_f, g2o_f, "same", 64, 64, 32, 7, dtype)
