@@ -488,6 +488,23 @@ void orc_deform_slice_raw(const double* X, int64_t ldx, int C, const int64_t* id
   }
 }
 
+// DeformSlice fused with the last linear classification layer
+// (Implementation): logits_p = Wc f_p + bc with f_p the DeformSlice output
+// of point p, Wc laid out [class][channel] (K x C), bc optional.
+int orc_deform_slice_classify(const orc_lattice* L, const double* X, int64_t ldx, int C, const double* wv,
+                              double beta, const double* Wc, const double* bc, int K, double* logits) {
+  if (!L || !X || !wv || !Wc || !logits || C <= 0 || K <= 0) return EINVAL_;
+  std::vector<double> f(static_cast<size_t>(L->m) * C);
+  orc_deform_slice_raw(X, ldx, C, L->idx.data(), L->bary.data(), L->m, wv, beta, nullptr, f.data(), nullptr);
+  for (int64_t p = 0; p < L->m; ++p)
+    for (int j = 0; j < K; ++j) {
+      double a = bc ? bc[j] : 0.0;
+      for (int c = 0; c < C; ++c) a += Wc[static_cast<int64_t>(j) * C + c] * f[p * C + c];
+      logits[p * K + j] = a;
+    }
+  return OK;
+}
+
 int orc_slice(const orc_lattice* L, const double* X, int64_t ldx, int C,
               const int64_t* pts, int64_t npts, double* out) {
   if (!L || !X || !out || C <= 0) return EINVAL_;

@@ -58,6 +58,7 @@ def lib():
             "orc_distribute_pointnet": (i32, [p, p, p, i32, p, p, i32, p, p, i32, p, p, i32, p]),
             "orc_splat_backward": (i32, [p, p, i32, i32, p]),
             "orc_groupnorm": (i32, [p, i64, i32, i64, i32, p, p, dbl, i32, p, i64]),
+            "orc_deform_slice_classify": (i32, [p, p, i64, i32, p, dbl, p, p, i32, p]),
             "orc_slice_backward": (i32, [p, p, i32, p]),
             "orc_conv_backward": (i32, [p, p, p, i32, p, i32, i32, p, p, p, p, p]),
             "orc_deform_slice_backward": (i32, [p, p, i32, p, dbl, p, p, p, p]),
@@ -279,6 +280,18 @@ class Lattice:
         npt = self.m if p is None else p.shape[0]
         out = np.zeros((npt, Cc), np.float64)
         _check(lib().orc_slice(self._h, _ptr(X), Cc, Cc, _ptr(p), npt, _ptr(out)))
+        return out
+
+    def deform_slice_classify(self, X, wv, beta, Wc, bc=None):
+        """DeformSlice fused with a linear classifier: m x K logits,
+        Wc [class][channel]."""
+        X, wv, Wc = _f64(X), _f64(wv), _f64(Wc)
+        Cc, K = X.shape[1], Wc.shape[0]
+        assert Wc.shape[1] == Cc
+        b = None if bc is None else _f64(bc)
+        out = np.zeros((self.m, K), np.float64)
+        _check(lib().orc_deform_slice_classify(self._h, _ptr(X), Cc, Cc, _ptr(wv), float(beta), _ptr(Wc), _ptr(b), K,
+                                               _ptr(out)))
         return out
 
     def deform_slice(self, X, wv, beta, pts=None):

@@ -624,3 +624,26 @@ def test_groupnorm_invariants(oracle_mod):
     assert np.abs(Yab - (oracle_mod.groupnorm(X, 32, eps=1e-5) * gam + bet)).max() < 1e-12
     Yr = oracle_mod.groupnorm(X, 32, gam, bet, eps=1e-5, relu=True)
     assert np.array_equal(Yr, np.maximum(Yab, 0.0))
+
+
+def test_deform_slice_classify_special_cases(oracle_mod):
+    """The fused classifier reduces to DeformSlice with Wc = I and no bias,
+    picks channel c with the one-hot row e_c, returns the bias with Wc = 0,
+    and is linear in Wc."""
+    L = oracle_mod.Lattice.create(_tiny_cloud(61, 300), np.full(3, 0.1, np.float32))
+    rng = np.random.default_rng(61)
+    C = 12
+    X = rng.normal(size=(L.n, C))
+    wv = rng.normal(size=C) * 0.3
+    ds, _ = L.deform_slice(X, wv, 0.2)
+    assert np.abs(L.deform_slice_classify(X, wv, 0.2, np.eye(C)) - ds).max() < 1e-12
+    for c in (0, 5, C - 1):
+        e = np.zeros((1, C))
+        e[0, c] = 1.0
+        assert np.abs(L.deform_slice_classify(X, wv, 0.2, e)[:, 0] - ds[:, c]).max() < 1e-12
+    bc = rng.normal(size=7)
+    assert np.abs(L.deform_slice_classify(X, wv, 0.2, np.zeros((7, C)), bc) - bc).max() == 0
+    W1, W2 = rng.normal(size=(7, C)), rng.normal(size=(7, C))
+    lhs = L.deform_slice_classify(X, wv, 0.2, W1 + W2)
+    rhs = L.deform_slice_classify(X, wv, 0.2, W1) + L.deform_slice_classify(X, wv, 0.2, W2)
+    assert np.abs(lhs - rhs).max() < 1e-12
