@@ -232,6 +232,20 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
                          hipStream_t stream);
 
 /*
+ * DeformSlice fused with the last linear classification layer
+ * (Implementation: fused to avoid storing the high-dimensional per-point
+ * features): logits_p = Wc f_p + bc, f_p the DeformSlice output of point p
+ * (as lattice_deform_slice, which this does not store).
+ *   Wc_dev     K x C float32 [class][channel], 16-byte aligned;
+ *   bc_dev     optional K float32;  1 <= K <= 64, K x C <= 16384.
+ *   logits_dev m x K float32, row stride K.
+ * Other arguments as for lattice_deform_slice.
+ */
+int lattice_deform_slice_classify(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
+                                  const float* wv_dev, float beta, const float* Wc_dev, const float* bc_dev, int K,
+                                  float* logits_dev, hipStream_t stream);
+
+/*
  * Backward passes (Implementation: the lattice operators have forward and
  * backward passes on the GPU).  Each returns the gradient of a scalar loss
  * with respect to the forward's inputs, given its gradient with respect to

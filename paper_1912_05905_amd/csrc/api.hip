@@ -853,6 +853,28 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
   return check_launch("deform slice");
 }
 
+int lattice_deform_slice_classify(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
+                                  const float* wv_dev, float beta, const float* Wc_dev, const float* bc_dev, int K,
+                                  float* logits_dev, hipStream_t stream) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = check_dtype(dt)) != LAT_OK) return st;
+  if (ld_vals == 0) ld_vals = C;
+  if ((st = check_matrix(vals_dev, ld_vals, C, dt, "vals", L->n > 0)) != LAT_OK) return st;
+  if (!wv_dev || !Wc_dev) return fail(LAT_EINVAL, "wv and Wc must not be null");
+  if (L->m > 0 && !logits_dev) return fail(LAT_EINVAL, "logits is null");
+  if (!std::isfinite(beta)) return fail(LAT_EINVAL, "beta must be finite");
+  if (K <= 0 || K > deform_classify_max_classes())
+    return fail(LAT_EUNSUPPORTED, "K must be in [1, " + std::to_string(deform_classify_max_classes()) + "]");
+  if (C > deform_max_channels(dt == LAT_BF16) || static_cast<int64_t>(K) * C > deform_classify_max_weights())
+    return fail(LAT_EUNSUPPORTED, "the classifier takes at most " + std::to_string(deform_classify_max_weights()) +
+                                      " weights (K x C) and DeformSlice's channel limit");
+  if (!aligned16(Wc_dev)) return fail(LAT_EINVAL, "Wc must be 16-byte aligned");
+  launch_deform_classify(L->idx, L->w, L->m, vals_dev, ld_vals, C, dt == LAT_BF16, wv_dev, beta, Wc_dev, bc_dev, K,
+                         logits_dev, stream);
+  return check_launch("deform slice classify");
+}
+
 // ---- backward passes ----
 
 int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int C, int normalize,

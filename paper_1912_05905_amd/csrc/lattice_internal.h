@@ -155,6 +155,11 @@ void launch_slice(const int32_t* idx, const float* w, int64_t m, const void* val
 void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const void* vals,
                          int64_t ld_vals, int C, int bf16, const float* wv, float beta, float* out,
                          float* delta, hipStream_t s);
+int deform_classify_max_classes();
+int deform_classify_max_weights();
+void launch_deform_classify(const int32_t* idx, const float* w, int64_t m, const void* vals, int64_t ld_vals, int C,
+                            int bf16, const float* wv, float beta, const float* Wc, const float* bc, int K, float* out,
+                            hipStream_t s);
 int64_t deform_backward_workspace_bytes(int64_t m, int C, int64_t total, int chunk);
 void launch_deform_slice_backward(const int32_t* idx, const float* w, int64_t m, const int32_t* offsets,
                                   const int32_t* entries, const int32_t* chunk_first, int chunk, int64_t n,

@@ -11,6 +11,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int64_t kDeformBwdGrid = 1024;   // workgroups of the DeformSlice backward's per-point pass
+constexpr int kClassifyMaxWeights = 16384; // K x C classifier weights staged in LDS
 
 // float -> bfloat16, round to nearest even (NaN stays NaN).
 __device__ inline uint16_t f32_to_bf16(float f) {
@@ -510,6 +511,123 @@ k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64
 }
 
 // lanes per row: enough 16-byte chunks to cover C, at most 64 (a wavefront)
+// One exchange of the reduce-scatter in k_deform_classify: lanes whose bit
+// OFF is set keep the upper LEN values, the others the lower LEN, and each
+// adds the half its partner gives away.
+template <int LPR, int OFF, int LEN, int KP>
+__device__ inline void reduce_scatter_step(float (&lg)[KP], int lane) {
+  const bool up = (lane & OFF) != 0;
+#pragma unroll
+  for (int i = 0; i < LEN; ++i) {
+    const float give = up ? lg[i] : lg[i + LEN];
+    const float keep = up ? lg[i + LEN] : lg[i];
+    lg[i] = keep + __shfl_xor(give, OFF, LPR);
+  }
+}
+
+// DeformSlice fused with the last linear classification layer
+// (Implementation): the DeformSlice row of a point is formed in registers as
+// in k_deform_slice and multiplied by Wc (K x C, staged in LDS); the KP >= K
+// logit partials of a lane group are summed by a reduce-scatter, after which
+// lane L holds classes L * KP / LPR .. + KP / LPR - 1.  The high-dimensional
+// per-point row is never stored.
+template <bool BF16, int LPR, int CPL, int KP>
+__global__ void __launch_bounds__(kBlock)
+k_deform_classify(const int4* __restrict__ idx, const float4* __restrict__ w, int64_t m,
+                  const void* __restrict__ vals, int64_t ld_vals, int C, const float* __restrict__ wvec, float beta,
+                  const float* __restrict__ Wc, const float* __restrict__ bc, int K, float* __restrict__ out,
+                  unsigned nblk) {
+  using Ch = Chunk<BF16>;
+  extern __shared__ __align__(16) float wl[];   // [K][C]
+  for (int i = threadIdx.x; i < K * C; i += kBlock) wl[i] = Wc[i];
+  __syncthreads();
+  const int lane = threadIdx.x & (LPR - 1);
+  const int64_t p = xcd_item<LPR>(nblk);
+  const bool live = p < m;
+  const int nchunk = C / Ch::N;
+  int4 iv = make_int4(-1, -1, -1, -1);
+  float4 wq = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (live) { iv = idx[p]; wq = w[p]; }
+  const int32_t vi[4] = {iv.x, iv.y, iv.z, iv.w};
+  const float bw[4] = {wq.x, wq.y, wq.z, wq.w};
+  float x[CPL][4][Ch::N];
+  float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
+    const int ch = lane + q * LPR;
+    const bool on = live && ch < nchunk;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (on && vi[k] >= 0) {
+        Ch c;
+        c.load(vals, static_cast<int64_t>(vi[k]) * ld_vals + static_cast<int64_t>(ch) * Ch::N);
+#pragma unroll
+        for (int i = 0; i < Ch::N; ++i) x[q][k][i] = c.v[i];
+      } else {
+#pragma unroll
+        for (int i = 0; i < Ch::N; ++i) x[q][k][i] = 0.f;
+      }
+    }
+    if (on) {
+#pragma unroll
+      for (int i = 0; i < Ch::N; ++i) {
+        const float wc = wvec[ch * Ch::N + i];
+        float qk[4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          qk[k] = bw[k] * x[q][k][i];
+          mx = fmaxf(mx, qk[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) part[k] += (qk[k] - mx) * wc;
+      }
+    }
+  }
+#pragma unroll
+  for (int off = LPR / 2; off > 0; off >>= 1)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) part[k] += __shfl_xor(part[k], off, LPR);
+  float coef[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) coef[k] = bw[k] + tanhf(beta + part[k]);
+  float lg[KP];
+#pragma unroll
+  for (int j = 0; j < KP; ++j) lg[j] = 0.f;
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
+    const int ch = lane + q * LPR;
+    if (!(live && ch < nchunk)) continue;
+#pragma unroll
+    for (int i = 0; i < Ch::N; i += 4) {
+      float f[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        f[u] = coef[0] * x[q][0][i + u] + coef[1] * x[q][1][i + u] + coef[2] * x[q][2][i + u] +
+               coef[3] * x[q][3][i + u];
+#pragma unroll
+      for (int j = 0; j < KP; ++j) {
+        if (j >= K) break;
+        const float4 wv4 = *reinterpret_cast<const float4*>(wl + j * C + ch * Ch::N + i);
+        lg[j] += wv4.x * f[0] + wv4.y * f[1] + wv4.z * f[2] + wv4.w * f[3];
+      }
+    }
+  }
+  if constexpr (LPR >= 2) reduce_scatter_step<LPR, LPR / 2, KP / 2>(lg, lane);
+  if constexpr (LPR >= 4) reduce_scatter_step<LPR, LPR / 4, KP / 4>(lg, lane);
+  if constexpr (LPR >= 8) reduce_scatter_step<LPR, LPR / 8, KP / 8>(lg, lane);
+  if constexpr (LPR >= 16) reduce_scatter_step<LPR, LPR / 16, KP / 16>(lg, lane);
+  if constexpr (LPR >= 32) reduce_scatter_step<LPR, LPR / 32, KP / 32>(lg, lane);
+  if constexpr (LPR >= 64) reduce_scatter_step<LPR, LPR / 64, KP / 64>(lg, lane);
+  if (!live) return;
+  constexpr int OWN = KP / LPR;
+#pragma unroll
+  for (int i = 0; i < OWN; ++i) {
+    const int j = lane * OWN + i;
+    if (j < K) out[p * K + j] = lg[i] + (bc ? bc[j] : 0.f);
+  }
+}
+
 // DeformSlice backward, per point (C channels over LPR lanes, CPL 16-byte
 // chunks per lane, as in the forward), with g = dL/dout_p:
 //   q_k = b_k x_k; am_c = the first slot k whose float32 q_k is maximal,
@@ -839,7 +957,57 @@ void launch_slice(const int32_t* idx, const float* w, int64_t m, const void* val
   else slice_dispatch<false>(lpr, idx, w, m, vals, ld_vals, C, out, s);
 }
 
-// Work space of launch_deform_slice_backward, in bytes.
+template <bool BF16, int CPL, int KP>
+void deform_classify_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, const void* vals, int64_t ldv,
+                              int C, const float* wv, float beta, const float* Wc, const float* bc, int K,
+                              float* out, hipStream_t s) {
+  const unsigned nblk = grid_for(m, lpr);
+  const dim3 g(xcd_grid(nblk)), b(kBlock);
+  const int4* i4 = reinterpret_cast<const int4*>(idx);
+  const float4* w4 = reinterpret_cast<const float4*>(w);
+  const uint32_t lds = static_cast<uint32_t>(4 * K * C);
+#define DCL_CASE(L)                                                                                              \
+  if (lpr == L) {                                                                                                \
+    static bool set = false;                                                                                     \
+    if (!set) {                                                                                                  \
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_deform_classify<BF16, L, CPL, KP>),               \
+                                hipFuncAttributeMaxDynamicSharedMemorySize, 4 * kClassifyMaxWeights);           \
+      set = true;                                                                                                \
+    }                                                                                                            \
+    return launch((k_deform_classify<BF16, L, CPL, KP>), g, b, lds, s, i4, w4, m, vals, ldv, C, wv, beta, Wc, bc, K, \
+                  out, nblk);                                                                                    \
+  }
+  if constexpr (KP >= 64) { DCL_CASE(64) }
+  DCL_CASE(1) DCL_CASE(2) DCL_CASE(4) DCL_CASE(8) DCL_CASE(16) DCL_CASE(32)
+#undef DCL_CASE
+}
+
+int deform_classify_max_classes() { return 64; }
+int deform_classify_max_weights() { return kClassifyMaxWeights; }
+
+void launch_deform_classify(const int32_t* idx, const float* w, int64_t m, const void* vals, int64_t ld_vals, int C,
+                            int bf16, const float* wv, float beta, const float* Wc, const float* bc, int K, float* out,
+                            hipStream_t s) {
+  if (m <= 0) return;
+  const int lpr = lanes_per_row(C, bf16 != 0);
+  const int chunks = C / (bf16 ? 8 : 4);
+  ScopedKernelTimer tm("deform_slice", s);
+  const bool two = chunks > lpr;
+  const bool kp64 = K > 32 || lpr > 32;
+#define DCL_GO(BFV, CPLV)                                                                                          \
+  (kp64 ? deform_classify_dispatch<BFV, CPLV, 64>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, Wc, bc, K, out, s)  \
+        : deform_classify_dispatch<BFV, CPLV, 32>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, Wc, bc, K, out, s))
+  if (bf16) {
+    if (two) DCL_GO(true, 2);
+    else DCL_GO(true, 1);
+  } else {
+    if (two) DCL_GO(false, 2);
+    else DCL_GO(false, 1);
+  }
+#undef DCL_GO
+}
+
+// Work space of launch_deform_slice_backward, in bytes.// Work space of launch_deform_slice_backward, in bytes.
 int64_t deform_backward_workspace_bytes(int64_t m, int C, int64_t total, int chunk) {
   return 16 * 4 * m + m * C + 4 * (kDeformBwdGrid * (static_cast<int64_t>(C) + 1)) +
          4 * splat_partial_floats(total, chunk, C) + 64;

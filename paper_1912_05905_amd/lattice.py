@@ -47,6 +47,7 @@ SIGNATURES = {
                                    _P]),
     "lattice_refine_preact": (_I32, [_P, _P, _P, _I64, _I32, _I32, _P, _P, _F32, _P, _P, _I32, _I32, _I32, _P,
                                      _I64, _P]),
+    "lattice_deform_slice_classify": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _I32, _P, _P]),
     "lattice_distribute_pointnet": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _P, _P, _I32, _P, _P, _I32,
                                            _P, _I64, _P]),
     "lattice_splat_backward": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P, _P]),
@@ -357,6 +358,22 @@ class Lattice:
                                                    dp, dld, C.c_void_p(dwv.data_ptr()), C.c_void_p(dbeta.data_ptr()),
                                                    _stream(stream)))
         return dx, dwv, dbeta
+
+    def deform_slice_classify(self, x: torch.Tensor, wv: torch.Tensor, beta: float, Wc: torch.Tensor,
+                              bc: torch.Tensor | None = None, out: torch.Tensor | None = None,
+                              stream=None) -> torch.Tensor:
+        """DeformSlice fused with the classifier: m x K logits, Wc K x C."""
+        K, Cc = Wc.shape[0], x.shape[1]
+        if Wc.dtype != torch.float32 or not Wc.is_contiguous() or Wc.shape[1] != Cc:
+            raise ValueError("Wc must be a contiguous K x C float32 tensor")
+        if out is None:
+            out = torch.empty((self.m, K), dtype=torch.float32, device="cuda")
+        xp, xld = _rows(x)
+        _check(lib().lattice_deform_slice_classify(self._h, xp, xld, Cc, _dtype_code(x), C.c_void_p(wv.data_ptr()),
+                                                   float(beta), C.c_void_p(Wc.data_ptr()),
+                                                   None if bc is None else C.c_void_p(bc.data_ptr()), K,
+                                                   C.c_void_p(out.data_ptr()), _stream(stream)))
+        return out
 
     def deform_slice(self, x: torch.Tensor, wv: torch.Tensor, beta: float,
                      out: torch.Tensor | None = None, delta: torch.Tensor | None = None,

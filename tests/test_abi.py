@@ -32,7 +32,7 @@ def test_header_declares_the_boundary():
                  "lattice_refine", "lattice_slice", "lattice_deform_slice", "lattice_destroy",
                  "lattice_num_vertices", "lattice_export_keys", "lattice_export_neighbors",
                  "lattice_export_simplices", "lattice_distribute_pointnet", "lattice_splat_backward",
-                 "lattice_slice_backward", "lattice_conv_backward", "lattice_deform_slice_backward", "lattice_conv_preact",
+                 "lattice_slice_backward", "lattice_conv_backward", "lattice_deform_slice_backward", "lattice_conv_preact", "lattice_deform_slice_classify",
                  "lattice_refine_preact"):
         assert need in names
 

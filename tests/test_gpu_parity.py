@@ -751,3 +751,24 @@ def test_conv_preact_across_levels(L, O, dtype):
     _preact_case(L, O, gl, gc, ol, oc, g2o_f, g2o_c, "upsample", 128, 64, 32, 6, dtype)
     if dtype == "bf16":
         _preact_case(L, O, gl, gl, ol, ol, g2o_f, g2o_f, "same", 64, 64, 32, 7, dtype)
+
+
+@pytest.mark.parametrize("C,K,dtype", [(4, 7, "f32"), (16, 20, "f32"), (64, 20, "f32"), (64, 64, "f32"),
+                                       (128, 33, "f32"), (256, 20, "f32"), (512, 32, "f32"), (64, 20, "bf16"),
+                                       (256, 1, "bf16")])
+def test_deform_slice_classify(L, O, C, K, dtype):
+    pos = _cloud(1200 + C + K, 7000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.06)
+    rng = np.random.default_rng(C * 100 + K)
+    bf = dtype == "bf16"
+    X = rng.normal(size=(ol.n, C))
+    if bf:
+        X = O.round_bf16(X)
+    wv = (rng.normal(size=C) / np.sqrt(C)).astype(np.float32)
+    Wc = (rng.normal(size=(K, C)) / np.sqrt(C)).astype(np.float32)
+    bc = rng.normal(size=K).astype(np.float32) if K != 64 else None
+    gy = gl.deform_slice_classify(_dev(X[g2o].astype(np.float32), torch.bfloat16 if bf else None), _dev(wv), 0.1,
+                                  _dev(Wc), None if bc is None else _dev(bc))
+    oy = ol.deform_slice_classify(X, wv.astype(np.float64), 0.1, Wc.astype(np.float64),
+                                  None if bc is None else bc.astype(np.float64))
+    P.assert_close(_host(gy), oy, P.TOL_F32, f"DeformSlice+classifier C={C} K={K} {dtype}")
