@@ -178,12 +178,17 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
  * normalised input is never stored.
  *   groups     divides Cin (the paper uses 32); gamma_dev / beta_dev
  *              optional Cin float32 (NULL = 1 / 0); eps > 0.
+ *   res_dev    lattice_conv_preact only: optional n_dst x Cout residual
+ *              (dtype dt, row stride ld_res, 0 = Cout) added to the output
+ *              after its activation -- the identity branch of a ResNet
+ *              block (architecture figure).  It may be out_dev itself (same
+ *              row stride), any other overlap with out_dev is rejected.
  *   Other arguments as for lattice_conv / lattice_refine.  Cin <= 1024.
  */
 int lattice_conv_preact(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in, int Cin, int groups,
                         const float* gamma_dev, const float* beta_dev, float eps, const void* W_dev,
-                        const float* bias_dev, int Cout, lat_dtype dt, int flags, void* out_dev, int64_t ld_out,
-                        hipStream_t stream);
+                        const float* bias_dev, int Cout, lat_dtype dt, int flags, const void* res_dev,
+                        int64_t ld_res, void* out_dev, int64_t ld_out, hipStream_t stream);
 int lattice_refine_preact(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t ld_in, int Cin, int groups,
                           const float* gamma_dev, const float* beta_dev, float eps, const void* W_dev,
                           const float* bias_dev, int Cout, lat_dtype dt, int flags, void* out_dev, int64_t ld_out,

@@ -533,6 +533,8 @@ struct GnArgs {
   const float* gamma;
   const float* beta;
   float eps;
+  const void* res;   // optional residual added to the output
+  int64_t ld_res;
 };
 
 int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
@@ -554,6 +556,15 @@ int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, 
     return fail(LAT_EINVAL, "in and out overlap");
   if (gn) {
     if (gn->groups <= 0 || Cin % gn->groups != 0) return fail(LAT_EINVAL, "groups must divide Cin");
+    if (gn->res) {
+      const int64_t ld_res = gn->ld_res ? gn->ld_res : Cout;
+      if ((st = check_matrix(gn->res, ld_res, Cout, dt, "res", true)) != LAT_OK) return st;
+      if (rows) return fail(LAT_EUNSUPPORTED, "a residual is not supported for Upsample");
+      if (n_out > 0 && overlaps(gn->res, static_cast<size_t>((n_out - 1) * ld_res + Cout) * u, out,
+                                static_cast<size_t>((n_out - 1) * ld_out + Cout) * u) &&
+          !(gn->res == out && ld_res == ld_out))
+        return fail(LAT_EINVAL, "res and out overlap (other than res == out with the same row stride)");
+    }
     if (!(gn->eps > 0.f) || !std::isfinite(gn->eps)) return fail(LAT_EINVAL, "eps must be positive and finite");
     if (Cin > conv_max_pre_channels() || Cin > gn_max_channels())
       return fail(LAT_EUNSUPPORTED, "pre-activated convolutions take at most " +
@@ -570,7 +581,8 @@ int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, 
                      pre.as<float>(), work.p, s);
   }
   launch_conv(table, ldn, n_out, n_in, in, ld_in, Cin, W, bias, Cout, dt == LAT_BF16, flags & LAT_RELU, out,
-              ld_out, rows, s, gn ? pre.as<float>() : nullptr);
+              ld_out, rows, s, gn ? pre.as<float>() : nullptr, gn ? gn->res : nullptr,
+              gn && gn->res ? (gn->ld_res ? gn->ld_res : Cout) : 0);
   return check_launch("conv");
 }
 
@@ -766,8 +778,8 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
 
 int lattice_conv_preact(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in, int Cin, int groups,
                         const float* gamma_dev, const float* beta_dev, float eps, const void* W_dev,
-                        const float* bias_dev, int Cout, lat_dtype dt, int flags, void* out_dev, int64_t ld_out,
-                        hipStream_t stream) {
+                        const float* bias_dev, int Cout, lat_dtype dt, int flags, const void* res_dev,
+                        int64_t ld_res, void* out_dev, int64_t ld_out, hipStream_t stream) {
   int st;
   if ((st = check_handle(dst)) != LAT_OK) return st;
   if ((st = check_handle(src)) != LAT_OK) return st;
@@ -775,7 +787,7 @@ int lattice_conv_preact(lattice_t dst, lattice_t src, const void* in_dev, int64_
   if (dst == src) table = dst->nbr;
   else if (dst->parent == src) table = dst->down;
   else return fail(LAT_ELEVEL, "dst must be src or lattice_coarsen(src)");
-  const GnArgs gn{groups, gamma_dev, beta_dev, eps};
+  const GnArgs gn{groups, gamma_dev, beta_dev, eps, res_dev, ld_res};
   return conv_common(table, dst->nmax, dst->n, src->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt, flags,
                      out_dev, ld_out, nullptr, stream, &gn);
 }
@@ -788,7 +800,7 @@ int lattice_refine_preact(lattice_t fine, lattice_t coarse, const void* in_dev, 
   if ((st = check_handle(fine)) != LAT_OK) return st;
   if ((st = check_handle(coarse)) != LAT_OK) return st;
   if (coarse->parent != fine) return fail(LAT_ELEVEL, "coarse must be lattice_coarsen(fine)");
-  const GnArgs gn{groups, gamma_dev, beta_dev, eps};
+  const GnArgs gn{groups, gamma_dev, beta_dev, eps, nullptr, 0};
   return conv_common(coarse->up, fine->nmax, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
                      flags, out_dev, ld_out, coarse->up_rows, stream, &gn);
 }

@@ -240,7 +240,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
            int64_t ld_in, int Cin, const void* __restrict__ W, const float* __restrict__ bias, int Cout,
            int relu, void* __restrict__ out, int64_t ld_out, const int32_t* __restrict__ rows,
            unsigned row_tiles, int splits, float* __restrict__ part, uint32_t in_bytes, uint32_t w_bytes,
-           const float* __restrict__ pre) {
+           const float* __restrict__ pre, const void* __restrict__ res, int64_t ld_res) {
   using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
   using E = typename std::conditional<BF16, uint16_t, float>::type;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -493,10 +493,13 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
         const int64_t row = rows ? rows[r0] : r0;
         float v = acc[i][j][r] + bv;
         if (relu) v = fmaxf(v, 0.f);
-        if constexpr (BF16)
+        if constexpr (BF16) {
+          if (res) v += __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(res)[row * ld_res + col]) << 16);
           static_cast<uint16_t*>(out)[row * ld_out + col] = f32_to_bf16(v);
-        else
+        } else {
+          if (res) v += static_cast<const float*>(res)[row * ld_res + col];
           static_cast<float*>(out)[row * ld_out + col] = v;
+        }
       }
   }
 }
@@ -505,7 +508,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
 template <bool BF16>
 __global__ void __launch_bounds__(kBlock)
 k_conv_reduce(const float* __restrict__ part, int splits, int64_t n_out, int Cout, const float* __restrict__ bias,
-              int relu, void* __restrict__ out, int64_t ld_out) {
+              int relu, void* __restrict__ out, int64_t ld_out, const void* __restrict__ res, int64_t ld_res) {
   const int64_t quads = n_out * (Cout / 4);
   const int64_t plane = n_out * Cout;
   for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < quads;
@@ -522,6 +525,12 @@ k_conv_reduce(const float* __restrict__ part, int splits, int64_t n_out, int Cou
     for (int i = 0; i < 4; ++i) {
       if (bias) v[i] += bias[col + i];
       if (relu) v[i] = fmaxf(v[i], 0.f);
+      if (res) {
+        if constexpr (BF16)
+          v[i] += __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(res)[row * ld_res + col + i]) << 16);
+        else
+          v[i] += static_cast<const float*>(res)[row * ld_res + col + i];
+      }
     }
     if constexpr (BF16) {
       const uint32_t lo = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
@@ -544,7 +553,7 @@ template <bool BF16, int BM, int BN, int WM, int WN, int KCB, int NS = 2, bool B
 void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                      int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
                      int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s, const float* pre = nullptr,
-                     int splits = 1, float* part = nullptr) {
+                     const void* res = nullptr, int64_t ld_res = 0, int splits = 1, float* part = nullptr) {
   using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
   if (rows) splits = 1;  // partial sums are kept in permuted row order
   const int lds = P::LDS_BYTES + (PRE ? 8 * Cin : 0);
@@ -561,12 +570,12 @@ void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void*
   launch((k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED, PRE>), grid, dim3(kBlock), static_cast<uint32_t>(lds),
          s, nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, static_cast<unsigned>(tiles),
          splits, splits > 1 ? part : nullptr, static_cast<uint32_t>(BUF ? ext.in_bytes : 0),
-         static_cast<uint32_t>(BUF ? ext.w_bytes : 0), pre);
+         static_cast<uint32_t>(BUF ? ext.w_bytes : 0), pre, res, ld_res);
   if (splits > 1) {
     const int64_t quads = n_out * (Cout / 4);
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((quads + kBlock - 1) / kBlock, 8192));
     launch((k_conv_reduce<BF16>), dim3(blocks), dim3(kBlock), 0, s, part, splits, n_out, Cout, bias,
-                       relu, out, ld_out);
+                       relu, out, ld_out, res, ld_res);
   }
 }
 
@@ -585,35 +594,36 @@ int64_t blocks_of(int64_t n_out, int Cout, int rows, int cols) {
 template <bool BF16, bool PRE>
 void conv_dispatch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in, int64_t ld_in,
                    int Cin, const void* W, const float* bias, int Cout, int relu, void* out,
-                   int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s, const float* pre) {
-  if (!PRE && Cout <= 16)
+                   int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s, const float* pre,
+                   const void* res, int64_t ld_res) {
+  if (!PRE && !res && Cout <= 16)
     return conv_launch<BF16, 1, 1, 4, 1>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, s);
   if (!ext.buffer_ok())  // operands beyond the reach of a buffer resource
     return conv_lds_launch<BF16, 64, 64, 2, 2, 128, 2, false, 0, PRE>(
-        nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+        nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
   if constexpr (BF16) {
     const int64_t b128 = blocks_of(n_out, Cout, 128, 128);
     const int64_t b64 = blocks_of(n_out, Cout, 64, 64);
     if (Cout >= 128 && (b128 >= 1500 || (Cin >= 256 && Cout % 128 == 0)))
       return conv_lds_launch<true, 128, 128, 2, 2, 64, 3, true, 1, PRE>(
-          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
     if (Cout > 32 && b64 >= 8192)
       return conv_lds_launch<true, 64, 64, 2, 2, 128, 3, true, 1, PRE>(
-          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
     if (Cout > 32 && b64 >= 256)
       return conv_lds_launch<true, 64, 64, 2, 2, 128, 2, true, 1, PRE>(
-          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
     return conv_lds_launch<true, 32, 32, 2, 2, 128, 2, true, 0, PRE>(
-        nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+        nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
   } else {
     if (Cout > 32 && blocks_of(n_out, Cout, 64, 64) >= 2048)
       return conv_lds_launch<false, 64, 64, 2, 2, 128, 3, true, 1, PRE>(
-          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
     if (Cout > 64 && blocks_of(n_out, Cout, 32, 64) >= 1024)
       return conv_lds_launch<false, 32, 64, 2, 2, 128, 3, true, 1, PRE>(
-          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
     return conv_lds_launch<false, 32, 32, 2, 2, 256, 2, true, 1, PRE>(
-        nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre);
+        nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
   }
 }
 
@@ -623,14 +633,15 @@ int conv_max_pre_channels() { return kMaxPreChannels; }
 
 void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
-                 int64_t ld_out, const int32_t* rows, hipStream_t s, const float* pre) {
+                 int64_t ld_out, const int32_t* rows, hipStream_t s, const float* pre, const void* res,
+                 int64_t ld_res) {
   if (n_out <= 0) return;
   ScopedKernelTimer tm("conv", s);
   const int64_t u = bf16 ? 2 : 4;
   const ConvExtent ext{n_in > 0 ? ((n_in - 1) * ld_in + Cin) * u : 0, int64_t{kTaps} * Cout * Cin * u};
   auto go = [&](auto bf_c, auto pre_c) {
     conv_dispatch<decltype(bf_c)::value, decltype(pre_c)::value>(nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout,
-                                                                  relu, out, ld_out, rows, ext, s, pre);
+                                                                  relu, out, ld_out, rows, ext, s, pre, res, ld_res);
   };
   using T = std::true_type;
   using F = std::false_type;

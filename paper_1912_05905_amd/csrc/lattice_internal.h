@@ -185,10 +185,13 @@ void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const flo
                        hipStream_t s);
 // conv.hip
 // pre: optional Cin scales then Cin shifts of the pre-activation (applied,
-// with a ReLU, to the gathered input values of existing neighbours)
+// with a ReLU, to the gathered input values of existing neighbours);
+// res: optional residual (n_out x Cout, out's dtype) added after the
+// activation of the output
 void launch_conv(const int32_t* nbr, int64_t ldn, int64_t n_out, int64_t n_in, const void* in, int64_t ld_in,
                  int Cin, const void* W, const float* bias, int Cout, int bf16, int relu, void* out,
-                 int64_t ld_out, const int32_t* rows, hipStream_t s, const float* pre = nullptr);
+                 int64_t ld_out, const int32_t* rows, hipStream_t s, const float* pre = nullptr,
+                 const void* res = nullptr, int64_t ld_res = 0);
 int conv_max_pre_channels();
 // norm.hip
 int gn_max_channels();

@@ -2,7 +2,7 @@
 // (Implementation: every convolution is pre-activated by Group Normalization
 // with 32 groups and a ReLU).  Over the n vertices of a lattice and the
 // channels of each group: mean and biased variance, summed in fp64 in a fixed
-// order (per-workgroup partials, then one pass over the partials).  The
+// order (per-workgroup partials, then a tree over the partials).  The
 // result is the per-channel affine map the convolution applies to every
 // gathered input value before its ReLU:
 //   scale_c = gamma_c / sqrt(var_g + eps),  shift_c = beta_c - mean_g scale_c.
@@ -74,25 +74,38 @@ k_gn_partial(const void* __restrict__ x, int64_t ld, int C, int64_t n, int64_t r
   }
 }
 
-// One thread per group: the partials in workgroup order, then the group's
-// channels; writes scale (pre[0..C)) and shift (pre[C..2C)).
+// One workgroup per group: the threads stride over the partials (and the
+// group's channels), then a fixed tree adds their sums; writes scale
+// (pre[0..C)) and shift (pre[C..2C)) of the group's channels.
 __global__ void __launch_bounds__(kBlock)
 k_gn_finalize(const double* __restrict__ part, int nparts, int C, int groups, int64_t n,
               const float* __restrict__ gamma, const float* __restrict__ beta, float eps, float* __restrict__ pre) {
-  const int g = static_cast<int>(blockIdx.x) * kBlock + threadIdx.x;
-  if (g >= groups) return;
+  __shared__ double sh[2][kBlock];
+  const int g = blockIdx.x;
   const int per = C / groups;
+  const int t = threadIdx.x;
   double s = 0.0, ss = 0.0;
-  for (int w = 0; w < nparts; ++w)
-    for (int c = g * per; c < (g + 1) * per; ++c) {
-      s += part[static_cast<int64_t>(w) * 2 * C + c];
-      ss += part[static_cast<int64_t>(w) * 2 * C + C + c];
+  for (int64_t q = t; q < static_cast<int64_t>(nparts) * per; q += kBlock) {
+    const int64_t w = q / per;
+    const int c = g * per + static_cast<int>(q - w * per);
+    s += part[w * 2 * C + c];
+    ss += part[w * 2 * C + C + c];
+  }
+  sh[0][t] = s;
+  sh[1][t] = ss;
+  __syncthreads();
+  for (int off = kBlock / 2; off > 0; off >>= 1) {
+    if (t < off) {
+      sh[0][t] += sh[0][t + off];
+      sh[1][t] += sh[1][t + off];
     }
+    __syncthreads();
+  }
   const double cnt = static_cast<double>(n) * per;
-  const double mean = cnt > 0 ? s / cnt : 0.0;
-  const double var = cnt > 0 ? max(ss / cnt - mean * mean, 0.0) : 0.0;
+  const double mean = cnt > 0 ? sh[0][0] / cnt : 0.0;
+  const double var = cnt > 0 ? max(sh[1][0] / cnt - mean * mean, 0.0) : 0.0;
   const double inv = 1.0 / sqrt(var + static_cast<double>(eps));
-  for (int c = g * per; c < (g + 1) * per; ++c) {
+  for (int c = g * per + t; c < (g + 1) * per; c += kBlock) {
     const double sc = (gamma ? gamma[c] : 1.0) * inv;
     pre[c] = static_cast<float>(sc);
     pre[C + c] = static_cast<float>((beta ? beta[c] : 0.0) - mean * sc);
@@ -127,7 +140,7 @@ void launch_gn_affine(const void* x, int64_t ld, int C, int bf16, int64_t n, int
     if (bf16) launch(k_gn_partial<true>, dim3(static_cast<unsigned>(np)), dim3(kBlock), 0, s, x, ld, C, n, rp, part);
     else launch(k_gn_partial<false>, dim3(static_cast<unsigned>(np)), dim3(kBlock), 0, s, x, ld, C, n, rp, part);
   }
-  launch(k_gn_finalize, dim3(static_cast<unsigned>((groups + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
+  launch(k_gn_finalize, dim3(static_cast<unsigned>(groups)), dim3(kBlock), 0, s,
          static_cast<const double*>(part), n > 0 ? static_cast<int>(np) : 0, C, groups, n, gamma, beta, eps, pre);
 }
 

@@ -44,7 +44,7 @@ SIGNATURES = {
     "lattice_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
     "lattice_deform_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _P]),
     "lattice_conv_preact": (_I32, [_P, _P, _P, _I64, _I32, _I32, _P, _P, _F32, _P, _P, _I32, _I32, _I32, _P, _I64,
-                                   _P]),
+                                   _P, _I64, _P]),
     "lattice_refine_preact": (_I32, [_P, _P, _P, _I64, _I32, _I32, _P, _P, _F32, _P, _P, _I32, _I32, _I32, _P,
                                      _I64, _P]),
     "lattice_deform_slice_classify": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _I32, _P, _P]),
@@ -249,9 +249,10 @@ class Lattice:
     def conv_preact(self, src: "Lattice", x: torch.Tensor, W: torch.Tensor, groups: int = 32,
                     gamma: torch.Tensor | None = None, beta: torch.Tensor | None = None, eps: float = 1e-5,
                     bias: torch.Tensor | None = None, relu: bool = False, out: torch.Tensor | None = None,
-                    refine: bool = False, stream=None) -> torch.Tensor:
-        """conv(relu(GroupNorm(x))): self is the destination; src as for conv
-        (refine=False) or the coarse lattice of an Upsample (refine=True)."""
+                    refine: bool = False, res: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """conv(relu(GroupNorm(x))) (+ res): self is the destination; src as
+        for conv (refine=False) or the coarse lattice of an Upsample
+        (refine=True, no residual)."""
         cout, cin = W.shape[1], W.shape[2]
         if out is None:
             out = torch.empty((self.n, cout), dtype=x.dtype, device="cuda")
@@ -260,9 +261,15 @@ class Lattice:
         if not W.is_contiguous() or W.dtype != x.dtype:
             raise ValueError("W must be contiguous with the dtype of x")
         ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
-        fn = lib().lattice_refine_preact if refine else lib().lattice_conv_preact
-        _check(fn(self._h, src._h, xp, xld, cin, int(groups), ptr(gamma), ptr(beta), float(eps), ptr(W), ptr(bias),
-                  cout, _dtype_code(x), LAT_RELU if relu else 0, op, old, _stream(stream)))
+        args = [self._h, src._h, xp, xld, cin, int(groups), ptr(gamma), ptr(beta), float(eps), ptr(W), ptr(bias),
+                cout, _dtype_code(x), LAT_RELU if relu else 0]
+        if refine:
+            if res is not None:
+                raise ValueError("no residual for an Upsample")
+            _check(lib().lattice_refine_preact(*args, op, old, _stream(stream)))
+        else:
+            rp, rld = _rows(res) if res is not None else (None, 0)
+            _check(lib().lattice_conv_preact(*args, rp, rld, op, old, _stream(stream)))
         return out
 
     def slice(self, x: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

@@ -30,6 +30,11 @@ class GpuPipeline:
                         torch.from_numpy(np.ascontiguousarray(b, dtype=np.float32)).cuda())
                     for k, (W, b) in wl.mlp.items()}
         self.grads = {k: torch.from_numpy(np.ascontiguousarray(g)).cuda() for k, g in wl.grads.items()}
+        self.norms = {k: (torch.from_numpy(np.ascontiguousarray(g)).cuda(), torch.from_numpy(np.ascontiguousarray(b))
+                          .cuda()) for k, (g, b) in wl.norms.items()}
+        self.classifiers = {k: (torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32)).cuda(),
+                                torch.from_numpy(np.ascontiguousarray(b, dtype=np.float32)).cuda())
+                            for k, (W, b) in wl.classifiers.items()}
         self.sigma = [float(s) for s in wl.sigma]
         self._store: dict[str, torch.Tensor] = {}
         self._wsum: torch.Tensor | None = None
@@ -81,7 +86,13 @@ class GpuPipeline:
                 x = self._view(bufs, levels, op["src"])
                 y = self._view(bufs, levels, op["dst"])
                 W = self.weights[op["w"]]
-                if kind == "conv":
+                if "pre" in op:
+                    gam, bet = self.norms[op["pre"]["norm"]]
+                    src = levels[{"conv": lv, "conv_down": lv - 1, "refine": lv + 1}[kind]]
+                    res = self._view(bufs, levels, op["res"]) if "res" in op else None
+                    levels[lv].conv_preact(src, x, W, groups=op["pre"]["groups"], gamma=gam, beta=bet,
+                                           relu=op["relu"], out=y, refine=kind == "refine", res=res)
+                elif kind == "conv":
                     levels[lv].conv(levels[lv], x, W, relu=op["relu"], out=y)
                 elif kind == "conv_down":
                     levels[lv].conv(levels[lv - 1], x, W, relu=op["relu"], out=y)
@@ -96,6 +107,11 @@ class GpuPipeline:
                 wv, beta = self.vectors[op["wv"]]
                 outs[op["out"]] = levels[op["level"]].deform_slice(
                     self._view(bufs, levels, op["src"]), wv, beta)
+            elif kind == "deform_classify":
+                wv, beta = self.vectors[op["wv"]]
+                Wc, bc = self.classifiers[op["cls"]]
+                outs[op["out"]] = levels[op["level"]].deform_slice_classify(
+                    self._view(bufs, levels, op["src"]), wv, beta, Wc, bc)
             elif kind == "deform_slice_bwd":
                 wv, beta = self.vectors[op["wv"]]
                 _, dwv, dbeta = levels[op["level"]].deform_slice_backward(

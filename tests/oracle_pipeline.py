@@ -47,12 +47,20 @@ class OraclePipeline:
                 lv = op["level"]
                 x = np.ascontiguousarray(view_src(op["src"]))
                 W = wl.weights[op["w"]].astype(np.float64)
+                if "pre" in op:
+                    gam, bet = wl.norms[op["pre"]["norm"]]
+                    x = O.groupnorm(x, op["pre"]["groups"], gam.astype(np.float64), bet.astype(np.float64),
+                                    eps=1e-5, relu=True)
+                    if self.bf16:
+                        x = O.round_bf16(x)
                 if kind == "conv":
                     y = levels[lv].conv(levels[lv], x, W, relu=op["relu"])
                 elif kind == "conv_down":
                     y = levels[lv].conv(levels[lv - 1], x, W, relu=op["relu"])
                 else:
                     y = levels[lv].refine_into(levels[lv + 1], x, W, relu=op["relu"])
+                if "res" in op:
+                    y = y + view_src(op["res"])
                 write(op["dst"], y)
             elif kind == "distribute":
                 layers = [tuple(a.astype(np.float64) for a in wl.mlp[n]) for n in op["layers"]]
@@ -64,6 +72,12 @@ class OraclePipeline:
                 wv, beta = wl.vectors[op["wv"]]
                 outs[op["out"]], _ = levels[op["level"]].deform_slice(
                     np.ascontiguousarray(view_src(op["src"])), wv.astype(np.float64), beta)
+            elif kind == "deform_classify":
+                wv, beta = wl.vectors[op["wv"]]
+                Wc, bc = wl.classifiers[op["cls"]]
+                outs[op["out"]] = levels[op["level"]].deform_slice_classify(
+                    np.ascontiguousarray(view_src(op["src"])), wv.astype(np.float64), beta, Wc.astype(np.float64),
+                    bc.astype(np.float64))
             elif kind == "deform_slice_bwd":
                 wv, beta = wl.vectors[op["wv"]]
                 dx, dwv, dbeta = levels[op["level"]].deform_slice_backward(

@@ -396,6 +396,18 @@ def test_pipeline_full_size(L, O, cfg):
     _run_both(L, O, configs.make(cfg))
 
 
+def test_latticenet_reduced(L, O):
+    """The whole LatticeNet forward (Distribute + PointNet, eight ResNet
+    blocks of pre-activated convolutions, two Downsamples, two Upsamples with
+    concatenated skips, DeformSlice fused with the classifier) on reduced
+    clouds of the LiDAR and room generators: the oracle takes seconds there,
+    minutes at full size."""
+    for wl in (configs.config8(m=6000), configs.config9(m=12_000, size=(2.0, 2.0, 2.0), nboxes=3)):
+        levels = _run_both(L, O, wl)
+        from paper_1912_05905_amd.pipeline import GpuPipeline
+        GpuPipeline.release(levels)
+
+
 @pytest.mark.parametrize("seed", [100, 101])
 def test_pipeline_other_seeds(L, O, seed):
     for cfg in (1, 2):

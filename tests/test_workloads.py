@@ -28,7 +28,7 @@ def test_stream_is_deterministic_and_counter_based():
     assert abs(z.mean()) < 0.01 and abs(z.std() - 1.0) < 0.01
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 6, 7])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 6, 7, 8, 9])
 def test_config_shapes_and_determinism(cfg):
     a = configs.make(cfg)
     b = configs.make(cfg)
@@ -36,7 +36,7 @@ def test_config_shapes_and_determinism(cfg):
     assert _digest(a.features) == _digest(b.features)
     assert a.positions.dtype == np.float32 and a.positions.shape[1] == 3
     assert np.isfinite(a.positions).all()
-    expect_m = {1: 4096, 2: 2048, 3: 200_000, 4: 120_000, 6: 120_000, 7: 120_000}[cfg]
+    expect_m = {1: 4096, 2: 2048, 3: 200_000, 4: 120_000, 6: 120_000, 7: 120_000, 8: 120_000, 9: 200_000}[cfg]
     assert a.m == expect_m
     for name, w in a.weights.items():
         assert w.shape[0] == configs.TAPS

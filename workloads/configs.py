@@ -45,6 +45,8 @@ class Workload:
     vectors: dict = field(default_factory=dict)    # DeformSlice weight vectors
     mlp: dict = field(default_factory=dict)        # name -> (W [out][in], b) of 1x1 layers
     grads: dict = field(default_factory=dict)      # point output -> dL/d(output), m x C float32
+    norms: dict = field(default_factory=dict)      # name -> (gamma, beta) of a GroupNorm pre-activation
+    classifiers: dict = field(default_factory=dict)  # name -> (W [class][channel], b)
     buffers: dict = field(default_factory=dict)    # name -> (level, channels)
     ops: list = field(default_factory=list)
     levels: int = 1
@@ -216,6 +218,88 @@ def config6(seed: int = 3, m: int = 120_000) -> Workload:
     return _finish(wl)
 
 
+def _preact(wl, kind, level, src, dst, seed, res=None, groups=32):
+    """A pre-activated convolution conv(relu(GN(src))) (+ res)."""
+    name = f"{kind}{level}_{src[0]}{src[1]}_{dst[0]}{dst[1]}_{len(wl.ops)}"
+    wl.weights[name] = gen.conv_weights(seed, name, TAPS, src[2], dst[2])
+    gam = 1.0 + gen.normal_matrix(seed, "gn-gamma:" + name, 1, src[2], 0.1)[0]
+    bet = gen.normal_matrix(seed, "gn-beta:" + name, 1, src[2], 0.1)[0]
+    wl.norms[name] = (gam.astype(np.float32), bet.astype(np.float32))
+    op = dict(op=kind, level=level, src=src, dst=dst, w=name, relu=False, pre=dict(norm=name, groups=groups))
+    if res is not None:
+        op["res"] = res
+    wl.ops.append(op)
+
+
+def _resnet(wl, level, x, tmp, out, seed):
+    """ResNet block of the architecture figure: out = x + [GN, ReLU, conv]^2 (x)."""
+    _preact(wl, "conv", level, x, tmp, seed)
+    _preact(wl, "conv", level, tmp, out, seed, res=x)
+
+
+def _latticenet(wl, seed, widths=(64, 128, 256), classes=20):
+    """The LatticeNet forward network of the architecture figure on wl's
+    points (raw features wl.features): Distribute + PointNet (16/32/64) ->
+    ResNet -> Downsample -> ResNet x2 -> Downsample -> ResNet x2 -> Upsample
+    -> concatenate the level-1 skip -> ResNet x2 -> Upsample -> concatenate
+    the level-0 skip -> ResNet -> DeformSlice fused with the linear
+    classifier.  Every convolution is pre-activated by GroupNorm(32) + ReLU;
+    levels carry widths[0..2] channels; the concatenations are column ranges
+    of one buffer per level (no copies)."""
+    c0, c1, c2 = widths
+    wl.buffers = {"p0": (0, c0), "h0": (0, c0), "cat0": (0, 2 * c0), "d1": (1, c1), "h1": (1, c1), "r1": (1, c1),
+                  "cat1": (1, 2 * c1), "d2": (2, c2), "h2": (2, c2), "r2": (2, c2), "b2": (2, c2),
+                  "hu1": (1, 2 * c1), "ru1": (1, 2 * c1), "u1": (1, 2 * c1), "hu0": (0, 2 * c0), "u0": (0, 2 * c0)}
+    wl.ops = [dict(op="create", level=0), dict(op="coarsen", level=1), dict(op="coarsen", level=2)]
+    k = 3 + wl.features.shape[1]
+    names = []
+    for i, c in enumerate((16, 32, c0)):
+        W = gen.normal_matrix(seed, f"pointnet{i}", c, k, 1.0 / np.sqrt(k))
+        b = gen.normal_matrix(seed, f"pointnet{i}:bias", 1, c, 0.1)[0]
+        wl.mlp[f"pointnet{i}"] = (W, b)
+        names.append(f"pointnet{i}")
+        k = c
+    wl.ops.append(dict(op="distribute", level=0, dst=("p0", 0, c0), layers=names))
+    _resnet(wl, 0, ("p0", 0, c0), ("h0", 0, c0), ("cat0", c0, c0), seed)           # skip of level 0
+    _preact(wl, "conv_down", 1, ("cat0", c0, c0), ("d1", 0, c1), seed)
+    _resnet(wl, 1, ("d1", 0, c1), ("h1", 0, c1), ("r1", 0, c1), seed)
+    _resnet(wl, 1, ("r1", 0, c1), ("h1", 0, c1), ("cat1", c1, c1), seed)          # skip of level 1
+    _preact(wl, "conv_down", 2, ("cat1", c1, c1), ("d2", 0, c2), seed)
+    _resnet(wl, 2, ("d2", 0, c2), ("h2", 0, c2), ("r2", 0, c2), seed)
+    _resnet(wl, 2, ("r2", 0, c2), ("h2", 0, c2), ("b2", 0, c2), seed)
+    _preact(wl, "refine", 1, ("b2", 0, c2), ("cat1", 0, c1), seed)
+    _resnet(wl, 1, ("cat1", 0, 2 * c1), ("hu1", 0, 2 * c1), ("ru1", 0, 2 * c1), seed)
+    _resnet(wl, 1, ("ru1", 0, 2 * c1), ("hu1", 0, 2 * c1), ("u1", 0, 2 * c1), seed)
+    _preact(wl, "refine", 0, ("u1", 0, 2 * c1), ("cat0", 0, c0), seed)
+    _resnet(wl, 0, ("cat0", 0, 2 * c0), ("hu0", 0, 2 * c0), ("u0", 0, 2 * c0), seed)
+    _deform_vector(wl, seed, 2 * c0)
+    wl.classifiers["classifier"] = (gen.normal_matrix(seed, "classifier", classes, 2 * c0, 1.0 / np.sqrt(2 * c0)),
+                                    gen.normal_matrix(seed, "classifier:bias", 1, classes, 0.1)[0])
+    wl.ops.append(dict(op="deform_classify", level=0, src=("u0", 0, 2 * c0), wv="deform", cls="classifier",
+                       out="logits"))
+
+
+def config8(seed: int = 3, m: int = 120_000) -> Workload:
+    """LatticeNet forward on the SemanticKITTI-sized LiDAR scan of config 4:
+    raw feature = intensity, sigma 0.3 m, widths 64/128/256, 20 classes,
+    fp32."""
+    pos = gen.lidar_scan(seed, m)
+    inten = gen.Stream(seed, "intensity").uniform(m).reshape(m, 1).astype(np.float32)
+    wl = Workload(8, "latticenet-lidar", seed, pos, np.full(3, 0.3, np.float32), "f32", inten)
+    _latticenet(wl, seed)
+    return _finish(wl)
+
+
+def config9(seed: int = 2, m: int = 200_000, size=(8.0, 8.0, 3.0), nboxes: int = 20) -> Workload:
+    """LatticeNet forward on the ScanNet-sized room of config 3: raw
+    features = RGB, sigma 0.05 m, widths 64/128/256, 20 classes, fp32."""
+    pos = gen.room(seed, m, size, nboxes, 0.01)
+    rgb = gen.Stream(seed, "rgb").uniform(3 * m).reshape(m, 3).astype(np.float32)
+    wl = Workload(9, "latticenet-room", seed, pos, np.full(3, 0.05, np.float32), "f32", rgb)
+    _latticenet(wl, seed)
+    return _finish(wl)
+
+
 def _backward(wl, loss_out):
     """Append the backward pass of wl's forward ops for a loss whose gradient
     with respect to the point output `loss_out` is wl.grads[loss_out]: the
@@ -258,7 +342,8 @@ def config7(seed: int = 3, m: int = 120_000) -> Workload:
     return wl
 
 
-CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5, 6: config6, 7: config7}
+CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5, 6: config6, 7: config7, 8: config8,
+           9: config9}
 
 
 def make(cfg: int, seed: int | None = None, **kw) -> Workload:
