@@ -282,13 +282,17 @@ k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
 #pragma unroll
       for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
     float ws = 0.f;
-    for (int64_t s = s0; s < s1; s += B) {
-      int32_t e[B];
+    // the entries of the next batch are loaded while this batch's rows
+    // arrive and are added
+    int32_t e[B];
 #pragma unroll
-      for (int j = 0; j < B; ++j) e[j] = s + j < s1 ? entries[s + j] : 0;
+    for (int j = 0; j < B; ++j) e[j] = s0 + j < s1 ? entries[s0 + j] : 0;
+    for (int64_t s = s0; s < s1; s += B) {
       typename Rows::Batch bt;
 #pragma unroll
       for (int j = 0; j < B; ++j) rows.load(bt, j, s + j, e[j], s + j < s1, lane, nchunk);
+#pragma unroll
+      for (int j = 0; j < B; ++j) e[j] = s + B + j < s1 ? entries[s + B + j] : 0;
 #pragma unroll
       for (int j = 0; j < B; ++j) {
         if (s + j >= s1) break;
@@ -394,36 +398,56 @@ k_splat_finish(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
   splat_store<BF16, LPR, Q>(v, acc, ws, lane, nchunk, normalize, vals, ld_vals, wsum);
 }
 
-// Slice (Eq. slice): out_p = sum_k b_pk x_{idx_pk}; one lane group per point.
+// Slice (Eq. slice): out_p = sum_k b_pk x_{idx_pk}.  A lane group takes two
+// consecutive points and issues the loads of both before using them (twice
+// the bytes in flight per lane).  A vertex slot without a vertex (a lattice
+// the build flagged) reads row 0 with weight 0, so that the loads are issued
+// without branches.
 template <bool BF16, int LPR>
 __global__ void __launch_bounds__(kBlock)
 k_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64_t m,
         const void* __restrict__ vals, int64_t ld_vals, int C, float* __restrict__ out, unsigned nblk) {
   using Ch = Chunk<BF16>;
+  constexpr int PP = 2;
   const int lane = threadIdx.x & (LPR - 1);
-  const int64_t p = xcd_item<LPR>(nblk);
-  if (p >= m) return;
-  const int4 iv = idx[p];
-  const float4 wv = w[p];
-  const int32_t vi[4] = {iv.x, iv.y, iv.z, iv.w};
-  const float bw[4] = {wv.x, wv.y, wv.z, wv.w};
+  const int64_t p0 = PP * xcd_item<LPR>(nblk);
+  if (p0 >= m) return;
+  int32_t vi[PP][4];
+  float bw[PP][4];
+#pragma unroll
+  for (int u = 0; u < PP; ++u) {
+    const int64_t p = min(p0 + u, m - 1);
+    const int4 iv = idx[p];
+    const float4 wv = w[p];
+    vi[u][0] = max(iv.x, 0); vi[u][1] = max(iv.y, 0); vi[u][2] = max(iv.z, 0); vi[u][3] = max(iv.w, 0);
+    bw[u][0] = iv.x < 0 ? 0.f : wv.x;
+    bw[u][1] = iv.y < 0 ? 0.f : wv.y;
+    bw[u][2] = iv.z < 0 ? 0.f : wv.z;
+    bw[u][3] = iv.w < 0 ? 0.f : wv.w;
+  }
   const int nchunk = C / Ch::N;
   for (int ch = lane; ch < nchunk; ch += LPR) {
-    float acc[Ch::N];
+    Ch x[PP][4];
 #pragma unroll
-    for (int i = 0; i < Ch::N; ++i) acc[i] = 0.f;
+    for (int u = 0; u < PP; ++u)
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (vi[k] < 0) continue;
-      Ch x;
-      x.load(vals, static_cast<int64_t>(vi[k]) * ld_vals + static_cast<int64_t>(ch) * Ch::N);
+      for (int k = 0; k < 4; ++k)
+        x[u][k].load(vals, static_cast<int64_t>(vi[u][k]) * ld_vals + static_cast<int64_t>(ch) * Ch::N);
 #pragma unroll
-      for (int i = 0; i < Ch::N; ++i) acc[i] += bw[k] * x.v[i];
+    for (int u = 0; u < PP; ++u) {
+      if (p0 + u >= m) break;
+      float acc[Ch::N];
+#pragma unroll
+      for (int i = 0; i < Ch::N; ++i) acc[i] = 0.f;
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int i = 0; i < Ch::N; ++i) acc[i] += bw[u][k] * x[u][k].v[i];
+      float* o = out + (p0 + u) * C + static_cast<int64_t>(ch) * Ch::N;
+#pragma unroll
+      for (int i = 0; i < Ch::N; i += 4)
+        *reinterpret_cast<float4*>(o + i) = make_float4(acc[i], acc[i + 1], acc[i + 2], acc[i + 3]);
     }
-    float* o = out + p * C + static_cast<int64_t>(ch) * Ch::N;
-#pragma unroll
-    for (int i = 0; i < Ch::N; i += 4)
-      *reinterpret_cast<float4*>(o + i) = make_float4(acc[i], acc[i + 1], acc[i + 2], acc[i + 3]);
   }
 }
 
@@ -792,7 +816,7 @@ template <bool BF16, int LPR, int Q>
 void splat_launch(const int32_t* off, const int32_t* ent, const float* ew, const int32_t* cf, int chunk, int64_t n, int64_t total,
                   const void* feat, int64_t ldf, int C, int norm, void* vals, int64_t ldv, float* wsum,
                   float* ph, float* pt, float* pw, hipStream_t s) {
-  constexpr int B = (BF16 ? 8 : 16) / Q;
+  constexpr int B = 8 / Q;   // entries in flight per lane group (more would cost occupancy)
   constexpr int G = kBlock / LPR;
   const int64_t span_len = static_cast<int64_t>(G) * chunk;
   const int64_t nspans = (total + span_len - 1) / span_len;
@@ -879,7 +903,7 @@ void deform_bwd_point_dispatch(int lpr, unsigned grid, const int32_t* idx, const
 template <bool BF16>
 void slice_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, const void* vals,
                     int64_t ldv, int C, float* out, hipStream_t s) {
-  const unsigned nblk = grid_for(m, lpr);
+  const unsigned nblk = grid_for((m + 1) / 2, lpr);   // two points per lane group
   const dim3 g(xcd_grid(nblk)), b(kBlock);
   const int4* i4 = reinterpret_cast<const int4*>(idx);
   const float4* w4 = reinterpret_cast<const float4*>(w);
