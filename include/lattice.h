@@ -95,7 +95,11 @@ int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_ho
  * with elevated positions halved, and a table mapping each coarse vertex c
  * and tap t to the fine vertex at 2c + o_t.  The coarse handle refers to
  * `fine`, which must outlive it (destroying a parent with live children
- * returns LAT_ELEVEL).
+ * returns LAT_ELEVEL).  The coarse level builds its point lists J_v and
+ * per-point simplices on the stream of the first operator that reads them
+ * (splat, slice, their backward passes, DeformSlice, Distribute, the
+ * simplex export); the convolutions need only its tables.  Work on other
+ * streams that uses the handle must be ordered after that call.
  */
 int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, lattice_t* coarse);
 

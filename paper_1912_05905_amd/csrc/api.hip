@@ -260,6 +260,15 @@ struct lattice_s {
   int32_t* up = nullptr;         // 9 x parent->nmax table from the parent into this level
   int32_t* up_rows = nullptr;    // parent vertices, grouped by the tap mask of their up row
   int64_t retry_cap = 0;          // coarse levels: table size of a rebuild after overflow
+  // A coarse level builds its vertex lists J_v (and the per-point vertex
+  // indices) only when an operator first needs them: the convolutions only
+  // need the tables.  Until then it keeps what the list build reads.
+  bool lists_ready = true;
+  int32_t* slot_count = nullptr;  // per table slot: references
+  int32_t* vslot = nullptr;       // per vertex: its slot
+  int32_t* slot = nullptr;        // per reference: slot of its vertex
+  int32_t* rank = nullptr;        // per reference: rank within its vertex
+  void* scan_work = nullptr;      // status words of the count scan (cleared by the build)
 
   HashView hash() const { return HashView{table, static_cast<uint64_t>(cap - 1)}; }
 
@@ -396,35 +405,72 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
     ALLOC(up, int32_t, kTaps * parent->nmax);
     ALLOC(up_rows, int32_t, parent->nmax);
   }
+  // the finest level builds its lists now (splat needs them); a coarse level
+  // keeps the inputs of its list build in buffers of its own
+  const bool defer_lists = parent != nullptr;
+  Scratch t_slot_count, t_vslot, t_slot, t_rank, t_work;
+  int32_t *slot_count, *vslot, *slot, *rank;
+  void* work;
+  if (defer_lists) {
+    ALLOC(slot_count, int32_t, cap);
+    ALLOC(vslot, int32_t, nmax);
+    ALLOC(slot, int32_t, refs);
+    ALLOC(rank, int32_t, refs);
+    if ((st = L->alloc(static_cast<size_t>(scan_workspace_bytes()), s, &p)) != LAT_OK) return st;
+    L->scan_work = p;
+    slot_count = L->slot_count;
+    vslot = L->vslot;
+    slot = L->slot;
+    rank = L->rank;
+    work = L->scan_work;
+  } else {
+    if ((st = t_slot_count.get(sizeof(int32_t) * cap, s)) != LAT_OK) return st;
+    if ((st = t_vslot.get(sizeof(int32_t) * nmax, s)) != LAT_OK) return st;
+    if ((st = t_slot.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
+    if ((st = t_rank.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
+    if ((st = t_work.get(scan_workspace_bytes(), s)) != LAT_OK) return st;
+    slot_count = t_slot_count.as<int32_t>();
+    vslot = t_vslot.as<int32_t>();
+    slot = t_slot.as<int32_t>();
+    rank = t_rank.as<int32_t>();
+    work = t_work.p;
+  }
 #undef ALLOC
-  Scratch slot_count, vslot, slot, rank, work;
-  if ((st = slot_count.get(sizeof(int32_t) * cap, s)) != LAT_OK) return st;
-  if ((st = vslot.get(sizeof(int32_t) * nmax, s)) != LAT_OK) return st;
-  if ((st = slot.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
-  if ((st = rank.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
-  if ((st = work.get(scan_workspace_bytes(), s)) != LAT_OK) return st;
   if (!L->host_dc && !(L->host_dc = HostSlots::get().take())) return fail(LAT_ENOMEM, "pinned host slot");
   if (!L->counts_ready && !(L->counts_ready = HostSlots::get().take_event()))
     return fail(LAT_EDEVICE, "event creation failed");
 
   int32_t* host_counts = nullptr;  // device view of the pinned landing slot
   HIP_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&host_counts), L->host_dc, 0));
-  launch_clear_table(L->table, slot_count.as<int32_t>(), cap, L->dc, work.p, s);
-  launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], m, L->hash(),
-                       &L->dc->counter, slot_count.as<int32_t>(), L->vkeys, vslot.as<int32_t>(),
-                       slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->y, &L->dc->err, host_counts, s);
+  launch_clear_table(L->table, slot_count, cap, L->dc, work, s);
+  launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], m, L->hash(), &L->dc->counter, slot_count, L->vkeys,
+                       vslot, slot, rank, L->w, L->y, &L->dc->err, host_counts, s);
   HIP_TRY(hipEventRecord(L->counts_ready, s));
   L->counts_known = false;
   const int32_t* n_dev = &L->dc->counter;
-  launch_count_scan(slot_count.as<int32_t>(), vslot.as<int32_t>(), n_dev, L->offsets, work.p, s);
-  launch_fill_lists(L->hash(), slot.as<int32_t>(), rank.as<int32_t>(), L->w, L->offsets, L->idx,
-                    L->entries, L->entry_w, L->chunk_first, L->chunk, refs, s);
+  L->lists_ready = !defer_lists;
+  if (!defer_lists) {
+    launch_count_scan(slot_count, vslot, n_dev, L->offsets, work, s);
+    launch_fill_lists(L->hash(), slot, rank, L->w, L->offsets, L->idx, L->entries, L->entry_w, L->chunk_first,
+                      L->chunk, refs, s);
+  }
   if (parent)
     launch_coarse_tables(L->hash(), parent->hash(), L->vkeys, parent->vkeys, n_dev, &parent->dc->counter, nmax,
                          parent->nmax, L->nbr, L->down, L->up, L->up_rows, s);
   else
     launch_neighbor_table(L->hash(), L->vkeys, n_dev, nmax, L->nbr, nmax, s);
   return check_launch("lattice build");
+}
+
+// The vertex lists J_v and the per-point vertex indices of a coarse level,
+// built on first use (on the stream of the operator that needs them).
+int ensure_lists(lattice_s* L, hipStream_t s) {
+  if (L->lists_ready) return LAT_OK;
+  launch_count_scan(L->slot_count, L->vslot, &L->dc->counter, L->offsets, L->scan_work, s);
+  launch_fill_lists(L->hash(), L->slot, L->rank, L->w, L->offsets, L->idx, L->entries, L->entry_w, L->chunk_first,
+                    L->chunk, L->total, s);
+  L->lists_ready = true;
+  return check_launch("lattice lists");
 }
 
 // Table size for a build: the caller's hint, else 2 slots per point for
@@ -715,6 +761,7 @@ int lattice_export_keys(lattice_t L, int32_t* keys_dev, hipStream_t stream) {
 int lattice_export_simplices(lattice_t L, int32_t* idx_dev, float* w_dev, hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (L->m == 0) return LAT_OK;
   if (!idx_dev || !w_dev) return fail(LAT_EINVAL, "idx / w is null");
   HIP_TRY(hipMemcpyAsync(idx_dev, L->idx, sizeof(int32_t) * 4 * L->m, hipMemcpyDeviceToDevice, stream));
@@ -735,6 +782,7 @@ int lattice_splat(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat
                   int normalize, void* vals_dev, int64_t ld_vals, float* wsum_dev, hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_feat == 0) ld_feat = C;
   if (ld_vals == 0) ld_vals = C;
@@ -811,6 +859,7 @@ int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* 
                                 float* out_dev, int64_t ld_out, hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (Cf < 0 || Cf > distribute_max_features())
     return fail(LAT_EUNSUPPORTED, "Cf must be in [0, " + std::to_string(distribute_max_features()) + "]");
   for (int c : {C1, C2, C3})
@@ -837,6 +886,7 @@ int lattice_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat
                   float* out_dev, hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_vals == 0) ld_vals = C;
   if ((st = check_matrix(vals_dev, ld_vals, C, dt, "vals", L->n > 0)) != LAT_OK) return st;
@@ -850,6 +900,7 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
                          hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_vals == 0) ld_vals = C;
   if ((st = check_matrix(vals_dev, ld_vals, C, dt, "vals", L->n > 0)) != LAT_OK) return st;
@@ -870,6 +921,7 @@ int lattice_deform_slice_classify(lattice_t L, const void* vals_dev, int64_t ld_
                                   float* logits_dev, hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_vals == 0) ld_vals = C;
   if ((st = check_matrix(vals_dev, ld_vals, C, dt, "vals", L->n > 0)) != LAT_OK) return st;
@@ -893,6 +945,7 @@ int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int 
                            const float* wsum_dev, float* dF_dev, hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (ld_dX == 0) ld_dX = C;
   if ((st = check_matrix(dX_dev, ld_dX, C, LAT_F32, "dX", L->n > 0)) != LAT_OK) return st;
   if ((st = check_matrix(dF_dev, C, C, LAT_F32, "dF", L->m > 0)) != LAT_OK) return st;
@@ -916,6 +969,7 @@ int lattice_slice_backward(lattice_t L, const float* dOut_dev, int64_t ld_dOut, 
                            hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (ld_dOut == 0) ld_dOut = C;
   if (ld_dX == 0) ld_dX = C;
   if ((st = check_matrix(dOut_dev, ld_dOut, C, LAT_F32, "dOut", L->m > 0)) != LAT_OK) return st;
@@ -1014,6 +1068,7 @@ int lattice_deform_slice_backward(lattice_t L, const float* vals_dev, int64_t ld
                                   int64_t ld_dvals, float* dwv_dev, float* dbeta_dev, hipStream_t stream) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (ld_vals == 0) ld_vals = C;
   if (ld_dOut == 0) ld_dOut = C;
   if (ld_dvals == 0) ld_dvals = C;
