@@ -15,8 +15,11 @@
  *    stay valid until the work enqueued on the given stream has finished.
  *    Pointers named *_host are read before the call returns.
  *  - All calls enqueue work on `stream` and return without waiting, except
- *    lattice_num_vertices (and lattice_create / lattice_coarsen when the
- *    library has to learn n, which they do with one stream synchronisation).
+ *    the first call that needs the vertex count n of a lattice
+ *    (lattice_num_vertices, or an operator or export on it): it waits once
+ *    for the event that follows the lattice's insert kernel.
+ *    lattice_create, lattice_coarsen, lattice_num_points and lattice_level
+ *    never wait.
  *  - Matrices are row-major.  ld_* arguments are row strides in elements
  *    (0 = dense, i.e. the number of channels); they let several ops write
  *    disjoint column ranges of one buffer (channel concatenation).
@@ -28,8 +31,8 @@
  *  - Return value: LAT_OK (0) or a negative LAT_E* status.  Host-detectable
  *    errors return immediately with nothing enqueued.  Errors found on the
  *    device (hash full, coordinate range, non-finite positions) are reported
- *    by the next call that synchronises (lattice_create, lattice_coarsen,
- *    lattice_num_vertices); the handle is then poisoned and every later call
+ *    by the call that waits for that lattice's count (a coarse lattice also
+ *    reports its parent's); the handle is then poisoned and every later call
  *    on it returns the same status.  lattice_last_error() gives the text of
  *    the last non-OK status of the calling thread.
  *  - Handles are not thread-safe; distinct handles are independent.

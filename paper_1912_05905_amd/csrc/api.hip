@@ -1,6 +1,7 @@
 // liblattice C ABI: argument validation, handle lifetime, device memory and
 // kernel-family timing.  Every lattice operation is a hand-written kernel in
 // create.hip, splat_slice.hip or conv.hip; this file only orchestrates them.
+#include <atomic>
 #include <cmath>
 #include <cstddef>
 #include <cstdio>
@@ -222,10 +223,12 @@ struct DeviceCounters {
 static_assert(offsetof(DeviceCounters, done) == 4, "count and done share one aligned 64-bit word");
 
 // Pinned host landing slot, written by the last workgroup of the insert
-// kernel: [0] vertex count, [1] error bits.
+// kernel: [0] vertex count, [1] error bits, then [2] the stamp of the build.
 struct HostCounts {
   int32_t n;
   uint32_t err;
+  uint32_t stamp;
+  uint32_t pad;
 };
 
 struct lattice_s {
@@ -260,6 +263,9 @@ struct lattice_s {
   int32_t* up = nullptr;         // 9 x parent->nmax table from the parent into this level
   int32_t* up_rows = nullptr;    // parent vertices, grouped by the tap mask of their up row
   int64_t retry_cap = 0;          // coarse levels: table size of a rebuild after overflow
+  uint32_t stamp = 0;             // stamp of the current build's count readback
+  uint64_t generation = 0;        // rebuilds of this handle after an overflow
+  uint64_t parent_generation = 0; // the parent's generation this level was built from
   // A coarse level builds its vertex lists J_v (and the per-point vertex
   // indices) only when an operator first needs them: the convolutions only
   // need the tables.  Until then it keeps what the list build reads.
@@ -442,10 +448,13 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
 
   int32_t* host_counts = nullptr;  // device view of the pinned landing slot
   HIP_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&host_counts), L->host_dc, 0));
+  static std::atomic<uint32_t> g_stamp{0};
+  L->stamp = m > 0 ? ++g_stamp : 0;
+  L->host_dc->stamp = ~L->stamp;
   launch_clear_table(L->table, slot_count, cap, L->dc, work, s);
   launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], m, L->hash(), &L->dc->counter, slot_count, L->vkeys,
-                       vslot, slot, rank, L->w, L->y, &L->dc->err, host_counts, s);
-  HIP_TRY(hipEventRecord(L->counts_ready, s));
+                       vslot, slot, rank, L->w, L->y, &L->dc->err, host_counts, L->stamp, L->counts_ready, s);
+  HIP_TRY(hipGetLastError());
   L->counts_known = false;
   const int32_t* n_dev = &L->dc->counter;
   L->lists_ready = !defer_lists;
@@ -483,14 +492,49 @@ int64_t initial_capacity(const lattice_s* L, const lattice_s* parent, int64_t ca
   const int64_t full = next_pow2(std::max<int64_t>(1024, 2 * refs));
   if (capacity_hint > 0) return next_pow2(std::max<int64_t>(1024, 2 * std::min(capacity_hint, refs)));
   if (parent && parent->counts_known) return std::min(full, next_pow2(std::max<int64_t>(1024, 2 * parent->n)));
-  if (!parent) return std::min(full, next_pow2(std::max<int64_t>(1024, 2 * L->m)));
-  return full;
+  // a finest level, or a coarse one whose parent's count is not read back
+  // yet: 2 slots per point (a coarse level has at most about as many
+  // vertices as its parent)
+  return std::min(full, next_pow2(std::max<int64_t>(1024, 2 * L->m)));
 }
 
 // Wait for a handle's counter readback; report device-side errors.
 int ensure_counts(lattice_s* L) {
   if (L->counts_known) return L->status;
+  if (L->parent) {
+    // A coarse level is enqueued without waiting for its parent: the
+    // parent's errors poison it, and a parent rebuilt after an overflow
+    // (new vertex numbering) means this level is rebuilt from it as well.
+    lattice_s* P = L->parent;
+    const int pst = ensure_counts(P);
+    if (pst != LAT_OK) {
+      HIP_TRY(hipEventSynchronize(L->counts_ready));
+      L->counts_known = true;
+      L->status = pst;
+      return fail(pst, "the lattice this one was coarsened from failed to build");
+    }
+    if (P->generation != L->parent_generation) {
+      L->free_all();
+      L->parent_generation = P->generation;
+      const float a[3] = {0.f, 0.f, 0.f};
+      const int st = enqueue_build(L, nullptr, P->y, 0.5f, a, P, initial_capacity(L, P, 0), L->stream);
+      if (st != LAT_OK) {
+        L->status = st;
+        return st;
+      }
+      ++L->generation;  // its own coarser levels were built from the old numbering
+    }
+  }
   HIP_TRY(hipEventSynchronize(L->counts_ready));
+  if (L->m > 0 && static_cast<volatile HostCounts*>(L->host_dc)->stamp != L->stamp) {
+    // the readback must belong to this build; wait for the whole stream once
+    HIP_TRY(hipStreamSynchronize(L->stream));
+    if (static_cast<volatile HostCounts*>(L->host_dc)->stamp != L->stamp) {
+      L->status = LAT_EDEVICE;
+      return fail(LAT_EDEVICE, "vertex count readback missing after the build finished");
+    }
+  }
+  std::atomic_thread_fence(std::memory_order_acquire);
   L->counts_known = true;
   L->n = L->host_dc->n;
   const int dev_status = status_from_err_bits(L->host_dc->err);
@@ -512,6 +556,7 @@ int ensure_counts(lattice_s* L) {
     const float* src = L->parent ? L->parent->y : static_cast<const float*>(old_y.p);
     int st = enqueue_build(L, nullptr, src, L->parent ? 0.5f : 1.0f, a, L->parent, cap, L->stream);
     Pool::get().release(old_y.p, old_y.bytes, L->stream);
+    ++L->generation;
     if (st != LAT_OK) { L->status = st; return st; }
     return ensure_counts(L);
   }
@@ -536,6 +581,13 @@ int build_lattice(lattice_s* L, const float* pos, const float a[3], const lattic
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// A handle not known to be poisoned; does not wait for its build.
+int check_handle_nowait(const lattice_s* L) {
+  if (!L) return fail(LAT_EINVAL, "null lattice handle");
+  if (L->status != LAT_OK) return fail(L->status, "lattice handle is poisoned by an earlier error");
+  return LAT_OK;
+}
 
 // A usable handle: not null, its vertex count read back, no device error.
 int check_handle(lattice_s* L) {
@@ -693,12 +745,13 @@ int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, l
   if (!coarse) return fail(LAT_EINVAL, "out is null");
   *coarse = nullptr;
   int st;
-  if ((st = check_handle(fine)) != LAT_OK) return st;
+  if ((st = check_handle_nowait(fine)) != LAT_OK) return st;
   if (capacity_hint < 0) return fail(LAT_EINVAL, "capacity_hint < 0");
   lattice_s* L = new lattice_s();
   L->m = fine->m;
   L->level = fine->level + 1;
   L->parent = fine;
+  L->parent_generation = fine->generation;
   L->stream = stream;
   const float a[3] = {0.f, 0.f, 0.f};
   st = build_lattice(L, nullptr, a, fine, capacity_hint, stream);
@@ -736,7 +789,7 @@ int lattice_num_vertices(lattice_t L, int64_t* n) {
 int lattice_num_points(lattice_t L, int64_t* m) {
   int st;
   if (!m) return fail(LAT_EINVAL, "m is null");
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = check_handle_nowait(L)) != LAT_OK) return st;
   *m = L->m;
   return LAT_OK;
 }
@@ -744,7 +797,7 @@ int lattice_num_points(lattice_t L, int64_t* m) {
 int lattice_level(lattice_t L, int* level) {
   int st;
   if (!level) return fail(LAT_EINVAL, "level is null");
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = check_handle_nowait(L)) != LAT_OK) return st;
   *level = L->level;
   return LAT_OK;
 }

@@ -10,7 +10,11 @@
 // merges its 1024 vertex references in an LDS hash table, then touches the
 // global table once per distinct key, adds its reference count for that key
 // with one atomic, and numbers all vertices it created with one atomic on
-// the vertex counter.
+// the vertex counter.  With one wave of workgroups the kernel's time is the
+// latency of that chain, so a thread probes for all of its distinct keys at
+// once (each probe a compare-and-swap, whose result also says whether the
+// slot holds the key) and leaves its count atomics in flight while the
+// workgroup numbers its new vertices.
 #pragma clang fp contract(off)
 
 #include <algorithm>
@@ -46,30 +50,6 @@ k_clear_table(HashEntry* __restrict__ entries, int32_t* __restrict__ counts, int
   }
   if (i == 0) *dev_counters = make_uint4(0u, 0u, 0u, 0u);
   if (i < kScanBlocks) scan_status[i] = 0ull;
-}
-
-// Global insert of a key; returns its slot (or -1 when the table is full)
-// and whether this call created it.
-__device__ inline int32_t global_insert(const HashView& h, uint64_t key, bool* created, uint32_t* err) {
-  *created = false;
-  uint64_t slot = hash_key(key) & h.mask;
-  for (uint64_t probe = 0; probe <= h.mask; ++probe) {
-    const uint64_t cur = h.e[slot].key;
-    if (cur == key) return static_cast<int32_t>(slot);
-    if (cur == kEmptyKey) {
-      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(&h.e[slot].key),
-                                      static_cast<unsigned long long>(kEmptyKey),
-                                      static_cast<unsigned long long>(key));
-      if (prev == kEmptyKey) {
-        *created = true;
-        return static_cast<int32_t>(slot);
-      }
-      if (prev == key) return static_cast<int32_t>(slot);
-    }
-    slot = (slot + 1) & h.mask;
-  }
-  atomicOr(err, kErrHashFull);
-  return -1;
 }
 
 // Exclusive prefix sum over the workgroup (wave shuffles, then the four
@@ -119,7 +99,7 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
                 int32_t* __restrict__ slot_count, uint64_t* __restrict__ vkeys,
                 int32_t* __restrict__ vslot, int4* __restrict__ slot_out, int4* __restrict__ rank_out,
                 float4* __restrict__ w_out, float4* __restrict__ y_out, uint32_t* err,
-                int32_t* __restrict__ host_counts) {
+                int32_t* __restrict__ host_counts, uint32_t stamp) {
   __shared__ uint64_t lkey[kLdsSlots];
   __shared__ int32_t lcount[kLdsSlots];
   __shared__ int32_t lslot[kLdsSlots];
@@ -137,12 +117,14 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
 
   const int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + tid;
   bool live = p < m;
+  bool raised = false;  // this thread set an error bit
   float y[kVerts] = {0.f, 0.f, 0.f, 0.f};
   if (live) {
     if (pos != nullptr) {
       const float g0 = pos[3 * p + 0], g1 = pos[3 * p + 1], g2 = pos[3 * p + 2];
       if (!isfinite(g0) || !isfinite(g1) || !isfinite(g2)) {
         atomicOr(err, kErrNonFinite);
+        raised = true;
         live = false;
       } else {
         const float t0 = g0 * a0, t1 = g1 * a1, t2 = g2 * a2;
@@ -173,6 +155,7 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
       if (!(fabsf(y[i]) < 2.0f * static_cast<float>(kCoordLimit))) ok = false;
     if (!ok) {
       atomicOr(err, isfinite(y[0] + y[1] + y[2] + y[3]) ? kErrKeyRange : kErrNonFinite);
+      raised = true;
       live = false;
     }
   }
@@ -233,7 +216,10 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
 #pragma unroll
       for (int i = 0; i < kVerts; ++i) c[i] = base[i] + k - (rank[i] > kDim - k ? kVerts : 0);
       if (coords_in_range(c[0], c[1], c[2], c[3])) keys[k] = pack_key(c[0], c[1], c[2]);
-      else atomicOr(err, kErrKeyRange);
+      else {
+        atomicOr(err, kErrKeyRange);
+        raised = true;
+      }
     }
   }
 
@@ -268,26 +254,61 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
     if (lkey[sl] != kEmptyKey) ulist[at++] = sl;
   }
   __syncthreads();
+  // a thread's distinct keys: u = tid + j * kBlock, j < kVerts (nunique is
+  // at most kBlock * kVerts)
+  int32_t usl[kVerts], gsl[kVerts];
+  uint64_t ukey[kVerts], probe_at[kVerts];
+  uint32_t pending = 0;
+#pragma unroll
+  for (int j = 0; j < kVerts; ++j) {
+    const int u = tid + j * kBlock;
+    usl[j] = u < nunique ? ulist[u] : 0;
+    ukey[j] = lkey[usl[j]];
+    probe_at[j] = hash_key(ukey[j]) & h.mask;
+    gsl[j] = -1;
+    if (u < nunique) pending |= 1u << j;
+  }
   uint32_t created_mask = 0;
-  int32_t ncreated = 0;
-  for (int u = tid, j = 0; u < nunique; u += kBlock, ++j) {
-    const int sl = ulist[u];
-    bool created = false;
-    const int32_t gs = global_insert(h, lkey[sl], &created, err);
-    lslot[sl] = gs;
-    lbase[sl] = gs >= 0 ? atomicAdd(&slot_count[gs], lcount[sl]) : 0;
-    if (created) {
-      created_mask |= 1u << j;
-      ++ncreated;
+  for (uint64_t probe = 0; pending != 0 && probe <= h.mask; ++probe) {
+    uint64_t prev[kVerts];
+#pragma unroll
+    for (int j = 0; j < kVerts; ++j)
+      if (pending & (1u << j))
+        prev[j] = atomicCAS(reinterpret_cast<unsigned long long*>(&h.e[probe_at[j]].key),
+                            static_cast<unsigned long long>(kEmptyKey), static_cast<unsigned long long>(ukey[j]));
+#pragma unroll
+    for (int j = 0; j < kVerts; ++j) {
+      if (!(pending & (1u << j))) continue;
+      if (prev[j] == kEmptyKey || prev[j] == ukey[j]) {
+        gsl[j] = static_cast<int32_t>(probe_at[j]);
+        if (prev[j] == kEmptyKey) created_mask |= 1u << j;
+        pending &= ~(1u << j);
+      } else {
+        probe_at[j] = (probe_at[j] + 1) & h.mask;
+      }
     }
   }
+  if (pending) {
+    atomicOr(err, kErrHashFull);
+    raised = true;
+  }
+  // an error bit must have landed before this workgroup counts as finished
+  if (raised) __threadfence();
+  // reference counts: the returned bases are first needed after the
+  // numbering below, so these atomics overlap it
+  int32_t gbase[kVerts];
+#pragma unroll
+  for (int j = 0; j < kVerts; ++j)
+    gbase[j] = gsl[j] >= 0 ? atomicAdd(&slot_count[gsl[j]], lcount[usl[j]]) : 0;
+  const int32_t ncreated = __builtin_popcount(created_mask);
   int32_t nblock = 0;
   const int32_t my_first = block_exclusive_sum(ncreated, scan_buf, &nblock);
   // One 64-bit atomic per workgroup claims the numbers of its new vertices
   // (low word: the vertex count) and counts the workgroup as finished with
   // its inserts (high word); the last one copies the count and the error
   // bits into pinned host memory (read by the host after an event).  Error
-  // bits are set with atomics before this point in every workgroup.
+  // bits are set with atomics, and fenced, before this point in every
+  // workgroup.
   if (tid == 0) {
     const unsigned long long old =
         __hip_atomic_fetch_add(reinterpret_cast<unsigned long long*>(counter),
@@ -298,17 +319,22 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
       host_counts[0] = id_base + nblock;
       host_counts[1] = static_cast<int32_t>(__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
       __threadfence_system();
+      host_counts[2] = static_cast<int32_t>(stamp);  // the build this readback belongs to
+      __threadfence_system();
     }
   }
   __syncthreads();
   int32_t id = id_base + my_first;
-  for (int u = tid, j = 0; u < nunique; u += kBlock, ++j) {
+#pragma unroll
+  for (int j = 0; j < kVerts; ++j) {
+    if (tid + j * kBlock < nunique) {
+      lslot[usl[j]] = gsl[j];
+      lbase[usl[j]] = gbase[j];
+    }
     if (!(created_mask & (1u << j))) continue;
-    const int sl = ulist[u];
-    const int32_t gs = lslot[sl];
-    h.e[gs].val = id;
-    vkeys[id] = lkey[sl];
-    vslot[id] = gs;
+    h.e[gsl[j]].val = id;
+    vkeys[id] = ukey[j];
+    vslot[id] = gsl[j];
     ++id;
   }
   __syncthreads();
@@ -597,14 +623,18 @@ void launch_clear_table(HashEntry* keys, int32_t* counts, int64_t cap, void* dev
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
                           float a2, int64_t m, HashView h, int32_t* counter, int32_t* slot_count,
                           uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
-                          float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, hipStream_t s) {
-  if (m <= 0) return;
+                          float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, uint32_t stamp,
+                          hipEvent_t done, hipStream_t s) {
+  if (m <= 0) {
+    (void)hipEventRecord(done, s);
+    return;
+  }
   ScopedKernelTimer tm("insert", s);
-  launch(k_insert_points, dim3(blocks_for(m)), dim3(kBlock), 0, s, pos,
+  launch_signal(k_insert_points, dim3(blocks_for(m)), dim3(kBlock), 0, s, done, pos,
                      reinterpret_cast<const float4*>(y_in), y_scale, a0, a1, a2, m, h, counter,
                      slot_count, vkeys, vslot, reinterpret_cast<int4*>(slot_out),
                      reinterpret_cast<int4*>(rank_out), reinterpret_cast<float4*>(w_out),
-                     reinterpret_cast<float4*>(y_out), err, host_counts);
+                     reinterpret_cast<float4*>(y_out), err, host_counts, stamp);
 }
 
 int64_t scan_workspace_bytes() { return kScanBlocks * sizeof(uint64_t); }

@@ -114,13 +114,29 @@ struct ScopedKernelTimer {
   ~ScopedKernelTimer() { timer_end(); }
 };
 
+// Timed launches bind their events to the kernel's own dispatch
+// (hipExtLaunchKernel), so timing adds no marker packets between kernels.
 template <typename K, typename... Args>
 inline void launch(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  const bool timed = timer_take_events(&e0, &e1);
-  if (timed) (void)hipEventRecord(e0, s);
-  hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
-  if (timed) (void)hipEventRecord(e1, s);
+  if (timer_take_events(&e0, &e1))
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, e0, e1, 0u, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+}
+
+// A launch whose completion also completes `done` (bound to the dispatch;
+// a separate event record only when the launch is timed as well).
+template <typename K, typename... Args>
+inline void launch_signal(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, hipEvent_t done,
+                          Args... args) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (timer_take_events(&e0, &e1)) {
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, e0, e1, 0u, args...);
+    (void)hipEventRecord(done, s);
+  } else {
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, static_cast<hipEvent_t>(nullptr), done, 0u, args...);
+  }
 }
 
 // Launchers (each .hip file implements its own kernels' launchers).
@@ -130,7 +146,8 @@ void launch_clear_table(HashEntry* entries, int32_t* counts, int64_t cap, void* 
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
                           float a2, int64_t m, HashView h, int32_t* counter, int32_t* slot_count,
                           uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
-                          float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, hipStream_t s);
+                          float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, uint32_t stamp,
+                          hipEvent_t done, hipStream_t s);
 int64_t scan_workspace_bytes();
 void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, const int32_t* n_dev,
                        int32_t* offsets, void* work, hipStream_t s);

@@ -129,20 +129,59 @@ def test_device_errors(L):
     pos = _cloud(5, 1000)
     bad = pos.copy()
     bad[17, 1] = np.nan
+    # creation does not wait: the error comes with the first read of n
+    gl = L.Lattice.create(_dev(bad), [0.1] * 3)
     with pytest.raises(L.LatticeError) as e:
-        L.Lattice.create(_dev(bad), [0.1] * 3)
+        gl.n
     assert e.value.status == -6
     far = pos.copy()
     far[3] = [1e6, 0, 0]
     with pytest.raises(L.LatticeError) as e:
-        L.Lattice.create(_dev(far), [0.1] * 3)
+        L.Lattice.create(_dev(far), [0.1] * 3).n
     assert e.value.status == -5
+    # a coarse level enqueued from a failed one reports the parent's error,
+    # and so does every later call on the parent
+    gl = L.Lattice.create(_dev(_cloud(6, 5000)), [0.01] * 3, capacity_hint=16)
+    gc = gl.coarsen()
     with pytest.raises(L.LatticeError) as e:
-        L.Lattice.create(_dev(_cloud(6, 5000)), [0.01] * 3, capacity_hint=16)
+        gc.n
+    assert e.value.status == -4
+    with pytest.raises(L.LatticeError) as e:
+        gl.keys()
     assert e.value.status == -4
     # the library stays usable after device-side errors
     ok = L.Lattice.create(_dev(pos), [0.1] * 3)
     assert ok.n > 0
+
+
+def test_overflow_rebuild_of_a_hierarchy(L, O):
+    """Points far apart on the lattice's scale: nearly 4 vertices per point
+    overflow the table sized from the point count.  The coarse levels are
+    enqueued before the fine level's count is read back, so each is built
+    from a table that overflowed; the first read rebuilds the fine level,
+    then each coarse level from the rebuilt one.  Structure and the
+    strided / transposed convolutions must match the oracle."""
+    pos = _cloud(71, 3000, 1.0)
+    sigma = 0.002
+    g0 = L.Lattice.create(_dev(pos), [sigma] * 3)
+    g1 = g0.coarsen()
+    g2 = g1.coarsen()
+    o0 = O.Lattice.create(pos, np.full(3, sigma, np.float32))
+    o1 = o0.coarsen()
+    o2 = o1.coarsen()
+    assert o0.n > 2 * 3000 * 1.3          # beyond the first table's reach
+    g2o = [_check_structure(g, o) for g, o in ((g2, o2), (g1, o1), (g0, o0))][::-1]
+    rng = np.random.default_rng(12)
+    for (gf, of, pf), (gc, oc, pc) in (((g0, o0, g2o[0]), (g1, o1, g2o[1])), ((g1, o1, g2o[1]), (g2, o2, g2o[2]))):
+        Xf = rng.normal(size=(of.n, 16))
+        Wd = _rand_w(rng, 16, 32, 1.0 / 12)
+        gy = gc.conv(gf, _dev(Xf[pf].astype(np.float32)), _gpu_w(Wd.astype(np.float32), torch.float32))
+        P.assert_close(P.rows_in_oracle_order(_host(gy), pc), oc.conv(of, Xf, Wd), P.TOL_F32, "strided conv")
+        Xc = rng.normal(size=(oc.n, 32))
+        Wu = _rand_w(rng, 32, 16, 1.0 / 12)
+        gz = gf.refine(gc, _dev(Xc[pc].astype(np.float32)), _gpu_w(Wu.astype(np.float32), torch.float32))
+        P.assert_close(P.rows_in_oracle_order(_host(gz), pf), of.refine_into(oc, Xc, Wu), P.TOL_F32,
+                       "transposed conv")
 
 
 def test_host_validation_on_gpu(L):
