@@ -1,6 +1,7 @@
 // liblattice C ABI: argument validation, handle lifetime, device memory and
 // kernel-family timing.  Every lattice operation is a hand-written kernel in
 // create.hip, splat_slice.hip or conv.hip; this file only orchestrates them.
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstddef>
@@ -112,6 +113,15 @@ class Pool {
     if (hipGetDevice(&dev) != hipSuccess) return;
     std::lock_guard<std::mutex> lk(mu_);
     free_[{dev, size_class(bytes)}].push_back(Block{p, bytes, s});
+    ++releases_[s];
+  }
+
+  // Number of releases to stream s so far (a block released later may still
+  // have uses pending on s).
+  uint64_t release_count(hipStream_t s) {
+    std::lock_guard<std::mutex> lk(mu_);
+    auto it = releases_.find(s);
+    return it == releases_.end() ? 0 : it->second;
   }
 
  private:
@@ -127,6 +137,7 @@ class Pool {
 
   std::mutex mu_;
   std::map<std::pair<int, size_t>, std::vector<Block>> free_;
+  std::map<hipStream_t, uint64_t> releases_;
 };
 
 // ---------------------------------------------------------------------------
@@ -245,7 +256,12 @@ struct lattice_s {
   int status = LAT_OK;           // poisoned when != LAT_OK
   int children = 0;
   lattice_s* parent = nullptr;
-  hipStream_t stream = nullptr;  // stream the handle's buffers were produced on
+  hipStream_t stream = nullptr;  // the caller's stream: owner of the handle's buffers
+  hipStream_t bstream = nullptr;  // stream the build ran on (the library's side stream for a coarse level)
+  uint64_t side_seq = 0;          // built on the side stream: its build's number there (0: not)
+  hipEvent_t built = nullptr;     // side-stream build: completes with its last kernel
+  std::vector<hipStream_t> joined;  // streams already ordered after that build
+  uint64_t releases_at_insert = 0;  // owner pool's release count when the insert was enqueued
   std::vector<DevBuf> owned;
 
   float* y = nullptr;            // m x 4 elevated positions
@@ -284,11 +300,15 @@ struct lattice_s {
     return st;
   }
 
-  void free_all() {
-    if (!counts_known && counts_ready) (void)hipEventSynchronize(counts_ready);
-    for (auto& b : owned) Pool::get().release(b.p, b.bytes, stream);
-    owned.clear();
+  bool joined_by(hipStream_t s) const {
+    for (hipStream_t j : joined)
+      if (j == s) return true;
+    return false;
   }
+
+  // Buffers go back to the pool of the owner stream, which must first be
+  // ordered after a side-stream build.
+  void free_all();
 };
 
 namespace {
@@ -380,7 +400,7 @@ struct Scratch {
 // scan, the vertex lists and the tables, which take the vertex count from
 // device memory.  Nothing waits here.
 int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_scale, const float a[3],
-                  const lattice_s* parent, int64_t cap, hipStream_t s) {
+                  const lattice_s* parent, int64_t cap, hipStream_t s, hipEvent_t built = nullptr) {
   const int64_t m = L->m;
   const int64_t refs = 4 * m;
   const int64_t nmax = std::min(cap, refs);
@@ -389,11 +409,12 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   L->total = refs;
   L->chunk = refs >= 64 * 32768 ? 64 : (refs >= 32 * 32768 ? 32 : 16);
   const int64_t nchunks = (refs + L->chunk - 1) / L->chunk;
+  L->bstream = s;
   int st;
   void* p;
-#define ALLOC(field, type, count)                                                 \
-  if ((st = L->alloc(sizeof(type) * static_cast<size_t>(count), s, &p)) != LAT_OK) \
-    return st;                                                                    \
+#define ALLOC(field, type, count)                                                         \
+  if ((st = L->alloc(sizeof(type) * static_cast<size_t>(count), L->stream, &p)) != LAT_OK) \
+    return st;                                                                            \
   L->field = static_cast<type*>(p)
   ALLOC(y, float, 4 * m);
   ALLOC(idx, int32_t, refs);
@@ -411,36 +432,22 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
     ALLOC(up, int32_t, kTaps * parent->nmax);
     ALLOC(up_rows, int32_t, parent->nmax);
   }
-  // the finest level builds its lists now (splat needs them); a coarse level
-  // keeps the inputs of its list build in buffers of its own
+  // The finest level builds its lists now (splat needs them); a coarse level
+  // when an operator first needs them.  Either way the inputs of the list
+  // build are the handle's own buffers: a build releases nothing to the
+  // pool, so a coarse level can start after the finer level's insert.
   const bool defer_lists = parent != nullptr;
-  Scratch t_slot_count, t_vslot, t_slot, t_rank, t_work;
-  int32_t *slot_count, *vslot, *slot, *rank;
-  void* work;
-  if (defer_lists) {
-    ALLOC(slot_count, int32_t, cap);
-    ALLOC(vslot, int32_t, nmax);
-    ALLOC(slot, int32_t, refs);
-    ALLOC(rank, int32_t, refs);
-    if ((st = L->alloc(static_cast<size_t>(scan_workspace_bytes()), s, &p)) != LAT_OK) return st;
-    L->scan_work = p;
-    slot_count = L->slot_count;
-    vslot = L->vslot;
-    slot = L->slot;
-    rank = L->rank;
-    work = L->scan_work;
-  } else {
-    if ((st = t_slot_count.get(sizeof(int32_t) * cap, s)) != LAT_OK) return st;
-    if ((st = t_vslot.get(sizeof(int32_t) * nmax, s)) != LAT_OK) return st;
-    if ((st = t_slot.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
-    if ((st = t_rank.get(sizeof(int32_t) * refs, s)) != LAT_OK) return st;
-    if ((st = t_work.get(scan_workspace_bytes(), s)) != LAT_OK) return st;
-    slot_count = t_slot_count.as<int32_t>();
-    vslot = t_vslot.as<int32_t>();
-    slot = t_slot.as<int32_t>();
-    rank = t_rank.as<int32_t>();
-    work = t_work.p;
-  }
+  ALLOC(slot_count, int32_t, cap);
+  ALLOC(vslot, int32_t, nmax);
+  ALLOC(slot, int32_t, refs);
+  ALLOC(rank, int32_t, refs);
+  if ((st = L->alloc(static_cast<size_t>(scan_workspace_bytes()), L->stream, &p)) != LAT_OK) return st;
+  L->scan_work = p;
+  int32_t* slot_count = L->slot_count;
+  int32_t* vslot = L->vslot;
+  int32_t* slot = L->slot;
+  int32_t* rank = L->rank;
+  void* work = L->scan_work;
 #undef ALLOC
   if (!L->host_dc && !(L->host_dc = HostSlots::get().take())) return fail(LAT_ENOMEM, "pinned host slot");
   if (!L->counts_ready && !(L->counts_ready = HostSlots::get().take_event()))
@@ -454,6 +461,7 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   launch_clear_table(L->table, slot_count, cap, L->dc, work, s);
   launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], m, L->hash(), &L->dc->counter, slot_count, L->vkeys,
                        vslot, slot, rank, L->w, L->y, &L->dc->err, host_counts, L->stamp, L->counts_ready, s);
+  L->releases_at_insert = Pool::get().release_count(L->stream);
   HIP_TRY(hipGetLastError());
   L->counts_known = false;
   const int32_t* n_dev = &L->dc->counter;
@@ -465,7 +473,7 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   }
   if (parent)
     launch_coarse_tables(L->hash(), parent->hash(), L->vkeys, parent->vkeys, n_dev, &parent->dc->counter, nmax,
-                         parent->nmax, L->nbr, L->down, L->up, L->up_rows, s);
+                         parent->nmax, L->nbr, L->down, L->up, L->up_rows, built, s);
   else
     launch_neighbor_table(L->hash(), L->vkeys, n_dev, nmax, L->nbr, nmax, s);
   return check_launch("lattice build");
@@ -498,6 +506,99 @@ int64_t initial_capacity(const lattice_s* L, const lattice_s* parent, int64_t ca
   return std::min(full, next_pow2(std::max<int64_t>(1024, 2 * L->m)));
 }
 
+// The library's own stream per device (default priority) on which coarse
+// levels are built, so that their construction overlaps the caller's work
+// on the finer levels.  Ordering with the callers' streams:
+//  - fork: a coarse build must start after the finer level's insert and
+//    after every earlier use of the pool blocks it allocates from the
+//    caller's stream.  When the finer level was built on the caller's
+//    stream and nothing was released to that stream's pool since its
+//    insert was enqueued, the side stream waits for the insert's own
+//    completion event; when the finer level is side-built and nothing was
+//    released since the last fork from this caller stream, no wait is
+//    needed; otherwise the side stream waits for the caller's stream as it
+//    is at that moment;
+//  - join: before a caller's stream touches a side-built level, it waits
+//    for the event that completes with that level's last build kernel.
+struct SideStream {
+  hipStream_t s = nullptr;
+  uint64_t seq = 0;                  // side builds enqueued
+  hipStream_t forked_from = nullptr; // caller stream of the last fork
+  uint64_t fork_releases = 0;        // its pool's release count at that fork
+  hipEvent_t ev[8] = {};             // fork / join events, used round-robin
+  int next_ev = 0;
+  std::vector<lattice_s*> live;      // side-built levels not yet destroyed
+  hipEvent_t event() { hipEvent_t e = ev[next_ev]; next_ev = (next_ev + 1) % 8; return e; }
+};
+std::mutex g_side_mu;
+
+int side_state(SideStream** out) {
+  static std::map<int, SideStream*> sides;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  auto it = sides.find(dev);
+  if (it == sides.end()) {
+    SideStream* st = new SideStream();  // lives until exit
+    HIP_TRY(hipStreamCreateWithFlags(&st->s, hipStreamNonBlocking));
+    for (auto& e : st->ev) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    it = sides.emplace(dev, st).first;
+  }
+  *out = it->second;
+  return LAT_OK;
+}
+
+// Order stream s after the side-stream build of L.
+int join_side(lattice_s* L, hipStream_t s) {
+  if (!L->side_seq || L->joined_by(s)) return LAT_OK;
+  HIP_TRY(hipStreamWaitEvent(s, L->built, 0));
+  L->joined.push_back(s);
+  return LAT_OK;
+}
+
+}  // namespace
+
+void lattice_s::free_all() {
+  if (!counts_known && counts_ready) (void)hipEventSynchronize(counts_ready);
+  if (side_seq && join_side(this, stream) != LAT_OK) (void)hipStreamSynchronize(bstream);
+  for (auto& b : owned) Pool::get().release(b.p, b.bytes, stream);
+  owned.clear();
+}
+
+namespace {
+
+// Before a handle's buffers are freed and rebuilt on its owner stream: no
+// side-stream work may still read them (its own build, or that of a coarser
+// level built from it).
+int settle_for_rebuild(lattice_s* L) {
+  SideStream* side = nullptr;
+  int st;
+  {
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    if ((st = side_state(&side)) != LAT_OK) return st;
+  }
+  HIP_TRY(hipStreamSynchronize(side->s));
+  HIP_TRY(hipStreamSynchronize(L->stream));
+  return LAT_OK;
+}
+
+// Leave the side stream's bookkeeping (rebuilt on the owner stream, or
+// destroyed).
+void leave_side(lattice_s* L) {
+  if (L->side_seq) {
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    SideStream* side = nullptr;
+    if (side_state(&side) == LAT_OK)
+      side->live.erase(std::remove(side->live.begin(), side->live.end(), L), side->live.end());
+  }
+  L->side_seq = 0;
+  L->joined.clear();
+  HostSlots::get().give_event(L->built);
+  L->built = nullptr;
+}
+
+// After a rebuild on the owner stream: later work there is ordered after it.
+void rebuilt_on_owner_stream(lattice_s* L) { leave_side(L); }
+
 // Wait for a handle's counter readback; report device-side errors.
 int ensure_counts(lattice_s* L) {
   if (L->counts_known) return L->status;
@@ -514,10 +615,13 @@ int ensure_counts(lattice_s* L) {
       return fail(pst, "the lattice this one was coarsened from failed to build");
     }
     if (P->generation != L->parent_generation) {
+      int st = settle_for_rebuild(L);
+      if (st != LAT_OK) return st;
       L->free_all();
+      rebuilt_on_owner_stream(L);
       L->parent_generation = P->generation;
       const float a[3] = {0.f, 0.f, 0.f};
-      const int st = enqueue_build(L, nullptr, P->y, 0.5f, a, P, initial_capacity(L, P, 0), L->stream);
+      st = enqueue_build(L, nullptr, P->y, 0.5f, a, P, initial_capacity(L, P, 0), L->stream);
       if (st != LAT_OK) {
         L->status = st;
         return st;
@@ -528,7 +632,7 @@ int ensure_counts(lattice_s* L) {
   HIP_TRY(hipEventSynchronize(L->counts_ready));
   if (L->m > 0 && static_cast<volatile HostCounts*>(L->host_dc)->stamp != L->stamp) {
     // the readback must belong to this build; wait for the whole stream once
-    HIP_TRY(hipStreamSynchronize(L->stream));
+    HIP_TRY(hipStreamSynchronize(L->bstream));
     if (static_cast<volatile HostCounts*>(L->host_dc)->stamp != L->stamp) {
       L->status = LAT_EDEVICE;
       return fail(LAT_EDEVICE, "vertex count readback missing after the build finished");
@@ -542,6 +646,8 @@ int ensure_counts(lattice_s* L) {
     // table sized from an estimate overflowed: rebuild at the worst case
     const int64_t cap = L->retry_cap;
     L->retry_cap = 0;
+    int st = settle_for_rebuild(L);
+    if (st != LAT_OK) return st;
     DevBuf old_y{};
     if (!L->parent) {
       for (size_t i = 0; i < L->owned.size(); ++i)
@@ -552,9 +658,10 @@ int ensure_counts(lattice_s* L) {
         }
     }
     L->free_all();
+    rebuilt_on_owner_stream(L);
     const float a[3] = {0.f, 0.f, 0.f};
     const float* src = L->parent ? L->parent->y : static_cast<const float*>(old_y.p);
-    int st = enqueue_build(L, nullptr, src, L->parent ? 0.5f : 1.0f, a, L->parent, cap, L->stream);
+    st = enqueue_build(L, nullptr, src, L->parent ? 0.5f : 1.0f, a, L->parent, cap, L->stream);
     Pool::get().release(old_y.p, old_y.bytes, L->stream);
     ++L->generation;
     if (st != LAT_OK) { L->status = st; return st; }
@@ -571,13 +678,13 @@ int ensure_counts(lattice_s* L) {
 }
 
 int build_lattice(lattice_s* L, const float* pos, const float a[3], const lattice_s* parent,
-                  int64_t capacity_hint, hipStream_t s) {
+                  int64_t capacity_hint, hipStream_t s, hipEvent_t built = nullptr) {
   const int64_t m = L->m;
   if (m == 0) return LAT_OK;
   if (4 * m > INT32_MAX) return fail(LAT_EUNSUPPORTED, "more than 2^29 points");
   const int64_t cap = initial_capacity(L, parent, capacity_hint);
   L->retry_cap = capacity_hint == 0 ? next_pow2(std::max<int64_t>(1024, 8 * m)) : 0;
-  return enqueue_build(L, pos, parent ? parent->y : nullptr, 0.5f, a, parent, cap, s);
+  return enqueue_build(L, pos, parent ? parent->y : nullptr, 0.5f, a, parent, cap, s, built);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -598,6 +705,14 @@ int check_handle(lattice_s* L) {
   }
   if (L->status != LAT_OK) return fail(L->status, "lattice handle is poisoned by an earlier error");
   return LAT_OK;
+}
+
+// A usable handle whose device data work on stream s may read: s is ordered
+// after the handle's build when that ran on the side stream.
+int use(lattice_s* L, hipStream_t s) {
+  int st;
+  if ((st = check_handle(L)) != LAT_OK) return st;
+  return join_side(L, s);
 }
 
 // channel count / stride / alignment rules of one feature matrix
@@ -754,8 +869,47 @@ int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, l
   L->parent_generation = fine->generation;
   L->stream = stream;
   const float a[3] = {0.f, 0.f, 0.f};
-  st = build_lattice(L, nullptr, a, fine, capacity_hint, stream);
+  // The build runs on the side stream (see SideStream), after the caller's
+  // stream as it is now; callers' later work is ordered after it by use().
+  SideStream* side = nullptr;
+  if (L->m > 0) {
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    if ((st = side_state(&side)) != LAT_OK) {
+      delete L;
+      return st;
+    }
+    const uint64_t rel = Pool::get().release_count(stream);
+    hipError_t e = hipSuccess;
+    if (fine->side_seq != 0 && side->forked_from == stream && side->fork_releases == rel) {
+      // ordered already: the finer level was built on the side stream
+    } else if (fine->side_seq == 0 && fine->bstream == stream && fine->releases_at_insert == rel) {
+      e = hipStreamWaitEvent(side->s, fine->counts_ready, 0);  // after the finer level's insert
+      side->forked_from = stream;
+      side->fork_releases = rel;
+    } else {
+      const hipEvent_t f = side->event();
+      e = hipEventRecord(f, stream);
+      if (e == hipSuccess) e = hipStreamWaitEvent(side->s, f, 0);
+      side->forked_from = stream;
+      side->fork_releases = rel;
+    }
+    L->built = HostSlots::get().take_event();
+    if (e != hipSuccess || !L->built) {
+      HostSlots::get().give_event(L->built);
+      delete L;
+      return fail(LAT_EDEVICE, "event record / stream wait failed");
+    }
+    st = build_lattice(L, nullptr, a, fine, capacity_hint, side->s, L->built);
+    if (st == LAT_OK) {
+      L->side_seq = ++side->seq;
+      side->live.push_back(L);
+    }
+  } else {
+    st = build_lattice(L, nullptr, a, fine, capacity_hint, stream);
+  }
   if (st != LAT_OK) {
+    if (side) (void)hipStreamSynchronize(side->s);
+    leave_side(L);
     L->free_all();
     HostSlots::get().give(L->host_dc);
     HostSlots::get().give_event(L->counts_ready);
@@ -774,6 +928,7 @@ int lattice_destroy(lattice_t L) {
   L->free_all();
   HostSlots::get().give(L->host_dc);
   HostSlots::get().give_event(L->counts_ready);
+  leave_side(L);
   delete L;
   return LAT_OK;
 }
@@ -804,7 +959,7 @@ int lattice_level(lattice_t L, int* level) {
 
 int lattice_export_keys(lattice_t L, int32_t* keys_dev, hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if (L->n > 0 && !keys_dev) return fail(LAT_EINVAL, "keys is null");
   if (L->n > 0 && !aligned16(keys_dev)) return fail(LAT_EINVAL, "keys must be 16-byte aligned");
   launch_export_keys(L->vkeys, L->n, keys_dev, stream);
@@ -813,7 +968,7 @@ int lattice_export_keys(lattice_t L, int32_t* keys_dev, hipStream_t stream) {
 
 int lattice_export_simplices(lattice_t L, int32_t* idx_dev, float* w_dev, hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (L->m == 0) return LAT_OK;
   if (!idx_dev || !w_dev) return fail(LAT_EINVAL, "idx / w is null");
@@ -824,7 +979,7 @@ int lattice_export_simplices(lattice_t L, int32_t* idx_dev, float* w_dev, hipStr
 
 int lattice_export_neighbors(lattice_t L, int32_t* nbr_dev, hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if (L->n == 0) return LAT_OK;
   if (!nbr_dev) return fail(LAT_EINVAL, "nbr is null");
   launch_transpose_table(L->nbr, L->nmax, L->n, nbr_dev, stream);
@@ -834,7 +989,7 @@ int lattice_export_neighbors(lattice_t L, int32_t* nbr_dev, hipStream_t stream) 
 int lattice_splat(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat_dtype dt,
                   int normalize, void* vals_dev, int64_t ld_vals, float* wsum_dev, hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_feat == 0) ld_feat = C;
@@ -856,8 +1011,8 @@ int lattice_conv(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in
                  const void* W_dev, const float* bias_dev, int Cout, lat_dtype dt, int flags,
                  void* out_dev, int64_t ld_out, hipStream_t stream) {
   int st;
-  if ((st = check_handle(dst)) != LAT_OK) return st;
-  if ((st = check_handle(src)) != LAT_OK) return st;
+  if ((st = use(dst, stream)) != LAT_OK) return st;
+  if ((st = use(src, stream)) != LAT_OK) return st;
   const int32_t* table;
   if (dst == src) table = dst->nbr;
   else if (dst->parent == src) table = dst->down;
@@ -870,8 +1025,8 @@ int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t
                    const void* W_dev, const float* bias_dev, int Cout, lat_dtype dt, int flags,
                    void* out_dev, int64_t ld_out, hipStream_t stream) {
   int st;
-  if ((st = check_handle(fine)) != LAT_OK) return st;
-  if ((st = check_handle(coarse)) != LAT_OK) return st;
+  if ((st = use(fine, stream)) != LAT_OK) return st;
+  if ((st = use(coarse, stream)) != LAT_OK) return st;
   if (coarse->parent != fine) return fail(LAT_ELEVEL, "coarse must be lattice_coarsen(fine)");
   return conv_common(coarse->up, fine->nmax, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
                      flags, out_dev, ld_out, coarse->up_rows, stream);
@@ -882,8 +1037,8 @@ int lattice_conv_preact(lattice_t dst, lattice_t src, const void* in_dev, int64_
                         const float* bias_dev, int Cout, lat_dtype dt, int flags, const void* res_dev,
                         int64_t ld_res, void* out_dev, int64_t ld_out, hipStream_t stream) {
   int st;
-  if ((st = check_handle(dst)) != LAT_OK) return st;
-  if ((st = check_handle(src)) != LAT_OK) return st;
+  if ((st = use(dst, stream)) != LAT_OK) return st;
+  if ((st = use(src, stream)) != LAT_OK) return st;
   const int32_t* table;
   if (dst == src) table = dst->nbr;
   else if (dst->parent == src) table = dst->down;
@@ -898,8 +1053,8 @@ int lattice_refine_preact(lattice_t fine, lattice_t coarse, const void* in_dev, 
                           const float* bias_dev, int Cout, lat_dtype dt, int flags, void* out_dev, int64_t ld_out,
                           hipStream_t stream) {
   int st;
-  if ((st = check_handle(fine)) != LAT_OK) return st;
-  if ((st = check_handle(coarse)) != LAT_OK) return st;
+  if ((st = use(fine, stream)) != LAT_OK) return st;
+  if ((st = use(coarse, stream)) != LAT_OK) return st;
   if (coarse->parent != fine) return fail(LAT_ELEVEL, "coarse must be lattice_coarsen(fine)");
   const GnArgs gn{groups, gamma_dev, beta_dev, eps, nullptr, 0};
   return conv_common(coarse->up, fine->nmax, fine->n, coarse->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt,
@@ -911,7 +1066,7 @@ int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* 
                                 const float* b2_dev, int C2, const float* W3_dev, const float* b3_dev, int C3,
                                 float* out_dev, int64_t ld_out, hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (Cf < 0 || Cf > distribute_max_features())
     return fail(LAT_EUNSUPPORTED, "Cf must be in [0, " + std::to_string(distribute_max_features()) + "]");
@@ -938,7 +1093,7 @@ int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* 
 int lattice_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
                   float* out_dev, hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_vals == 0) ld_vals = C;
@@ -952,7 +1107,7 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
                          const float* wv_dev, float beta, float* out_dev, float* delta_dev,
                          hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_vals == 0) ld_vals = C;
@@ -973,7 +1128,7 @@ int lattice_deform_slice_classify(lattice_t L, const void* vals_dev, int64_t ld_
                                   const float* wv_dev, float beta, const float* Wc_dev, const float* bc_dev, int K,
                                   float* logits_dev, hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if ((st = check_dtype(dt)) != LAT_OK) return st;
   if (ld_vals == 0) ld_vals = C;
@@ -997,7 +1152,7 @@ int lattice_deform_slice_classify(lattice_t L, const void* vals_dev, int64_t ld_
 int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int C, int normalize,
                            const float* wsum_dev, float* dF_dev, hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (ld_dX == 0) ld_dX = C;
   if ((st = check_matrix(dX_dev, ld_dX, C, LAT_F32, "dX", L->n > 0)) != LAT_OK) return st;
@@ -1021,7 +1176,7 @@ int lattice_splat_backward(lattice_t L, const float* dX_dev, int64_t ld_dX, int 
 int lattice_slice_backward(lattice_t L, const float* dOut_dev, int64_t ld_dOut, int C, float* dX_dev, int64_t ld_dX,
                            hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (ld_dOut == 0) ld_dOut = C;
   if (ld_dX == 0) ld_dX = C;
@@ -1043,8 +1198,8 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
                           int Cout, int flags, const float* Y_dev, int64_t ld_Y, const float* dY_dev, int64_t ld_dY,
                           float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream) {
   int st;
-  if ((st = check_handle(dst)) != LAT_OK) return st;
-  if ((st = check_handle(src)) != LAT_OK) return st;
+  if ((st = use(dst, stream)) != LAT_OK) return st;
+  if ((st = use(src, stream)) != LAT_OK) return st;
   // the forward's table (dst rows, src values) and the adjoint's (src rows,
   // dst values)
   const int32_t *fwd, *adj, *adj_rows = nullptr;
@@ -1120,7 +1275,7 @@ int lattice_deform_slice_backward(lattice_t L, const float* vals_dev, int64_t ld
                                   float beta, const float* dOut_dev, int64_t ld_dOut, float* dvals_dev,
                                   int64_t ld_dvals, float* dwv_dev, float* dbeta_dev, hipStream_t stream) {
   int st;
-  if ((st = check_handle(L)) != LAT_OK) return st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
   if (ld_vals == 0) ld_vals = C;
   if (ld_dOut == 0) ld_dOut = C;

@@ -671,13 +671,19 @@ void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_d
 
 void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse_keys, const uint64_t* fine_keys,
                           const int32_t* nc_dev, const int32_t* nf_dev, int64_t nc_max, int64_t nf_max, int32_t* nbr,
-                          int32_t* down, int32_t* up, int32_t* up_rows, hipStream_t s) {
-  if (nc_max <= 0 || nf_max <= 0) return;
+                          int32_t* down, int32_t* up, int32_t* up_rows, hipEvent_t done, hipStream_t s) {
+  if (nc_max <= 0 || nf_max <= 0) {
+    if (done) (void)hipEventRecord(done, s);
+    return;
+  }
   ScopedKernelTimer tm("nbr", s);
   launch(k_coarse_tables, dim3(stride_grid((2 * nc_max + nf_max) * kTaps)), dim3(kBlock), 0, s, coarse,
                      fine, coarse_keys, fine_keys, nc_dev, nf_dev, nbr, down, nc_max, up, nf_max);
-  launch(k_mask_order, dim3(static_cast<unsigned>((nf_max + kOrderRange - 1) / kOrderRange)),
-                     dim3(kOrderThreads), 0, s, up, nf_max, nf_dev, up_rows);
+  const dim3 grid(static_cast<unsigned>((nf_max + kOrderRange - 1) / kOrderRange));
+  if (done)
+    launch_signal(k_mask_order, grid, dim3(kOrderThreads), 0, s, done, up, nf_max, nf_dev, up_rows);
+  else
+    launch(k_mask_order, grid, dim3(kOrderThreads), 0, s, up, nf_max, nf_dev, up_rows);
 }
 
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s) {

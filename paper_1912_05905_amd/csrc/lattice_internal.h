@@ -158,7 +158,7 @@ void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_d
                            int32_t* nbr, int64_t ldn, hipStream_t s);
 void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse_keys, const uint64_t* fine_keys,
                           const int32_t* nc_dev, const int32_t* nf_dev, int64_t nc_max, int64_t nf_max, int32_t* nbr,
-                          int32_t* down, int32_t* up, int32_t* up_rows, hipStream_t s);
+                          int32_t* down, int32_t* up, int32_t* up_rows, hipEvent_t done, hipStream_t s);
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s);
 void launch_transpose_table(const int32_t* tab, int64_t ld, int64_t n, int32_t* out, hipStream_t s);
 // splat_slice.hip

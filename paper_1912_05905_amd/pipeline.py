@@ -12,7 +12,25 @@ from __future__ import annotations
 import numpy as np
 import torch
 
+from . import lattice as _lat
 from .lattice import Lattice
+
+
+class _Buffers(dict):
+    """name -> the n x total buffer of a step, sliced from its store when
+    first read (the forward operators pass raw pointers instead)."""
+
+    def __init__(self, stores, rows):
+        super().__init__()
+        self._stores, self._rows = stores, rows
+
+    def __missing__(self, name):
+        v = self._stores[name][:self._rows[name]]
+        self[name] = v
+        return v
+
+    def __contains__(self, name):
+        return name in self._rows
 
 
 class GpuPipeline:
@@ -38,20 +56,21 @@ class GpuPipeline:
         self.sigma = [float(s) for s in wl.sigma]
         self._store: dict[str, torch.Tensor] = {}
         self._wsum: torch.Tensor | None = None
+        # static arguments of the forward operators, converted once
+        self._lib = _lat.lib()
+        self._esize = 2 if self.dtype == torch.bfloat16 else 4
+        self._dt = _lat.LAT_BF16 if self.dtype == torch.bfloat16 else _lat.LAT_F32
+        self._wptr = {k: (w.data_ptr(), w.shape[1], w.shape[2]) for k, w in self.weights.items()}
+        self._outs: dict[str, torch.Tensor] = {}
 
-    def _view(self, bufs, levels, spec):
-        name, c0, cc = spec
-        if name not in bufs:
-            lv, total = self.wl.buffers[name]
-            n = levels[lv].n
-            # device buffers are kept across steps (same stream, so a step's
-            # kernels finish with a buffer before the next step's reuse it)
-            store = self._store.get(name)
-            if store is None or store.shape[0] < n:
-                store = torch.empty((n, total), dtype=self.dtype, device="cuda")
-                self._store[name] = store
-            bufs[name] = store[:n]
-        return bufs[name][:, c0:c0 + cc]
+    def _out(self, name, rows, cols, keep):
+        """Point output buffer (float32), kept across steps unless keep."""
+        t = None if keep else self._outs.get(name)
+        if t is None or t.shape != (rows, cols):
+            t = torch.empty((rows, cols), dtype=torch.float32, device="cuda")
+            if not keep:
+                self._outs[name] = t
+        return t
 
     def step(self, keep=False):
         """One pass of the pipeline.  Returns (levels, buffers, point outputs).
@@ -60,83 +79,140 @@ class GpuPipeline:
         level depends only on the positions, and issuing every build before
         the feature operations keeps the device busy while the host waits
         for vertex counts.  With keep=True the buffers are fresh tensors
-        that later steps do not overwrite."""
+        that later steps do not overwrite.  Forward operators are called
+        with raw pointers into the buffers (column ranges by offset), which
+        keeps the host's cost per operator near the library call itself."""
+        wl, lib, es, dt = self.wl, self._lib, self._esize, self._dt
         levels: dict[int, Lattice] = {}
-        bufs: dict[str, torch.Tensor] = {}
+        rows: dict[str, int] = {}
+        base: dict[str, tuple] = {}
         outs: dict[str, torch.Tensor] = {}
         if keep:
             self._store = {}
-        for op in self.wl.ops:
+        stream = _lat._stream()
+
+        def check(status):
+            if status != 0:
+                _lat._check(status)
+
+        def ptr(spec):
+            name, c0, _ = spec
+            b = base.get(name)
+            if b is None:
+                lv, total = wl.buffers[name]
+                n = levels[lv].n
+                store = self._store.get(name)
+                if store is None or store.shape[0] < n:
+                    store = torch.empty((n, total), dtype=self.dtype, device="cuda")
+                    self._store[name] = store
+                rows[name] = n
+                b = base[name] = (store.data_ptr(), total)
+            return b[0] + c0 * es, b[1]
+
+        for op in wl.ops:
             if op["op"] == "create":
                 levels[0] = Lattice.create(self.pos, self.sigma)
             elif op["op"] == "coarsen":
                 levels[op["level"]] = levels[op["level"] - 1].coarsen()
-        for op in self.wl.ops:
+        for op in wl.ops:
             kind = op["op"]
             if kind in ("create", "coarsen"):
                 continue
             elif kind == "splat":
+                L0 = levels[0]
                 # the weight sums are kept for a backward pass
-                if self._wsum is None or self._wsum.shape[0] < levels[0].n:
-                    self._wsum = torch.empty(levels[0].n, dtype=torch.float32, device="cuda")
-                levels[0].splat(self.feat, normalize=bool(op["normalize"]),
-                                out=self._view(bufs, levels, op["dst"]), wsum=self._wsum[:levels[0].n])
+                if self._wsum is None or self._wsum.shape[0] < L0.n:
+                    self._wsum = torch.empty(L0.n, dtype=torch.float32, device="cuda")
+                op_, old = ptr(op["dst"])
+                check(lib.lattice_splat(L0._h, self.feat.data_ptr(), self.feat.stride(0), self.feat.shape[1], dt,
+                                        int(bool(op["normalize"])), op_, old, self._wsum.data_ptr(), stream))
             elif kind in ("conv", "conv_down", "refine"):
                 lv = op["level"]
-                x = self._view(bufs, levels, op["src"])
-                y = self._view(bufs, levels, op["dst"])
-                W = self.weights[op["w"]]
+                xp, xld = ptr(op["src"])
+                yp, yld = ptr(op["dst"])
+                wp, cout, cin = self._wptr[op["w"]]
+                flags = _lat.LAT_RELU if op["relu"] else 0
+                dst = levels[lv]
+                src = levels[{"conv": lv, "conv_down": lv - 1, "refine": lv + 1}[kind]]
                 if "pre" in op:
                     gam, bet = self.norms[op["pre"]["norm"]]
-                    src = levels[{"conv": lv, "conv_down": lv - 1, "refine": lv + 1}[kind]]
-                    res = self._view(bufs, levels, op["res"]) if "res" in op else None
-                    levels[lv].conv_preact(src, x, W, groups=op["pre"]["groups"], gamma=gam, beta=bet,
-                                           relu=op["relu"], out=y, refine=kind == "refine", res=res)
-                elif kind == "conv":
-                    levels[lv].conv(levels[lv], x, W, relu=op["relu"], out=y)
-                elif kind == "conv_down":
-                    levels[lv].conv(levels[lv - 1], x, W, relu=op["relu"], out=y)
+                    args = (dst._h, src._h, xp, xld, cin, int(op["pre"]["groups"]), gam.data_ptr(), bet.data_ptr(),
+                            1e-5, wp, None, cout, dt, flags)
+                    if kind == "refine":
+                        check(lib.lattice_refine_preact(*args, yp, yld, stream))
+                    else:
+                        rp, rld = ptr(op["res"]) if "res" in op else (None, 0)
+                        check(lib.lattice_conv_preact(*args, rp, rld, yp, yld, stream))
+                elif kind == "refine":
+                    check(lib.lattice_refine(dst._h, src._h, xp, xld, cin, wp, None, cout, dt, flags, yp, yld, stream))
                 else:
-                    levels[lv].refine(levels[lv + 1], x, W, relu=op["relu"], out=y)
+                    check(lib.lattice_conv(dst._h, src._h, xp, xld, cin, wp, None, cout, dt, flags, yp, yld, stream))
             elif kind == "distribute":
-                levels[op["level"]].distribute_pointnet(self.pos, self.feat, [self.mlp[n] for n in op["layers"]],
-                                                        out=self._view(bufs, levels, op["dst"]))
+                yp, yld = ptr(op["dst"])
+                layers = [self.mlp[n] for n in op["layers"]]
+                (W1, b1), (W2, b2), (W3, b3) = layers
+                check(lib.lattice_distribute_pointnet(
+                    levels[op["level"]]._h, self.pos.data_ptr(), self.feat.data_ptr(), self.feat.stride(0),
+                    self.feat.shape[1], W1.data_ptr(), b1.data_ptr(), W1.shape[0], W2.data_ptr(), b2.data_ptr(),
+                    W2.shape[0], W3.data_ptr(), b3.data_ptr(), W3.shape[0], yp, yld, stream))
             elif kind == "slice":
-                outs[op["out"]] = levels[op["level"]].slice(self._view(bufs, levels, op["src"]))
+                L = levels[op["level"]]
+                xp, xld = ptr(op["src"])
+                cc = op["src"][2]
+                out = outs[op["out"]] = self._out(op["out"], L.m, cc, keep)
+                check(lib.lattice_slice(L._h, xp, xld, cc, dt, out.data_ptr(), stream))
             elif kind == "deform_slice":
+                L = levels[op["level"]]
                 wv, beta = self.vectors[op["wv"]]
-                outs[op["out"]] = levels[op["level"]].deform_slice(
-                    self._view(bufs, levels, op["src"]), wv, beta)
+                xp, xld = ptr(op["src"])
+                cc = op["src"][2]
+                out = outs[op["out"]] = self._out(op["out"], L.m, cc, keep)
+                check(lib.lattice_deform_slice(L._h, xp, xld, cc, dt, wv.data_ptr(), beta, out.data_ptr(), None,
+                                               stream))
             elif kind == "deform_classify":
+                L = levels[op["level"]]
                 wv, beta = self.vectors[op["wv"]]
                 Wc, bc = self.classifiers[op["cls"]]
-                outs[op["out"]] = levels[op["level"]].deform_slice_classify(
-                    self._view(bufs, levels, op["src"]), wv, beta, Wc, bc)
-            elif kind == "deform_slice_bwd":
-                wv, beta = self.vectors[op["wv"]]
-                _, dwv, dbeta = levels[op["level"]].deform_slice_backward(
-                    self._view(bufs, levels, op["x"]), wv, beta, self.grads[op["grad"]],
-                    dx_out=self._view(bufs, levels, op["dst"]))
-                outs[op["out"]], outs["dbeta:" + op["wv"]] = dwv, dbeta
-            elif kind == "conv_bwd":
-                lv = op["level"]
-                dst = levels[lv]
-                src = {"conv": lv, "conv_down": lv - 1, "refine": lv + 1}[op["kind"]]
-                _, dW, db = dst.conv_backward(levels[src], self._view(bufs, levels, op["x"]), self.weights[op["w"]],
-                                              self._view(bufs, levels, op["src"]), relu=op["relu"],
-                                              y=self._view(bufs, levels, op["y"]) if op["relu"] else None,
-                                              dx_out=self._view(bufs, levels, op["dst"]))
-                outs[op["out"]] = dW.transpose(1, 2)          # taps x Cin x Cout, the workload's layout
-                outs["db:" + op["w"]] = db
-            elif kind == "splat_bwd":
-                outs[op["out"]] = levels[0].splat_backward(self._view(bufs, levels, op["src"]),
-                                                           normalize=bool(op["normalize"]),
-                                                           wsum=self._wsum[:levels[0].n])
+                xp, xld = ptr(op["src"])
+                cc = op["src"][2]
+                out = outs[op["out"]] = self._out(op["out"], L.m, Wc.shape[0], keep)
+                check(lib.lattice_deform_slice_classify(L._h, xp, xld, cc, dt, wv.data_ptr(), beta, Wc.data_ptr(),
+                                                        bc.data_ptr(), Wc.shape[0], out.data_ptr(), stream))
+            elif kind in ("deform_slice_bwd", "conv_bwd", "splat_bwd"):
+                # backward operators: through the Lattice methods, on views
+                for key in ("x", "src", "y", "dst"):
+                    if key in op:
+                        ptr(op[key])
+                self._backward_op(op, levels, _Buffers(self._store, rows), outs)
             else:
                 raise ValueError(f"unknown op {kind}")
+        stores = self._store
         if keep:
             self._store = {}
-        return levels, bufs, outs
+        return levels, _Buffers(stores, rows), outs
+
+    def _backward_op(self, op, levels, bufs, outs):
+        def view(spec):
+            name, c0, cc = spec
+            return bufs[name][:, c0:c0 + cc]
+
+        kind = op["op"]
+        if kind == "deform_slice_bwd":
+            wv, beta = self.vectors[op["wv"]]
+            _, dwv, dbeta = levels[op["level"]].deform_slice_backward(
+                view(op["x"]), wv, beta, self.grads[op["grad"]], dx_out=view(op["dst"]))
+            outs[op["out"]], outs["dbeta:" + op["wv"]] = dwv, dbeta
+        elif kind == "conv_bwd":
+            lv = op["level"]
+            src = {"conv": lv, "conv_down": lv - 1, "refine": lv + 1}[op["kind"]]
+            _, dW, db = levels[lv].conv_backward(levels[src], view(op["x"]), self.weights[op["w"]], view(op["src"]),
+                                                 relu=op["relu"], y=view(op["y"]) if op["relu"] else None,
+                                                 dx_out=view(op["dst"]))
+            outs[op["out"]] = dW.transpose(1, 2)          # taps x Cin x Cout, the workload's layout
+            outs["db:" + op["w"]] = db
+        else:
+            outs[op["out"]] = levels[0].splat_backward(view(op["src"]), normalize=bool(op["normalize"]),
+                                                       wsum=self._wsum[:levels[0].n])
 
     @staticmethod
     def release(levels):

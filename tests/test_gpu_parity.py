@@ -362,6 +362,46 @@ def test_strided_and_transposed_conv(L, O, dtype):
     P.assert_close(P.rows_in_oracle_order(_host(gz), g2o_f), oz, tol, "transposed conv")
 
 
+def test_coarse_levels_used_on_another_stream(L, O):
+    """Coarse levels are built on the library's own stream.  A second caller
+    stream that is ordered only after the coarsen calls were issued (not
+    after the builds themselves) must still see finished tables, and their
+    point lists built on first use there."""
+    pos = _cloud(72, 9000, 0.8)
+    sigma = 0.05
+    o0 = O.Lattice.create(pos, np.full(3, sigma, np.float32))
+    o1 = o0.coarsen()
+    o2 = o1.coarsen()
+    rng = np.random.default_rng(13)
+    Xf = rng.normal(size=(o0.n, 32))
+    Wd = _rand_w(rng, 32, 64, 1.0 / 16)
+    W2 = _rand_w(rng, 64, 32, 1.0 / 24)
+    Wdev, W2dev, posdev = _gpu_w(Wd), _gpu_w(W2), _dev(pos)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s1):
+        g0 = L.Lattice.create(posdev, [sigma] * 3)
+        g1 = g0.coarsen()
+        g2 = g1.coarsen()
+    s2.wait_stream(s1)
+    with torch.cuda.stream(s2):
+        g2o0 = P.key_permutation(_host(g0.keys()), o0.keys())
+        x = _dev(Xf[g2o0].astype(np.float32))
+        y1 = g1.conv(g0, x, Wdev)
+        y2 = g2.conv(g1, y1, W2dev)
+        vals = g2.slice(y2)
+    torch.cuda.synchronize()
+    g2o1 = P.key_permutation(_host(g1.keys()), o1.keys())
+    g2o2 = P.key_permutation(_host(g2.keys()), o2.keys())
+    oy1 = o1.conv(o0, Xf, Wd)
+    P.assert_close(P.rows_in_oracle_order(_host(y1), g2o1), oy1, P.TOL_F32, "strided conv, level 1")
+    oy2 = o2.conv(o1, oy1, W2)
+    P.assert_close(P.rows_in_oracle_order(_host(y2), g2o2), oy2, P.TOL_F32, "strided conv, level 2")
+    P.assert_close(_host(vals), o2.slice(oy2), P.TOL_F32, "slice on level 2")
+    for g in (g2, g1, g0):
+        g.destroy()
+
+
 @pytest.mark.parametrize("C,dtype", [(4, "f32"), (16, "f32"), (64, "f32"), (128, "f32"),
                                      (512, "f32"), (64, "bf16"), (256, "bf16")])
 def test_slice_and_deform_slice(L, O, C, dtype):
