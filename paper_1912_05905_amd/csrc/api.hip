@@ -411,44 +411,68 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   const int64_t nchunks = (refs + L->chunk - 1) / L->chunk;
   L->bstream = s;
   int st;
-  void* p;
-#define ALLOC(field, type, count)                                                         \
-  if ((st = L->alloc(sizeof(type) * static_cast<size_t>(count), L->stream, &p)) != LAT_OK) \
-    return st;                                                                            \
-  L->field = static_cast<type*>(p)
-  ALLOC(y, float, 4 * m);
-  ALLOC(idx, int32_t, refs);
-  ALLOC(w, float, refs);
-  ALLOC(table, HashEntry, cap);
-  ALLOC(vkeys, uint64_t, nmax);
-  ALLOC(dc, DeviceCounters, 1);
-  ALLOC(offsets, int32_t, nmax + 1);
-  ALLOC(entries, int32_t, refs);
-  ALLOC(entry_w, float, refs);
-  ALLOC(chunk_first, int32_t, nchunks);
-  ALLOC(nbr, int32_t, kTaps * nmax);
-  if (parent) {
-    ALLOC(down, int32_t, kTaps * nmax);
-    ALLOC(up, int32_t, kTaps * parent->nmax);
-    ALLOC(up_rows, int32_t, parent->nmax);
-  }
+  // One pool block per build, carved into the handle's buffers (256-byte
+  // aligned); the elevated positions come first, so the block's address is
+  // theirs.
+  size_t off = 0;
+  auto carve = [&](size_t bytes) {
+    const size_t o = off;
+    off += (bytes + 255) & ~static_cast<size_t>(255);
+    return o;
+  };
+  const size_t o_y = carve(sizeof(float) * 4 * m);
+  const size_t o_idx = carve(sizeof(int32_t) * refs);
+  const size_t o_w = carve(sizeof(float) * refs);
+  const size_t o_table = carve(sizeof(HashEntry) * cap);
+  const size_t o_vkeys = carve(sizeof(uint64_t) * nmax);
+  const size_t o_dc = carve(sizeof(DeviceCounters));
+  const size_t o_offsets = carve(sizeof(int32_t) * (nmax + 1));
+  const size_t o_entries = carve(sizeof(int32_t) * refs);
+  const size_t o_entry_w = carve(sizeof(float) * refs);
+  const size_t o_chunk_first = carve(sizeof(int32_t) * nchunks);
+  const size_t o_nbr = carve(sizeof(int32_t) * kTaps * nmax);
+  const size_t o_down = parent ? carve(sizeof(int32_t) * kTaps * nmax) : 0;
+  const size_t o_up = parent ? carve(sizeof(int32_t) * kTaps * parent->nmax) : 0;
+  const size_t o_up_rows = parent ? carve(sizeof(int32_t) * parent->nmax) : 0;
   // The finest level builds its lists now (splat needs them); a coarse level
   // when an operator first needs them.  Either way the inputs of the list
   // build are the handle's own buffers: a build releases nothing to the
   // pool, so a coarse level can start after the finer level's insert.
   const bool defer_lists = parent != nullptr;
-  ALLOC(slot_count, int32_t, cap);
-  ALLOC(vslot, int32_t, nmax);
-  ALLOC(slot, int32_t, refs);
-  ALLOC(rank, int32_t, refs);
-  if ((st = L->alloc(static_cast<size_t>(scan_workspace_bytes()), L->stream, &p)) != LAT_OK) return st;
-  L->scan_work = p;
+  const size_t o_slot_count = carve(sizeof(int32_t) * cap);
+  const size_t o_vslot = carve(sizeof(int32_t) * nmax);
+  const size_t o_slot = carve(sizeof(int32_t) * refs);
+  const size_t o_rank = carve(sizeof(int32_t) * refs);
+  const size_t o_work = carve(static_cast<size_t>(scan_workspace_bytes()));
+  void* blk = nullptr;
+  if ((st = L->alloc(off, L->stream, &blk)) != LAT_OK) return st;
+  auto at = [&](size_t o) { return static_cast<void*>(static_cast<char*>(blk) + o); };
+  L->y = static_cast<float*>(at(o_y));
+  L->idx = static_cast<int32_t*>(at(o_idx));
+  L->w = static_cast<float*>(at(o_w));
+  L->table = static_cast<HashEntry*>(at(o_table));
+  L->vkeys = static_cast<uint64_t*>(at(o_vkeys));
+  L->dc = static_cast<DeviceCounters*>(at(o_dc));
+  L->offsets = static_cast<int32_t*>(at(o_offsets));
+  L->entries = static_cast<int32_t*>(at(o_entries));
+  L->entry_w = static_cast<float*>(at(o_entry_w));
+  L->chunk_first = static_cast<int32_t*>(at(o_chunk_first));
+  L->nbr = static_cast<int32_t*>(at(o_nbr));
+  if (parent) {
+    L->down = static_cast<int32_t*>(at(o_down));
+    L->up = static_cast<int32_t*>(at(o_up));
+    L->up_rows = static_cast<int32_t*>(at(o_up_rows));
+  }
+  L->slot_count = static_cast<int32_t*>(at(o_slot_count));
+  L->vslot = static_cast<int32_t*>(at(o_vslot));
+  L->slot = static_cast<int32_t*>(at(o_slot));
+  L->rank = static_cast<int32_t*>(at(o_rank));
+  L->scan_work = at(o_work);
   int32_t* slot_count = L->slot_count;
   int32_t* vslot = L->vslot;
   int32_t* slot = L->slot;
   int32_t* rank = L->rank;
   void* work = L->scan_work;
-#undef ALLOC
   if (!L->host_dc && !(L->host_dc = HostSlots::get().take())) return fail(LAT_ENOMEM, "pinned host slot");
   if (!L->counts_ready && !(L->counts_ready = HostSlots::get().take_event()))
     return fail(LAT_EDEVICE, "event creation failed");

@@ -586,7 +586,9 @@ int64_t blocks_of(int64_t n_out, int Cout, int rows, int cols) {
 // Tile choice, from a sweep of tile shapes, pipeline depths and step
 // schedules over the lattices of the LiDAR scan (fp32) and of the 1M-point
 // room (bf16) on MI355X.  fp32: small tiles win; the levels are small and a
-// stage costs several times its MFMA time.  bf16: 128 x 128 tiles halve the
+// stage costs several times its MFMA time.  Around a thousand 32 x 32 tiles
+// a third stage in flight (with half the channels per stage) pays; a few
+// hundred 32 x 64 tiles do best with two stages of 64 channels.  bf16: 128 x 128 tiles halve the
 // gathered bytes per flop and win once there are enough of them (wide
 // layers, large levels); 64 x 64 otherwise.
 // PRE (the pre-activated convolution) uses the same tiles, apart from the
@@ -621,6 +623,12 @@ void conv_dispatch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* i
           nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
     if (Cout > 64 && blocks_of(n_out, Cout, 32, 64) >= 1024)
       return conv_lds_launch<false, 32, 64, 2, 2, 128, 3, true, 1, PRE>(
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
+    if (Cout > 64 && blocks_of(n_out, Cout, 32, 64) >= 400)
+      return conv_lds_launch<false, 32, 64, 2, 2, 256, 2, true, 1, PRE>(
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
+    if (blocks_of(n_out, Cout, 32, 32) >= 1024)
+      return conv_lds_launch<false, 32, 32, 2, 2, 128, 3, true, 1, PRE>(
           nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
     return conv_lds_launch<false, 32, 32, 2, 2, 256, 2, true, 1, PRE>(
         nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
