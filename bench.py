@@ -104,7 +104,7 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mb,
             ent[field] += sum(vals) * scale
             if counter == "FETCH_SIZE":
                 ent["dispatches"] += len(vals)
-    runs = warmup + 1 + steps     # warmup, instrumented and timed steps of the profiled bench run
+    runs = warmup + 1 + 2 * steps  # warmup, instrumented step, the two timed regions of the profiled run
     for ent in fams.values():
         ent["fetch_bytes_per_step"] = ent.pop("fetch_bytes") / runs
         ent["write_bytes_per_step"] = ent.pop("write_bytes") / runs
