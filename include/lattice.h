@@ -244,6 +244,17 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
                          hipStream_t stream);
 
 /*
+ * Slice (Eq. slice) and DeformSlice (Eq. deformSlice) of the same values in
+ * one pass over the gathered vertex rows: slice_dev receives what
+ * lattice_slice writes, deform_dev what lattice_deform_slice writes (same
+ * arithmetic, same results).  Both m x C float32, dense, not overlapping;
+ * the rest as lattice_deform_slice (no offsets output).
+ */
+int lattice_slice_and_deform(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
+                             const float* wv_dev, float beta, float* slice_dev, float* deform_dev,
+                             hipStream_t stream);
+
+/*
  * DeformSlice fused with the last linear classification layer
  * (Implementation: fused to avoid storing the high-dimensional per-point
  * features): logits_p = Wc f_p + bc, f_p the DeformSlice output of point p

@@ -1144,8 +1144,32 @@ int lattice_deform_slice(lattice_t L, const void* vals_dev, int64_t ld_vals, int
     return fail(LAT_EUNSUPPORTED, "DeformSlice supports at most " +
                                       std::to_string(deform_max_channels(dt == LAT_BF16)) + " channels");
   launch_deform_slice(L->idx, L->w, L->m, vals_dev, ld_vals, C, dt == LAT_BF16, wv_dev, beta, out_dev,
-                      delta_dev, stream);
+                      delta_dev, nullptr, stream);
   return check_launch("deform slice");
+}
+
+int lattice_slice_and_deform(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,
+                             const float* wv_dev, float beta, float* slice_dev, float* deform_dev,
+                             hipStream_t stream) {
+  int st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
+  if ((st = check_dtype(dt)) != LAT_OK) return st;
+  if (ld_vals == 0) ld_vals = C;
+  if ((st = check_matrix(vals_dev, ld_vals, C, dt, "vals", L->n > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(slice_dev, C, C, LAT_F32, "slice_out", L->m > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(deform_dev, C, C, LAT_F32, "deform_out", L->m > 0)) != LAT_OK) return st;
+  if (L->m > 0 && overlaps(slice_dev, sizeof(float) * static_cast<size_t>(L->m) * C, deform_dev,
+                           sizeof(float) * static_cast<size_t>(L->m) * C))
+    return fail(LAT_EINVAL, "slice_out and deform_out overlap");
+  if (!wv_dev) return fail(LAT_EINVAL, "wv is null");
+  if (!std::isfinite(beta)) return fail(LAT_EINVAL, "beta must be finite");
+  if (C > deform_max_channels(dt == LAT_BF16))
+    return fail(LAT_EUNSUPPORTED, "DeformSlice supports at most " +
+                                      std::to_string(deform_max_channels(dt == LAT_BF16)) + " channels");
+  launch_deform_slice(L->idx, L->w, L->m, vals_dev, ld_vals, C, dt == LAT_BF16, wv_dev, beta, deform_dev,
+                      nullptr, slice_dev, stream);
+  return check_launch("slice and deform slice");
 }
 
 int lattice_deform_slice_classify(lattice_t L, const void* vals_dev, int64_t ld_vals, int C, lat_dtype dt,

@@ -171,7 +171,7 @@ void launch_slice(const int32_t* idx, const float* w, int64_t m, const void* val
                   int C, int bf16, float* out, hipStream_t s);
 void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const void* vals,
                          int64_t ld_vals, int C, int bf16, const float* wv, float beta, float* out,
-                         float* delta, hipStream_t s);
+                         float* delta, float* plain, hipStream_t s);
 int deform_classify_max_classes();
 int deform_classify_max_weights();
 void launch_deform_classify(const int32_t* idx, const float* w, int64_t m, const void* vals, int64_t ld_vals, int C,

@@ -459,7 +459,8 @@ template <bool BF16, int LPR, int CPL>
 __global__ void __launch_bounds__(kBlock)
 k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64_t m,
                const void* __restrict__ vals, int64_t ld_vals, int C, const float* __restrict__ wvec,
-               float beta, float* __restrict__ out, float4* __restrict__ delta, unsigned nblk) {
+               float beta, float* __restrict__ out, float4* __restrict__ delta, float* __restrict__ plain,
+               unsigned nblk) {
   using Ch = Chunk<BF16>;
   const int lane = threadIdx.x & (LPR - 1);
   const int64_t p = xcd_item<LPR>(nblk);
@@ -530,6 +531,22 @@ k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64
         r[u] = coef[0] * x[q][0][i + u] + coef[1] * x[q][1][i + u] + coef[2] * x[q][2][i + u] +
                coef[3] * x[q][3][i + u];
       *reinterpret_cast<float4*>(o + i) = make_float4(r[0], r[1], r[2], r[3]);
+    }
+    if (plain) {
+      // the plain slice of the same rows (Eq. slice), in the order of k_slice
+      float* o2 = plain + p * C + static_cast<int64_t>(ch) * Ch::N;
+#pragma unroll
+      for (int i = 0; i < Ch::N; i += 4) {
+        float r[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          float a = 0.f;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) a += bw[k] * x[q][k][i + u];
+          r[u] = a;
+        }
+        *reinterpret_cast<float4*>(o2 + i) = make_float4(r[0], r[1], r[2], r[3]);
+      }
     }
   }
 }
@@ -920,7 +937,7 @@ void slice_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, cons
 
 template <bool BF16, int CPL>
 void deform_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, const void* vals,
-                     int64_t ldv, int C, const float* wv, float beta, float* out, float* delta,
+                     int64_t ldv, int C, const float* wv, float beta, float* out, float* delta, float* plain,
                      hipStream_t s) {
   const unsigned nblk = grid_for(m, lpr);
   const dim3 g(xcd_grid(nblk)), b(kBlock);
@@ -928,13 +945,13 @@ void deform_dispatch(int lpr, const int32_t* idx, const float* w, int64_t m, con
   const float4* w4 = reinterpret_cast<const float4*>(w);
   float4* d4 = reinterpret_cast<float4*>(delta);
   switch (lpr) {
-    case 1: launch((k_deform_slice<BF16, 1, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 2: launch((k_deform_slice<BF16, 2, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 4: launch((k_deform_slice<BF16, 4, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 8: launch((k_deform_slice<BF16, 8, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 16: launch((k_deform_slice<BF16, 16, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    case 32: launch((k_deform_slice<BF16, 32, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
-    default: launch((k_deform_slice<BF16, 64, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, nblk); break;
+    case 1: launch((k_deform_slice<BF16, 1, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, plain, nblk); break;
+    case 2: launch((k_deform_slice<BF16, 2, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, plain, nblk); break;
+    case 4: launch((k_deform_slice<BF16, 4, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, plain, nblk); break;
+    case 8: launch((k_deform_slice<BF16, 8, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, plain, nblk); break;
+    case 16: launch((k_deform_slice<BF16, 16, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, plain, nblk); break;
+    case 32: launch((k_deform_slice<BF16, 32, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, plain, nblk); break;
+    default: launch((k_deform_slice<BF16, 64, CPL>), g, b, 0, s, i4, w4, m, vals, ldv, C, wv, beta, out, d4, plain, nblk); break;
   }
 }
 
@@ -1080,18 +1097,18 @@ void launch_deform_slice_backward(const int32_t* idx, const float* w, int64_t m,
 
 void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const void* vals,
                          int64_t ld_vals, int C, int bf16, const float* wv, float beta, float* out,
-                         float* delta, hipStream_t s) {
+                         float* delta, float* plain, hipStream_t s) {
   if (m <= 0) return;
   const int lpr = lanes_per_row(C, bf16 != 0);
   const int chunks = C / (bf16 ? 8 : 4);
   ScopedKernelTimer tm("deform_slice", s);
   const bool two = chunks > lpr;
   if (bf16) {
-    if (two) deform_dispatch<true, 2>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, out, delta, s);
-    else deform_dispatch<true, 1>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, out, delta, s);
+    if (two) deform_dispatch<true, 2>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, out, delta, plain, s);
+    else deform_dispatch<true, 1>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, out, delta, plain, s);
   } else {
-    if (two) deform_dispatch<false, 2>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, out, delta, s);
-    else deform_dispatch<false, 1>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, out, delta, s);
+    if (two) deform_dispatch<false, 2>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, out, delta, plain, s);
+    else deform_dispatch<false, 1>(lpr, idx, w, m, vals, ld_vals, C, wv, beta, out, delta, plain, s);
   }
 }
 

@@ -43,6 +43,7 @@ SIGNATURES = {
     "lattice_refine": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _I32, _I32, _P, _I64, _P]),
     "lattice_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
     "lattice_deform_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _P]),
+    "lattice_slice_and_deform": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _P]),
     "lattice_conv_preact": (_I32, [_P, _P, _P, _I64, _I32, _I32, _P, _P, _F32, _P, _P, _I32, _I32, _I32, _P, _I64,
                                    _P, _I64, _P]),
     "lattice_refine_preact": (_I32, [_P, _P, _P, _I64, _I32, _I32, _P, _P, _F32, _P, _P, _I32, _I32, _I32, _P,
@@ -395,3 +396,18 @@ class Lattice:
                                           None if delta is None else C.c_void_p(delta.data_ptr()),
                                           _stream(stream)))
         return out
+
+    def slice_and_deform(self, x: torch.Tensor, wv: torch.Tensor, beta: float, slice_out: torch.Tensor | None = None,
+                         deform_out: torch.Tensor | None = None, stream=None):
+        """(slice(x), deform_slice(x, wv, beta)) from one pass over the
+        gathered rows."""
+        Cc = x.shape[1]
+        if slice_out is None:
+            slice_out = torch.empty((self.m, Cc), dtype=torch.float32, device="cuda")
+        if deform_out is None:
+            deform_out = torch.empty((self.m, Cc), dtype=torch.float32, device="cuda")
+        xp, xld = _rows(x)
+        _check(lib().lattice_slice_and_deform(self._h, xp, xld, Cc, _dtype_code(x), C.c_void_p(wv.data_ptr()),
+                                              float(beta), C.c_void_p(slice_out.data_ptr()),
+                                              C.c_void_p(deform_out.data_ptr()), _stream(stream)))
+        return slice_out, deform_out

@@ -62,6 +62,11 @@ class GpuPipeline:
         self._dt = _lat.LAT_BF16 if self.dtype == torch.bfloat16 else _lat.LAT_F32
         self._wptr = {k: (w.data_ptr(), w.shape[1], w.shape[2]) for k, w in self.weights.items()}
         self._outs: dict[str, torch.Tensor] = {}
+        # a slice followed by a DeformSlice of the same values runs as one pass
+        ops = wl.ops
+        self._fused = {i for i in range(len(ops) - 1)
+                       if ops[i]["op"] == "slice" and ops[i + 1]["op"] == "deform_slice"
+                       and ops[i]["level"] == ops[i + 1]["level"] and ops[i]["src"] == ops[i + 1]["src"]}
 
     def _out(self, name, rows, cols, keep):
         """Point output buffer (float32), kept across steps unless keep."""
@@ -114,9 +119,25 @@ class GpuPipeline:
                 levels[0] = Lattice.create(self.pos, self.sigma)
             elif op["op"] == "coarsen":
                 levels[op["level"]] = levels[op["level"] - 1].coarsen()
-        for op in wl.ops:
+        skip = False
+        for i, op in enumerate(wl.ops):
             kind = op["op"]
+            if skip:
+                skip = False
+                continue
             if kind in ("create", "coarsen"):
+                continue
+            if i in self._fused:
+                dop = wl.ops[i + 1]
+                L = levels[op["level"]]
+                wv, beta = self.vectors[dop["wv"]]
+                xp, xld = ptr(op["src"])
+                cc = op["src"][2]
+                out = outs[op["out"]] = self._out(op["out"], L.m, cc, keep)
+                dout = outs[dop["out"]] = self._out(dop["out"], L.m, cc, keep)
+                check(lib.lattice_slice_and_deform(L._h, xp, xld, cc, dt, wv.data_ptr(), beta, out.data_ptr(),
+                                                   dout.data_ptr(), stream))
+                skip = True
                 continue
             elif kind == "splat":
                 L0 = levels[0]

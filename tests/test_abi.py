@@ -33,7 +33,7 @@ def test_header_declares_the_boundary():
                  "lattice_num_vertices", "lattice_export_keys", "lattice_export_neighbors",
                  "lattice_export_simplices", "lattice_distribute_pointnet", "lattice_splat_backward",
                  "lattice_slice_backward", "lattice_conv_backward", "lattice_deform_slice_backward", "lattice_conv_preact", "lattice_deform_slice_classify",
-                 "lattice_refine_preact"):
+                 "lattice_refine_preact", "lattice_slice_and_deform"):
         assert need in names
 
 
@@ -72,6 +72,7 @@ def test_host_validation_without_gpu(lib):
     assert lib.lattice_refine(None, None, None, 0, 8, None, None, 8, 0, 0, None, 0, None) == -1
     assert lib.lattice_slice(None, None, 0, 8, 0, None, None) == -1
     assert lib.lattice_deform_slice(None, None, 0, 8, 0, None, 0.0, None, None, None) == -1
+    assert lib.lattice_slice_and_deform(None, None, 0, 8, 0, None, 0.0, None, None, None) == -1
     assert lib.lattice_distribute_pointnet(None, None, None, 0, 4, None, None, 16, None, None, 32, None, None, 64,
                                            None, 0, None) == -1
     assert lib.lattice_coarsen(None, 0, None, C.byref(out)) == -1

@@ -422,6 +422,12 @@ def test_slice_and_deform_slice(L, O, C, dtype):
         oo, od = ol.deform_slice(X, wv.astype(np.float64), 0.1)
         P.assert_close(_host(out), oo, P.TOL_F32, "deform slice")
         P.assert_close(_host(delta), od, P.TOL_F32, "deform offsets")
+        # both from one pass: the oracle's values, and the separate calls' bits
+        s2, d2 = gl.slice_and_deform(Xg, _dev(wv), 0.1)
+        P.assert_close(_host(s2), ol.slice(X), P.TOL_F32, "fused slice")
+        P.assert_close(_host(d2), oo, P.TOL_F32, "fused deform slice")
+        assert np.array_equal(_host(d2), _host(out)), "fused DeformSlice differs from the separate call"
+        assert np.array_equal(_host(s2), _host(gl.slice(Xg))), "fused slice differs from the separate call"
 
 
 # ----------------------------------------------------------------------------
