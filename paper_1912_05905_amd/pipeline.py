@@ -34,8 +34,17 @@ class _Buffers(dict):
 
 
 class GpuPipeline:
-    def __init__(self, wl):
+    """overlap=True builds each step's lattices on a stream of their own, so
+    that the next cloud's lattice construction runs while this cloud's
+    operators still execute (steps are independent).  A step's lattices are
+    then destroyed by finish_step() one step later, once the build stream is
+    ordered after the step's operators."""
+
+    def __init__(self, wl, overlap=False):
         self.wl = wl
+        self.overlap = overlap
+        self._build_stream = torch.cuda.Stream() if overlap else None
+        self._pending: list = []      # (levels, operators-done event) of finished steps
         self.dtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
         self.pos = torch.from_numpy(np.ascontiguousarray(wl.positions)).cuda()
         self.feat = torch.from_numpy(np.ascontiguousarray(wl.features)).cuda().to(self.dtype)
@@ -114,11 +123,30 @@ class GpuPipeline:
                 b = base[name] = (store.data_ptr(), total)
             return b[0] + c0 * es, b[1]
 
-        for op in wl.ops:
-            if op["op"] == "create":
-                levels[0] = Lattice.create(self.pos, self.sigma)
-            elif op["op"] == "coarsen":
-                levels[op["level"]] = levels[op["level"] - 1].coarsen()
+        def build():
+            for op in wl.ops:
+                if op["op"] == "create":
+                    levels[0] = Lattice.create(self.pos, self.sigma)
+                elif op["op"] == "coarsen":
+                    levels[op["level"]] = levels[op["level"] - 1].coarsen()
+
+        if self.overlap and not keep:
+            # destroy the lattices of all but the last finished step; their
+            # buffers return to the build stream's pool once that stream has
+            # passed the step's operators
+            bs = self._build_stream
+            while len(self._pending) > 1:
+                old, done = self._pending.pop(0)
+                bs.wait_event(done)
+                with torch.cuda.stream(bs):
+                    GpuPipeline.release(old)
+            with torch.cuda.stream(bs):
+                build()
+            built = torch.cuda.Event()
+            built.record(bs)
+            torch.cuda.current_stream().wait_event(built)
+        else:
+            build()
         skip = False
         for i, op in enumerate(wl.ops):
             kind = op["op"]
@@ -234,6 +262,23 @@ class GpuPipeline:
         else:
             outs[op["out"]] = levels[0].splat_backward(view(op["src"]), normalize=bool(op["normalize"]),
                                                        wsum=self._wsum[:levels[0].n])
+
+    def finish_step(self, levels):
+        """Release a step's lattices: at once, or (overlap) after the next
+        step's build has been ordered behind this step's operators."""
+        if not self.overlap:
+            GpuPipeline.release(levels)
+            return
+        done = torch.cuda.Event()
+        done.record(torch.cuda.current_stream())
+        self._pending.append((levels, done))
+
+    def flush(self):
+        """Release every lattice still held (overlap mode)."""
+        torch.cuda.synchronize()
+        for old, _ in self._pending:
+            GpuPipeline.release(old)
+        self._pending = []
 
     @staticmethod
     def release(levels):

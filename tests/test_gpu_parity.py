@@ -481,6 +481,21 @@ def test_pipeline_full_size(L, O, cfg):
     _run_both(L, O, configs.make(cfg))
 
 
+def test_pipeline_overlapped_steps(L, O):
+    """Steps whose lattice builds overlap the previous step's operators (the
+    bench's mode): every step's point outputs match the oracle."""
+    from paper_1912_05905_amd.pipeline import GpuPipeline
+    wl = configs.make(4)
+    _, _, oouts = OraclePipeline(wl).run()
+    pipe = GpuPipeline(wl, overlap=True)
+    for _ in range(4):
+        levels, _, outs = pipe.step()
+        for name in ("slice", "deform"):
+            P.assert_close(_host(outs[name]), oouts[name], P.TOL_F32, name)
+        pipe.finish_step(levels)
+    pipe.flush()
+
+
 def test_latticenet_reduced(L, O):
     """The whole LatticeNet forward (Distribute + PointNet, eight ResNet
     blocks of pre-activated convolutions, two Downsamples, two Upsamples with
