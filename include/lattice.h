@@ -64,6 +64,7 @@ enum {
 };
 
 #define LAT_RELU 1         /* flags bit: apply max(0, .) after bias */
+#define LAT_ON_STREAM 1    /* lattice_coarsen_ex flags bit: build on the given stream */
 #define LAT_TAPS 9         /* 2(d+1)+1 vertices of the 1-hop neighbourhood */
 
 /* Text of the calling thread's last non-OK status ("" if none). */
@@ -105,6 +106,15 @@ int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_ho
  * streams that uses the handle must be ordered after that call.
  */
 int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, lattice_t* coarse);
+
+/*
+ * lattice_coarsen with flags.  LAT_ON_STREAM builds the coarse level on
+ * `stream` itself, after the work enqueued there so far, instead of on the
+ * library's side stream: for callers that already build their lattices on a
+ * stream of their own (overlapping the construction with other work there).
+ * Unknown flag bits return LAT_EINVAL.
+ */
+int lattice_coarsen_ex(lattice_t fine, int64_t capacity_hint, int flags, hipStream_t stream, lattice_t* coarse);
 
 /* Release a handle and its device memory (LAT_ELEVEL while it has children). */
 int lattice_destroy(lattice_t L);

@@ -881,11 +881,16 @@ int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_ho
 }
 
 int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, lattice_t* coarse) {
+  return lattice_coarsen_ex(fine, capacity_hint, 0, stream, coarse);
+}
+
+int lattice_coarsen_ex(lattice_t fine, int64_t capacity_hint, int flags, hipStream_t stream, lattice_t* coarse) {
   if (!coarse) return fail(LAT_EINVAL, "out is null");
   *coarse = nullptr;
   int st;
   if ((st = check_handle_nowait(fine)) != LAT_OK) return st;
   if (capacity_hint < 0) return fail(LAT_EINVAL, "capacity_hint < 0");
+  if (flags & ~LAT_ON_STREAM) return fail(LAT_EINVAL, "unknown flags");
   lattice_s* L = new lattice_s();
   L->m = fine->m;
   L->level = fine->level + 1;
@@ -896,7 +901,7 @@ int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, l
   // The build runs on the side stream (see SideStream), after the caller's
   // stream as it is now; callers' later work is ordered after it by use().
   SideStream* side = nullptr;
-  if (L->m > 0) {
+  if (L->m > 0 && !(flags & LAT_ON_STREAM)) {
     std::lock_guard<std::mutex> lk(g_side_mu);
     if ((st = side_state(&side)) != LAT_OK) {
       delete L;

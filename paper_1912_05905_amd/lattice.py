@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "liblattice.so")
 
 LAT_F32, LAT_BF16 = 0, 1
 LAT_RELU = 1
+LAT_ON_STREAM = 1
 TAPS = 9
 STATUS = {0: "LAT_OK", -1: "LAT_EINVAL", -2: "LAT_EUNSUPPORTED", -3: "LAT_ENOMEM",
           -4: "LAT_EHASHFULL", -5: "LAT_EKEYRANGE", -6: "LAT_ENONFINITE", -7: "LAT_EDEVICE",
@@ -31,6 +32,7 @@ SIGNATURES = {
     "lattice_status_string": (C.c_char_p, [_I32]),
     "lattice_create": (_I32, [_P, _I64, _I32, _P, _I64, _P, C.POINTER(_P)]),
     "lattice_coarsen": (_I32, [_P, _I64, _P, C.POINTER(_P)]),
+    "lattice_coarsen_ex": (_I32, [_P, _I64, _I32, _P, C.POINTER(_P)]),
     "lattice_destroy": (_I32, [_P]),
     "lattice_num_vertices": (_I32, [_P, C.POINTER(_I64)]),
     "lattice_num_points": (_I32, [_P, C.POINTER(_I64)]),
@@ -132,14 +134,18 @@ def timing_read(family: str):
 class Lattice:
     """A sparse permutohedral lattice owned by liblattice."""
 
-    def __init__(self, handle: C.c_void_p, parent: "Lattice | None" = None):
+    def __init__(self, handle: C.c_void_p, parent: "Lattice | None" = None, m: int | None = None):
         self._h = handle
         self.parent = parent
         self._n = None
-        m, lv = C.c_int64(), C.c_int()
-        _check(lib().lattice_num_points(handle, C.byref(m)))
-        _check(lib().lattice_level(handle, C.byref(lv)))
-        self.m, self.level = int(m.value), int(lv.value)
+        if m is None:
+            mm, lv = C.c_int64(), C.c_int()
+            _check(lib().lattice_num_points(handle, C.byref(mm)))
+            _check(lib().lattice_level(handle, C.byref(lv)))
+            self.m, self.level = int(mm.value), int(lv.value)
+        else:
+            # known to the caller: the points of a new lattice, or of its parent
+            self.m, self.level = m, (parent.level + 1 if parent is not None else 0)
 
     @property
     def n(self) -> int:
@@ -160,12 +166,15 @@ class Lattice:
         h = C.c_void_p()
         _check(lib().lattice_create(C.c_void_p(pos.data_ptr()), pos.shape[0], pos.shape[1], sig,
                                     int(capacity_hint), _stream(stream), C.byref(h)))
-        return cls(h)
+        return cls(h, m=pos.shape[0])
 
-    def coarsen(self, capacity_hint: int = 0, stream=None) -> "Lattice":
+    def coarsen(self, capacity_hint: int = 0, stream=None, on_stream: bool = False) -> "Lattice":
+        """Coarser lattice (Downsample).  on_stream=True builds it on the
+        given (or current) stream instead of the library's side stream."""
         h = C.c_void_p()
-        _check(lib().lattice_coarsen(self._h, int(capacity_hint), _stream(stream), C.byref(h)))
-        return Lattice(h, parent=self)
+        _check(lib().lattice_coarsen_ex(self._h, int(capacity_hint), LAT_ON_STREAM if on_stream else 0,
+                                        _stream(stream), C.byref(h)))
+        return Lattice(h, parent=self, m=self.m)
 
     def destroy(self):
         if getattr(self, "_h", None):

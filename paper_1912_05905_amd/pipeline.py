@@ -45,6 +45,9 @@ class GpuPipeline:
         self.overlap = overlap
         self._build_stream = torch.cuda.Stream() if overlap else None
         self._pending: list = []      # (levels, operators-done event) of finished steps
+        self._events = [torch.cuda.Event() for _ in range(8)] if overlap else []
+        self._next_event = 0
+        self._cur = None                    # the caller's stream of the last step
         self.dtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
         self.pos = torch.from_numpy(np.ascontiguousarray(wl.positions)).cuda()
         self.feat = torch.from_numpy(np.ascontiguousarray(wl.features)).cuda().to(self.dtype)
@@ -123,12 +126,15 @@ class GpuPipeline:
                 b = base[name] = (store.data_ptr(), total)
             return b[0] + c0 * es, b[1]
 
-        def build():
+        def build(bstream=None):
             for op in wl.ops:
                 if op["op"] == "create":
-                    levels[0] = Lattice.create(self.pos, self.sigma)
+                    levels[0] = Lattice.create(self.pos, self.sigma, stream=bstream)
                 elif op["op"] == "coarsen":
-                    levels[op["level"]] = levels[op["level"] - 1].coarsen()
+                    # on a build stream of its own the hierarchy is already off
+                    # the operators' stream: no side stream needed
+                    levels[op["level"]] = levels[op["level"] - 1].coarsen(stream=bstream,
+                                                                          on_stream=bstream is not None)
 
         if self.overlap and not keep:
             # destroy the lattices of all but the last finished step; their
@@ -138,13 +144,12 @@ class GpuPipeline:
             while len(self._pending) > 1:
                 old, done = self._pending.pop(0)
                 bs.wait_event(done)
-                with torch.cuda.stream(bs):
-                    GpuPipeline.release(old)
-            with torch.cuda.stream(bs):
-                build()
-            built = torch.cuda.Event()
+                GpuPipeline.release(old)
+            build(bs)
+            built = self._event()
             built.record(bs)
-            torch.cuda.current_stream().wait_event(built)
+            self._cur = torch.cuda.current_stream()
+            self._cur.wait_event(built)
         else:
             build()
         skip = False
@@ -269,9 +274,16 @@ class GpuPipeline:
         if not self.overlap:
             GpuPipeline.release(levels)
             return
-        done = torch.cuda.Event()
-        done.record(torch.cuda.current_stream())
+        done = self._event()
+        done.record(self._cur)
         self._pending.append((levels, done))
+
+    def _event(self):
+        # a ring of events: a re-record does not affect waits already enqueued,
+        # and at most two steps are pending
+        e = self._events[self._next_event]
+        self._next_event = (self._next_event + 1) % len(self._events)
+        return e
 
     def flush(self):
         """Release every lattice still held (overlap mode)."""

@@ -33,7 +33,7 @@ def test_header_declares_the_boundary():
                  "lattice_num_vertices", "lattice_export_keys", "lattice_export_neighbors",
                  "lattice_export_simplices", "lattice_distribute_pointnet", "lattice_splat_backward",
                  "lattice_slice_backward", "lattice_conv_backward", "lattice_deform_slice_backward", "lattice_conv_preact", "lattice_deform_slice_classify",
-                 "lattice_refine_preact", "lattice_slice_and_deform"):
+                 "lattice_refine_preact", "lattice_slice_and_deform", "lattice_coarsen_ex"):
         assert need in names
 
 
@@ -76,6 +76,7 @@ def test_host_validation_without_gpu(lib):
     assert lib.lattice_distribute_pointnet(None, None, None, 0, 4, None, None, 16, None, None, 32, None, None, 64,
                                            None, 0, None) == -1
     assert lib.lattice_coarsen(None, 0, None, C.byref(out)) == -1
+    assert lib.lattice_coarsen_ex(None, 0, 0, None, C.byref(out)) == -1
     assert lib.lattice_splat_backward(None, None, 0, 8, 1, None, None, None) == -1
     assert lib.lattice_slice_backward(None, None, 0, 8, None, 0, None) == -1
     assert lib.lattice_conv_backward(None, None, None, 0, 8, None, 8, 0, None, 0, None, 0, None, 0, None, None,

@@ -7,6 +7,8 @@ Every call goes through the C ABI via the ctypes binding.
 """
 from __future__ import annotations
 
+import ctypes
+
 import numpy as np
 import pytest
 
@@ -97,16 +99,19 @@ def test_create_structure_configs(L, O, cfg):
     _check_structure(gl, ol)
 
 
-@pytest.mark.parametrize("cfg", [2, 4])
-def test_coarsen_structure(L, O, cfg):
+@pytest.mark.parametrize("cfg,on_stream", [(2, False), (4, False), (4, True)])
+def test_coarsen_structure(L, O, cfg, on_stream):
     wl = configs.make(cfg)
     gl = L.Lattice.create(_dev(wl.positions), wl.sigma)
     ol = O.Lattice.create(wl.positions, wl.sigma)
     glv, olv = [gl], [ol]
     for lvl in range(1, 4):
-        glv.append(glv[-1].coarsen())
+        glv.append(glv[-1].coarsen(on_stream=on_stream))
         olv.append(olv[-1].coarsen())
         assert glv[-1].level == lvl
+        lv_c, m_c = ctypes.c_int(), ctypes.c_int64()
+        assert L.lib().lattice_level(glv[-1].handle, ctypes.byref(lv_c)) == 0 and lv_c.value == lvl
+        assert L.lib().lattice_num_points(glv[-1].handle, ctypes.byref(m_c)) == 0 and m_c.value == gl.m
         _check_structure(glv[-1], olv[-1])
 
 
