@@ -11,6 +11,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int64_t kDeformBwdGrid = 1024;   // workgroups of the DeformSlice backward's per-point pass
+constexpr unsigned kClassifyGrid = 2048;   // workgroups of the fused classifier (a multiple of 8)
 constexpr int kClassifyMaxWeights = 16384; // K x C classifier weights staged in LDS
 
 // float -> bfloat16, round to nearest even (NaN stays NaN).
@@ -555,23 +556,52 @@ k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64
 // One exchange of the reduce-scatter in k_deform_classify: lanes whose bit
 // OFF is set keep the upper LEN values, the others the lower LEN, and each
 // adds the half its partner gives away.
-template <int LPR, int OFF, int LEN, int KP>
-__device__ inline void reduce_scatter_step(float (&lg)[KP], int lane) {
+// Value of lane ^ OFF: DPP for partners inside a 16-lane row that DPP can
+// name (xor 1 and 2 by quad permutation, xor 8 as a rotation by 8), a
+// swizzle for xor 4 and 16 (within 32 lanes), a permute across halves.
+template <int OFF>
+__device__ inline float xor_lane(float v) {
+  const int x = __float_as_int(v);
+  if constexpr (OFF == 1) return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false));
+  else if constexpr (OFF == 2) return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false));
+  else if constexpr (OFF == 8) return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x128, 0xF, 0xF, false));
+  else if constexpr (OFF == 4 || OFF == 16) return __int_as_float(__builtin_amdgcn_ds_swizzle(x, 0x1F | (OFF << 10)));
+  else return __shfl_xor(v, OFF);
+}
+
+// One exchange of the reduce-scatter in k_deform_classify: lanes whose bit
+// OFF is set keep the upper LEN values, the others the lower LEN, and each
+// adds the half its partner gives away; blk gathers the kept halves' bits.
+template <int OFF, int LEN, int KP>
+__device__ inline void reduce_scatter_step(float (&lg)[KP], int lane, int& blk) {
   const bool up = (lane & OFF) != 0;
 #pragma unroll
   for (int i = 0; i < LEN; ++i) {
     const float give = up ? lg[i] : lg[i + LEN];
     const float keep = up ? lg[i + LEN] : lg[i];
-    lg[i] = keep + __shfl_xor(give, OFF, LPR);
+    lg[i] = keep + xor_lane<OFF>(give);
   }
+  blk = 2 * blk + (up ? 1 : 0);
+}
+
+// Sum over the LPR lanes of a group, every lane receiving it.
+template <int LPR>
+__device__ inline float group_sum(float v) {
+  if constexpr (LPR > 1) v += xor_lane<1>(v);
+  if constexpr (LPR > 2) v += xor_lane<2>(v);
+  if constexpr (LPR > 4) v += xor_lane<4>(v);
+  if constexpr (LPR > 8) v += xor_lane<8>(v);
+  if constexpr (LPR > 16) v += xor_lane<16>(v);
+  if constexpr (LPR > 32) v += xor_lane<32>(v);
+  return v;
 }
 
 // DeformSlice fused with the last linear classification layer
 // (Implementation): the DeformSlice row of a point is formed in registers as
 // in k_deform_slice and multiplied by Wc (K x C, staged in LDS); the KP >= K
 // logit partials of a lane group are summed by a reduce-scatter, after which
-// lane L holds classes L * KP / LPR .. + KP / LPR - 1.  The high-dimensional
-// per-point row is never stored.
+// each lane holds KP / LPR finished classes (the block its exchange bits
+// name).  The high-dimensional per-point row is never stored.
 template <bool BF16, int LPR, int CPL, int KP>
 __global__ void __launch_bounds__(kBlock)
 k_deform_classify(const int4* __restrict__ idx, const float4* __restrict__ w, int64_t m,
@@ -583,9 +613,17 @@ k_deform_classify(const int4* __restrict__ idx, const float4* __restrict__ w, in
   for (int i = threadIdx.x; i < K * C; i += kBlock) wl[i] = Wc[i];
   __syncthreads();
   const int lane = threadIdx.x & (LPR - 1);
-  const int64_t p = xcd_item<LPR>(nblk);
-  const bool live = p < m;
   const int nchunk = C / Ch::N;
+  // The weights are staged once per workgroup, which then walks a
+  // contiguous range of the nblk logical blocks (each XCD a contiguous
+  // share of the ranges, as xcd_item).
+  const unsigned G = gridDim.x;   // a multiple of 8
+  const unsigned r = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
+  const unsigned per = (nblk + G - 1) / G;
+  const unsigned lb1 = min((r + 1) * per, nblk);
+  for (unsigned lb = r * per; lb < lb1; ++lb) {
+  const int64_t p = (static_cast<int64_t>(lb) * kBlock + threadIdx.x) / LPR;
+  const bool live = p < m;
   int4 iv = make_int4(-1, -1, -1, -1);
   float4 wq = make_float4(0.f, 0.f, 0.f, 0.f);
   if (live) { iv = idx[p]; wq = w[p]; }
@@ -626,9 +664,7 @@ k_deform_classify(const int4* __restrict__ idx, const float4* __restrict__ w, in
     }
   }
 #pragma unroll
-  for (int off = LPR / 2; off > 0; off >>= 1)
-#pragma unroll
-    for (int k = 0; k < 4; ++k) part[k] += __shfl_xor(part[k], off, LPR);
+  for (int k = 0; k < 4; ++k) part[k] = group_sum<LPR>(part[k]);
   float coef[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) coef[k] = bw[k] + tanhf(beta + part[k]);
@@ -654,18 +690,25 @@ k_deform_classify(const int4* __restrict__ idx, const float4* __restrict__ w, in
       }
     }
   }
-  if constexpr (LPR >= 2) reduce_scatter_step<LPR, LPR / 2, KP / 2>(lg, lane);
-  if constexpr (LPR >= 4) reduce_scatter_step<LPR, LPR / 4, KP / 4>(lg, lane);
-  if constexpr (LPR >= 8) reduce_scatter_step<LPR, LPR / 8, KP / 8>(lg, lane);
-  if constexpr (LPR >= 16) reduce_scatter_step<LPR, LPR / 16, KP / 16>(lg, lane);
-  if constexpr (LPR >= 32) reduce_scatter_step<LPR, LPR / 32, KP / 32>(lg, lane);
-  if constexpr (LPR >= 64) reduce_scatter_step<LPR, LPR / 64, KP / 64>(lg, lane);
-  if (!live) return;
-  constexpr int OWN = KP / LPR;
+  // the exchanges in the order of their cost (cheap ones move the most
+  // values); blk = the class block this lane keeps
+  int blk = 0;
+  constexpr int S = (LPR >= 2) + (LPR >= 4) + (LPR >= 8) + (LPR >= 16) + (LPR >= 32) + (LPR >= 64);
+  static_assert((KP >> S) >= 1, "at least one class per lane");
+  if constexpr (LPR >= 2) reduce_scatter_step<1, (KP >> 1)>(lg, lane, blk);
+  if constexpr (LPR >= 4) reduce_scatter_step<2, (KP >> 2)>(lg, lane, blk);
+  if constexpr (LPR >= 16) reduce_scatter_step<8, (KP >> 3)>(lg, lane, blk);
+  if constexpr (LPR >= 8) reduce_scatter_step<4, (KP >> (LPR >= 16 ? 4 : 3))>(lg, lane, blk);
+  if constexpr (LPR >= 32) reduce_scatter_step<16, (KP >> 5)>(lg, lane, blk);
+  if constexpr (LPR >= 64) reduce_scatter_step<32, (KP >> 6)>(lg, lane, blk);
+  if (live) {
+    constexpr int OWN = KP / LPR;
 #pragma unroll
-  for (int i = 0; i < OWN; ++i) {
-    const int j = lane * OWN + i;
-    if (j < K) out[p * K + j] = lg[i] + (bc ? bc[j] : 0.f);
+    for (int i = 0; i < OWN; ++i) {
+      const int j = blk * OWN + i;
+      if (j < K) out[p * K + j] = lg[i] + (bc ? bc[j] : 0.f);
+    }
+  }
   }
 }
 
@@ -1003,7 +1046,7 @@ void deform_classify_dispatch(int lpr, const int32_t* idx, const float* w, int64
                               int C, const float* wv, float beta, const float* Wc, const float* bc, int K,
                               float* out, hipStream_t s) {
   const unsigned nblk = grid_for(m, lpr);
-  const dim3 g(xcd_grid(nblk)), b(kBlock);
+  const dim3 g(std::min(xcd_grid(nblk), kClassifyGrid)), b(kBlock);
   const int4* i4 = reinterpret_cast<const int4*>(idx);
   const float4* w4 = reinterpret_cast<const float4*>(w);
   const uint32_t lds = static_cast<uint32_t>(4 * K * C);
