@@ -35,6 +35,32 @@ __device__ inline int64_t xcd_item(unsigned nblocks_logical) {
 
 inline unsigned xcd_grid(unsigned nblocks_logical) { return ((nblocks_logical + 7) / 8) * 8; }
 
+// Value of lane ^ OFF: DPP for partners inside a 16-lane row that DPP can
+// name (xor 1 and 2 by quad permutation, xor 8 as a rotation by 8), a
+// swizzle for xor 4 and 16 (within 32 lanes), a permute across halves.
+template <int OFF>
+__device__ inline float xor_lane(float v) {
+  const int x = __float_as_int(v);
+  if constexpr (OFF == 1) return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false));
+  else if constexpr (OFF == 2) return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false));
+  else if constexpr (OFF == 8) return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x128, 0xF, 0xF, false));
+  else if constexpr (OFF == 4 || OFF == 16) return __int_as_float(__builtin_amdgcn_ds_swizzle(x, 0x1F | (OFF << 10)));
+  else return __shfl_xor(v, OFF);
+}
+
+// Sum over the LPR lanes of a group, every lane receiving it.
+template <int LPR>
+__device__ inline float group_sum(float v) {
+  if constexpr (LPR > 1) v += xor_lane<1>(v);
+  if constexpr (LPR > 2) v += xor_lane<2>(v);
+  if constexpr (LPR > 4) v += xor_lane<4>(v);
+  if constexpr (LPR > 8) v += xor_lane<8>(v);
+  if constexpr (LPR > 16) v += xor_lane<16>(v);
+  if constexpr (LPR > 32) v += xor_lane<32>(v);
+  return v;
+}
+
+
 // A 16-byte chunk of a row as 8 floats (bf16) or 4 floats (fp32).
 template <bool BF16> struct Chunk;
 template <> struct Chunk<false> {
@@ -507,9 +533,7 @@ k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64
     }
   }
 #pragma unroll
-  for (int off = LPR / 2; off > 0; off >>= 1)
-#pragma unroll
-    for (int k = 0; k < 4; ++k) part[k] += __shfl_xor(part[k], off, LPR);
+  for (int k = 0; k < 4; ++k) part[k] = group_sum<LPR>(part[k]);
   if (!live) return;
   float coef[4];
 #pragma unroll
@@ -556,18 +580,9 @@ k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64
 // One exchange of the reduce-scatter in k_deform_classify: lanes whose bit
 // OFF is set keep the upper LEN values, the others the lower LEN, and each
 // adds the half its partner gives away.
-// Value of lane ^ OFF: DPP for partners inside a 16-lane row that DPP can
-// name (xor 1 and 2 by quad permutation, xor 8 as a rotation by 8), a
-// swizzle for xor 4 and 16 (within 32 lanes), a permute across halves.
-template <int OFF>
-__device__ inline float xor_lane(float v) {
-  const int x = __float_as_int(v);
-  if constexpr (OFF == 1) return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false));
-  else if constexpr (OFF == 2) return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false));
-  else if constexpr (OFF == 8) return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x128, 0xF, 0xF, false));
-  else if constexpr (OFF == 4 || OFF == 16) return __int_as_float(__builtin_amdgcn_ds_swizzle(x, 0x1F | (OFF << 10)));
-  else return __shfl_xor(v, OFF);
-}
+// One exchange of the reduce-scatter in k_deform_classify: lanes whose bit
+// OFF is set keep the upper LEN values, the others the lower LEN, and each
+// adds the half its partner gives away.
 
 // One exchange of the reduce-scatter in k_deform_classify: lanes whose bit
 // OFF is set keep the upper LEN values, the others the lower LEN, and each
@@ -584,17 +599,6 @@ __device__ inline void reduce_scatter_step(float (&lg)[KP], int lane, int& blk) 
   blk = 2 * blk + (up ? 1 : 0);
 }
 
-// Sum over the LPR lanes of a group, every lane receiving it.
-template <int LPR>
-__device__ inline float group_sum(float v) {
-  if constexpr (LPR > 1) v += xor_lane<1>(v);
-  if constexpr (LPR > 2) v += xor_lane<2>(v);
-  if constexpr (LPR > 4) v += xor_lane<4>(v);
-  if constexpr (LPR > 8) v += xor_lane<8>(v);
-  if constexpr (LPR > 16) v += xor_lane<16>(v);
-  if constexpr (LPR > 32) v += xor_lane<32>(v);
-  return v;
-}
 
 // DeformSlice fused with the last linear classification layer
 // (Implementation): the DeformSlice row of a point is formed in registers as
@@ -789,12 +793,10 @@ k_deform_bwd_point(const int4* __restrict__ idx, const float4* __restrict__ w, i
       if (on) *reinterpret_cast<uint32_t*>(am + p * C + 4 * ch) = word;
     }
 #pragma unroll
-    for (int off = LPR / 2; off > 0; off >>= 1)
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        sp[k] += __shfl_xor(sp[k], off, LPR);
-        ap[k] += __shfl_xor(ap[k], off, LPR);
-      }
+    for (int k = 0; k < 4; ++k) {
+      sp[k] = group_sum<LPR>(sp[k]);
+      ap[k] = group_sum<LPR>(ap[k]);
+    }
     float e[4], esum = 0.f;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
