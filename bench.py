@@ -23,6 +23,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"hbm": 8.0e12, "mfma_f32": 157.3e12, "mfma_bf16": 2.5e15}
+BUILD_FAMILIES = {"fill", "insert", "scan", "lists", "nbr"}
 FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "distribute", "groupnorm", "conv", "slice",
             "deform_slice", "deform_bwd", "conv_bwd", "splat_bwd", "slice_bwd"]
 # kernel symbol fragments of each family (rocprofv3 kernel names; first match
@@ -105,10 +106,12 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mb,
             if counter == "FETCH_SIZE":
                 ent["dispatches"] += len(vals)
     runs = warmup + 1 + 2 * steps  # warmup, instrumented step, the two timed regions of the profiled run
-    for ent in fams.values():
-        ent["fetch_bytes_per_step"] = ent.pop("fetch_bytes") / runs
-        ent["write_bytes_per_step"] = ent.pop("write_bytes") / runs
-        ent["dispatches_per_step"] = ent.pop("dispatches") / runs
+    for fam, ent in fams.items():
+        # lattices are built one cloud ahead: one more hierarchy than steps
+        n = runs + 1 if fam in BUILD_FAMILIES else runs
+        ent["fetch_bytes_per_step"] = ent.pop("fetch_bytes") / n
+        ent["write_bytes_per_step"] = ent.pop("write_bytes") / n
+        ent["dispatches_per_step"] = ent.pop("dispatches") / n
     data = json.load(open(TRAFFIC_FILE)) if os.path.exists(TRAFFIC_FILE) else {}
     stamp = os.path.join(fetch_dir, "source_hash.txt")
     if not os.path.exists(stamp):

@@ -34,17 +34,22 @@ class _Buffers(dict):
 
 
 class GpuPipeline:
-    """overlap=True builds each step's lattices on a stream of their own, so
-    that the next cloud's lattice construction runs while this cloud's
-    operators still execute (steps are independent).  A step's lattices are
-    then destroyed by finish_step() one step later, once the build stream is
-    ordered after the step's operators."""
+    """overlap=True builds the lattices on a stream of their own and one
+    cloud ahead: a step issues the next cloud's hierarchy, then runs this
+    cloud's operators on the hierarchy the previous step issued, so the next
+    cloud's lattice construction runs while this cloud's operators execute
+    (steps are independent; every step builds one hierarchy and runs one
+    pass of operators).  A step's lattices are destroyed by finish_step() one
+    step later, once the build stream is ordered after the step's operators;
+    flush() releases what is still held, the hierarchy built ahead
+    included."""
 
     def __init__(self, wl, overlap=False):
         self.wl = wl
         self.overlap = overlap
         self._build_stream = torch.cuda.Stream() if overlap else None
         self._pending: list = []      # (levels, operators-done event) of finished steps
+        self._ahead = None            # (levels, built event) of the next cloud
         self._events = [torch.cuda.Event() for _ in range(8)] if overlap else []
         self._next_event = 0
         self._cur = None                    # the caller's stream of the last step
@@ -126,32 +131,48 @@ class GpuPipeline:
                 b = base[name] = (store.data_ptr(), total)
             return b[0] + c0 * es, b[1]
 
-        def build(bstream=None):
+        def build(into, bstream=None):
             for op in wl.ops:
                 if op["op"] == "create":
-                    levels[0] = Lattice.create(self.pos, self.sigma, stream=bstream)
+                    into[0] = Lattice.create(self.pos, self.sigma, stream=bstream)
                 elif op["op"] == "coarsen":
                     # on a build stream of its own the hierarchy is already off
                     # the operators' stream: no side stream needed
-                    levels[op["level"]] = levels[op["level"] - 1].coarsen(stream=bstream,
-                                                                          on_stream=bstream is not None)
+                    into[op["level"]] = into[op["level"] - 1].coarsen(stream=bstream,
+                                                                      on_stream=bstream is not None)
 
         if self.overlap and not keep:
+            # Builds run one cloud ahead: this step issues the next cloud's
+            # hierarchy on the build stream, then this cloud's operators on
+            # the caller's stream, on the hierarchy issued a step earlier.
+            # The next build then runs under this cloud's operators, and the
+            # vertex counts the operators need are normally home already.
+            bs = self._build_stream
+            ahead = self._ahead
+            if ahead is None:
+                first: dict[int, Lattice] = {}
+                build(first, bs)
+                ev = self._event()
+                ev.record(bs)
+                ahead = (first, ev)
             # destroy the lattices of all but the last finished step; their
             # buffers return to the build stream's pool once that stream has
             # passed the step's operators
-            bs = self._build_stream
             while len(self._pending) > 1:
                 old, done = self._pending.pop(0)
                 bs.wait_event(done)
                 GpuPipeline.release(old)
-            build(bs)
-            built = self._event()
-            built.record(bs)
+            nxt: dict[int, Lattice] = {}
+            build(nxt, bs)
+            ev = self._event()
+            ev.record(bs)
+            self._ahead = (nxt, ev)
+            levels.update(ahead[0])
             self._cur = torch.cuda.current_stream()
-            self._cur.wait_event(built)
+            self._cur.wait_event(ahead[1])
         else:
-            build()
+            build(levels)
+
         skip = False
         for i, op in enumerate(wl.ops):
             kind = op["op"]
@@ -291,6 +312,9 @@ class GpuPipeline:
         for old, _ in self._pending:
             GpuPipeline.release(old)
         self._pending = []
+        if self._ahead is not None:
+            GpuPipeline.release(self._ahead[0])
+            self._ahead = None
 
     @staticmethod
     def release(levels):
