@@ -221,7 +221,8 @@ def _pair(L, O, pos, sigma):
     return gl, ol, g2o
 
 
-@pytest.mark.parametrize("C,normalize", [(4, True), (8, True), (36, False), (64, True), (256, True)])
+@pytest.mark.parametrize("C,normalize", [(4, True), (8, True), (36, False), (64, True), (256, True), (320, False),
+                                         (512, True)])
 def test_splat(L, O, C, normalize):
     pos = _cloud(10 + C, 9000, 0.7)
     gl, ol, g2o = _pair(L, O, pos, 0.06)
@@ -233,8 +234,8 @@ def test_splat(L, O, C, normalize):
     P.assert_close(P.rows_in_oracle_order(_host(ws), g2o), ow, P.TOL_F32, "wsum")
 
 
-@pytest.mark.parametrize("C,dtype", [(4, "f32"), (36, "f32"), (64, "f32"), (256, "f32"), (64, "bf16"),
-                                     (512, "bf16")])
+@pytest.mark.parametrize("C,dtype", [(4, "f32"), (36, "f32"), (64, "f32"), (256, "f32"), (512, "f32"), (64, "bf16"),
+                                     (512, "bf16"), (1024, "bf16")])
 def test_splat_skewed(L, O, C, dtype):
     """Vertex lists far longer than a workgroup span (a 6000-point clump
     inside one simplex), next to short ones and a ragged end."""
