@@ -487,6 +487,64 @@ def test_pipeline_full_size(L, O, cfg):
     _run_both(L, O, configs.make(cfg))
 
 
+def test_pipeline_config5_full_size_sampled(L, O):
+    """The 1M-point bf16 U-Net at full size, operator by operator on the
+    GPU's own inputs (the oracle would need minutes for the whole network):
+    the four-level hierarchy bit-exact, splat on every vertex, each of the
+    thirteen convolutions on a seeded sample of 4,000 output rows (1-hop,
+    strided and Upsample, concatenated column ranges included), DeformSlice
+    on 50,000 points.  Every operator's inputs are the bf16 values the GPU
+    stored, so each comparison is one rounding deep."""
+    from paper_1912_05905_amd.pipeline import GpuPipeline
+    wl = configs.make(5)
+    pipe = GpuPipeline(wl)
+    levels, bufs, outs = pipe.step(keep=True)
+    olv = {}
+    for op in wl.ops:
+        if op["op"] == "create":
+            olv[0] = O.Lattice.create(wl.positions, wl.sigma)
+        elif op["op"] == "coarsen":
+            olv[op["level"]] = olv[op["level"] - 1].coarsen()
+    g2o = {lv: _check_structure(levels[lv], olv[lv]) for lv in sorted(levels)}
+    host = {}
+
+    def cols(spec):
+        name, c0, cc = spec
+        if name not in host:
+            host[name] = P.rows_in_oracle_order(_host(bufs[name]), g2o[wl.buffers[name][0]])
+        return np.ascontiguousarray(host[name][:, c0:c0 + cc], dtype=np.float64)
+
+    rng = np.random.default_rng(55)
+    checked = 0
+    for op in wl.ops:
+        kind = op["op"]
+        if kind == "splat":
+            X, _ = olv[0].splat(wl.features.astype(np.float64), normalize=bool(op["normalize"]))
+            P.assert_close(cols(op["dst"]), O.round_bf16(X), P.TOL_BF16, "splat")
+            checked += 1
+        elif kind in ("conv", "conv_down", "refine"):
+            lv = op["level"]
+            x = cols(op["src"])
+            W = wl.weights[op["w"]].astype(np.float64)
+            rows = np.sort(rng.choice(olv[lv].n, size=min(4000, olv[lv].n), replace=False))
+            if kind == "conv":
+                y = olv[lv].conv(olv[lv], x, W, relu=op["relu"], rows=rows)
+            elif kind == "conv_down":
+                y = olv[lv].conv(olv[lv - 1], x, W, relu=op["relu"], rows=rows)
+            else:
+                y = olv[lv].refine_into(olv[lv + 1], x, W, relu=op["relu"], rows=rows)
+            P.assert_close(cols(op["dst"])[rows], O.round_bf16(y), P.TOL_BF16, f"{kind} -> {op['dst']}")
+            checked += 1
+        elif kind == "deform_slice":
+            wv, beta = wl.vectors[op["wv"]]
+            pts = np.sort(rng.choice(wl.m, size=50_000, replace=False))
+            ref, _ = olv[0].deform_slice(cols(op["src"]), wv.astype(np.float64), beta, pts=pts)
+            P.assert_close(_host(outs[op["out"]])[pts], ref, P.TOL_F32, "deform slice")
+            checked += 1
+    assert checked == 15
+    GpuPipeline.release(levels)
+
+
 def test_pipeline_overlapped_steps(L, O):
     """Steps whose lattice builds overlap the previous step's operators (the
     bench's mode): every step's point outputs match the oracle."""
