@@ -4,6 +4,9 @@
 // per access so that a row is one contiguous, fully used transaction.
 #include <algorithm>
 
+#include <type_traits>
+#include <utility>
+
 #include "lattice_internal.h"
 
 namespace lat {
@@ -34,6 +37,22 @@ __device__ inline int64_t xcd_item(unsigned nblocks_logical) {
 }
 
 inline unsigned xcd_grid(unsigned nblocks_logical) { return ((nblocks_logical + 7) / 8) * 8; }
+
+// f(std::integral_constant<int, i>) for i = 0 .. N-1, unrolled.
+template <class F, int... I>
+__device__ inline void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ inline void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Value of lane J of this lane's 16-lane row (DPP row broadcast).
+template <int J>
+__device__ inline int32_t row_bcast(int32_t x) {
+  return __builtin_amdgcn_update_dpp(0, x, 0x150 + J, 0xF, 0xF, false);
+}
 
 // Value of lane ^ OFF: DPP for partners inside a 16-lane row that DPP can
 // name (xor 1 and 2 by quad permutation, xor 8 as a rotation by 8), a
@@ -179,7 +198,20 @@ struct WeightedRows {
     float wt[B];
     Ch f[B][Q];
   };
+  static constexpr bool kGivenWeights = true;   // the kernel may load entry_w itself
   __device__ inline void init(int, int) {}
+  __device__ inline void load_given(Batch& bt, int j, float w, int32_t e, bool in, int lane, int nchunk) const {
+    bt.wt[j] = in ? w : 0.f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int ch = lane + q * LPR;
+      if (in && ch < nchunk)
+        bt.f[j][q].load(feat, static_cast<int64_t>(e >> 2) * ld_feat + static_cast<int64_t>(ch) * Ch::N);
+      else
+#pragma unroll
+        for (int i = 0; i < Ch::N; ++i) bt.f[j][q].v[i] = 0.f;
+    }
+  }
   __device__ inline void load(Batch& bt, int j, int64_t s, int32_t e, bool in, int lane, int nchunk) const {
     bt.wt[j] = in ? entry_w[s] : 0.f;
 #pragma unroll
@@ -208,6 +240,7 @@ struct WeightedRows {
 template <int LPR, int Q, int B>
 struct DeformGradRows {
   using Ch = Chunk<false>;
+  static constexpr bool kGivenWeights = false;
   const float* g;
   int64_t ld_g;
   const float4* coef;
@@ -309,48 +342,87 @@ k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
 #pragma unroll
       for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
     float ws = 0.f;
-    // the entries of the next batch are loaded while this batch's rows
-    // arrive and are added
-    int32_t e[B];
+    // what entry s (and the batch slot j it sits in) adds: the vertex's
+    // running sum, and at the vertex's last entry (or the chunk's) its row or
+    // piece
+    auto consume = [&](const typename Rows::Batch& bt, int j, int64_t s) {
+      ws += rows.add(bt, j, acc);
+      const int64_t nxt = s + 1;
+      if (nxt == ve || nxt == s1) {
+        if (vb >= s0 && ve <= s1) {
+          splat_store<BF16, LPR, Q>(v, acc, ws, lane, nchunk, normalize, vals, ld_vals, wsum);
+        } else if (vb < s0) {
+          splat_partial<BF16, LPR, Q>(sh_head, sh_w, g, 0, acc, ws, lane, C);
+          if (lane == 0) sh_flag[g] |= 1;
+        } else {
+          splat_partial<BF16, LPR, Q>(sh_tail, sh_w, g, 1, acc, ws, lane, C);
+          if (lane == 0) sh_flag[g] |= 2;
+          tail_v = v;
+          tail_ve = ve;
+        }
 #pragma unroll
-    for (int j = 0; j < B; ++j) e[j] = s0 + j < s1 ? entries[s0 + j] : 0;
-    for (int64_t s = s0; s < s1; s += B) {
-      typename Rows::Batch bt;
+        for (int q = 0; q < Q; ++q)
 #pragma unroll
-      for (int j = 0; j < B; ++j) rows.load(bt, j, s + j, e[j], s + j < s1, lane, nchunk);
-#pragma unroll
-      for (int j = 0; j < B; ++j) e[j] = s + B + j < s1 ? entries[s + B + j] : 0;
-#pragma unroll
-      for (int j = 0; j < B; ++j) {
-        if (s + j >= s1) break;
-        ws += rows.add(bt, j, acc);
-        const int64_t nxt = s + j + 1;
-        if (nxt == ve || nxt == s1) {
-          if (vb >= s0 && ve <= s1) {
-            splat_store<BF16, LPR, Q>(v, acc, ws, lane, nchunk, normalize, vals, ld_vals, wsum);
-          } else if (vb < s0) {
-            splat_partial<BF16, LPR, Q>(sh_head, sh_w, g, 0, acc, ws, lane, C);
-            if (lane == 0) sh_flag[g] |= 1;
-          } else {
-            splat_partial<BF16, LPR, Q>(sh_tail, sh_w, g, 1, acc, ws, lane, C);
-            if (lane == 0) sh_flag[g] |= 2;
-            tail_v = v;
-            tail_ve = ve;
+          for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
+        ws = 0.f;
+        if (nxt == ve && nxt < s1) {
+          v += 1;
+          vb = ve;
+          if (v - v_win >= LPR) {
+            v_win = v;
+            win = offsets[min(static_cast<int64_t>(v) + 1 + lane, n)];
           }
+          ve = __shfl(win, v - v_win, LPR);
+        }
+      }
+    };
+    if constexpr (LPR == 16 && Rows::kGivenWeights) {
+      // 16 entries at a time: lane i loads the index and weight of entry i,
+      // and a row broadcast (DPP, a 16-lane row is one lane group) hands
+      // entry j's to the whole group; the next 16 are loaded while this
+      // round's rows arrive
+      int32_t E = s0 + lane < s1 ? entries[s0 + lane] : 0;
+      float Wt = s0 + lane < s1 ? rows.entry_w[s0 + lane] : 0.f;
+      for (int64_t sb = s0; sb < s1; sb += 16) {
+        const int64_t nx = sb + 16 + lane;
+        const int32_t En = nx < s1 ? entries[nx] : 0;
+        const float Wn = nx < s1 ? rows.entry_w[nx] : 0.f;
+        static_for<16 / B>([&](auto h_c) {
+          constexpr int J0 = decltype(h_c)::value * B;
+          if (sb + J0 < s1) {
+            typename Rows::Batch bt;
+            static_for<B>([&](auto j_c) {
+              constexpr int J = decltype(j_c)::value;
+              const int32_t e = row_bcast<J0 + J>(E);
+              const float w = __int_as_float(row_bcast<J0 + J>(__float_as_int(Wt)));
+              rows.load_given(bt, J, w, e, sb + J0 + J < s1, lane, nchunk);
+            });
 #pragma unroll
-          for (int q = 0; q < Q; ++q)
-#pragma unroll
-            for (int i = 0; i < Ch::N; ++i) acc[q][i] = 0.f;
-          ws = 0.f;
-          if (nxt == ve && nxt < s1) {
-            v += 1;
-            vb = ve;
-            if (v - v_win >= LPR) {
-              v_win = v;
-              win = offsets[min(static_cast<int64_t>(v) + 1 + lane, n)];
+            for (int j = 0; j < B; ++j) {
+              if (sb + J0 + j >= s1) break;
+              consume(bt, j, sb + J0 + j);
             }
-            ve = __shfl(win, v - v_win, LPR);
           }
+        });
+        E = En;
+        Wt = Wn;
+      }
+    } else {
+      // the entries of the next batch are loaded while this batch's rows
+      // arrive and are added
+      int32_t e[B];
+#pragma unroll
+      for (int j = 0; j < B; ++j) e[j] = s0 + j < s1 ? entries[s0 + j] : 0;
+      for (int64_t s = s0; s < s1; s += B) {
+        typename Rows::Batch bt;
+#pragma unroll
+        for (int j = 0; j < B; ++j) rows.load(bt, j, s + j, e[j], s + j < s1, lane, nchunk);
+#pragma unroll
+        for (int j = 0; j < B; ++j) e[j] = s + B + j < s1 ? entries[s + B + j] : 0;
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+          if (s + j >= s1) break;
+          consume(bt, j, s + j);
         }
       }
     }
