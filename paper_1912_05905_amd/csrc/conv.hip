@@ -248,7 +248,6 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   E* Bs = reinterpret_cast<E*>(smem + 2 * P::A_BYTES);
   int32_t* nbt = reinterpret_cast<int32_t*>(smem + 2 * (P::A_BYTES + P::B_BYTES));
   int32_t* tflag = nbt + kTaps * BM;  // [16] tap used by some row of the tile
-  int32_t* tlist = tflag + 16;        // [16] used taps, count in tlist[15]
   float* pre_s = reinterpret_cast<float*>(smem + P::LDS_BYTES);   // PRE: [Cin] scales, [Cin] shifts
 
   const int tid = threadIdx.x;
@@ -284,16 +283,19 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
     if (nb >= 0) tflag[t] = 1;
   }
   __syncthreads();
-  if (tid == 0) {
-    int k = 0;
-    for (int t = 0; t < te - tb; ++t)
-      if (tflag[t]) tlist[k++] = t;
-    tlist[15] = k;
-  }
-  __syncthreads();
+  // the used taps in order, 4 bits each; every thread packs them itself
+  uint64_t tpack = 0;
+  int ntaps = 0;
+#pragma unroll
+  for (int t = 0; t < kTaps; ++t)
+    if (t < te - tb && tflag[t]) {
+      tpack |= static_cast<uint64_t>(t) << (4 * ntaps);
+      ++ntaps;
+    }
+  auto tap_at = [&](int ti) { return static_cast<int>((tpack >> (4 * ti)) & 15); };
 
   const int kc_steps = (Cin + P::KC - 1) / P::KC;
-  const int stages = tlist[15] * kc_steps;
+  const int stages = ntaps * kc_steps;
 
   // global -> register copies of one stage.  Every load is issued, also for
   // a missing neighbour, a channel past Cin or a stage past the last: with
@@ -322,7 +324,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
     constexpr int set = decltype(set_c)::value;
     const bool live = st < stages;
     const int ti = min(st / kc_steps, 15);
-    const int t = live ? tlist[ti] : 0;
+    const int t = live ? tap_at(ti) : 0;
     const int kc = (st - ti * kc_steps) * P::KC;
 #pragma unroll
     for (int j = 0; j < P::A_PER_T; ++j) {
@@ -350,7 +352,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
     int t = 0, kc = 0;
     if constexpr (PRE) {
       const int ti = min(st / kc_steps, 15);
-      t = st < stages ? tlist[ti] : 0;
+      t = st < stages ? tap_at(ti) : 0;
       kc = (st - ti * kc_steps) * P::KC;
     }
 #pragma unroll
