@@ -248,6 +248,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   E* Bs = reinterpret_cast<E*>(smem + 2 * P::A_BYTES);
   int32_t* nbt = reinterpret_cast<int32_t*>(smem + 2 * (P::A_BYTES + P::B_BYTES));
   int32_t* tflag = nbt + kTaps * BM;  // [16] tap used by some row of the tile
+  int32_t* tlist = tflag + 16;        // [16] bf16: used taps, count in tlist[15]
   float* pre_s = reinterpret_cast<float*>(smem + P::LDS_BYTES);   // PRE: [Cin] scales, [Cin] shifts
 
   const int tid = threadIdx.x;
@@ -283,16 +284,37 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
     if (nb >= 0) tflag[t] = 1;
   }
   __syncthreads();
-  // the used taps in order, 4 bits each; every thread packs them itself
+  // The used taps in order.  fp32: every thread packs them itself, 4 bits
+  // each (no serial list, one barrier fewer).  bf16: one thread lists them
+  // in LDS; the packed form costs the 128 x 128 tile enough registers to
+  // lose a wave per SIMD.
   uint64_t tpack = 0;
   int ntaps = 0;
-#pragma unroll
-  for (int t = 0; t < kTaps; ++t)
-    if (t < te - tb && tflag[t]) {
-      tpack |= static_cast<uint64_t>(t) << (4 * ntaps);
-      ++ntaps;
+  if constexpr (BF16) {
+    if (tid == 0) {
+      int k = 0;
+      for (int t = 0; t < te - tb; ++t)
+        if (tflag[t]) tlist[k++] = t;
+      tlist[15] = k;
     }
-  auto tap_at = [&](int ti) { return static_cast<int>((tpack >> (4 * ti)) & 15); };
+    __syncthreads();
+    ntaps = tlist[15];
+  } else {
+#pragma unroll
+    for (int t = 0; t < kTaps; ++t)
+      if (t < te - tb && tflag[t]) {
+        tpack |= static_cast<uint64_t>(t) << (4 * ntaps);
+        ++ntaps;
+      }
+    // the same for every thread: keep it in scalar registers
+    tpack = (static_cast<uint64_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(tpack >> 32))) << 32) |
+            static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(tpack)));
+    ntaps = __builtin_amdgcn_readfirstlane(ntaps);
+  }
+  auto tap_at = [&](int ti) {
+    if constexpr (BF16) return static_cast<int>(tlist[ti]);
+    else return static_cast<int>((tpack >> (4 * ti)) & 15);
+  };
 
   const int kc_steps = (Cin + P::KC - 1) / P::KC;
   const int stages = ntaps * kc_steps;

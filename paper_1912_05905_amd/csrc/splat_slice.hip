@@ -39,8 +39,20 @@ __device__ inline int64_t xcd_item(unsigned nblocks_logical) {
 inline unsigned xcd_grid(unsigned nblocks_logical) { return ((nblocks_logical + 7) / 8) * 8; }
 
 // Point outputs (slice, DeformSlice) are written once and not read back by
-// the kernel's neighbours: non-temporal stores keep them out of the L2.
+// the kernel: non-temporal stores keep them out of the L2.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Store of 4 floats of a point row.  Non-temporal when a lane's part of the
+// row is 16 bytes (fp32 inputs: a wave's store covers whole lines); with
+// wider parts (bf16 inputs, 32 bytes a lane) one store instruction leaves
+// gaps in every line, which the L2 has to merge, so those stay ordinary.
+template <bool NT>
+__device__ inline void store_row4(float* o, float a, float b, float c, float d) {
+  if constexpr (NT)
+    __builtin_nontemporal_store(f32x4_t{a, b, c, d}, reinterpret_cast<f32x4_t*>(o));
+  else
+    *reinterpret_cast<float4*>(o) = make_float4(a, b, c, d);
+}
 
 // f(std::integral_constant<int, i>) for i = 0 .. N-1, unrolled.
 template <class F, int... I>
@@ -549,8 +561,7 @@ k_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64_t m,
       float* o = out + (p0 + u) * C + static_cast<int64_t>(ch) * Ch::N;
 #pragma unroll
       for (int i = 0; i < Ch::N; i += 4)
-        __builtin_nontemporal_store(f32x4_t{acc[i], acc[i + 1], acc[i + 2], acc[i + 3]},
-                                    reinterpret_cast<f32x4_t*>(o + i));
+        store_row4<Ch::N == 4>(o + i, acc[i], acc[i + 1], acc[i + 2], acc[i + 3]);
     }
   }
 }
@@ -632,7 +643,7 @@ k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64
       for (int u = 0; u < 4; ++u)
         r[u] = coef[0] * x[q][0][i + u] + coef[1] * x[q][1][i + u] + coef[2] * x[q][2][i + u] +
                coef[3] * x[q][3][i + u];
-      __builtin_nontemporal_store(f32x4_t{r[0], r[1], r[2], r[3]}, reinterpret_cast<f32x4_t*>(o + i));
+      store_row4<Ch::N == 4>(o + i, r[0], r[1], r[2], r[3]);
     }
     if (plain) {
       // the plain slice of the same rows (Eq. slice), in the order of k_slice
@@ -647,7 +658,7 @@ k_deform_slice(const int4* __restrict__ idx, const float4* __restrict__ w, int64
           for (int k = 0; k < 4; ++k) a += bw[k] * x[q][k][i + u];
           r[u] = a;
         }
-        __builtin_nontemporal_store(f32x4_t{r[0], r[1], r[2], r[3]}, reinterpret_cast<f32x4_t*>(o2 + i));
+        store_row4<Ch::N == 4>(o2 + i, r[0], r[1], r[2], r[3]);
       }
     }
   }
