@@ -258,6 +258,32 @@ def test_splat_skewed(L, O, C, dtype):
         P.assert_close(P.rows_in_oracle_order(_host(ws), g2o), ow, P.TOL_F32, "skewed wsum")
 
 
+@pytest.mark.parametrize("m,C,dtype", [(300_000, 64, "f32"), (600_000, 64, "f32"), (600_000, 36, "f32"),
+                                       (600_000, 64, "bf16"), (300_000, 128, "bf16")])
+def test_splat_long_chunks(L, O, m, C, dtype):
+    """Clouds with over a million list entries, where a lane group takes 32
+    or 64 entries per chunk instead of 16, with a 20,000-point clump in one
+    simplex (a list that runs through many chunks and workgroup spans)."""
+    rng0 = np.random.default_rng(m)
+    clump = (np.array([0.31, 0.42, 0.53]) + 1e-5 * rng0.random((20_000, 3))).astype(np.float32)
+    spread = _cloud(700 + C, m, 0.9)
+    pos = np.concatenate([spread[: m // 3], clump, spread[m // 3:]]).astype(np.float32)
+    gl, ol, g2o = _pair(L, O, pos, 0.02)
+    rng = np.random.default_rng(m + C)
+    F = rng.normal(size=(pos.shape[0], C)).astype(np.float32)
+    if dtype == "bf16":
+        F = O.round_bf16(F).astype(np.float32)
+        gx = gl.splat(_dev(F, torch.bfloat16))
+        ox, _ = ol.splat(F.astype(np.float64))
+        P.assert_close(P.rows_in_oracle_order(_host(gx), g2o), O.round_bf16(ox), P.TOL_BF16, "splat bf16")
+    else:
+        ws = torch.empty(gl.n, device="cuda")
+        gx = gl.splat(_dev(F), wsum=ws)
+        ox, ow = ol.splat(F.astype(np.float64))
+        P.assert_close(P.rows_in_oracle_order(_host(gx), g2o), ox, P.TOL_F32, "splat")
+        P.assert_close(P.rows_in_oracle_order(_host(ws), g2o), ow, P.TOL_F32, "wsum")
+
+
 def test_splat_bf16(L, O):
     pos = _cloud(31, 9000, 0.7)
     gl, ol, g2o = _pair(L, O, pos, 0.06)
