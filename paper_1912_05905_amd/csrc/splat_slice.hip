@@ -64,10 +64,14 @@ __device__ inline void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// Value of lane J of this lane's 16-lane row (DPP row broadcast).
-template <int J>
-__device__ inline int32_t row_bcast(int32_t x) {
-  return __builtin_amdgcn_update_dpp(0, x, 0x150 + J, 0xF, 0xF, false);
+// Value of lane J of this lane's group of G lanes: a DPP row broadcast for
+// G = 16 (a group is a row), a swizzle for G = 8 (bit mask mode: keep the
+// group bits of the lane, set the low three to J).
+template <int G, int J>
+__device__ inline int32_t group_bcast(int32_t x) {
+  static_assert(G == 16 || G == 8, "16- or 8-lane groups");
+  if constexpr (G == 16) return __builtin_amdgcn_update_dpp(0, x, 0x150 + J, 0xF, 0xF, false);
+  else return __builtin_amdgcn_ds_swizzle(x, 0x18 | (J << 5));
 }
 
 // Value of lane ^ OFF: DPP for partners inside a 16-lane row that DPP can
@@ -392,25 +396,25 @@ k_splat_chunks(const int32_t* __restrict__ offsets, const int32_t* __restrict__ 
         }
       }
     };
-    if constexpr (LPR == 16 && Rows::kGivenWeights) {
-      // 16 entries at a time: lane i loads the index and weight of entry i,
-      // and a row broadcast (DPP, a 16-lane row is one lane group) hands
-      // entry j's to the whole group; the next 16 are loaded while this
-      // round's rows arrive
+    if constexpr ((LPR == 16 || LPR == 8) && Rows::kGivenWeights) {
+      // LPR entries at a time: lane i loads the index and weight of entry i,
+      // and a broadcast inside the lane group (DPP or swizzle) hands entry
+      // j's to the whole group; the next LPR are loaded while this round's
+      // rows arrive
       int32_t E = s0 + lane < s1 ? entries[s0 + lane] : 0;
       float Wt = s0 + lane < s1 ? rows.entry_w[s0 + lane] : 0.f;
-      for (int64_t sb = s0; sb < s1; sb += 16) {
-        const int64_t nx = sb + 16 + lane;
+      for (int64_t sb = s0; sb < s1; sb += LPR) {
+        const int64_t nx = sb + LPR + lane;
         const int32_t En = nx < s1 ? entries[nx] : 0;
         const float Wn = nx < s1 ? rows.entry_w[nx] : 0.f;
-        static_for<16 / B>([&](auto h_c) {
+        static_for<LPR / B>([&](auto h_c) {
           constexpr int J0 = decltype(h_c)::value * B;
           if (sb + J0 < s1) {
             typename Rows::Batch bt;
             static_for<B>([&](auto j_c) {
               constexpr int J = decltype(j_c)::value;
-              const int32_t e = row_bcast<J0 + J>(E);
-              const float w = __int_as_float(row_bcast<J0 + J>(__float_as_int(Wt)));
+              const int32_t e = group_bcast<LPR, J0 + J>(E);
+              const float w = __int_as_float(group_bcast<LPR, J0 + J>(__float_as_int(Wt)));
               rows.load_given(bt, J, w, e, sb + J0 + J < s1, lane, nchunk);
             });
 #pragma unroll
@@ -995,7 +999,7 @@ void splat_dispatch(int lpr, int q, const int32_t* off, const int32_t* ent, cons
 #define SPLAT_CASE(L, QQ) \
   if (lpr == L && q == QQ) return splat_launch<BF16, L, QQ>(off, ent, ew, cf, chunk, n, total, feat, ldf, C, norm, vals, ldv, wsum, ph, pt, pw, s);
   SPLAT_CASE(1, 1) SPLAT_CASE(2, 1) SPLAT_CASE(4, 1) SPLAT_CASE(8, 1) SPLAT_CASE(16, 1)
-  SPLAT_CASE(32, 1) SPLAT_CASE(64, 1) SPLAT_CASE(64, 2) SPLAT_CASE(64, 4)
+  SPLAT_CASE(32, 1) SPLAT_CASE(64, 1) SPLAT_CASE(64, 2) SPLAT_CASE(64, 4) SPLAT_CASE(8, 2)
 #undef SPLAT_CASE
 }
 
@@ -1110,8 +1114,13 @@ void launch_splat(const int32_t* offsets, const int32_t* entries, const float* e
                   hipStream_t s) {
   if (total <= 0) return;
   const int chunks = C / (bf16 ? 8 : 4);
-  const int lpr = lanes_per_row(C, bf16 != 0);
-  const int q = chunks <= lpr ? 1 : (chunks <= 2 * lpr ? 2 : 4);
+  int lpr = lanes_per_row(C, bf16 != 0);
+  int q = chunks <= lpr ? 1 : (chunks <= 2 * lpr ? 2 : 4);
+  // 64 fp32 channels: 8 lanes of two chunks each (half the per-entry work)
+  if (!bf16 && chunks == 16) {
+    lpr = 8;
+    q = 2;
+  }
   const int64_t span_len = static_cast<int64_t>(kBlock / lpr) * chunk;
   const int64_t nspans = (total + span_len - 1) / span_len;
   float* ph = partials;
