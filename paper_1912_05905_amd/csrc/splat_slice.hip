@@ -1172,8 +1172,10 @@ void launch_deform_classify(const int32_t* idx, const float* w, int64_t m, const
                             int bf16, const float* wv, float beta, const float* Wc, const float* bc, int K, float* out,
                             hipStream_t s) {
   if (m <= 0) return;
-  const int lpr = lanes_per_row(C, bf16 != 0);
   const int chunks = C / (bf16 ? 8 : 4);
+  // 64 fp32 channels: 8 lanes of two chunks each, twice the points per wave
+  // for the same per-point work (indices, weights, the group's dot products)
+  const int lpr = !bf16 && chunks == 16 ? 8 : lanes_per_row(C, bf16 != 0);
   ScopedKernelTimer tm("deform_slice", s);
   const bool two = chunks > lpr;
   const bool kp64 = K > 32 || lpr > 32;
@@ -1241,8 +1243,10 @@ void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const vo
                          int64_t ld_vals, int C, int bf16, const float* wv, float beta, float* out,
                          float* delta, float* plain, hipStream_t s) {
   if (m <= 0) return;
-  const int lpr = lanes_per_row(C, bf16 != 0);
   const int chunks = C / (bf16 ? 8 : 4);
+  // 64 fp32 channels: 8 lanes of two chunks each, twice the points per wave
+  // for the same per-point work (indices, weights, the group's dot products)
+  const int lpr = !bf16 && chunks == 16 ? 8 : lanes_per_row(C, bf16 != 0);
   ScopedKernelTimer tm("deform_slice", s);
   const bool two = chunks > lpr;
   if (bf16) {
