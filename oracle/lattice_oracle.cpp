@@ -43,10 +43,11 @@
 //    congruent mod d+1); every other tap, the centre included, is ignored.
 //  * DeformSlice: max per channel over all d+1 weighted vertex values (the
 //    vertex itself included), nonlinearity tanh.
-//  * Distribute + PointNet: coordinates are the raw positions g_p minus the
-//    unweighted mean over J_v; three 1x1 layers with ReLU before the second
-//    and the third (none on the raw rows), then the per-vertex maximum;
-//    GroupNorm is not part of this operator.
+//  * Distribute + PointNet: coordinates are the positions in lattice units
+//    (g_p / sigma) minus their unweighted mean over J_v; three blocks of
+//    GroupNorm, ReLU and a 1x1 layer, GroupNorm's statistics taken over all
+//    distributed rows with one channel per group up to 32 channels and 32
+//    groups above; then the per-vertex maximum.
 //  * Group Normalization: statistics over all vertices of the lattice and the
 //    group's channels, biased variance, eps inside the square root.
 //  * Backward passes: gradients of the forward operators above; the ReLU's
@@ -81,6 +82,7 @@ struct Lattice {
   std::vector<int64_t> idx;             // m x (d+1) simplex vertices of each point
   std::vector<float> bary;              // m x (d+1) barycentric weights
   const Lattice* parent = nullptr;      // finer lattice this one was coarsened from
+  double scale[kDim] = {1.0, 1.0, 1.0}; // sigma_j * 2^level: positions in lattice units are g / scale
 };
 
 // ---------------------------------------------------------------------------
@@ -335,6 +337,7 @@ int orc_create(const float* pos, int64_t m, int d, const float* sigma, orc_latti
     if (!std::isfinite(pos[e])) return ENONFINITE;
   Lattice* L = new Lattice();
   L->m = m;
+  for (int j = 0; j < kDim; ++j) L->scale[j] = sigma[j];
   L->y.resize(static_cast<size_t>(m) * kD1);
   orc_elevate(pos, m, sigma, L->y.data());
   const int st = build_from_elevated(L);
@@ -351,6 +354,7 @@ int orc_coarsen(const orc_lattice* fine, orc_lattice** out) {
   L->m = fine->m;
   L->level = fine->level + 1;
   L->parent = fine;
+  for (int j = 0; j < kDim; ++j) L->scale[j] = 2.0 * fine->scale[j];
   L->y.resize(fine->y.size());
   for (size_t e = 0; e < fine->y.size(); ++e) L->y[e] = fine->y[e] * 0.5f;
   const int st = build_from_elevated(L);
@@ -521,50 +525,90 @@ int orc_deform_slice(const orc_lattice* L, const double* X, int64_t ldx, int C, 
 }
 
 // Distribute + PointNet (Proposed Operations, Eq. (distribute), and the
-// PointNet block of the architecture figure).  For every vertex v and every
-// point p of J_v (the points whose simplex contains v) the distributed row is
-// [g_p - mu_v ; f_p], mu_v the mean position of the points of J_v.  Each row
-// goes through three 1x1 layers, h1 = W1 r + b1, h2 = W2 relu(h1) + b2,
-// h3 = W3 relu(h2) + b3 (W_i laid out [out][in]), and x_v is the per-channel
-// maximum of h3 over J_v.  G is m x d positions, F m x Cf features; X gets
-// n x C3.  Plain loops in double, following the definition vertex by vertex.
-int orc_distribute_pointnet(const orc_lattice* L, const double* G, const double* F, int cf,
-                            const double* W1, const double* b1, int c1, const double* W2,
-                            const double* b2, int c2, const double* W3, const double* b3, int c3,
+// PointNet block of the architecture figure).
+//  * Distribute: every vertex v receives one row per point p of J_v (the
+//    points whose simplex contains v), r = [g_p - mu_v ; f_p], where g_p are
+//    the positions in lattice units (G_s = G / sigma of the Method section,
+//    sigma doubled per coarsening level) and mu_v is the mean of g_p over J_v.
+//  * PointNet: three blocks [GroupNorm, ReLU, 1x1], h_i = W_i relu(GN_i(h_{i-1})) + b_i
+//    (h_0 = r, W_i laid out [out][in]), then x_v = the per-channel maximum
+//    of h_3 over the rows of v (MaxPool).
+//  * GroupNorm over the whole set of distributed rows (all (v, p) pairs) and
+//    the channels of a group; a layer of C <= 32 channels has one channel
+//    per group, a wider one 32 groups (C a multiple of 32).  gamma / beta
+//    hold the per-channel affine parameters of the three normalisations one
+//    after the other ((d + Cf) + C1 + C2 values each); null means 1 / 0.
+// G is m x d raw positions, F m x Cf features; X gets n x C3.  Plain loops in
+// double over the distributed-row matrix; a NaN anywhere propagates to the
+// outputs (the ReLU and the maximum keep NaN).
+int orc_groupnorm(const double* X, int64_t n, int C, int64_t ldx, int groups, const double* gamma,
+                  const double* beta, double eps, int relu, double* Y, int64_t ldy);
+
+int orc_distribute_pointnet(const orc_lattice* L, const double* G, const double* F, int cf, const double* gamma,
+                            const double* beta, double eps, const double* W1, const double* b1, int c1,
+                            const double* W2, const double* b2, int c2, const double* W3, const double* b3, int c3,
                             double* X) {
-  if (!L || !X || cf < 0 || c1 <= 0 || c2 <= 0 || c3 <= 0 || !W1 || !W2 || !W3) return EINVAL_;
+  if (!L || !X || cf < 0 || c1 <= 0 || c2 <= 0 || c3 <= 0 || !W1 || !W2 || !W3 || !(eps >= 0.0)) return EINVAL_;
   if (L->m > 0 && (!G || (cf > 0 && !F))) return EINVAL_;
+  const int cin = kDim + cf;
+  const int widths[3] = {cin, c1, c2};
+  for (int w : widths)
+    if (w > 32 && w % 32 != 0) return EUNSUPPORTED;
   const int64_t n = static_cast<int64_t>(L->keys.size());
   // J_v: the points whose simplex has v among its d+1 vertices
   std::vector<std::vector<int64_t>> J(n);
   for (int64_t p = 0; p < L->m; ++p)
     for (int k = 0; k < kD1; ++k) J[L->idx[p * kD1 + k]].push_back(p);
-  const int cin = kDim + cf;
-  std::vector<double> r(cin), h1(c1), h2(c2), h3(c3);
+  // the distributed rows, vertex by vertex
+  const int64_t rows = L->m * kD1;
+  std::vector<int64_t> row_vertex;
+  row_vertex.reserve(rows);
+  std::vector<double> h(static_cast<size_t>(rows) * cin);
+  int64_t r = 0;
   for (int64_t v = 0; v < n; ++v) {
     double mu[kDim] = {0.0, 0.0, 0.0};
     for (int64_t p : J[v])
-      for (int j = 0; j < kDim; ++j) mu[j] += G[p * kDim + j];
+      for (int j = 0; j < kDim; ++j) mu[j] += G[p * kDim + j] / L->scale[j];
     for (int j = 0; j < kDim; ++j) mu[j] /= static_cast<double>(J[v].size());
-    for (int c = 0; c < c3; ++c) X[v * c3 + c] = -INFINITY;
     for (int64_t p : J[v]) {
-      for (int j = 0; j < kDim; ++j) r[j] = G[p * kDim + j] - mu[j];
-      for (int c = 0; c < cf; ++c) r[kDim + c] = F[p * cf + c];
-      for (int o = 0; o < c1; ++o) {
-        double a = b1 ? b1[o] : 0.0;
-        for (int i = 0; i < cin; ++i) a += W1[o * cin + i] * r[i];
-        h1[o] = a;
+      for (int j = 0; j < kDim; ++j) h[r * cin + j] = G[p * kDim + j] / L->scale[j] - mu[j];
+      for (int c = 0; c < cf; ++c) h[r * cin + kDim + c] = F[p * cf + c];
+      row_vertex.push_back(v);
+      ++r;
+    }
+  }
+  // three [GN, ReLU, 1x1] blocks
+  const double* Ws[3] = {W1, W2, W3};
+  const double* bs[3] = {b1, b2, b3};
+  const int outs[3] = {c1, c2, c3};
+  int off = 0;   // first affine parameter of the current normalisation
+  for (int layer = 0; layer < 3; ++layer) {
+    const int ci = widths[layer], co = outs[layer];
+    const int groups = ci <= 32 ? ci : 32;
+    std::vector<double> a(h.size());
+    if (rows > 0) {
+      const int st = orc_groupnorm(h.data(), rows, ci, ci, groups, gamma ? gamma + off : nullptr,
+                                   beta ? beta + off : nullptr, eps, 1, a.data(), ci);
+      if (st != OK) return st;
+    }
+    off += ci;
+    std::vector<double> next(static_cast<size_t>(rows) * co);
+    for (int64_t q = 0; q < rows; ++q)
+      for (int o = 0; o < co; ++o) {
+        double acc = bs[layer] ? bs[layer][o] : 0.0;
+        for (int i = 0; i < ci; ++i) acc += Ws[layer][o * ci + i] * a[q * ci + i];
+        next[q * co + o] = acc;
       }
-      for (int o = 0; o < c2; ++o) {
-        double a = b2 ? b2[o] : 0.0;
-        for (int i = 0; i < c1; ++i) a += W2[o * c1 + i] * std::max(h1[i], 0.0);
-        h2[o] = a;
-      }
-      for (int o = 0; o < c3; ++o) {
-        double a = b3 ? b3[o] : 0.0;
-        for (int i = 0; i < c2; ++i) a += W3[o * c2 + i] * std::max(h2[i], 0.0);
-        X[v * c3 + o] = std::max(X[v * c3 + o], a);
-      }
+    h.swap(next);
+  }
+  // MaxPool over the rows of each vertex (NaN wins)
+  for (int64_t e = 0; e < n * c3; ++e) X[e] = -INFINITY;
+  for (int64_t q = 0; q < rows; ++q) {
+    double* x = X + row_vertex[q] * c3;
+    for (int o = 0; o < c3; ++o) {
+      const double val = h[q * c3 + o];
+      if (std::isnan(x[o])) continue;
+      if (std::isnan(val) || val > x[o]) x[o] = val;
     }
   }
   return OK;

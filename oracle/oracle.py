@@ -55,7 +55,7 @@ def lib():
             "orc_slice": (i32, [p, p, i64, i32, p, i64, p]),
             "orc_deform_slice": (i32, [p, p, i64, i32, p, dbl, p, i64, p, p]),
             "orc_round_bf16": (None, [p, i64]),
-            "orc_distribute_pointnet": (i32, [p, p, p, i32, p, p, i32, p, p, i32, p, p, i32, p]),
+            "orc_distribute_pointnet": (i32, [p, p, p, i32, p, p, dbl, p, p, i32, p, p, i32, p, p, i32, p]),
             "orc_splat_backward": (i32, [p, p, i32, i32, p]),
             "orc_groupnorm": (i32, [p, i64, i32, i64, i32, p, p, dbl, i32, p, i64]),
             "orc_deform_slice_classify": (i32, [p, p, i64, i32, p, dbl, p, p, i32, p]),
@@ -189,19 +189,28 @@ class Lattice:
         _check(lib().orc_splat(self._h, _ptr(F), Cc, int(bool(normalize)), _ptr(X), _ptr(W)))
         return X, W
 
-    def distribute_pointnet(self, G, F, layers):
+    def distribute_pointnet(self, G, F, layers, gn=None, eps=1e-5):
         """Distribute + PointNet: layers = [(W1, b1), (W2, b2), (W3, b3)],
         W_i laid out [out][in] (the first layer's inputs: d coordinates, then
-        the Cf features).  Returns n x C3."""
+        the Cf features); gn = None or (gamma, beta), each the concatenated
+        per-channel parameters of the three GroupNorms ((d + Cf) + C1 + C2).
+        G are the raw positions (divided by the lattice's sigma inside).
+        Returns n x C3."""
         G = _f64(G)
         F = _f64(F) if F is not None else np.zeros((G.shape[0], 0))
         (W1, b1), (W2, b2), (W3, b3) = [(_f64(W), None if b is None else _f64(b)) for W, b in layers]
         cf = F.shape[1]
         c1, c2, c3 = W1.shape[0], W2.shape[0], W3.shape[0]
         assert W1.shape[1] == G.shape[1] + cf and W2.shape[1] == c1 and W3.shape[1] == c2
+        gam = bet = None
+        if gn is not None:
+            gam, bet = (None if a is None else _f64(a) for a in gn)
+            for a in (gam, bet):
+                assert a is None or a.shape == (G.shape[1] + cf + c1 + c2,)
         X = np.zeros((self.n, c3), np.float64)
-        _check(lib().orc_distribute_pointnet(self._h, _ptr(G), _ptr(F) if cf else None, cf, _ptr(W1), _ptr(b1), c1,
-                                             _ptr(W2), _ptr(b2), c2, _ptr(W3), _ptr(b3), c3, _ptr(X)))
+        _check(lib().orc_distribute_pointnet(self._h, _ptr(G), _ptr(F) if cf else None, cf, _ptr(gam), _ptr(bet),
+                                             float(eps), _ptr(W1), _ptr(b1), c1, _ptr(W2), _ptr(b2), c2, _ptr(W3),
+                                             _ptr(b3), c3, _ptr(X)))
         return X
 
     def conv(self, src: "Lattice", X, W, bias=None, relu=False, rows=None):

@@ -320,12 +320,21 @@ def test_deform_slice_special_cases_and_equivariance(oracle_mod):
     o2, d2 = oracle_mod.deform_slice_raw(X, idx[:, perm], w[:, perm], wv, 0.1)
     assert np.abs(o1 - o2).max() < 1e-12
     assert np.abs(d1[:, perm] - d2).max() < 1e-15
-    # offsets by the definition for a few points
-    for p in (0, 17, 4095):
-        q = w[p, :, None].astype(np.float64) * X[idx[p]]
-        dd = np.tanh(0.1 + (q - q.max(axis=0)) @ wv)
-        assert np.abs(dd - d1[p]).max() < 1e-12
-        assert np.abs((w[p] + dd) @ X[idx[p]] - o1[p]).max() < 1e-12
+
+
+def test_deform_slice_golden(oracle_mod):
+    """Hand-worked DeformSlice of two points with explicit weights and vertex
+    values (tests/golden/deform_slice_cases.json): the maximum per channel
+    over b_k x_k of all d+1 vertices, the vertex itself included, subtracted
+    before the linear map and tanh."""
+    doc = json.load(open(os.path.join(GOLDEN, "deform_slice_cases.json")))
+    X = np.array(doc["X"], np.float64)
+    idx = np.array([c["idx"] for c in doc["points"]], np.int64)
+    w = np.array([c["b"] for c in doc["points"]], np.float32)
+    out, delta = oracle_mod.deform_slice_raw(X, idx, w, np.array(doc["wv"]), doc["beta"])
+    for p, c in enumerate(doc["points"]):
+        np.testing.assert_allclose(delta[p], c["delta"], rtol=0, atol=1e-14)
+        np.testing.assert_allclose(out[p], c["out"], rtol=0, atol=1e-13)
 
 
 def test_end_to_end_bruteforce(oracle_mod):
@@ -379,6 +388,14 @@ def _selector(rows, cols, pick, sign=1.0):
     return W
 
 
+def _pointnet_layers(st, cin, widths=(16, 32, 64)):
+    layers, k = [], cin
+    for c in widths:
+        layers.append((st.normal(c * k).reshape(c, k), st.normal(c)))
+        k = c
+    return layers
+
+
 def test_distribute_invariances(oracle_mod):
     """Translating the cloud leaves g_p - mu_v unchanged; the operator does
     not depend on the order of the points."""
@@ -386,90 +403,143 @@ def test_distribute_invariances(oracle_mod):
     G = _tiny_cloud(91, m=300)
     st = Stream(91, "dist-f")
     F = st.normal(300 * 5).reshape(300, 5)
-    layers = [(st.normal(16 * 8).reshape(16, 8), st.normal(16)), (st.normal(32 * 16).reshape(32, 16), st.normal(32)),
-              (st.normal(64 * 32).reshape(64, 32), st.normal(64))]
+    layers = _pointnet_layers(st, 8)
+    gn = (1.0 + 0.1 * st.normal(8 + 16 + 32), 0.1 * st.normal(8 + 16 + 32))
     ol = O.Lattice.create(G, np.full(3, 0.15, np.float32))
-    X = ol.distribute_pointnet(G.astype(np.float64), F, layers)
-    shift = np.array([0.25, -0.5, 0.125])       # exact in float; lattice rebuilt from the shifted cloud
-    Gs = (G.astype(np.float64) + shift)
+    X = ol.distribute_pointnet(G.astype(np.float64), F, layers, gn)
+    shift = np.array([0.25, -0.5, 0.125])
     # same lattice (built from G), shifted coordinates: mu shifts with them
-    Xs = ol.distribute_pointnet(Gs, F, layers)
-    np.testing.assert_allclose(Xs, X, rtol=1e-12, atol=1e-11)
+    Xs = ol.distribute_pointnet(G.astype(np.float64) + shift, F, layers, gn)
+    np.testing.assert_allclose(Xs, X, rtol=1e-9, atol=1e-9)
     perm = st.permutation(300)
     olp = O.Lattice.create(G[perm], np.full(3, 0.15, np.float32))
     assert np.array_equal(olp.keys(), ol.keys())    # vertices numbered by key: same rows
-    Xp = olp.distribute_pointnet(G[perm].astype(np.float64), F[perm], layers)
-    np.testing.assert_allclose(Xp, X, rtol=1e-12, atol=1e-12)
+    Xp = olp.distribute_pointnet(G[perm].astype(np.float64), F[perm], layers, gn)
+    np.testing.assert_allclose(Xp, X, rtol=1e-9, atol=1e-9)
 
 
-def test_distribute_coordinates_mean_and_max(oracle_mod):
-    """With selector weights and a bias that keeps every ReLU open, x_v is
-    max_p (g_p - mu_v) + B per coordinate; with negated selectors it is
-    B - min_p (g_p - mu_v).  Checked against the point sets of the exported
-    simplices."""
+def _pointnet_golden_case(c):
+    def dense(rows, cols, nz):
+        W = np.zeros((rows, cols))
+        for o, i, v in nz:
+            W[o, i] = v
+        return W
+    c1, c2, c3 = c["widths"]
+    layers = [(dense(c1, 4, c["W1_nonzero"]), np.array(c["b1"])), (dense(c2, c1, c["W2_nonzero"]), np.array(c["b2"])),
+              (dense(c3, c2, c["W3_nonzero"]), np.array(c["b3"]))]
+    return layers, (np.array(c["gamma"]), np.array(c["beta"]))
+
+
+def test_distribute_golden(oracle_mod):
+    """Hand-worked Distribute + PointNet of two points sharing one simplex
+    (tests/golden/distribute_cases.json): positions in units of sigma, mean
+    subtracted, three [GroupNorm, ReLU, 1x1] blocks with statistics over all
+    distributed rows (one channel per group up to 32 channels, 32 groups of
+    two for a 64-wide layer), MaxPool over J_v."""
+    doc = json.load(open(os.path.join(GOLDEN, "distribute_cases.json")))
+    for c in doc["cases"]:
+        G = np.array(c["positions"], np.float32)
+        ol = oracle_mod.Lattice.create(G, np.full(3, c["sigma"], np.float32))
+        idx, _ = ol.simplices()
+        assert ol.n == 4 and sorted(idx[0]) == sorted(idx[1]) == [0, 1, 2, 3], "both points in one simplex"
+        layers, gn = _pointnet_golden_case(c)
+        X = ol.distribute_pointnet(G.astype(np.float64), np.array(c["features"]), layers, gn, eps=c["eps"])
+        for v in range(4):
+            np.testing.assert_allclose(X[v], c["expected"], rtol=0, atol=1e-12, err_msg=c["name"])
+
+
+def test_distribute_positions_in_units_of_sigma(oracle_mod):
+    """The coordinates enter as g / sigma: scaling the cloud and sigma by 8
+    (exact in float32: the same lattice bit for bit) changes nothing, while
+    with eps > 0 a raw-position reading would (the normalisation's eps acts
+    on a variance 64 times larger)."""
     O = oracle_mod
-    G = _tiny_cloud(92, m=400).astype(np.float64)
-    ol = O.Lattice.create(G.astype(np.float32), np.full(3, 0.12, np.float32))
-    J = _point_sets(ol)
-    B = 100.0
-    for sign in (1.0, -1.0):
-        layers = [(_selector(16, 3, [0, 1, 2], sign), np.full(16, B)),
-                  (_selector(32, 16, [0, 1, 2]), None), (_selector(64, 32, [0, 1, 2]), None)]
-        X = ol.distribute_pointnet(G, None, layers)
-        for v in range(ol.n):
-            pts = G[J[v]]
-            d = sign * (pts - pts.mean(axis=0))
-            np.testing.assert_allclose(X[v, :3], d.max(axis=0) + B, rtol=0, atol=1e-9)
-        assert np.all(X[:, 3:] == 0.0)
+    G = _tiny_cloud(95, m=300)
+    st = Stream(95, "dist-sigma")
+    F = st.normal(300 * 2).reshape(300, 2)
+    layers = _pointnet_layers(st, 5)
+    ol = O.Lattice.create(G, np.full(3, 0.15, np.float32))
+    ol8 = O.Lattice.create(G * 8, np.full(3, 1.2, np.float32))
+    assert np.array_equal(ol.keys(), ol8.keys())
+    X = ol.distribute_pointnet(G.astype(np.float64), F, layers, eps=0.1)
+    X8 = ol8.distribute_pointnet(G.astype(np.float64) * 8, F, layers, eps=0.1)
+    np.testing.assert_allclose(X8, X, rtol=1e-10, atol=1e-10)
+    # the same raw positions against a lattice of sigma/2 (positions halved
+    # relative to sigma): no longer equal, so sigma is not ignored
+    Xh = O.Lattice.create(G * 2, np.full(3, 0.3, np.float32)).distribute_pointnet(G.astype(np.float64), F, layers,
+                                                                                  eps=0.1)
+    assert np.abs(Xh - X).max() > 1e-3
 
 
-def test_distribute_relu_placement(oracle_mod):
-    """Feature selectors with zero biases: h1 = f (may be negative), ReLU
-    before the second and third layers only, none after the last: x_v =
-    relu(max f) with identity layers, -relu(min f) with a negated last layer."""
+def test_distribute_normalises_each_raw_channel(oracle_mod):
+    """With eps = 0 the first normalisation makes the result invariant to a
+    positive affine map of every raw feature channel and to a positive
+    scale of every coordinate axis (one channel per group, statistics over
+    all distributed rows)."""
     O = oracle_mod
-    G = _tiny_cloud(93, m=300).astype(np.float64)
-    st = Stream(93, "dist-relu")
-    F = st.normal(300 * 4).reshape(300, 4)
-    ol = O.Lattice.create(G.astype(np.float32), np.full(3, 0.15, np.float32))
-    J = _point_sets(ol)
-    pick = [3, 4, 5, 6]                          # the feature inputs follow the 3 coordinates
-    for sign in (1.0, -1.0):
-        layers = [(_selector(16, 7, pick), None), (_selector(32, 16, [0, 1, 2, 3]), None),
-                  (_selector(64, 32, [0, 1, 2, 3], sign), None)]
-        X = ol.distribute_pointnet(G, F, layers)
-        for v in range(ol.n):
-            f = F[J[v]]
-            want = np.maximum(f.max(axis=0), 0.0) if sign > 0 else -np.maximum(f.min(axis=0), 0.0)
-            np.testing.assert_allclose(X[v, :4], want, rtol=0, atol=1e-12)
+    G = _tiny_cloud(96, m=300)
+    st = Stream(96, "dist-affine")
+    F = st.normal(300 * 3).reshape(300, 3)
+    layers = _pointnet_layers(st, 6)
+    ol = O.Lattice.create(G, np.full(3, 0.15, np.float32))
+    X = ol.distribute_pointnet(G.astype(np.float64), F, layers, eps=0.0)
+    a = np.array([3.0, 0.25, 7.0])
+    b = np.array([-2.0, 5.0, 0.5])
+    Xa = ol.distribute_pointnet(G.astype(np.float64) * np.array([2.0, 0.5, 4.0]), F * a + b, layers, eps=0.0)
+    np.testing.assert_allclose(Xa, X, rtol=1e-9, atol=1e-9)
 
 
-def test_distribute_each_relu_matters(oracle_mod):
-    """Constructions in which each ReLU changes the result:
-    W1 = I, W2 = -I, W3 = I            -> 0 (the ReLU before layer 3 clips -relu(f));
-    W1 = I, W2 = I, b2 = -c, W3 = I     -> relu(relu(max f) - c);
-    W1 = -I, W2 = I, W3 = I             -> relu(-min f) (no ReLU on the raw rows)."""
+def test_distribute_selectors_reduce_to_zscores(oracle_mod):
+    """Selector weights (each output copies one input) with eps = 0 and the
+    identity affine: every block is a per-column z-score (scipy.stats.zscore,
+    population variance) over the distributed rows followed by a ReLU, so
+    x_v = max over J_v of relu(z(relu(z(relu(z(r)))))) column by column,
+    with the rows r_p = [g_p / sigma - mean over J_v ; f_p] built here from
+    the exported simplices."""
+    from scipy.stats import zscore
     O = oracle_mod
-    G = _tiny_cloud(94, m=300).astype(np.float64)
-    st = Stream(94, "dist-relu2")
-    F = st.normal(300 * 4).reshape(300, 4)
-    ol = O.Lattice.create(G.astype(np.float32), np.full(3, 0.15, np.float32))
+    G = _tiny_cloud(97, m=250).astype(np.float64)
+    st = Stream(97, "dist-z")
+    F = st.normal(250 * 2).reshape(250, 2)
+    sigma = 0.15
+    ol = O.Lattice.create(G.astype(np.float32), np.full(3, sigma, np.float32))
     J = _point_sets(ol)
-    feat = [3, 4, 5, 6]
-    four = [0, 1, 2, 3]
-    c = 0.5
-    cases = [
-        ([(_selector(16, 7, feat), None), (_selector(32, 16, four, -1.0), None), (_selector(64, 32, four), None)],
-         lambda f: np.zeros(4)),
-        ([(_selector(16, 7, feat), None), (_selector(32, 16, four), np.full(32, -c)), (_selector(64, 32, four), None)],
-         lambda f: np.maximum(np.maximum(f.max(axis=0), 0.0) - c, 0.0)),
-        ([(_selector(16, 7, feat, -1.0), None), (_selector(32, 16, four), None), (_selector(64, 32, four), None)],
-         lambda f: np.maximum(-f.min(axis=0), 0.0)),
-    ]
-    for layers, want in cases:
-        X = ol.distribute_pointnet(G, F, layers)
-        for v in range(ol.n):
-            np.testing.assert_allclose(X[v, :4], want(F[J[v]]), rtol=0, atol=1e-12)
+    rows, owner = [], []
+    for v in range(ol.n):
+        pts = G[J[v]] / sigma
+        for p, g in zip(J[v], pts):
+            rows.append(np.concatenate([g - pts.mean(axis=0), F[p]]))
+            owner.append(v)
+    R = np.array(rows)
+    owner = np.array(owner)
+    cin = R.shape[1]
+    dup = lambda rows_, cols: _selector(rows_, cols, [o % cols for o in range(rows_)])
+    layers = [(dup(16, cin), None), (dup(32, 16), None), (dup(16, 32), None)]
+    X = ol.distribute_pointnet(G, F, layers, eps=0.0)
+    relu = lambda x: np.maximum(x, 0.0)
+    A = relu(zscore(R, axis=0))
+    H1 = A[:, [o % cin for o in range(16)]]
+    A = relu(zscore(H1, axis=0))
+    H2 = A[:, [o % 16 for o in range(32)]]
+    A = relu(zscore(H2, axis=0))
+    H3 = A[:, [o % 32 for o in range(16)]]
+    want = np.full((ol.n, 16), -np.inf)
+    for q, v in enumerate(owner):
+        want[v] = np.maximum(want[v], H3[q])
+    np.testing.assert_allclose(X, want, rtol=1e-9, atol=1e-9)
+
+
+def test_distribute_nan_propagates(oracle_mod):
+    """A NaN feature poisons the statistics of its channel and, through the
+    first layer, every output value."""
+    O = oracle_mod
+    G = _tiny_cloud(98, m=100)
+    st = Stream(98, "dist-nan")
+    F = st.normal(100 * 2).reshape(100, 2)
+    F[7, 1] = np.nan
+    ol = O.Lattice.create(G, np.full(3, 0.15, np.float32))
+    X = ol.distribute_pointnet(G.astype(np.float64), F, _pointnet_layers(st, 5))
+    assert np.isnan(X).all()
 
 
 # ----------------------------------------------------------------------------
