@@ -212,25 +212,38 @@ int lattice_refine_preact(lattice_t fine, lattice_t coarse, const void* in_dev, 
                           hipStream_t stream);
 
 /*
- * Distribute + PointNet (Proposed Operations, Eq. (distribute); PointNet
- * block of the architecture figure).  For every vertex v the rows
- * r_p = [g_p - mu_v ; f_p], p in J_v, mu_v the mean of g_p over J_v, pass
- * through three 1x1 layers and the per-channel maximum over J_v:
- *   x_v = max_{p in J_v} W3 relu(W2 relu(W1 r_p + b1) + b2) + b3.
- * No activation is applied to the raw rows; GroupNorm is not part of this
- * operator.  float32 only (the mean is formed in float64).
- *   pos_dev   m x d float32, the positions the lattice was built from.
- *   feat_dev  m x Cf float32, row stride ld_feat (0 = Cf); may be NULL when
- *             Cf = 0.  0 <= Cf <= 60.
- *   W1_dev    C1 x (d + Cf) float32, [out][in]: inputs 0..d-1 are the
- *             coordinates, d.. the features.  W2_dev C2 x C1, W3_dev C3 x C2.
- *   b*_dev    optional C1 / C2 / C3 float32 biases (NULL = 0).
- *   C1, C2, C3  multiples of 16, at most 64 (the paper uses 16, 32, 64).
- *   out_dev   n x C3 float32, row stride ld_out (0 = C3).
- * Uses a work space of O(n + 4m / 256) from the library's pool.
+ * Distribute + PointNet (Proposed Operations, Eq. (distribute); the scaled
+ * positions G_s = G / sigma of the Method section; PointNet block of the
+ * architecture figure).  For every vertex v each point p of J_v gives a row
+ *   r = [g_p / sigma - mu_v ; f_p],  mu_v = mean of g_p / sigma over J_v,
+ * with sigma the lattice's scale (doubled per coarsening level).  The rows
+ * pass three blocks [GroupNorm, ReLU, 1x1]:
+ *   h_i = W_i relu(GN_i(h_{i-1})) + b_i   (h_0 = r, i = 1, 2, 3),
+ * and x_v is the per-channel maximum of h_3 over J_v (MaxPool).
+ * GN_i: mean and biased variance over all distributed rows (every (v, p)
+ * pair, (d+1) m rows) and the channels of a group; a layer input of at most
+ * 32 channels has one channel per group, a wider one 32 groups; then
+ * (x - mean) / sqrt(var + eps) * gamma_c + beta_c.  Statistics are summed
+ * in float64 in a fixed order.  float32 only.
+ *   pos_dev    m x d float32, the positions the lattice was built from.
+ *   feat_dev   m x Cf float32, row stride ld_feat (0 = Cf); may be NULL when
+ *              Cf = 0.  0 <= Cf <= 29 (d + Cf <= 32).
+ *   gn_gamma_dev, gn_beta_dev  optional per-channel parameters of the
+ *              three normalisations, concatenated: (d + Cf) for the raw
+ *              rows (coordinates first), then C1, then C2 (NULL = 1 / 0).
+ *   eps        >= 0, finite (the paper's default is 1e-5).
+ *   W1_dev     C1 x (d + Cf) float32, [out][in]: inputs 0..d-1 are the
+ *              coordinates, d.. the features.  W2_dev C2 x C1, W3_dev C3 x C2.
+ *   b*_dev     optional C1 / C2 / C3 float32 biases (NULL = 0).
+ *   C1, C2, C3  16, 32 or 64 (C3 also 48; the paper uses 16, 32, 64).
+ *   out_dev    n x C3 float32, row stride ld_out (0 = C3).
+ * A non-finite feature makes every output value NaN (the statistics it
+ * reaches are not finite).  Uses a work space of O(n + 4m) bytes from the
+ * library's pool.
  */
 int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* feat_dev, int64_t ld_feat,
-                                int Cf, const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
+                                int Cf, const float* gn_gamma_dev, const float* gn_beta_dev, float eps,
+                                const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
                                 const float* b2_dev, int C2, const float* W3_dev, const float* b3_dev, int C3,
                                 float* out_dev, int64_t ld_out, hipStream_t stream);
 

@@ -2,9 +2,7 @@
 
 Every source is compiled for gfx950 only, with packed-FP32 instructions
 disabled.  The lattice-construction unit is compiled without float
-contraction: its vertex set depends on every float rounding.  The
-Distribute unit assumes no NaN inputs, so its maxima and ReLUs compile to
-single v_max instructions (no canonicalisation).
+contraction: its vertex set depends on every float rounding.
 """
 from __future__ import annotations
 
@@ -25,7 +23,7 @@ SOURCES = {
     "create.hip": ["-ffp-contract=off"],
     "splat_slice.hip": [],
     "conv.hip": [],
-    "distribute.hip": ["-fno-honor-nans"],
+    "distribute.hip": [],
     "backward.hip": [],
     "norm.hip": [],
     "api.hip": [],

@@ -244,6 +244,7 @@ struct HostCounts {
 
 struct lattice_s {
   int level = 0;
+  double scale[3] = {1.0, 1.0, 1.0};  // sigma_j * 2^level: positions in lattice units are pos / scale
   int64_t m = 0;
   int64_t n = 0;                 // valid once counts_known
   int64_t nmax = 0;              // host-side bound on n (buffer sizes)
@@ -868,6 +869,7 @@ int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_ho
   lattice_s* L = new lattice_s();
   L->m = m;
   L->stream = stream;
+  for (int j = 0; j < kDim; ++j) L->scale[j] = sigma_host[j];
   const int st = build_lattice(L, pos_dev, a, nullptr, capacity_hint, stream);
   if (st != LAT_OK) {
     L->free_all();
@@ -895,6 +897,7 @@ int lattice_coarsen_ex(lattice_t fine, int64_t capacity_hint, int flags, hipStre
   L->m = fine->m;
   L->level = fine->level + 1;
   L->parent = fine;
+  for (int j = 0; j < kDim; ++j) L->scale[j] = 2.0 * fine->scale[j];
   L->parent_generation = fine->generation;
   L->stream = stream;
   const float a[3] = {0.f, 0.f, 0.f};
@@ -1091,7 +1094,8 @@ int lattice_refine_preact(lattice_t fine, lattice_t coarse, const void* in_dev, 
 }
 
 int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* feat_dev, int64_t ld_feat,
-                                int Cf, const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
+                                int Cf, const float* gn_gamma_dev, const float* gn_beta_dev, float eps,
+                                const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
                                 const float* b2_dev, int C2, const float* W3_dev, const float* b3_dev, int C3,
                                 float* out_dev, int64_t ld_out, hipStream_t stream) {
   int st;
@@ -1101,6 +1105,9 @@ int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* 
     return fail(LAT_EUNSUPPORTED, "Cf must be in [0, " + std::to_string(distribute_max_features()) + "]");
   for (int c : {C1, C2, C3})
     if (c <= 0 || c % 16 != 0 || c > 64) return fail(LAT_EUNSUPPORTED, "C1, C2, C3 must be 16, 32, 48 or 64");
+  if (C1 == 48 || C2 == 48)
+    return fail(LAT_EUNSUPPORTED, "a normalised layer input of 48 channels does not split into 32 groups");
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return fail(LAT_EINVAL, "eps must be finite and >= 0");
   if (ld_feat == 0) ld_feat = Cf;
   if (ld_out == 0) ld_out = C3;
   if (ld_feat < Cf) return fail(LAT_EINVAL, "ld_feat < Cf");
@@ -1110,12 +1117,11 @@ int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* 
   if (L->m > 0 && Cf > 0 && !feat_dev) return fail(LAT_EINVAL, "feat is null");
   if (L->n > 0 && !out_dev) return fail(LAT_EINVAL, "out is null");
   if (L->n == 0) return LAT_OK;
-  Scratch mu, work;
-  if ((st = mu.get(sizeof(double) * 4 * static_cast<size_t>(L->n), stream)) != LAT_OK) return st;
-  if ((st = work.get(static_cast<size_t>(distribute_workspace_bytes(L->total, C3)), stream)) != LAT_OK) return st;
-  launch_distribute(L->offsets, L->entries, L->chunk_first, L->chunk, L->n, L->total, pos_dev, feat_dev, ld_feat, Cf,
-                    W1_dev, b1_dev, C1, W2_dev, b2_dev, C2, W3_dev, b3_dev, C3, out_dev, ld_out, mu.as<double>(),
-                    work.p, stream);
+  Scratch work;
+  if ((st = work.get(static_cast<size_t>(distribute_workspace_bytes(L->n, L->total)), stream)) != LAT_OK) return st;
+  launch_distribute(L->offsets, L->entries, L->chunk_first, L->chunk, L->n, L->total, pos_dev, L->scale, feat_dev,
+                    ld_feat, Cf, gn_gamma_dev, gn_beta_dev, eps, W1_dev, b1_dev, C1, W2_dev, b2_dev, C2, W3_dev,
+                    b3_dev, C3, out_dev, ld_out, work.p, stream);
   return check_launch("distribute");
 }
 

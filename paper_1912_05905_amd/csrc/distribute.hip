@@ -1,17 +1,26 @@
 // Distribute + PointNet on gfx950 (Proposed Operations, Eq. (distribute),
-// and the PointNet block of the architecture figure):
-//   x_v = max_{p in J_v} W3 relu(W2 relu(W1 [g_p - mu_v ; f_p] + b1) + b2) + b3,
-//   mu_v = mean of g_p over J_v.
+// the scaled positions G_s = G / sigma of the Method section, and the
+// PointNet block of the architecture figure):
+//   r = [g_p / sigma - mu_v ; f_p] for every p in J_v, mu_v = mean of g_p / sigma over J_v,
+//   h_i = W_i relu(GN_i(h_{i-1})) + b_i  (h_0 = r, i = 1..3),  x_v = max over J_v of h_3.
+// GroupNorm's statistics span all distributed rows; a layer of at most 32
+// channels has one channel per group, a wider one 32 groups.
 // J_v are the vertex lists built with the lattice (entries grouped by vertex).
 // The mean runs over spans of 256 consecutive list entries, so the work is
 // balanced however skewed the list lengths are: a vertex inside a span is
 // finished there; the vertex a span starts inside and the vertex that runs
 // past its end leave a head and a tail partial, which a finishing pass joins
-// in span order.  The mean is summed in fp64 (positions can be tens of
-// metres from the origin while g - mu is a fraction of sigma) and g - mu is
-// rounded to fp32 once.  The three 1x1 layers run on
-// v_mfma_f32_16x16x4_f32 with the activations held in registers; each wave
-// takes an equal range of list entries and reduces the maximum across lanes.
+// in span order.  The mean is summed in fp64 (positions can be hundreds of
+// sigma from the origin while g - mu is a fraction of one) and g - mu is
+// rounded to fp32 once.  Each normalisation needs the statistics of its
+// whole input before any row can pass it, so the rows are walked four
+// times: the statistics of r, then of h_1 and of h_2 (each pass recomputes
+// the cheaper layers before it rather than storing them), then the full
+// block with the maximum.  Statistics are fp64 per-workgroup partials added
+// in a fixed order, so the result does not depend on scheduling.  The 1x1
+// layers run on v_mfma_f32_16x16x4_f32 with the activations held in
+// registers; each wave takes an equal range of list entries and reduces
+// the maximum across lanes.
 #include <algorithm>
 
 #include "lattice_internal.h"
@@ -22,6 +31,9 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kMeanSpan = kBlock;  // list entries per workgroup of the mean pass
 constexpr int kMaxC = 64;          // widest 1x1 layer
+constexpr int kMaxIn = 32;         // widest raw row (d + Cf): one channel per normalisation group
+constexpr int kPreStride = 2 * kMaxC;   // floats per normalisation table: scales, then shifts
+constexpr int kStatsMaxParts = 512;     // partials of the raw-row statistics
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -48,13 +60,13 @@ __device__ inline int window_vertex(const int32_t* win, int count, int64_t s) {
   return lo;
 }
 
-// ---- mean of the positions over J_v (fp64) ----
+// ---- mean of the positions over J_v (fp64, in units of sigma) ----
 __global__ void __launch_bounds__(kBlock)
 k_dist_mean(const int32_t* __restrict__ offsets, const int32_t* __restrict__ entries,
             const int32_t* __restrict__ chunk_first, int chunk, int64_t n, int64_t total,
-            const float* __restrict__ pos, double4* __restrict__ mu, double4* __restrict__ part_head,
-            double4* __restrict__ part_tail, int32_t* __restrict__ entry_vertex, int64_t R,
-            float* __restrict__ out, int64_t ld_out, int C3) {
+            const float* __restrict__ pos, double sc0, double sc1, double sc2, double4* __restrict__ mu,
+            double4* __restrict__ part_head, double4* __restrict__ part_tail, int32_t* __restrict__ entry_vertex,
+            int64_t R, float* __restrict__ out, int64_t ld_out, int C3) {
   constexpr int W = kMeanSpan + 2;
   __shared__ int32_t win[W];
   __shared__ double sx[2][kBlock], sy[2][kBlock], sz[2][kBlock];
@@ -74,9 +86,9 @@ k_dist_mean(const int32_t* __restrict__ offsets, const int32_t* __restrict__ ent
     vi = window_vertex(win, W, s);
     entry_vertex[s] = v0 + vi;
     const int64_t p = entries[s] >> 2;
-    x = pos[3 * p];
-    y = pos[3 * p + 1];
-    z = pos[3 * p + 2];
+    x = static_cast<double>(pos[3 * p]) / sc0;
+    y = static_cast<double>(pos[3 * p + 1]) / sc1;
+    z = static_cast<double>(pos[3 * p + 2]) / sc2;
   }
   // segmented inclusive scan (Hillis-Steele, fixed order): a segment starts
   // where a vertex's list starts or at the span's first entry
@@ -143,7 +155,59 @@ k_dist_mean_finish(const int32_t* __restrict__ offsets, const int32_t* __restric
   mu[v] = make_double4(a.x * inv, a.y * inv, a.z * inv, 0.0);
 }
 
-// ---- the three 1x1 layers and the maximum over J_v ----
+// Coordinate c (< 3) of the distributed row of entry (point p, vertex mean m):
+// g / sigma - mu in fp64, rounded to fp32 once.  The statistics pass and the
+// MLP passes form it by this one expression, so they see the same rows.
+__device__ inline float row_coord(float g, double sc, double m) {
+  return static_cast<float>(static_cast<double>(g) / sc - m);
+}
+
+// ---- statistics of the raw distributed rows (first normalisation) ----
+// Workgroup w sums rows [w * rows_per, (w + 1) * rows_per): thread t takes
+// channel t % cp of rows t / cp, t / cp + slots, ...; the slots are then
+// added in order.  part[w] holds the cin sums, then the cin sums of squares.
+__global__ void __launch_bounds__(kBlock)
+k_dist_in_stats(const int32_t* __restrict__ entries, const int32_t* __restrict__ entry_vertex, int64_t total,
+                int64_t rows_per, const float* __restrict__ pos, double sc0, double sc1, double sc2,
+                const double4* __restrict__ mu, const float* __restrict__ feat, int64_t ld_feat, int cin, int cp,
+                double* __restrict__ part) {
+  __shared__ double sh[2][kBlock];
+  const int t = threadIdx.x;
+  const int c = t % cp, slot = t / cp, slots = kBlock / cp;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per;
+  const int64_t r1 = min(r0 + rows_per, total);
+  double s = 0.0, ss = 0.0;
+  if (c < cin) {
+    const double sc = c == 0 ? sc0 : (c == 1 ? sc1 : sc2);
+    for (int64_t e = r0 + slot; e < r1; e += slots) {
+      const int64_t p = entries[e] >> 2;
+      float x;
+      if (c < 3) {
+        const double4 m = mu[entry_vertex[e]];
+        x = row_coord(pos[3 * p + c], sc, c == 0 ? m.x : (c == 1 ? m.y : m.z));
+      } else {
+        x = feat[p * ld_feat + (c - 3)];
+      }
+      s += x;
+      ss += static_cast<double>(x) * x;
+    }
+  }
+  sh[0][t] = s;
+  sh[1][t] = ss;
+  __syncthreads();
+  if (t < cin) {
+    double a = 0.0, b = 0.0;
+    for (int sl = 0; sl < slots; ++sl) {
+      a += sh[0][sl * cp + t];
+      b += sh[1][sl * cp + t];
+    }
+    double* o = part + static_cast<int64_t>(blockIdx.x) * 2 * cin;
+    o[t] = a;
+    o[cin + t] = b;
+  }
+}
+
+// ---- the three [GN, ReLU, 1x1] blocks and the maximum over J_v ----
 // A wave owns the list entries [r0, r0 + R) and walks them 64 at a time (one
 // entry per lane for the gathers), then 16 at a time through the layers.
 // The activations stay in registers: with A = weights (16 outputs x 4
@@ -151,53 +215,70 @@ k_dist_mean_finish(const int32_t* __restrict__ offsets, const int32_t* __restric
 // v_mfma_f32_16x16x4_f32 leaves in lane (entry i, group g) the outputs
 // 4g..4g+3 of entry i, which is the B operand of the next layer once that
 // layer takes its inputs in the order (block b, register r): input
-// 16b + 4g + r in lane group g.  The weights sit in LDS in that fragment
-// order, one 64-float run per k step, so every A read is one conflict-free
-// ds_read_b32.  The maximum over J_v is a segmented scan across the 16
-// entry lanes (lists are contiguous and sorted by vertex); the segment
-// still open at the end of 16 entries is carried into the next 16.  A list
-// cut by a range boundary is finished with an order-independent atomic
-// maximum on a row the mean pass set to -inf; every other list is stored.
+// 16b + 4g + r in lane group g.  The normalisation and ReLU of a layer's
+// input are applied to those registers (per-channel scale and shift from
+// LDS).  The weights sit in LDS in fragment order, one 64-float run per k
+// step, so every A read is one conflict-free ds_read_b32.
+// STAGE 1 and 2 stop after layer 1 / 2 and add up, in fp64, the values and
+// squares of that layer's outputs over the rows (the next normalisation's
+// statistics): per lane over its rows, then across the 16 row lanes of a
+// lane group by a fixed butterfly, then over the waves in order into one
+// partial per workgroup.  STAGE 3 runs all three layers and the maximum over
+// J_v: a segmented scan across the 16 entry lanes (lists are contiguous and
+// sorted by vertex); the segment still open at the end of 16 entries is
+// carried into the next 16.  A list cut by a range boundary is finished with
+// an order-independent atomic maximum on a row the mean pass set to -inf;
+// every other list is stored.  If any normalisation parameter is not finite
+// (a NaN or infinite input reached the statistics) every output is NaN.
 constexpr int kWaves = kBlock / 64;
 constexpr int kMaxBlocks = kMaxC / 16;
 constexpr int kMaxK1Steps = kMaxC / 4;
 
-constexpr int kTilePitch = 64 + 4;
-constexpr int kMlpRange = 128;       // list entries per wave of the MLP pass   // row pitch of a wave's 16 x 64 output tile
+constexpr int kTilePitch = 64 + 4;   // row pitch of a wave's 16 x 64 output tile
+constexpr int kMlpRange = 128;       // list entries per wave of the MLP pass
 
 struct MlpLds {
-  size_t a1, a2, a3, b, x, o, end;   // in floats
+  size_t a1, a2, a3, b, g, x, o, end;   // in floats
   __host__ __device__ MlpLds(int ks1, int nb1, int nb2, int nb3) {
     a1 = 0;
     a2 = a1 + static_cast<size_t>(nb1) * ks1 * 64;
     a3 = a2 + static_cast<size_t>(nb2) * nb1 * 4 * 64;
     b = a3 + static_cast<size_t>(nb3) * nb2 * 4 * 64;
-    x = b + 16 * static_cast<size_t>(nb1 + nb2 + nb3);
+    g = b + 16 * static_cast<size_t>(nb1 + nb2 + nb3);
+    x = g + 3 * static_cast<size_t>(kPreStride);   // normalisation tables of the three layer inputs
     o = x + static_cast<size_t>(kWaves) * 4 * ks1 * 64;   // per wave: 4 groups of 16 entries x ks1 k steps
     end = o + static_cast<size_t>(kWaves) * 16 * kTilePitch;
   }
   __host__ __device__ size_t bytes() const { return end * 4; }
 };
+static_assert(16 * kTilePitch * 4 >= 2 * kMaxC * 8, "a wave's output tile holds its statistics");
 
 __device__ inline f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-// max into *a for any mix of signs: non-negative floats order like their bit
-// patterns as signed integers, negative ones inversely as unsigned integers
-__device__ inline void atomic_max_f32(float* a, float x) {
-  const unsigned u = __float_as_uint(x);
+// max into *a of the float with bits u, for any mix of signs: non-negative
+// floats order like their bit patterns as signed integers, negative ones
+// inversely as unsigned integers (a NaN with a clear sign bit, as written
+// here, wins over every number)
+__device__ inline void atomic_max_f32_bits(float* a, unsigned u) {
   if (u >> 31) atomicMin(reinterpret_cast<unsigned*>(a), u);
   else atomicMax(reinterpret_cast<int*>(a), static_cast<int>(u));
 }
 
-// Lane c holds output channel c of vertex v's maximum.
-__device__ inline void emit_col(float* __restrict__ out, int64_t ld_out, int32_t v, bool shared, float m, int c3,
-                                int lane) {
+// Lane c holds output channel c of vertex v's maximum, or NaN when `bad`.
+__device__ inline void emit_col(float* __restrict__ out, int64_t ld_out, int32_t v, bool shared, float m, bool bad,
+                                int c3, int lane) {
   if (lane >= c3) return;
+  const unsigned u = bad ? 0x7fc00000u : __float_as_uint(m);
   float* o = out + static_cast<int64_t>(v) * ld_out + lane;
-  if (shared) atomic_max_f32(o, m);
-  else *o = m;
+  if (shared) atomic_max_f32_bits(o, u);
+  else *reinterpret_cast<unsigned*>(o) = u;
+}
+
+// not finite (NaN or infinite), tested on the bits
+__device__ inline bool nonfinite_bits(float x) {
+  return (__float_as_uint(x) & 0x7f800000u) == 0x7f800000u;
 }
 
 // dst[q] = f(q) for q < count, BATCH independent loads in flight per thread
@@ -242,24 +323,76 @@ struct Staged {
   }
 };
 
+// Per-lane fp64 sums of a layer's outputs (channels 16 nb + 4 g + r of the
+// lane's row) and of their squares.
+template <int NB>
+struct LayerStats {
+  double s[NB][4], q[NB][4];
+  __device__ LayerStats() {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) s[nb][r] = q[nb][r] = 0.0;
+  }
+  __device__ void add(const f32x4* h, bool valid) {
+    if (!valid) return;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const double x = h[nb][r];
+        s[nb][r] += x;
+        q[nb][r] += x * x;
+      }
+  }
+  // sums over the 16 row lanes of each lane group (xor butterfly), then
+  // lane 16 g writes channels 16 nb + 4 g + r of its wave's column
+  __device__ void to_lds(double* red, int lane) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          s[nb][r] += __shfl_xor(s[nb][r], off);
+          q[nb][r] += __shfl_xor(q[nb][r], off);
+        }
+    if ((lane & 15) == 0) {
+      const int g = lane >> 4;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          red[16 * nb + 4 * g + r] = s[nb][r];
+          red[kMaxC + 16 * nb + 4 * g + r] = q[nb][r];
+        }
+    }
+  }
+};
+
 // NB1..NB3: blocks of 16 outputs per layer; KS1: k steps of the first layer,
 // or 0 for the runtime ks1.  Layers narrower than the instance run
-// zero-padded (zero weights and biases: the padded hidden units are
-// relu(0) = 0 and the padded outputs are not written).  With KS1 > 0 the
-// whole range's gathers and the weights are loaded into registers before
-// the workgroup's first barrier, so their latencies overlap; with KS1 = 0
-// (any feature count) the rows are gathered into LDS 64 at a time.  WPE:
-// waves per SIMD the register allocation must allow.
-template <int NB1, int NB2, int NB3, int KS1, int WPE>
+// zero-padded (zero weights, biases and normalisation parameters: the padded
+// hidden units are relu(0) = 0 and the padded outputs are not written).
+// With KS1 > 0 the whole range's gathers and the weights are loaded into
+// registers before the workgroup's first barrier, so their latencies
+// overlap; with KS1 = 0 (any feature count) the rows are gathered into LDS
+// 64 at a time.  WPE: waves per SIMD the register allocation must allow.
+// pre: the three normalisation tables, kPreStride floats apart, each the C
+// scales then the C shifts of its layer's input (C = 3 + cf, c1, c2).
+// part (STAGE 1, 2): per workgroup the sums, then the sums of squares, of
+// the c1 (STAGE 1) or c2 (STAGE 2) outputs.
+template <int NB1, int NB2, int NB3, int KS1, int WPE, int STAGE>
 __global__ void __launch_bounds__(kBlock, WPE)
 k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entry_vertex, int64_t total,
-           const float* __restrict__ pos, const float* __restrict__ feat, int64_t ld_feat, int cf,
-           const double4* __restrict__ mu, const float* __restrict__ W1, const float* __restrict__ b1,
-           const float* __restrict__ W2, const float* __restrict__ b2, const float* __restrict__ W3,
-           const float* __restrict__ b3, int ks1_rt, int c1, int c2, int c3, float* __restrict__ out,
-           int64_t ld_out) {
+           const float* __restrict__ pos, double sc0, double sc1, double sc2, const float* __restrict__ feat,
+           int64_t ld_feat, int cf, const double4* __restrict__ mu, const float* __restrict__ pre,
+           const float* __restrict__ W1, const float* __restrict__ b1, const float* __restrict__ W2,
+           const float* __restrict__ b2, const float* __restrict__ W3, const float* __restrict__ b3, int ks1_rt,
+           int c1, int c2, int c3, float* __restrict__ out, int64_t ld_out, double* __restrict__ part) {
   constexpr bool kPre = KS1 > 0;
   constexpr int kPer = kMlpRange / 64;   // groups of 64 entries per wave
+  constexpr int NBS = STAGE == 1 ? NB1 : (STAGE == 2 ? NB2 : 1);
   extern __shared__ __align__(16) float sm[];
   const int ks1 = kPre ? KS1 : ks1_rt;
   const MlpLds lay(ks1, NB1, NB2, NB3);
@@ -268,10 +401,10 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
   const int64_t r0 = (static_cast<int64_t>(blockIdx.x) * kWaves + wave) * kMlpRange;
   const bool active = r0 < total;
   const int64_t r1 = active ? min(r0 + kMlpRange, total) : r0;
+  const int cin = 3 + cf;
 
   // weight fragments: run (nb, k step) holds, for lane (i, g), the weight of
   // output 16 nb + i and the k step's input for lane group g
-  const int cin = 3 + cf;
   auto w1_at = [&](int q) {
     const int run = q >> 6, L = q & 63;
     const int nb = run / ks1, ks = run - nb * ks1;
@@ -301,22 +434,50 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
     i -= 16 * NB2;
     return (i < c3 && b3) ? b3[i] : 0.f;
   };
+  // normalisation tables by input slot: table 0 indexed by the first layer's
+  // k (k = 3 is the zero pad), tables 1 and 2 by channel; scales at [0, 64),
+  // shifts at [64, 128) of each table
+  auto g_at = [&](int q) {
+    const int tab = q / kPreStride, w = q - tab * kPreStride;
+    const int sh = w >= kMaxC, k = w - (sh ? kMaxC : 0);
+    int ch, C;
+    if (tab == 0) {
+      ch = k < 3 ? k : (k == 3 ? -1 : (k - 4 < cf ? k - 1 : -1));
+      C = cin;
+    } else {
+      C = tab == 1 ? c1 : c2;
+      ch = k < C ? k : -1;
+    }
+    return ch >= 0 ? pre[tab * kPreStride + sh * C + ch] : 0.f;
+  };
+  // any parameter of the used normalisations that is not finite
+  bool bad_local = false;
+  if constexpr (STAGE == 3) {
+    for (int q = t; q < 3 * kPreStride; q += kBlock) {
+      const int tab = q / kPreStride, w = q - tab * kPreStride;
+      const int C = tab == 0 ? cin : (tab == 1 ? c1 : c2);
+      if ((w % kMaxC) < C && nonfinite_bits(pre[tab * kPreStride + (w >= kMaxC ? C : 0) + (w % kMaxC)]))
+        bad_local = true;
+    }
+  }
 
-  // per lane: vertex and input row [g - mu (fp64, rounded once), 0, f] of
-  // entry r0 + 64 j + lane (registers only when kPre)
+  // per lane: vertex and input row [g / sigma - mu (fp64, rounded once), 0, f]
+  // of entry r0 + 64 j + lane (registers only when kPre)
   constexpr int kRow = kPre ? 4 * KS1 : 1;
   int32_t vtx[kPer];
   float xr[kPre ? kPer : 1][kRow];
   int32_t key_before = -1, key_after = -1;   // the vertices whose lists run past the range's two ends
   if constexpr (kPre) {
     Staged<NB1 * KS1 * 64> s1;
-    Staged<NB2 * NB1 * 4 * 64> s2;
-    Staged<NB3 * NB2 * 4 * 64> s3;
+    Staged<(STAGE >= 2 ? NB2 * NB1 * 4 * 64 : 1)> s2;
+    Staged<(STAGE >= 3 ? NB3 * NB2 * 4 * 64 : 1)> s3;
     Staged<16 * (NB1 + NB2 + NB3)> sb;
+    Staged<3 * kPreStride> sg;
     s1.load(w1_at);
-    s2.load(w2_at);
-    s3.load(w3_at);
+    if constexpr (STAGE >= 2) s2.load(w2_at);
+    if constexpr (STAGE >= 3) s3.load(w3_at);
     sb.load(b_at);
+    sg.load(g_at);
     int32_t ent[kPer];
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
@@ -340,49 +501,56 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
     for (int j = 0; j < kPer; ++j) {
       double4 m = make_double4(0.0, 0.0, 0.0, 0.0);
       if (vtx[j] >= 0) m = mu[vtx[j]];
-      xr[j][0] = static_cast<float>(static_cast<double>(g[j][0]) - m.x);
-      xr[j][1] = static_cast<float>(static_cast<double>(g[j][1]) - m.y);
-      xr[j][2] = static_cast<float>(static_cast<double>(g[j][2]) - m.z);
+      xr[j][0] = row_coord(g[j][0], sc0, m.x);
+      xr[j][1] = row_coord(g[j][1], sc1, m.y);
+      xr[j][2] = row_coord(g[j][2], sc2, m.z);
     }
     s1.store(sm + lay.a1);
-    s2.store(sm + lay.a2);
-    s3.store(sm + lay.a3);
+    if constexpr (STAGE >= 2) s2.store(sm + lay.a2);
+    if constexpr (STAGE >= 3) s3.store(sm + lay.a3);
     sb.store(sm + lay.b);
+    sg.store(sm + lay.g);
   } else {
     stage<8>(sm + lay.a1, NB1 * ks1 * 64, w1_at);
-    stage<8>(sm + lay.a2, NB2 * NB1 * 4 * 64, w2_at);
-    stage<8>(sm + lay.a3, NB3 * NB2 * 4 * 64, w3_at);
+    if constexpr (STAGE >= 2) stage<8>(sm + lay.a2, NB2 * NB1 * 4 * 64, w2_at);
+    if constexpr (STAGE >= 3) stage<8>(sm + lay.a3, NB3 * NB2 * 4 * 64, w3_at);
     stage<2>(sm + lay.b, 16 * (NB1 + NB2 + NB3), b_at);
+    stage<2>(sm + lay.g, 3 * kPreStride, g_at);
     if (active) {
       key_before = r0 > 0 ? entry_vertex[r0 - 1] : -1;
       key_after = r1 < total ? entry_vertex[r1] : -1;
     }
   }
-  __syncthreads();
-  if (!active) return;
+  const bool bad = __syncthreads_or(bad_local) != 0;
+  if (STAGE == 3 && !active) return;
 
   const float* A1 = sm + lay.a1 + lane;
   const f32x4* A2 = reinterpret_cast<const f32x4*>(sm + lay.a2) + lane;
   const f32x4* A3 = reinterpret_cast<const f32x4*>(sm + lay.a3) + lane;
   const float* bias = sm + lay.b + 4 * lg;
+  const float* G0 = sm + lay.g;                               // by first-layer k
+  const float* G1 = sm + lay.g + kPreStride + 4 * lg;         // by channel 16 kb + 4 g + r
+  const float* G2 = sm + lay.g + 2 * kPreStride + 4 * lg;
   float* X = sm + lay.x + static_cast<size_t>(wave) * 4 * ks1 * 64;
   float* T = sm + lay.o + static_cast<size_t>(wave) * 16 * kTilePitch;
   int32_t ckey = -1;   // vertex whose maximum is open (wave-uniform)
   float cmax = 0.f;    // its running maximum, channel `lane`
+  LayerStats<NBS> stats;
 
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     const int64_t base = r0 + 64 * j;
     if (base >= r1) break;
-    // the 64 rows as B fragments: group lane/16, k step k/4, slot
-    // 16 (k%4) + lane%16
+    // the 64 rows, normalised and rectified, as B fragments: group lane/16,
+    // k step k/4, slot 16 (k%4) + lane%16
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // the last group's reads of X come first
     float* xs = X + (lane >> 4) * ks1 * 64 + (lane & 15);
+    auto norm0 = [&](int k, float x) { return fmaxf(fmaf(x, G0[k], G0[kMaxC + k]), 0.f); };
     int32_t v;
     if constexpr (kPre) {
       v = vtx[j];
 #pragma unroll
-      for (int k = 0; k < kRow; ++k) xs[(k >> 2) * 64 + (k & 3) * 16] = xr[j][k];
+      for (int k = 0; k < kRow; ++k) xs[(k >> 2) * 64 + (k & 3) * 16] = v >= 0 ? norm0(k, xr[j][k]) : 0.f;
     } else {
       const int64_t s = base + lane;
       v = -1;
@@ -391,12 +559,12 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
         v = entry_vertex[s];
         const int64_t p = e >> 2;
         const double4 m = mu[v];
-        xs[0] = static_cast<float>(static_cast<double>(pos[3 * p]) - m.x);
-        xs[16] = static_cast<float>(static_cast<double>(pos[3 * p + 1]) - m.y);
-        xs[32] = static_cast<float>(static_cast<double>(pos[3 * p + 2]) - m.z);
+        xs[0] = norm0(0, row_coord(pos[3 * p], sc0, m.x));
+        xs[16] = norm0(1, row_coord(pos[3 * p + 1], sc1, m.y));
+        xs[32] = norm0(2, row_coord(pos[3 * p + 2], sc2, m.z));
         xs[48] = 0.f;
         for (int k = 4; k < 4 * ks1; ++k)
-          xs[(k >> 2) * 64 + (k & 3) * 16] = k - 4 < cf ? feat[p * ld_feat + (k - 4)] : 0.f;
+          xs[(k >> 2) * 64 + (k & 3) * 16] = k - 4 < cf ? norm0(k, feat[p * ld_feat + (k - 4)]) : 0.f;
       } else {
         for (int k = 0; k < 4 * ks1; ++k) xs[(k >> 2) * 64 + (k & 3) * 16] = 0.f;
       }
@@ -412,6 +580,8 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
       // (this compiler barrier stops them from being hoisted into registers
       // for the whole loop, which would cut the resident waves)
       __asm__ volatile("" ::: "memory");
+      // (the shuffles run on all lanes: a lane masked off would read as 0)
+      const int32_t krow = __shfl(v, 16 * grp + li);
       f32x4 h1[NB1], h2[NB2], o3[NB3];
 #pragma unroll
       for (int nb = 0; nb < NB1; ++nb) h1[nb] = *reinterpret_cast<const f32x4*>(bias + 16 * nb);
@@ -430,6 +600,10 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
           for (int nb = 0; nb < NB1; ++nb) h1[nb] = mfma4(A1[(nb * ks1 + ks) * 64], x, h1[nb]);
         }
       }
+      if constexpr (STAGE == 1) {
+        stats.add(h1, krow >= 0);
+        continue;
+      }
 #pragma unroll
       for (int nb = 0; nb < NB2; ++nb) h2[nb] = *reinterpret_cast<const f32x4*>(bias + 16 * NB1 + 16 * nb);
 #pragma unroll
@@ -437,12 +611,18 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
         f32x4 w[NB2];
 #pragma unroll
         for (int nb = 0; nb < NB2; ++nb) w[nb] = A2[(nb * NB1 + kb) * 64];
+        const f32x4 gs = *reinterpret_cast<const f32x4*>(G1 + 16 * kb);
+        const f32x4 gt = *reinterpret_cast<const f32x4*>(G1 + kMaxC + 16 * kb);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float x = fmaxf(h1[kb][r], 0.f);
+          const float x = fmaxf(fmaf(h1[kb][r], gs[r], gt[r]), 0.f);
 #pragma unroll
           for (int nb = 0; nb < NB2; ++nb) h2[nb] = mfma4(w[nb][r], x, h2[nb]);
         }
+      }
+      if constexpr (STAGE == 2) {
+        stats.add(h2, krow >= 0);
+        continue;
       }
 #pragma unroll
       for (int nb = 0; nb < NB3; ++nb)
@@ -452,9 +632,11 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
         f32x4 w[NB3];
 #pragma unroll
         for (int nb = 0; nb < NB3; ++nb) w[nb] = A3[(nb * NB2 + kb) * 64];
+        const f32x4 gs = *reinterpret_cast<const f32x4*>(G2 + 16 * kb);
+        const f32x4 gt = *reinterpret_cast<const f32x4*>(G2 + kMaxC + 16 * kb);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float x = fmaxf(h2[kb][r], 0.f);
+          const float x = fmaxf(fmaf(h2[kb][r], gs[r], gt[r]), 0.f);
 #pragma unroll
           for (int nb = 0; nb < NB3; ++nb) o3[nb] = mfma4(w[nb][r], x, o3[nb]);
         }
@@ -467,8 +649,6 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
       // vertex -1, which is never written.
 #pragma unroll
       for (int nb = 0; nb < NB3; ++nb) *reinterpret_cast<f32x4*>(T + li * kTilePitch + 16 * nb + 4 * lg) = o3[nb];
-      // (both shuffles run on all lanes: a lane masked off would read as 0)
-      const int32_t krow = __shfl(v, 16 * grp + li);
       const int32_t kup = __shfl(v, (16 * grp + li + 63) & 63);
       const int32_t kprev = li > 0 ? kup : ckey;
       const uint32_t starts = static_cast<uint32_t>(__ballot(krow != kprev)) & 0xffffu;
@@ -478,7 +658,8 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
       for (int i = 0; i < 16; ++i) {
         const float x = T[i * kTilePitch + lane];
         if ((starts >> i) & 1u) {
-          if (ckey >= 0) emit_col(out, ld_out, ckey, ckey == key_before || ckey == key_after, cmax, c3, lane);
+          if (ckey >= 0)
+            emit_col(out, ld_out, ckey, ckey == key_before || ckey == key_after, cmax, bad, c3, lane);
           ckey = __builtin_amdgcn_readlane(v, 16 * grp + i);
           cmax = x;
         } else {
@@ -488,55 +669,141 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // the walk's reads come before the next tile's writes
     }
   }
-  if (ckey >= 0) emit_col(out, ld_out, ckey, ckey == key_before || ckey == key_after, cmax, c3, lane);
+  if constexpr (STAGE == 3) {
+    if (ckey >= 0)
+      emit_col(out, ld_out, ckey, ckey == key_before || ckey == key_after, cmax, bad, c3, lane);
+  } else {
+    // the workgroup's partial: the waves' columns added in wave order
+    double* red = reinterpret_cast<double*>(T);
+    stats.to_lds(red, lane);
+    __syncthreads();
+    const int cst = STAGE == 1 ? c1 : c2;
+    if (t < cst) {
+      double a = 0.0, b = 0.0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const double* rw = reinterpret_cast<const double*>(sm + lay.o + static_cast<size_t>(w) * 16 * kTilePitch);
+        a += rw[t];
+        b += rw[kMaxC + t];
+      }
+      double* o = part + static_cast<int64_t>(blockIdx.x) * 2 * cst;
+      o[t] = a;
+      o[cst + t] = b;
+    }
+  }
 }
 
+void stats_parts(int64_t total, int cp, int64_t* nparts, int64_t* rows_per) {
+  const int slots = kBlock / cp;
+  int64_t rp = std::max<int64_t>(slots, (total + kStatsMaxParts - 1) / kStatsMaxParts);
+  rp = (rp + slots - 1) / slots * slots;
+  *rows_per = rp;
+  *nparts = std::max<int64_t>(1, (total + rp - 1) / rp);
+}
+
+int64_t mlp_grid(int64_t total) {
+  const int64_t waves = (total + kMlpRange - 1) / kMlpRange;
+  return (waves + kWaves - 1) / kWaves;
+}
+
+template <int NB1, int NB2, int NB3, int KS1, int WPE>
+void run_mlp(int stage, const MlpLds& lay, unsigned grid, hipStream_t s, const int32_t* entries, const int32_t* ev,
+             int64_t total, const float* pos, const double sc[3], const float* feat, int64_t ld_feat, int cf,
+             const double4* mu, const float* pre, const float* W1, const float* b1, const float* W2, const float* b2,
+             const float* W3, const float* b3, int ks1, int C1, int C2, int C3, float* out, int64_t ld_out,
+             double* part) {
+  auto k1 = k_dist_mlp<NB1, NB2, NB3, KS1, WPE, 1>;
+  auto k2 = k_dist_mlp<NB1, NB2, NB3, KS1, WPE, 2>;
+  auto k3 = k_dist_mlp<NB1, NB2, NB3, KS1, WPE, 3>;
+  auto kernel = stage == 1 ? k1 : (stage == 2 ? k2 : k3);
+  if (!KS1) {
+    // the runtime-width instance may need more than the default LDS limit
+    static bool lds_limit_set[3] = {false, false, false};
+    if (!lds_limit_set[stage - 1]) {
+      const MlpLds worst(kMaxK1Steps, kMaxBlocks, kMaxBlocks, kMaxBlocks);
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                static_cast<int>(worst.bytes()));
+      lds_limit_set[stage - 1] = true;
+    }
+  }
+  launch(kernel, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s, entries, ev, total, pos, sc[0],
+         sc[1], sc[2], feat, ld_feat, cf, mu, pre, W1, b1, W2, b2, W3, b3, ks1, C1, C2, C3, out, ld_out, part);
+}
 
 }  // namespace
 
-int64_t distribute_workspace_bytes(int64_t total, int C3) {
-  (void)C3;
+// Work space: the vertex means (n double4), the mean pass's span partials, the
+// vertex of every list entry, the three normalisation tables, and the
+// statistics partials (at most max(512, MLP workgroups) x 2 x 64 doubles).
+int64_t distribute_workspace_bytes(int64_t n, int64_t total) {
   const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
-  return 2 * mean_spans * static_cast<int64_t>(sizeof(double4)) + 4 * total;
+  const int64_t parts = std::max<int64_t>(kStatsMaxParts, mlp_grid(total));
+  auto up = [](int64_t b) { return (b + 255) / 256 * 256; };
+  return up(32 * n) + up(2 * mean_spans * 32) + up(4 * total) + up(3 * kPreStride * 4) + up(parts * 2 * kMaxC * 8);
 }
 
-int distribute_max_features() { return kMaxC - 4; }
+int distribute_max_features() { return kMaxIn - 3; }
 
 void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* chunk_first, int chunk,
-                       int64_t n, int64_t total, const float* pos, const float* feat, int64_t ld_feat, int cf,
-                       const float* W1, const float* b1, int C1, const float* W2, const float* b2, int C2,
-                       const float* W3, const float* b3, int C3, float* out, int64_t ld_out, double* mu, void* work,
-                       hipStream_t s) {
+                       int64_t n, int64_t total, const float* pos, const double scale[3], const float* feat,
+                       int64_t ld_feat, int cf, const float* gamma, const float* beta, float eps, const float* W1,
+                       const float* b1, int C1, const float* W2, const float* b2, int C2, const float* W3,
+                       const float* b3, int C3, float* out, int64_t ld_out, void* work, hipStream_t s) {
   if (total <= 0 || n <= 0) return;
   ScopedKernelTimer tm("distribute", s);
   const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
-  double4* mh = static_cast<double4*>(work);
+  auto up = [](int64_t b) { return (b + 255) / 256 * 256; };
+  char* w = static_cast<char*>(work);
+  double4* mu4 = reinterpret_cast<double4*>(w);
+  w += up(32 * n);
+  double4* mh = reinterpret_cast<double4*>(w);
   double4* mt = mh + mean_spans;
-  int32_t* ev = reinterpret_cast<int32_t*>(mt + mean_spans);   // vertex of every list entry
-  double4* mu4 = reinterpret_cast<double4*>(mu);
+  w += up(2 * mean_spans * 32);
+  int32_t* ev = reinterpret_cast<int32_t*>(w);   // vertex of every list entry
+  w += up(4 * total);
+  float* pre = reinterpret_cast<float*>(w);
+  w += up(3 * kPreStride * 4);
+  double* part = reinterpret_cast<double*>(w);
   launch(k_dist_mean, dim3(static_cast<unsigned>(mean_spans)), dim3(kBlock), 0, s, offsets, entries, chunk_first,
-         chunk, n, total, pos, mu4, mh, mt, ev, static_cast<int64_t>(kMlpRange), out, ld_out, C3);
+         chunk, n, total, pos, scale[0], scale[1], scale[2], mu4, mh, mt, ev, static_cast<int64_t>(kMlpRange), out,
+         ld_out, C3);
   if (mean_spans > 1)
     launch(k_dist_mean_finish, dim3(static_cast<unsigned>((mean_spans + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
            offsets, chunk_first, chunk, mean_spans, mu4, static_cast<const double4*>(mh),
            static_cast<const double4*>(mt));
+  // the raw rows' statistics -> table 0
+  const int cin = 3 + cf;
+  int cp = 4;
+  while (cp < cin) cp <<= 1;
+  int64_t np0, rp0;
+  stats_parts(total, cp, &np0, &rp0);
+  launch(k_dist_in_stats, dim3(static_cast<unsigned>(np0)), dim3(kBlock), 0, s, entries,
+         static_cast<const int32_t*>(ev), total, rp0, pos, scale[0], scale[1], scale[2],
+         static_cast<const double4*>(mu4), feat, ld_feat, cin, cp, part);
+  auto groups = [](int C) { return C <= 32 ? C : 32; };
+  launch_gn_finalize(part, np0, cin, groups(cin), total, gamma, beta, eps, pre, s);
+
   const int ks1 = (4 + cf + 3) / 4;   // coordinates, a zero pad, features, in k steps of 4
   // the paper's 16-32-64 block (up to 4 raw features) has its own instance;
   // every other shape runs zero-padded to 64-64-64
   const bool paper = C1 == 16 && C2 == 32 && C3 == 64 && ks1 <= 2;
-  auto kernel = paper ? k_dist_mlp<1, 2, 4, 2, 4> : k_dist_mlp<kMaxBlocks, kMaxBlocks, kMaxBlocks, 0, 1>;
   const MlpLds lay = paper ? MlpLds(2, 1, 2, 4) : MlpLds(ks1, kMaxBlocks, kMaxBlocks, kMaxBlocks);
-  static bool lds_limit_set = false;
-  if (!lds_limit_set) {
-    const MlpLds worst(kMaxK1Steps, kMaxBlocks, kMaxBlocks, kMaxBlocks);
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_dist_mlp<kMaxBlocks, kMaxBlocks, kMaxBlocks, 0, 1>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(worst.bytes()));
-    lds_limit_set = true;
+  const unsigned grid = static_cast<unsigned>(mlp_grid(total));
+  const int64_t offs[3] = {0, cin, static_cast<int64_t>(cin) + C1};
+  for (int stage = 1; stage <= 3; ++stage) {
+    if (paper)
+      run_mlp<1, 2, 4, 2, 4>(stage, lay, grid, s, entries, ev, total, pos, scale, feat, ld_feat, cf, mu4, pre, W1,
+                             b1, W2, b2, W3, b3, ks1, C1, C2, C3, out, ld_out, part);
+    else
+      run_mlp<kMaxBlocks, kMaxBlocks, kMaxBlocks, 0, 1>(stage, lay, grid, s, entries, ev, total, pos, scale, feat,
+                                                        ld_feat, cf, mu4, pre, W1, b1, W2, b2, W3, b3, ks1, C1, C2,
+                                                        C3, out, ld_out, part);
+    if (stage < 3) {
+      const int C = stage == 1 ? C1 : C2;
+      launch_gn_finalize(part, grid, C, groups(C), total, gamma ? gamma + offs[stage] : nullptr,
+                         beta ? beta + offs[stage] : nullptr, eps, pre + stage * kPreStride, s);
+    }
   }
-  const int64_t waves = (total + kMlpRange - 1) / kMlpRange;
-  const unsigned grid = static_cast<unsigned>((waves + kWaves - 1) / kWaves);
-  launch(kernel, dim3(grid), dim3(kBlock), static_cast<uint32_t>(lay.bytes()), s, entries,
-         static_cast<const int32_t*>(ev), total, pos, feat, ld_feat, cf, static_cast<const double4*>(mu4), W1, b1, W2, b2, W3, b3, ks1, C1, C2, C3, out, ld_out);
 }
 
 }  // namespace lat

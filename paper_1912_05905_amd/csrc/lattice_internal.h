@@ -184,13 +184,16 @@ void launch_deform_slice_backward(const int32_t* idx, const float* w, int64_t m,
                                   float beta, const float* dout, int64_t ld_dout, float* dvals, int64_t ld_dvals,
                                   float* dwv, float* dbeta, void* work, hipStream_t s);
 // distribute.hip
-int64_t distribute_workspace_bytes(int64_t total, int C3);
+int64_t distribute_workspace_bytes(int64_t n, int64_t total);
 int distribute_max_features();
+// scale: sigma per axis at the lattice's level (positions enter as pos / scale);
+// gamma / beta: optional per-channel parameters of the three GroupNorms,
+// concatenated ((3 + cf) + C1 + C2 values)
 void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* chunk_first, int chunk,
-                       int64_t n, int64_t total, const float* pos, const float* feat, int64_t ld_feat, int cf,
-                       const float* W1, const float* b1, int C1, const float* W2, const float* b2, int C2,
-                       const float* W3, const float* b3, int C3, float* out, int64_t ld_out, double* mu, void* work,
-                       hipStream_t s);
+                       int64_t n, int64_t total, const float* pos, const double scale[3], const float* feat,
+                       int64_t ld_feat, int cf, const float* gamma, const float* beta, float eps, const float* W1,
+                       const float* b1, int C1, const float* W2, const float* b2, int C2, const float* W3,
+                       const float* b3, int C3, float* out, int64_t ld_out, void* work, hipStream_t s);
 // backward.hip
 void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, const float* wsum, int64_t n,
                                 const float* in, int64_t ld_in, int C, float* out, int64_t ld_out, hipStream_t s);
@@ -215,5 +218,9 @@ int gn_max_channels();
 int64_t gn_workspace_bytes(int64_t n, int C);
 void launch_gn_affine(const void* x, int64_t ld, int C, int bf16, int64_t n, int groups, const float* gamma,
                       const float* beta, float eps, float* pre, void* work, hipStream_t s);
+// per-group statistics from nparts partials (part[w][0..C) sums, part[w][C..2C)
+// sums of squares over `rows` rows) -> pre[0..C) scales, pre[C..2C) shifts
+void launch_gn_finalize(const double* part, int64_t nparts, int C, int groups, int64_t rows, const float* gamma,
+                        const float* beta, float eps, float* pre, hipStream_t s);
 
 }  // namespace lat

@@ -122,6 +122,12 @@ void gn_parts(int64_t n, int C, int64_t* nparts, int64_t* rows_per) {
 
 }  // namespace
 
+void launch_gn_finalize(const double* part, int64_t nparts, int C, int groups, int64_t rows, const float* gamma,
+                        const float* beta, float eps, float* pre, hipStream_t s) {
+  launch(k_gn_finalize, dim3(static_cast<unsigned>(groups)), dim3(kBlock), 0, s, part,
+         rows > 0 ? static_cast<int>(nparts) : 0, C, groups, rows, gamma, beta, eps, pre);
+}
+
 int gn_max_channels() { return 4 * kBlock; }
 
 int64_t gn_workspace_bytes(int64_t n, int C) {

@@ -51,8 +51,8 @@ SIGNATURES = {
     "lattice_refine_preact": (_I32, [_P, _P, _P, _I64, _I32, _I32, _P, _P, _F32, _P, _P, _I32, _I32, _I32, _P,
                                      _I64, _P]),
     "lattice_deform_slice_classify": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _I32, _P, _P]),
-    "lattice_distribute_pointnet": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _P, _P, _I32, _P, _P, _I32,
-                                           _P, _I64, _P]),
+    "lattice_distribute_pointnet": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, C.c_float, _P, _P, _I32, _P, _P,
+                                           _I32, _P, _P, _I32, _P, _I64, _P]),
     "lattice_splat_backward": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "lattice_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _I64, _P]),
     "lattice_conv_backward": (_I32, [_P, _P, _P, _I64, _I32, _P, _I32, _I32, _P, _I64, _P, _I64, _P, _I64, _P, _P,
@@ -291,10 +291,12 @@ class Lattice:
                                    _stream(stream)))
         return out
 
-    def distribute_pointnet(self, pos: torch.Tensor, feat: torch.Tensor | None, layers,
+    def distribute_pointnet(self, pos: torch.Tensor, feat: torch.Tensor | None, layers, gn=None, eps: float = 1e-5,
                             out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
         """Distribute + PointNet; layers = [(W1, b1), (W2, b2), (W3, b3)] with
-        W_i float32 [out][in] device tensors and optional biases."""
+        W_i float32 [out][in] device tensors and optional biases; gn = None or
+        (gamma, beta), the concatenated parameters of the three GroupNorms
+        ((3 + Cf) + C1 + C2 float32 values each, either may be None)."""
         (W1, b1), (W2, b2), (W3, b3) = layers
         c1, c2, c3 = W1.shape[0], W2.shape[0], W3.shape[0]
         for W in (W1, W2, W3):
@@ -303,13 +305,19 @@ class Lattice:
         if pos.dtype != torch.float32 or not pos.is_contiguous():
             raise ValueError("positions must be a contiguous m x d float32 tensor")
         cf = 0 if feat is None else feat.shape[1]
+        gam, bet = (None, None) if gn is None else gn
+        for a in (gam, bet):
+            if a is not None and (a.dtype != torch.float32 or not a.is_contiguous()
+                                  or a.numel() != 3 + cf + c1 + c2):
+                raise ValueError("GroupNorm parameters must be contiguous float32 of (3 + Cf) + C1 + C2 values")
         fp, fld = (None, 0) if feat is None else _rows(feat)
         if out is None:
             out = torch.empty((self.n, c3), dtype=torch.float32, device="cuda")
         op, old = _rows(out)
         ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
-        _check(lib().lattice_distribute_pointnet(self._h, ptr(pos), fp, fld, cf, ptr(W1), ptr(b1), c1, ptr(W2),
-                                                 ptr(b2), c2, ptr(W3), ptr(b3), c3, op, old, _stream(stream)))
+        _check(lib().lattice_distribute_pointnet(self._h, ptr(pos), fp, fld, cf, ptr(gam), ptr(bet), float(eps),
+                                                 ptr(W1), ptr(b1), c1, ptr(W2), ptr(b2), c2, ptr(W3), ptr(b3), c3,
+                                                 op, old, _stream(stream)))
         return out
 
     # ---- backward passes (float32) ----

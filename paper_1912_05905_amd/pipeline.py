@@ -226,10 +226,12 @@ class GpuPipeline:
                 yp, yld = ptr(op["dst"])
                 layers = [self.mlp[n] for n in op["layers"]]
                 (W1, b1), (W2, b2), (W3, b3) = layers
+                gam, bet = self.norms[op["norm"]]
                 check(lib.lattice_distribute_pointnet(
                     levels[op["level"]]._h, self.pos.data_ptr(), self.feat.data_ptr(), self.feat.stride(0),
-                    self.feat.shape[1], W1.data_ptr(), b1.data_ptr(), W1.shape[0], W2.data_ptr(), b2.data_ptr(),
-                    W2.shape[0], W3.data_ptr(), b3.data_ptr(), W3.shape[0], yp, yld, stream))
+                    self.feat.shape[1], gam.data_ptr(), bet.data_ptr(), 1e-5, W1.data_ptr(), b1.data_ptr(),
+                    W1.shape[0], W2.data_ptr(), b2.data_ptr(), W2.shape[0], W3.data_ptr(), b3.data_ptr(),
+                    W3.shape[0], yp, yld, stream))
             elif kind == "slice":
                 L = levels[op["level"]]
                 xp, xld = ptr(op["src"])

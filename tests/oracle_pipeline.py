@@ -64,8 +64,9 @@ class OraclePipeline:
                 write(op["dst"], y)
             elif kind == "distribute":
                 layers = [tuple(a.astype(np.float64) for a in wl.mlp[n]) for n in op["layers"]]
+                gn = tuple(a.astype(np.float64) for a in wl.norms[op["norm"]])
                 write(op["dst"], levels[op["level"]].distribute_pointnet(
-                    wl.positions.astype(np.float64), wl.features.astype(np.float64), layers))
+                    wl.positions.astype(np.float64), wl.features.astype(np.float64), layers, gn))
             elif kind == "slice":
                 outs[op["out"]] = levels[op["level"]].slice(np.ascontiguousarray(view_src(op["src"])))
             elif kind == "deform_slice":

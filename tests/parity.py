@@ -3,18 +3,18 @@
 Lattice structure is compared bit for bit after ordering the GPU's vertices
 by key (the oracle numbers vertices in lexicographic key order).  Features
 are compared with the elementwise bound
-    |g - r| <= tol * |r| + tol * sqrt(depth) * rms(r)
+    |g - r| <= tol * |r| + tol * rms(r)
 per tensor (relative, with an absolute floor at the tensor's RMS so that
-entries near zero do not demand more than the arithmetic can give).
+entries near zero do not demand more than the arithmetic can give), and
+with the normwise relative error ||g - r|| / ||r|| <= tol.
 
-depth is the number of bf16 storage roundings on the longest path from the
-inputs to the tensor (1 for fp32 and for a single bf16 op).  Both sides round
-every stored bf16 activation, but from accumulators of different precision
-(fp32 on the GPU, float64 in the oracle), so a value near a rounding boundary
-can land one bf16 ulp (2^-8 relative) apart; downstream layers mix such
-differences with random signs, so they grow like the square root of the
-number of rounding stages.  bf16 tensors must in addition have a normwise
-relative error ||g - r|| / ||r|| <= tol.
+The elementwise bound holds for one operator at a time.  In a bf16 network
+both sides round every stored activation, but from accumulators of
+different precision (fp32 on the GPU, float64 in the oracle), so a value
+near a rounding boundary can land one bf16 ulp (2^-8 relative) apart and
+later layers carry that difference on; bf16 networks are therefore checked
+operator by operator on the inputs the GPU stored (assert_close) and end to
+end by the normwise error alone (assert_normwise).
 """
 from __future__ import annotations
 
@@ -48,7 +48,7 @@ def rows_in_oracle_order(x: np.ndarray, gpu2orc: np.ndarray) -> np.ndarray:
     return out
 
 
-def assert_close(got, ref, tol, what="", depth=1):
+def assert_close(got, ref, tol, what=""):
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     assert got.shape == ref.shape, f"{what}: shape {got.shape} vs {ref.shape}"
@@ -57,7 +57,7 @@ def assert_close(got, ref, tol, what="", depth=1):
     assert np.isfinite(got).all(), f"{what}: non-finite values"
     rms = float(np.sqrt(np.mean(ref * ref)))
     err = np.abs(got - ref)
-    bound = tol * np.abs(ref) + tol * np.sqrt(depth) * rms
+    bound = tol * np.abs(ref) + tol * rms
     nrm = float(np.linalg.norm(ref))
     if nrm > 0:
         rel = float(np.linalg.norm(got - ref)) / nrm
@@ -68,6 +68,16 @@ def assert_close(got, ref, tol, what="", depth=1):
         raise AssertionError(
             f"{what}: {int(bad.sum())}/{ref.size} entries out of tolerance {tol}; worst at {i}: "
             f"got {got[i]!r} ref {ref[i]!r} (rms {rms:.3g}, max abs err {err.max():.3g})")
+
+
+def assert_normwise(got, ref, tol, what=""):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, f"{what}: shape {got.shape} vs {ref.shape}"
+    assert np.isfinite(got).all(), f"{what}: non-finite values"
+    nrm = float(np.linalg.norm(ref))
+    rel = float(np.linalg.norm(got - ref)) / nrm if nrm > 0 else float(np.linalg.norm(got))
+    assert rel <= tol, f"{what}: normwise relative error {rel:.3g} > {tol}"
 
 
 def max_errors(got, ref):

@@ -8,6 +8,8 @@ Every call goes through the C ABI via the ctypes binding.
 from __future__ import annotations
 
 import ctypes
+import json
+import os
 
 import numpy as np
 import pytest
@@ -465,46 +467,93 @@ def test_slice_and_deform_slice(L, O, C, dtype):
 # ----------------------------------------------------------------------------
 # whole pipelines
 # ----------------------------------------------------------------------------
-def rounding_depths(wl):
-    """bf16 storage roundings on the longest path to every written column
-    range and point output (see tests/parity.py)."""
-    cols = {name: np.zeros(total, dtype=np.int64) for name, (_, total) in wl.buffers.items()}
-    depth = {}
+def _check_ops_on_stored_inputs(O, wl, levels, bufs, outs, olv, g2o, rng=None, rows_per_op=None, points=None):
+    """Every operator of a workload against the oracle, each on the inputs
+    the GPU stored for it (its source columns as the GPU wrote them), so
+    every comparison is one operator deep: splat from the point features;
+    convolutions (1-hop, strided, Upsample, concatenated column ranges
+    included) on all rows or on a seeded sample of rows_per_op; DeformSlice
+    and slice on all points or a sample of `points`.  Returns the number of
+    operators checked."""
+    bf = wl.dtype == "bf16"
+    rnd = O.round_bf16 if bf else (lambda a: a)
+    tol = P.TOL_BF16 if bf else P.TOL_F32
+    host = {}
+
+    def cols(spec):
+        name, c0, cc = spec
+        if name not in host:
+            host[name] = P.rows_in_oracle_order(_host(bufs[name]), g2o[wl.buffers[name][0]])
+        return np.ascontiguousarray(host[name][:, c0:c0 + cc], dtype=np.float64)
+
+    checked = 0
     for op in wl.ops:
-        if "src" in op:
-            name, c0, cc = op["src"]
-            d_in = int(cols[name][c0:c0 + cc].max())
+        kind = op["op"]
+        if kind in ("create", "coarsen"):
+            continue
+        if kind == "splat":
+            X, _ = olv[0].splat(wl.features.astype(np.float64), normalize=bool(op["normalize"]))
+            P.assert_close(cols(op["dst"]), rnd(X), tol, "splat")
+        elif kind in ("conv", "conv_down", "refine"):
+            assert "pre" not in op and "res" not in op, "pre-activated operators are checked elsewhere"
+            lv = op["level"]
+            x = cols(op["src"])
+            W = wl.weights[op["w"]].astype(np.float64)
+            rows = None
+            if rows_per_op is not None and olv[lv].n > rows_per_op:
+                rows = np.sort(rng.choice(olv[lv].n, size=rows_per_op, replace=False))
+            if kind == "conv":
+                y = olv[lv].conv(olv[lv], x, W, relu=op["relu"], rows=rows)
+            elif kind == "conv_down":
+                y = olv[lv].conv(olv[lv - 1], x, W, relu=op["relu"], rows=rows)
+            else:
+                y = olv[lv].refine_into(olv[lv + 1], x, W, relu=op["relu"], rows=rows)
+            got = cols(op["dst"]) if rows is None else cols(op["dst"])[rows]
+            P.assert_close(got, rnd(y), tol, f"{kind} -> {op['dst']}")
+        elif kind in ("slice", "deform_slice"):
+            pts = None
+            if points is not None and wl.m > points:
+                pts = np.sort(rng.choice(wl.m, size=points, replace=False))
+            lat = olv[op["level"]]
+            if kind == "slice":
+                ref = lat.slice(cols(op["src"]), pts=pts)
+            else:
+                wv, beta = wl.vectors[op["wv"]]
+                ref, _ = lat.deform_slice(cols(op["src"]), wv.astype(np.float64), beta, pts=pts)
+            got = _host(outs[op["out"]])
+            P.assert_close(got if pts is None else got[pts], ref, P.TOL_F32, kind)
         else:
-            d_in = 0
-        if "dst" in op:
-            name, c0, cc = op["dst"]
-            cols[name][c0:c0 + cc] = d_in + 1
-            depth[(name, c0, cc)] = d_in + 1
-        if "out" in op:
-            depth[op["out"]] = d_in + 1
-    return depth
+            raise AssertionError(f"no stored-input check for operator {kind}")
+        checked += 1
+    return checked
 
 
 def _run_both(L, O, wl):
+    """Whole pipeline on the GPU and in the oracle, structure bit-exact on
+    every level.  fp32: every written column range and point output
+    elementwise.  bf16: every operator elementwise on its stored inputs, and
+    every tensor normwise end to end."""
     from paper_1912_05905_amd.pipeline import GpuPipeline
-    levels, bufs, outs = GpuPipeline(wl).step()
+    levels, bufs, outs = GpuPipeline(wl).step(keep=wl.dtype == "bf16")
     olv, obufs, oouts = OraclePipeline(wl).run()
     bf = wl.dtype == "bf16"
     tol = P.TOL_BF16 if bf else P.TOL_F32
-    depth = rounding_depths(wl)
+    check = P.assert_normwise if bf else P.assert_close
     g2o = {}
     for lv in sorted(levels):
         g2o[lv] = _check_structure(levels[lv], olv[lv])
-    for key, d in depth.items():
-        if not isinstance(key, tuple):
-            continue
-        name, c0, cc = key
+    written = []
+    for op in wl.ops:
+        if "dst" in op and op["dst"] not in written:
+            written.append(op["dst"])
+    for name, c0, cc in written:
         lv = wl.buffers[name][0]
         got = P.rows_in_oracle_order(_host(bufs[name]), g2o[lv])[:, c0:c0 + cc]
-        P.assert_close(got, obufs[name][:, c0:c0 + cc], tol, f"{name}[{c0}:{c0 + cc}]",
-                       depth=d if bf else 1)
+        check(got, obufs[name][:, c0:c0 + cc], tol, f"{name}[{c0}:{c0 + cc}]")
     for name in outs:
-        P.assert_close(_host(outs[name]), oouts[name], tol, name, depth=depth[name] if bf else 1)
+        check(_host(outs[name]), oouts[name], tol, name)
+    if bf:
+        _check_ops_on_stored_inputs(O, wl, levels, bufs, outs, olv, g2o)
     return levels
 
 
@@ -520,7 +569,7 @@ def test_pipeline_config5_full_size_sampled(L, O):
     thirteen convolutions on a seeded sample of 4,000 output rows (1-hop,
     strided and Upsample, concatenated column ranges included), DeformSlice
     on 50,000 points.  Every operator's inputs are the bf16 values the GPU
-    stored, so each comparison is one rounding deep."""
+    stored, so each comparison is one operator deep."""
     from paper_1912_05905_amd.pipeline import GpuPipeline
     wl = configs.make(5)
     pipe = GpuPipeline(wl)
@@ -532,41 +581,8 @@ def test_pipeline_config5_full_size_sampled(L, O):
         elif op["op"] == "coarsen":
             olv[op["level"]] = olv[op["level"] - 1].coarsen()
     g2o = {lv: _check_structure(levels[lv], olv[lv]) for lv in sorted(levels)}
-    host = {}
-
-    def cols(spec):
-        name, c0, cc = spec
-        if name not in host:
-            host[name] = P.rows_in_oracle_order(_host(bufs[name]), g2o[wl.buffers[name][0]])
-        return np.ascontiguousarray(host[name][:, c0:c0 + cc], dtype=np.float64)
-
-    rng = np.random.default_rng(55)
-    checked = 0
-    for op in wl.ops:
-        kind = op["op"]
-        if kind == "splat":
-            X, _ = olv[0].splat(wl.features.astype(np.float64), normalize=bool(op["normalize"]))
-            P.assert_close(cols(op["dst"]), O.round_bf16(X), P.TOL_BF16, "splat")
-            checked += 1
-        elif kind in ("conv", "conv_down", "refine"):
-            lv = op["level"]
-            x = cols(op["src"])
-            W = wl.weights[op["w"]].astype(np.float64)
-            rows = np.sort(rng.choice(olv[lv].n, size=min(4000, olv[lv].n), replace=False))
-            if kind == "conv":
-                y = olv[lv].conv(olv[lv], x, W, relu=op["relu"], rows=rows)
-            elif kind == "conv_down":
-                y = olv[lv].conv(olv[lv - 1], x, W, relu=op["relu"], rows=rows)
-            else:
-                y = olv[lv].refine_into(olv[lv + 1], x, W, relu=op["relu"], rows=rows)
-            P.assert_close(cols(op["dst"])[rows], O.round_bf16(y), P.TOL_BF16, f"{kind} -> {op['dst']}")
-            checked += 1
-        elif kind == "deform_slice":
-            wv, beta = wl.vectors[op["wv"]]
-            pts = np.sort(rng.choice(wl.m, size=50_000, replace=False))
-            ref, _ = olv[0].deform_slice(cols(op["src"]), wv.astype(np.float64), beta, pts=pts)
-            P.assert_close(_host(outs[op["out"]])[pts], ref, P.TOL_F32, "deform slice")
-            checked += 1
+    checked = _check_ops_on_stored_inputs(O, wl, levels, bufs, outs, olv, g2o, rng=np.random.default_rng(55),
+                                          rows_per_op=4000, points=50_000)
     assert checked == 15
     GpuPipeline.release(levels)
 
@@ -621,25 +637,66 @@ def _pointnet_layers(rng, cin, widths):
     return layers
 
 
-def _distribute_pair(L, O, gl, ol, g2o, pos, F, widths, seed):
+def _distribute_pair(L, O, gl, ol, g2o, pos, F, widths, seed, affine=True, eps=1e-5):
     rng = np.random.default_rng(seed)
     cf = 0 if F is None else F.shape[1]
     layers = _pointnet_layers(rng, 3 + cf, widths)
     dev_layers = [(_dev(W), _dev(b)) for W, b in layers]
-    gy = gl.distribute_pointnet(_dev(pos), None if F is None else _dev(F), dev_layers)
+    tot = 3 + cf + widths[0] + widths[1]
+    gn = ((1.0 + 0.1 * rng.normal(size=tot)).astype(np.float32), (0.1 * rng.normal(size=tot)).astype(np.float32)) \
+        if affine else None
+    gy = gl.distribute_pointnet(_dev(pos), None if F is None else _dev(F), dev_layers,
+                                None if gn is None else (_dev(gn[0]), _dev(gn[1])), eps=eps)
     oy = ol.distribute_pointnet(pos.astype(np.float64), None if F is None else F.astype(np.float64),
-                                [(W.astype(np.float64), b.astype(np.float64)) for W, b in layers])
+                                [(W.astype(np.float64), b.astype(np.float64)) for W, b in layers],
+                                None if gn is None else tuple(a.astype(np.float64) for a in gn), eps=eps)
     return P.rows_in_oracle_order(_host(gy), g2o), oy
 
 
-@pytest.mark.parametrize("cf,widths", [(4, (16, 32, 64)), (0, (16, 32, 64)), (13, (32, 32, 48)),
-                                        (60, (64, 64, 64)), (3, (16, 16, 16))])
-def test_distribute_pointnet(L, O, cf, widths):
+@pytest.mark.parametrize("cf,widths,affine", [(4, (16, 32, 64), True), (0, (16, 32, 64), True),
+                                               (13, (32, 32, 48), True), (29, (64, 64, 64), True),
+                                               (3, (16, 16, 16), False), (1, (64, 32, 64), True)])
+def test_distribute_pointnet(L, O, cf, widths, affine):
     pos = _cloud(200 + cf, 9000, 0.7)
     gl, ol, g2o = _pair(L, O, pos, 0.06)
     F = None if cf == 0 else np.random.default_rng(cf).normal(size=(pos.shape[0], cf)).astype(np.float32)
-    g, o = _distribute_pair(L, O, gl, ol, g2o, pos, F, widths, cf)
+    g, o = _distribute_pair(L, O, gl, ol, g2o, pos, F, widths, cf, affine)
     P.assert_close(g, o, P.TOL_F32, f"distribute cf={cf} {widths}")
+
+
+def test_distribute_pointnet_golden_cases(L, O):
+    """The hand-worked two-point cases of the oracle's pins, on the GPU."""
+    doc = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "distribute_cases.json")))
+    for c in doc["cases"]:
+        pos = np.array(c["positions"], np.float32)
+        gl = L.Lattice.create(_dev(pos), [c["sigma"]] * 3)
+        layers = []
+        k = 4
+        for i, w in enumerate(c["widths"]):
+            W = np.zeros((w, k), np.float32)
+            for o, j, v in c[f"W{i + 1}_nonzero"]:
+                W[o, j] = v
+            layers.append((_dev(W), _dev(np.array(c[f"b{i + 1}"], np.float32))))
+            k = w
+        got = _host(gl.distribute_pointnet(_dev(pos), _dev(np.array(c["features"], np.float32)), layers,
+                                           (_dev(np.array(c["gamma"], np.float32)),
+                                            _dev(np.array(c["beta"], np.float32))), eps=c["eps"]))
+        want = np.array(c["expected"])
+        assert got.shape == (4, len(want))
+        assert np.abs(got - want[None]).max() <= 1e-5 * (1 + np.abs(want).max()), c["name"]
+        gl.destroy()
+
+
+def test_distribute_pointnet_nonfinite_feature(L, O):
+    """A NaN or infinite feature reaches the statistics of its channel; the
+    whole output is then NaN, as in the oracle."""
+    pos = _cloud(231, 3000, 0.6)
+    gl, ol, g2o = _pair(L, O, pos, 0.08)
+    for bad in (np.nan, np.inf):
+        F = np.random.default_rng(3).normal(size=(pos.shape[0], 2)).astype(np.float32)
+        F[1234, 1] = bad
+        g, o = _distribute_pair(L, O, gl, ol, g2o, pos, F, (16, 32, 64), 4)
+        assert np.isnan(o).all() and np.isnan(g).all()
 
 
 def test_distribute_pointnet_skewed_and_far(L, O):
@@ -928,7 +985,7 @@ def _preact_case(L, O, gd, gs, od, os_, g2o_d, g2o_s, form, cin, cout, groups, s
                         bias=_dev(b), refine=form == "upsample")
     tol = P.TOL_BF16 if bf else P.TOL_F32
     P.assert_close(P.rows_in_oracle_order(_host(gy), g2o_d), rnd(oy), tol,
-                   f"preact {form} {cin}->{cout} G={groups} {dtype}", depth=2 if bf else 1)
+                   f"preact {form} {cin}->{cout} G={groups} {dtype}")
 
 
 @pytest.mark.parametrize("cin,cout,groups", [(64, 64, 32), (12, 20, 4), (128, 128, 32), (32, 96, 1), (64, 16, 64),

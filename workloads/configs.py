@@ -14,9 +14,10 @@ Operations (fields in brackets):
   refine        [level, src, dst, w, relu]        transposed convolution level+1 -> level
   slice         [level, src, out]                 vertex values -> points
   deform_slice  [level, src, wv, beta, out]       DeformSlice to points
-  distribute    [level, dst, layers]              Distribute + PointNet of the point
+  distribute    [level, dst, layers, norm]        Distribute + PointNet of the point
                                                   positions and features (layers: names
-                                                  of (W [out][in], b) pairs in `mlp`)
+                                                  of (W [out][in], b) pairs in `mlp`;
+                                                  norm: the GroupNorm parameters in `norms`)
 `src`/`dst` are (buffer, first column, channels); buffers are row-major
 (vertices of their level) x (total channels), so several ops can write
 disjoint column ranges of one buffer (concatenation without a copy).
@@ -205,17 +206,32 @@ def config6(seed: int = 3, m: int = 120_000) -> Workload:
     F = np.concatenate([inten, u], axis=1).astype(np.float32)
     wl = Workload(6, "lidar-distribute", seed, pos, np.full(3, 0.3, np.float32), "f32", F)
     wl.buffers = {"p0": (0, 64), "e0": (0, 64)}
-    k = 3 + F.shape[1]
-    for i, c in enumerate((16, 32, 64)):
-        W = gen.normal_matrix(seed, f"pointnet{i}", c, k, 1.0 / np.sqrt(k))
-        b = gen.normal_matrix(seed, f"pointnet{i}:bias", 1, c, 0.1)[0]
-        wl.mlp[f"pointnet{i}"] = (W, b)
-        k = c
+    names = _pointnet(wl, seed, (16, 32, 64))
     wl.ops = [dict(op="create", level=0),
-              dict(op="distribute", level=0, dst=("p0", 0, 64), layers=["pointnet0", "pointnet1", "pointnet2"])]
+              dict(op="distribute", level=0, dst=("p0", 0, 64), layers=names, norm="pointnet")]
     _conv(wl, "conv", 0, ("p0", 0, 64), ("e0", 0, 64), True, seed)
     wl.ops.append(dict(op="slice", level=0, src=("e0", 0, 64), out="slice"))
     return _finish(wl)
+
+
+def _pointnet(wl, seed, widths):
+    """The PointNet block's three 1x1 layers (W ~ N(0, 1/fan_in), biases
+    N(0, 0.1^2)) and its three GroupNorms (gamma ~ 1 + N(0, 0.1^2), beta ~
+    N(0, 0.1^2), concatenated over the layer inputs); returns the layer names."""
+    k = 3 + wl.features.shape[1]
+    names, fan_ins = [], []
+    for i, c in enumerate(widths):
+        W = gen.normal_matrix(seed, f"pointnet{i}", c, k, 1.0 / np.sqrt(k))
+        b = gen.normal_matrix(seed, f"pointnet{i}:bias", 1, c, 0.1)[0]
+        wl.mlp[f"pointnet{i}"] = (W, b)
+        names.append(f"pointnet{i}")
+        fan_ins.append(k)
+        k = c
+    tot = sum(fan_ins)
+    gam = 1.0 + gen.normal_matrix(seed, "gn-gamma:pointnet", 1, tot, 0.1)[0]
+    bet = gen.normal_matrix(seed, "gn-beta:pointnet", 1, tot, 0.1)[0]
+    wl.norms["pointnet"] = (gam.astype(np.float32), bet.astype(np.float32))
+    return names
 
 
 def _preact(wl, kind, level, src, dst, seed, res=None, groups=32):
@@ -251,15 +267,8 @@ def _latticenet(wl, seed, widths=(64, 128, 256), classes=20):
                   "cat1": (1, 2 * c1), "d2": (2, c2), "h2": (2, c2), "r2": (2, c2), "b2": (2, c2),
                   "hu1": (1, 2 * c1), "ru1": (1, 2 * c1), "u1": (1, 2 * c1), "hu0": (0, 2 * c0), "u0": (0, 2 * c0)}
     wl.ops = [dict(op="create", level=0), dict(op="coarsen", level=1), dict(op="coarsen", level=2)]
-    k = 3 + wl.features.shape[1]
-    names = []
-    for i, c in enumerate((16, 32, c0)):
-        W = gen.normal_matrix(seed, f"pointnet{i}", c, k, 1.0 / np.sqrt(k))
-        b = gen.normal_matrix(seed, f"pointnet{i}:bias", 1, c, 0.1)[0]
-        wl.mlp[f"pointnet{i}"] = (W, b)
-        names.append(f"pointnet{i}")
-        k = c
-    wl.ops.append(dict(op="distribute", level=0, dst=("p0", 0, c0), layers=names))
+    names = _pointnet(wl, seed, (16, 32, c0))
+    wl.ops.append(dict(op="distribute", level=0, dst=("p0", 0, c0), layers=names, norm="pointnet"))
     _resnet(wl, 0, ("p0", 0, c0), ("h0", 0, c0), ("cat0", c0, c0), seed)           # skip of level 0
     _preact(wl, "conv_down", 1, ("cat0", c0, c0), ("d1", 0, c1), seed)
     _resnet(wl, 1, ("d1", 0, c1), ("h1", 0, c1), ("r1", 0, c1), seed)
