@@ -151,6 +151,22 @@ int lattice_splat(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat
                   hipStream_t stream);
 
 /*
+ * lattice_splat without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, arithmetic and
+ * results as lattice_splat; its partial sums live in a fixed 16 MiB scratch
+ * array in device memory, one per GPU, held until the process ends and
+ * shared by every call on that GPU:
+ * calls that overlap on one GPU (concurrent streams or threads) race.
+ * Requires the lattice's vertex count to have been read
+ * (lattice_num_vertices; else LAT_EINVAL).  A splat whose partials need
+ * more than the scratch (about (2C + 2) floats per 256 list entries) returns
+ * LAT_EUNSUPPORTED with nothing enqueued.  Never calls hipMalloc or hipFree.
+ */
+int lattice_splat_noalloc(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat_dtype dt, int normalize,
+                          void* vals_dev, int64_t ld_vals, float* wsum_dev, hipStream_t stream);
+
+/*
  * Lattice convolution (Method, Convolving; Downsample):
  *   out[v] = bias + sum_{t<9} in[nb(v,t)] W[t]^T   (missing neighbours add 0)
  *   dst == src: 1-hop convolution, nb(v,t) = vertex at c_v + o_t.

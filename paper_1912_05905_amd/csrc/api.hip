@@ -1039,6 +1039,77 @@ int lattice_splat(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat
   return check_launch("splat");
 }
 
+// ---------------------------------------------------------------------------
+// Splat without allocation.  Its partials live in a file-scope device array
+// (each GPU holds its own copy for the life of the process).  In host code
+// the array's name is only a stand-in for its device address: the address is
+// looked up once per device with hipGetSymbolAddress and only that pointer
+// is ever passed on.  Every call on one GPU shares the array; the splat
+// writes each partial before its finishing pass reads it, so nothing needs
+// clearing between calls, but calls that overlap on one GPU race.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) float scratch[(size_t(16) << 20) / sizeof(float)];
+
+namespace {
+constexpr size_t kNoAllocScratchBytes = sizeof(scratch);
+constexpr int kMaxDevices = 64;
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch` (looked up on the first call on
+// that device).
+int noalloc_scratch(void** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(LAT_EUNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(LAT_EDEVICE, "hipGetSymbolAddress returned no address for the scratch array");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return LAT_OK;
+}
+}  // namespace
+
+int lattice_splat_noalloc(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat_dtype dt, int normalize,
+                          void* vals_dev, int64_t ld_vals, float* wsum_dev, hipStream_t stream) {
+  int st;
+  if (!L) return fail(LAT_EINVAL, "null lattice handle");
+  if (L->status != LAT_OK) return fail(L->status, "lattice handle is poisoned by an earlier error");
+  // waiting for the count may rebuild an overflowed table (an allocation):
+  // the caller reads it first, as it must to size vals
+  if (!L->counts_known)
+    return fail(LAT_EINVAL, "read the vertex count (lattice_num_vertices) before the allocation-free splat");
+  // ordered after a side-stream build without recording the join (no host
+  // allocation either)
+  if (L->side_seq && !L->joined_by(stream)) HIP_TRY(hipStreamWaitEvent(stream, L->built, 0));
+  if ((st = check_dtype(dt)) != LAT_OK) return st;
+  if (ld_feat == 0) ld_feat = C;
+  if (ld_vals == 0) ld_vals = C;
+  if ((st = check_matrix(feat_dev, ld_feat, C, dt, "feat", L->m > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(vals_dev, ld_vals, C, dt, "vals", L->n > 0)) != LAT_OK) return st;
+  if (C > splat_max_channels(dt == LAT_BF16))
+    return fail(LAT_EUNSUPPORTED, "splat supports at most " + std::to_string(splat_max_channels(dt == LAT_BF16)) +
+                                      " channels");
+  const size_t need = sizeof(float) * static_cast<size_t>(splat_partial_floats(L->total, L->chunk, C));
+  if (need > kNoAllocScratchBytes)
+    return fail(LAT_EUNSUPPORTED, "the allocation-free splat needs " + std::to_string(need) +
+                                      " bytes of partials, more than its " + std::to_string(kNoAllocScratchBytes) +
+                                      "-byte scratch; use lattice_splat");
+  // a coarse level's lists are built in its own buffers (no allocation)
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
+  if (L->n == 0) return LAT_OK;
+  void* part = nullptr;
+  if ((st = noalloc_scratch(&part)) != LAT_OK) return st;
+  launch_splat(L->offsets, L->entries, L->entry_w, L->chunk_first, L->chunk, L->nmax, L->total, feat_dev, ld_feat, C,
+               dt == LAT_BF16, normalize != 0, vals_dev, ld_vals, wsum_dev, static_cast<float*>(part), stream);
+  return check_launch("splat (no allocation)");
+}
+
 int lattice_conv(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in, int Cin,
                  const void* W_dev, const float* bias_dev, int Cout, lat_dtype dt, int flags,
                  void* out_dev, int64_t ld_out, hipStream_t stream) {

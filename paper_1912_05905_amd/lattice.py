@@ -41,6 +41,7 @@ SIGNATURES = {
     "lattice_export_simplices": (_I32, [_P, _P, _P, _P]),
     "lattice_export_neighbors": (_I32, [_P, _P, _P]),
     "lattice_splat": (_I32, [_P, _P, _I64, _I32, _I32, _I32, _P, _I64, _P, _P]),
+    "lattice_splat_noalloc": (_I32, [_P, _P, _I64, _I32, _I32, _I32, _P, _I64, _P, _P]),
     "lattice_conv": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _I32, _I32, _P, _I64, _P]),
     "lattice_refine": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _I32, _I32, _P, _I64, _P]),
     "lattice_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
@@ -222,6 +223,21 @@ class Lattice:
         _check(lib().lattice_splat(self._h, fp, fld, Cc, _dtype_code(feat), int(bool(normalize)),
                                    op, old, None if wsum is None else C.c_void_p(wsum.data_ptr()),
                                    _stream(stream)))
+        return out
+
+    def splat_noalloc(self, feat: torch.Tensor, normalize: bool = True, out: torch.Tensor | None = None,
+                      wsum: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """splat through lattice_splat_noalloc (its partials in the library's
+        fixed device scratch; out must be given by callers that cannot
+        allocate)."""
+        Cc = feat.shape[1]
+        if out is None:
+            out = torch.empty((self.n, Cc), dtype=feat.dtype, device="cuda")
+        fp, fld = _rows(feat)
+        op, old = _rows(out)
+        _check(lib().lattice_splat_noalloc(self._h, fp, fld, Cc, _dtype_code(feat), int(bool(normalize)),
+                                           op, old, None if wsum is None else C.c_void_p(wsum.data_ptr()),
+                                           _stream(stream)))
         return out
 
     def conv(self, src: "Lattice", x: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = None,
