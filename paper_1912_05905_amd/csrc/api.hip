@@ -279,6 +279,8 @@ struct lattice_s {
   int32_t* down = nullptr;       // 9 x nmax table into the parent (coarse levels, ld nmax)
   int32_t* up = nullptr;         // 9 x parent->nmax table from the parent into this level
   int32_t* up_rows = nullptr;    // parent vertices, grouped by the tap mask of their up row
+  int32_t* nbr_rows = nullptr;   // this level's vertices grouped by the tap mask of their same-level row
+  int32_t* down_rows = nullptr;  // this level's vertices grouped by the tap mask of their down row
   int64_t retry_cap = 0;          // coarse levels: table size of a rebuild after overflow
   uint32_t stamp = 0;             // stamp of the current build's count readback
   uint64_t generation = 0;        // rebuilds of this handle after an overflow
@@ -435,6 +437,8 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   const size_t o_down = parent ? carve(sizeof(int32_t) * kTaps * nmax) : 0;
   const size_t o_up = parent ? carve(sizeof(int32_t) * kTaps * parent->nmax) : 0;
   const size_t o_up_rows = parent ? carve(sizeof(int32_t) * parent->nmax) : 0;
+  const size_t o_nbr_rows = carve(sizeof(int32_t) * nmax);
+  const size_t o_down_rows = parent ? carve(sizeof(int32_t) * nmax) : 0;
   // The finest level builds its lists now (splat needs them); a coarse level
   // when an operator first needs them.  Either way the inputs of the list
   // build are the handle's own buffers: a build releases nothing to the
@@ -459,10 +463,12 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   L->entry_w = static_cast<float*>(at(o_entry_w));
   L->chunk_first = static_cast<int32_t*>(at(o_chunk_first));
   L->nbr = static_cast<int32_t*>(at(o_nbr));
+  L->nbr_rows = static_cast<int32_t*>(at(o_nbr_rows));
   if (parent) {
     L->down = static_cast<int32_t*>(at(o_down));
     L->up = static_cast<int32_t*>(at(o_up));
     L->up_rows = static_cast<int32_t*>(at(o_up_rows));
+    L->down_rows = static_cast<int32_t*>(at(o_down_rows));
   }
   L->slot_count = static_cast<int32_t*>(at(o_slot_count));
   L->vslot = static_cast<int32_t*>(at(o_vslot));
@@ -498,9 +504,9 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   }
   if (parent)
     launch_coarse_tables(L->hash(), parent->hash(), L->vkeys, parent->vkeys, n_dev, &parent->dc->counter, nmax,
-                         parent->nmax, L->nbr, L->down, L->up, L->up_rows, built, s);
+                         parent->nmax, L->nbr, L->down, L->up, L->up_rows, L->nbr_rows, L->down_rows, built, s);
   else
-    launch_neighbor_table(L->hash(), L->vkeys, n_dev, nmax, L->nbr, nmax, s);
+    launch_neighbor_table(L->hash(), L->vkeys, n_dev, nmax, L->nbr, nmax, L->nbr_rows, s);
   return check_launch("lattice build");
 }
 
@@ -797,7 +803,6 @@ int conv_common(const int32_t* table, int64_t ldn, int64_t n_out, int64_t n_in, 
     if (gn->res) {
       const int64_t ld_res = gn->ld_res ? gn->ld_res : Cout;
       if ((st = check_matrix(gn->res, ld_res, Cout, dt, "res", true)) != LAT_OK) return st;
-      if (rows) return fail(LAT_EUNSUPPORTED, "a residual is not supported for Upsample");
       if (n_out > 0 && overlaps(gn->res, static_cast<size_t>((n_out - 1) * ld_res + Cout) * u, out,
                                 static_cast<size_t>((n_out - 1) * ld_out + Cout) * u) &&
           !(gn->res == out && ld_res == ld_out))
@@ -1116,12 +1121,12 @@ int lattice_conv(lattice_t dst, lattice_t src, const void* in_dev, int64_t ld_in
   int st;
   if ((st = use(dst, stream)) != LAT_OK) return st;
   if ((st = use(src, stream)) != LAT_OK) return st;
-  const int32_t* table;
-  if (dst == src) table = dst->nbr;
-  else if (dst->parent == src) table = dst->down;
+  const int32_t *table, *rows;
+  if (dst == src) table = dst->nbr, rows = dst->nbr_rows;
+  else if (dst->parent == src) table = dst->down, rows = dst->down_rows;
   else return fail(LAT_ELEVEL, "dst must be src or lattice_coarsen(src)");
   return conv_common(table, dst->nmax, dst->n, src->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt, flags,
-                     out_dev, ld_out, nullptr, stream);
+                     out_dev, ld_out, rows, stream);
 }
 
 int lattice_refine(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t ld_in, int Cin,
@@ -1142,13 +1147,13 @@ int lattice_conv_preact(lattice_t dst, lattice_t src, const void* in_dev, int64_
   int st;
   if ((st = use(dst, stream)) != LAT_OK) return st;
   if ((st = use(src, stream)) != LAT_OK) return st;
-  const int32_t* table;
-  if (dst == src) table = dst->nbr;
-  else if (dst->parent == src) table = dst->down;
+  const int32_t *table, *rows;
+  if (dst == src) table = dst->nbr, rows = dst->nbr_rows;
+  else if (dst->parent == src) table = dst->down, rows = dst->down_rows;
   else return fail(LAT_ELEVEL, "dst must be src or lattice_coarsen(src)");
   const GnArgs gn{groups, gamma_dev, beta_dev, eps, res_dev, ld_res};
   return conv_common(table, dst->nmax, dst->n, src->n, in_dev, ld_in, Cin, W_dev, bias_dev, Cout, dt, flags,
-                     out_dev, ld_out, nullptr, stream, &gn);
+                     out_dev, ld_out, rows, stream, &gn);
 }
 
 int lattice_refine_preact(lattice_t fine, lattice_t coarse, const void* in_dev, int64_t ld_in, int Cin, int groups,
@@ -1337,6 +1342,7 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
   if (dst == src) {
     fwd = adj = dst->nbr;
     fwd_ld = adj_ld = dst->nmax;
+    adj_rows = dst->nbr_rows;
   } else if (dst->parent == src) {            // strided: adjoint is the Upsample into src
     fwd = dst->down;
     fwd_ld = dst->nmax;
@@ -1348,6 +1354,7 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
     fwd_ld = dst->nmax;
     adj = src->down;
     adj_ld = src->nmax;
+    adj_rows = src->down_rows;
   } else {
     return fail(LAT_ELEVEL, "dst and src must be one lattice, or one a coarsening of the other");
   }

@@ -530,9 +530,24 @@ constexpr int kOrderRange = 4096;
 
 constexpr int kOrderThreads = 1024;
 
+// Up to three tables ordered in one launch: blockIdx.y picks the table.
+struct MaskOrderJob {
+  const int32_t* nbr;     // tap-major table, row stride ldn
+  int64_t ldn;
+  const int32_t* n_dev;   // its row count (device)
+  int32_t* rows;          // out: its rows grouped by tap mask within ranges
+};
+struct MaskOrderJobs {
+  MaskOrderJob job[3];
+};
+
 __global__ void __launch_bounds__(kOrderThreads)
-k_mask_order(const int32_t* __restrict__ nbr, int64_t ldn, const int32_t* __restrict__ n_dev,
-             int32_t* __restrict__ rows) {
+k_mask_order(MaskOrderJobs jobs) {
+  const MaskOrderJob& J = jobs.job[blockIdx.y];
+  const int32_t* __restrict__ nbr = J.nbr;
+  const int64_t ldn = J.ldn;
+  const int32_t* __restrict__ n_dev = J.n_dev;
+  int32_t* __restrict__ rows = J.rows;
   __shared__ int32_t hist[kMaskBins];
   __shared__ int32_t wave_sum[kMaskBins / 64];
   __shared__ uint16_t mk[kOrderRange];
@@ -662,16 +677,21 @@ inline unsigned stride_grid(int64_t work) {
 }
 
 void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_dev, int64_t n_max,
-                           int32_t* nbr, int64_t ldn, hipStream_t s) {
+                           int32_t* nbr, int64_t ldn, int32_t* nbr_rows, hipStream_t s) {
   if (n_max <= 0) return;
   ScopedKernelTimer tm("nbr", s);
   launch(k_neighbor_table, dim3(stride_grid(n_max * kTaps)), dim3(kBlock), 0, s, h, vkeys, n_dev,
                      nbr, ldn);
+  MaskOrderJobs jobs{};
+  jobs.job[0] = MaskOrderJob{nbr, ldn, n_dev, nbr_rows};
+  launch(k_mask_order, dim3(static_cast<unsigned>((n_max + kOrderRange - 1) / kOrderRange), 1), dim3(kOrderThreads),
+         0, s, jobs);
 }
 
 void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse_keys, const uint64_t* fine_keys,
                           const int32_t* nc_dev, const int32_t* nf_dev, int64_t nc_max, int64_t nf_max, int32_t* nbr,
-                          int32_t* down, int32_t* up, int32_t* up_rows, hipEvent_t done, hipStream_t s) {
+                          int32_t* down, int32_t* up, int32_t* up_rows, int32_t* nbr_rows, int32_t* down_rows,
+                          hipEvent_t done, hipStream_t s) {
   if (nc_max <= 0 || nf_max <= 0) {
     if (done) (void)hipEventRecord(done, s);
     return;
@@ -679,11 +699,16 @@ void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse
   ScopedKernelTimer tm("nbr", s);
   launch(k_coarse_tables, dim3(stride_grid((2 * nc_max + nf_max) * kTaps)), dim3(kBlock), 0, s, coarse,
                      fine, coarse_keys, fine_keys, nc_dev, nf_dev, nbr, down, nc_max, up, nf_max);
-  const dim3 grid(static_cast<unsigned>((nf_max + kOrderRange - 1) / kOrderRange));
+  // the rows of all three tables grouped by tap mask, in one launch
+  MaskOrderJobs jobs{};
+  jobs.job[0] = MaskOrderJob{up, nf_max, nf_dev, up_rows};
+  jobs.job[1] = MaskOrderJob{nbr, nc_max, nc_dev, nbr_rows};
+  jobs.job[2] = MaskOrderJob{down, nc_max, nc_dev, down_rows};
+  const dim3 grid(static_cast<unsigned>((std::max(nf_max, nc_max) + kOrderRange - 1) / kOrderRange), 3);
   if (done)
-    launch_signal(k_mask_order, grid, dim3(kOrderThreads), 0, s, done, up, nf_max, nf_dev, up_rows);
+    launch_signal(k_mask_order, grid, dim3(kOrderThreads), 0, s, done, jobs);
   else
-    launch(k_mask_order, grid, dim3(kOrderThreads), 0, s, up, nf_max, nf_dev, up_rows);
+    launch(k_mask_order, grid, dim3(kOrderThreads), 0, s, jobs);
 }
 
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s) {

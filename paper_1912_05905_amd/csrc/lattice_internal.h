@@ -154,11 +154,13 @@ void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, const in
 void launch_fill_lists(HashView h, const int32_t* slot, const int32_t* rank, const float* w,
                        const int32_t* offsets, int32_t* idx, int32_t* entries, float* entry_w,
                        int32_t* chunk_first, int chunk, int64_t m4, hipStream_t s);
+// the table, then its rows grouped by tap mask within ranges of 4096 (nbr_rows)
 void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_dev, int64_t n_max,
-                           int32_t* nbr, int64_t ldn, hipStream_t s);
+                           int32_t* nbr, int64_t ldn, int32_t* nbr_rows, hipStream_t s);
 void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse_keys, const uint64_t* fine_keys,
                           const int32_t* nc_dev, const int32_t* nf_dev, int64_t nc_max, int64_t nf_max, int32_t* nbr,
-                          int32_t* down, int32_t* up, int32_t* up_rows, hipEvent_t done, hipStream_t s);
+                          int32_t* down, int32_t* up, int32_t* up_rows, int32_t* nbr_rows, int32_t* down_rows,
+                          hipEvent_t done, hipStream_t s);
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s);
 void launch_transpose_table(const int32_t* tab, int64_t ld, int64_t n, int32_t* out, hipStream_t s);
 // splat_slice.hip
