@@ -179,7 +179,25 @@ def distribute_flops(wl):
     return total
 
 
-def algorithmic_bytes(wl, levels, family):
+def point_ops(wl, pipe):
+    """The point-output operators of a step as they are launched: a slice
+    followed by a DeformSlice of the same values runs as one fused pass."""
+    fused = getattr(pipe, "_fused", set())
+    out, skip = [], False
+    for i, op in enumerate(wl.ops):
+        if skip:
+            skip = False
+            continue
+        if op["op"] in ("slice", "deform_slice"):
+            if i in fused:
+                out.append(("slice+deform", op))
+                skip = True
+            else:
+                out.append((op["op"], op))
+    return out
+
+
+def algorithmic_bytes(wl, levels, family, pipe=None):
     """Bytes a kernel family must move per step (each input read once, each
     output written once), for the HBM-bound families."""
     u = 2 if wl.dtype == "bf16" else 4
@@ -192,13 +210,19 @@ def algorithmic_bytes(wl, levels, family):
         # features m*C*u, lists 4m*(4 entry + 4 weight), offsets, output n*C*u
         return m * C * u + 4 * m * 8 + (n + 1) * 4 + n * C * u
     if family in ("slice", "deform_slice"):
+        # per point 32 B of vertex indices and weights and C*4 out per output,
+        # the vertex rows n*C*u once; DeformSlice also reads wv.  The fused
+        # slice + DeformSlice pass (timed as deform_slice) writes both rows.
         tot = 0
-        for op in wl.ops:
-            if op["op"] == ("slice" if family == "slice" else "deform_slice"):
-                C = op["src"][2]
-                n = levels[op["level"]].n
-                tot += m * 32 + n * C * u + m * C * 4 + (C * 4 if family == "deform_slice" else 0)
-        return tot
+        for kind, op in point_ops(wl, pipe):
+            fam = "slice" if kind == "slice" else "deform_slice"
+            if fam != family:
+                continue
+            C = op["src"][2]
+            n = levels[op["level"]].n
+            outs = 2 if kind == "slice+deform" else 1
+            tot += m * 32 + n * C * u + outs * m * C * 4 + (C * 4 if kind != "slice" else 0)
+        return tot or None
     if family == "insert":
         per_level = m * 12 + m * (16 + 16 + 16)       # positions in, y / slots / weights out
         nlev = len(levels)
@@ -206,13 +230,104 @@ def algorithmic_bytes(wl, levels, family):
     return None
 
 
+def conv_occupied_flops(wl, levels):
+    """Flops of all convolutions of one step counted on the taps that exist:
+    2 Cin Cout per (output vertex, tap) pair whose neighbour is allocated
+    (a missing neighbour contributes nothing).  Waits for the device."""
+    total = 0
+    for op in wl.ops:
+        lv = op.get("level")
+        if op["op"] == "conv":
+            pairs = levels[lv].conv_taps(levels[lv])
+        elif op["op"] == "conv_down":
+            pairs = levels[lv].conv_taps(levels[lv - 1])
+        elif op["op"] == "refine":
+            pairs = levels[lv].conv_taps(levels[lv + 1])
+        else:
+            continue
+        total += 2 * pairs * op["src"][2] * op["dst"][2]
+    return total
+
+
+def host_cpu():
+    """CPU model of this host and its logical CPU count."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
+def _oracle_worker(args):
+    """One process of the all-core CPU baseline: whole oracle steps of the
+    workload for about `seconds`; returns (steps, seconds)."""
+    cfg, seconds = args
+    sys.path.insert(0, ROOT)
+    from tests.oracle_pipeline import OraclePipeline
+    from workloads import configs
+    wl = configs.make(cfg)
+    OraclePipeline(wl).run()           # first step untimed (library load, page-in)
+    c0 = time.perf_counter()
+    n = 0
+    while True:
+        OraclePipeline(wl).run()
+        n += 1
+        if time.perf_counter() - c0 >= seconds:
+            break
+    return n, time.perf_counter() - c0
+
+
+def cpu_baseline(wl, seconds=10.0, workers=None):
+    """The CPU oracle on this host: one thread (whole steps for about
+    `seconds`, with per-operation times), then all cores (one process per
+    core, each running whole steps for about `seconds`)."""
+    from concurrent.futures import ProcessPoolExecutor
+    import multiprocessing as mp
+    from tests.oracle_pipeline import OraclePipeline
+    model, ncpu = host_cpu()
+    times = {}
+    c0 = time.perf_counter()
+    nsteps = 0
+    while True:
+        OraclePipeline(wl).run(times=times)
+        nsteps += 1
+        if time.perf_counter() - c0 >= seconds or nsteps >= 50:
+            break
+    t1 = time.perf_counter() - c0
+    one = nsteps * wl.m / t1
+    # GPU boxes give a process a share of 16 cores whatever nproc says
+    workers = workers or max(1, min(ncpu or 1, 16))
+    with ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("spawn")) as ex:
+        res = list(ex.map(_oracle_worker, [(wl.cfg, seconds)] * workers))
+    allc = sum(n * wl.m / t for n, t in res)
+    return {"value": allc, "unit": "points/s", "cores": workers, "kind": "oracle",
+            "sample": f"whole steps of the same {wl.m}-point workload on the CPU oracle (std::map lattice, scalar "
+                      f"float64): {workers} processes, one per core, each for about {seconds:.0f} s "
+                      f"({sum(n for n, _ in res)} steps in all); single thread {nsteps} steps in {t1:.1f} s",
+            "cpu_model": model, "nproc": ncpu, "value_1thread": one,
+            "ms_per_step_1thread": t1 * 1e3 / nsteps,
+            "op_ms_1thread": {k: v * 1e3 / nsteps for k, v in times.items()}}
+
+
+def _hbm_entry(nbytes, ms):
+    if not nbytes or not ms:
+        return None
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"algorithmic_bytes": nbytes, "ms_per_step": ms, "achieved_GBps": gbs, "frac": gbs * 1e9 / PEAK["hbm"]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work per CPU-baseline leg")
     ap.add_argument("--report", default=None, help="write a per-family timing report (JSON) here")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run device-to-device copies of MIB MiB (PMC scale calibration)")
@@ -241,7 +356,8 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
+    import statistics
+
     import torch
 
     from paper_1912_05905_amd import lattice
@@ -266,7 +382,8 @@ def main():
         pipe.finish_step(levels)
     torch.cuda.synchronize()
 
-    # one instrumented step: per-family device time, to find the dominant family
+    # one instrumented step: per-family device time, to find the dominant
+    # family; the tap occupancy of its convolutions
     for f in FAMILIES:
         lattice.timing_enable(f, True)
     levels, _, _ = one_step()
@@ -276,26 +393,43 @@ def main():
         lattice.timing_enable(f, False)
     ns = {lv: levels[lv].n for lv in levels}
     flops = conv_flops(wl, levels)
+    occ_flops = conv_occupied_flops(wl, levels) if flops else 0
     bwd_flops = conv_bwd_flops(wl, levels)
-    bytes_by_fam = {f: algorithmic_bytes(wl, levels, f) for f in FAMILIES}
+    bytes_by_fam = {f: algorithmic_bytes(wl, levels, f, pipe) for f in FAMILIES}
     pipe.finish_step(levels)
+    torch.cuda.synchronize()
     dominant = max(fam_ms, key=lambda f: fam_ms[f][1])
 
-    # timed region: K steps, nothing instrumented
+    # timed region: K steps, nothing instrumented; an event on the stream
+    # every `win` steps gives per-window device throughput (median reported)
+    win = max(1, args.steps // 20)
+    marks = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
+        if i % win == 0:
+            ev = torch.cuda.Event(enable_timing=True)
+            ev.record(stream)
+            marks.append((i, ev))
         levels, _, _ = one_step()
         pipe.finish_step(levels)
+    end = torch.cuda.Event(enable_timing=True)
+    end.record(stream)
+    marks.append((args.steps, end))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    windows = [marks[j][1].elapsed_time(marks[j + 1][1]) / (marks[j + 1][0] - marks[j][0])
+               for j in range(len(marks) - 1)]
 
-    # the same K steps again with the dominant family's kernels timed: each
-    # launch's start / stop HIP events are bound to its dispatch on the
-    # stream it runs on, so the sum is that family's kernel time; these
-    # completion events delay the next kernel, so this region's wall time is
-    # reported beside the first, not as the throughput
-    lattice.timing_enable(dominant, True)
+    # the same K steps again with the kernels of the dominant family and of
+    # the HBM-bound operators timed: each launch's start / stop HIP events
+    # are bound to its dispatch on the stream it runs on, so a family's sum
+    # is its kernel time; these completion events delay the next kernel, so
+    # this region's wall time is reported beside the first, not as the
+    # throughput
+    timed = [dominant] + [f for f in ("splat", "slice", "deform_slice") if f != dominant and bytes_by_fam.get(f)]
+    for f in timed:
+        lattice.timing_enable(f, True)
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     for _ in range(args.steps):
@@ -303,9 +437,11 @@ def main():
         pipe.finish_step(levels)
     torch.cuda.synchronize()
     t3 = time.perf_counter()
-    launches, dom_ms = lattice.timing_read(dominant)
-    lattice.timing_enable(dominant, False)
+    fam_timed = {f: lattice.timing_read(f) for f in timed}
+    for f in timed:
+        lattice.timing_enable(f, False)
     pipe.flush()
+    launches, dom_ms = fam_timed[dominant]
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = wl.m / (ms_per_step * 1e-3)
@@ -317,38 +453,44 @@ def main():
         achieved = mfma_flops[dominant] / (dom_ms_step * 1e-3)
         roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
                 "frac": achieved / peak, "traffic": None}
-        t = measured_traffic(f"config{wl.cfg}", dominant)
-        if t is not None:
-            roof["traffic"] = t / max(launches / args.steps, 1)
+        if dominant == "conv" and occ_flops:
+            # the same launches counted on the taps that exist
+            occ = occ_flops / (dom_ms_step * 1e-3)
+            roof["flops_definition"] = ("nominal: 2*9*Cin*Cout per output vertex (per coarse vertex for "
+                                        "Upsample); occupied: 2*Cin*Cout per (vertex, tap) pair whose "
+                                        "neighbour exists")
+            roof["gflop_per_step_nominal"] = flops / 1e9
+            roof["gflop_per_step_occupied"] = occ_flops / 1e9
+            roof["occupied_tap_fraction"] = occ_flops / flops
+            roof["achieved_occupied"] = occ / 1e12
+            roof["frac_occupied"] = occ / peak
     else:
         b = bytes_by_fam.get(dominant)
         achieved = (b / (dom_ms_step * 1e-3)) if b else None
         roof = {"bound": "hbm", "achieved": None if achieved is None else achieved / 1e9,
                 "peak": PEAK["hbm"] / 1e9, "unit": "GB/s",
                 "frac": None if achieved is None else achieved / PEAK["hbm"], "traffic": None}
-        t = measured_traffic(f"config{wl.cfg}", dominant)
-        if t is not None:
-            roof["traffic"] = t / max(launches / args.steps, 1)
+    t = measured_traffic(f"config{wl.cfg}", dominant)
+    if t is not None:
+        roof["traffic"] = t / max(launches / args.steps, 1)
     roof["kernel"] = dominant
     roof["launches_per_step"] = launches / args.steps
     roof["ms_per_step"] = dom_ms_step
+    roof["ms_per_launch"] = dom_ms / max(launches, 1)
     roof["timed_region_ms_per_step"] = (t3 - t2) * 1e3 / args.steps
+    # the HBM-bound operators, each over its own launches in the same region
+    hbm = {}
+    for f in timed:
+        if f == dominant:
+            continue
+        e = _hbm_entry(bytes_by_fam.get(f), fam_timed[f][1] / args.steps)
+        if e:
+            tr = measured_traffic(f"config{wl.cfg}", f)
+            e["traffic_bytes_per_step"] = tr
+            hbm[f] = e
+    roof["hbm_families"] = hbm
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        from tests.oracle_pipeline import OraclePipeline
-        # whole steps of the same workload until about 10 s of CPU work
-        c0 = time.perf_counter()
-        nsteps = 0
-        while True:
-            OraclePipeline(wl).run()
-            nsteps += 1
-            if time.perf_counter() - c0 >= 10.0 or nsteps >= 50:
-                break
-        c1 = time.perf_counter()
-        cpu = {"value": nsteps * wl.m / (c1 - c0), "unit": "points/s", "cores": 1, "kind": "oracle",
-               "sample": f"{nsteps} full steps of the same {wl.m}-point workload on the CPU oracle "
-                         f"(std::map lattice, scalar float64, one thread), {c1 - c0:.1f} s"}
+    cpu = None if args.no_cpu_baseline else cpu_baseline(wl, args.cpu_seconds)
 
     line = {
         "metric": "points/s for splat+conv+slice at 120k pts; lattice-conv GFLOP/s (% MFMA peak)",
@@ -358,10 +500,14 @@ def main():
         "config": {"workload": f"config{wl.cfg}:{wl.name}", "points": wl.m,
                    "sigma": float(wl.sigma[0]), "vertices_per_level": [ns[k] for k in sorted(ns)],
                    "conv_gflop_per_step": flops / 1e9,
+                   "conv_gflop_per_step_occupied_taps": occ_flops / 1e9,
                    "distribute_gflop_per_step": mfma_flops["distribute"] / 1e9,
                    "conv_bwd_gflop_per_step": bwd_flops / 1e9,
                    "steps_overlap": "the next cloud's lattice build runs on its own stream during this "
                                     "cloud's operators; every step does all of its work"},
+        "timing": {"timed_ms": (t1 - t0) * 1e3, "windows": len(windows), "steps_per_window": win,
+                   "ms_per_step_median_window": statistics.median(windows),
+                   "ms_per_step_min_window": min(windows), "ms_per_step_max_window": max(windows)},
         "roofline": roof,
         "cpu_baseline": cpu,
     }
@@ -370,6 +516,7 @@ def main():
         rep = {"families_ms_one_step": {f: fam_ms[f][1] for f in FAMILIES},
                "launches_one_step": {f: fam_ms[f][0] for f in FAMILIES},
                "bytes_per_step": bytes_by_fam, "conv_flops_per_step": flops,
+               "conv_flops_per_step_occupied": occ_flops,
                "ms_per_step": ms_per_step, "vertices": ns}
         with open(args.report, "w") as fh:
             json.dump(rep, fh, indent=1)

@@ -139,6 +139,16 @@ int lattice_export_simplices(lattice_t L, int32_t* idx_dev, float* w_dev, hipStr
 int lattice_export_neighbors(lattice_t L, int32_t* nbr_dev, hipStream_t stream);
 
 /*
+ * Occupied taps of a convolution (Fig. (convolve): a missing neighbour
+ * contributes nothing): the number of (output vertex, tap) pairs whose
+ * neighbour exists, for the 1-hop (dst == src), strided (dst =
+ * lattice_coarsen(src)) or Upsample (src = lattice_coarsen(dst)) form.
+ * The work the convolution must do is 2 Cin Cout per pair.  Written to
+ * *pairs_host; waits for the stream (for measurement, not for hot loops).
+ */
+int lattice_conv_taps(lattice_t dst, lattice_t src, int64_t* pairs_host, hipStream_t stream);
+
+/*
  * Splat, Eq. (splat): x_v = sum_{p in J_v} b_pv f_p.
  *   feat_dev   m x C features (dtype dt), row stride ld_feat.
  *   normalize  nonzero: divide by sum_{p in J_v} b_pv (the weighted average

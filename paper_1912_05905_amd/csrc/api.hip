@@ -1023,6 +1023,31 @@ int lattice_export_neighbors(lattice_t L, int32_t* nbr_dev, hipStream_t stream) 
   return check_launch("export neighbours");
 }
 
+int lattice_conv_taps(lattice_t dst, lattice_t src, int64_t* pairs_host, hipStream_t stream) {
+  int st;
+  if (!pairs_host) return fail(LAT_EINVAL, "pairs is null");
+  *pairs_host = 0;
+  if ((st = use(dst, stream)) != LAT_OK) return st;
+  if ((st = use(src, stream)) != LAT_OK) return st;
+  const int32_t* table;
+  int64_t ld;
+  if (dst == src) table = dst->nbr, ld = dst->nmax;
+  else if (dst->parent == src) table = dst->down, ld = dst->nmax;
+  else if (src->parent == dst) table = src->up, ld = dst->nmax;
+  else return fail(LAT_ELEVEL, "dst and src must be one lattice, or one a coarsening of the other");
+  if (dst->n == 0) return LAT_OK;
+  Scratch cnt;
+  if ((st = cnt.get(sizeof(unsigned long long), stream)) != LAT_OK) return st;
+  HIP_TRY(hipMemsetAsync(cnt.p, 0, sizeof(unsigned long long), stream));
+  launch_count_taps(table, ld, dst->n, cnt.as<unsigned long long>(), stream);
+  if ((st = check_launch("count taps")) != LAT_OK) return st;
+  unsigned long long h = 0;
+  HIP_TRY(hipMemcpyAsync(&h, cnt.p, sizeof(h), hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipStreamSynchronize(stream));
+  *pairs_host = static_cast<int64_t>(h);
+  return LAT_OK;
+}
+
 int lattice_splat(lattice_t L, const void* feat_dev, int64_t ld_feat, int C, lat_dtype dt,
                   int normalize, void* vals_dev, int64_t ld_vals, float* wsum_dev, hipStream_t stream) {
   int st;

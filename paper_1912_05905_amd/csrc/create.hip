@@ -622,6 +622,28 @@ k_transpose_table(const int32_t* __restrict__ tab, int64_t ld, int64_t n, int32_
   out[i] = tab[static_cast<int64_t>(t) * ld + v];
 }
 
+// Number of entries >= 0 among the first n rows of a tap-major table: the
+// (row, tap) pairs whose neighbour exists.  Integer sums, so the count does
+// not depend on the order of the atomics.
+__global__ void __launch_bounds__(kBlock)
+k_count_taps(const int32_t* __restrict__ tab, int64_t ld, int64_t n, unsigned long long* __restrict__ count) {
+  __shared__ unsigned long long part[kBlock / 64];
+  unsigned long long c = 0;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n * kTaps;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int64_t t = i / n, v = i - t * n;
+    c += tab[t * ld + v] >= 0 ? 1u : 0u;
+  }
+  for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long s = 0;
+    for (int w = 0; w < kBlock / 64; ++w) s += part[w];
+    atomicAdd(count, s);
+  }
+}
+
 inline unsigned blocks_for(int64_t n) { return static_cast<unsigned>((n + kBlock - 1) / kBlock); }
 
 }  // namespace
@@ -715,6 +737,12 @@ void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStrea
   if (n <= 0) return;
   launch(k_export_keys, dim3(blocks_for(n)), dim3(kBlock), 0, s, vkeys, n,
                      reinterpret_cast<int4*>(out));
+}
+
+void launch_count_taps(const int32_t* tab, int64_t ld, int64_t n, unsigned long long* count, hipStream_t s) {
+  if (n <= 0) return;
+  launch(k_count_taps, dim3(static_cast<unsigned>(std::min<int64_t>((n * kTaps + kBlock - 1) / kBlock, 1024))),
+         dim3(kBlock), 0, s, tab, ld, n, count);
 }
 
 void launch_transpose_table(const int32_t* tab, int64_t ld, int64_t n, int32_t* out, hipStream_t s) {

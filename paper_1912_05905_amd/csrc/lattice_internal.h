@@ -162,6 +162,8 @@ void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse
                           int32_t* down, int32_t* up, int32_t* up_rows, int32_t* nbr_rows, int32_t* down_rows,
                           hipEvent_t done, hipStream_t s);
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s);
+// adds to *count the (row, tap) pairs of the first n rows whose entry is >= 0
+void launch_count_taps(const int32_t* tab, int64_t ld, int64_t n, unsigned long long* count, hipStream_t s);
 void launch_transpose_table(const int32_t* tab, int64_t ld, int64_t n, int32_t* out, hipStream_t s);
 // splat_slice.hip
 int64_t splat_partial_floats(int64_t total, int chunk, int C);

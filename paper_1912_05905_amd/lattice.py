@@ -42,6 +42,7 @@ SIGNATURES = {
     "lattice_export_neighbors": (_I32, [_P, _P, _P]),
     "lattice_splat": (_I32, [_P, _P, _I64, _I32, _I32, _I32, _P, _I64, _P, _P]),
     "lattice_splat_noalloc": (_I32, [_P, _P, _I64, _I32, _I32, _I32, _P, _I64, _P, _P]),
+    "lattice_conv_taps": (_I32, [_P, _P, C.POINTER(_I64), _P]),
     "lattice_conv": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _I32, _I32, _P, _I64, _P]),
     "lattice_refine": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, _I32, _I32, _I32, _P, _I64, _P]),
     "lattice_slice": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
@@ -239,6 +240,13 @@ class Lattice:
                                            op, old, None if wsum is None else C.c_void_p(wsum.data_ptr()),
                                            _stream(stream)))
         return out
+
+    def conv_taps(self, src: "Lattice") -> int:
+        """(vertex, tap) pairs with an existing neighbour of the convolution
+        from src into self (1-hop, strided or Upsample); waits."""
+        n = _I64()
+        _check(lib().lattice_conv_taps(self._h, src._h, C.byref(n), _stream(None)))
+        return int(n.value)
 
     def conv(self, src: "Lattice", x: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = None,
              relu: bool = False, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

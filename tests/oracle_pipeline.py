@@ -6,6 +6,8 @@ bfloat16 where the GPU stores bf16 (splat, convolution outputs).
 """
 from __future__ import annotations
 
+import time
+
 import numpy as np
 
 from oracle import oracle as O
@@ -19,7 +21,9 @@ class OraclePipeline:
     def _store(self, x):
         return O.round_bf16(x) if self.bf16 else x
 
-    def run(self, stop_after=None):
+    def run(self, stop_after=None, times=None):
+        """The whole operation list; `times`, if given, accumulates the
+        seconds spent per operation kind."""
         wl = self.wl
         levels, bufs, outs = {}, {}, {}
 
@@ -36,6 +40,7 @@ class OraclePipeline:
 
         for i, op in enumerate(wl.ops):
             kind = op["op"]
+            t_op = time.perf_counter()
             if kind == "create":
                 levels[0] = O.Lattice.create(wl.positions, wl.sigma)
             elif kind == "coarsen":
@@ -98,6 +103,8 @@ class OraclePipeline:
             elif kind == "splat_bwd":
                 outs[op["out"]] = levels[0].splat_backward(np.ascontiguousarray(view_src(op["src"])),
                                                            normalize=bool(op["normalize"]))
+            if times is not None:
+                times[kind] = times.get(kind, 0.0) + time.perf_counter() - t_op
             if stop_after is not None and i == stop_after:
                 break
         return levels, bufs, outs

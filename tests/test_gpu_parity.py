@@ -1031,3 +1031,19 @@ def test_deform_slice_classify(L, O, C, K, dtype):
     oy = ol.deform_slice_classify(X, wv.astype(np.float64), 0.1, Wc.astype(np.float64),
                                   None if bc is None else bc.astype(np.float64))
     P.assert_close(_host(gy), oy, P.TOL_F32, f"DeformSlice+classifier C={C} K={K} {dtype}")
+
+
+def test_conv_taps_count_existing_neighbours(L, O):
+    """lattice_conv_taps: the (vertex, tap) pairs with an existing neighbour
+    of the 1-hop, strided and Upsample tables, against the oracle's tables."""
+    pos = _cloud(61, 20_000, 1.0)
+    g0 = L.Lattice.create(_dev(pos), [0.05] * 3)
+    g1 = g0.coarsen()
+    o0 = O.Lattice.create(pos, np.full(3, 0.05, np.float32))
+    o1 = o0.coarsen()
+    assert g0.conv_taps(g0) == int((o0.neighbors() >= 0).sum())
+    assert g1.conv_taps(g1) == int((o1.neighbors() >= 0).sum())
+    assert g1.conv_taps(g0) == int((o1.down_table() >= 0).sum())
+    assert g0.conv_taps(g1) == int((o1.up_table() >= 0).sum())
+    g1.destroy()
+    g0.destroy()
