@@ -262,7 +262,9 @@ int lattice_refine_preact(lattice_t fine, lattice_t coarse, const void* in_dev, 
  *              coordinates, d.. the features.  W2_dev C2 x C1, W3_dev C3 x C2.
  *   b*_dev     optional C1 / C2 / C3 float32 biases (NULL = 0).
  *   C1, C2, C3  16, 32 or 64 (C3 also 48; the paper uses 16, 32, 64).
- *   out_dev    n x C3 float32, row stride ld_out (0 = C3).
+ *   out_dt     LAT_F32, or LAT_BF16 (the float32 maxima rounded to nearest
+ *              even, for a bfloat16 network).
+ *   out_dev    n x C3 of out_dt, row stride ld_out (0 = C3).
  * A non-finite feature makes every output value NaN (the statistics it
  * reaches are not finite).  Uses a work space of O(n + 4m) bytes from the
  * library's pool.
@@ -271,7 +273,7 @@ int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* 
                                 int Cf, const float* gn_gamma_dev, const float* gn_beta_dev, float eps,
                                 const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
                                 const float* b2_dev, int C2, const float* W3_dev, const float* b3_dev, int C3,
-                                float* out_dev, int64_t ld_out, hipStream_t stream);
+                                lat_dtype out_dt, void* out_dev, int64_t ld_out, hipStream_t stream);
 
 /*
  * Slice, Eq. (slice): out_p = sum_{v in I_p} b_pv x_v.

@@ -1198,7 +1198,7 @@ int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* 
                                 int Cf, const float* gn_gamma_dev, const float* gn_beta_dev, float eps,
                                 const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
                                 const float* b2_dev, int C2, const float* W3_dev, const float* b3_dev, int C3,
-                                float* out_dev, int64_t ld_out, hipStream_t stream) {
+                                lat_dtype out_dt, void* out_dev, int64_t ld_out, hipStream_t stream) {
   int st;
   if ((st = use(L, stream)) != LAT_OK) return st;
   if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
@@ -1212,17 +1212,20 @@ int lattice_distribute_pointnet(lattice_t L, const float* pos_dev, const float* 
   if (ld_feat == 0) ld_feat = Cf;
   if (ld_out == 0) ld_out = C3;
   if (ld_feat < Cf) return fail(LAT_EINVAL, "ld_feat < Cf");
-  if (ld_out < C3) return fail(LAT_EINVAL, "ld_out < C3");
+  if ((st = check_dtype(out_dt)) != LAT_OK) return st;
+  if ((st = check_matrix(out_dev, ld_out, C3, out_dt, "out", L->n > 0)) != LAT_OK) return st;
   if (!W1_dev || !W2_dev || !W3_dev) return fail(LAT_EINVAL, "weights are null");
   if (L->m > 0 && !pos_dev) return fail(LAT_EINVAL, "pos is null");
   if (L->m > 0 && Cf > 0 && !feat_dev) return fail(LAT_EINVAL, "feat is null");
   if (L->n > 0 && !out_dev) return fail(LAT_EINVAL, "out is null");
   if (L->n == 0) return LAT_OK;
   Scratch work;
-  if ((st = work.get(static_cast<size_t>(distribute_workspace_bytes(L->n, L->total)), stream)) != LAT_OK) return st;
+  const int bf = out_dt == LAT_BF16;
+  if ((st = work.get(static_cast<size_t>(distribute_workspace_bytes(L->n, L->total, C3, bf)), stream)) != LAT_OK)
+    return st;
   launch_distribute(L->offsets, L->entries, L->chunk_first, L->chunk, L->n, L->total, pos_dev, L->scale, feat_dev,
                     ld_feat, Cf, gn_gamma_dev, gn_beta_dev, eps, W1_dev, b1_dev, C1, W2_dev, b2_dev, C2, W3_dev,
-                    b3_dev, C3, out_dev, ld_out, work.p, stream);
+                    b3_dev, C3, out_dev, bf, ld_out, work.p, stream);
   return check_launch("distribute");
 }
 

@@ -693,6 +693,29 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
   }
 }
 
+// n x C rows of float32 (dense) to bfloat16 rows of stride ld, rounded to
+// nearest even (NaN stays NaN).
+__global__ void __launch_bounds__(kBlock)
+k_dist_to_bf16(const float* __restrict__ src, int64_t n, int C, uint16_t* __restrict__ dst, int64_t ld) {
+  const int q4 = C / 4;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n * q4;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int64_t v = i / q4;
+    const int c = static_cast<int>(i - v * q4) * 4;
+    const float4 x = *reinterpret_cast<const float4*>(src + v * C + c);
+    const float f[4] = {x.x, x.y, x.z, x.w};
+    uint16_t h[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t u = __float_as_uint(f[k]);
+      h[k] = (u & 0x7fffffffu) > 0x7f800000u ? static_cast<uint16_t>((u >> 16) | 0x40u)
+                                              : static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+    }
+    *reinterpret_cast<uint2*>(dst + v * ld + c) =
+        make_uint2(h[0] | (static_cast<uint32_t>(h[1]) << 16), h[2] | (static_cast<uint32_t>(h[3]) << 16));
+  }
+}
+
 void stats_parts(int64_t total, int cp, int64_t* nparts, int64_t* rows_per) {
   const int slots = kBlock / cp;
   int64_t rp = std::max<int64_t>(slots, (total + kStatsMaxParts - 1) / kStatsMaxParts);
@@ -733,13 +756,15 @@ void run_mlp(int stage, const MlpLds& lay, unsigned grid, hipStream_t s, const i
 }  // namespace
 
 // Work space: the vertex means (n double4), the mean pass's span partials, the
-// vertex of every list entry, the three normalisation tables, and the
-// statistics partials (at most max(512, MLP workgroups) x 2 x 64 doubles).
-int64_t distribute_workspace_bytes(int64_t n, int64_t total) {
+// vertex of every list entry, the three normalisation tables, the
+// statistics partials (at most max(512, MLP workgroups) x 2 x 64 doubles),
+// and for a bfloat16 output the float32 rows (n x C3) it is rounded from.
+int64_t distribute_workspace_bytes(int64_t n, int64_t total, int C3, int out_bf16) {
   const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
   const int64_t parts = std::max<int64_t>(kStatsMaxParts, mlp_grid(total));
   auto up = [](int64_t b) { return (b + 255) / 256 * 256; };
-  return up(32 * n) + up(2 * mean_spans * 32) + up(4 * total) + up(3 * kPreStride * 4) + up(parts * 2 * kMaxC * 8);
+  return up(32 * n) + up(2 * mean_spans * 32) + up(4 * total) + up(3 * kPreStride * 4) + up(parts * 2 * kMaxC * 8) +
+         (out_bf16 ? up(4 * n * static_cast<int64_t>(C3)) : 0);
 }
 
 int distribute_max_features() { return kMaxIn - 3; }
@@ -748,7 +773,8 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
                        int64_t n, int64_t total, const float* pos, const double scale[3], const float* feat,
                        int64_t ld_feat, int cf, const float* gamma, const float* beta, float eps, const float* W1,
                        const float* b1, int C1, const float* W2, const float* b2, int C2, const float* W3,
-                       const float* b3, int C3, float* out, int64_t ld_out, void* work, hipStream_t s) {
+                       const float* b3, int C3, void* out_dev, int out_bf16, int64_t ld_out_dev, void* work,
+                       hipStream_t s) {
   if (total <= 0 || n <= 0) return;
   ScopedKernelTimer tm("distribute", s);
   const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
@@ -764,6 +790,11 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
   float* pre = reinterpret_cast<float*>(w);
   w += up(3 * kPreStride * 4);
   double* part = reinterpret_cast<double*>(w);
+  w += up(std::max<int64_t>(kStatsMaxParts, mlp_grid(total)) * 2 * kMaxC * 8);
+  // the maxima are taken in float32: into the caller's rows, or into dense
+  // work rows that are rounded to bfloat16 at the end
+  float* out = out_bf16 ? reinterpret_cast<float*>(w) : static_cast<float*>(out_dev);
+  const int64_t ld_out = out_bf16 ? C3 : ld_out_dev;
   launch(k_dist_mean, dim3(static_cast<unsigned>(mean_spans)), dim3(kBlock), 0, s, offsets, entries, chunk_first,
          chunk, n, total, pos, scale[0], scale[1], scale[2], mu4, mh, mt, ev, static_cast<int64_t>(kMlpRange), out,
          ld_out, C3);
@@ -804,6 +835,9 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
                          beta ? beta + offs[stage] : nullptr, eps, pre + stage * kPreStride, s);
     }
   }
+  if (out_bf16)
+    launch(k_dist_to_bf16, dim3(static_cast<unsigned>(std::min<int64_t>((n * C3 / 4 + kBlock - 1) / kBlock, 4096))),
+           dim3(kBlock), 0, s, static_cast<const float*>(out), n, C3, static_cast<uint16_t*>(out_dev), ld_out_dev);
 }
 
 }  // namespace lat

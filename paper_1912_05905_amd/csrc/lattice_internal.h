@@ -188,7 +188,7 @@ void launch_deform_slice_backward(const int32_t* idx, const float* w, int64_t m,
                                   float beta, const float* dout, int64_t ld_dout, float* dvals, int64_t ld_dvals,
                                   float* dwv, float* dbeta, void* work, hipStream_t s);
 // distribute.hip
-int64_t distribute_workspace_bytes(int64_t n, int64_t total);
+int64_t distribute_workspace_bytes(int64_t n, int64_t total, int C3, int out_bf16);
 int distribute_max_features();
 // scale: sigma per axis at the lattice's level (positions enter as pos / scale);
 // gamma / beta: optional per-channel parameters of the three GroupNorms,
@@ -197,7 +197,7 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
                        int64_t n, int64_t total, const float* pos, const double scale[3], const float* feat,
                        int64_t ld_feat, int cf, const float* gamma, const float* beta, float eps, const float* W1,
                        const float* b1, int C1, const float* W2, const float* b2, int C2, const float* W3,
-                       const float* b3, int C3, float* out, int64_t ld_out, void* work, hipStream_t s);
+                       const float* b3, int C3, void* out, int out_bf16, int64_t ld_out, void* work, hipStream_t s);
 // backward.hip
 void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, const float* wsum, int64_t n,
                                 const float* in, int64_t ld_in, int C, float* out, int64_t ld_out, hipStream_t s);

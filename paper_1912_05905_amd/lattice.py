@@ -54,7 +54,7 @@ SIGNATURES = {
                                      _I64, _P]),
     "lattice_deform_slice_classify": (_I32, [_P, _P, _I64, _I32, _I32, _P, _F32, _P, _P, _I32, _P, _P]),
     "lattice_distribute_pointnet": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, C.c_float, _P, _P, _I32, _P, _P,
-                                           _I32, _P, _P, _I32, _P, _I64, _P]),
+                                           _I32, _P, _P, _I32, _I32, _P, _I64, _P]),
     "lattice_splat_backward": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "lattice_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _I64, _P]),
     "lattice_conv_backward": (_I32, [_P, _P, _P, _I64, _I32, _P, _I32, _I32, _P, _I64, _P, _I64, _P, _I64, _P, _P,
@@ -316,11 +316,12 @@ class Lattice:
         return out
 
     def distribute_pointnet(self, pos: torch.Tensor, feat: torch.Tensor | None, layers, gn=None, eps: float = 1e-5,
-                            out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+                            out: torch.Tensor | None = None, stream=None, dtype=torch.float32) -> torch.Tensor:
         """Distribute + PointNet; layers = [(W1, b1), (W2, b2), (W3, b3)] with
         W_i float32 [out][in] device tensors and optional biases; gn = None or
         (gamma, beta), the concatenated parameters of the three GroupNorms
-        ((3 + Cf) + C1 + C2 float32 values each, either may be None)."""
+        ((3 + Cf) + C1 + C2 float32 values each, either may be None).  The
+        output is float32 or bfloat16 (out's dtype, else `dtype`)."""
         (W1, b1), (W2, b2), (W3, b3) = layers
         c1, c2, c3 = W1.shape[0], W2.shape[0], W3.shape[0]
         for W in (W1, W2, W3):
@@ -336,12 +337,12 @@ class Lattice:
                 raise ValueError("GroupNorm parameters must be contiguous float32 of (3 + Cf) + C1 + C2 values")
         fp, fld = (None, 0) if feat is None else _rows(feat)
         if out is None:
-            out = torch.empty((self.n, c3), dtype=torch.float32, device="cuda")
+            out = torch.empty((self.n, c3), dtype=dtype, device="cuda")
         op, old = _rows(out)
         ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
         _check(lib().lattice_distribute_pointnet(self._h, ptr(pos), fp, fld, cf, ptr(gam), ptr(bet), float(eps),
                                                  ptr(W1), ptr(b1), c1, ptr(W2), ptr(b2), c2, ptr(W3), ptr(b3), c3,
-                                                 op, old, _stream(stream)))
+                                                 _dtype_code(out), op, old, _stream(stream)))
         return out
 
     # ---- backward passes (float32) ----

@@ -56,6 +56,8 @@ class GpuPipeline:
         self.dtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
         self.pos = torch.from_numpy(np.ascontiguousarray(wl.positions)).cuda()
         self.feat = torch.from_numpy(np.ascontiguousarray(wl.features)).cuda().to(self.dtype)
+        # Distribute reads float32 features (a bf16 workload's are bf16 values)
+        self.feat32 = torch.from_numpy(np.ascontiguousarray(wl.features, dtype=np.float32)).cuda()
         # library weight layout: taps x Cout x Cin
         self.weights = {k: torch.from_numpy(np.ascontiguousarray(np.transpose(w, (0, 2, 1))))
                         .cuda().to(self.dtype).contiguous() for k, w in wl.weights.items()}
@@ -94,7 +96,7 @@ class GpuPipeline:
                 self._outs[name] = t
         return t
 
-    def step(self, keep=False):
+    def step(self, keep=False, after_op=None):
         """One pass of the pipeline.  Returns (levels, buffers, point outputs).
 
         The lattice hierarchy (create, coarsen) is issued first: a coarse
@@ -103,7 +105,10 @@ class GpuPipeline:
         for vertex counts.  With keep=True the buffers are fresh tensors
         that later steps do not overwrite.  Forward operators are called
         with raw pointers into the buffers (column ranges by offset), which
-        keeps the host's cost per operator near the library call itself."""
+        keeps the host's cost per operator near the library call itself.
+        after_op(i, op, levels, buffers, outputs), if given, is called once
+        each operation i has been enqueued (for checks of every operator on
+        the inputs it saw)."""
         wl, lib, es, dt = self.wl, self._lib, self._esize, self._dt
         levels: dict[int, Lattice] = {}
         rows: dict[str, int] = {}
@@ -192,6 +197,9 @@ class GpuPipeline:
                 check(lib.lattice_slice_and_deform(L._h, xp, xld, cc, dt, wv.data_ptr(), beta, out.data_ptr(),
                                                    dout.data_ptr(), stream))
                 skip = True
+                if after_op is not None:
+                    after_op(i, op, levels, _Buffers(self._store, rows), outs)
+                    after_op(i + 1, dop, levels, _Buffers(self._store, rows), outs)
                 continue
             elif kind == "splat":
                 L0 = levels[0]
@@ -228,10 +236,10 @@ class GpuPipeline:
                 (W1, b1), (W2, b2), (W3, b3) = layers
                 gam, bet = self.norms[op["norm"]]
                 check(lib.lattice_distribute_pointnet(
-                    levels[op["level"]]._h, self.pos.data_ptr(), self.feat.data_ptr(), self.feat.stride(0),
-                    self.feat.shape[1], gam.data_ptr(), bet.data_ptr(), 1e-5, W1.data_ptr(), b1.data_ptr(),
+                    levels[op["level"]]._h, self.pos.data_ptr(), self.feat32.data_ptr(), self.feat32.stride(0),
+                    self.feat32.shape[1], gam.data_ptr(), bet.data_ptr(), 1e-5, W1.data_ptr(), b1.data_ptr(),
                     W1.shape[0], W2.data_ptr(), b2.data_ptr(), W2.shape[0], W3.data_ptr(), b3.data_ptr(),
-                    W3.shape[0], yp, yld, stream))
+                    W3.shape[0], dt, yp, yld, stream))
             elif kind == "slice":
                 L = levels[op["level"]]
                 xp, xld = ptr(op["src"])
@@ -263,6 +271,8 @@ class GpuPipeline:
                 self._backward_op(op, levels, _Buffers(self._store, rows), outs)
             else:
                 raise ValueError(f"unknown op {kind}")
+            if after_op is not None:
+                after_op(i, op, levels, _Buffers(self._store, rows), outs)
         stores = self._store
         if keep:
             self._store = {}

@@ -74,7 +74,7 @@ def test_host_validation_without_gpu(lib):
     assert lib.lattice_deform_slice(None, None, 0, 8, 0, None, 0.0, None, None, None) == -1
     assert lib.lattice_slice_and_deform(None, None, 0, 8, 0, None, 0.0, None, None, None) == -1
     assert lib.lattice_distribute_pointnet(None, None, None, 0, 4, None, None, C.c_float(1e-5), None, None, 16,
-                                           None, None, 32, None, None, 64, None, 0, None) == -1
+                                           None, None, 32, None, None, 64, 0, None, 0, None) == -1
     assert lib.lattice_coarsen(None, 0, None, C.byref(out)) == -1
     assert lib.lattice_coarsen_ex(None, 0, 0, None, C.byref(out)) == -1
     assert lib.lattice_splat_backward(None, None, 0, 8, 1, None, None, None) == -1

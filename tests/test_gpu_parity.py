@@ -467,76 +467,132 @@ def test_slice_and_deform_slice(L, O, C, dtype):
 # ----------------------------------------------------------------------------
 # whole pipelines
 # ----------------------------------------------------------------------------
-def _check_ops_on_stored_inputs(O, wl, levels, bufs, outs, olv, g2o, rng=None, rows_per_op=None, points=None):
-    """Every operator of a workload against the oracle, each on the inputs
-    the GPU stored for it (its source columns as the GPU wrote them), so
-    every comparison is one operator deep: splat from the point features;
-    convolutions (1-hop, strided, Upsample, concatenated column ranges
-    included) on all rows or on a seeded sample of rows_per_op; DeformSlice
-    and slice on all points or a sample of `points`.  Returns the number of
-    operators checked."""
+def _step_checked(L, O, wl, olv=None, rng=None, rows_per_op=None, points=None):
+    """One GPU step with every operator compared with the oracle as it runs,
+    on the inputs the GPU stored for it (its source columns as the GPU wrote
+    them, kept on the host as each operator finishes, so buffers reused
+    later in the step do not matter): every comparison is one operator deep.
+    Lattice structure bit-exact on every level.  Operators: splat and
+    Distribute + PointNet on every vertex; convolutions (1-hop, strided,
+    Upsample; pre-activated ones with GroupNorm over the whole stored input
+    and the residual added) on all rows or on a seeded sample of
+    rows_per_op; slice, DeformSlice and DeformSlice + classifier on all
+    points or a sample of `points`.  Returns (levels, buffers, outputs,
+    oracle levels, number of operators checked)."""
+    from paper_1912_05905_amd.pipeline import GpuPipeline
     bf = wl.dtype == "bf16"
     rnd = O.round_bf16 if bf else (lambda a: a)
     tol = P.TOL_BF16 if bf else P.TOL_F32
-    host = {}
+    if olv is None:
+        olv = {}
+        for op in wl.ops:
+            if op["op"] == "create":
+                olv[0] = O.Lattice.create(wl.positions, wl.sigma)
+            elif op["op"] == "coarsen":
+                olv[op["level"]] = olv[op["level"] - 1].coarsen()
+    state = {"g2o": None, "checked": 0}
+    mirror = {}
 
     def cols(spec):
         name, c0, cc = spec
-        if name not in host:
-            host[name] = P.rows_in_oracle_order(_host(bufs[name]), g2o[wl.buffers[name][0]])
-        return np.ascontiguousarray(host[name][:, c0:c0 + cc], dtype=np.float64)
+        return np.ascontiguousarray(mirror[name][:, c0:c0 + cc], dtype=np.float64)
 
-    checked = 0
-    for op in wl.ops:
+    def sample_rows(n):
+        if rows_per_op is None or n <= rows_per_op:
+            return None
+        return np.sort(rng.choice(n, size=rows_per_op, replace=False))
+
+    def sample_points():
+        if points is None or wl.m <= points:
+            return None
+        return np.sort(rng.choice(wl.m, size=points, replace=False))
+
+    def after(i, op, levels, bufs, outs):
+        torch.cuda.synchronize()
+        if state["g2o"] is None:
+            state["g2o"] = {lv: _check_structure(levels[lv], olv[lv]) for lv in sorted(levels)}
+        g2o = state["g2o"]
         kind = op["op"]
-        if kind in ("create", "coarsen"):
-            continue
+
+        def gpu_cols(spec):
+            name, c0, cc = spec
+            return P.rows_in_oracle_order(_host(bufs[name][:, c0:c0 + cc]), g2o[wl.buffers[name][0]])
+
+        what = f"op {i} {kind} -> {op.get('dst', op.get('out'))}"
         if kind == "splat":
             X, _ = olv[0].splat(wl.features.astype(np.float64), normalize=bool(op["normalize"]))
-            P.assert_close(cols(op["dst"]), rnd(X), tol, "splat")
+            P.assert_close(gpu_cols(op["dst"]), rnd(X), tol, what)
+        elif kind == "distribute":
+            layers = [tuple(a.astype(np.float64) for a in wl.mlp[n]) for n in op["layers"]]
+            gn = tuple(a.astype(np.float64) for a in wl.norms[op["norm"]])
+            X = olv[op["level"]].distribute_pointnet(wl.positions.astype(np.float64), wl.features.astype(np.float64),
+                                                     layers, gn)
+            P.assert_close(gpu_cols(op["dst"]), rnd(X), tol, what)
         elif kind in ("conv", "conv_down", "refine"):
-            assert "pre" not in op and "res" not in op, "pre-activated operators are checked elsewhere"
             lv = op["level"]
             x = cols(op["src"])
+            if "pre" in op:
+                gam, bet = wl.norms[op["pre"]["norm"]]
+                x = rnd(O.groupnorm(x, op["pre"]["groups"], gam.astype(np.float64), bet.astype(np.float64),
+                                    eps=1e-5, relu=True))
             W = wl.weights[op["w"]].astype(np.float64)
-            rows = None
-            if rows_per_op is not None and olv[lv].n > rows_per_op:
-                rows = np.sort(rng.choice(olv[lv].n, size=rows_per_op, replace=False))
+            rows = sample_rows(olv[lv].n)
             if kind == "conv":
                 y = olv[lv].conv(olv[lv], x, W, relu=op["relu"], rows=rows)
             elif kind == "conv_down":
                 y = olv[lv].conv(olv[lv - 1], x, W, relu=op["relu"], rows=rows)
             else:
                 y = olv[lv].refine_into(olv[lv + 1], x, W, relu=op["relu"], rows=rows)
-            got = cols(op["dst"]) if rows is None else cols(op["dst"])[rows]
-            P.assert_close(got, rnd(y), tol, f"{kind} -> {op['dst']}")
-        elif kind in ("slice", "deform_slice"):
-            pts = None
-            if points is not None and wl.m > points:
-                pts = np.sort(rng.choice(wl.m, size=points, replace=False))
+            if "res" in op:
+                r = cols(op["res"])
+                y = y + (r if rows is None else r[rows])
+            got = gpu_cols(op["dst"])
+            P.assert_close(got if rows is None else got[rows], rnd(y), tol, what)
+        elif kind in ("slice", "deform_slice", "deform_classify"):
+            pts = sample_points()
             lat = olv[op["level"]]
             if kind == "slice":
                 ref = lat.slice(cols(op["src"]), pts=pts)
-            else:
+            elif kind == "deform_slice":
                 wv, beta = wl.vectors[op["wv"]]
                 ref, _ = lat.deform_slice(cols(op["src"]), wv.astype(np.float64), beta, pts=pts)
+            else:
+                wv, beta = wl.vectors[op["wv"]]
+                Wc, bc = wl.classifiers[op["cls"]]
+                if pts is None:
+                    ref = lat.deform_slice_classify(cols(op["src"]), wv.astype(np.float64), beta,
+                                                    Wc.astype(np.float64), bc.astype(np.float64))
+                else:
+                    f, _ = lat.deform_slice(cols(op["src"]), wv.astype(np.float64), beta, pts=pts)
+                    ref = f @ Wc.astype(np.float64).T + bc.astype(np.float64)
             got = _host(outs[op["out"]])
-            P.assert_close(got if pts is None else got[pts], ref, P.TOL_F32, kind)
+            P.assert_close(got if pts is None else got[pts], ref, P.TOL_F32, what)
         else:
             raise AssertionError(f"no stored-input check for operator {kind}")
-        checked += 1
-    return checked
+        if "dst" in op:
+            name, c0, cc = op["dst"]
+            if name not in mirror:
+                lv, total = wl.buffers[name]
+                mirror[name] = np.zeros((olv[lv].n, total), np.float32)
+            mirror[name][:, c0:c0 + cc] = gpu_cols(op["dst"])
+        state["checked"] += 1
+
+    levels, bufs, outs = GpuPipeline(wl).step(keep=True, after_op=after)
+    return levels, bufs, outs, olv, state["checked"]
 
 
 def _run_both(L, O, wl):
     """Whole pipeline on the GPU and in the oracle, structure bit-exact on
     every level.  fp32: every written column range and point output
-    elementwise.  bf16: every operator elementwise on its stored inputs, and
-    every tensor normwise end to end."""
+    elementwise.  bf16: every operator elementwise on its stored inputs
+    (_step_checked), and every tensor normwise end to end."""
     from paper_1912_05905_amd.pipeline import GpuPipeline
-    levels, bufs, outs = GpuPipeline(wl).step(keep=wl.dtype == "bf16")
-    olv, obufs, oouts = OraclePipeline(wl).run()
     bf = wl.dtype == "bf16"
+    if bf:
+        levels, bufs, outs, _, _ = _step_checked(L, O, wl)
+    else:
+        levels, bufs, outs = GpuPipeline(wl).step()
+    olv, obufs, oouts = OraclePipeline(wl).run()
     tol = P.TOL_BF16 if bf else P.TOL_F32
     check = P.assert_normwise if bf else P.assert_close
     g2o = {}
@@ -552,8 +608,6 @@ def _run_both(L, O, wl):
         check(got, obufs[name][:, c0:c0 + cc], tol, f"{name}[{c0}:{c0 + cc}]")
     for name in outs:
         check(_host(outs[name]), oouts[name], tol, name)
-    if bf:
-        _check_ops_on_stored_inputs(O, wl, levels, bufs, outs, olv, g2o)
     return levels
 
 
@@ -568,22 +622,35 @@ def test_pipeline_config5_full_size_sampled(L, O):
     the four-level hierarchy bit-exact, splat on every vertex, each of the
     thirteen convolutions on a seeded sample of 4,000 output rows (1-hop,
     strided and Upsample, concatenated column ranges included), DeformSlice
-    on 50,000 points.  Every operator's inputs are the bf16 values the GPU
-    stored, so each comparison is one operator deep."""
+    on 50,000 points."""
     from paper_1912_05905_amd.pipeline import GpuPipeline
-    wl = configs.make(5)
-    pipe = GpuPipeline(wl)
-    levels, bufs, outs = pipe.step(keep=True)
-    olv = {}
-    for op in wl.ops:
-        if op["op"] == "create":
-            olv[0] = O.Lattice.create(wl.positions, wl.sigma)
-        elif op["op"] == "coarsen":
-            olv[op["level"]] = olv[op["level"] - 1].coarsen()
-    g2o = {lv: _check_structure(levels[lv], olv[lv]) for lv in sorted(levels)}
-    checked = _check_ops_on_stored_inputs(O, wl, levels, bufs, outs, olv, g2o, rng=np.random.default_rng(55),
-                                          rows_per_op=4000, points=50_000)
+    levels, _, _, _, checked = _step_checked(L, O, configs.make(5), rng=np.random.default_rng(55),
+                                             rows_per_op=4000, points=50_000)
     assert checked == 15
+    GpuPipeline.release(levels)
+
+
+def test_latticenet_bf16_full_size_sampled(L, O):
+    """The LatticeNet forward on the 1M-point room in bf16 (workload 10) at
+    full size, operator by operator on the GPU's own inputs: the three-level
+    hierarchy bit-exact, Distribute + PointNet on every vertex, each of the
+    twenty pre-activated convolutions (GroupNorm over the whole stored input)
+    on 4,000 sampled rows with its residual, the fused DeformSlice +
+    classifier on 50,000 points."""
+    from paper_1912_05905_amd.pipeline import GpuPipeline
+    print("latticenet bf16, 1M points, stored-input checks", flush=True)
+    levels, _, _, _, checked = _step_checked(L, O, configs.make(10), rng=np.random.default_rng(56),
+                                             rows_per_op=4000, points=50_000)
+    assert checked == 22
+    GpuPipeline.release(levels)
+
+
+def test_latticenet_bf16_reduced(L, O):
+    """The bf16 LatticeNet forward on a reduced room of the same generator:
+    every operator on its stored inputs and every tensor normwise against
+    the whole oracle network."""
+    from paper_1912_05905_amd.pipeline import GpuPipeline
+    levels = _run_both(L, O, configs.config10(m=12_000, size=(2.0, 2.0, 2.0), nboxes=3))
     GpuPipeline.release(levels)
 
 

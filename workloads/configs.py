@@ -351,8 +351,22 @@ def config7(seed: int = 3, m: int = 120_000) -> Workload:
     return wl
 
 
+def config10(seed: int = 4, m: int = 1_000_000, size=(20.0, 20.0, 3.0), nboxes: int = 125) -> Workload:
+    """LatticeNet forward on the large indoor stack of config 5 (1M points,
+    20x20x3 m room, 125 boxes): raw features = RGB, sigma 0.05 m, widths
+    64/128/256, 20 classes, bf16 storage of every lattice activation and
+    bf16 MFMA inputs with fp32 accumulation (Distribute + PointNet in fp32,
+    its output rounded to bf16; the classifier in fp32 from the bf16
+    values)."""
+    pos = gen.room(seed, m, size, nboxes, 0.01)
+    rgb = gen.Stream(seed, "rgb").uniform(3 * m).reshape(m, 3).astype(np.float32)
+    wl = Workload(10, "latticenet-large-indoor", seed, pos, np.full(3, 0.05, np.float32), "bf16", rgb)
+    _latticenet(wl, seed)
+    return _finish(wl)
+
+
 CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5, 6: config6, 7: config7, 8: config8,
-           9: config9}
+           9: config9, 10: config10}
 
 
 def make(cfg: int, seed: int | None = None, **kw) -> Workload:
