@@ -203,11 +203,14 @@ void conv_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* in,
 // workgroup gathers the stage's A tile (BM neighbour rows, KC channels) and
 // B tile (BN weight rows, KC channels) into LDS with 16-byte loads, 8 or 16
 // lanes per row segment; the next stage's global loads are issued before the
-// current stage is multiplied, so their latency hides behind the MFMAs.  Rows
-// of the LDS tiles are padded by 16 bytes so that the 16 rows read by one
-// MFMA fragment fall in different banks.  Workgroups are numbered so that
-// each XCD gets a contiguous range of row tiles: neighbouring rows (the
-// gather's halo) then stay in that XCD's L2.
+// current stage is multiplied, so their latency hides behind the MFMAs.  The
+// 16-byte chunks of an LDS row are stored in an order permuted by the row
+// (chunk c of row r at c ^ swz(r)), so that the 16 rows an MFMA fragment
+// reads, and the chunks a copy writes, fall in different banks: measured on
+// gfx950 with rocprofv3 (SQ_LDS_BANK_CONFLICT), rows padded by 16 bytes cost
+// about 3 conflict cycles per ds_read_b128, these permutations none.
+// Workgroups are numbered so that each XCD gets a contiguous range of row
+// tiles: neighbouring rows (the gather's halo) then stay in that XCD's L2.
 // ---------------------------------------------------------------------------
 template <bool BF16, int BM, int BN, int WM, int WN, int KCB>
 struct LdsConv {
@@ -215,7 +218,11 @@ struct LdsConv {
   static constexpr int EPC = 16 / U;                // elements per 16-byte chunk
   static constexpr int KC = KCB / U;                // channels per stage
   static constexpr int CPR = KCB / 16;              // chunks per row per stage
-  static constexpr int LDR = KC + EPC;              // padded LDS row (elements)
+  static constexpr int LDR = KC;                    // LDS row (elements), chunks permuted by swz
+  // chunk permutation of row r: 4 chunks by (r / 2) mod 4, 8 or 16 chunks by r
+  __device__ static inline int swz(int r) { return CPR == 4 ? (r >> 1) & 3 : r & (CPR - 1); }
+  // element offset of channel chunk c of row r
+  __device__ static inline int at(int r, int c) { return r * LDR + ((c ^ swz(r)) & (CPR - 1)) * EPC; }
   static constexpr int RM = BM / (16 * WM);
   static constexpr int RN = BN / (16 * WN);
   static constexpr int KS = BF16 ? 32 : 16;         // channels per MFMA step
@@ -228,6 +235,8 @@ struct LdsConv {
   static_assert(WM * WN == kWaves, "four waves");
   static_assert(RM >= 1 && RN >= 1, "wave tile");
   static_assert(A_PER_T >= 1 && BM * CPR % kBlock == 0, "A copy split");
+  static_assert(CPR == 4 || CPR == 8 || CPR == 16, "chunk permutation");
+  static_assert(KC % KS == 0 && KS * U == 64, "an MFMA step reads 4 chunks of a row");
 };
 
 // PRE: the pre-activation of the input (Group Normalization folded into a
@@ -402,14 +411,14 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
           v = make_uint4(w[0], w[1], w[2], w[3]);
         }
       }
-      *reinterpret_cast<V*>(a + r * P::LDR + cc * P::EPC) = v;
+      *reinterpret_cast<V*>(a + P::at(r, cc)) = v;
     }
 #pragma unroll
     for (int j = 0; j < P::B_PER_T; ++j) {
       const int q = tid + j * kBlock;
       if (q < BN * P::CPR) {
         const int r = q / P::CPR, cc = q % P::CPR;
-        *reinterpret_cast<V*>(bb + r * P::LDR + cc * P::EPC) = rb[set][j];
+        *reinterpret_cast<V*>(bb + P::at(r, cc)) = rb[set][j];
       }
     }
   };
@@ -442,16 +451,20 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
       stash(std::integral_constant<int, NEXT>{}, buf ^ 1, st + 1);
       fetch(set_c, st + NS);
     }
-    const E* a = As + buf * (BM * P::LDR) + (wm * P::RM * 16 + li) * P::LDR + lg * P::EPL;
-    const E* bb = Bs + buf * (BN * P::LDR) + (wn * P::RN * 16 + li) * P::LDR + lg * P::EPL;
+    // rows of a fragment are 16-aligned blocks plus li, so the permutation
+    // of the lane's row is that of li: MFMA step k reads chunk 4 k + lg
+    const E* a = As + buf * (BM * P::LDR) + (wm * P::RM * 16 + li) * P::LDR;
+    const E* bb = Bs + buf * (BN * P::LDR) + (wn * P::RN * 16 + li) * P::LDR;
+    const int sw = P::swz(li);
     constexpr int NK = P::KC / P::KS;
     Frag<BF16> fa[NK][P::RM], fb[NK][P::RN];
 #pragma unroll
     for (int k = 0; k < NK; ++k) {
+      const int ck = (((4 * k + lg) ^ sw) & (P::CPR - 1)) * P::EPC;
 #pragma unroll
-      for (int i = 0; i < P::RM; ++i) fa[k][i].load(a, i * 16 * P::LDR + k * P::KS);
+      for (int i = 0; i < P::RM; ++i) fa[k][i].load(a, i * 16 * P::LDR + ck);
 #pragma unroll
-      for (int j = 0; j < P::RN; ++j) fb[k][j].load(bb, j * 16 * P::LDR + k * P::KS);
+      for (int j = 0; j < P::RN; ++j) fb[k][j].load(bb, j * 16 * P::LDR + ck);
     }
 #pragma unroll
     for (int k = 0; k < NK; ++k) {
