@@ -44,12 +44,6 @@ constexpr int kMaxPreChannels = 1024;   // widest input of a pre-activated convo
 constexpr int kOutOfRange = static_cast<int>(0x80000000u);
 constexpr int64_t kMaxBufferBytes = (int64_t{1} << 31) - 64;
 
-__device__ inline uint16_t f32_to_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
-}
-
 // f(std::integral_constant<int, i>) for i = 0 .. N-1, unrolled.
 template <class F, int... I>
 __device__ inline void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
@@ -401,7 +395,7 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
               const float lo = fmaxf(fmaf(__uint_as_float(w[i] << 16), pre_s[ch + 2 * i], pre_s[Cin + ch + 2 * i]), 0.f);
               const float hi = fmaxf(fmaf(__uint_as_float(w[i] & 0xffff0000u), pre_s[ch + 2 * i + 1],
                                           pre_s[Cin + ch + 2 * i + 1]), 0.f);
-              w[i] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+              w[i] = pack_bf16x2(lo, hi);
             }
           } else {
 #pragma unroll
@@ -570,8 +564,8 @@ k_conv_reduce(const float* __restrict__ part, int splits, int64_t n_out, int Cou
       }
     }
     if constexpr (BF16) {
-      const uint32_t lo = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
-      const uint32_t hi = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+      const uint32_t lo = pack_bf16x2(v[0], v[1]);
+      const uint32_t hi = pack_bf16x2(v[2], v[3]);
       *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + row * ld_out + col) = make_uint2(lo, hi);
     } else {
       *reinterpret_cast<float4*>(static_cast<float*>(out) + row * ld_out + col) = make_float4(v[0], v[1], v[2], v[3]);

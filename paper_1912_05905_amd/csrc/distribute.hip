@@ -694,7 +694,7 @@ k_dist_mlp(const int32_t* __restrict__ entries, const int32_t* __restrict__ entr
 }
 
 // n x C rows of float32 (dense) to bfloat16 rows of stride ld, rounded to
-// nearest even (NaN stays NaN).
+// nearest even.
 __global__ void __launch_bounds__(kBlock)
 k_dist_to_bf16(const float* __restrict__ src, int64_t n, int C, uint16_t* __restrict__ dst, int64_t ld) {
   const int q4 = C / 4;
@@ -703,16 +703,7 @@ k_dist_to_bf16(const float* __restrict__ src, int64_t n, int C, uint16_t* __rest
     const int64_t v = i / q4;
     const int c = static_cast<int>(i - v * q4) * 4;
     const float4 x = *reinterpret_cast<const float4*>(src + v * C + c);
-    const float f[4] = {x.x, x.y, x.z, x.w};
-    uint16_t h[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t u = __float_as_uint(f[k]);
-      h[k] = (u & 0x7fffffffu) > 0x7f800000u ? static_cast<uint16_t>((u >> 16) | 0x40u)
-                                              : static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
-    }
-    *reinterpret_cast<uint2*>(dst + v * ld + c) =
-        make_uint2(h[0] | (static_cast<uint32_t>(h[1]) << 16), h[2] | (static_cast<uint32_t>(h[3]) << 16));
+    *reinterpret_cast<uint2*>(dst + v * ld + c) = make_uint2(pack_bf16x2(x.x, x.y), pack_bf16x2(x.z, x.w));
   }
 }
 

@@ -44,6 +44,14 @@ __host__ __device__ inline void unpack_key(uint64_t k, int32_t c[kVerts]) {
   c[3] = -(c[0] + c[1] + c[2]);
 }
 
+// float32 -> bfloat16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+typedef __bf16 lat_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float lat_f32x2 __attribute__((ext_vector_type(2)));
+__device__ inline uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(lat_f32x2{lo, hi}, lat_bf16x2));
+}
+__device__ inline uint16_t f32_to_bf16(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
+
 // Slot hash: the murmur3 64-bit finaliser.
 __host__ __device__ inline uint64_t hash_key(uint64_t k) {
   k ^= k >> 33;

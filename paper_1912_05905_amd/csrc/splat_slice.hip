@@ -18,12 +18,6 @@ constexpr unsigned kClassifyGrid = 2048;   // workgroups of the fused classifier
 constexpr int kClassifyMaxWeights = 16384; // K x C classifier weights staged in LDS
 
 // float -> bfloat16, round to nearest even (NaN stays NaN).
-__device__ inline uint16_t f32_to_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
-}
-
 // Row / chunk index of a lane group with XCD-contiguous workgroup order:
 // workgroup b runs on XCD b % 8, so consecutive work items (which share
 // feature or vertex rows) are given to workgroups of the same XCD and meet in
@@ -129,7 +123,7 @@ template <> struct Chunk<true> {
     uint32_t w[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      w[i] = static_cast<uint32_t>(f32_to_bf16(v[2 * i])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * i + 1])) << 16);
+      w[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
     *reinterpret_cast<uint4*>(static_cast<uint16_t*>(base) + elem) = make_uint4(w[0], w[1], w[2], w[3]);
   }
 };
