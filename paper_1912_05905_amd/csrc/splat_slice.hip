@@ -956,6 +956,16 @@ inline int lanes_per_row(int C, bool bf16) {
   return l;
 }
 
+// Lane group of one row (one vertex list entry or one point) for the splat,
+// DeformSlice, the fused classifier and the DeformSlice gradient's point
+// pass: 64 fp32 channels take 8 lanes of two 16-byte chunks each (half the
+// per-entry bookkeeping per channel), every other width one chunk per lane.
+// DeformSlice and its gradient must agree: the gradient recomputes the
+// offsets, and the same lane groups sum the dot products in the same order.
+inline int point_lanes_per_row(int C, bool bf16) {
+  return !bf16 && C / 4 == 16 ? 8 : lanes_per_row(C, bf16);
+}
+
 inline unsigned grid_for(int64_t rows, int lpr) {
   return static_cast<unsigned>((rows * lpr + kBlock - 1) / kBlock);
 }
@@ -1108,13 +1118,8 @@ void launch_splat(const int32_t* offsets, const int32_t* entries, const float* e
                   hipStream_t s) {
   if (total <= 0) return;
   const int chunks = C / (bf16 ? 8 : 4);
-  int lpr = lanes_per_row(C, bf16 != 0);
-  int q = chunks <= lpr ? 1 : (chunks <= 2 * lpr ? 2 : 4);
-  // 64 fp32 channels: 8 lanes of two chunks each (half the per-entry work)
-  if (!bf16 && chunks == 16) {
-    lpr = 8;
-    q = 2;
-  }
+  const int lpr = point_lanes_per_row(C, bf16 != 0);
+  const int q = chunks <= lpr ? 1 : (chunks <= 2 * lpr ? 2 : 4);
   const int64_t span_len = static_cast<int64_t>(kBlock / lpr) * chunk;
   const int64_t nspans = (total + span_len - 1) / span_len;
   float* ph = partials;
@@ -1167,9 +1172,7 @@ void launch_deform_classify(const int32_t* idx, const float* w, int64_t m, const
                             hipStream_t s) {
   if (m <= 0) return;
   const int chunks = C / (bf16 ? 8 : 4);
-  // 64 fp32 channels: 8 lanes of two chunks each, twice the points per wave
-  // for the same per-point work (indices, weights, the group's dot products)
-  const int lpr = !bf16 && chunks == 16 ? 8 : lanes_per_row(C, bf16 != 0);
+  const int lpr = point_lanes_per_row(C, bf16 != 0);
   ScopedKernelTimer tm("deform_slice", s);
   const bool two = chunks > lpr;
   const bool kp64 = K > 32 || lpr > 32;
@@ -1186,7 +1189,7 @@ void launch_deform_classify(const int32_t* idx, const float* w, int64_t m, const
 #undef DCL_GO
 }
 
-// Work space of launch_deform_slice_backward, in bytes.// Work space of launch_deform_slice_backward, in bytes.
+// Work space of launch_deform_slice_backward, in bytes.
 int64_t deform_backward_workspace_bytes(int64_t m, int C, int64_t total, int chunk) {
   return 16 * 4 * m + m * C + 4 * (kDeformBwdGrid * (static_cast<int64_t>(C) + 1)) +
          4 * splat_partial_floats(total, chunk, C) + 64;
@@ -1215,15 +1218,18 @@ void launch_deform_slice_backward(const int32_t* idx, const float* w, int64_t m,
   float* parts = reinterpret_cast<float*>(wp);
   wp += 4 * splat_partial_floats(total, chunk, C);
   uint8_t* am = reinterpret_cast<uint8_t*>(wp);
+  // the point pass on the forward's lane groups (the same offsets); the
+  // gather over the vertex lists on one chunk per lane
+  const int plpr = point_lanes_per_row(C, false);
   const int lpr = lanes_per_row(C, false);
   const int chunks = C / 4;
-  const int G = kBlock / lpr;
+  const int G = kBlock / plpr;
   const int64_t groups = (m + G - 1) / G;
   const unsigned grid = static_cast<unsigned>(std::min<int64_t>(groups, kDeformBwdGrid));
-  if (chunks > lpr)
-    deform_bwd_point_dispatch<2>(lpr, grid, idx, w, m, vals, ld_vals, C, wv, beta, dout, ld_dout, coef, am, pwv, pb, s);
+  if (chunks > plpr)
+    deform_bwd_point_dispatch<2>(plpr, grid, idx, w, m, vals, ld_vals, C, wv, beta, dout, ld_dout, coef, am, pwv, pb, s);
   else
-    deform_bwd_point_dispatch<1>(lpr, grid, idx, w, m, vals, ld_vals, C, wv, beta, dout, ld_dout, coef, am, pwv, pb, s);
+    deform_bwd_point_dispatch<1>(plpr, grid, idx, w, m, vals, ld_vals, C, wv, beta, dout, ld_dout, coef, am, pwv, pb, s);
   launch(k_deform_bwd_reduce, dim3(static_cast<unsigned>(C + 1)), dim3(kBlock), 0, s, static_cast<const float*>(pwv),
          static_cast<const float*>(pb), static_cast<int64_t>(grid), C, dwv, dbeta);
   const int q = chunks <= lpr ? 1 : 2;
@@ -1238,9 +1244,7 @@ void launch_deform_slice(const int32_t* idx, const float* w, int64_t m, const vo
                          float* delta, float* plain, hipStream_t s) {
   if (m <= 0) return;
   const int chunks = C / (bf16 ? 8 : 4);
-  // 64 fp32 channels: 8 lanes of two chunks each, twice the points per wave
-  // for the same per-point work (indices, weights, the group's dot products)
-  const int lpr = !bf16 && chunks == 16 ? 8 : lanes_per_row(C, bf16 != 0);
+  const int lpr = point_lanes_per_row(C, bf16 != 0);
   ScopedKernelTimer tm("deform_slice", s);
   const bool two = chunks > lpr;
   if (bf16) {
