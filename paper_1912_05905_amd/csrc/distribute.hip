@@ -33,7 +33,7 @@ constexpr int kMeanSpan = kBlock;  // list entries per workgroup of the mean pas
 constexpr int kMaxC = 64;          // widest 1x1 layer
 constexpr int kMaxIn = 32;         // widest raw row (d + Cf): one channel per normalisation group
 constexpr int kPreStride = 2 * kMaxC;   // floats per normalisation table: scales, then shifts
-constexpr int kStatsMaxParts = 512;     // partials of the raw-row statistics
+constexpr int kStatsMaxParts = 2048;    // partials of the raw-row statistics
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -163,47 +163,57 @@ __device__ inline float row_coord(float g, double sc, double m) {
 }
 
 // ---- statistics of the raw distributed rows (first normalisation) ----
-// Workgroup w sums rows [w * rows_per, (w + 1) * rows_per): thread t takes
-// channel t % cp of rows t / cp, t / cp + slots, ...; the slots are then
-// added in order.  part[w] holds the cin sums, then the cin sums of squares.
+// Thread t of workgroup w takes the entries w * 256 + t, + 256 * grid, ...,
+// and sums channels [c0, c0 + 8) of their rows (for each block of 8 of the
+// cin channels in turn); the workgroup adds its 256 threads by a fixed tree.
+// part[w] holds the cin sums, then the cin sums of squares.
+constexpr int kStatsCh = 8;
 __global__ void __launch_bounds__(kBlock)
 k_dist_in_stats(const int32_t* __restrict__ entries, const int32_t* __restrict__ entry_vertex, int64_t total,
-                int64_t rows_per, const float* __restrict__ pos, double sc0, double sc1, double sc2,
-                const double4* __restrict__ mu, const float* __restrict__ feat, int64_t ld_feat, int cin, int cp,
-                double* __restrict__ part) {
+                const float* __restrict__ pos, double sc0, double sc1, double sc2, const double4* __restrict__ mu,
+                const float* __restrict__ feat, int64_t ld_feat, int cin, double* __restrict__ part) {
   __shared__ double sh[2][kBlock];
   const int t = threadIdx.x;
-  const int c = t % cp, slot = t / cp, slots = kBlock / cp;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per;
-  const int64_t r1 = min(r0 + rows_per, total);
-  double s = 0.0, ss = 0.0;
-  if (c < cin) {
-    const double sc = c == 0 ? sc0 : (c == 1 ? sc1 : sc2);
-    for (int64_t e = r0 + slot; e < r1; e += slots) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int c0 = 0; c0 < cin; c0 += kStatsCh) {
+    double s[kStatsCh], ss[kStatsCh];
+#pragma unroll
+    for (int i = 0; i < kStatsCh; ++i) s[i] = ss[i] = 0.0;
+    for (int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + t; e < total; e += stride) {
       const int64_t p = entries[e] >> 2;
-      float x;
-      if (c < 3) {
-        const double4 m = mu[entry_vertex[e]];
-        x = row_coord(pos[3 * p + c], sc, c == 0 ? m.x : (c == 1 ? m.y : m.z));
-      } else {
-        x = feat[p * ld_feat + (c - 3)];
+      double4 m = make_double4(0.0, 0.0, 0.0, 0.0);
+      if (c0 < 3) m = mu[entry_vertex[e]];
+#pragma unroll
+      for (int i = 0; i < kStatsCh; ++i) {
+        const int c = c0 + i;
+        if (c >= cin) break;
+        float x;
+        if (c == 0) x = row_coord(pos[3 * p], sc0, m.x);
+        else if (c == 1) x = row_coord(pos[3 * p + 1], sc1, m.y);
+        else if (c == 2) x = row_coord(pos[3 * p + 2], sc2, m.z);
+        else x = feat[p * ld_feat + (c - 3)];
+        s[i] += x;
+        ss[i] += static_cast<double>(x) * x;
       }
-      s += x;
-      ss += static_cast<double>(x) * x;
-    }
-  }
-  sh[0][t] = s;
-  sh[1][t] = ss;
-  __syncthreads();
-  if (t < cin) {
-    double a = 0.0, b = 0.0;
-    for (int sl = 0; sl < slots; ++sl) {
-      a += sh[0][sl * cp + t];
-      b += sh[1][sl * cp + t];
     }
     double* o = part + static_cast<int64_t>(blockIdx.x) * 2 * cin;
-    o[t] = a;
-    o[cin + t] = b;
+    for (int i = 0; i < kStatsCh && c0 + i < cin; ++i) {
+      __syncthreads();
+      sh[0][t] = s[i];
+      sh[1][t] = ss[i];
+      __syncthreads();
+      for (int off = kBlock / 2; off > 0; off >>= 1) {
+        if (t < off) {
+          sh[0][t] += sh[0][t + off];
+          sh[1][t] += sh[1][t + off];
+        }
+        __syncthreads();
+      }
+      if (t == 0) {
+        o[c0 + i] = sh[0][0];
+        o[cin + c0 + i] = sh[1][0];
+      }
+    }
   }
 }
 
@@ -707,14 +717,6 @@ k_dist_to_bf16(const float* __restrict__ src, int64_t n, int C, uint16_t* __rest
   }
 }
 
-void stats_parts(int64_t total, int cp, int64_t* nparts, int64_t* rows_per) {
-  const int slots = kBlock / cp;
-  int64_t rp = std::max<int64_t>(slots, (total + kStatsMaxParts - 1) / kStatsMaxParts);
-  rp = (rp + slots - 1) / slots * slots;
-  *rows_per = rp;
-  *nparts = std::max<int64_t>(1, (total + rp - 1) / rp);
-}
-
 int64_t mlp_grid(int64_t total) {
   const int64_t waves = (total + kMlpRange - 1) / kMlpRange;
   return (waves + kWaves - 1) / kWaves;
@@ -795,13 +797,10 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
            static_cast<const double4*>(mt));
   // the raw rows' statistics -> table 0
   const int cin = 3 + cf;
-  int cp = 4;
-  while (cp < cin) cp <<= 1;
-  int64_t np0, rp0;
-  stats_parts(total, cp, &np0, &rp0);
+  const int64_t np0 = std::min<int64_t>(kStatsMaxParts, (total + kBlock - 1) / kBlock);
   launch(k_dist_in_stats, dim3(static_cast<unsigned>(np0)), dim3(kBlock), 0, s, entries,
-         static_cast<const int32_t*>(ev), total, rp0, pos, scale[0], scale[1], scale[2],
-         static_cast<const double4*>(mu4), feat, ld_feat, cin, cp, part);
+         static_cast<const int32_t*>(ev), total, pos, scale[0], scale[1], scale[2], static_cast<const double4*>(mu4),
+         feat, ld_feat, cin, part);
   auto groups = [](int C) { return C <= 32 ? C : 32; };
   launch_gn_finalize(part, np0, cin, groups(cin), total, gamma, beta, eps, pre, s);
 

@@ -14,62 +14,71 @@ namespace lat {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kGnMaxParts = 512;
+constexpr int kGnMaxParts = 2048;
 
 // Workgroup w sums rows [w * rows_per, (w + 1) * rows_per): thread t takes
-// channels 4 (t % quads) .. + 3 of rows t / quads, t / quads + slots, ...
+// the EPT channels EPT (t % groups_of_c) .. + EPT - 1 (16 bytes: 8 bf16 or 4
+// fp32) of rows t / groups_of_c, + slots, ...; the slots are then added in
+// order.
 template <bool BF16>
 __global__ void __launch_bounds__(kBlock)
 k_gn_partial(const void* __restrict__ x, int64_t ld, int C, int64_t n, int64_t rows_per,
              double* __restrict__ part) {
-  __shared__ double sh[2][kBlock][4];
+  constexpr int EPT = BF16 ? 8 : 4;
+  __shared__ double sh[2][kBlock][EPT];
   const int t = threadIdx.x;
-  const int quads = C / 4;
+  const int quads = C / EPT;
   const int slots = kBlock / quads;
   const int q = t % quads, slot = t / quads;
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per;
   const int64_t r1 = min(r0 + rows_per, n);
-  double s[4] = {0.0, 0.0, 0.0, 0.0}, ss[4] = {0.0, 0.0, 0.0, 0.0};
+  double s[EPT], ss[EPT];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) s[i] = ss[i] = 0.0;
   if (slot < slots) {
     for (int64_t v = r0 + slot; v < r1; v += slots) {
-      float f[4];
+      float f[EPT];
       if constexpr (BF16) {
-        const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(x) + v * ld + 4 * q);
-        f[0] = __uint_as_float(u.x << 16);
-        f[1] = __uint_as_float(u.x & 0xffff0000u);
-        f[2] = __uint_as_float(u.y << 16);
-        f[3] = __uint_as_float(u.y & 0xffff0000u);
+        const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(x) + v * ld + EPT * q);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          f[2 * i] = __uint_as_float(w[i] << 16);
+          f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
       } else {
-        const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(x) + v * ld + 4 * q);
+        const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(x) + v * ld + EPT * q);
         f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < EPT; ++i) {
         s[i] += f[i];
         ss[i] += static_cast<double>(f[i]) * f[i];
       }
     }
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < EPT; ++i) {
     sh[0][t][i] = s[i];
     sh[1][t][i] = ss[i];
   }
   __syncthreads();
-  // thread q < quads: its 4 channels summed over the slots in order
+  // thread q < quads: its EPT channels summed over the slots in order
   if (t < quads) {
-    double a[4] = {0.0, 0.0, 0.0, 0.0}, b[4] = {0.0, 0.0, 0.0, 0.0};
+    double a[EPT], b[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) a[i] = b[i] = 0.0;
     for (int sl = 0; sl < slots; ++sl)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < EPT; ++i) {
         a[i] += sh[0][sl * quads + t][i];
         b[i] += sh[1][sl * quads + t][i];
       }
     double* p = part + static_cast<int64_t>(blockIdx.x) * 2 * C;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      p[4 * t + i] = a[i];
-      p[C + 4 * t + i] = b[i];
+    for (int i = 0; i < EPT; ++i) {
+      p[EPT * t + i] = a[i];
+      p[C + EPT * t + i] = b[i];
     }
   }
 }
@@ -112,8 +121,8 @@ k_gn_finalize(const double* __restrict__ part, int nparts, int C, int groups, in
   }
 }
 
-void gn_parts(int64_t n, int C, int64_t* nparts, int64_t* rows_per) {
-  const int slots = kBlock / (C / 4);
+void gn_parts(int64_t n, int C, int bf16, int64_t* nparts, int64_t* rows_per) {
+  const int slots = kBlock / (C / (bf16 ? 8 : 4));
   int64_t rp = std::max<int64_t>(slots, (n + kGnMaxParts - 1) / kGnMaxParts);
   rp = (rp + slots - 1) / slots * slots;
   *rows_per = rp;
@@ -132,7 +141,7 @@ int gn_max_channels() { return 4 * kBlock; }
 
 int64_t gn_workspace_bytes(int64_t n, int C) {
   int64_t np, rp;
-  gn_parts(n, C, &np, &rp);
+  gn_parts(n, C, 0, &np, &rp);   // fp32 splits into at least as many parts as bf16
   return np * 2 * C * static_cast<int64_t>(sizeof(double));
 }
 
@@ -140,7 +149,7 @@ void launch_gn_affine(const void* x, int64_t ld, int C, int bf16, int64_t n, int
                       const float* beta, float eps, float* pre, void* work, hipStream_t s) {
   ScopedKernelTimer tm("groupnorm", s);
   int64_t np, rp;
-  gn_parts(n, C, &np, &rp);
+  gn_parts(n, C, bf16, &np, &rp);
   double* part = static_cast<double*>(work);
   if (n > 0) {
     if (bf16) launch(k_gn_partial<true>, dim3(static_cast<unsigned>(np)), dim3(kBlock), 0, s, x, ld, C, n, rp, part);
