@@ -801,6 +801,90 @@ int orc_groupnorm(const double* X, int64_t n, int C, int64_t ldx, int groups, co
   return OK;
 }
 
+// Group Normalization backward: the gradient of orc_groupnorm for a scalar
+// loss with dL/dY = dY (n x C, dense), written from the forward's definition.
+// Per group g (N = n * C / groups values), xhat = (x - mean_g) inv_g with
+// inv_g = 1 / sqrt(var_g + eps), z = xhat gamma_c + beta_c, Y = max(z, 0)
+// (relu) or z:
+//   gz = dY, times [z > 0] with the ReLU (derivative taken as 0 at 0);
+//   dbeta_c = sum_v gz,  dgamma_c = sum_v gz xhat,  dxhat = gz gamma_c;
+//   dX = inv_g (dxhat - mean_g(dxhat) - xhat mean_g(dxhat xhat)),
+// the last line from differentiating mean_g and var_g through xhat.
+// dgamma / dbeta may be null.
+int orc_groupnorm_backward(const double* X, int64_t n, int C, int groups, const double* gamma,
+                           const double* beta, double eps, int relu, const double* dY, double* dX,
+                           double* dgamma, double* dbeta) {
+  if (n < 0 || C <= 0 || groups <= 0 || C % groups != 0 || !(eps >= 0.0)) return EINVAL_;
+  if (n > 0 && (!X || !dY || !dX)) return EINVAL_;
+  const int per = C / groups;
+  if (dgamma) std::fill(dgamma, dgamma + C, 0.0);
+  if (dbeta) std::fill(dbeta, dbeta + C, 0.0);
+  std::vector<double> xh(static_cast<size_t>(n) * per), gz(static_cast<size_t>(n) * per);
+  for (int g = 0; g < groups; ++g) {
+    const double cnt = static_cast<double>(n) * per;
+    if (cnt == 0) continue;
+    double mean = 0.0;
+    for (int64_t v = 0; v < n; ++v)
+      for (int c = g * per; c < (g + 1) * per; ++c) mean += X[v * C + c];
+    mean /= cnt;
+    double var = 0.0;
+    for (int64_t v = 0; v < n; ++v)
+      for (int c = g * per; c < (g + 1) * per; ++c) var += (X[v * C + c] - mean) * (X[v * C + c] - mean);
+    var /= cnt;
+    const double inv = 1.0 / std::sqrt(var + eps);
+    double m1 = 0.0, m2 = 0.0;   // sums of dxhat and dxhat * xhat over the group
+    for (int64_t v = 0; v < n; ++v)
+      for (int j = 0; j < per; ++j) {
+        const int c = g * per + j;
+        const double gm = gamma ? gamma[c] : 1.0;
+        const double x_hat = (X[v * C + c] - mean) * inv;
+        const double z = x_hat * gm + (beta ? beta[c] : 0.0);
+        const double d = relu && !(z > 0.0) ? 0.0 : dY[v * C + c];
+        xh[v * per + j] = x_hat;
+        gz[v * per + j] = d;
+        if (dbeta) dbeta[c] += d;
+        if (dgamma) dgamma[c] += d * x_hat;
+        m1 += d * gm;
+        m2 += d * gm * x_hat;
+      }
+    m1 /= cnt;
+    m2 /= cnt;
+    for (int64_t v = 0; v < n; ++v)
+      for (int j = 0; j < per; ++j) {
+        const int c = g * per + j;
+        const double dxh = gz[v * per + j] * (gamma ? gamma[c] : 1.0);
+        dX[v * C + c] = inv * (dxh - m1 - xh[v * per + j] * m2);
+      }
+  }
+  return OK;
+}
+
+// Backward of orc_deform_slice_classify for dL/dlogits = dZ (m x K): with f_p
+// the DeformSlice output of point p,
+//   dWc[j][c] = sum_p dZ[p][j] f_p[c],  dbc[j] = sum_p dZ[p][j],
+//   df_p = sum_j dZ[p][j] Wc[j]   (what reaches the DeformSlice output),
+// and the DeformSlice backward of df gives dX, dwv and dbeta.
+// dWc / dbc may be null.
+int orc_deform_slice_classify_backward(const orc_lattice* L, const double* X, int C, const double* wv,
+                                       double beta, const double* Wc, int K, const double* dZ, double* dX,
+                                       double* dwv, double* dbeta, double* dWc, double* dbc) {
+  if (!L || !X || !wv || !Wc || C <= 0 || K <= 0 || !dX || !dwv || !dbeta || (L->m > 0 && !dZ)) return EINVAL_;
+  std::vector<double> f(static_cast<size_t>(L->m) * C), df(static_cast<size_t>(L->m) * C, 0.0);
+  orc_deform_slice_raw(X, C, C, L->idx.data(), L->bary.data(), L->m, wv, beta, nullptr, f.data(), nullptr);
+  if (dWc) std::fill(dWc, dWc + static_cast<int64_t>(K) * C, 0.0);
+  if (dbc) std::fill(dbc, dbc + K, 0.0);
+  for (int64_t p = 0; p < L->m; ++p)
+    for (int j = 0; j < K; ++j) {
+      const double z = dZ[p * K + j];
+      if (dbc) dbc[j] += z;
+      for (int c = 0; c < C; ++c) {
+        if (dWc) dWc[static_cast<int64_t>(j) * C + c] += z * f[p * C + c];
+        df[p * C + c] += z * Wc[static_cast<int64_t>(j) * C + c];
+      }
+    }
+  return orc_deform_slice_backward(L, X, C, wv, beta, df.data(), dX, dwv, dbeta);
+}
+
 // Round to the nearest bfloat16 (8 significant bits), ties to even, in place.
 // Used where the bf16 pipeline stores activations; normal range only.
 void orc_round_bf16(double* x, int64_t n) {

@@ -62,6 +62,8 @@ def lib():
             "orc_slice_backward": (i32, [p, p, i32, p]),
             "orc_conv_backward": (i32, [p, p, p, i32, p, i32, i32, p, p, p, p, p]),
             "orc_deform_slice_backward": (i32, [p, p, i32, p, dbl, p, p, p, p]),
+            "orc_groupnorm_backward": (i32, [p, i64, i32, i32, p, p, dbl, i32, p, p, p, p]),
+            "orc_deform_slice_classify_backward": (i32, [p, p, i32, p, dbl, p, i32, p, p, p, p, p, p]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -282,6 +284,22 @@ class Lattice:
                                                _ptr(dwv), _ptr(dbeta)))
         return dX, dwv, float(dbeta[0])
 
+    def deform_slice_classify_backward(self, X, wv, beta, Wc, dZ):
+        """Gradients of deform_slice_classify(X, wv, beta, Wc, bc) for
+        dL/dlogits = dZ: (dX, dwv, dbeta, dWc, dbc)."""
+        X, wv, Wc, dZ = _f64(X), _f64(wv), _f64(Wc), _f64(dZ)
+        Cc, K = X.shape[1], Wc.shape[0]
+        assert Wc.shape[1] == Cc and dZ.shape == (self.m, K)
+        dX = np.zeros((self.n, Cc), np.float64)
+        dwv = np.zeros(Cc, np.float64)
+        dbeta = np.zeros(1, np.float64)
+        dWc = np.zeros((K, Cc), np.float64)
+        dbc = np.zeros(K, np.float64)
+        _check(lib().orc_deform_slice_classify_backward(self._h, _ptr(X), Cc, _ptr(wv), float(beta), _ptr(Wc), K,
+                                                        _ptr(dZ), _ptr(dX), _ptr(dwv), _ptr(dbeta), _ptr(dWc),
+                                                        _ptr(dbc)))
+        return dX, dwv, float(dbeta[0]), dWc, dbc
+
     def slice(self, X, pts=None):
         X = _f64(X)
         Cc = X.shape[1]
@@ -325,6 +343,22 @@ def groupnorm(X, groups, gamma=None, beta=None, eps=1e-5, relu=False):
     _check(lib().orc_groupnorm(_ptr(X), n, Cc, Cc, int(groups), _ptr(g), _ptr(b), float(eps), int(bool(relu)),
                                _ptr(Y), Cc))
     return Y
+
+
+def groupnorm_backward(X, dY, groups, gamma=None, beta=None, eps=1e-5, relu=False):
+    """Gradients of groupnorm(X, groups, gamma, beta, eps, relu) for
+    dL/dY = dY: (dX, dgamma, dbeta)."""
+    X, dY = _f64(X), _f64(dY)
+    n, Cc = X.shape
+    assert dY.shape == X.shape
+    g = None if gamma is None else _f64(gamma)
+    b = None if beta is None else _f64(beta)
+    dX = np.zeros_like(X)
+    dg = np.zeros(Cc, np.float64)
+    db = np.zeros(Cc, np.float64)
+    _check(lib().orc_groupnorm_backward(_ptr(X), n, Cc, int(groups), _ptr(g), _ptr(b), float(eps), int(bool(relu)),
+                                        _ptr(dY), _ptr(dX), _ptr(dg), _ptr(db)))
+    return dX, dg, db
 
 
 def slice_raw(X, idx, w):

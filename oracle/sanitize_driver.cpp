@@ -48,6 +48,12 @@ int orc_conv_backward(const orc_lattice* dst, const orc_lattice* src, const doub
                       int cout, int relu, const double* Y, const double* dY, double* dX, double* dW, double* dbias);
 int orc_deform_slice_backward(const orc_lattice* L, const double* X, int C, const double* wv, double beta,
                               const double* dOut, double* dX, double* dwv, double* dbeta);
+int orc_groupnorm_backward(const double* X, int64_t n, int C, int groups, const double* gamma,
+                           const double* beta, double eps, int relu, const double* dY, double* dX,
+                           double* dgamma, double* dbeta);
+int orc_deform_slice_classify_backward(const orc_lattice* L, const double* X, int C, const double* wv,
+                                       double beta, const double* Wc, int K, const double* dZ, double* dX,
+                                       double* dwv, double* dbeta, double* dWc, double* dbc);
 void orc_round_bf16(double* x, int64_t n);
 }
 
@@ -147,6 +153,16 @@ int main() {
        "strided backward, bias only");
   need(orc_deform_slice_backward(L0, X.data(), C, wv.data(), 0.1, dOut.data(), dXs.data(), dwv.data(), &dbeta),
        "deform backward");
+  auto gg = vec(C), gb = vec(C);
+  std::vector<double> dXg(n0 * C), dgg(C), dgb(C);
+  need(orc_groupnorm_backward(X.data(), n0, C, 4, gg.data(), gb.data(), 1e-5, 1, dX.data(), dXg.data(), dgg.data(),
+                              dgb.data()),
+       "groupnorm backward");
+  auto dZ = vec(m * K);
+  std::vector<double> dWk(K * C), dbk(K);
+  need(orc_deform_slice_classify_backward(L0, X.data(), C, wv.data(), 0.1, Wc.data(), K, dZ.data(), dXs.data(),
+                                          dwv.data(), &dbeta, dWk.data(), dbk.data()),
+       "classify backward");
   orc_round_bf16(X.data(), n0 * C);
   orc_destroy(E);
   orc_destroy(L2);

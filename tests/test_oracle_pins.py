@@ -717,3 +717,113 @@ def test_deform_slice_classify_special_cases(oracle_mod):
     lhs = L.deform_slice_classify(X, wv, 0.2, W1 + W2)
     rhs = L.deform_slice_classify(X, wv, 0.2, W1) + L.deform_slice_classify(X, wv, 0.2, W2)
     assert np.abs(lhs - rhs).max() < 1e-12
+
+
+# ----------------------------------------------------------------------------
+# Backward of GroupNorm (+ ReLU), of the pre-activated convolution and of the
+# fused classifier: finite differences of the oracle's forwards, invariances
+# ----------------------------------------------------------------------------
+def test_groupnorm_backward_finite_differences(oracle_mod):
+    """L = <GN(X), G> (with and without the ReLU, with gamma and beta):
+    central differences in random directions of X, gamma and beta match the
+    gradients."""
+    h = 1e-6
+    rng = np.random.default_rng(71)
+    for n, C, groups, relu in ((40, 8, 2, False), (40, 8, 8, True), (25, 12, 1, True), (30, 16, 4, False)):
+        X = rng.normal(size=(n, C)) * rng.uniform(0.5, 2.0, size=C) + rng.normal(size=C)
+        gam, bet = rng.normal(size=C), rng.normal(size=C) * 0.5
+        G = rng.normal(size=(n, C))
+        dX, dg, db = oracle_mod.groupnorm_backward(X, G, groups, gam, bet, 1e-3, relu)
+        loss = lambda X_, g_, b_: _dot(oracle_mod.groupnorm(X_, groups, g_, b_, 1e-3, relu), G)
+        for _ in range(3):
+            D = rng.normal(size=X.shape)
+            fd = (loss(X + h * D, gam, bet) - loss(X - h * D, gam, bet)) / (2 * h)
+            assert abs(fd - _dot(dX, D)) <= 1e-6 * max(1.0, abs(fd)), (n, C, groups, relu, fd, _dot(dX, D))
+            e = rng.normal(size=C)
+            fd = (loss(X, gam + h * e, bet) - loss(X, gam - h * e, bet)) / (2 * h)
+            assert abs(fd - _dot(dg, e)) <= 1e-6 * max(1.0, abs(fd)), (n, C, groups, relu)
+            fd = (loss(X, gam, bet + h * e) - loss(X, gam, bet - h * e)) / (2 * h)
+            assert abs(fd - _dot(db, e)) <= 1e-6 * max(1.0, abs(fd)), (n, C, groups, relu)
+
+
+def test_groupnorm_backward_invariances(oracle_mod):
+    """GN's output does not change when one group's inputs are shifted by a
+    constant, so each group's input gradient sums to zero (any loss, ReLU or
+    not); with eps = 0 it does not change when a group is scaled either, so
+    sum (x - mean_g) dX = 0 per group.  Two values of a group normalise to
+    -1 and +1 whatever they are: their gradient is zero."""
+    rng = np.random.default_rng(72)
+    X = rng.normal(size=(60, 16)) * 2 + 3
+    G = rng.normal(size=(60, 16))
+    gam, bet = rng.normal(size=16), rng.normal(size=16)
+    for groups, relu in ((4, False), (4, True), (16, True), (1, False)):
+        per = 16 // groups
+        for eps in (1e-5, 0.0):
+            dX, _, _ = oracle_mod.groupnorm_backward(X, G, groups, gam, bet, eps, relu)
+            for g in range(groups):
+                blk = slice(g * per, (g + 1) * per)
+                scale = np.abs(dX[:, blk]).sum()
+                assert abs(dX[:, blk].sum()) <= 1e-12 * scale
+                if eps == 0.0:
+                    xc = X[:, blk] - X[:, blk].mean()
+                    assert abs((xc * dX[:, blk]).sum()) <= 1e-12 * np.abs(xc * dX[:, blk]).sum()
+    dX, dg, db = oracle_mod.groupnorm_backward(np.array([[0.0], [2.0]]), np.array([[1.0], [0.0]]), 1, eps=0.0)
+    assert np.abs(dX).max() < 1e-15
+    assert dg[0] == -1.0 and db[0] == 1.0       # sum dY xhat with xhat = (-1, +1); sum dY
+
+
+def test_preact_conv_backward_composite(oracle_mod):
+    """L = <conv(relu(GN(X)), W) + b, G> over the three forms (1-hop,
+    strided, Upsample): the chain conv backward (on relu(GN(X))) then GN
+    backward (with the ReLU) matches central differences of the forward in
+    X, W, b, gamma and beta."""
+    h = 1e-6
+    rng = np.random.default_rng(73)
+    for name, dst, src, fwd in _conv_forms(oracle_mod, 73):
+        C, Co, groups = 8, 5, 4
+        X = rng.normal(size=(src.n, C)) * 1.5 + 0.5
+        W = rng.normal(size=(9, C, Co))
+        b = rng.normal(size=Co) * 0.5
+        gam, bet = rng.normal(size=C), rng.normal(size=C) * 0.3
+        G = rng.normal(size=(dst.n, Co))
+        A = oracle_mod.groupnorm(X, groups, gam, bet, 1e-5, relu=True)
+        dA, dW, db = dst.conv_backward(src, A, W, G)
+        dX, dg, dbe = oracle_mod.groupnorm_backward(X, dA, groups, gam, bet, 1e-5, relu=True)
+
+        def loss(X_, W_, b_, g_, be_):
+            return _dot(fwd(oracle_mod.groupnorm(X_, groups, g_, be_, 1e-5, relu=True), W_, b_, False), G)
+
+        base = (X, W, b, gam, bet)
+        for i, grad in enumerate((dX, dW, db, dg, dbe)):
+            D = rng.normal(size=base[i].shape)
+            up = list(base)
+            dn = list(base)
+            up[i] = base[i] + h * D
+            dn[i] = base[i] - h * D
+            fd = (loss(*up) - loss(*dn)) / (2 * h)
+            assert abs(fd - _dot(grad, D)) <= 1e-6 * max(1.0, abs(fd)), (name, i, fd, _dot(grad, D))
+
+
+def test_deform_slice_classify_backward_finite_differences(oracle_mod):
+    """L = <classify(X, wv, beta, Wc, bc), Z>: central differences in random
+    directions of X, wv, Wc and bc, and in beta, match the gradients."""
+    h = 1e-6
+    L = oracle_mod.Lattice.create(_tiny_cloud(74, 250, 0.6), np.full(3, 0.1, np.float32))
+    rng = np.random.default_rng(74)
+    C, K = 8, 5
+    X = rng.normal(size=(L.n, C))
+    wv = rng.normal(size=C) * 0.5
+    Wc, bc = rng.normal(size=(K, C)), rng.normal(size=K)
+    Z = rng.normal(size=(L.m, K))
+    dX, dwv, dbeta, dWc, dbc = L.deform_slice_classify_backward(X, wv, 0.15, Wc, Z)
+    loss = lambda X_, w_, be_, Wc_, bc_: _dot(L.deform_slice_classify(X_, w_, be_, Wc_, bc_), Z)
+    base = (X, wv, 0.15, Wc, bc)
+    for i, grad in enumerate((dX, dwv, dbeta, dWc, dbc)):
+        D = rng.normal(size=np.shape(base[i])) if i != 2 else 1.0
+        up = list(base)
+        dn = list(base)
+        up[i] = base[i] + h * D
+        dn[i] = base[i] - h * D
+        fd = (loss(*up) - loss(*dn)) / (2 * h)
+        an = _dot(grad, D) if i != 2 else grad
+        assert abs(fd - an) <= 1e-6 * max(1.0, abs(fd)), (i, fd, an)
