@@ -372,6 +372,38 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
                           float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream);
 
 /*
+ * Backward of the pre-activated convolution (Implementation: Group
+ * Normalization with a ReLU before every convolution) for
+ *   Y = act(conv(relu(GN(X)), W) + bias)
+ * as lattice_conv_preact / lattice_refine_preact compute it (1-hop,
+ * strided or Upsample: the form follows from dst and src as for
+ * lattice_conv_backward), given dY = dL/dY:
+ *   A = relu(GN(X)) is recomputed exactly as the forward applied it, the
+ *   convolution's backward on A gives dW, dbias and dA, and the GroupNorm +
+ *   ReLU backward of dA gives
+ *     dbeta_c = sum_v g,  dgamma_c = sum_v g xhat,  g = dA [GN(X) > 0],
+ *     dX = inv_g (gamma_c g - mean_g(gamma g) - xhat mean_g(gamma g xhat))
+ *   with xhat = (X - mean_g) inv_g, inv_g = 1 / sqrt(var_g + eps), the
+ *   group means over all rows of src and the group's channels (sums in
+ *   float64, fixed order).
+ *   X_dev      n_src x Cin float32, row stride ld_X (0 = Cin): the input the
+ *              forward normalised; Cin <= 1024, a multiple of 4.
+ *   groups, gamma_dev, beta_dev, eps   as for lattice_conv_preact.
+ *   W_dev, Cout, flags, Y_dev, dY_dev  as for lattice_conv_backward (Y is
+ *              the output before any residual was added; a residual's own
+ *              gradient is dY itself).
+ *   dX_dev     n_src x Cin, row stride ld_dX, or NULL; must not overlap X.
+ *   dW_dev, dbias_dev  as for lattice_conv_backward, or NULL.
+ *   dgamma_dev, dbeta_dev  Cin float32 each, or NULL.
+ * float32 only.  Uses work space of O(n_src Cin) bytes from the pool.
+ */
+int lattice_conv_preact_backward(lattice_t dst, lattice_t src, const float* X_dev, int64_t ld_X, int Cin, int groups,
+                                 const float* gamma_dev, const float* beta_dev, float eps, const float* W_dev,
+                                 int Cout, int flags, const float* Y_dev, int64_t ld_Y, const float* dY_dev,
+                                 int64_t ld_dY, float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev,
+                                 float* dgamma_dev, float* dbeta_dev, hipStream_t stream);
+
+/*
  * DeformSlice backward (Eq. (deformSlice) with the equivariant offset
  * regressor) for out_p = sum_k (b_pk + db_pk) x_k, db_pk = tanh(beta +
  * (b_pk x_k - max_j b_pj x_j) . wv), given dOut = dL/dout:
@@ -387,6 +419,27 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
 int lattice_deform_slice_backward(lattice_t L, const float* vals_dev, int64_t ld_vals, int C, const float* wv_dev,
                                   float beta, const float* dOut_dev, int64_t ld_dOut, float* dvals_dev,
                                   int64_t ld_dvals, float* dwv_dev, float* dbeta_dev, hipStream_t stream);
+
+/*
+ * Backward of DeformSlice fused with the linear classifier (Implementation:
+ * the last linear layer fused with DeformSlice) for logits_p = Wc f_p + bc
+ * as lattice_deform_slice_classify computes it, given dlogits = dL/dlogits
+ * (m x K float32, row stride ld_dlogits, 0 = K):
+ *   dWc = sum_p dlogits_p f_p^T (K x C), dbc = sum_p dlogits_p (K), each
+ *   summed over chunks of points added in a fixed order; df_p = Wc^T
+ *   dlogits_p, and the DeformSlice backward of df (as
+ *   lattice_deform_slice_backward) gives dvals, dwv and dbeta.
+ * f is recomputed from vals (float32, as lattice_deform_slice) and not
+ * stored by the caller.  dWc_dev / dbc_dev may be NULL; the other outputs
+ * are required.  Limits as lattice_deform_slice_classify (K <= 64, K x C <=
+ * 16384, C <= 512); dvals must not overlap vals.  Uses work space of
+ * O(m C) bytes from the pool.
+ */
+int lattice_deform_slice_classify_backward(lattice_t L, const float* vals_dev, int64_t ld_vals, int C,
+                                           const float* wv_dev, float beta, const float* Wc_dev, int K,
+                                           const float* dlogits_dev, int64_t ld_dlogits, float* dvals_dev,
+                                           int64_t ld_dvals, float* dwv_dev, float* dbeta_dev, float* dWc_dev,
+                                           float* dbc_dev, hipStream_t stream);
 
 /*
  * Timing of the library's kernels with HIP events on the launch stream, for

@@ -1357,12 +1357,13 @@ int lattice_slice_backward(lattice_t L, const float* dOut_dev, int64_t ld_dOut, 
   return check_launch("slice backward");
 }
 
-int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int64_t ld_X, int Cin, const float* W_dev,
-                          int Cout, int flags, const float* Y_dev, int64_t ld_Y, const float* dY_dev, int64_t ld_dY,
-                          float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream) {
+namespace {
+
+// The body of lattice_conv_backward once both lattices are in use on stream.
+int conv_backward_impl(lattice_t dst, lattice_t src, const float* X_dev, int64_t ld_X, int Cin, const float* W_dev,
+                       int Cout, int flags, const float* Y_dev, int64_t ld_Y, const float* dY_dev, int64_t ld_dY,
+                       float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream) {
   int st;
-  if ((st = use(dst, stream)) != LAT_OK) return st;
-  if ((st = use(src, stream)) != LAT_OK) return st;
   // the forward's table (dst rows, src values) and the adjoint's (src rows,
   // dst values)
   const int32_t *fwd, *adj, *adj_rows = nullptr;
@@ -1436,6 +1437,66 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
   return check_launch("conv backward");
 }
 
+}  // namespace
+
+int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int64_t ld_X, int Cin, const float* W_dev,
+                          int Cout, int flags, const float* Y_dev, int64_t ld_Y, const float* dY_dev, int64_t ld_dY,
+                          float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream) {
+  int st;
+  if ((st = use(dst, stream)) != LAT_OK) return st;
+  if ((st = use(src, stream)) != LAT_OK) return st;
+  return conv_backward_impl(dst, src, X_dev, ld_X, Cin, W_dev, Cout, flags, Y_dev, ld_Y, dY_dev, ld_dY, dX_dev, ld_dX,
+                            dW_dev, dbias_dev, stream);
+}
+
+int lattice_conv_preact_backward(lattice_t dst, lattice_t src, const float* X_dev, int64_t ld_X, int Cin, int groups,
+                                 const float* gamma_dev, const float* beta_dev, float eps, const float* W_dev,
+                                 int Cout, int flags, const float* Y_dev, int64_t ld_Y, const float* dY_dev,
+                                 int64_t ld_dY, float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev,
+                                 float* dgamma_dev, float* dbeta_dev, hipStream_t stream) {
+  int st;
+  if ((st = use(dst, stream)) != LAT_OK) return st;
+  if ((st = use(src, stream)) != LAT_OK) return st;
+  if (!(dst == src || dst->parent == src || src->parent == dst))
+    return fail(LAT_ELEVEL, "dst and src must be one lattice, or one a coarsening of the other");
+  if (groups <= 0 || Cin % groups != 0) return fail(LAT_EINVAL, "groups must divide Cin");
+  if (!(eps > 0.f) || !std::isfinite(eps)) return fail(LAT_EINVAL, "eps must be positive and finite");
+  if (Cin > gn_max_channels())
+    return fail(LAT_EUNSUPPORTED, "the pre-activated convolution's backward takes at most " +
+                                      std::to_string(gn_max_channels()) + " input channels");
+  if (ld_X == 0) ld_X = Cin;
+  if (ld_dX == 0) ld_dX = Cin;
+  const int64_t n_in = src->n;
+  if ((st = check_matrix(X_dev, ld_X, Cin, LAT_F32, "X", n_in > 0)) != LAT_OK) return st;
+  if (dX_dev) {
+    if ((st = check_matrix(dX_dev, ld_dX, Cin, LAT_F32, "dX", n_in > 0)) != LAT_OK) return st;
+    if (n_in > 0 && overlaps(dX_dev, sizeof(float) * static_cast<size_t>((n_in - 1) * ld_dX + Cin), X_dev,
+                             sizeof(float) * static_cast<size_t>((n_in - 1) * ld_X + Cin)))
+      return fail(LAT_EINVAL, "dX and X overlap");
+  }
+  const bool need_dA = dX_dev || dgamma_dev || dbeta_dev;
+  if (!need_dA && !dW_dev && !dbias_dev) return LAT_OK;
+  const size_t nc = static_cast<size_t>(n_in) * Cin;
+  Scratch pre, stats, work, act, dact, coef;
+  if ((st = pre.get(sizeof(float) * 2 * static_cast<size_t>(Cin), stream)) != LAT_OK) return st;
+  if ((st = stats.get(sizeof(double) * 2 * static_cast<size_t>(groups), stream)) != LAT_OK) return st;
+  if ((st = work.get(static_cast<size_t>(gn_workspace_bytes(n_in, Cin)), stream)) != LAT_OK) return st;
+  if ((st = act.get(sizeof(float) * std::max<size_t>(nc, 4), stream)) != LAT_OK) return st;
+  if (need_dA && (st = dact.get(sizeof(float) * std::max<size_t>(nc, 4), stream)) != LAT_OK) return st;
+  if ((st = coef.get(sizeof(float) * 4 * static_cast<size_t>(Cin), stream)) != LAT_OK) return st;
+  // the forward's pre-activated input, then the convolution's backward on it
+  launch_gn_affine(X_dev, ld_X, Cin, 0, n_in, groups, gamma_dev, beta_dev, eps, pre.as<float>(), work.p, stream,
+                   stats.as<double>());
+  launch_gn_relu_apply(X_dev, ld_X, Cin, n_in, pre.as<float>(), act.as<float>(), Cin, stream);
+  if ((st = conv_backward_impl(dst, src, act.as<float>(), Cin, Cin, W_dev, Cout, flags, Y_dev, ld_Y, dY_dev, ld_dY,
+                               need_dA ? dact.as<float>() : nullptr, Cin, dW_dev, dbias_dev, stream)) != LAT_OK)
+    return st;
+  if (need_dA)
+    launch_gn_backward(X_dev, ld_X, dact.as<float>(), Cin, Cin, groups, n_in, gamma_dev, pre.as<float>(),
+                       stats.as<double>(), dgamma_dev, dbeta_dev, coef.as<float>(), dX_dev, ld_dX, work.p, stream);
+  return check_launch("pre-activated conv backward");
+}
+
 int lattice_deform_slice_backward(lattice_t L, const float* vals_dev, int64_t ld_vals, int C, const float* wv_dev,
                                   float beta, const float* dOut_dev, int64_t ld_dOut, float* dvals_dev,
                                   int64_t ld_dvals, float* dwv_dev, float* dbeta_dev, hipStream_t stream) {
@@ -1465,6 +1526,54 @@ int lattice_deform_slice_backward(lattice_t L, const float* vals_dev, int64_t ld
                                L->total, vals_dev, ld_vals, C, wv_dev, beta, dOut_dev, ld_dOut, dvals_dev, ld_dvals,
                                dwv_dev, dbeta_dev, work.p, stream);
   return check_launch("deform slice backward");
+}
+
+int lattice_deform_slice_classify_backward(lattice_t L, const float* vals_dev, int64_t ld_vals, int C,
+                                           const float* wv_dev, float beta, const float* Wc_dev, int K,
+                                           const float* dlogits_dev, int64_t ld_dlogits, float* dvals_dev,
+                                           int64_t ld_dvals, float* dwv_dev, float* dbeta_dev, float* dWc_dev,
+                                           float* dbc_dev, hipStream_t stream) {
+  int st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
+  if (ld_vals == 0) ld_vals = C;
+  if (ld_dvals == 0) ld_dvals = C;
+  if (ld_dlogits == 0) ld_dlogits = K;
+  if ((st = check_matrix(vals_dev, ld_vals, C, LAT_F32, "vals", L->n > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(dvals_dev, ld_dvals, C, LAT_F32, "dvals", L->n > 0)) != LAT_OK) return st;
+  if (!wv_dev || !Wc_dev || !dwv_dev || !dbeta_dev) return fail(LAT_EINVAL, "wv, Wc, dwv and dbeta must not be null");
+  if (L->m > 0 && !dlogits_dev) return fail(LAT_EINVAL, "dlogits is null");
+  if (!std::isfinite(beta)) return fail(LAT_EINVAL, "beta must be finite");
+  if (K <= 0 || K > deform_classify_max_classes())
+    return fail(LAT_EUNSUPPORTED, "K must be in [1, " + std::to_string(deform_classify_max_classes()) + "]");
+  if (ld_dlogits < K) return fail(LAT_EINVAL, "ld_dlogits < K");
+  if (C > deform_max_channels(false) || static_cast<int64_t>(K) * C > deform_classify_max_weights())
+    return fail(LAT_EUNSUPPORTED, "the classifier takes at most " + std::to_string(deform_classify_max_weights()) +
+                                      " weights (K x C) and DeformSlice's channel limit");
+  if (!aligned16(Wc_dev)) return fail(LAT_EINVAL, "Wc must be 16-byte aligned");
+  if (L->n > 0 &&
+      overlaps(dvals_dev, sizeof(float) * static_cast<size_t>((L->n - 1) * ld_dvals + C), vals_dev,
+               sizeof(float) * static_cast<size_t>((L->n - 1) * ld_vals + C)))
+    return fail(LAT_EINVAL, "dvals and vals overlap");
+  const size_t mc = std::max<size_t>(static_cast<size_t>(L->m) * C, 4);
+  Scratch feat, dfeat, part, work;
+  if ((st = feat.get(sizeof(float) * mc, stream)) != LAT_OK) return st;
+  if ((st = dfeat.get(sizeof(float) * mc, stream)) != LAT_OK) return st;
+  if ((st = part.get(sizeof(float) * static_cast<size_t>(classify_backward_partial_floats(L->m, K, C)), stream)) !=
+      LAT_OK)
+    return st;
+  if ((st = work.get(static_cast<size_t>(deform_backward_workspace_bytes(L->m, C, L->total, L->chunk)), stream)) !=
+      LAT_OK)
+    return st;
+  // the forward's per-point features, then their gradient and the classifier's
+  launch_deform_slice(L->idx, L->w, L->m, vals_dev, ld_vals, C, 0, wv_dev, beta, feat.as<float>(), nullptr, nullptr,
+                      stream);
+  launch_classify_backward(dlogits_dev, ld_dlogits, Wc_dev, K, C, L->m, feat.as<float>(), dfeat.as<float>(), dWc_dev,
+                           dbc_dev, part.as<float>(), stream);
+  launch_deform_slice_backward(L->idx, L->w, L->m, L->offsets, L->entries, L->chunk_first, L->chunk, L->nmax,
+                               L->total, vals_dev, ld_vals, C, wv_dev, beta, dfeat.as<float>(), C, dvals_dev,
+                               ld_dvals, dwv_dev, dbeta_dev, work.p, stream);
+  return check_launch("deform slice classify backward");
 }
 
 int lattice_timing_enable(const char* name, int enable) {

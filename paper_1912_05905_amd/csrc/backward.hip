@@ -13,6 +13,10 @@
 //             gathered GEMM that reduces over vertices (k_conv_wgrad, split
 //             over vertex chunks, partials added in chunk order).
 // A ReLU in the forward masks dL/dY with Y > 0 first (derivative 0 at 0).
+//   classifier fused with DeformSlice -> with f_p the DeformSlice output and
+//             z_p = dL/dlogits_p: df_p = sum_j z_pj Wc[j] (then the
+//             DeformSlice backward), dWc = sum_p z_p f_p^T, dbc = sum_p z_p
+//             (point chunks, partials added in chunk order).
 #include <algorithm>
 
 #include "lattice_internal.h"
@@ -238,6 +242,102 @@ void wgrad_chunks(int64_t n_out, int tiles, int64_t* chunks, int64_t* V) {
   *chunks = (n_out + v - 1) / v;
 }
 
+
+// ---- classifier backward ----
+constexpr int kClsPts = 32;        // points staged per step of k_cls_wgrad
+constexpr int kClsMaxChunks = 1024;
+
+// df_p[c] = sum_j z_pj Wc[j][c]: one thread per (point, 4 channels).
+__global__ void __launch_bounds__(kBlock)
+k_cls_dfeat(const float* __restrict__ z, int64_t ld_z, const float* __restrict__ Wc, int K, int C, int64_t m,
+            float* __restrict__ df) {
+  const int quads = C / 4;
+  const int64_t total = m * quads;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < total;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int64_t p = i / quads;
+    const int c = 4 * static_cast<int>(i - p * quads);
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = 0; j < K; ++j) {
+      const float zj = z[p * ld_z + j];
+      const float4 w = *reinterpret_cast<const float4*>(Wc + static_cast<int64_t>(j) * C + c);
+      a.x = fmaf(zj, w.x, a.x);
+      a.y = fmaf(zj, w.y, a.y);
+      a.z = fmaf(zj, w.z, a.z);
+      a.w = fmaf(zj, w.w, a.w);
+    }
+    *reinterpret_cast<float4*>(df + p * C + c) = a;
+  }
+}
+
+// Workgroup w: over its chunk of points, part[w][j C + c] = sum_p z_pj f_pc
+// and part[w][K C + j] = sum_p z_pj, points in order; rows of z and f are
+// staged kClsPts at a time in LDS.  Thread t owns outputs t, t + 256, ...
+template <int NO>
+__global__ void __launch_bounds__(kBlock)
+k_cls_wgrad(const float* __restrict__ z, int64_t ld_z, const float* __restrict__ f, int K, int C, int64_t m,
+            int64_t chunk, float* __restrict__ part) {
+  extern __shared__ float sm[];
+  float* sz = sm;                    // [kClsPts][K]
+  float* sf = sm + kClsPts * K;      // [kClsPts][C]
+  const int t = threadIdx.x;
+  const int nout = K * C + K;
+  const int64_t p0 = static_cast<int64_t>(blockIdx.x) * chunk;
+  const int64_t p1 = min(p0 + chunk, m);
+  float acc[NO];
+#pragma unroll
+  for (int k = 0; k < NO; ++k) acc[k] = 0.f;
+  for (int64_t pb = p0; pb < p1; pb += kClsPts) {
+    const int np = static_cast<int>(min<int64_t>(kClsPts, p1 - pb));
+    __syncthreads();
+    for (int e = t; e < np * K; e += kBlock) sz[e] = z[(pb + e / K) * ld_z + e % K];
+    for (int e = t; e < np * (C / 4); e += kBlock) {
+      const int r = e / (C / 4), q = e - r * (C / 4);
+      *reinterpret_cast<float4*>(sf + r * C + 4 * q) = *reinterpret_cast<const float4*>(f + (pb + r) * C + 4 * q);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < NO; ++k) {
+      const int o = t + k * kBlock;
+      if (o >= nout) break;
+      float a = acc[k];
+      if (o < K * C) {
+        const int j = o / C, c = o - j * C;
+        for (int r = 0; r < np; ++r) a = fmaf(sz[r * K + j], sf[r * C + c], a);
+      } else {
+        for (int r = 0; r < np; ++r) a += sz[r * K + (o - K * C)];
+      }
+      acc[k] = a;
+    }
+  }
+  float* dst = part + static_cast<int64_t>(blockIdx.x) * nout;
+#pragma unroll
+  for (int k = 0; k < NO; ++k)
+    if (t + k * kBlock < nout) dst[t + k * kBlock] = acc[k];
+}
+
+// out[o] = sum over the chunks of part[w][o], in chunk order.
+__global__ void __launch_bounds__(kBlock)
+k_cls_reduce(const float* __restrict__ part, int chunks, int K, int C, float* __restrict__ dWc,
+             float* __restrict__ dbc) {
+  const int nout = K * C + K;
+  const int o = blockIdx.x * kBlock + threadIdx.x;
+  if (o >= nout) return;
+  float a = 0.f;
+  for (int w = 0; w < chunks; ++w) a += part[static_cast<int64_t>(w) * nout + o];
+  if (o < K * C) {
+    if (dWc) dWc[o] = a;
+  } else if (dbc) {
+    dbc[o - K * C] = a;
+  }
+}
+
+void cls_chunks(int64_t m, int64_t* chunk, int* chunks) {
+  int64_t c = std::max<int64_t>(kClsPts, (m + kClsMaxChunks - 1) / kClsMaxChunks);
+  c = (c + kClsPts - 1) / kClsPts * kClsPts;
+  *chunk = c;
+  *chunks = static_cast<int>(std::max<int64_t>(1, (m + c - 1) / c));
+}
 }  // namespace
 
 void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, const float* wsum, int64_t n,
@@ -278,6 +378,54 @@ void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const flo
   // with no output vertex (chunks = 0) the sums below are zero
   launch(k_wgrad_reduce, dim3(blocks_for((count + Cout) / 4)), dim3(kBlock), 0, s, static_cast<const float*>(part),
          static_cast<const float*>(part_b), chunks, count, Cout, dW, dbias);
+}
+
+}  // namespace lat
+
+namespace lat {
+
+int64_t classify_backward_partial_floats(int64_t m, int K, int C) {
+  int64_t chunk;
+  int chunks;
+  cls_chunks(m, &chunk, &chunks);
+  return static_cast<int64_t>(chunks) * (static_cast<int64_t>(K) * C + K);
+}
+
+void launch_classify_backward(const float* z, int64_t ld_z, const float* Wc, int K, int C, int64_t m, const float* f,
+                              float* df, float* dWc, float* dbc, float* part, hipStream_t s) {
+  ScopedKernelTimer tm("classify_bwd", s);
+  if (m > 0) {
+    const int64_t b = (m * (C / 4) + kBlock - 1) / kBlock;
+    launch(k_cls_dfeat, dim3(static_cast<unsigned>(std::min<int64_t>(b, 8192))), dim3(kBlock), 0, s, z, ld_z, Wc, K,
+           C, m, df);
+  }
+  if (!dWc && !dbc) return;
+  const int nout = K * C + K;
+  int64_t chunk;
+  int chunks;
+  cls_chunks(m, &chunk, &chunks);
+  if (m > 0) {
+    const size_t lds = sizeof(float) * kClsPts * static_cast<size_t>(K + C);
+    auto go = [&](auto no_c) {
+      constexpr int NO = decltype(no_c)::value;
+      static bool lds_limit_set = false;
+      if (!lds_limit_set) {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_cls_wgrad<NO>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  static_cast<int>(sizeof(float) * kClsPts * (64 + 512)));
+        lds_limit_set = true;
+      }
+      launch(k_cls_wgrad<NO>, dim3(static_cast<unsigned>(chunks)), dim3(kBlock), static_cast<uint32_t>(lds), s, z,
+             ld_z, f, K, C, m, chunk, part);
+    };
+    const int no = (nout + kBlock - 1) / kBlock;
+    if (no <= 2) go(std::integral_constant<int, 2>{});
+    else if (no <= 8) go(std::integral_constant<int, 8>{});
+    else if (no <= 24) go(std::integral_constant<int, 24>{});
+    else go(std::integral_constant<int, 65>{});
+  }
+  launch(k_cls_reduce, dim3(static_cast<unsigned>((nout + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
+         static_cast<const float*>(part), m > 0 ? chunks : 0, K, C, dWc, dbc);
 }
 
 }  // namespace lat

@@ -228,8 +228,25 @@ int conv_max_pre_channels();
 // norm.hip
 int gn_max_channels();
 int64_t gn_workspace_bytes(int64_t n, int C);
+// stats (optional): per group the mean and 1 / sqrt(var + eps), as doubles
 void launch_gn_affine(const void* x, int64_t ld, int C, int bf16, int64_t n, int groups, const float* gamma,
-                      const float* beta, float eps, float* pre, void* work, hipStream_t s);
+                      const float* beta, float eps, float* pre, void* work, hipStream_t s, double* stats = nullptr);
+// classifier backward (z = dL/dlogits, m x K; f the DeformSlice output,
+// m x C dense): df = z Wc (m x C dense), dWc = z^T f, dbc = column sums of
+// z (either may be NULL); part holds classify_backward_partial_floats
+int64_t classify_backward_partial_floats(int64_t m, int K, int C);
+void launch_classify_backward(const float* z, int64_t ld_z, const float* Wc, int K, int C, int64_t m, const float* f,
+                              float* df, float* dWc, float* dbc, float* part, hipStream_t s);
+// a = max(x pre[c] + pre[C + c], 0) for fp32 x (n x C), the pre-activated
+// input the convolution gathered
+void launch_gn_relu_apply(const float* x, int64_t ldx, int C, int64_t n, const float* pre, float* a, int64_t lda,
+                          hipStream_t s);
+// GroupNorm + ReLU backward from dA = dL/d(pre-activated input): dgamma,
+// dbeta (optional, C floats), dX (optional, n x C, row stride lddx); coef
+// is a 4 C float work array; work holds gn_workspace_bytes(n, C)
+void launch_gn_backward(const float* x, int64_t ldx, const float* dA, int64_t lda, int C, int groups, int64_t n,
+                        const float* gamma, const float* pre, const double* stats, float* dgamma, float* dbeta,
+                        float* coef, float* dX, int64_t lddx, void* work, hipStream_t s);
 // per-group statistics from nparts partials (part[w][0..C) sums, part[w][C..2C)
 // sums of squares over `rows` rows) -> pre[0..C) scales, pre[C..2C) shifts
 void launch_gn_finalize(const double* part, int64_t nparts, int C, int groups, int64_t rows, const float* gamma,

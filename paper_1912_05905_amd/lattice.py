@@ -59,6 +59,10 @@ SIGNATURES = {
     "lattice_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _I64, _P]),
     "lattice_conv_backward": (_I32, [_P, _P, _P, _I64, _I32, _P, _I32, _I32, _P, _I64, _P, _I64, _P, _I64, _P, _P,
                                      _P]),
+    "lattice_conv_preact_backward": (_I32, [_P, _P, _P, _I64, _I32, _I32, _P, _P, _F32, _P, _I32, _I32, _P, _I64,
+                                            _P, _I64, _P, _I64, _P, _P, _P, _P, _P]),
+    "lattice_deform_slice_classify_backward": (_I32, [_P, _P, _I64, _I32, _P, _F32, _P, _I32, _P, _I64, _P, _I64,
+                                                      _P, _P, _P, _P, _P]),
     "lattice_deform_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _F32, _P, _I64, _P, _I64, _P, _P, _P]),
     "lattice_timing_enable": (_I32, [C.c_char_p, _I32]),
     "lattice_timing_read": (_I32, [C.c_char_p, C.POINTER(_I64), C.POINTER(C.c_double)]),
@@ -393,6 +397,32 @@ class Lattice:
                                            yp, yld, gp, gld, dp, dld, ptr(dW), ptr(db), _stream(stream)))
         return dx, dW, db
 
+    def conv_preact_backward(self, src: "Lattice", x: torch.Tensor, W: torch.Tensor, dy: torch.Tensor,
+                             groups: int = 32, gamma: torch.Tensor | None = None, beta: torch.Tensor | None = None,
+                             eps: float = 1e-5, relu: bool = False, y: torch.Tensor | None = None,
+                             want_dx: bool = True, want_dw: bool = True, want_dbias: bool = True,
+                             want_dgn: bool = True, stream=None):
+        """Gradients of the pre-activated convolution self <- src
+        (Y = act(conv(relu(GN(x)), W) + bias)) for dL/dY = dy:
+        (dx, dW, dbias, dgamma, dbeta), None where not asked for."""
+        cout, cin = dy.shape[1], x.shape[1]
+        dev = dict(dtype=torch.float32, device="cuda")
+        dx = torch.empty((src.n, cin), **dev) if want_dx else None
+        dW = torch.empty((9, cout, cin), **dev) if want_dw else None
+        db = torch.empty((cout,), **dev) if want_dbias else None
+        dg = torch.empty((cin,), **dev) if want_dgn else None
+        dbe = torch.empty((cin,), **dev) if want_dgn else None
+        xp, xld = _rows(x)
+        yp, yld = _rows(y) if y is not None else (None, 0)
+        gp, gld = _rows(dy)
+        dp, dld = _rows(dx) if dx is not None else (None, 0)
+        ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
+        _check(lib().lattice_conv_preact_backward(self._h, src._h, xp, xld, cin, int(groups), ptr(gamma), ptr(beta),
+                                                  float(eps), ptr(W), cout, LAT_RELU if relu else 0, yp, yld, gp,
+                                                  gld, dp, dld, ptr(dW), ptr(db), ptr(dg), ptr(dbe),
+                                                  _stream(stream)))
+        return dx, dW, db, dg, dbe
+
     def deform_slice_backward(self, x: torch.Tensor, wv: torch.Tensor, beta: float, dout: torch.Tensor,
                               dx_out: torch.Tensor | None = None, stream=None):
         """Gradients of deform_slice(x, wv, beta) for dL/dout = dout:
@@ -408,6 +438,27 @@ class Lattice:
                                                    dp, dld, C.c_void_p(dwv.data_ptr()), C.c_void_p(dbeta.data_ptr()),
                                                    _stream(stream)))
         return dx, dwv, dbeta
+
+    def deform_slice_classify_backward(self, x: torch.Tensor, wv: torch.Tensor, beta: float, Wc: torch.Tensor,
+                                       dlogits: torch.Tensor, want_dwc: bool = True, stream=None):
+        """Gradients of deform_slice_classify(x, wv, beta, Wc, bc) for
+        dL/dlogits = dlogits: (dx, dwv, dbeta, dWc, dbc), dWc and dbc None
+        unless asked for."""
+        Cc, K = x.shape[1], Wc.shape[0]
+        dev = dict(dtype=torch.float32, device="cuda")
+        dx = torch.empty((self.n, Cc), **dev)
+        dwv = torch.empty((Cc,), **dev)
+        dbeta = torch.empty((1,), **dev)
+        dWc = torch.empty((K, Cc), **dev) if want_dwc else None
+        dbc = torch.empty((K,), **dev) if want_dwc else None
+        xp, xld = _rows(x)
+        zp, zld = _rows(dlogits)
+        dp, dld = _rows(dx)
+        ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
+        _check(lib().lattice_deform_slice_classify_backward(self._h, xp, xld, Cc, ptr(wv), float(beta), ptr(Wc), K,
+                                                            zp, zld, dp, dld, ptr(dwv), ptr(dbeta), ptr(dWc),
+                                                            ptr(dbc), _stream(stream)))
+        return dx, dwv, dbeta, dWc, dbc
 
     def deform_slice_classify(self, x: torch.Tensor, wv: torch.Tensor, beta: float, Wc: torch.Tensor,
                               bc: torch.Tensor | None = None, out: torch.Tensor | None = None,

@@ -1114,3 +1114,133 @@ def test_conv_taps_count_existing_neighbours(L, O):
     assert g0.conv_taps(g1) == int((o1.up_table() >= 0).sum())
     g1.destroy()
     g0.destroy()
+
+
+# ----------------------------------------------------------------------------
+# backward of the pre-activated convolution: GroupNorm + ReLU + conv
+# ----------------------------------------------------------------------------
+def _preact_backward_case(L, O, gd, gs, od, os_, g2o_d, g2o_s, form, cin, cout, groups, seed, relu, affine=True,
+                          offset=0.0):
+    rng = np.random.default_rng(seed)
+    X = (offset + rng.normal(size=(os_.n, cin)) * rng.uniform(0.5, 2.0, size=cin)).astype(np.float32)
+    W = _rand_w(rng, cin, cout, 1.0 / np.sqrt(9 * cin))
+    gam = rng.uniform(0.5, 1.5, size=cin).astype(np.float32) if affine else None
+    bet = (0.2 * rng.normal(size=cin)).astype(np.float32) if affine else None
+    b = rng.normal(size=cout).astype(np.float32)
+    dY = rng.normal(size=(od.n, cout)).astype(np.float32)
+    X64 = X.astype(np.float64)
+    A = O.groupnorm(X64, groups, gam, bet, eps=1e-5, relu=True)
+    if form == "upsample":
+        Y = od.refine_into(os_, A, W.astype(np.float64), bias=b.astype(np.float64), relu=relu)
+    else:
+        Y = od.conv(os_, A, W.astype(np.float64), bias=b.astype(np.float64), relu=relu)
+    odA, odW, odb = od.conv_backward(os_, A, W.astype(np.float64), dY.astype(np.float64), relu=relu,
+                                     Y=Y if relu else None)
+    odX, odg, odbe = O.groupnorm_backward(X64, odA, groups, gam, bet, eps=1e-5, relu=True)
+    gdX, gdW, gdb, gdg, gdbe = gd.conv_preact_backward(
+        gs, _dev(X[g2o_s]), _gpu_w(W), _dev(dY[g2o_d]), groups=groups, gamma=None if gam is None else _dev(gam),
+        beta=None if bet is None else _dev(bet), eps=1e-5, relu=relu,
+        y=_dev(Y[g2o_d].astype(np.float32)) if relu else None)
+    what = f"preact backward {form} {cin}->{cout} G={groups} relu={relu}"
+    P.assert_close(P.rows_in_oracle_order(_host(gdX), g2o_s), odX, P.TOL_F32, "dX " + what)
+    P.assert_close(np.transpose(_host(gdW), (0, 2, 1)), odW, P.TOL_F32, "dW " + what)
+    P.assert_close(_host(gdb), odb, P.TOL_F32, "dbias " + what)
+    P.assert_close(_host(gdg), odg, P.TOL_F32, "dgamma " + what)
+    P.assert_close(_host(gdbe), odbe, P.TOL_F32, "dbeta " + what)
+
+
+@pytest.mark.parametrize("cin,cout,groups,relu,affine,offset", [
+    (64, 64, 32, False, True, 0.0), (12, 20, 4, True, True, 0.0), (128, 128, 32, True, False, 300.0),
+    (32, 96, 1, False, True, 0.0), (64, 16, 64, True, True, 0.0), (256, 64, 32, False, True, 0.0)])
+def test_conv_preact_backward_same_level(L, O, cin, cout, groups, relu, affine, offset):
+    pos = _cloud(1300 + cin + groups, 6000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.07)
+    _preact_backward_case(L, O, gl, gl, ol, ol, g2o, g2o, "same", cin, cout, groups, cin + cout + groups, relu,
+                          affine, offset)
+
+
+def test_conv_preact_backward_across_levels(L, O):
+    pos = _cloud(1400, 8000, 0.8)
+    gl = L.Lattice.create(_dev(pos), [0.05] * 3)
+    ol = O.Lattice.create(pos, np.full(3, 0.05, np.float32))
+    gc, oc = gl.coarsen(), ol.coarsen()
+    g2o_f = P.key_permutation(_host(gl.keys()), ol.keys())
+    g2o_c = P.key_permutation(_host(gc.keys()), oc.keys())
+    _preact_backward_case(L, O, gc, gl, oc, ol, g2o_c, g2o_f, "strided", 64, 128, 32, 11, True)
+    _preact_backward_case(L, O, gl, gc, ol, oc, g2o_f, g2o_c, "upsample", 128, 64, 32, 12, False)
+    _preact_backward_case(L, O, gl, gc, ol, oc, g2o_f, g2o_c, "upsample", 32, 32, 8, 13, True)
+
+
+def test_conv_preact_backward_partial_outputs_and_tiny(L, O):
+    """Only the weight gradients (no GroupNorm backward), only dX, and a
+    one-point cloud."""
+    pos = _cloud(1450, 3000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.08)
+    rng = np.random.default_rng(1450)
+    X = rng.normal(size=(ol.n, 16)).astype(np.float32)
+    W = _rand_w(rng, 16, 8, 0.1)
+    dY = rng.normal(size=(ol.n, 8)).astype(np.float32)
+    A = O.groupnorm(X.astype(np.float64), 4, eps=1e-5, relu=True)
+    odA, odW, odb = ol.conv_backward(ol, A, W.astype(np.float64), dY.astype(np.float64))
+    odX, odg, odbe = O.groupnorm_backward(X.astype(np.float64), odA, 4, eps=1e-5, relu=True)
+    gdX, gdW, gdb, gdg, gdbe = gl.conv_preact_backward(gl, _dev(X[g2o]), _gpu_w(W), _dev(dY[g2o]), groups=4,
+                                                       want_dx=False, want_dgn=False)
+    assert gdX is None and gdg is None and gdbe is None
+    P.assert_close(np.transpose(_host(gdW), (0, 2, 1)), odW, P.TOL_F32, "preact dW only")
+    P.assert_close(_host(gdb), odb, P.TOL_F32, "preact dbias only")
+    gdX, gdW, gdb, gdg, gdbe = gl.conv_preact_backward(gl, _dev(X[g2o]), _gpu_w(W), _dev(dY[g2o]), groups=4,
+                                                       want_dw=False, want_dbias=False, want_dgn=False)
+    P.assert_close(P.rows_in_oracle_order(_host(gdX), g2o), odX, P.TOL_F32, "preact dX only")
+    g1, o1, g2o1 = _pair(L, O, _cloud(1451, 1, 0.5), 0.1)
+    X1 = rng.normal(size=(o1.n, 8)).astype(np.float32)
+    W1 = _rand_w(rng, 8, 8, 0.3)
+    dY1 = rng.normal(size=(o1.n, 8)).astype(np.float32)
+    A1 = O.groupnorm(X1.astype(np.float64), 2, eps=1e-5, relu=True)
+    odA, odW, odb = o1.conv_backward(o1, A1, W1.astype(np.float64), dY1.astype(np.float64))
+    odX, odg, odbe = O.groupnorm_backward(X1.astype(np.float64), odA, 2, eps=1e-5, relu=True)
+    gdX, gdW, gdb, gdg, gdbe = g1.conv_preact_backward(g1, _dev(X1[g2o1]), _gpu_w(W1), _dev(dY1[g2o1]), groups=2)
+    P.assert_close(P.rows_in_oracle_order(_host(gdX), g2o1), odX, P.TOL_F32, "tiny preact dX")
+    P.assert_close(_host(gdg), odg, P.TOL_F32, "tiny preact dgamma")
+
+
+# ----------------------------------------------------------------------------
+# backward of DeformSlice fused with the linear classifier
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("C,K", [(4, 7), (16, 20), (64, 20), (64, 64), (128, 33), (512, 32)])
+def test_deform_slice_classify_backward(L, O, C, K):
+    pos = _cloud(1500 + C + K, 7000, 0.8)
+    gl, ol, g2o = _pair(L, O, pos, 0.06)
+    rng = np.random.default_rng(C * 10 + K)
+    X = rng.normal(size=(ol.n, C)).astype(np.float32)
+    wv = (rng.normal(size=C) / np.sqrt(C)).astype(np.float32)
+    Wc = (rng.normal(size=(K, C)) / np.sqrt(C)).astype(np.float32)
+    Z = rng.normal(size=(ol.m, K)).astype(np.float32)
+    odx, odw, odb, odWc, odbc = ol.deform_slice_classify_backward(X.astype(np.float64), wv.astype(np.float64), 0.1,
+                                                                  Wc.astype(np.float64), Z.astype(np.float64))
+    gdx, gdw, gdb, gdWc, gdbc = gl.deform_slice_classify_backward(_dev(X[g2o]), _dev(wv), 0.1, _dev(Wc), _dev(Z))
+    what = f"classifier backward C={C} K={K}"
+    P.assert_close(P.rows_in_oracle_order(_host(gdx), g2o), odx, P.TOL_F32, "dX " + what)
+    P.assert_close(_host(gdw), odw, P.TOL_F32, "dwv " + what)
+    P.assert_close(_host(gdb), np.array([odb]), P.TOL_F32, "dbeta " + what)
+    P.assert_close(_host(gdWc), odWc, P.TOL_F32, "dWc " + what)
+    P.assert_close(_host(gdbc), odbc, P.TOL_F32, "dbc " + what)
+
+
+def test_deform_slice_classify_backward_tiny_and_strided_logits(L, O):
+    """A one-point cloud, and dlogits as a column slice of a wider matrix."""
+    for m in (1, 2000):
+        gl, ol, g2o = _pair(L, O, _cloud(1600 + m, m, 0.6), 0.08)
+        rng = np.random.default_rng(m)
+        C, K = 32, 5
+        X = rng.normal(size=(ol.n, C)).astype(np.float32)
+        wv = (rng.normal(size=C) / np.sqrt(C)).astype(np.float32)
+        Wc = (rng.normal(size=(K, C)) / np.sqrt(C)).astype(np.float32)
+        Zw = rng.normal(size=(ol.m, K + 3)).astype(np.float32)
+        odx, odw, odb, odWc, odbc = ol.deform_slice_classify_backward(X.astype(np.float64), wv.astype(np.float64),
+                                                                      -0.2, Wc.astype(np.float64),
+                                                                      Zw[:, 1:1 + K].astype(np.float64))
+        gdx, gdw, gdb, gdWc, gdbc = gl.deform_slice_classify_backward(_dev(X[g2o]), _dev(wv), -0.2, _dev(Wc),
+                                                                      _dev(Zw)[:, 1:1 + K])
+        P.assert_close(P.rows_in_oracle_order(_host(gdx), g2o), odx, P.TOL_F32, f"classifier backward dX m={m}")
+        P.assert_close(_host(gdWc), odWc, P.TOL_F32, f"classifier backward dWc m={m}")
+        P.assert_close(_host(gdbc), odbc, P.TOL_F32, f"classifier backward dbc m={m}")
