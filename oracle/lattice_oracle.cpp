@@ -885,6 +885,141 @@ int orc_deform_slice_classify_backward(const orc_lattice* L, const double* X, in
   return orc_deform_slice_backward(L, X, C, wv, beta, df.data(), dX, dwv, dbeta);
 }
 
+// Distribute + PointNet backward: the gradient of orc_distribute_pointnet
+// for dL/dX = dX (n x C3) with respect to the features F, the three layers'
+// weights and biases, and the three normalisations' gamma and beta (same
+// concatenated layout as the forward's); the positions are inputs, not
+// parameters.  The maximum over J_v passes dX[v][c] to the row of J_v
+// holding channel c's maximum (the first such row in J_v's order, points in
+// increasing order).  Each [GN, ReLU, 1x1] block then goes backward:
+//   dW_i = sum_rows dh_i a_{i-1}^T,  db_i = sum_rows dh_i,  da_{i-1} = W_i^T dh_i,
+//   dh_{i-1} = the GroupNorm + ReLU backward of da_{i-1} (orc_groupnorm_backward),
+// and dF_p = sum over the rows of point p (one per vertex of its simplex) of
+// the feature part of dh_0.  margin (optional, n x C3): per vertex and
+// channel, the largest row minus the second largest (+inf for a single
+// row); where it is tiny either row is a valid choice for the maximum.
+// Any output pointer may be null.
+int orc_distribute_pointnet_backward(const orc_lattice* L, const double* G, const double* F, int cf,
+                                     const double* gamma, const double* beta, double eps, const double* W1,
+                                     const double* b1, int c1, const double* W2, const double* b2, int c2,
+                                     const double* W3, const double* b3, int c3, const double* dX, double* dF,
+                                     double* dW1, double* db1, double* dW2, double* db2, double* dW3, double* db3,
+                                     double* dgamma, double* dbeta, double* margin) {
+  if (!L || !dX || cf < 0 || c1 <= 0 || c2 <= 0 || c3 <= 0 || !W1 || !W2 || !W3 || !(eps >= 0.0)) return EINVAL_;
+  if (L->m > 0 && (!G || (cf > 0 && !F))) return EINVAL_;
+  const int cin = kDim + cf;
+  const int widths[3] = {cin, c1, c2};
+  const int outs[3] = {c1, c2, c3};
+  for (int w : widths)
+    if (w > 32 && w % 32 != 0) return EUNSUPPORTED;
+  const int64_t n = static_cast<int64_t>(L->keys.size());
+  std::vector<std::vector<int64_t>> J(n);
+  for (int64_t p = 0; p < L->m; ++p)
+    for (int k = 0; k < kD1; ++k) J[L->idx[p * kD1 + k]].push_back(p);
+  // the distributed rows, vertex by vertex, as in the forward
+  const int64_t rows = L->m * kD1;
+  std::vector<int64_t> row_point, first_row(n + 1, 0);
+  row_point.reserve(rows);
+  std::vector<std::vector<double>> h(4), a(3);
+  h[0].assign(static_cast<size_t>(rows) * cin, 0.0);
+  int64_t r = 0;
+  for (int64_t v = 0; v < n; ++v) {
+    first_row[v] = r;
+    double mu[kDim] = {0.0, 0.0, 0.0};
+    for (int64_t p : J[v])
+      for (int j = 0; j < kDim; ++j) mu[j] += G[p * kDim + j] / L->scale[j];
+    for (int j = 0; j < kDim; ++j) mu[j] /= static_cast<double>(J[v].size());
+    for (int64_t p : J[v]) {
+      for (int j = 0; j < kDim; ++j) h[0][r * cin + j] = G[p * kDim + j] / L->scale[j] - mu[j];
+      for (int c = 0; c < cf; ++c) h[0][r * cin + kDim + c] = F[p * cf + c];
+      row_point.push_back(p);
+      ++r;
+    }
+  }
+  first_row[n] = r;
+  const double* Ws[3] = {W1, W2, W3};
+  const double* bs[3] = {b1, b2, b3};
+  double* dWs[3] = {dW1, dW2, dW3};
+  double* dbs[3] = {db1, db2, db3};
+  int offs[3] = {0, cin, cin + c1};
+  // forward, keeping every layer's input h and its activation a
+  for (int layer = 0; layer < 3; ++layer) {
+    const int ci = widths[layer], co = outs[layer];
+    a[layer].assign(static_cast<size_t>(rows) * ci, 0.0);
+    if (rows > 0) {
+      const int st = orc_groupnorm(h[layer].data(), rows, ci, ci, ci <= 32 ? ci : 32,
+                                   gamma ? gamma + offs[layer] : nullptr, beta ? beta + offs[layer] : nullptr, eps,
+                                   1, a[layer].data(), ci);
+      if (st != OK) return st;
+    }
+    h[layer + 1].assign(static_cast<size_t>(rows) * co, 0.0);
+    for (int64_t q = 0; q < rows; ++q)
+      for (int o = 0; o < co; ++o) {
+        double acc = bs[layer] ? bs[layer][o] : 0.0;
+        for (int i = 0; i < ci; ++i) acc += Ws[layer][o * ci + i] * a[layer][q * ci + i];
+        h[layer + 1][q * co + o] = acc;
+      }
+  }
+  // MaxPool backward
+  std::vector<double> g(static_cast<size_t>(rows) * c3, 0.0);
+  for (int64_t v = 0; v < n; ++v)
+    for (int c = 0; c < c3; ++c) {
+      int64_t best = -1;
+      double top = -INFINITY, second = -INFINITY;
+      for (int64_t q = first_row[v]; q < first_row[v + 1]; ++q) {
+        const double val = h[3][q * c3 + c];
+        if (best < 0 || val > top) {
+          second = top;
+          top = val;
+          best = q;
+        } else if (val > second) {
+          second = val;
+        }
+      }
+      if (best >= 0) g[best * c3 + c] = dX[v * c3 + c];
+      if (margin) margin[v * c3 + c] = best >= 0 && first_row[v + 1] - first_row[v] > 1 ? top - second : INFINITY;
+    }
+  // the three blocks backward
+  if (dgamma) std::fill(dgamma, dgamma + cin + c1 + c2, 0.0);
+  if (dbeta) std::fill(dbeta, dbeta + cin + c1 + c2, 0.0);
+  for (int layer = 2; layer >= 0; --layer) {
+    const int ci = widths[layer], co = outs[layer];
+    if (dWs[layer]) {
+      std::fill(dWs[layer], dWs[layer] + static_cast<int64_t>(co) * ci, 0.0);
+      for (int64_t q = 0; q < rows; ++q)
+        for (int o = 0; o < co; ++o)
+          for (int i = 0; i < ci; ++i) dWs[layer][o * ci + i] += g[q * co + o] * a[layer][q * ci + i];
+    }
+    if (dbs[layer]) {
+      std::fill(dbs[layer], dbs[layer] + co, 0.0);
+      for (int64_t q = 0; q < rows; ++q)
+        for (int o = 0; o < co; ++o) dbs[layer][o] += g[q * co + o];
+    }
+    std::vector<double> da(static_cast<size_t>(rows) * ci, 0.0), dh(static_cast<size_t>(rows) * ci, 0.0);
+    for (int64_t q = 0; q < rows; ++q)
+      for (int i = 0; i < ci; ++i) {
+        double acc = 0.0;
+        for (int o = 0; o < co; ++o) acc += Ws[layer][o * ci + i] * g[q * co + o];
+        da[q * ci + i] = acc;
+      }
+    if (rows > 0) {
+      const int st = orc_groupnorm_backward(h[layer].data(), rows, ci, ci <= 32 ? ci : 32,
+                                            gamma ? gamma + offs[layer] : nullptr,
+                                            beta ? beta + offs[layer] : nullptr, eps, 1, da.data(), dh.data(),
+                                            dgamma ? dgamma + offs[layer] : nullptr,
+                                            dbeta ? dbeta + offs[layer] : nullptr);
+      if (st != OK) return st;
+    }
+    g.swap(dh);
+  }
+  if (dF && cf > 0) {
+    std::fill(dF, dF + L->m * cf, 0.0);
+    for (int64_t q = 0; q < rows; ++q)
+      for (int c = 0; c < cf; ++c) dF[row_point[q] * cf + c] += g[q * cin + kDim + c];
+  }
+  return OK;
+}
+
 // Round to the nearest bfloat16 (8 significant bits), ties to even, in place.
 // Used where the bf16 pipeline stores activations; normal range only.
 void orc_round_bf16(double* x, int64_t n) {

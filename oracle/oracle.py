@@ -63,6 +63,8 @@ def lib():
             "orc_conv_backward": (i32, [p, p, p, i32, p, i32, i32, p, p, p, p, p]),
             "orc_deform_slice_backward": (i32, [p, p, i32, p, dbl, p, p, p, p]),
             "orc_groupnorm_backward": (i32, [p, i64, i32, i32, p, p, dbl, i32, p, p, p, p]),
+            "orc_distribute_pointnet_backward": (i32, [p, p, p, i32, p, p, dbl, p, p, i32, p, p, i32, p, p, i32, p, p,
+                                                       p, p, p, p, p, p, p, p, p]),
             "orc_deform_slice_classify_backward": (i32, [p, p, i32, p, dbl, p, i32, p, p, p, p, p, p]),
         }
         for name, (res, args) in sig.items():
@@ -214,6 +216,32 @@ class Lattice:
                                              float(eps), _ptr(W1), _ptr(b1), c1, _ptr(W2), _ptr(b2), c2, _ptr(W3),
                                              _ptr(b3), c3, _ptr(X)))
         return X
+
+    def distribute_pointnet_backward(self, G, F, layers, dX, gn=None, eps=1e-5):
+        """Gradients of distribute_pointnet(G, F, layers, gn, eps) for
+        dL/dX = dX: a dict with dF (m x Cf), dW1..dW3 ([out][in]),
+        db1..db3, dgamma and dbeta (concatenated as gn), and margin (n x C3:
+        the largest minus the second largest row of J_v per channel)."""
+        G = _f64(G)
+        F = _f64(F) if F is not None else np.zeros((G.shape[0], 0))
+        (W1, b1), (W2, b2), (W3, b3) = [(_f64(W), None if b is None else _f64(b)) for W, b in layers]
+        cf = F.shape[1]
+        c1, c2, c3 = W1.shape[0], W2.shape[0], W3.shape[0]
+        gam = bet = None
+        if gn is not None:
+            gam, bet = (None if a is None else _f64(a) for a in gn)
+        dX = _f64(dX)
+        assert dX.shape == (self.n, c3)
+        ng = G.shape[1] + cf + c1 + c2
+        out = dict(dF=np.zeros((G.shape[0], cf)), dW1=np.zeros_like(W1), db1=np.zeros(c1), dW2=np.zeros_like(W2),
+                   db2=np.zeros(c2), dW3=np.zeros_like(W3), db3=np.zeros(c3), dgamma=np.zeros(ng),
+                   dbeta=np.zeros(ng), margin=np.zeros((self.n, c3)))
+        _check(lib().orc_distribute_pointnet_backward(
+            self._h, _ptr(G), _ptr(F) if cf else None, cf, _ptr(gam), _ptr(bet), float(eps), _ptr(W1), _ptr(b1), c1,
+            _ptr(W2), _ptr(b2), c2, _ptr(W3), _ptr(b3), c3, _ptr(dX), _ptr(out["dF"]) if cf else None,
+            _ptr(out["dW1"]), _ptr(out["db1"]), _ptr(out["dW2"]), _ptr(out["db2"]), _ptr(out["dW3"]),
+            _ptr(out["db3"]), _ptr(out["dgamma"]), _ptr(out["dbeta"]), _ptr(out["margin"])))
+        return out
 
     def conv(self, src: "Lattice", X, W, bias=None, relu=False, rows=None):
         """dst = self.  src is self (1-hop conv) or self.parent (strided)."""

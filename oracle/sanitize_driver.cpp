@@ -54,6 +54,12 @@ int orc_groupnorm_backward(const double* X, int64_t n, int C, int groups, const 
 int orc_deform_slice_classify_backward(const orc_lattice* L, const double* X, int C, const double* wv,
                                        double beta, const double* Wc, int K, const double* dZ, double* dX,
                                        double* dwv, double* dbeta, double* dWc, double* dbc);
+int orc_distribute_pointnet_backward(const orc_lattice* L, const double* G, const double* F, int cf,
+                                     const double* gamma, const double* beta, double eps, const double* W1,
+                                     const double* b1, int c1, const double* W2, const double* b2, int c2,
+                                     const double* W3, const double* b3, int c3, const double* dX, double* dF,
+                                     double* dW1, double* db1, double* dW2, double* db2, double* dW3, double* db3,
+                                     double* dgamma, double* dbeta, double* margin);
 void orc_round_bf16(double* x, int64_t n);
 }
 
@@ -163,6 +169,14 @@ int main() {
   need(orc_deform_slice_classify_backward(L0, X.data(), C, wv.data(), 0.1, Wc.data(), K, dZ.data(), dXs.data(),
                                           dwv.data(), &dbeta, dWk.data(), dbk.data()),
        "classify backward");
+  auto dD = vec(n0 * 16);
+  std::vector<double> dFd(m * cf), dP1(16 * (3 + cf)), dp1(16), dP2(32 * 16), dp2(32), dP3(16 * 32), dp3(16),
+      dgam(3 + cf + 16 + 32), dbet(3 + cf + 16 + 32), marg(n0 * 16);
+  need(orc_distribute_pointnet_backward(L0, Gp.data(), Fd.data(), cf, gam.data(), bet.data(), 1e-5, P1.data(),
+                                        p1.data(), 16, P2.data(), p2.data(), 32, P3.data(), p3.data(), 16, dD.data(),
+                                        dFd.data(), dP1.data(), dp1.data(), dP2.data(), dp2.data(), dP3.data(),
+                                        dp3.data(), dgam.data(), dbet.data(), marg.data()),
+       "distribute backward");
   orc_round_bf16(X.data(), n0 * C);
   orc_destroy(E);
   orc_destroy(L2);

@@ -827,3 +827,71 @@ def test_deform_slice_classify_backward_finite_differences(oracle_mod):
         fd = (loss(*up) - loss(*dn)) / (2 * h)
         an = _dot(grad, D) if i != 2 else grad
         assert abs(fd - an) <= 1e-6 * max(1.0, abs(fd)), (i, fd, an)
+
+
+def test_distribute_backward_finite_differences(oracle_mod):
+    """L = <Distribute+PointNet(G, F), D>: central differences in random
+    directions of F, of each layer's weights and bias and of the three
+    normalisations' gamma and beta match the gradients (tiny cloud, widths
+    8/16/16, with and without features)."""
+    h = 1e-6
+    O = oracle_mod
+    for seed, cf in ((93, 3), (94, 0)):
+        G = _tiny_cloud(seed, m=120)
+        st = Stream(seed, "dist-bwd")
+        F = st.normal(120 * cf).reshape(120, cf) if cf else None
+        cin = 3 + cf
+        layers = _pointnet_layers(st, cin, (8, 16, 16))
+        ng = cin + 8 + 16
+        gam, bet = 1.0 + 0.2 * st.normal(ng), 0.2 * st.normal(ng)
+        ol = O.Lattice.create(G, np.full(3, 0.2, np.float32))
+        Gd = G.astype(np.float64)
+        D = st.normal(ol.n * 16).reshape(ol.n, 16)
+        gr = ol.distribute_pointnet_backward(Gd, F, layers, D, (gam, bet))
+
+        def loss(F_, layers_, gam_, bet_):
+            return _dot(ol.distribute_pointnet(Gd, F_, layers_, (gam_, bet_)), D)
+
+        rng = np.random.default_rng(seed)
+        checks = []
+        if cf:
+            E = rng.normal(size=F.shape)
+            checks.append((lambda t, E=E: loss(F + t * E, layers, gam, bet), _dot(gr["dF"], E), "dF"))
+        for li in range(3):
+            for j, name in ((0, f"dW{li + 1}"), (1, f"db{li + 1}")):
+                E = rng.normal(size=layers[li][j].shape)
+
+                def f(t, li=li, j=j, E=E):
+                    ls = [list(x) for x in layers]
+                    ls[li][j] = ls[li][j] + t * E
+                    return loss(F, [tuple(x) for x in ls], gam, bet)
+                checks.append((f, _dot(gr[name], E), name))
+        E = rng.normal(size=ng)
+        checks.append((lambda t, E=E: loss(F, layers, gam + t * E, bet), _dot(gr["dgamma"], E), "dgamma"))
+        checks.append((lambda t, E=E: loss(F, layers, gam, bet + t * E), _dot(gr["dbeta"], E), "dbeta"))
+        for f, an, name in checks:
+            fd = (f(h) - f(-h)) / (2 * h)
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(fd)), (seed, name, fd, an)
+        m = gr["margin"]
+        assert (m >= 0).all()
+        single = np.bincount(ol.simplices()[0].reshape(-1), minlength=ol.n) == 1
+        assert np.isinf(m[single]).all() and np.isfinite(m[~single]).all()
+
+
+def test_distribute_backward_routes_to_the_maximum(oracle_mod):
+    """Only the row holding a channel's maximum receives that channel's
+    gradient: with dX one-hot at (v, c), dW3 is the outer product e_c a_2^T
+    of that single row, so db3 = e_c exactly."""
+    O = oracle_mod
+    G = _tiny_cloud(95, m=80)
+    st = Stream(95, "dist-bwd2")
+    layers = _pointnet_layers(st, 3, (8, 16, 16))
+    ol = O.Lattice.create(G, np.full(3, 0.2, np.float32))
+    D = np.zeros((ol.n, 16))
+    v = int(np.argmax(np.bincount(ol.simplices()[0].reshape(-1), minlength=ol.n)))   # the vertex with most points
+    D[v, 5] = 1.0
+    gr = O.Lattice.distribute_pointnet_backward(ol, G.astype(np.float64), None, layers, D)
+    e5 = np.zeros(16)
+    e5[5] = 1.0
+    assert np.array_equal(gr["db3"], e5)
+    assert np.abs(gr["dW3"][np.arange(16) != 5]).max() == 0.0
