@@ -442,6 +442,40 @@ int lattice_deform_slice_classify_backward(lattice_t L, const float* vals_dev, i
                                            float* dbc_dev, hipStream_t stream);
 
 /*
+ * Distribute + PointNet backward (Proposed Operations, Eq. (distribute);
+ * PointNet block of the architecture figure) for x = the
+ * lattice_distribute_pointnet output, given dX = dL/dx (n x C3 float32, row
+ * stride ld_dX, 0 = C3):
+ *   the maximum over J_v passes dX[v][c] to the row of J_v holding channel
+ *   c's maximum (the first such row in the lattice's list order);
+ *   each block h_i = W_i relu(GN_i(h_{i-1})) + b_i goes backward as
+ *     dW_i = sum_rows dh_i a_{i-1}^T,  db_i = sum_rows dh_i,  da_{i-1} = W_i^T dh_i,
+ *   then the GroupNorm + ReLU backward of da_{i-1} (as described for
+ *   lattice_conv_preact_backward, statistics over all rows) gives dh_{i-1}
+ *   and the normalisation's dgamma / dbeta;
+ *   dfeat_p = sum over the d+1 rows of point p of the feature part of dh_0.
+ * The forward is recomputed in float32 (every block's input kept in the
+ * work space); positions are inputs and get no gradient.
+ *   Arguments pos_dev .. C3 as for lattice_distribute_pointnet (W2_dev and
+ *   W3_dev 16-byte aligned).
+ *   dfeat_dev  m x Cf float32, row stride ld_dfeat (0 = Cf), or NULL.
+ *   dW*_dev    C1 x (d + Cf), C2 x C1, C3 x C2 ([out][in]) or NULL;
+ *   db*_dev    C1 / C2 / C3 or NULL.
+ *   dgamma_dev, dbeta_dev  (d + Cf) + C1 + C2 floats each (the layout of
+ *              gn_gamma_dev), or NULL.
+ * Sums over rows run in a fixed order.  Uses work space of about
+ * 4 m ((d + Cf) + C1 + C2 + 4 max width) floats from the pool.
+ */
+int lattice_distribute_pointnet_backward(lattice_t L, const float* pos_dev, const float* feat_dev, int64_t ld_feat,
+                                         int Cf, const float* gn_gamma_dev, const float* gn_beta_dev, float eps,
+                                         const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
+                                         const float* b2_dev, int C2, const float* W3_dev, const float* b3_dev, int C3,
+                                         const float* dX_dev, int64_t ld_dX, float* dfeat_dev, int64_t ld_dfeat,
+                                         float* dW1_dev, float* db1_dev, float* dW2_dev, float* db2_dev,
+                                         float* dW3_dev, float* db3_dev, float* dgamma_dev, float* dbeta_dev,
+                                         hipStream_t stream);
+
+/*
  * Timing of the library's kernels with HIP events on the launch stream, for
  * measurement.  enable != 0 records a start/stop event pair around every
  * launch of the kernel family `name` ("conv", "splat", "slice", "insert",

@@ -1576,6 +1576,44 @@ int lattice_deform_slice_classify_backward(lattice_t L, const float* vals_dev, i
   return check_launch("deform slice classify backward");
 }
 
+int lattice_distribute_pointnet_backward(lattice_t L, const float* pos_dev, const float* feat_dev, int64_t ld_feat,
+                                         int Cf, const float* gn_gamma_dev, const float* gn_beta_dev, float eps,
+                                         const float* W1_dev, const float* b1_dev, int C1, const float* W2_dev,
+                                         const float* b2_dev, int C2, const float* W3_dev, const float* b3_dev, int C3,
+                                         const float* dX_dev, int64_t ld_dX, float* dfeat_dev, int64_t ld_dfeat,
+                                         float* dW1_dev, float* db1_dev, float* dW2_dev, float* db2_dev,
+                                         float* dW3_dev, float* db3_dev, float* dgamma_dev, float* dbeta_dev,
+                                         hipStream_t stream) {
+  int st;
+  if ((st = use(L, stream)) != LAT_OK) return st;
+  if ((st = ensure_lists(L, stream)) != LAT_OK) return st;
+  if (Cf < 0 || Cf > distribute_max_features())
+    return fail(LAT_EUNSUPPORTED, "Cf must be in [0, " + std::to_string(distribute_max_features()) + "]");
+  for (int c : {C1, C2, C3})
+    if (c <= 0 || c % 16 != 0 || c > 64) return fail(LAT_EUNSUPPORTED, "C1, C2, C3 must be 16, 32, 48 or 64");
+  if (C1 == 48 || C2 == 48)
+    return fail(LAT_EUNSUPPORTED, "a normalised layer input of 48 channels does not split into 32 groups");
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return fail(LAT_EINVAL, "eps must be finite and >= 0");
+  if (ld_feat == 0) ld_feat = Cf;
+  if (ld_dfeat == 0) ld_dfeat = Cf;
+  if (ld_dX == 0) ld_dX = C3;
+  if (ld_feat < Cf || ld_dfeat < Cf) return fail(LAT_EINVAL, "feature row strides must be >= Cf");
+  if ((st = check_matrix(dX_dev, ld_dX, C3, LAT_F32, "dX", L->n > 0)) != LAT_OK) return st;
+  if (!W1_dev || !W2_dev || !W3_dev) return fail(LAT_EINVAL, "weights are null");
+  if (!aligned16(W2_dev) || !aligned16(W3_dev)) return fail(LAT_EINVAL, "W2 and W3 must be 16-byte aligned");
+  if (L->m > 0 && !pos_dev) return fail(LAT_EINVAL, "pos is null");
+  if (L->m > 0 && Cf > 0 && !feat_dev) return fail(LAT_EINVAL, "feat is null");
+  Scratch work;
+  if ((st = work.get(static_cast<size_t>(distribute_backward_workspace_bytes(L->n, L->m, L->total, Cf, C1, C2, C3)),
+                     stream)) != LAT_OK)
+    return st;
+  launch_distribute_backward(L->offsets, L->entries, L->chunk_first, L->chunk, L->n, L->m, L->total, pos_dev,
+                             L->scale, feat_dev, ld_feat, Cf, gn_gamma_dev, gn_beta_dev, eps, W1_dev, b1_dev, C1,
+                             W2_dev, b2_dev, C2, W3_dev, b3_dev, C3, dX_dev, ld_dX, dfeat_dev, ld_dfeat, dW1_dev,
+                             db1_dev, dW2_dev, db2_dev, dW3_dev, db3_dev, dgamma_dev, dbeta_dev, work.p, stream);
+  return check_launch("distribute backward");
+}
+
 int lattice_timing_enable(const char* name, int enable) {
   if (!name) return fail(LAT_EINVAL, "name is null");
   std::lock_guard<std::mutex> lk(g_timer_mu);

@@ -243,14 +243,21 @@ void wgrad_chunks(int64_t n_out, int tiles, int64_t* chunks, int64_t* V) {
 }
 
 
-// ---- classifier backward ----
-constexpr int kClsPts = 32;        // points staged per step of k_cls_wgrad
+// ---- linear layers backward (the classifier fused with DeformSlice, the
+// 1x1 layers of Distribute + PointNet) ----
+// For out_p = W a_p + b over rows p (W: K x C, [out][in]) and G = dL/dout:
+//   dA_p = sum_j G_pj W[j]   (k_lin_dinput),
+//   dW = sum_p G_p a_p^T, db = sum_p G_p   (k_lin_wgrad over chunks of rows,
+//   then k_lin_reduce adds the chunks' partials in chunk order).
+// a_p is either given or max(x_p scale + shift, 0) of given rows x_p (the
+// pre-activation table pre = [C scales][C shifts]).
+constexpr int kClsPts = 32;        // rows staged per step of k_lin_wgrad
 constexpr int kClsMaxChunks = 1024;
 
-// df_p[c] = sum_j z_pj Wc[j][c]: one thread per (point, 4 channels).
+// dA_p[c] = sum_j G_pj W[j][c]: one thread per (row, 4 channels).
 __global__ void __launch_bounds__(kBlock)
-k_cls_dfeat(const float* __restrict__ z, int64_t ld_z, const float* __restrict__ Wc, int K, int C, int64_t m,
-            float* __restrict__ df) {
+k_lin_dinput(const float* __restrict__ z, int64_t ld_z, const float* __restrict__ Wc, int K, int C, int64_t m,
+             float* __restrict__ df, int64_t ld_df) {
   const int quads = C / 4;
   const int64_t total = m * quads;
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < total;
@@ -266,17 +273,18 @@ k_cls_dfeat(const float* __restrict__ z, int64_t ld_z, const float* __restrict__
       a.z = fmaf(zj, w.z, a.z);
       a.w = fmaf(zj, w.w, a.w);
     }
-    *reinterpret_cast<float4*>(df + p * C + c) = a;
+    *reinterpret_cast<float4*>(df + p * ld_df + c) = a;
   }
 }
 
-// Workgroup w: over its chunk of points, part[w][j C + c] = sum_p z_pj f_pc
-// and part[w][K C + j] = sum_p z_pj, points in order; rows of z and f are
-// staged kClsPts at a time in LDS.  Thread t owns outputs t, t + 256, ...
+// Workgroup w: over its chunk of rows, part[w][j C + c] = sum_p G_pj a_pc and
+// part[w][K C + j] = sum_p G_pj, rows in order; rows of G and a are staged
+// kClsPts at a time in LDS (a pre-activated as they are staged when pre is
+// given).  Thread t owns outputs t, t + 256, ...
 template <int NO>
 __global__ void __launch_bounds__(kBlock)
-k_cls_wgrad(const float* __restrict__ z, int64_t ld_z, const float* __restrict__ f, int K, int C, int64_t m,
-            int64_t chunk, float* __restrict__ part) {
+k_lin_wgrad(const float* __restrict__ z, int64_t ld_z, const float* __restrict__ f, int64_t ld_f,
+            const float* __restrict__ pre, int K, int C, int64_t m, int64_t chunk, float* __restrict__ part) {
   extern __shared__ float sm[];
   float* sz = sm;                    // [kClsPts][K]
   float* sf = sm + kClsPts * K;      // [kClsPts][C]
@@ -293,7 +301,14 @@ k_cls_wgrad(const float* __restrict__ z, int64_t ld_z, const float* __restrict__
     for (int e = t; e < np * K; e += kBlock) sz[e] = z[(pb + e / K) * ld_z + e % K];
     for (int e = t; e < np * (C / 4); e += kBlock) {
       const int r = e / (C / 4), q = e - r * (C / 4);
-      *reinterpret_cast<float4*>(sf + r * C + 4 * q) = *reinterpret_cast<const float4*>(f + (pb + r) * C + 4 * q);
+      float4 v = *reinterpret_cast<const float4*>(f + (pb + r) * ld_f + 4 * q);
+      if (pre) {
+        v.x = fmaxf(fmaf(v.x, pre[4 * q], pre[C + 4 * q]), 0.f);
+        v.y = fmaxf(fmaf(v.y, pre[4 * q + 1], pre[C + 4 * q + 1]), 0.f);
+        v.z = fmaxf(fmaf(v.z, pre[4 * q + 2], pre[C + 4 * q + 2]), 0.f);
+        v.w = fmaxf(fmaf(v.w, pre[4 * q + 3], pre[C + 4 * q + 3]), 0.f);
+      }
+      *reinterpret_cast<float4*>(sf + r * C + 4 * q) = v;
     }
     __syncthreads();
 #pragma unroll
@@ -316,9 +331,10 @@ k_cls_wgrad(const float* __restrict__ z, int64_t ld_z, const float* __restrict__
     if (t + k * kBlock < nout) dst[t + k * kBlock] = acc[k];
 }
 
-// out[o] = sum over the chunks of part[w][o], in chunk order.
+// dW[j][c] (c < C_out, row stride C_out) and db[j]: sums over the chunks of
+// part[w][o], in chunk order.
 __global__ void __launch_bounds__(kBlock)
-k_cls_reduce(const float* __restrict__ part, int chunks, int K, int C, float* __restrict__ dWc,
+k_lin_reduce(const float* __restrict__ part, int chunks, int K, int C, int C_out, float* __restrict__ dWc,
              float* __restrict__ dbc) {
   const int nout = K * C + K;
   const int o = blockIdx.x * kBlock + threadIdx.x;
@@ -326,7 +342,8 @@ k_cls_reduce(const float* __restrict__ part, int chunks, int K, int C, float* __
   float a = 0.f;
   for (int w = 0; w < chunks; ++w) a += part[static_cast<int64_t>(w) * nout + o];
   if (o < K * C) {
-    if (dWc) dWc[o] = a;
+    const int j = o / C, c = o - j * C;
+    if (dWc && c < C_out) dWc[j * C_out + c] = a;
   } else if (dbc) {
     dbc[o - K * C] = a;
   }
@@ -338,6 +355,7 @@ void cls_chunks(int64_t m, int64_t* chunk, int* chunks) {
   *chunk = c;
   *chunks = static_cast<int>(std::max<int64_t>(1, (m + c - 1) / c));
 }
+
 }  // namespace
 
 void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, const float* wsum, int64_t n,
@@ -391,15 +409,15 @@ int64_t classify_backward_partial_floats(int64_t m, int K, int C) {
   return static_cast<int64_t>(chunks) * (static_cast<int64_t>(K) * C + K);
 }
 
-void launch_classify_backward(const float* z, int64_t ld_z, const float* Wc, int K, int C, int64_t m, const float* f,
-                              float* df, float* dWc, float* dbc, float* part, hipStream_t s) {
-  ScopedKernelTimer tm("classify_bwd", s);
-  if (m > 0) {
+void launch_linear_backward(const float* z, int64_t ld_z, const float* W, int K, int C, int64_t m, const float* f,
+                            int64_t ld_f, const float* pre, float* df, int64_t ld_df, float* dW, int C_out, float* db,
+                            float* part, hipStream_t s) {
+  if (df && m > 0) {
     const int64_t b = (m * (C / 4) + kBlock - 1) / kBlock;
-    launch(k_cls_dfeat, dim3(static_cast<unsigned>(std::min<int64_t>(b, 8192))), dim3(kBlock), 0, s, z, ld_z, Wc, K,
-           C, m, df);
+    launch(k_lin_dinput, dim3(static_cast<unsigned>(std::min<int64_t>(b, 8192))), dim3(kBlock), 0, s, z, ld_z, W, K,
+           C, m, df, ld_df);
   }
-  if (!dWc && !dbc) return;
+  if (!dW && !db) return;
   const int nout = K * C + K;
   int64_t chunk;
   int chunks;
@@ -410,13 +428,13 @@ void launch_classify_backward(const float* z, int64_t ld_z, const float* Wc, int
       constexpr int NO = decltype(no_c)::value;
       static bool lds_limit_set = false;
       if (!lds_limit_set) {
-        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_cls_wgrad<NO>),
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_lin_wgrad<NO>),
                                   hipFuncAttributeMaxDynamicSharedMemorySize,
                                   static_cast<int>(sizeof(float) * kClsPts * (64 + 512)));
         lds_limit_set = true;
       }
-      launch(k_cls_wgrad<NO>, dim3(static_cast<unsigned>(chunks)), dim3(kBlock), static_cast<uint32_t>(lds), s, z,
-             ld_z, f, K, C, m, chunk, part);
+      launch(k_lin_wgrad<NO>, dim3(static_cast<unsigned>(chunks)), dim3(kBlock), static_cast<uint32_t>(lds), s, z,
+             ld_z, f, ld_f, pre, K, C, m, chunk, part);
     };
     const int no = (nout + kBlock - 1) / kBlock;
     if (no <= 2) go(std::integral_constant<int, 2>{});
@@ -424,8 +442,14 @@ void launch_classify_backward(const float* z, int64_t ld_z, const float* Wc, int
     else if (no <= 24) go(std::integral_constant<int, 24>{});
     else go(std::integral_constant<int, 65>{});
   }
-  launch(k_cls_reduce, dim3(static_cast<unsigned>((nout + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
-         static_cast<const float*>(part), m > 0 ? chunks : 0, K, C, dWc, dbc);
+  launch(k_lin_reduce, dim3(static_cast<unsigned>((nout + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
+         static_cast<const float*>(part), m > 0 ? chunks : 0, K, C, C_out, dW, db);
+}
+
+void launch_classify_backward(const float* z, int64_t ld_z, const float* Wc, int K, int C, int64_t m, const float* f,
+                              float* df, float* dWc, float* dbc, float* part, hipStream_t s) {
+  ScopedKernelTimer tm("classify_bwd", s);
+  launch_linear_backward(z, ld_z, Wc, K, C, m, f, C, nullptr, df, C, dWc, C, dbc, part, s);
 }
 
 }  // namespace lat

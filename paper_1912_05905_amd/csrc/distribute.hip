@@ -746,6 +746,197 @@ void run_mlp(int stage, const MlpLds& lay, unsigned grid, hipStream_t s, const i
          sc[1], sc[2], feat, ld_feat, cf, mu, pre, W1, b1, W2, b2, W3, b3, ks1, C1, C2, C3, out, ld_out, part);
 }
 
+
+// ---- Distribute + PointNet backward ----
+// The forward is recomputed in fp64 with every block's input and
+// activation kept (rows of list entries, in list order): the ReLU and the
+// maximum are discrete decisions, and fp64 takes them as exact arithmetic
+// does except within ~1e-15 of a tie.  The maximum routes dL/dx_v[c] to the
+// row of J_v holding channel c's maximum (the first in list order); each
+// block then goes backward in fp32 as a linear layer
+// (launch_linear_backward, on the fp32 activations) and a GroupNorm + ReLU
+// (launch_gn_backward, whose ReLU passes where the activation is > 0).  The
+// raw rows are zero-padded to a multiple of 4 channels, each padding
+// channel a group of its own that no weight reads.
+
+// Raw rows (total x cin4) in fp64: g / sigma - mu, the features, zeros.
+__global__ void __launch_bounds__(kBlock)
+k_dist_raw_rows64(const int32_t* __restrict__ entries, const int32_t* __restrict__ entry_vertex, int64_t total,
+                  const float* __restrict__ pos, double sc0, double sc1, double sc2, const double4* __restrict__ mu,
+                  const float* __restrict__ feat, int64_t ld_feat, int cf, int cin4, double* __restrict__ H64) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (e >= total) return;
+  const int64_t p = entries[e] >> 2;
+  const double4 m = mu[entry_vertex[e]];
+  double* r = H64 + e * cin4;
+  r[0] = static_cast<double>(pos[3 * p]) / sc0 - m.x;
+  r[1] = static_cast<double>(pos[3 * p + 1]) / sc1 - m.y;
+  r[2] = static_cast<double>(pos[3 * p + 2]) / sc2 - m.z;
+  for (int c = 0; c < cf; ++c) r[3 + c] = feat[p * ld_feat + c];
+  for (int c = 3 + cf; c < cin4; ++c) r[c] = 0.0;
+}
+
+// Per-workgroup fp64 sums and sums of squares of each channel of fp64 rows
+// [w rows_per, (w + 1) rows_per): thread t takes channel t % C of rows
+// t / C, + slots, ...; the slots are added in order.  Layout as
+// launch_gn_finalize reads it.
+__global__ void __launch_bounds__(kBlock)
+k_dist_stats64(const double* __restrict__ H, int C, int64_t n, int64_t rows_per, double* __restrict__ part) {
+  __shared__ double sh[2][kBlock];
+  const int t = threadIdx.x;
+  const int slots = kBlock / C;
+  const int c = t % C, slot = t / C;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per;
+  const int64_t r1 = min(r0 + rows_per, n);
+  double s = 0.0, ss = 0.0;
+  if (slot < slots)
+    for (int64_t v = r0 + slot; v < r1; v += slots) {
+      const double x = H[v * C + c];
+      s += x;
+      ss += x * x;
+    }
+  sh[0][t] = s;
+  sh[1][t] = ss;
+  __syncthreads();
+  if (t < C) {
+    double a = 0.0, b = 0.0;
+    for (int sl = 0; sl < slots; ++sl) {
+      a += sh[0][sl * C + t];
+      b += sh[1][sl * C + t];
+    }
+    part[static_cast<int64_t>(blockIdx.x) * 2 * C + t] = a;
+    part[static_cast<int64_t>(blockIdx.x) * 2 * C + C + t] = b;
+  }
+}
+
+// One block forward in fp64 for every row:
+//   xhat = (h - mean_g) inv_g,  a = max(xhat gamma_c + beta_c, 0),  h' = W a + b,
+// writing xhat and a (fp32: what the backward of the block reads) and h'
+// (fp64).  W (co x ci fp32, dense) is staged in LDS as fp64 rows of kMaxC,
+// zero-padded; one thread per row.
+__global__ void __launch_bounds__(kBlock)
+k_dist_layer64(const double* __restrict__ Hin, int ci, const double* __restrict__ stats, int groups,
+               const float* __restrict__ gamma, const float* __restrict__ beta, const float* __restrict__ W,
+               const float* __restrict__ b, int co, int64_t rows, float* __restrict__ Xh32, float* __restrict__ A32,
+               double* __restrict__ Hout) {
+  __shared__ double sw[kMaxC * kMaxC];
+  __shared__ double sb[kMaxC], smu[kMaxC], siv[kMaxC], sg[kMaxC], sbt[kMaxC];
+  for (int i = threadIdx.x; i < co * kMaxC; i += kBlock) {
+    const int o = i / kMaxC, c = i - o * kMaxC;
+    sw[i] = c < ci ? static_cast<double>(W[o * ci + c]) : 0.0;
+  }
+  for (int i = threadIdx.x; i < co; i += kBlock) sb[i] = b ? b[i] : 0.0;
+  const int per = ci / groups;
+  for (int i = threadIdx.x; i < kMaxC; i += kBlock) {
+    const bool in = i < ci;
+    smu[i] = in ? stats[2 * (i / per)] : 0.0;
+    siv[i] = in ? stats[2 * (i / per) + 1] : 0.0;
+    sg[i] = in && gamma ? gamma[i] : 1.0;
+    sbt[i] = in && beta ? beta[i] : 0.0;
+  }
+  __syncthreads();
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (r >= rows) return;
+  double a[kMaxC];
+#pragma unroll
+  for (int i = 0; i < kMaxC; ++i) {
+    const double x = i < ci ? Hin[r * ci + i] : 0.0;
+    const double xh = (x - smu[i]) * siv[i];
+    a[i] = i < ci ? fmax(xh * sg[i] + sbt[i], 0.0) : 0.0;
+    if (i < ci) {
+      Xh32[r * ci + i] = static_cast<float>(xh);
+      A32[r * ci + i] = static_cast<float>(a[i]);
+    }
+  }
+  for (int o = 0; o < co; ++o) {
+    double v = sb[o];
+#pragma unroll
+    for (int i = 0; i < kMaxC; ++i) v = fma(sw[o * kMaxC + i], a[i], v);
+    Hout[r * co + o] = v;
+  }
+}
+
+// The maximum's gradient: thread (v, c) finds the first row of J_v holding
+// channel c's maximum (fp64 rows) and writes dX[v][c] there (dH3 is zero
+// elsewhere).
+__global__ void __launch_bounds__(kBlock)
+k_dist_route_max(const int32_t* __restrict__ offsets, int64_t n, const double* __restrict__ H3, int C3,
+                 const float* __restrict__ dX, int64_t ld_dX, float* __restrict__ dH3) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n * C3) return;
+  const int64_t v = i / C3;
+  const int c = static_cast<int>(i - v * C3);
+  const int64_t b = offsets[v], e = offsets[v + 1];
+  if (b >= e) return;
+  int64_t best = b;
+  double top = H3[b * C3 + c];
+  for (int64_t r = b + 1; r < e; ++r) {
+    const double x = H3[r * C3 + c];
+    if (x > top) {
+      top = x;
+      best = r;
+    }
+  }
+  dH3[best * C3 + c] = dX[v * ld_dX + c];
+}
+
+__global__ void __launch_bounds__(kBlock)
+k_dist_zero(float* __restrict__ x, int64_t count) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * kBlock)
+    x[i] = 0.f;
+}
+
+// List position of every reference: at[entries[s]] = s.
+__global__ void __launch_bounds__(kBlock)
+k_dist_entry_at(const int32_t* __restrict__ entries, int64_t total, int32_t* __restrict__ at) {
+  const int64_t s = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (s < total) at[entries[s]] = static_cast<int32_t>(s);
+}
+
+// dF_p[c] = sum over the d+1 rows of point p (vertex slots in order) of the
+// feature part of dH0.
+__global__ void __launch_bounds__(kBlock)
+k_dist_dfeat(const int32_t* __restrict__ at, int64_t m, const float* __restrict__ dH0, int cin4, int cf,
+             float* __restrict__ dF, int64_t ld_dF) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= m * cf) return;
+  const int64_t p = i / cf;
+  const int c = static_cast<int>(i - p * cf);
+  float a = 0.f;
+  for (int k = 0; k < 4; ++k) a += dH0[static_cast<int64_t>(at[4 * p + k]) * cin4 + 3 + c];
+  dF[p * ld_dF + c] = a;
+}
+
+// Zero-padded copies of the first layer's weights (C1 x cin -> C1 x cin4)
+// and of the raw rows' gamma / beta (padding: 1 / 0).
+__global__ void __launch_bounds__(kBlock)
+k_dist_pad_params(const float* __restrict__ W1, int C1, int cin, int cin4, const float* __restrict__ gamma,
+                  const float* __restrict__ beta, float* __restrict__ W1p, float* __restrict__ gp,
+                  float* __restrict__ bp) {
+  for (int i = threadIdx.x; i < C1 * cin4; i += kBlock) {
+    const int o = i / cin4, c = i - o * cin4;
+    W1p[i] = c < cin ? W1[o * cin + c] : 0.f;
+  }
+  for (int c = threadIdx.x; c < cin4; c += kBlock) {
+    gp[c] = c < cin && gamma ? gamma[c] : 1.f;
+    bp[c] = c < cin && beta ? beta[c] : 0.f;
+  }
+}
+
+// rows per workgroup of k_dist_stats64 and the number of workgroups
+void stats64_parts(int64_t n, int C, int64_t* nparts, int64_t* rows_per) {
+  const int slots = kBlock / C;
+  int64_t rp = std::max<int64_t>(slots, (n + kStatsMaxParts - 1) / kStatsMaxParts);
+  rp = (rp + slots - 1) / slots * slots;
+  *rows_per = rp;
+  *nparts = std::max<int64_t>(1, (n + rp - 1) / rp);
+}
+
+inline unsigned grid_rows(int64_t rows) {
+  return static_cast<unsigned>(std::max<int64_t>(1, (rows + kBlock - 1) / kBlock));
+}
+
 }  // namespace
 
 // Work space: the vertex means (n double4), the mean pass's span partials, the
@@ -828,6 +1019,144 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
   if (out_bf16)
     launch(k_dist_to_bf16, dim3(static_cast<unsigned>(std::min<int64_t>((n * C3 / 4 + kBlock - 1) / kBlock, 4096))),
            dim3(kBlock), 0, s, static_cast<const float*>(out), n, C3, static_cast<uint16_t*>(out_dev), ld_out_dev);
+}
+
+}  // namespace lat
+
+namespace lat {
+
+// Work space of the backward, carved in this order (each piece 256-byte
+// aligned): means, mean partials, entry vertices, list positions, two fp64
+// row buffers, the blocks' normalised inputs and activations (fp32), dH3, two gradient
+// buffers, padded parameters, normalisation tables, stats, coefficients,
+// statistics partials, linear-layer partials.
+int64_t distribute_backward_workspace_bytes(int64_t n, int64_t m, int64_t total, int cf, int C1, int C2, int C3) {
+  auto up = [](int64_t b) { return (b + 255) / 256 * 256; };
+  const int cin4 = (3 + cf + 3) / 4 * 4;
+  const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
+  const int64_t widest = std::max<int64_t>(std::max(cin4, C1), std::max(C2, C3));
+  int64_t b = up(32 * n) + up(2 * mean_spans * 32) + up(4 * total) + up(4 * std::max<int64_t>(4 * m, 1));
+  b += 2 * up(8 * total * widest);
+  b += 2 * (up(4 * total * cin4) + up(4 * total * C1) + up(4 * total * C2));
+  b += up(4 * total * C3) + 2 * up(4 * total * widest);
+  b += up(4 * (C1 * cin4 + 2 * cin4 + 2 * cin4));
+  b += 3 * up(4 * 2 * widest) + 3 * up(8 * 2 * widest) + up(4 * 4 * widest);
+  // k_dist_stats64 runs at most kStatsMaxParts workgroups
+  b += up(std::max<int64_t>(gn_workspace_bytes(total, static_cast<int>(widest)), kStatsMaxParts * 2 * widest * 8));
+  int64_t lin = 0;
+  const int ks[3] = {C1, C2, C3}, cs[3] = {cin4, C1, C2};
+  for (int i = 0; i < 3; ++i) lin = std::max(lin, classify_backward_partial_floats(total, ks[i], cs[i]));
+  b += up(4 * lin);
+  return b;
+}
+
+void launch_distribute_backward(const int32_t* offsets, const int32_t* entries, const int32_t* chunk_first, int chunk,
+                                int64_t n, int64_t m, int64_t total, const float* pos, const double scale[3],
+                                const float* feat, int64_t ld_feat, int cf, const float* gamma, const float* beta,
+                                float eps, const float* W1, const float* b1, int C1, const float* W2, const float* b2,
+                                int C2, const float* W3, const float* b3, int C3, const float* dX, int64_t ld_dX,
+                                float* dF, int64_t ld_dF, float* dW1, float* db1, float* dW2, float* db2, float* dW3,
+                                float* db3, float* dgamma, float* dbeta, void* work, hipStream_t s) {
+  ScopedKernelTimer tm("distribute_bwd", s);
+  auto up = [](int64_t b) { return (b + 255) / 256 * 256; };
+  const int cin = 3 + cf, cin4 = (cin + 3) / 4 * 4;
+  const int64_t mean_spans = (total + kMeanSpan - 1) / kMeanSpan;
+  const int64_t widest = std::max<int64_t>(std::max(cin4, C1), std::max(C2, C3));
+  char* w = static_cast<char*>(work);
+  auto take = [&](int64_t bytes) {
+    char* p = w;
+    w += up(bytes);
+    return p;
+  };
+  double4* mu4 = reinterpret_cast<double4*>(take(32 * n));
+  double4* mh = reinterpret_cast<double4*>(take(2 * mean_spans * 32));
+  double4* mt = mh + mean_spans;
+  int32_t* ev = reinterpret_cast<int32_t*>(take(4 * total));
+  int32_t* at = reinterpret_cast<int32_t*>(take(4 * std::max<int64_t>(4 * m, 1)));
+  double* h64[2] = {reinterpret_cast<double*>(take(8 * total * widest)),
+                    reinterpret_cast<double*>(take(8 * total * widest))};
+  const int ci[3] = {cin4, C1, C2}, co[3] = {C1, C2, C3};
+  float* Xh32[3];   // each block's normalised input
+  float* A32[3];    // and its activation
+  for (int i = 0; i < 3; ++i) Xh32[i] = reinterpret_cast<float*>(take(4 * total * ci[i]));
+  for (int i = 0; i < 3; ++i) A32[i] = reinterpret_cast<float*>(take(4 * total * ci[i]));
+  float* dH3 = reinterpret_cast<float*>(take(4 * total * C3));
+  float* gA = reinterpret_cast<float*>(take(4 * total * widest));
+  float* gB = reinterpret_cast<float*>(take(4 * total * widest));
+  float* W1p = reinterpret_cast<float*>(take(4 * (C1 * cin4 + 2 * cin4 + 2 * cin4)));
+  float* g0p = W1p + C1 * cin4;
+  float* b0p = g0p + cin4;
+  float* dg0 = b0p + cin4;
+  float* db0 = dg0 + cin4;
+  float* pre[3];
+  double* stats[3];
+  for (int i = 0; i < 3; ++i) pre[i] = reinterpret_cast<float*>(take(4 * 2 * widest));
+  for (int i = 0; i < 3; ++i) stats[i] = reinterpret_cast<double*>(take(8 * 2 * widest));
+  float* coef = reinterpret_cast<float*>(take(4 * 4 * widest));
+  void* gnw = take(std::max<int64_t>(gn_workspace_bytes(total, static_cast<int>(widest)), kStatsMaxParts * 2 * widest * 8));
+  float* part = reinterpret_cast<float*>(w);
+
+  auto groups = [](int C) { return C <= 32 ? C : 32; };
+  const float* gam[3] = {g0p, gamma ? gamma + cin : nullptr, gamma ? gamma + cin + C1 : nullptr};
+  const float* bet[3] = {b0p, beta ? beta + cin : nullptr, beta ? beta + cin + C1 : nullptr};
+  const float* Ws[3] = {W1p, W2, W3};
+  const float* bs[3] = {b1, b2, b3};
+  float* dWs[3] = {dW1, dW2, dW3};
+  float* dbs[3] = {db1, db2, db3};
+  const int wout[3] = {cin, C1, C2};
+  float* dgam[3] = {dg0, dgamma ? dgamma + cin : nullptr, dgamma ? dgamma + cin + C1 : nullptr};
+  float* dbet[3] = {db0, dbeta ? dbeta + cin : nullptr, dbeta ? dbeta + cin + C1 : nullptr};
+
+  // forward in fp64, keeping every block's input and activation
+  launch(k_dist_pad_params, dim3(1), dim3(kBlock), 0, s, W1, C1, cin, cin4, gamma, beta, W1p, g0p, b0p);
+  if (total > 0) {
+    launch(k_dist_mean, dim3(static_cast<unsigned>(mean_spans)), dim3(kBlock), 0, s, offsets, entries, chunk_first,
+           chunk, n, total, pos, scale[0], scale[1], scale[2], mu4, mh, mt, ev, INT64_MAX, static_cast<float*>(nullptr),
+           static_cast<int64_t>(0), 0);
+    if (mean_spans > 1)
+      launch(k_dist_mean_finish, dim3(static_cast<unsigned>((mean_spans + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
+             offsets, chunk_first, chunk, mean_spans, mu4, static_cast<const double4*>(mh),
+             static_cast<const double4*>(mt));
+    launch(k_dist_raw_rows64, dim3(grid_rows(total)), dim3(kBlock), 0, s, entries, static_cast<const int32_t*>(ev),
+           total, pos, scale[0], scale[1], scale[2], static_cast<const double4*>(mu4), feat, ld_feat, cf, cin4, h64[0]);
+  }
+  for (int i = 0; i < 3; ++i) {
+    int64_t np, rp;
+    stats64_parts(total, ci[i], &np, &rp);
+    double* gpart = static_cast<double*>(gnw);
+    if (total > 0)
+      launch(k_dist_stats64, dim3(static_cast<unsigned>(np)), dim3(kBlock), 0, s, static_cast<const double*>(h64[i & 1]),
+             ci[i], total, rp, gpart);
+    launch_gn_finalize(gpart, np, ci[i], groups(ci[i]), total, gam[i], bet[i], eps, pre[i], s, stats[i]);
+    if (total > 0)
+      launch(k_dist_layer64, dim3(grid_rows(total)), dim3(kBlock), 0, s, static_cast<const double*>(h64[i & 1]), ci[i],
+             static_cast<const double*>(stats[i]), groups(ci[i]), gam[i], bet[i], Ws[i], bs[i], co[i], total, Xh32[i],
+             A32[i], h64[(i + 1) & 1]);
+  }
+  // the maximum, then the three blocks backward in fp32
+  const unsigned zg = static_cast<unsigned>(std::min<int64_t>(8192, (total * C3 + kBlock - 1) / kBlock + 1));
+  launch(k_dist_zero, dim3(zg), dim3(kBlock), 0, s, dH3, total * C3);
+  if (n > 0)
+    launch(k_dist_route_max, dim3(grid_rows(n * C3)), dim3(kBlock), 0, s, offsets, n,
+           static_cast<const double*>(h64[1]), C3, dX, ld_dX, dH3);
+  const float* g = dH3;
+  for (int i = 2; i >= 0; --i) {
+    // dA = g W_i, dW_i, db_i on the activations; then dH_i = GroupNorm +
+    // ReLU backward of dA
+    launch_linear_backward(g, co[i], Ws[i], co[i], ci[i], total, A32[i], ci[i], nullptr, gA, ci[i], dWs[i], wout[i],
+                           dbs[i], part, s);
+    launch_gn_backward(Xh32[i], ci[i], gA, ci[i], ci[i], groups(ci[i]), total, gam[i], nullptr, stats[i], dgam[i],
+                       dbet[i], coef, gB, ci[i], gnw, s, A32[i], ci[i], true);
+    g = gB;   // read by the next block's linear backward, which writes gA again
+  }
+  // g now holds dH0 (total x cin4)
+  if (dgamma) (void)hipMemcpyAsync(dgamma, dg0, sizeof(float) * cin, hipMemcpyDeviceToDevice, s);
+  if (dbeta) (void)hipMemcpyAsync(dbeta, db0, sizeof(float) * cin, hipMemcpyDeviceToDevice, s);
+  if (dF && cf > 0 && m > 0) {
+    launch(k_dist_entry_at, dim3(grid_rows(total)), dim3(kBlock), 0, s, entries, total, at);
+    launch(k_dist_dfeat, dim3(grid_rows(m * cf)), dim3(kBlock), 0, s, static_cast<const int32_t*>(at), m, g, cin4,
+           cf, dF, ld_dF);
+  }
 }
 
 }  // namespace lat

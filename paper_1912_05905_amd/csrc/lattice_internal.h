@@ -201,6 +201,17 @@ int distribute_max_features();
 // scale: sigma per axis at the lattice's level (positions enter as pos / scale);
 // gamma / beta: optional per-channel parameters of the three GroupNorms,
 // concatenated ((3 + cf) + C1 + C2 values)
+// Distribute + PointNet backward (dL/dx = dX, n x C3): dF (m x cf), the
+// layers' dW ([out][in]) and db, dgamma / dbeta (concatenated as gamma); any
+// output may be NULL.  work holds distribute_backward_workspace_bytes.
+int64_t distribute_backward_workspace_bytes(int64_t n, int64_t m, int64_t total, int cf, int C1, int C2, int C3);
+void launch_distribute_backward(const int32_t* offsets, const int32_t* entries, const int32_t* chunk_first, int chunk,
+                                int64_t n, int64_t m, int64_t total, const float* pos, const double scale[3],
+                                const float* feat, int64_t ld_feat, int cf, const float* gamma, const float* beta,
+                                float eps, const float* W1, const float* b1, int C1, const float* W2, const float* b2,
+                                int C2, const float* W3, const float* b3, int C3, const float* dX, int64_t ld_dX,
+                                float* dF, int64_t ld_dF, float* dW1, float* db1, float* dW2, float* db2, float* dW3,
+                                float* db3, float* dgamma, float* dbeta, void* work, hipStream_t s);
 void launch_distribute(const int32_t* offsets, const int32_t* entries, const int32_t* chunk_first, int chunk,
                        int64_t n, int64_t total, const float* pos, const double scale[3], const float* feat,
                        int64_t ld_feat, int cf, const float* gamma, const float* beta, float eps, const float* W1,
@@ -235,6 +246,15 @@ void launch_gn_affine(const void* x, int64_t ld, int C, int bf16, int64_t n, int
 // m x C dense): df = z Wc (m x C dense), dWc = z^T f, dbc = column sums of
 // z (either may be NULL); part holds classify_backward_partial_floats
 int64_t classify_backward_partial_floats(int64_t m, int K, int C);
+// backward of out_p = W a_p + b over m rows (W: K x C [out][in], dense, 16-byte
+// aligned, C a multiple of 4) for z = dL/dout (m x K, row stride ld_z):
+// df = z W (m x C, row stride ld_df; NULL: skipped), dW = z^T a written as
+// K x C_out (the first C_out columns), db = column sums of z (either NULL:
+// skipped).  a = f (row stride ld_f), or max(f scale + shift, 0) with pre =
+// [C scales][C shifts].  part holds classify_backward_partial_floats(m, K, C).
+void launch_linear_backward(const float* z, int64_t ld_z, const float* W, int K, int C, int64_t m, const float* f,
+                            int64_t ld_f, const float* pre, float* df, int64_t ld_df, float* dW, int C_out, float* db,
+                            float* part, hipStream_t s);
 void launch_classify_backward(const float* z, int64_t ld_z, const float* Wc, int K, int C, int64_t m, const float* f,
                               float* df, float* dWc, float* dbc, float* part, hipStream_t s);
 // a = max(x pre[c] + pre[C + c], 0) for fp32 x (n x C), the pre-activated
@@ -243,13 +263,17 @@ void launch_gn_relu_apply(const float* x, int64_t ldx, int C, int64_t n, const f
                           hipStream_t s);
 // GroupNorm + ReLU backward from dA = dL/d(pre-activated input): dgamma,
 // dbeta (optional, C floats), dX (optional, n x C, row stride lddx); coef
-// is a 4 C float work array; work holds gn_workspace_bytes(n, C)
+// is a 4 C float work array; work holds gn_workspace_bytes(n, C).  The ReLU
+// passed where act > 0 when the forward's activations act (n x C, row
+// stride ldact) are given, else where x pre[c] + pre[C + c] > 0.  With
+// xhat the rows x are given already normalised ((x - mean_g) inv_g).
 void launch_gn_backward(const float* x, int64_t ldx, const float* dA, int64_t lda, int C, int groups, int64_t n,
                         const float* gamma, const float* pre, const double* stats, float* dgamma, float* dbeta,
-                        float* coef, float* dX, int64_t lddx, void* work, hipStream_t s);
+                        float* coef, float* dX, int64_t lddx, void* work, hipStream_t s,
+                        const float* act = nullptr, int64_t ldact = 0, bool xhat = false);
 // per-group statistics from nparts partials (part[w][0..C) sums, part[w][C..2C)
 // sums of squares over `rows` rows) -> pre[0..C) scales, pre[C..2C) shifts
 void launch_gn_finalize(const double* part, int64_t nparts, int C, int groups, int64_t rows, const float* gamma,
-                        const float* beta, float eps, float* pre, hipStream_t s);
+                        const float* beta, float eps, float* pre, hipStream_t s, double* stats = nullptr);
 
 }  // namespace lat

@@ -151,12 +151,15 @@ k_gn_relu_apply(const float* __restrict__ x, int64_t ldx, int C, int64_t n, cons
 // Backward of GroupNorm + ReLU, first pass: per-channel sums over the rows
 // of workgroup w's range (fp64, rows in the order of k_gn_partial)
 //   S1_c = sum g,  S2_c = sum g xhat,
-// g = dA where x scale_c + shift_c > 0 (else 0), xhat = (x - mean_g) inv_g;
+// g = dA where the ReLU passed (else 0), xhat = (x - mean_g) inv_g (x itself
+// when the rows given are already normalised); the ReLU passed where act > 0
+// when the activations act are given, else where x scale_c + shift_c > 0.
 // part[w][0..C) holds S1, part[w][C..2C) S2.
 __global__ void __launch_bounds__(kBlock)
 k_gn_bwd_partial(const float* __restrict__ x, int64_t ldx, const float* __restrict__ dA, int64_t lda, int C,
                  int groups, int64_t n, int64_t rows_per, const float* __restrict__ pre,
-                 const double* __restrict__ stats, double* __restrict__ part) {
+                 const float* __restrict__ act, int64_t ldact, const double* __restrict__ stats, int xhat,
+                 double* __restrict__ part) {
   __shared__ double sh[2][kBlock][4];
   const int t = threadIdx.x;
   const int quads = C / 4;
@@ -172,18 +175,26 @@ k_gn_bwd_partial(const float* __restrict__ x, int64_t ldx, const float* __restri
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int c = 4 * q + i;
-      sc[i] = pre[c];
-      sf[i] = pre[C + c];
-      mu[i] = stats[2 * (c / per)];
-      iv[i] = stats[2 * (c / per) + 1];
+      sc[i] = pre ? pre[c] : 0.f;
+      sf[i] = pre ? pre[C + c] : 0.f;
+      mu[i] = xhat ? 0.0 : stats[2 * (c / per)];
+      iv[i] = xhat ? 1.0 : stats[2 * (c / per) + 1];
     }
     for (int64_t v = r0 + slot; v < r1; v += slots) {
       const float4 a = *reinterpret_cast<const float4*>(x + v * ldx + 4 * q);
       const float4 d = *reinterpret_cast<const float4*>(dA + v * lda + 4 * q);
       const float xv[4] = {a.x, a.y, a.z, a.w}, dv[4] = {d.x, d.y, d.z, d.w};
+      bool on[4];
+      if (act) {
+        const float4 u = *reinterpret_cast<const float4*>(act + v * ldact + 4 * q);
+        on[0] = u.x > 0.f; on[1] = u.y > 0.f; on[2] = u.z > 0.f; on[3] = u.w > 0.f;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) on[i] = fmaf(xv[i], sc[i], sf[i]) > 0.f;
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const double g = fmaf(xv[i], sc[i], sf[i]) > 0.f ? static_cast<double>(dv[i]) : 0.0;
+        const double g = on[i] ? static_cast<double>(dv[i]) : 0.0;
         s[i] += g;
         ss[i] += g * ((static_cast<double>(xv[i]) - mu[i]) * iv[i]);
       }
@@ -218,11 +229,12 @@ k_gn_bwd_partial(const float* __restrict__ x, int64_t ldx, const float* __restri
 //   dX = g c1 + c0 + (x - mean) cx,
 //   c1 = inv gamma_c,  c0 = -inv A,  cx = -inv^2 B,
 //   A = sum_c gamma_c S1_c / N,  B = sum_c gamma_c S2_c / N  (N = n per),
-// stored as coef[c] = (c1, c0, cx, mean).
+// stored as coef[c] = (c1, c0, cx, mean); for rows given normalised,
+// dX = g c1 + c0 + xhat (-inv B), stored as (c1, c0, -inv B, 0).
 __global__ void __launch_bounds__(kBlock)
 k_gn_bwd_finalize(const double* __restrict__ part, int nparts, int C, int groups, int64_t n,
-                  const float* __restrict__ gamma, const double* __restrict__ stats, float* __restrict__ dgamma,
-                  float* __restrict__ dbeta, float4* __restrict__ coef) {
+                  const float* __restrict__ gamma, const double* __restrict__ stats, int xhat,
+                  float* __restrict__ dgamma, float* __restrict__ dbeta, float4* __restrict__ coef) {
   __shared__ double sh[2][kBlock];
   __shared__ double tot[2][kBlock];
   __shared__ double ab[2];
@@ -275,7 +287,8 @@ k_gn_bwd_finalize(const double* __restrict__ part, int nparts, int C, int groups
     for (int c = g * per + t; c < (g + 1) * per; c += kBlock) {
       const double gm = gamma ? gamma[c] : 1.0;
       coef[c] = make_float4(static_cast<float>(inv * gm), static_cast<float>(-inv * ab[0]),
-                            static_cast<float>(-inv * inv * ab[1]), static_cast<float>(mean));
+                            static_cast<float>(xhat ? -inv * ab[1] : -inv * inv * ab[1]),
+                            static_cast<float>(xhat ? 0.0 : mean));
     }
   }
 }
@@ -283,7 +296,8 @@ k_gn_bwd_finalize(const double* __restrict__ part, int nparts, int C, int groups
 // Third pass: dX = g c1 + c0 + (x - mean) cx, with g = dA masked as above.
 __global__ void __launch_bounds__(kBlock)
 k_gn_bwd_apply(const float* __restrict__ x, int64_t ldx, const float* __restrict__ dA, int64_t lda, int C, int64_t n,
-               const float* __restrict__ pre, const float4* __restrict__ coef, float* __restrict__ dX, int64_t lddx) {
+               const float* __restrict__ pre, const float* __restrict__ act, int64_t ldact,
+               const float4* __restrict__ coef, float* __restrict__ dX, int64_t lddx) {
   const int quads = C / 4;
   const int64_t total = n * quads;
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < total;
@@ -293,10 +307,18 @@ k_gn_bwd_apply(const float* __restrict__ x, int64_t ldx, const float* __restrict
     const float4 a = *reinterpret_cast<const float4*>(x + v * ldx + c);
     const float4 d = *reinterpret_cast<const float4*>(dA + v * lda + c);
     const float xv[4] = {a.x, a.y, a.z, a.w}, dv[4] = {d.x, d.y, d.z, d.w};
+    bool on[4];
+    if (act) {
+      const float4 u = *reinterpret_cast<const float4*>(act + v * ldact + c);
+      on[0] = u.x > 0.f; on[1] = u.y > 0.f; on[2] = u.z > 0.f; on[3] = u.w > 0.f;
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) on[k] = fmaf(xv[k], pre[c + k], pre[C + c + k]) > 0.f;
+    }
     float o[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const float g = fmaf(xv[k], pre[c + k], pre[C + c + k]) > 0.f ? dv[k] : 0.f;
+      const float g = on[k] ? dv[k] : 0.f;
       const float4 cf = coef[c + k];
       o[k] = fmaf(xv[k] - cf.w, cf.z, fmaf(g, cf.x, cf.y));
     }
@@ -320,10 +342,9 @@ void gn_parts(int64_t n, int C, int bf16, int64_t* nparts, int64_t* rows_per) {
 }  // namespace
 
 void launch_gn_finalize(const double* part, int64_t nparts, int C, int groups, int64_t rows, const float* gamma,
-                        const float* beta, float eps, float* pre, hipStream_t s) {
+                        const float* beta, float eps, float* pre, hipStream_t s, double* stats) {
   launch(k_gn_finalize, dim3(static_cast<unsigned>(groups)), dim3(kBlock), 0, s, part,
-         rows > 0 ? static_cast<int>(nparts) : 0, C, groups, rows, gamma, beta, eps, pre,
-         static_cast<double*>(nullptr));
+         rows > 0 ? static_cast<int>(nparts) : 0, C, groups, rows, gamma, beta, eps, pre, stats);
 }
 
 int gn_max_channels() { return 4 * kBlock; }
@@ -357,19 +378,20 @@ void launch_gn_relu_apply(const float* x, int64_t ldx, int C, int64_t n, const f
 
 void launch_gn_backward(const float* x, int64_t ldx, const float* dA, int64_t lda, int C, int groups, int64_t n,
                         const float* gamma, const float* pre, const double* stats, float* dgamma, float* dbeta,
-                        float* coef, float* dX, int64_t lddx, void* work, hipStream_t s) {
+                        float* coef, float* dX, int64_t lddx, void* work, hipStream_t s, const float* act,
+                        int64_t ldact, bool xhat) {
   ScopedKernelTimer tm("groupnorm_bwd", s);
   int64_t np, rp;
   gn_parts(n, C, 0, &np, &rp);
   double* part = static_cast<double*>(work);
   if (n > 0)
     launch(k_gn_bwd_partial, dim3(static_cast<unsigned>(np)), dim3(kBlock), 0, s, x, ldx, dA, lda, C, groups, n, rp,
-           pre, stats, part);
+           pre, act, ldact, stats, xhat ? 1 : 0, part);
   launch(k_gn_bwd_finalize, dim3(static_cast<unsigned>(groups)), dim3(kBlock), 0, s,
-         static_cast<const double*>(part), n > 0 ? static_cast<int>(np) : 0, C, groups, n, gamma, stats, dgamma,
-         dbeta, dX ? reinterpret_cast<float4*>(coef) : nullptr);
+         static_cast<const double*>(part), n > 0 ? static_cast<int>(np) : 0, C, groups, n, gamma, stats, xhat ? 1 : 0,
+         dgamma, dbeta, dX ? reinterpret_cast<float4*>(coef) : nullptr);
   if (dX && n > 0)
-    launch(k_gn_bwd_apply, dim3(elementwise_grid(n, C)), dim3(kBlock), 0, s, x, ldx, dA, lda, C, n, pre,
+    launch(k_gn_bwd_apply, dim3(elementwise_grid(n, C)), dim3(kBlock), 0, s, x, ldx, dA, lda, C, n, pre, act, ldact,
            reinterpret_cast<const float4*>(coef), dX, lddx);
 }
 

@@ -63,6 +63,9 @@ SIGNATURES = {
                                             _P, _I64, _P, _I64, _P, _P, _P, _P, _P]),
     "lattice_deform_slice_classify_backward": (_I32, [_P, _P, _I64, _I32, _P, _F32, _P, _I32, _P, _I64, _P, _I64,
                                                       _P, _P, _P, _P, _P]),
+    "lattice_distribute_pointnet_backward": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, C.c_float, _P, _P, _I32, _P, _P,
+                                                    _I32, _P, _P, _I32, _P, _I64, _P, _I64, _P, _P, _P, _P, _P, _P,
+                                                    _P, _P, _P]),
     "lattice_deform_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _F32, _P, _I64, _P, _I64, _P, _P, _P]),
     "lattice_timing_enable": (_I32, [C.c_char_p, _I32]),
     "lattice_timing_read": (_I32, [C.c_char_p, C.POINTER(_I64), C.POINTER(C.c_double)]),
@@ -422,6 +425,33 @@ class Lattice:
                                                   gld, dp, dld, ptr(dW), ptr(db), ptr(dg), ptr(dbe),
                                                   _stream(stream)))
         return dx, dW, db, dg, dbe
+
+    def distribute_pointnet_backward(self, pos: torch.Tensor, feat: torch.Tensor | None, layers, dx: torch.Tensor,
+                                     gn=None, eps: float = 1e-5, stream=None) -> dict:
+        """Gradients of distribute_pointnet(pos, feat, layers, gn, eps) for
+        dL/dx = dx (n x C3): a dict with dF (m x Cf, None without features),
+        dW1..dW3 ([out][in]), db1..db3, dgamma and dbeta (concatenated as
+        gn)."""
+        (W1, b1), (W2, b2), (W3, b3) = layers
+        c1, c2, c3 = W1.shape[0], W2.shape[0], W3.shape[0]
+        cf = 0 if feat is None else feat.shape[1]
+        gam, bet = (None, None) if gn is None else gn
+        dev = dict(dtype=torch.float32, device="cuda")
+        ng = 3 + cf + c1 + c2
+        out = dict(dF=torch.empty((self.m, cf), **dev) if cf else None, dW1=torch.empty_like(W1),
+                   db1=torch.empty((c1,), **dev), dW2=torch.empty_like(W2), db2=torch.empty((c2,), **dev),
+                   dW3=torch.empty_like(W3), db3=torch.empty((c3,), **dev), dgamma=torch.empty((ng,), **dev),
+                   dbeta=torch.empty((ng,), **dev))
+        fp, fld = (None, 0) if feat is None else _rows(feat)
+        dfp, dfld = (None, 0) if out["dF"] is None else _rows(out["dF"])
+        xp, xld = _rows(dx)
+        ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
+        _check(lib().lattice_distribute_pointnet_backward(
+            self._h, ptr(pos), fp, fld, cf, ptr(gam), ptr(bet), float(eps), ptr(W1), ptr(b1), c1, ptr(W2), ptr(b2),
+            c2, ptr(W3), ptr(b3), c3, xp, xld, dfp, dfld, ptr(out["dW1"]), ptr(out["db1"]), ptr(out["dW2"]),
+            ptr(out["db2"]), ptr(out["dW3"]), ptr(out["db3"]), ptr(out["dgamma"]), ptr(out["dbeta"]),
+            _stream(stream)))
+        return out
 
     def deform_slice_backward(self, x: torch.Tensor, wv: torch.Tensor, beta: float, dout: torch.Tensor,
                               dx_out: torch.Tensor | None = None, stream=None):

@@ -1244,3 +1244,99 @@ def test_deform_slice_classify_backward_tiny_and_strided_logits(L, O):
         P.assert_close(P.rows_in_oracle_order(_host(gdx), g2o), odx, P.TOL_F32, f"classifier backward dX m={m}")
         P.assert_close(_host(gdWc), odWc, P.TOL_F32, f"classifier backward dWc m={m}")
         P.assert_close(_host(gdbc), odbc, P.TOL_F32, f"classifier backward dbc m={m}")
+
+
+# ----------------------------------------------------------------------------
+# backward of Distribute + PointNet
+# ----------------------------------------------------------------------------
+def _distribute_backward_case(L, O, gl, ol, g2o, pos, F, widths, seed, affine=True):
+    rng = np.random.default_rng(seed)
+    cf = 0 if F is None else F.shape[1]
+    layers = _pointnet_layers(rng, 3 + cf, widths)
+    tot = 3 + cf + widths[0] + widths[1]
+    gn = ((1.0 + 0.1 * rng.normal(size=tot)).astype(np.float32), (0.1 * rng.normal(size=tot)).astype(np.float32)) \
+        if affine else None
+    lay64 = [(W.astype(np.float64), b.astype(np.float64)) for W, b in layers]
+    gn64 = None if gn is None else tuple(a.astype(np.float64) for a in gn)
+    F64 = None if F is None else F.astype(np.float64)
+    D = rng.normal(size=(ol.n, widths[2])).astype(np.float32)
+    # Where a vertex's two largest rows of a channel lie within 1e-6 of its
+    # output's scale, either is a correct choice for the maximum: the
+    # upstream gradient is zero there, so the gradients are unique.
+    X = ol.distribute_pointnet(pos.astype(np.float64), F64, lay64, gn64)
+    margin = ol.distribute_pointnet_backward(pos.astype(np.float64), F64, lay64, D, gn64)["margin"]
+    near = margin < 1e-6 * np.sqrt(np.mean(X ** 2))
+    D[near] = 0.0
+    ref = ol.distribute_pointnet_backward(pos.astype(np.float64), F64, lay64, D.astype(np.float64), gn64)
+    got = gl.distribute_pointnet_backward(_dev(pos), None if F is None else _dev(F),
+                                          [(_dev(W), _dev(b)) for W, b in layers], _dev(D[g2o]),
+                                          None if gn is None else (_dev(gn[0]), _dev(gn[1])))
+    what = f"Distribute backward cf={cf} widths={widths}"
+    for k in ("dW1", "dW2", "dW3", "db3", "dgamma"):
+        P.assert_close(_host(got[k]), ref[k], P.TOL_F32, f"{k} {what}")
+    # Without the affine parameters (beta = 0) the coordinate channels of a
+    # vertex with a single point sit exactly on the ReLU's kink (g - mu_v = 0
+    # and the rows' mean is 0 in exact arithmetic, so the sign of the
+    # normalised value is rounding noise): their dbeta is not unique.
+    lo = 0 if affine else 3
+    P.assert_close(_host(got["dbeta"])[lo:], ref["dbeta"][lo:], P.TOL_F32, f"dbeta {what}")
+    for i in (1, 2):
+        db, dW = _host(got[f"db{i}"]), ref[f"dW{i}"]
+        if widths[i - 1] <= 32:
+            # the next normalisation has one channel per group and removes
+            # any per-channel shift, so this bias gradient is exactly zero: a
+            # sum that cancels, whose float32 error scales with its terms
+            # (measured by the layer's weight gradient)
+            scale = float(np.sqrt(np.mean(dW ** 2)))
+            assert np.abs(ref[f"db{i}"]).max() <= 1e-9 * scale, what
+            assert np.abs(db).max() <= P.TOL_F32 * scale, (f"db{i} {what}", np.abs(db).max(), scale)
+        else:
+            P.assert_close(db, ref[f"db{i}"], P.TOL_F32, f"db{i} {what}")
+    if cf:
+        P.assert_close(_host(got["dF"]), ref["dF"], P.TOL_F32, f"dF {what}")
+    return int(near.sum())
+
+
+@pytest.mark.parametrize("cf,widths,affine", [(4, (16, 32, 64), True), (0, (16, 32, 64), True),
+                                               (13, (32, 32, 48), False), (29, (64, 64, 64), True),
+                                               (1, (64, 32, 16), True)])
+def test_distribute_pointnet_backward(L, O, cf, widths, affine):
+    pos = _cloud(1700 + cf, 6000, 0.7)
+    gl, ol, g2o = _pair(L, O, pos, 0.06)
+    rng = np.random.default_rng(cf)
+    F = rng.normal(size=(pos.shape[0], cf)).astype(np.float32) if cf else None
+    _distribute_backward_case(L, O, gl, ol, g2o, pos, F, widths, 17 + cf, affine)
+
+
+def test_distribute_pointnet_backward_skewed_and_tiny(L, O):
+    """A clump of 3000 points in one simplex beside a spread cloud (lists of
+    very different lengths), a coarse level, and a one-point cloud."""
+    rng = np.random.default_rng(7)
+    clump = (np.array([0.31, 0.42, 0.53]) + 1e-4 * rng.random((3000, 3))).astype(np.float32)
+    spread = rng.random((2001, 3)).astype(np.float32)
+    pos = np.concatenate([spread[:1000], clump, spread[1000:]]).astype(np.float32)
+    F = rng.normal(size=(pos.shape[0], 4)).astype(np.float32)
+    gl, ol, g2o = _pair(L, O, pos, 0.05)
+    _distribute_backward_case(L, O, gl, ol, g2o, pos, F, (16, 32, 64), 21)
+    gc, oc = gl.coarsen(), ol.coarsen()
+    g2o_c = P.key_permutation(_host(gc.keys()), oc.keys())
+    _distribute_backward_case(L, O, gc, oc, g2o_c, pos, F, (16, 32, 64), 22)
+    pos5 = _cloud(1751, 5, 0.5)
+    g5, o5, g2o5 = _pair(L, O, pos5, 0.1)
+    _distribute_backward_case(L, O, g5, o5, g2o5, pos5, rng.normal(size=(5, 2)).astype(np.float32), (16, 16, 16), 24)
+    # one point: its d+1 rows share the features and every coordinate row
+    # is 0, so each normalisation sees identical rows and every gradient
+    # before the last layer cancels exactly; the last layer's are unique
+    pos1 = _cloud(1750, 1, 0.5)
+    g1, o1, g2o1 = _pair(L, O, pos1, 0.1)
+    lay = _pointnet_layers(np.random.default_rng(25), 5, (16, 16, 16))
+    F1 = rng.normal(size=(1, 2)).astype(np.float32)
+    D = np.random.default_rng(26).normal(size=(o1.n, 16))
+    ref = o1.distribute_pointnet_backward(pos1.astype(np.float64), F1.astype(np.float64),
+                                          [(W.astype(np.float64), b.astype(np.float64)) for W, b in lay], D)
+    got = g1.distribute_pointnet_backward(_dev(pos1), _dev(F1), [(_dev(W), _dev(b)) for W, b in lay],
+                                          _dev(D[g2o1].astype(np.float32)))
+    for k in ("dW3", "db3"):
+        P.assert_close(_host(got[k]), ref[k], P.TOL_F32, f"one-point Distribute backward {k}")
+    for k in ("dF", "dW1", "db1", "dW2", "db2", "dgamma", "dbeta"):
+        assert np.isfinite(_host(got[k])).all(), k
