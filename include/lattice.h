@@ -372,6 +372,19 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
                           float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream);
 
 /*
+ * lattice_conv_backward for a bfloat16 (or float32) network: X, W, Y, dY and
+ * dX are of dtype dt (LAT_BF16: channels and row strides multiples of 8).
+ * dX is the adjoint convolution on the matrix cores with bfloat16 operands
+ * and float32 accumulation, rounded to dt once; dW and dbias stay float32
+ * (the bfloat16 values are widened exactly and summed in float32).  Other
+ * arguments and rules as for lattice_conv_backward.
+ */
+int lattice_conv_backward_ex(lattice_t dst, lattice_t src, const void* X_dev, int64_t ld_X, int Cin, const void* W_dev,
+                             int Cout, lat_dtype dt, int flags, const void* Y_dev, int64_t ld_Y, const void* dY_dev,
+                             int64_t ld_dY, void* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev,
+                             hipStream_t stream);
+
+/*
  * Backward of the pre-activated convolution (Implementation: Group
  * Normalization with a ReLU before every convolution) for
  *   Y = act(conv(relu(GN(X)), W) + bias)

@@ -1360,10 +1360,14 @@ int lattice_slice_backward(lattice_t L, const float* dOut_dev, int64_t ld_dOut, 
 namespace {
 
 // The body of lattice_conv_backward once both lattices are in use on stream.
-int conv_backward_impl(lattice_t dst, lattice_t src, const float* X_dev, int64_t ld_X, int Cin, const float* W_dev,
-                       int Cout, int flags, const float* Y_dev, int64_t ld_Y, const float* dY_dev, int64_t ld_dY,
-                       float* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev, hipStream_t stream) {
+int conv_backward_impl(lattice_t dst, lattice_t src, const void* X_dev, int64_t ld_X, int Cin, const void* W_dev,
+                       int Cout, lat_dtype dt, int flags, const void* Y_dev, int64_t ld_Y, const void* dY_dev,
+                       int64_t ld_dY, void* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev,
+                       hipStream_t stream) {
   int st;
+  if ((st = check_dtype(dt)) != LAT_OK) return st;
+  const bool bf = dt == LAT_BF16;
+  const size_t u = bf ? 2 : 4;
   // the forward's table (dst rows, src values) and the adjoint's (src rows,
   // dst values)
   const int32_t *fwd, *adj, *adj_rows = nullptr;
@@ -1394,45 +1398,45 @@ int conv_backward_impl(lattice_t dst, lattice_t src, const float* X_dev, int64_t
   if (ld_X == 0) ld_X = Cin;
   if (ld_dX == 0) ld_dX = Cin;
   const int64_t n_out = dst->n, n_in = src->n;
-  if ((st = check_matrix(dY_dev, ld_dY, Cout, LAT_F32, "dY", n_out > 0)) != LAT_OK) return st;
-  if (relu && (st = check_matrix(Y_dev, ld_Y, Cout, LAT_F32, "Y", n_out > 0)) != LAT_OK) return st;
+  if ((st = check_matrix(dY_dev, ld_dY, Cout, dt, "dY", n_out > 0)) != LAT_OK) return st;
+  if (relu && (st = check_matrix(Y_dev, ld_Y, Cout, dt, "Y", n_out > 0)) != LAT_OK) return st;
   if (dX_dev) {
-    if ((st = check_matrix(dX_dev, ld_dX, Cin, LAT_F32, "dX", false)) != LAT_OK) return st;
+    if ((st = check_matrix(dX_dev, ld_dX, Cin, dt, "dX", false)) != LAT_OK) return st;
     if (!W_dev) return fail(LAT_EINVAL, "W is null");
     if (!aligned16(W_dev)) return fail(LAT_EINVAL, "W must be 16-byte aligned");
     if (n_in > 0 && n_out > 0 &&
-        overlaps(dX_dev, sizeof(float) * static_cast<size_t>((n_in - 1) * ld_dX + Cin), dY_dev,
-                 sizeof(float) * static_cast<size_t>((n_out - 1) * ld_dY + Cout)))
+        overlaps(dX_dev, u * static_cast<size_t>((n_in - 1) * ld_dX + Cin), dY_dev,
+                 u * static_cast<size_t>((n_out - 1) * ld_dY + Cout)))
       return fail(LAT_EINVAL, "dX and dY overlap");
   }
   if (dW_dev || dbias_dev) {
-    if ((st = check_matrix(X_dev, ld_X, Cin, LAT_F32, "X", dW_dev != nullptr && n_in > 0)) != LAT_OK) return st;
+    if ((st = check_matrix(X_dev, ld_X, Cin, dt, "X", dW_dev != nullptr && n_in > 0)) != LAT_OK) return st;
     if (dW_dev && !aligned16(dW_dev)) return fail(LAT_EINVAL, "dW must be 16-byte aligned");
     if (dbias_dev && !aligned16(dbias_dev)) return fail(LAT_EINVAL, "dbias must be 16-byte aligned");
   }
   if (!dX_dev && !dW_dev && !dbias_dev) return LAT_OK;
   ScopedKernelTimer tm("conv_bwd", stream);
-  const float* G = dY_dev;
+  const void* G = dY_dev;
   int64_t ld_G = ld_dY;
   Scratch masked, wt, partials;
   const bool need_mask = relu && n_out > 0, need_wt = dX_dev && n_in > 0;
-  if (need_mask && (st = masked.get(sizeof(float) * static_cast<size_t>(n_out) * Cout, stream)) != LAT_OK) return st;
-  if (need_wt && (st = wt.get(sizeof(float) * 9 * static_cast<size_t>(Cin) * Cout, stream)) != LAT_OK) return st;
-  launch_conv_bwd_prep(dY_dev, ld_dY, Y_dev, ld_Y, n_out, need_mask ? masked.as<float>() : nullptr, Cout, W_dev, Cout,
-                       Cin, need_wt ? wt.as<float>() : nullptr, stream);
+  if (need_mask && (st = masked.get(u * static_cast<size_t>(n_out) * Cout, stream)) != LAT_OK) return st;
+  if (need_wt && (st = wt.get(u * 9 * static_cast<size_t>(Cin) * Cout, stream)) != LAT_OK) return st;
+  launch_conv_bwd_prep(dY_dev, ld_dY, Y_dev, ld_Y, n_out, need_mask ? masked.p : nullptr, Cout, W_dev, Cout, Cin,
+                       need_wt ? wt.p : nullptr, bf ? 1 : 0, stream);
   if (need_mask) {
-    G = masked.as<float>();
+    G = masked.p;
     ld_G = Cout;
   }
   if (need_wt) {
-    launch_conv(adj, adj_ld, n_in, n_out, G, ld_G, Cout, wt.as<float>(), nullptr, Cin, false, false, dX_dev, ld_dX,
+    launch_conv(adj, adj_ld, n_in, n_out, G, ld_G, Cout, wt.p, nullptr, Cin, bf ? 1 : 0, false, dX_dev, ld_dX,
                 adj_rows, stream);
   }
   if (dW_dev || dbias_dev) {
     const int64_t pf = wgrad_partial_floats(n_out, Cout, Cin);
     if (pf > 0 && (st = partials.get(sizeof(float) * static_cast<size_t>(pf), stream)) != LAT_OK) return st;
     launch_conv_wgrad(fwd, fwd_ld, n_out, X_dev, ld_X, Cin, G, ld_G, Cout, dW_dev, dbias_dev, partials.as<float>(),
-                      stream);
+                      bf ? 1 : 0, stream);
   }
   return check_launch("conv backward");
 }
@@ -1445,8 +1449,19 @@ int lattice_conv_backward(lattice_t dst, lattice_t src, const float* X_dev, int6
   int st;
   if ((st = use(dst, stream)) != LAT_OK) return st;
   if ((st = use(src, stream)) != LAT_OK) return st;
-  return conv_backward_impl(dst, src, X_dev, ld_X, Cin, W_dev, Cout, flags, Y_dev, ld_Y, dY_dev, ld_dY, dX_dev, ld_dX,
-                            dW_dev, dbias_dev, stream);
+  return conv_backward_impl(dst, src, X_dev, ld_X, Cin, W_dev, Cout, LAT_F32, flags, Y_dev, ld_Y, dY_dev, ld_dY,
+                            dX_dev, ld_dX, dW_dev, dbias_dev, stream);
+}
+
+int lattice_conv_backward_ex(lattice_t dst, lattice_t src, const void* X_dev, int64_t ld_X, int Cin, const void* W_dev,
+                             int Cout, lat_dtype dt, int flags, const void* Y_dev, int64_t ld_Y, const void* dY_dev,
+                             int64_t ld_dY, void* dX_dev, int64_t ld_dX, float* dW_dev, float* dbias_dev,
+                             hipStream_t stream) {
+  int st;
+  if ((st = use(dst, stream)) != LAT_OK) return st;
+  if ((st = use(src, stream)) != LAT_OK) return st;
+  return conv_backward_impl(dst, src, X_dev, ld_X, Cin, W_dev, Cout, dt, flags, Y_dev, ld_Y, dY_dev, ld_dY, dX_dev,
+                            ld_dX, dW_dev, dbias_dev, stream);
 }
 
 int lattice_conv_preact_backward(lattice_t dst, lattice_t src, const float* X_dev, int64_t ld_X, int Cin, int groups,
@@ -1488,8 +1503,8 @@ int lattice_conv_preact_backward(lattice_t dst, lattice_t src, const float* X_de
   launch_gn_affine(X_dev, ld_X, Cin, 0, n_in, groups, gamma_dev, beta_dev, eps, pre.as<float>(), work.p, stream,
                    stats.as<double>());
   launch_gn_relu_apply(X_dev, ld_X, Cin, n_in, pre.as<float>(), act.as<float>(), Cin, stream);
-  if ((st = conv_backward_impl(dst, src, act.as<float>(), Cin, Cin, W_dev, Cout, flags, Y_dev, ld_Y, dY_dev, ld_dY,
-                               need_dA ? dact.as<float>() : nullptr, Cin, dW_dev, dbias_dev, stream)) != LAT_OK)
+  if ((st = conv_backward_impl(dst, src, act.as<float>(), Cin, Cin, W_dev, Cout, LAT_F32, flags, Y_dev, ld_Y, dY_dev,
+                               ld_dY, need_dA ? dact.as<float>() : nullptr, Cin, dW_dev, dbias_dev, stream)) != LAT_OK)
     return st;
   if (need_dA)
     launch_gn_backward(X_dev, ld_X, dact.as<float>(), Cin, Cin, groups, n_in, gamma_dev, pre.as<float>(),

@@ -18,6 +18,7 @@
 //             DeformSlice backward), dWc = sum_p z_p f_p^T, dbc = sum_p z_p
 //             (point chunks, partials added in chunk order).
 #include <algorithm>
+#include <type_traits>
 
 #include "lattice_internal.h"
 
@@ -63,25 +64,41 @@ k_scale_by_weight_sum(const int32_t* __restrict__ offsets, const float* __restri
 // offset.
 __device__ inline int mirror_tap(int t) { return t == 0 ? 0 : (t <= 4 ? t + 4 : t - 4); }
 
+// Four values of a row of fp32 or bf16 elements (8-byte aligned for bf16).
+template <bool BF16>
+__device__ inline float4 load4(const void* base, int64_t at) {
+  if constexpr (BF16) {
+    const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(base) + at);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xffff0000u));
+  } else {
+    return *reinterpret_cast<const float4*>(static_cast<const float*>(base) + at);
+  }
+}
+
 // The two preparations of the convolution backward in one launch: the first
 // mask_blocks workgroups write G = dY masked by Y > 0 (the forward's ReLU; 4
-// channels per thread), the rest write the adjoint convolution's weights
-// Wt[t][i][o] = W[mirror t][o][i] (W laid out [tap][Cout][Cin]).  Either
-// part may be empty.
+// channels per thread; bf16 values are masked as they are, so G stays
+// exact), the rest write the adjoint convolution's weights Wt[t][i][o] =
+// W[mirror t][o][i] (W laid out [tap][Cout][Cin]).  Either part may be empty.
+template <bool BF16>
 __global__ void __launch_bounds__(kBlock)
-k_conv_bwd_prep(const float* __restrict__ dY, int64_t ld_dy, const float* __restrict__ Y, int64_t ld_y, int64_t n,
-                float* __restrict__ G, int64_t ld_g, unsigned mask_blocks, const float* __restrict__ W, int Cout,
-                int Cin, float* __restrict__ Wt) {
+k_conv_bwd_prep(const void* __restrict__ dY, int64_t ld_dy, const void* __restrict__ Y, int64_t ld_y, int64_t n,
+                void* __restrict__ G, int64_t ld_g, unsigned mask_blocks, const void* __restrict__ W, int Cout,
+                int Cin, void* __restrict__ Wt) {
+  using E = typename std::conditional<BF16, uint16_t, float>::type;
   if (blockIdx.x < mask_blocks) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const int c4 = Cout / 4;
     const int64_t v = q / c4;
     if (v >= n) return;
     const int c = 4 * static_cast<int>(q - v * c4);
-    const float4 d = *reinterpret_cast<const float4*>(dY + v * ld_dy + c);
-    const float4 y = *reinterpret_cast<const float4*>(Y + v * ld_y + c);
-    *reinterpret_cast<float4*>(G + v * ld_g + c) =
-        make_float4(y.x > 0.f ? d.x : 0.f, y.y > 0.f ? d.y : 0.f, y.z > 0.f ? d.z : 0.f, y.w > 0.f ? d.w : 0.f);
+    const E* d = static_cast<const E*>(dY) + v * ld_dy + c;
+    const float4 y = load4<BF16>(Y, v * ld_y + c);
+    E* g = static_cast<E*>(G) + v * ld_g + c;
+    const bool on[4] = {y.x > 0.f, y.y > 0.f, y.z > 0.f, y.w > 0.f};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) g[k] = on[k] ? d[k] : E(0);
     return;
   }
   const int64_t q = static_cast<int64_t>(blockIdx.x - mask_blocks) * kBlock + threadIdx.x;
@@ -90,12 +107,12 @@ k_conv_bwd_prep(const float* __restrict__ dY, int64_t ld_dy, const float* __rest
   const int t = static_cast<int>(q / per);
   const int64_t r = q - t * per;
   const int i = static_cast<int>(r / Cout), o = static_cast<int>(r - static_cast<int64_t>(i) * Cout);
-  Wt[q] = W[(mirror_tap(t) * per) + static_cast<int64_t>(o) * Cin + i];
+  static_cast<E*>(Wt)[q] = static_cast<const E*>(W)[(mirror_tap(t) * per) + static_cast<int64_t>(o) * Cin + i];
 }
 
 // dW[t][o][i] = sum_v G[v][o] X[nb(v,t)][i] as a GEMM with the vertices as
 // the reduction dimension: A = G^T (Cout x K), B = the gathered rows
-// (K x Cin).  A workgroup owns one tap, one 64 x 64 tile of (o, i) and one
+// (K x Cin); bf16 G and X are widened to fp32 as they are staged.  A workgroup owns one tap, one 64 x 64 tile of (o, i) and one
 // chunk of V vertices; it stages 32 vertices at a time (G rows and gathered
 // X rows, a missing neighbour reads as zeros) in double-buffered LDS, each
 // wave multiplying a 32 x 32 sub-tile on v_mfma_f32_16x16x4_f32.  Partials
@@ -105,9 +122,10 @@ constexpr int kWgTile = 64;
 constexpr int kWgStage = 32;
 constexpr int kWgPitch = kWgTile + 4;
 
+template <bool BF16>
 __global__ void __launch_bounds__(kBlock)
-k_conv_wgrad(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, int64_t V, const float* __restrict__ X,
-             int64_t ld_x, int Cin, const float* __restrict__ G, int64_t ld_g, int Cout, int tiles_i,
+k_conv_wgrad(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, int64_t V, const void* __restrict__ X,
+             int64_t ld_x, int Cin, const void* __restrict__ G, int64_t ld_g, int Cout, int tiles_i,
              float* __restrict__ part, float* __restrict__ part_b) {
   __shared__ __align__(16) float Gs[2][kWgStage][kWgPitch];
   __shared__ __align__(16) float Xs[2][kWgStage][kWgPitch];
@@ -130,9 +148,9 @@ k_conv_wgrad(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, int64_
       const int64_t v = vb + lr + 16 * h;
       float4 g = make_float4(0.f, 0.f, 0.f, 0.f), x = g;
       if (v < v_end) {
-        if (o0 + lc < Cout) g = *reinterpret_cast<const float4*>(G + v * ld_g + o0 + lc);
+        if (o0 + lc < Cout) g = load4<BF16>(G, v * ld_g + o0 + lc);
         const int32_t u = tab[v];
-        if (u >= 0 && i0 + lc < Cin) x = *reinterpret_cast<const float4*>(X + static_cast<int64_t>(u) * ld_x + i0 + lc);
+        if (u >= 0 && i0 + lc < Cin) x = load4<BF16>(X, static_cast<int64_t>(u) * ld_x + i0 + lc);
       }
       ga[h] = g;
       xa[h] = x;
@@ -365,12 +383,17 @@ void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, co
          ld_in, C, out, ld_out);
 }
 
-void launch_conv_bwd_prep(const float* dY, int64_t ld_dy, const float* Y, int64_t ld_y, int64_t n, float* G,
-                          int64_t ld_g, const float* W, int Cout, int Cin, float* Wt, hipStream_t s) {
+void launch_conv_bwd_prep(const void* dY, int64_t ld_dy, const void* Y, int64_t ld_y, int64_t n, void* G,
+                          int64_t ld_g, const void* W, int Cout, int Cin, void* Wt, int bf16, hipStream_t s) {
   const unsigned mb = (G && n > 0) ? blocks_for(n * (Cout / 4)) : 0;
   const unsigned wb = Wt ? blocks_for(9LL * Cout * Cin) : 0;
   if (mb + wb == 0) return;
-  launch(k_conv_bwd_prep, dim3(mb + wb), dim3(kBlock), 0, s, dY, ld_dy, Y, ld_y, n, G, ld_g, mb, W, Cout, Cin, Wt);
+  if (bf16)
+    launch(k_conv_bwd_prep<true>, dim3(mb + wb), dim3(kBlock), 0, s, dY, ld_dy, Y, ld_y, n, G, ld_g, mb, W, Cout, Cin,
+           Wt);
+  else
+    launch(k_conv_bwd_prep<false>, dim3(mb + wb), dim3(kBlock), 0, s, dY, ld_dy, Y, ld_y, n, G, ld_g, mb, W, Cout, Cin,
+           Wt);
 }
 
 int64_t wgrad_partial_floats(int64_t n_out, int Cout, int Cin) {
@@ -381,8 +404,8 @@ int64_t wgrad_partial_floats(int64_t n_out, int Cout, int Cin) {
   return chunks * (9LL * Cout * Cin + Cout);
 }
 
-void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const float* X, int64_t ld_x, int Cin,
-                       const float* G, int64_t ld_g, int Cout, float* dW, float* dbias, float* partials,
+void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* X, int64_t ld_x, int Cin,
+                       const void* G, int64_t ld_g, int Cout, float* dW, float* dbias, float* partials, int bf16,
                        hipStream_t s) {
   const int tiles_o = (Cout + kWgTile - 1) / kWgTile, tiles_i = (Cin + kWgTile - 1) / kWgTile;
   const int64_t count = 9LL * Cout * Cin;
@@ -390,9 +413,15 @@ void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const flo
   if (n_out > 0) wgrad_chunks(n_out, tiles_o * tiles_i, &chunks, &V);
   float* part = partials;
   float* part_b = dbias ? partials + chunks * count : nullptr;
-  if (chunks > 0)
-    launch(k_conv_wgrad, dim3(static_cast<unsigned>(chunks), 9, static_cast<unsigned>(tiles_o * tiles_i)),
-           dim3(kBlock), 0, s, nbr, ldn, n_out, V, X, ld_x, Cin, G, ld_g, Cout, tiles_i, part, part_b);
+  if (chunks > 0) {
+    const dim3 grid(static_cast<unsigned>(chunks), 9, static_cast<unsigned>(tiles_o * tiles_i));
+    if (bf16)
+      launch(k_conv_wgrad<true>, grid, dim3(kBlock), 0, s, nbr, ldn, n_out, V, X, ld_x, Cin, G, ld_g, Cout, tiles_i,
+             part, part_b);
+    else
+      launch(k_conv_wgrad<false>, grid, dim3(kBlock), 0, s, nbr, ldn, n_out, V, X, ld_x, Cin, G, ld_g, Cout, tiles_i,
+             part, part_b);
+  }
   // with no output vertex (chunks = 0) the sums below are zero
   launch(k_wgrad_reduce, dim3(blocks_for((count + Cout) / 4)), dim3(kBlock), 0, s, static_cast<const float*>(part),
          static_cast<const float*>(part_b), chunks, count, Cout, dW, dbias);

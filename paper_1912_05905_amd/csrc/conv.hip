@@ -260,13 +260,18 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
   const int li = lane & 15;
   const int lg = lane >> 4;
   // XCD-aware tile order: workgroup b runs on XCD b % 8; give each XCD a
-  // contiguous range of row tiles.
+  // contiguous range of (row tile, column tile) items, column tiles of a row
+  // tile adjacent, so that the workgroups gathering the same input rows run
+  // at the same time on one XCD and share its L2.
   const unsigned b = blockIdx.x;
-  const unsigned per_xcd = (row_tiles + 7) / 8;
-  const unsigned tile = (b % 8) * per_xcd + b / 8;
-  if (tile >= row_tiles) return;
+  const unsigned col_tiles = (Cout + BN - 1) / BN;
+  const unsigned items = row_tiles * col_tiles;
+  const unsigned per_xcd = (items + 7) / 8;
+  const unsigned item = (b % 8) * per_xcd + b / 8;
+  if (item >= items) return;
+  const unsigned tile = item / col_tiles;
   const int64_t row0 = static_cast<int64_t>(tile) * BM;
-  const int col0 = blockIdx.y * BN;
+  const int col0 = static_cast<int>(item - tile * col_tiles) * BN;
   const int wm = wave % WM, wn = wave / WM;
 
   // split z of the K dimension takes taps [tb, te)
@@ -596,8 +601,9 @@ void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void*
     lds_limit_set = true;
   }
   const int64_t tiles = (n_out + BM - 1) / BM;
-  const unsigned per_xcd = static_cast<unsigned>((tiles + 7) / 8);
-  const dim3 grid(per_xcd * 8, static_cast<unsigned>((Cout + BN - 1) / BN), static_cast<unsigned>(splits));
+  const int64_t items = tiles * ((Cout + BN - 1) / BN);
+  const unsigned per_xcd = static_cast<unsigned>((items + 7) / 8);
+  const dim3 grid(per_xcd * 8, 1, static_cast<unsigned>(splits));
   launch((k_conv_lds<BF16, BM, BN, WM, WN, KCB, NS, BUF, SCHED, PRE>), grid, dim3(kBlock), static_cast<uint32_t>(lds),
          s, nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, static_cast<unsigned>(tiles),
          splits, splits > 1 ? part : nullptr, static_cast<uint32_t>(BUF ? ext.in_bytes : 0),
@@ -621,7 +627,9 @@ int64_t blocks_of(int64_t n_out, int Cout, int rows, int cols) {
 // a third stage in flight (with half the channels per stage) pays; a few
 // hundred 32 x 64 tiles do best with two stages of 64 channels.  bf16: 128 x 128 tiles halve the
 // gathered bytes per flop and win once there are enough of them (wide
-// layers, large levels); 64 x 64 otherwise.
+// layers, large levels); 128 x 64 with stages of 32 channels for 64 output
+// channels on large levels (half the weight rows per output row); 64 x 64
+// otherwise.
 // PRE (the pre-activated convolution) uses the same tiles, apart from the
 // register kernel for narrow outputs, which has no pre-activation.
 template <bool BF16, bool PRE>
@@ -639,6 +647,9 @@ void conv_dispatch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* i
     const int64_t b64 = blocks_of(n_out, Cout, 64, 64);
     if (Cout >= 128 && (b128 >= 1500 || (Cin >= 256 && Cout % 128 == 0)))
       return conv_lds_launch<true, 128, 128, 2, 2, 64, 3, true, 1, PRE>(
+          nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
+    if (Cout == 64 && b64 >= 8192)
+      return conv_lds_launch<true, 128, 64, 2, 2, 64, 3, true, 1, PRE>(
           nbr, ldn, n_out, in, ld_in, Cin, W, bias, Cout, relu, out, ld_out, rows, ext, s, pre, res, ld_res);
     if (Cout > 32 && b64 >= 8192)
       return conv_lds_launch<true, 64, 64, 2, 2, 128, 3, true, 1, PRE>(

@@ -220,11 +220,12 @@ void launch_distribute(const int32_t* offsets, const int32_t* entries, const int
 // backward.hip
 void launch_scale_by_weight_sum(const int32_t* offsets, const float* entry_w, const float* wsum, int64_t n,
                                 const float* in, int64_t ld_in, int C, float* out, int64_t ld_out, hipStream_t s);
-void launch_conv_bwd_prep(const float* dY, int64_t ld_dy, const float* Y, int64_t ld_y, int64_t n, float* G,
-                          int64_t ld_g, const float* W, int Cout, int Cin, float* Wt, hipStream_t s);
+// dY, Y, G, W, Wt (and X below) are float32, or bfloat16 with bf16 != 0
+void launch_conv_bwd_prep(const void* dY, int64_t ld_dy, const void* Y, int64_t ld_y, int64_t n, void* G,
+                          int64_t ld_g, const void* W, int Cout, int Cin, void* Wt, int bf16, hipStream_t s);
 int64_t wgrad_partial_floats(int64_t n_out, int Cout, int Cin);
-void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const float* X, int64_t ld_x, int Cin,
-                       const float* G, int64_t ld_g, int Cout, float* dW, float* dbias, float* partials,
+void launch_conv_wgrad(const int32_t* nbr, int64_t ldn, int64_t n_out, const void* X, int64_t ld_x, int Cin,
+                       const void* G, int64_t ld_g, int Cout, float* dW, float* dbias, float* partials, int bf16,
                        hipStream_t s);
 // conv.hip
 // pre: optional Cin scales then Cin shifts of the pre-activation (applied,

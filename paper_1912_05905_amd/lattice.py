@@ -66,6 +66,8 @@ SIGNATURES = {
     "lattice_distribute_pointnet_backward": (_I32, [_P, _P, _P, _I64, _I32, _P, _P, C.c_float, _P, _P, _I32, _P, _P,
                                                     _I32, _P, _P, _I32, _P, _I64, _P, _I64, _P, _P, _P, _P, _P, _P,
                                                     _P, _P, _P]),
+    "lattice_conv_backward_ex": (_I32, [_P, _P, _P, _I64, _I32, _P, _I32, _I32, _I32, _P, _I64, _P, _I64, _P, _I64,
+                                        _P, _P, _P]),
     "lattice_deform_slice_backward": (_I32, [_P, _P, _I64, _I32, _P, _F32, _P, _I64, _P, _I64, _P, _P, _P]),
     "lattice_timing_enable": (_I32, [C.c_char_p, _I32]),
     "lattice_timing_read": (_I32, [C.c_char_p, C.POINTER(_I64), C.POINTER(C.c_double)]),
@@ -398,6 +400,26 @@ class Lattice:
         ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
         _check(lib().lattice_conv_backward(self._h, src._h, xp, xld, cin, ptr(W), cout, LAT_RELU if relu else 0,
                                            yp, yld, gp, gld, dp, dld, ptr(dW), ptr(db), _stream(stream)))
+        return dx, dW, db
+
+    def conv_backward_bf16(self, src: "Lattice", x: torch.Tensor | None, W: torch.Tensor | None, dy: torch.Tensor,
+                           relu: bool = False, y: torch.Tensor | None = None, want_dx: bool = True,
+                           want_dw: bool = True, want_dbias: bool = True, stream=None):
+        """conv_backward for bfloat16 x, W, y, dy: (dx bfloat16, dW and dbias
+        float32), None where not asked for."""
+        cout = dy.shape[1]
+        cin = W.shape[2] if W is not None else x.shape[1]
+        dx = torch.empty((src.n, cin), dtype=torch.bfloat16, device="cuda") if want_dx else None
+        dW = torch.empty((9, cout, cin), dtype=torch.float32, device="cuda") if want_dw else None
+        db = torch.empty((cout,), dtype=torch.float32, device="cuda") if want_dbias else None
+        xp, xld = _rows(x) if x is not None else (None, 0)
+        yp, yld = _rows(y) if y is not None else (None, 0)
+        gp, gld = _rows(dy)
+        dp, dld = _rows(dx) if dx is not None else (None, 0)
+        ptr = lambda t: None if t is None else C.c_void_p(t.data_ptr())
+        _check(lib().lattice_conv_backward_ex(self._h, src._h, xp, xld, cin, ptr(W), cout, _dtype_code(dy),
+                                              LAT_RELU if relu else 0, yp, yld, gp, gld, dp, dld, ptr(dW), ptr(db),
+                                              _stream(stream)))
         return dx, dW, db
 
     def conv_preact_backward(self, src: "Lattice", x: torch.Tensor, W: torch.Tensor, dy: torch.Tensor,

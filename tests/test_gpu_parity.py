@@ -1340,3 +1340,52 @@ def test_distribute_pointnet_backward_skewed_and_tiny(L, O):
         P.assert_close(_host(got[k]), ref[k], P.TOL_F32, f"one-point Distribute backward {k}")
     for k in ("dF", "dW1", "db1", "dW2", "db2", "dgamma", "dbeta"):
         assert np.isfinite(_host(got[k])).all(), k
+
+
+# ----------------------------------------------------------------------------
+# convolution backward of a bfloat16 network
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("form,cin,cout,relu", [("same", 64, 64, True), ("same", 16, 128, False),
+                                                 ("strided", 64, 128, True), ("upsample", 128, 64, False),
+                                                 ("upsample", 32, 32, True)])
+def test_conv_backward_bf16(L, O, form, cin, cout, relu):
+    """bf16 X, W, Y and dY (the values a bf16 forward stores): dX in bf16
+    against the oracle's float64 gradient rounded once; dW and dbias in
+    float32 (bf16 values widen exactly, the error is float32 summation)."""
+    seed = 1800 + cin + cout
+    pos = _cloud(seed, 8000, 0.8)
+    gl = L.Lattice.create(_dev(pos), [0.05] * 3)
+    ol = O.Lattice.create(pos, np.full(3, 0.05, np.float32))
+    g2o_f = P.key_permutation(_host(gl.keys()), ol.keys())
+    keep = ()
+    if form == "same":
+        gd, gs, od, os_, g2o_d, g2o_s = gl, gl, ol, ol, g2o_f, g2o_f
+    else:
+        gc, oc = gl.coarsen(), ol.coarsen()
+        keep = (gc,)
+        g2o_c = P.key_permutation(_host(gc.keys()), oc.keys())
+        if form == "strided":
+            gd, gs, od, os_, g2o_d, g2o_s = gc, gl, oc, ol, g2o_c, g2o_f
+        else:
+            gd, gs, od, os_, g2o_d, g2o_s = gl, gc, ol, oc, g2o_f, g2o_c
+    rng = np.random.default_rng(seed)
+    X = O.round_bf16(rng.normal(size=(os_.n, cin)))
+    W = O.round_bf16(rng.normal(size=(9, cin, cout)) / np.sqrt(9 * cin))
+    b = O.round_bf16(0.3 * rng.normal(size=cout))
+    dY = O.round_bf16(rng.normal(size=(od.n, cout)))
+    if form == "upsample":
+        Y = od.refine_into(os_, X, W, bias=b, relu=relu)
+    else:
+        Y = od.conv(os_, X, W, bias=b, relu=relu)
+    Yb = O.round_bf16(Y)
+    odx, odw, odb = od.conv_backward(os_, X, W, dY, relu=relu, Y=Yb if relu else None)
+    bf = torch.bfloat16
+    gdx, gdw, gdb = gd.conv_backward_bf16(gs, _dev(X[g2o_s].astype(np.float32), bf), _gpu_w(W.astype(np.float32), bf),
+                                          _dev(dY[g2o_d].astype(np.float32), bf), relu=relu,
+                                          y=_dev(Yb[g2o_d].astype(np.float32), bf) if relu else None)
+    what = f"bf16 backward {form} {cin}->{cout} relu={relu}"
+    assert gdx.dtype == bf
+    P.assert_close(P.rows_in_oracle_order(_host(gdx.float()), g2o_s), O.round_bf16(odx), P.TOL_BF16, "dX " + what)
+    P.assert_close(np.transpose(_host(gdw), (0, 2, 1)), odw, P.TOL_F32, "dW " + what)
+    P.assert_close(_host(gdb), odb, P.TOL_F32, "dbias " + what)
+    del keep
