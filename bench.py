@@ -25,7 +25,7 @@ sys.path.insert(0, ROOT)
 PEAK = {"hbm": 8.0e12, "mfma_f32": 157.3e12, "mfma_bf16": 2.5e15}
 BUILD_FAMILIES = {"fill", "insert", "scan", "lists", "nbr"}
 FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "distribute", "groupnorm", "conv", "slice",
-            "deform_slice", "deform_bwd", "conv_bwd", "splat_bwd", "slice_bwd"]
+            "deform_slice", "deform_bwd", "conv_bwd", "splat_bwd", "slice_bwd", "linear_bwd"]
 # kernel symbol fragments of each family (rocprofv3 kernel names; first match
 # wins).  Backward operators that reuse a forward kernel (the adjoint
 # convolution on k_conv_lds, splat and slice as each other's adjoints, the
@@ -35,7 +35,7 @@ FAMILY_KERNELS = {
     "fill": ["k_clear_table"], "insert": ["k_insert_points"], "scan": ["k_scan("],
     "lists": ["k_fill_lists"], "nbr": ["k_neighbor_table", "k_coarse_tables", "k_mask_order"],
     "deform_bwd": ["k_deform_bwd", "DeformGradRows"],
-    "conv_bwd": ["k_conv_wgrad", "k_wgrad_reduce", "k_relu_mask", "k_adjoint_weights"],
+    "conv_bwd": ["k_conv_wgrad", "k_wgrad_reduce", "k_conv_bwd_prep"], "linear_bwd": ["k_lin_"],
     "splat_bwd": ["k_scale_by_weight_sum"], "groupnorm": ["k_gn_"],
     "splat": ["k_splat_chunks", "k_splat_finish"], "distribute": ["k_dist_"], "conv": ["k_conv"],
     "slice": ["k_slice<"],
