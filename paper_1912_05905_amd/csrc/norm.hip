@@ -15,6 +15,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kGnMaxParts = 2048;
+constexpr int kGnMinRows = 128;
 
 // Workgroup w sums rows [w * rows_per, (w + 1) * rows_per): thread t takes
 // the EPT channels EPT (t % groups_of_c) .. + EPT - 1 (16 bytes: 8 bf16 or 4
@@ -96,6 +97,9 @@ k_gn_finalize(const double* __restrict__ part, int nparts, int C, int groups, in
   const int per = C / groups;
   const int t = threadIdx.x;
   double s = 0.0, ss = 0.0;
+  // unrolled so that the loads of several partials are in flight at once;
+  // they are still added in q order
+#pragma unroll 8
   for (int64_t q = t; q < static_cast<int64_t>(nparts) * per; q += kBlock) {
     const int64_t w = q / per;
     const int c = g * per + static_cast<int>(q - w * per);
@@ -249,6 +253,7 @@ k_gn_bwd_finalize(const double* __restrict__ part, int nparts, int C, int groups
     const int c = g * per + cb + j;
     double s = 0.0, ss = 0.0;
     if (k < slices)
+#pragma unroll 8
       for (int w = k; w < nparts; w += slices) {
         s += part[static_cast<int64_t>(w) * 2 * C + c];
         ss += part[static_cast<int64_t>(w) * 2 * C + C + c];
@@ -331,9 +336,12 @@ inline unsigned elementwise_grid(int64_t n, int C) {
   return static_cast<unsigned>(std::max<int64_t>(1, std::min<int64_t>(b, 8192)));
 }
 
+// Rows per partial: at least kGnMinRows (small levels then leave a few
+// hundred partials, which the finalize reads in one or two loads per
+// thread), at most 2,048 partials on large ones.
 void gn_parts(int64_t n, int C, int bf16, int64_t* nparts, int64_t* rows_per) {
   const int slots = kBlock / (C / (bf16 ? 8 : 4));
-  int64_t rp = std::max<int64_t>(slots, (n + kGnMaxParts - 1) / kGnMaxParts);
+  int64_t rp = std::max<int64_t>(std::max<int64_t>(slots, kGnMinRows), (n + kGnMaxParts - 1) / kGnMaxParts);
   rp = (rp + slots - 1) / slots * slots;
   *rows_per = rp;
   *nparts = std::max<int64_t>(1, (n + rp - 1) / rp);
