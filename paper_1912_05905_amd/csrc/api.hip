@@ -289,7 +289,6 @@ struct lattice_s {
   // indices) only when an operator first needs them: the convolutions only
   // need the tables.  Until then it keeps what the list build reads.
   bool lists_ready = true;
-  int32_t* slot_count = nullptr;  // per table slot: references
   int32_t* vslot = nullptr;       // per vertex: its slot
   int32_t* slot = nullptr;        // per reference: slot of its vertex
   int32_t* rank = nullptr;        // per reference: rank within its vertex
@@ -444,7 +443,6 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   // build are the handle's own buffers: a build releases nothing to the
   // pool, so a coarse level can start after the finer level's insert.
   const bool defer_lists = parent != nullptr;
-  const size_t o_slot_count = carve(sizeof(int32_t) * cap);
   const size_t o_vslot = carve(sizeof(int32_t) * nmax);
   const size_t o_slot = carve(sizeof(int32_t) * refs);
   const size_t o_rank = carve(sizeof(int32_t) * refs);
@@ -470,12 +468,10 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
     L->up_rows = static_cast<int32_t*>(at(o_up_rows));
     L->down_rows = static_cast<int32_t*>(at(o_down_rows));
   }
-  L->slot_count = static_cast<int32_t*>(at(o_slot_count));
   L->vslot = static_cast<int32_t*>(at(o_vslot));
   L->slot = static_cast<int32_t*>(at(o_slot));
   L->rank = static_cast<int32_t*>(at(o_rank));
   L->scan_work = at(o_work);
-  int32_t* slot_count = L->slot_count;
   int32_t* vslot = L->vslot;
   int32_t* slot = L->slot;
   int32_t* rank = L->rank;
@@ -489,8 +485,8 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   static std::atomic<uint32_t> g_stamp{0};
   L->stamp = m > 0 ? ++g_stamp : 0;
   L->host_dc->stamp = ~L->stamp;
-  launch_clear_table(L->table, slot_count, cap, L->dc, work, s);
-  launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], m, L->hash(), &L->dc->counter, slot_count, L->vkeys,
+  launch_clear_table(L->table, cap, L->dc, work, s);
+  launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], m, L->hash(), &L->dc->counter, L->vkeys,
                        vslot, slot, rank, L->w, L->y, &L->dc->err, host_counts, L->stamp, L->counts_ready, s);
   L->releases_at_insert = Pool::get().release_count(L->stream);
   HIP_TRY(hipGetLastError());
@@ -498,7 +494,7 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   const int32_t* n_dev = &L->dc->counter;
   L->lists_ready = !defer_lists;
   if (!defer_lists) {
-    launch_count_scan(slot_count, vslot, n_dev, L->offsets, work, s);
+    launch_count_scan(L->table, vslot, n_dev, L->offsets, work, s);
     launch_fill_lists(L->hash(), slot, rank, L->w, L->offsets, L->idx, L->entries, L->entry_w, L->chunk_first,
                       L->chunk, refs, s);
   }
@@ -514,7 +510,7 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
 // built on first use (on the stream of the operator that needs them).
 int ensure_lists(lattice_s* L, hipStream_t s) {
   if (L->lists_ready) return LAT_OK;
-  launch_count_scan(L->slot_count, L->vslot, &L->dc->counter, L->offsets, L->scan_work, s);
+  launch_count_scan(L->table, L->vslot, &L->dc->counter, L->offsets, L->scan_work, s);
   launch_fill_lists(L->hash(), L->slot, L->rank, L->w, L->offsets, L->idx, L->entries, L->entry_w, L->chunk_first,
                     L->chunk, L->total, s);
   L->lists_ready = true;

@@ -541,21 +541,25 @@ k_conv_lds(const int32_t* __restrict__ nbr, int64_t ldn, int64_t n_out, const vo
 }
 
 // Sum of the split partials in split order, then bias, ReLU and conversion.
+// Partial row r belongs to output row rows[r] when the tiles ran over a row
+// order.
 template <bool BF16>
 __global__ void __launch_bounds__(kBlock)
 k_conv_reduce(const float* __restrict__ part, int splits, int64_t n_out, int Cout, const float* __restrict__ bias,
-              int relu, void* __restrict__ out, int64_t ld_out, const void* __restrict__ res, int64_t ld_res) {
+              int relu, void* __restrict__ out, int64_t ld_out, const void* __restrict__ res, int64_t ld_res,
+              const int32_t* __restrict__ rows) {
   const int64_t quads = n_out * (Cout / 4);
   const int64_t plane = n_out * Cout;
   for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < quads;
        q += static_cast<int64_t>(gridDim.x) * kBlock) {
-    const int64_t row = q / (Cout / 4);
-    const int col = static_cast<int>(q - row * (Cout / 4)) * 4;
-    float4 a = *reinterpret_cast<const float4*>(part + row * Cout + col);
+    const int64_t prow = q / (Cout / 4);
+    const int col = static_cast<int>(q - prow * (Cout / 4)) * 4;
+    float4 a = *reinterpret_cast<const float4*>(part + prow * Cout + col);
     for (int z = 1; z < splits; ++z) {
-      const float4 b = *reinterpret_cast<const float4*>(part + z * plane + row * Cout + col);
+      const float4 b = *reinterpret_cast<const float4*>(part + z * plane + prow * Cout + col);
       a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
     }
+    const int64_t row = rows ? rows[prow] : prow;
     float v[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -591,7 +595,6 @@ void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void*
                      int64_t ld_out, const int32_t* rows, ConvExtent ext, hipStream_t s, const float* pre = nullptr,
                      const void* res = nullptr, int64_t ld_res = 0, int splits = 1, float* part = nullptr) {
   using P = LdsConv<BF16, BM, BN, WM, WN, KCB>;
-  if (rows) splits = 1;  // partial sums are kept in permuted row order
   const int lds = P::LDS_BYTES + (PRE ? 8 * Cin : 0);
   static bool lds_limit_set = false;
   if (!lds_limit_set) {
@@ -612,7 +615,7 @@ void conv_lds_launch(const int32_t* nbr, int64_t ldn, int64_t n_out, const void*
     const int64_t quads = n_out * (Cout / 4);
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((quads + kBlock - 1) / kBlock, 8192));
     launch((k_conv_reduce<BF16>), dim3(blocks), dim3(kBlock), 0, s, part, splits, n_out, Cout, bias,
-                       relu, out, ld_out, res, ld_res);
+                       relu, out, ld_out, res, ld_res, rows);
   }
 }
 

@@ -30,24 +30,22 @@ constexpr int kLdsPerThread = kLdsSlots / kBlock;
 
 // ---- exclusive scan of per-vertex counts over a device-side n ----
 // kScanBlocks workgroups each own a contiguous range of vertices (the count
-// of vertex v is slot_count[vslot[v]]).  Single pass: a workgroup publishes
+// of vertex v is table[vslot[v]].count).  Single pass: a workgroup publishes
 // the sum of its range in scan_status, adds the published sums of the
 // earlier ranges and scans its own range.
 constexpr int kScanBlocks = 256;
 constexpr uint64_t kScanReady = 1ull << 32;  // flag of a published range sum
 constexpr int kScanPer = 8;                   // consecutive vertices per thread in a scan tile
 
-// Empty hash table and zero reference counts; zero device counters and scan
+// Empty hash table (reference counts 0); zero device counters and scan
 // status words for the build that follows.
 __global__ void __launch_bounds__(kBlock)
-k_clear_table(HashEntry* __restrict__ entries, int32_t* __restrict__ counts, int64_t cap,
-              uint4* __restrict__ dev_counters, uint64_t* __restrict__ scan_status) {
+k_clear_table(HashEntry* __restrict__ entries, int64_t cap, uint4* __restrict__ dev_counters,
+              uint64_t* __restrict__ scan_status) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-  for (int64_t e = i; e < cap; e += stride) {
+  for (int64_t e = i; e < cap; e += stride)
     *reinterpret_cast<uint4*>(&entries[e]) = make_uint4(0xffffffffu, 0xffffffffu, 0u, 0u);
-    counts[e] = 0;
-  }
   if (i == 0) *dev_counters = make_uint4(0u, 0u, 0u, 0u);
   if (i < kScanBlocks) scan_status[i] = 0ull;
 }
@@ -92,11 +90,11 @@ __device__ inline int32_t block_exclusive_sum(int32_t v, int32_t* lds4, int32_t*
 // Outputs per point: slot of each vertex in the global table, its rank in
 // that vertex's point list, the weights and the elevated position.  Per new
 // vertex: vals[slot] = vertex number, vkeys / vslot by vertex number.
-// slot_count[slot] ends as the number of references of the vertex.
+// The slot's count ends as the number of references of the vertex.
 __global__ void __launch_bounds__(kBlock)
 k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, float y_scale,
                 float a0, float a1, float a2, int64_t m, HashView h, int32_t* counter,
-                int32_t* __restrict__ slot_count, uint64_t* __restrict__ vkeys,
+                uint64_t* __restrict__ vkeys,
                 int32_t* __restrict__ vslot, int4* __restrict__ slot_out, int4* __restrict__ rank_out,
                 float4* __restrict__ w_out, float4* __restrict__ y_out, uint32_t* err,
                 int32_t* __restrict__ host_counts, uint32_t stamp) {
@@ -299,7 +297,7 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
   int32_t gbase[kVerts];
 #pragma unroll
   for (int j = 0; j < kVerts; ++j)
-    gbase[j] = gsl[j] >= 0 ? atomicAdd(&slot_count[gsl[j]], lcount[usl[j]]) : 0;
+    gbase[j] = gsl[j] >= 0 ? atomicAdd(&h.e[gsl[j]].count, lcount[usl[j]]) : 0;
   const int32_t ncreated = __builtin_popcount(created_mask);
   int32_t nblock = 0;
   const int32_t my_first = block_exclusive_sum(ncreated, scan_buf, &nblock);
@@ -355,7 +353,7 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
 }
 
 __global__ void __launch_bounds__(kBlock)
-k_scan(const int32_t* __restrict__ slot_count, const int32_t* __restrict__ vslot, const int32_t* __restrict__ n_dev,
+k_scan(const HashEntry* __restrict__ table, const int32_t* __restrict__ vslot, const int32_t* __restrict__ n_dev,
        uint64_t* __restrict__ status, int32_t* __restrict__ offsets) {
   static_assert(kScanBlocks <= kBlock, "one earlier range per thread");
   __shared__ int32_t lds4[kBlock / 64];
@@ -363,7 +361,7 @@ k_scan(const int32_t* __restrict__ slot_count, const int32_t* __restrict__ vslot
   const int64_t per = (n + kScanBlocks - 1) / kScanBlocks;
   const int64_t beg = blockIdx.x * per, end = min(beg + per, n);
   int32_t s = 0;
-  for (int64_t i = beg + threadIdx.x; i < end; i += kBlock) s += slot_count[vslot[i]];
+  for (int64_t i = beg + threadIdx.x; i < end; i += kBlock) s += table[vslot[i]].count;
   int32_t agg;
   block_exclusive_sum(s, lds4, &agg);
   // the status word carries the sum itself, so relaxed atomics suffice
@@ -385,7 +383,7 @@ k_scan(const int32_t* __restrict__ slot_count, const int32_t* __restrict__ vslot
       before = static_cast<int32_t>(static_cast<uint32_t>(st));
     } else {
       const int64_t b2 = j * per, e2 = min(b2 + per, n);
-      for (int64_t i = b2; i < e2; ++i) before += slot_count[vslot[i]];
+      for (int64_t i = b2; i < e2; ++i) before += table[vslot[i]].count;
     }
   }
   int32_t carry;
@@ -396,7 +394,7 @@ k_scan(const int32_t* __restrict__ slot_count, const int32_t* __restrict__ vslot
     int32_t loc = 0;
 #pragma unroll
     for (int q = 0; q < kScanPer; ++q) {
-      v[q] = base + q < end ? slot_count[vslot[base + q]] : 0;
+      v[q] = base + q < end ? table[vslot[base + q]].count : 0;
       loc += v[q];
     }
     int32_t tile_total;
@@ -648,17 +646,16 @@ inline unsigned blocks_for(int64_t n) { return static_cast<unsigned>((n + kBlock
 
 }  // namespace
 
-void launch_clear_table(HashEntry* keys, int32_t* counts, int64_t cap, void* dev_counters, void* scan_work,
-                        hipStream_t s) {
+void launch_clear_table(HashEntry* keys, int64_t cap, void* dev_counters, void* scan_work, hipStream_t s) {
   const int64_t want = (cap + kBlock * 4 - 1) / (kBlock * 4);
   const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : (want < 8192 ? want : 8192));
   ScopedKernelTimer tm("fill", s);
-  launch(k_clear_table, dim3(grid), dim3(kBlock), 0, s, keys, counts, cap,
+  launch(k_clear_table, dim3(grid), dim3(kBlock), 0, s, keys, cap,
                      static_cast<uint4*>(dev_counters), static_cast<uint64_t*>(scan_work));
 }
 
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
-                          float a2, int64_t m, HashView h, int32_t* counter, int32_t* slot_count,
+                          float a2, int64_t m, HashView h, int32_t* counter,
                           uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
                           float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, uint32_t stamp,
                           hipEvent_t done, hipStream_t s) {
@@ -669,17 +666,17 @@ void launch_insert_points(const float* pos, const float* y_in, float y_scale, fl
   ScopedKernelTimer tm("insert", s);
   launch_signal(k_insert_points, dim3(blocks_for(m)), dim3(kBlock), 0, s, done, pos,
                      reinterpret_cast<const float4*>(y_in), y_scale, a0, a1, a2, m, h, counter,
-                     slot_count, vkeys, vslot, reinterpret_cast<int4*>(slot_out),
+                     vkeys, vslot, reinterpret_cast<int4*>(slot_out),
                      reinterpret_cast<int4*>(rank_out), reinterpret_cast<float4*>(w_out),
                      reinterpret_cast<float4*>(y_out), err, host_counts, stamp);
 }
 
 int64_t scan_workspace_bytes() { return kScanBlocks * sizeof(uint64_t); }
 
-void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, const int32_t* n_dev,
+void launch_count_scan(const HashEntry* table, const int32_t* vslot, const int32_t* n_dev,
                        int32_t* offsets, void* work, hipStream_t s) {
   ScopedKernelTimer tm("scan", s);
-  launch(k_scan, dim3(kScanBlocks), dim3(kBlock), 0, s, slot_count, vslot, n_dev,
+  launch(k_scan, dim3(kScanBlocks), dim3(kBlock), 0, s, table, vslot, n_dev,
                      static_cast<uint64_t*>(work), offsets);
 }
 

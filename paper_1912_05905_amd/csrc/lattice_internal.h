@@ -63,12 +63,13 @@ __host__ __device__ inline uint64_t hash_key(uint64_t k) {
 }
 
 // Open-addressing table with linear probing.  A slot is 16 bytes: the
-// packed key (kEmptyKey when free) and the vertex number, so a probe reads
-// one aligned 16-byte entry.
+// packed key (kEmptyKey when free), the vertex number and the number of
+// point references of the vertex, so a probe reads one aligned 16-byte
+// entry and the reference count shares the cache line the insert claimed.
 struct alignas(16) HashEntry {
   uint64_t key;
   int32_t val;
-  int32_t pad;
+  int32_t count;
 };
 
 struct HashView {
@@ -149,15 +150,15 @@ inline void launch_signal(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipSt
 
 // Launchers (each .hip file implements its own kernels' launchers).
 // create.hip
-void launch_clear_table(HashEntry* entries, int32_t* counts, int64_t cap, void* dev_counters, void* scan_work,
+void launch_clear_table(HashEntry* entries, int64_t cap, void* dev_counters, void* scan_work,
                         hipStream_t s);
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
-                          float a2, int64_t m, HashView h, int32_t* counter, int32_t* slot_count,
+                          float a2, int64_t m, HashView h, int32_t* counter,
                           uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
                           float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, uint32_t stamp,
                           hipEvent_t done, hipStream_t s);
 int64_t scan_workspace_bytes();
-void launch_count_scan(const int32_t* slot_count, const int32_t* vslot, const int32_t* n_dev,
+void launch_count_scan(const HashEntry* table, const int32_t* vslot, const int32_t* n_dev,
                        int32_t* offsets, void* work, hipStream_t s);
 void launch_fill_lists(HashView h, const int32_t* slot, const int32_t* rank, const float* w,
                        const int32_t* offsets, int32_t* idx, int32_t* entries, float* entry_w,
