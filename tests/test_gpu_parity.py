@@ -1389,3 +1389,50 @@ def test_conv_backward_bf16(L, O, form, cin, cout, relu):
     P.assert_close(np.transpose(_host(gdw), (0, 2, 1)), odw, P.TOL_F32, "dW " + what)
     P.assert_close(_host(gdb), odb, P.TOL_F32, "dbias " + what)
     del keep
+
+
+def test_backward_entry_points_reject_bad_arguments(L):
+    """Host-side rejections of the backward calls added for the
+    pre-activated convolution, the classifier and Distribute + PointNet:
+    nothing is enqueued and the status names the problem."""
+    gl = L.Lattice.create(_dev(_cloud(9, 800)), [0.1] * 3)
+    dev = dict(dtype=torch.float32, device="cuda")
+    x = torch.randn((gl.n, 12), **dev)
+    W = torch.randn((9, 8, 12), **dev)
+    dy = torch.randn((gl.n, 8), **dev)
+    with pytest.raises(L.LatticeError) as e:
+        gl.conv_preact_backward(gl, x, W, dy, groups=5)                 # 5 does not divide 12
+    assert e.value.status == -1
+    with pytest.raises(L.LatticeError) as e:
+        gl.conv_preact_backward(gl, x, W, dy, groups=4, eps=0.0)        # eps must be positive
+    assert e.value.status == -1
+    other = L.Lattice.create(_dev(_cloud(10, 800)), [0.1] * 3)
+    with pytest.raises(L.LatticeError) as e:
+        gl.conv_preact_backward(other, x, W, dy, groups=4)             # unrelated lattices
+    assert e.value.status == -8
+    xv = torch.randn((gl.n, 16), **dev)
+    with pytest.raises(L.LatticeError) as e:                            # 65 classes
+        gl.deform_slice_classify_backward(xv, torch.randn(16, **dev), 0.1, torch.randn((65, 16), **dev),
+                                          torch.randn((gl.m, 65), **dev))
+    assert e.value.status == -2
+    with pytest.raises(L.LatticeError) as e:                            # beta not finite
+        gl.deform_slice_classify_backward(xv, torch.randn(16, **dev), float("nan"), torch.randn((4, 16), **dev),
+                                          torch.randn((gl.m, 4), **dev))
+    assert e.value.status == -1
+    pos = _dev(_cloud(9, 800))
+    lay = [(torch.randn((16, 5), **dev), None), (torch.randn((48, 16), **dev), None), (torch.randn((16, 48), **dev), None)]
+    with pytest.raises(L.LatticeError) as e:                            # a 48-wide normalised layer input
+        gl.distribute_pointnet_backward(pos, torch.randn((800, 2), **dev), lay, torch.randn((gl.n, 16), **dev))
+    assert e.value.status == -2
+    lay = [(torch.randn((16, 5), **dev), None), (torch.randn((32, 16), **dev), None), (torch.randn((16, 32), **dev), None)]
+    with pytest.raises(L.LatticeError) as e:                            # Cf = 30 > 29
+        gl.distribute_pointnet_backward(pos, torch.randn((800, 30), **dev),
+                                        [(torch.randn((16, 33), **dev), None)] + lay[1:],
+                                        torch.randn((gl.n, 16), **dev))
+    assert e.value.status == -2
+    xb = torch.randn((gl.n, 12), **dev).to(torch.bfloat16)
+    with pytest.raises(L.LatticeError) as e:                            # bf16 channels not a multiple of 8
+        gl.conv_backward_bf16(gl, xb, W.to(torch.bfloat16), dy.to(torch.bfloat16))
+    assert e.value.status == -2
+    other.destroy()
+    gl.destroy()
