@@ -427,7 +427,8 @@ def main():
     # is its kernel time; these completion events delay the next kernel, so
     # this region's wall time is reported beside the first, not as the
     # throughput
-    timed = [dominant] + [f for f in ("splat", "slice", "deform_slice") if f != dominant and bytes_by_fam.get(f)]
+    timed = [dominant] + [f for f in ("splat", "slice", "deform_slice", "insert")
+                          if f != dominant and bytes_by_fam.get(f)]
     for f in timed:
         lattice.timing_enable(f, True)
     torch.cuda.synchronize()
