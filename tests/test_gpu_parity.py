@@ -117,6 +117,23 @@ def test_coarsen_structure(L, O, cfg, on_stream):
         _check_structure(glv[-1], olv[-1])
 
 
+@pytest.mark.parametrize("on_stream", [False, True])
+def test_structure_of_large_inserts(L, O, on_stream):
+    """A 300k-point cloud at a fine scale (about a thousand insert
+    workgroups contending for the vertex counter, most vertices met by a
+    single point): the level and its coarsening are bit-exact against the
+    oracle, on the library's side stream and on the caller's."""
+    pos = _cloud(1900 + int(on_stream), 300_000, 1.0)
+    gl = L.Lattice.create(_dev(pos), [0.01] * 3)
+    ol = O.Lattice.create(pos, np.full(3, 0.01, np.float32))
+    _check_structure(gl, ol)
+    g1 = gl.coarsen(on_stream=on_stream)
+    o1 = ol.coarsen()
+    _check_structure(g1, o1)
+    g1.destroy()
+    gl.destroy()
+
+
 def test_empty_cloud(L):
     gl = L.Lattice.create(torch.zeros((0, 3), device="cuda"), [0.1] * 3)
     assert gl.n == 0 and gl.m == 0
