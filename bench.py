@@ -326,6 +326,8 @@ def main():
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--streams", type=int, default=2,
+                    help="compute streams: consecutive clouds' operators run on them in turn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work per CPU-baseline leg")
     ap.add_argument("--report", default=None, help="write a per-family timing report (JSON) here")
@@ -367,19 +369,34 @@ def main():
     torch.cuda.set_device(0)
     lattice.lib()
     wl = configs.make(args.config)
-    # consecutive steps overlap: the next cloud's lattices are built while
-    # this cloud's operators run (each step still does all of its work)
-    pipe = GpuPipeline(wl, overlap=True)
-    stream = torch.cuda.current_stream()
+    # Consecutive steps overlap.  Each cloud's lattices are built one step
+    # ahead on a build stream shared by all pipelines, and the clouds'
+    # operators run on `streams` compute streams in turn, each pipeline with
+    # buffers of its own, so that one cloud's operators on the small coarse
+    # levels (a few hundred workgroups) share the GPU with the next cloud's.
+    # Every step still does all of its work.
+    if args.streams < 1:
+        print("--streams must be at least 1", file=sys.stderr)
+        sys.exit(2)
+    build_stream = torch.cuda.Stream()
+    pipes = [GpuPipeline(wl, overlap=True, build_stream=build_stream) for _ in range(args.streams)]
+    streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(args.streams - 1)]
+    issued = [0]   # steps issued so far: step g runs on pipeline / stream g % streams
 
     def one_step():
-        levels, bufs, outs = pipe.step()
+        k = issued[0] % args.streams
+        issued[0] += 1
+        with torch.cuda.stream(streams[k]):
+            levels, bufs, outs = pipes[k].step()
+            pipes[k].finish_step(levels)
         return levels, bufs, outs
+
+    def last_stream():
+        return streams[(issued[0] - 1) % args.streams]
 
     # warmup (also sizes the pools)
     for _ in range(args.warmup):
-        levels, _, _ = one_step()
-        pipe.finish_step(levels)
+        one_step()
     torch.cuda.synchronize()
 
     # one instrumented step: per-family device time, to find the dominant
@@ -387,6 +404,7 @@ def main():
     for f in FAMILIES:
         lattice.timing_enable(f, True)
     levels, _, _ = one_step()
+    inst = pipes[(issued[0] - 1) % args.streams]
     torch.cuda.synchronize()
     fam_ms = {f: lattice.timing_read(f) for f in FAMILIES}
     for f in FAMILIES:
@@ -395,13 +413,13 @@ def main():
     flops = conv_flops(wl, levels)
     occ_flops = conv_occupied_flops(wl, levels) if flops else 0
     bwd_flops = conv_bwd_flops(wl, levels)
-    bytes_by_fam = {f: algorithmic_bytes(wl, levels, f, pipe) for f in FAMILIES}
-    pipe.finish_step(levels)
+    bytes_by_fam = {f: algorithmic_bytes(wl, levels, f, inst) for f in FAMILIES}
     torch.cuda.synchronize()
     dominant = max(fam_ms, key=lambda f: fam_ms[f][1])
 
-    # timed region: K steps, nothing instrumented; an event on the stream
-    # every `win` steps gives per-window device throughput (median reported)
+    # timed region: K steps, nothing instrumented; every `win` steps an
+    # event on the stream of the step issued last gives per-window device
+    # throughput (median reported)
     win = max(1, args.steps // 20)
     marks = []
     torch.cuda.synchronize()
@@ -409,12 +427,11 @@ def main():
     for i in range(args.steps):
         if i % win == 0:
             ev = torch.cuda.Event(enable_timing=True)
-            ev.record(stream)
+            ev.record(last_stream())
             marks.append((i, ev))
-        levels, _, _ = one_step()
-        pipe.finish_step(levels)
+        one_step()
     end = torch.cuda.Event(enable_timing=True)
-    end.record(stream)
+    end.record(last_stream())
     marks.append((args.steps, end))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -434,14 +451,14 @@ def main():
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     for _ in range(args.steps):
-        levels, _, _ = one_step()
-        pipe.finish_step(levels)
+        one_step()
     torch.cuda.synchronize()
     t3 = time.perf_counter()
     fam_timed = {f: lattice.timing_read(f) for f in timed}
     for f in timed:
         lattice.timing_enable(f, False)
-    pipe.flush()
+    for p in pipes:
+        p.flush()
     launches, dom_ms = fam_timed[dominant]
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
@@ -504,8 +521,10 @@ def main():
                    "conv_gflop_per_step_occupied_taps": occ_flops / 1e9,
                    "distribute_gflop_per_step": mfma_flops["distribute"] / 1e9,
                    "conv_bwd_gflop_per_step": bwd_flops / 1e9,
-                   "steps_overlap": "the next cloud's lattice build runs on its own stream during this "
-                                    "cloud's operators; every step does all of its work"},
+                   "compute_streams": args.streams,
+                   "steps_overlap": "each cloud's lattice build runs one step ahead on a build stream; "
+                                    "consecutive clouds' operators run on the compute streams in turn; "
+                                    "every step does all of its work"},
         "timing": {"timed_ms": (t1 - t0) * 1e3, "windows": len(windows), "steps_per_window": win,
                    "ms_per_step_median_window": statistics.median(windows),
                    "ms_per_step_min_window": min(windows), "ms_per_step_max_window": max(windows)},

@@ -9,6 +9,7 @@
 #include <cstring>
 #include <deque>
 #include <map>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -46,13 +47,19 @@ int hip_fail(hipError_t e, const char* what) {
 
 // ---------------------------------------------------------------------------
 // caching device allocator: freed blocks are kept per (device, size class)
-// and handed out again without hipMalloc.  A block released on one stream is
-// reused on another only after that stream has drained.
+// and handed out again without hipMalloc.  A block goes back first to the
+// stream that released it.  Handed to another stream, that stream waits for
+// an event recorded on the releasing stream at the release (the work that
+// still used the block), so neither the host nor the new stream waits for
+// anything queued later: steps on two streams that take turns with the same
+// scratch sizes keep running side by side.  One event covers all blocks of
+// a release; events are recycled once no free block refers to them.
 // ---------------------------------------------------------------------------
 struct Block {
   void* ptr;
   size_t bytes;
   hipStream_t stream;
+  std::shared_ptr<hipEvent_t> ready;   // recorded on `stream` at the release (null: not recorded)
 };
 
 class Pool {
@@ -87,7 +94,8 @@ class Pool {
       if (!lst.empty()) {
         Block b = lst.back();
         lst.pop_back();
-        HIP_TRY(hipStreamSynchronize(b.stream));
+        if (b.ready) HIP_TRY(hipStreamWaitEvent(s, *b.ready, 0));
+        else HIP_TRY(hipStreamSynchronize(b.stream));
         *out = b.ptr;
         return LAT_OK;
       }
@@ -108,11 +116,21 @@ class Pool {
   }
 
   void release(void* p, size_t bytes, hipStream_t s) {
-    if (!p || bytes == 0) return;
+    const std::pair<void*, size_t> one{p, bytes};
+    release_all(&one, 1, s);
+  }
+
+  // Blocks whose last uses are queued on stream s.
+  void release_all(const std::pair<void*, size_t>* bufs, size_t n, hipStream_t s) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return;
     std::lock_guard<std::mutex> lk(mu_);
-    free_[{dev, size_class(bytes)}].push_back(Block{p, bytes, s});
+    std::shared_ptr<hipEvent_t> ready;
+    for (size_t i = 0; i < n; ++i) {
+      if (!bufs[i].first || bufs[i].second == 0) continue;
+      if (!ready) ready = record_ready(s);
+      free_[{dev, size_class(bufs[i].second)}].push_back(Block{bufs[i].first, bufs[i].second, s, ready});
+    }
     ++releases_[s];
   }
 
@@ -135,9 +153,33 @@ class Pool {
     }
   }
 
+  // An event recorded on s now, shared by the blocks of one release; it
+  // returns to the spare list when the last of them is handed out again.
+  // Called with mu_ held (so is the deleter: blocks change only under mu_).
+  std::shared_ptr<hipEvent_t> record_ready(hipStream_t s) {
+    hipEvent_t e = nullptr;
+    if (!spare_.empty()) {
+      e = spare_.back();
+      spare_.pop_back();
+    } else if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    if (hipEventRecord(e, s) != hipSuccess) {
+      (void)hipGetLastError();
+      spare_.push_back(e);
+      return nullptr;
+    }
+    return std::shared_ptr<hipEvent_t>(new hipEvent_t(e), [this](hipEvent_t* p) {
+      spare_.push_back(*p);
+      delete p;
+    });
+  }
+
   std::mutex mu_;
   std::map<std::pair<int, size_t>, std::vector<Block>> free_;
   std::map<hipStream_t, uint64_t> releases_;
+  std::vector<hipEvent_t> spare_;   // recorded events no free block refers to
 };
 
 // ---------------------------------------------------------------------------
@@ -587,7 +629,10 @@ int join_side(lattice_s* L, hipStream_t s) {
 void lattice_s::free_all() {
   if (!counts_known && counts_ready) (void)hipEventSynchronize(counts_ready);
   if (side_seq && join_side(this, stream) != LAT_OK) (void)hipStreamSynchronize(bstream);
-  for (auto& b : owned) Pool::get().release(b.p, b.bytes, stream);
+  std::vector<std::pair<void*, size_t>> bufs;
+  bufs.reserve(owned.size());
+  for (auto& b : owned) bufs.emplace_back(b.p, b.bytes);
+  Pool::get().release_all(bufs.data(), bufs.size(), stream);
   owned.clear();
 }
 

@@ -686,6 +686,33 @@ def test_pipeline_overlapped_steps(L, O):
     pipe.flush()
 
 
+def test_pipeline_steps_on_two_streams(L, O):
+    """Two pipelines that share a build stream take steps in turn on two
+    compute streams with no host synchronisation between steps (the bench's
+    mode): consecutive clouds' operators run side by side and the library's
+    scratch blocks pass from one stream to the other through events.  Every
+    step's point outputs, copied on its own stream, match the oracle."""
+    from paper_1912_05905_amd.pipeline import GpuPipeline
+    wl = configs.make(4)
+    _, _, oouts = OraclePipeline(wl).run()
+    bs = torch.cuda.Stream()
+    pipes = [GpuPipeline(wl, overlap=True, build_stream=bs) for _ in range(2)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    kept = []
+    for i in range(6):
+        k = i % 2
+        with torch.cuda.stream(streams[k]):
+            levels, _, outs = pipes[k].step()
+            kept.append({name: outs[name].clone() for name in ("slice", "deform")})
+            pipes[k].finish_step(levels)
+    torch.cuda.synchronize()
+    for got in kept:
+        for name, t in got.items():
+            P.assert_close(_host(t), oouts[name], P.TOL_F32, name)
+    for p in pipes:
+        p.flush()
+
+
 def test_latticenet_reduced(L, O):
     """The whole LatticeNet forward (Distribute + PointNet, eight ResNet
     blocks of pre-activated convolutions, two Downsamples, two Upsamples with
