@@ -369,17 +369,19 @@ def main():
     torch.cuda.set_device(0)
     lattice.lib()
     wl = configs.make(args.config)
-    # Consecutive steps overlap.  Each cloud's lattices are built one step
-    # ahead on a build stream shared by all pipelines, and the clouds'
-    # operators run on `streams` compute streams in turn, each pipeline with
-    # buffers of its own, so that one cloud's operators on the small coarse
-    # levels (a few hundred workgroups) share the GPU with the next cloud's.
-    # Every step still does all of its work.
+    # Consecutive steps overlap.  `streams` pipelines take the clouds in
+    # turn, each with buffers and a build stream of its own: a pipeline
+    # builds its next cloud's lattices one step ahead on its build stream
+    # and runs its operators on its compute stream (the first one on the
+    # current stream), so that the small coarse levels' kernels (a few
+    # hundred workgroups each) and the latency-bound build chains share the
+    # GPU.  Two pipelines use four streams, one per hardware queue of the
+    # HIP runtime's default; a fifth stream would share a queue with another
+    # and serialise behind it.  Every step still does all of its work.
     if args.streams < 1:
         print("--streams must be at least 1", file=sys.stderr)
         sys.exit(2)
-    build_stream = torch.cuda.Stream()
-    pipes = [GpuPipeline(wl, overlap=True, build_stream=build_stream) for _ in range(args.streams)]
+    pipes = [GpuPipeline(wl, overlap=True) for _ in range(args.streams)]
     streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(args.streams - 1)]
     issued = [0]   # steps issued so far: step g runs on pipeline / stream g % streams
 
@@ -522,9 +524,9 @@ def main():
                    "distribute_gflop_per_step": mfma_flops["distribute"] / 1e9,
                    "conv_bwd_gflop_per_step": bwd_flops / 1e9,
                    "compute_streams": args.streams,
-                   "steps_overlap": "each cloud's lattice build runs one step ahead on a build stream; "
-                                    "consecutive clouds' operators run on the compute streams in turn; "
-                                    "every step does all of its work"},
+                   "steps_overlap": "pipelines take the clouds in turn, each building its next cloud's "
+                                    "lattices one step ahead on its own build stream while its operators "
+                                    "run on its own compute stream; every step does all of its work"},
         "timing": {"timed_ms": (t1 - t0) * 1e3, "windows": len(windows), "steps_per_window": win,
                    "ms_per_step_median_window": statistics.median(windows),
                    "ms_per_step_min_window": min(windows), "ms_per_step_max_window": max(windows)},

@@ -42,14 +42,14 @@ class GpuPipeline:
     pass of operators).  A step's lattices are destroyed by finish_step() one
     step later, once the build stream is ordered after the step's operators;
     flush() releases what is still held, the hierarchy built ahead
-    included.  Pipelines may share one build_stream and take steps in turn
-    on compute streams of their own (each holds its own buffers), so that
+    included.  Several pipelines (each with its own buffers and build
+    stream) may take steps in turn on compute streams of their own, so that
     consecutive clouds' operators overlap as well."""
 
-    def __init__(self, wl, overlap=False, build_stream=None):
+    def __init__(self, wl, overlap=False):
         self.wl = wl
         self.overlap = overlap
-        self._build_stream = (build_stream or torch.cuda.Stream()) if overlap else None
+        self._build_stream = torch.cuda.Stream() if overlap else None
         self._pending: list = []      # (levels, operators-done event) of finished steps
         self._ahead = None            # (levels, built event) of the next cloud
         self._events = [torch.cuda.Event() for _ in range(8)] if overlap else []

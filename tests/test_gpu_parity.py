@@ -687,17 +687,16 @@ def test_pipeline_overlapped_steps(L, O):
 
 
 def test_pipeline_steps_on_two_streams(L, O):
-    """Two pipelines that share a build stream take steps in turn on two
-    compute streams with no host synchronisation between steps (the bench's
-    mode): consecutive clouds' operators run side by side and the library's
-    scratch blocks pass from one stream to the other through events.  Every
-    step's point outputs, copied on its own stream, match the oracle."""
+    """Two pipelines, each with its own build stream, take steps in turn on
+    two compute streams (the current one and another) with no host
+    synchronisation between steps, as the bench runs them: consecutive
+    clouds' builds and operators run side by side.  Every step's point
+    outputs, copied on its own stream, match the oracle."""
     from paper_1912_05905_amd.pipeline import GpuPipeline
     wl = configs.make(4)
     _, _, oouts = OraclePipeline(wl).run()
-    bs = torch.cuda.Stream()
-    pipes = [GpuPipeline(wl, overlap=True, build_stream=bs) for _ in range(2)]
-    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    pipes = [GpuPipeline(wl, overlap=True) for _ in range(2)]
+    streams = [torch.cuda.current_stream(), torch.cuda.Stream()]
     kept = []
     for i in range(6):
         k = i % 2
