@@ -63,7 +63,17 @@ def family_of(kernel_name: str):
     return None
 
 
-def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mb, steps, warmup, key):
+def default_pipelines(wl) -> int:
+    """Pipelines the bench runs by default.  A second one helps where one
+    cloud's kernels (small levels, a few hundred workgroups) cannot fill the
+    GPU.  On the 1M-point clouds they do: a second pipeline gains 2-7% there
+    and doubles every launch's duration.  A training step (gradients given)
+    is bound by the host's issue of its ~50 operators, which a second
+    pipeline only adds to."""
+    return 2 if wl.m < 500_000 and not wl.grads else 1
+
+
+def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mb, steps, warmup, key, pipelines=2):
     """Per-family HBM bytes per step from rocprofv3 --pmc FETCH_SIZE and
     WRITE_SIZE runs of this benchmark, each counter scaled by what it reads
     for a device-to-device copy of copy_mb MiB.  Appends the result to
@@ -107,8 +117,9 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mb,
                 ent["dispatches"] += len(vals)
     runs = warmup + 1 + 2 * steps  # warmup, instrumented step, the two timed regions of the profiled run
     for fam, ent in fams.items():
-        # lattices are built one cloud ahead: one more hierarchy than steps
-        n = runs + 1 if fam in BUILD_FAMILIES else runs
+        # each pipeline builds its next cloud's lattices one step ahead: one
+        # more hierarchy per pipeline than steps
+        n = runs + pipelines if fam in BUILD_FAMILIES else runs
         ent["fetch_bytes_per_step"] = ent.pop("fetch_bytes") / n
         ent["write_bytes_per_step"] = ent.pop("write_bytes") / n
         ent["dispatches_per_step"] = ent.pop("dispatches") / n
@@ -326,8 +337,9 @@ def main():
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=4)
-    ap.add_argument("--streams", type=int, default=2,
-                    help="compute streams: consecutive clouds' operators run on them in turn")
+    ap.add_argument("--streams", type=int, default=0,
+                    help="pipelines (each with a compute and a build stream) that take the clouds in turn; "
+                         "0: two for forward workloads below 500k points, else one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work per CPU-baseline leg")
     ap.add_argument("--report", default=None, help="write a per-family timing report (JSON) here")
@@ -342,7 +354,10 @@ def main():
         print(kernel_source_hash())
         return
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, args.copy_mib, args.steps, args.warmup, f"config{args.config}")
+        from workloads import configs
+        pipelines = args.streams or default_pipelines(configs.make(args.config))
+        summarize_pmc(*args.summarize_pmc, args.copy_mib, args.steps, args.warmup, f"config{args.config}",
+                      pipelines)
         return
     if args.calibrate_copy:
         import torch
@@ -378,9 +393,11 @@ def main():
     # GPU.  Two pipelines use four streams, one per hardware queue of the
     # HIP runtime's default; a fifth stream would share a queue with another
     # and serialise behind it.  Every step still does all of its work.
-    if args.streams < 1:
-        print("--streams must be at least 1", file=sys.stderr)
+    if args.streams < 0:
+        print("--streams must be 0 (automatic) or at least 1", file=sys.stderr)
         sys.exit(2)
+    if args.streams == 0:
+        args.streams = default_pipelines(wl)
     pipes = [GpuPipeline(wl, overlap=True) for _ in range(args.streams)]
     streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(args.streams - 1)]
     issued = [0]   # steps issued so far: step g runs on pipeline / stream g % streams
@@ -523,7 +540,7 @@ def main():
                    "conv_gflop_per_step_occupied_taps": occ_flops / 1e9,
                    "distribute_gflop_per_step": mfma_flops["distribute"] / 1e9,
                    "conv_bwd_gflop_per_step": bwd_flops / 1e9,
-                   "compute_streams": args.streams,
+                   "pipelines": args.streams,
                    "steps_overlap": "pipelines take the clouds in turn, each building its next cloud's "
                                     "lattices one step ahead on its own build stream while its operators "
                                     "run on its own compute stream; every step does all of its work"},

@@ -9,7 +9,6 @@
 #include <cstring>
 #include <deque>
 #include <map>
-#include <memory>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -48,22 +47,25 @@ int hip_fail(hipError_t e, const char* what) {
 // ---------------------------------------------------------------------------
 // caching device allocator: freed blocks are kept per (device, size class)
 // and handed out again without hipMalloc.  A block goes back first to the
-// stream that released it.  Handed to another stream, that stream waits for
-// an event recorded on the releasing stream at the release (the work that
-// still used the block), so neither the host nor the new stream waits for
-// anything queued later: steps on two streams that take turns with the same
-// scratch sizes keep running side by side.  One event covers all blocks of
-// a release; events are recycled once no free block refers to them.
+// stream that released it; else to another stream once the releasing stream
+// has drained (hipStreamQuery).  While that stream is still busy the pool
+// allocates a new block rather than wait, so steps on two streams that take
+// turns with the same scratch sizes each end up with blocks of their own and
+// run side by side; only when a size class already holds kMaxIdle blocks of
+// busy streams does the caller's thread wait for one (hipStreamSynchronize).
+// Nothing is recorded at a release: an event per release cost the host
+// more than the rest of a training step's scratch handling.
 // ---------------------------------------------------------------------------
 struct Block {
   void* ptr;
   size_t bytes;
   hipStream_t stream;
-  std::shared_ptr<hipEvent_t> ready;   // recorded on `stream` at the release (null: not recorded)
 };
 
 class Pool {
  public:
+  static constexpr size_t kMaxIdle = 4;   // idle blocks of busy streams per size class before waiting
+
   static Pool& get() {
     static Pool* p = new Pool();   // never destroyed: blocks live until exit
     return *p;
@@ -91,11 +93,19 @@ class Pool {
           return LAT_OK;
         }
       }
-      if (!lst.empty()) {
+      for (size_t i = 0; i < lst.size(); ++i) {
+        const hipError_t q = hipStreamQuery(lst[i].stream);
+        if (q == hipSuccess) {
+          *out = lst[i].ptr;
+          lst.erase(lst.begin() + static_cast<long>(i));
+          return LAT_OK;
+        }
+        (void)hipGetLastError();   // hipErrorNotReady is not an error of a later call
+      }
+      if (lst.size() >= kMaxIdle) {
         Block b = lst.back();
         lst.pop_back();
-        if (b.ready) HIP_TRY(hipStreamWaitEvent(s, *b.ready, 0));
-        else HIP_TRY(hipStreamSynchronize(b.stream));
+        HIP_TRY(hipStreamSynchronize(b.stream));
         *out = b.ptr;
         return LAT_OK;
       }
@@ -125,12 +135,9 @@ class Pool {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return;
     std::lock_guard<std::mutex> lk(mu_);
-    std::shared_ptr<hipEvent_t> ready;
-    for (size_t i = 0; i < n; ++i) {
-      if (!bufs[i].first || bufs[i].second == 0) continue;
-      if (!ready) ready = record_ready(s);
-      free_[{dev, size_class(bufs[i].second)}].push_back(Block{bufs[i].first, bufs[i].second, s, ready});
-    }
+    for (size_t i = 0; i < n; ++i)
+      if (bufs[i].first && bufs[i].second != 0)
+        free_[{dev, size_class(bufs[i].second)}].push_back(Block{bufs[i].first, bufs[i].second, s});
     ++releases_[s];
   }
 
@@ -153,33 +160,9 @@ class Pool {
     }
   }
 
-  // An event recorded on s now, shared by the blocks of one release; it
-  // returns to the spare list when the last of them is handed out again.
-  // Called with mu_ held (so is the deleter: blocks change only under mu_).
-  std::shared_ptr<hipEvent_t> record_ready(hipStream_t s) {
-    hipEvent_t e = nullptr;
-    if (!spare_.empty()) {
-      e = spare_.back();
-      spare_.pop_back();
-    } else if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
-      (void)hipGetLastError();
-      return nullptr;
-    }
-    if (hipEventRecord(e, s) != hipSuccess) {
-      (void)hipGetLastError();
-      spare_.push_back(e);
-      return nullptr;
-    }
-    return std::shared_ptr<hipEvent_t>(new hipEvent_t(e), [this](hipEvent_t* p) {
-      spare_.push_back(*p);
-      delete p;
-    });
-  }
-
   std::mutex mu_;
   std::map<std::pair<int, size_t>, std::vector<Block>> free_;
   std::map<hipStream_t, uint64_t> releases_;
-  std::vector<hipEvent_t> spare_;   // recorded events no free block refers to
 };
 
 // ---------------------------------------------------------------------------
