@@ -405,9 +405,10 @@ def main():
     def one_step():
         k = issued[0] % args.streams
         issued[0] += 1
-        with torch.cuda.stream(streams[k]):
-            levels, bufs, outs = pipes[k].step()
-            pipes[k].finish_step(levels)
+        if args.streams > 1:
+            torch.cuda.set_stream(streams[k])   # (cheaper than a stream context per step)
+        levels, bufs, outs = pipes[k].step()
+        pipes[k].finish_step(levels)
         return levels, bufs, outs
 
     def last_stream():

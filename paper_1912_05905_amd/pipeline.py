@@ -55,6 +55,7 @@ class GpuPipeline:
         self._events = [torch.cuda.Event() for _ in range(8)] if overlap else []
         self._next_event = 0
         self._cur = None                    # the caller's stream of the last step
+        self._cur_raw = None                # its raw handle
         self.dtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
         self.pos = torch.from_numpy(np.ascontiguousarray(wl.positions)).cuda()
         self.feat = torch.from_numpy(np.ascontiguousarray(wl.features)).cuda().to(self.dtype)
@@ -175,7 +176,7 @@ class GpuPipeline:
             ev.record(bs)
             self._ahead = (nxt, ev)
             levels.update(ahead[0])
-            self._cur = torch.cuda.current_stream()
+            self._cur = self._current_stream()
             self._cur.wait_event(ahead[1])
         else:
             build(levels)
@@ -312,6 +313,15 @@ class GpuPipeline:
         done = self._event()
         done.record(self._cur)
         self._pending.append((levels, done))
+
+    def _current_stream(self):
+        """The current stream as a torch Stream, rebuilt only when the raw
+        handle changed (torch.cuda.current_stream() costs microseconds)."""
+        raw = _lat._stream().value
+        if self._cur is None or self._cur_raw != raw:
+            self._cur = torch.cuda.current_stream()
+            self._cur_raw = raw
+        return self._cur
 
     def _event(self):
         # a ring of events: a re-record does not affect waits already enqueued,
