@@ -20,6 +20,11 @@
  *    for the event that follows the lattice's insert kernel.
  *    lattice_create, lattice_coarsen, lattice_num_points and lattice_level
  *    never wait.
+ *  - Work space comes from a caching pool of device blocks.  A block goes
+ *    back first to the stream that released it, else to another stream once
+ *    the releasing stream is idle, else a new block is allocated; only when
+ *    a size class already holds four idle blocks of busy streams does a
+ *    call wait for one of those streams (with no error).
  *  - Matrices are row-major.  ld_* arguments are row strides in elements
  *    (0 = dense, i.e. the number of channels); they let several ops write
  *    disjoint column ranges of one buffer (channel concatenation).
