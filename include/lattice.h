@@ -121,6 +121,22 @@ int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, l
  */
 int lattice_coarsen_ex(lattice_t fine, int64_t capacity_hint, int flags, hipStream_t stream, lattice_t* coarse);
 
+/*
+ * A hierarchy of `levels` lattices (1 to 8) in one call, all built on
+ * `stream`: out[0] as lattice_create with capacity_hint 0, out[l] as
+ * lattice_coarsen_ex(out[l - 1], 0, LAT_ON_STREAM, stream, ...) for
+ * l >= 1 (Proposed Operations: each coarser level is the same points with
+ * positions divided by 2).  The results are those of that sequence of
+ * calls; the device work is issued in fewer launches and in an order that
+ * gives the host every level's vertex count sooner: the levels' tables are
+ * cleared in one launch, the inserts run level after level, then the lists
+ * and neighbour tables, with the row orders of all tables in one launch.
+ * out must hold `levels` handles; on an error none is created.  Handles
+ * are destroyed coarsest first, as for lattice_coarsen.
+ */
+int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float* sigma_host, int levels,
+                             hipStream_t stream, lattice_t* out);
+
 /* Release a handle and its device memory (LAT_ELEVEL while it has children). */
 int lattice_destroy(lattice_t L);
 

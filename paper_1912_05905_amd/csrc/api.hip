@@ -278,6 +278,7 @@ struct lattice_s {
   DeviceCounters* dc = nullptr;  // device counters (vertex count, error bits)
   HostCounts* host_dc = nullptr;  // pinned landing slot of their readback
   hipEvent_t counts_ready = nullptr;  // recorded after the readback
+  int32_t* host_counts_dev = nullptr;  // device view of host_dc (the insert's landing slot)
   int chunk = 64;                // list entries per splat work item
   int status = LAT_OK;           // poisoned when != LAT_OK
   int children = 0;
@@ -286,6 +287,8 @@ struct lattice_s {
   hipStream_t bstream = nullptr;  // stream the build ran on (the library's side stream for a coarse level)
   uint64_t side_seq = 0;          // built on the side stream: its build's number there (0: not)
   hipEvent_t built = nullptr;     // side-stream build: completes with its last kernel
+  hipEvent_t rebuilt = nullptr;   // after a rebuild (overflow, or a rebuilt parent) on the owner stream
+  std::vector<hipStream_t> rebuilt_joined;  // other streams already ordered after it
   std::vector<hipStream_t> joined;  // streams already ordered after that build
   uint64_t releases_at_insert = 0;  // owner pool's release count when the insert was enqueued
   std::vector<DevBuf> owned;
@@ -314,6 +317,7 @@ struct lattice_s {
   // indices) only when an operator first needs them: the convolutions only
   // need the tables.  Until then it keeps what the list build reads.
   bool lists_ready = true;
+  bool defer_lists = false;       // a coarse level: lists built on first use
   int32_t* vslot = nullptr;       // per vertex: its slot
   int32_t* slot = nullptr;        // per reference: slot of its vertex
   int32_t* rank = nullptr;        // per reference: rank within its vertex
@@ -426,8 +430,13 @@ struct Scratch {
 // bits into the pinned host slot; an event marks its completion), then the
 // scan, the vertex lists and the tables, which take the vertex count from
 // device memory.  Nothing waits here.
-int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_scale, const float a[3],
-                  const lattice_s* parent, int64_t cap, hipStream_t s, hipEvent_t built = nullptr) {
+// A build in three parts, so that the levels of a hierarchy can share
+// launches (lattice_create_hierarchy): prepare_build sizes and allocates
+// the level and takes its host slots (no device work), issue_insert
+// enqueues the insert (the table must have been cleared on s before),
+// issue_tables the lists (finest level) and the neighbour tables, with the
+// row orders added to `defer` when given instead of launched.
+int prepare_build(lattice_s* L, const lattice_s* parent, int64_t cap, hipStream_t s) {
   const int64_t m = L->m;
   const int64_t refs = 4 * m;
   const int64_t nmax = std::min(cap, refs);
@@ -497,37 +506,54 @@ int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_sc
   L->slot = static_cast<int32_t*>(at(o_slot));
   L->rank = static_cast<int32_t*>(at(o_rank));
   L->scan_work = at(o_work);
-  int32_t* vslot = L->vslot;
-  int32_t* slot = L->slot;
-  int32_t* rank = L->rank;
-  void* work = L->scan_work;
   if (!L->host_dc && !(L->host_dc = HostSlots::get().take())) return fail(LAT_ENOMEM, "pinned host slot");
   if (!L->counts_ready && !(L->counts_ready = HostSlots::get().take_event()))
     return fail(LAT_EDEVICE, "event creation failed");
 
-  int32_t* host_counts = nullptr;  // device view of the pinned landing slot
-  HIP_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&host_counts), L->host_dc, 0));
+  HIP_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&L->host_counts_dev), L->host_dc, 0));
   static std::atomic<uint32_t> g_stamp{0};
   L->stamp = m > 0 ? ++g_stamp : 0;
   L->host_dc->stamp = ~L->stamp;
-  launch_clear_table(L->table, cap, L->dc, work, s);
-  launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], m, L->hash(), &L->dc->counter, L->vkeys,
-                       vslot, slot, rank, L->w, L->y, &L->dc->err, host_counts, L->stamp, L->counts_ready, s);
+  L->defer_lists = defer_lists;
+  // unknown until the insert reports (a coarser level prepared before this
+  // one's insert is enqueued must not size its table from n = 0)
+  L->counts_known = false;
+  return LAT_OK;
+}
+
+int issue_insert(lattice_s* L, const float* pos, const float* y_src, float y_scale, const float a[3], hipStream_t s) {
+  launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], L->m, L->hash(), &L->dc->counter, L->vkeys,
+                       L->vslot, L->slot, L->rank, L->w, L->y, &L->dc->err, L->host_counts_dev, L->stamp,
+                       L->counts_ready, s);
   L->releases_at_insert = Pool::get().release_count(L->stream);
   HIP_TRY(hipGetLastError());
   L->counts_known = false;
+  return LAT_OK;
+}
+
+void issue_tables(lattice_s* L, const lattice_s* parent, hipEvent_t built, hipStream_t s, RowOrderBatch* defer) {
   const int32_t* n_dev = &L->dc->counter;
-  L->lists_ready = !defer_lists;
-  if (!defer_lists) {
-    launch_count_scan(L->table, vslot, n_dev, L->offsets, work, s);
-    launch_fill_lists(L->hash(), slot, rank, L->w, L->offsets, L->idx, L->entries, L->entry_w, L->chunk_first,
-                      L->chunk, refs, s);
+  L->lists_ready = !L->defer_lists;
+  if (!L->defer_lists) {
+    launch_count_scan(L->table, L->vslot, n_dev, L->offsets, L->scan_work, s);
+    launch_fill_lists(L->hash(), L->slot, L->rank, L->w, L->offsets, L->idx, L->entries, L->entry_w,
+                      L->chunk_first, L->chunk, L->total, s);
   }
   if (parent)
-    launch_coarse_tables(L->hash(), parent->hash(), L->vkeys, parent->vkeys, n_dev, &parent->dc->counter, nmax,
-                         parent->nmax, L->nbr, L->down, L->up, L->up_rows, L->nbr_rows, L->down_rows, built, s);
+    launch_coarse_tables(L->hash(), parent->hash(), L->vkeys, parent->vkeys, n_dev, &parent->dc->counter, L->nmax,
+                         parent->nmax, L->nbr, L->down, L->up, L->up_rows, L->nbr_rows, L->down_rows, built, s,
+                         defer);
   else
-    launch_neighbor_table(L->hash(), L->vkeys, n_dev, nmax, L->nbr, nmax, L->nbr_rows, s);
+    launch_neighbor_table(L->hash(), L->vkeys, n_dev, L->nmax, L->nbr, L->nmax, L->nbr_rows, s, defer);
+}
+
+int enqueue_build(lattice_s* L, const float* pos, const float* y_src, float y_scale, const float a[3],
+                  const lattice_s* parent, int64_t cap, hipStream_t s, hipEvent_t built = nullptr) {
+  int st;
+  if ((st = prepare_build(L, parent, cap, s)) != LAT_OK) return st;
+  launch_clear_table(L->table, cap, L->dc, L->scan_work, s);
+  if ((st = issue_insert(L, pos, y_src, y_scale, a, s)) != LAT_OK) return st;
+  issue_tables(L, parent, built, s, nullptr);
   return check_launch("lattice build");
 }
 
@@ -654,6 +680,15 @@ void leave_side(lattice_s* L) {
 // After a rebuild on the owner stream: later work there is ordered after it.
 void rebuilt_on_owner_stream(lattice_s* L) { leave_side(L); }
 
+// After a rebuild enqueued on the owner stream (from inside a call that may
+// run on another stream): an event that use() makes other streams wait on.
+int mark_rebuilt(lattice_s* L) {
+  if (!L->rebuilt && !(L->rebuilt = HostSlots::get().take_event())) return fail(LAT_EDEVICE, "event creation failed");
+  HIP_TRY(hipEventRecord(L->rebuilt, L->stream));
+  L->rebuilt_joined.clear();
+  return LAT_OK;
+}
+
 // Wait for a handle's counter readback; report device-side errors.
 int ensure_counts(lattice_s* L) {
   if (L->counts_known) return L->status;
@@ -677,6 +712,7 @@ int ensure_counts(lattice_s* L) {
       L->parent_generation = P->generation;
       const float a[3] = {0.f, 0.f, 0.f};
       st = enqueue_build(L, nullptr, P->y, 0.5f, a, P, initial_capacity(L, P, 0), L->stream);
+      if (st == LAT_OK) st = mark_rebuilt(L);
       if (st != LAT_OK) {
         L->status = st;
         return st;
@@ -717,6 +753,7 @@ int ensure_counts(lattice_s* L) {
     const float a[3] = {0.f, 0.f, 0.f};
     const float* src = L->parent ? L->parent->y : static_cast<const float*>(old_y.p);
     st = enqueue_build(L, nullptr, src, L->parent ? 0.5f : 1.0f, a, L->parent, cap, L->stream);
+    if (st == LAT_OK) st = mark_rebuilt(L);
     Pool::get().release(old_y.p, old_y.bytes, L->stream);
     ++L->generation;
     if (st != LAT_OK) { L->status = st; return st; }
@@ -767,6 +804,12 @@ int check_handle(lattice_s* L) {
 int use(lattice_s* L, hipStream_t s) {
   int st;
   if ((st = check_handle(L)) != LAT_OK) return st;
+  if (L->rebuilt && s != L->stream &&
+      std::find(L->rebuilt_joined.begin(), L->rebuilt_joined.end(), s) == L->rebuilt_joined.end()) {
+    // a rebuild ran on the owner stream: order this stream after it
+    HIP_TRY(hipStreamWaitEvent(s, L->rebuilt, 0));
+    L->rebuilt_joined.push_back(s);
+  }
   return join_side(L, s);
 }
 
@@ -911,6 +954,83 @@ int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_ho
   return LAT_OK;
 }
 
+int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float* sigma_host, int levels,
+                             hipStream_t stream, lattice_t* out) {
+  if (!out) return fail(LAT_EINVAL, "out is null");
+  if (levels < 1 || levels > kMaxClearJobs)
+    return fail(LAT_EINVAL, "levels must be 1 to " + std::to_string(kMaxClearJobs));
+  for (int l = 0; l < levels; ++l) out[l] = nullptr;
+  if (d != kDim) return fail(LAT_EUNSUPPORTED, "only d = 3 is supported");
+  if (m < 0) return fail(LAT_EINVAL, "m < 0");
+  if (m > 0 && !pos_dev) return fail(LAT_EINVAL, "pos is null");
+  if (4 * m > INT32_MAX) return fail(LAT_EUNSUPPORTED, "more than 2^29 points");
+  if (!sigma_host) return fail(LAT_EINVAL, "sigma is null");
+  for (int j = 0; j < kDim; ++j)
+    if (!(sigma_host[j] > 0.0f) || !std::isfinite(sigma_host[j]))
+      return fail(LAT_EINVAL, "sigma must be positive and finite");
+  float a[kDim];
+  const double sc = (kDim + 1) * std::sqrt(2.0 / 3.0);
+  for (int j = 0; j < kDim; ++j)
+    a[j] = static_cast<float>(sc / (static_cast<double>(sigma_host[j]) *
+                                    std::sqrt(static_cast<double>((j + 1) * (j + 2)))));
+  const float a0[kDim] = {0.f, 0.f, 0.f};
+  lattice_s* Ls[kMaxClearJobs] = {};
+  auto discard = [&](int st) {
+    for (int l = levels - 1; l >= 0; --l) {
+      if (!Ls[l]) continue;
+      Ls[l]->free_all();
+      HostSlots::get().give(Ls[l]->host_dc);
+      HostSlots::get().give_event(Ls[l]->counts_ready);
+      delete Ls[l];
+    }
+    return st;
+  };
+  // every level sized and allocated before any device work
+  int st;
+  for (int l = 0; l < levels; ++l) {
+    lattice_s* L = new lattice_s();
+    Ls[l] = L;
+    L->m = m;
+    L->level = l;
+    L->stream = stream;
+    lattice_s* parent = l ? Ls[l - 1] : nullptr;
+    L->parent = parent;
+    for (int j = 0; j < kDim; ++j) L->scale[j] = parent ? 2.0 * parent->scale[j] : sigma_host[j];
+    if (parent) L->parent_generation = parent->generation;
+    if (m == 0) continue;
+    L->retry_cap = next_pow2(std::max<int64_t>(1024, 8 * m));
+    if ((st = prepare_build(L, parent, initial_capacity(L, parent, 0), stream)) != LAT_OK) return discard(st);
+  }
+  if (m > 0) {
+    // the levels' tables cleared in one launch, the inserts in level order
+    // (a level's insert reads the finer level's elevated positions), then
+    // the lists and tables, their row orders batched
+    ClearJob jobs[kMaxClearJobs];
+    for (int l = 0; l < levels; ++l) jobs[l] = ClearJob{Ls[l]->table, Ls[l]->cap, Ls[l]->dc, Ls[l]->scan_work};
+    launch_clear_tables(jobs, levels, stream);
+    for (int l = 0; l < levels; ++l)
+      if ((st = issue_insert(Ls[l], l ? nullptr : pos_dev, l ? Ls[l - 1]->y : nullptr, 0.5f, l ? a0 : a,
+                             stream)) != LAT_OK)
+        return discard(st);
+    RowOrderBatch batch;
+    for (int l = 0; l < levels; ++l) {
+      const int jobs_here = l ? 3 : 1;
+      if (batch.n + jobs_here > kMaxRowOrderJobs) {
+        launch_row_orders(batch, nullptr, stream);
+        batch = RowOrderBatch{};
+      }
+      issue_tables(Ls[l], l ? Ls[l - 1] : nullptr, nullptr, stream, &batch);
+    }
+    launch_row_orders(batch, nullptr, stream);
+    if ((st = check_launch("lattice hierarchy build")) != LAT_OK) return discard(st);
+  }
+  for (int l = 0; l < levels; ++l) {
+    if (l) Ls[l - 1]->children += 1;
+    out[l] = Ls[l];
+  }
+  return LAT_OK;
+}
+
 int lattice_coarsen(lattice_t fine, int64_t capacity_hint, hipStream_t stream, lattice_t* coarse) {
   return lattice_coarsen_ex(fine, capacity_hint, 0, stream, coarse);
 }
@@ -989,6 +1109,7 @@ int lattice_destroy(lattice_t L) {
   L->free_all();
   HostSlots::get().give(L->host_dc);
   HostSlots::get().give_event(L->counts_ready);
+  HostSlots::get().give_event(L->rebuilt);
   leave_side(L);
   delete L;
   return LAT_OK;

@@ -50,6 +50,22 @@ k_clear_table(HashEntry* __restrict__ entries, int64_t cap, uint4* __restrict__ 
   if (i < kScanBlocks) scan_status[i] = 0ull;
 }
 
+// k_clear_table for several tables at once: blockIdx.y picks the table.
+struct ClearJobs {
+  ClearJob job[kMaxClearJobs];
+};
+
+__global__ void __launch_bounds__(kBlock)
+k_clear_tables(ClearJobs jobs) {
+  const ClearJob& J = jobs.job[blockIdx.y];
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int64_t e = i; e < J.cap; e += stride)
+    *reinterpret_cast<uint4*>(&J.entries[e]) = make_uint4(0xffffffffu, 0xffffffffu, 0u, 0u);
+  if (i == 0) *static_cast<uint4*>(J.dev_counters) = make_uint4(0u, 0u, 0u, 0u);
+  if (i < kScanBlocks) static_cast<uint64_t*>(J.scan_work)[i] = 0ull;
+}
+
 // Exclusive prefix sum over the workgroup (wave shuffles, then the four
 // wave totals through LDS); *total receives the workgroup sum.
 __device__ inline int32_t block_exclusive_sum(int32_t v, int32_t* lds4, int32_t* total) {
@@ -528,22 +544,16 @@ constexpr int kOrderRange = 4096;
 
 constexpr int kOrderThreads = 1024;
 
-// Up to three tables ordered in one launch: blockIdx.y picks the table.
-struct MaskOrderJob {
-  const int32_t* nbr;     // tap-major table, row stride ldn
-  int64_t ldn;
-  const int32_t* n_dev;   // its row count (device)
-  int32_t* rows;          // out: its rows grouped by tap mask within ranges
-};
+// Several tables ordered in one launch: blockIdx.y picks the table.
 struct MaskOrderJobs {
-  MaskOrderJob job[3];
+  RowOrderJob job[kMaxRowOrderJobs];
 };
 
 __global__ void __launch_bounds__(kOrderThreads)
 k_mask_order(MaskOrderJobs jobs) {
-  const MaskOrderJob& J = jobs.job[blockIdx.y];
+  const RowOrderJob& J = jobs.job[blockIdx.y];
   const int32_t* __restrict__ nbr = J.nbr;
-  const int64_t ldn = J.ldn;
+  const int64_t ldn = J.ld;
   const int32_t* __restrict__ n_dev = J.n_dev;
   int32_t* __restrict__ rows = J.rows;
   __shared__ int32_t hist[kMaskBins];
@@ -696,21 +706,21 @@ inline unsigned stride_grid(int64_t work) {
 }
 
 void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_dev, int64_t n_max,
-                           int32_t* nbr, int64_t ldn, int32_t* nbr_rows, hipStream_t s) {
+                           int32_t* nbr, int64_t ldn, int32_t* nbr_rows, hipStream_t s, RowOrderBatch* defer) {
   if (n_max <= 0) return;
   ScopedKernelTimer tm("nbr", s);
   launch(k_neighbor_table, dim3(stride_grid(n_max * kTaps)), dim3(kBlock), 0, s, h, vkeys, n_dev,
                      nbr, ldn);
-  MaskOrderJobs jobs{};
-  jobs.job[0] = MaskOrderJob{nbr, ldn, n_dev, nbr_rows};
-  launch(k_mask_order, dim3(static_cast<unsigned>((n_max + kOrderRange - 1) / kOrderRange), 1), dim3(kOrderThreads),
-         0, s, jobs);
+  RowOrderBatch own;
+  RowOrderBatch& b = defer ? *defer : own;
+  b.add(RowOrderJob{nbr, ldn, n_dev, nbr_rows}, n_max);
+  if (!defer) launch_row_orders(b, nullptr, s);
 }
 
 void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse_keys, const uint64_t* fine_keys,
                           const int32_t* nc_dev, const int32_t* nf_dev, int64_t nc_max, int64_t nf_max, int32_t* nbr,
                           int32_t* down, int32_t* up, int32_t* up_rows, int32_t* nbr_rows, int32_t* down_rows,
-                          hipEvent_t done, hipStream_t s) {
+                          hipEvent_t done, hipStream_t s, RowOrderBatch* defer) {
   if (nc_max <= 0 || nf_max <= 0) {
     if (done) (void)hipEventRecord(done, s);
     return;
@@ -718,16 +728,43 @@ void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse
   ScopedKernelTimer tm("nbr", s);
   launch(k_coarse_tables, dim3(stride_grid((2 * nc_max + nf_max) * kTaps)), dim3(kBlock), 0, s, coarse,
                      fine, coarse_keys, fine_keys, nc_dev, nf_dev, nbr, down, nc_max, up, nf_max);
-  // the rows of all three tables grouped by tap mask, in one launch
+  // the rows of all three tables grouped by tap mask, in one launch (or in
+  // the caller's batch)
+  RowOrderBatch own;
+  RowOrderBatch& b = defer ? *defer : own;
+  b.add(RowOrderJob{up, nf_max, nf_dev, up_rows}, nf_max);
+  b.add(RowOrderJob{nbr, nc_max, nc_dev, nbr_rows}, nc_max);
+  b.add(RowOrderJob{down, nc_max, nc_dev, down_rows}, nc_max);
+  if (!defer) launch_row_orders(b, done, s);
+}
+
+void launch_row_orders(const RowOrderBatch& b, hipEvent_t done, hipStream_t s) {
+  if (b.n == 0 || b.max_rows <= 0) {
+    if (done) (void)hipEventRecord(done, s);
+    return;
+  }
+  ScopedKernelTimer tm("nbr", s);
   MaskOrderJobs jobs{};
-  jobs.job[0] = MaskOrderJob{up, nf_max, nf_dev, up_rows};
-  jobs.job[1] = MaskOrderJob{nbr, nc_max, nc_dev, nbr_rows};
-  jobs.job[2] = MaskOrderJob{down, nc_max, nc_dev, down_rows};
-  const dim3 grid(static_cast<unsigned>((std::max(nf_max, nc_max) + kOrderRange - 1) / kOrderRange), 3);
+  for (int i = 0; i < b.n; ++i) jobs.job[i] = b.job[i];
+  const dim3 grid(static_cast<unsigned>((b.max_rows + kOrderRange - 1) / kOrderRange), static_cast<unsigned>(b.n));
   if (done)
     launch_signal(k_mask_order, grid, dim3(kOrderThreads), 0, s, done, jobs);
   else
     launch(k_mask_order, grid, dim3(kOrderThreads), 0, s, jobs);
+}
+
+void launch_clear_tables(const ClearJob* jobs, int n, hipStream_t s) {
+  if (n <= 0) return;
+  ClearJobs J{};
+  int64_t cap_max = 0;
+  for (int i = 0; i < n; ++i) {
+    J.job[i] = jobs[i];
+    cap_max = std::max(cap_max, jobs[i].cap);
+  }
+  const int64_t want = (cap_max + kBlock * 4 - 1) / (kBlock * 4);
+  const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : (want < 8192 ? want : 8192));
+  ScopedKernelTimer tm("fill", s);
+  launch(k_clear_tables, dim3(grid, static_cast<unsigned>(n)), dim3(kBlock), 0, s, J);
 }
 
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s) {

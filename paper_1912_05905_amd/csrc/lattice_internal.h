@@ -148,10 +148,37 @@ inline void launch_signal(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipSt
   }
 }
 
+// Build work batched over the levels of a hierarchy: tables cleared in one
+// launch, tables' rows ordered by tap mask in one launch.
+struct ClearJob {
+  HashEntry* entries;
+  int64_t cap;
+  void* dev_counters;   // the level's device counters (zeroed)
+  void* scan_work;      // the level's scan status words (zeroed)
+};
+constexpr int kMaxClearJobs = 8;
+struct RowOrderJob {
+  const int32_t* nbr;   // tap-major table, row stride ld
+  int64_t ld;
+  const int32_t* n_dev; // its row count (device)
+  int32_t* rows;        // out: its rows grouped by tap mask within ranges
+};
+constexpr int kMaxRowOrderJobs = 8;
+struct RowOrderBatch {
+  RowOrderJob job[kMaxRowOrderJobs];
+  int n = 0;
+  int64_t max_rows = 0;  // bound on the jobs' row counts (host)
+  void add(const RowOrderJob& j, int64_t rows_max) {
+    job[n++] = j;
+    if (rows_max > max_rows) max_rows = rows_max;
+  }
+};
+
 // Launchers (each .hip file implements its own kernels' launchers).
 // create.hip
 void launch_clear_table(HashEntry* entries, int64_t cap, void* dev_counters, void* scan_work,
                         hipStream_t s);
+void launch_clear_tables(const ClearJob* jobs, int n, hipStream_t s);
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
                           float a2, int64_t m, HashView h, int32_t* counter,
                           uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
@@ -163,13 +190,18 @@ void launch_count_scan(const HashEntry* table, const int32_t* vslot, const int32
 void launch_fill_lists(HashView h, const int32_t* slot, const int32_t* rank, const float* w,
                        const int32_t* offsets, int32_t* idx, int32_t* entries, float* entry_w,
                        int32_t* chunk_first, int chunk, int64_t m4, hipStream_t s);
-// the table, then its rows grouped by tap mask within ranges of 4096 (nbr_rows)
+// the table, then its rows grouped by tap mask within ranges of 4096
+// (nbr_rows); with `defer` the row order is added to that batch instead of
+// launched
 void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_dev, int64_t n_max,
-                           int32_t* nbr, int64_t ldn, int32_t* nbr_rows, hipStream_t s);
+                           int32_t* nbr, int64_t ldn, int32_t* nbr_rows, hipStream_t s,
+                           RowOrderBatch* defer = nullptr);
 void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse_keys, const uint64_t* fine_keys,
                           const int32_t* nc_dev, const int32_t* nf_dev, int64_t nc_max, int64_t nf_max, int32_t* nbr,
                           int32_t* down, int32_t* up, int32_t* up_rows, int32_t* nbr_rows, int32_t* down_rows,
-                          hipEvent_t done, hipStream_t s);
+                          hipEvent_t done, hipStream_t s, RowOrderBatch* defer = nullptr);
+// the batch's row orders in one launch (`done`, if given, bound to it)
+void launch_row_orders(const RowOrderBatch& b, hipEvent_t done, hipStream_t s);
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s);
 // adds to *count the (row, tap) pairs of the first n rows whose entry is >= 0
 void launch_count_taps(const int32_t* tab, int64_t ld, int64_t n, unsigned long long* count, hipStream_t s);

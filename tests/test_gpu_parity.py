@@ -208,6 +208,102 @@ def test_overflow_rebuild_of_a_hierarchy(L, O):
                        "transposed conv")
 
 
+def _check_down_up(rng, g2o, levels_g, levels_o):
+    """Strided and transposed convolutions between consecutive levels (the
+    Downsample and Upsample tables) against the oracle."""
+    for (gf, of, pf), (gc, oc, pc) in zip(list(zip(levels_g, levels_o, g2o))[:-1],
+                                          list(zip(levels_g, levels_o, g2o))[1:]):
+        Xf = rng.normal(size=(of.n, 16))
+        Wd = _rand_w(rng, 16, 32, 1.0 / 12)
+        gy = gc.conv(gf, _dev(Xf[pf].astype(np.float32)), _gpu_w(Wd.astype(np.float32), torch.float32))
+        P.assert_close(P.rows_in_oracle_order(_host(gy), pc), oc.conv(of, Xf, Wd), P.TOL_F32, "strided conv")
+        Xc = rng.normal(size=(oc.n, 32))
+        Wu = _rand_w(rng, 32, 16, 1.0 / 12)
+        gz = gf.refine(gc, _dev(Xc[pc].astype(np.float32)), _gpu_w(Wu.astype(np.float32), torch.float32))
+        P.assert_close(P.rows_in_oracle_order(_host(gz), pf), of.refine_into(oc, Xc, Wu), P.TOL_F32,
+                       "transposed conv")
+
+
+@pytest.mark.parametrize("cfg,levels", [(2, 3), (4, 3), (4, 1)])
+def test_create_hierarchy(L, O, cfg, levels):
+    """lattice_create_hierarchy (one call, tables cleared together, inserts
+    level after level, row orders batched) gives the lattices of create +
+    coarsen: every level bit-exact, the Downsample / Upsample tables through
+    the strided and transposed convolutions, and a splat on the coarsest
+    level (whose lists are built on first use)."""
+    wl = configs.make(cfg)
+    gls = L.Lattice.create_hierarchy(_dev(wl.positions), wl.sigma, levels)
+    ols = [O.Lattice.create(wl.positions, wl.sigma)]
+    for _ in range(levels - 1):
+        ols.append(ols[-1].coarsen())
+    g2o = [_check_structure(g, o) for g, o in zip(gls, ols)]
+    _check_down_up(np.random.default_rng(31 + cfg), g2o, gls, ols)
+    F = np.random.default_rng(5).normal(size=(wl.m, 8)).astype(np.float32)
+    gv = gls[-1].splat(_dev(F))
+    P.assert_close(P.rows_in_oracle_order(_host(gv), g2o[-1]), ols[-1].splat(F)[0], P.TOL_F32, "splat")
+    for g in reversed(gls):
+        g.destroy()
+
+
+def test_create_hierarchy_overflow_rebuild(L, O):
+    """A hierarchy built in one call from points far apart on the lattice's
+    scale: every level's first table overflows (nearly 4 vertices per
+    point), the first read rebuilds the fine level and then each coarse
+    level from the rebuilt one, as for create + coarsen."""
+    pos = _cloud(72, 3000, 1.0)
+    sigma = 0.002
+    gls = L.Lattice.create_hierarchy(_dev(pos), [sigma] * 3, 3)
+    ols = [O.Lattice.create(pos, np.full(3, sigma, np.float32))]
+    for _ in range(2):
+        ols.append(ols[-1].coarsen())
+    assert ols[0].n > 2 * 3000 * 1.3
+    g2o = [_check_structure(g, o) for g, o in zip(gls[::-1], ols[::-1])][::-1]
+    _check_down_up(np.random.default_rng(13), g2o, gls, ols)
+
+
+def test_rebuild_ordered_for_another_stream(L, O):
+    """A lattice built on one stream whose table overflows is rebuilt there
+    by the first call that needs its vertex count; an operator called on
+    another stream (here with other work still queued on the first) is
+    ordered after that rebuild, without host synchronisation."""
+    pos = _cloud(73, 3000, 1.0)
+    sigma = 0.002
+    F = np.random.default_rng(74).normal(size=(3000, 8)).astype(np.float32)
+    pd, Fd = _dev(pos), _dev(F)
+    big = torch.randn((2048, 2048), device="cuda")
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(sa):
+        gl = L.Lattice.create(pd, [sigma] * 3)
+        for _ in range(8):
+            big = big @ big * 1e-3            # keeps the build stream busy
+    with torch.cuda.stream(sb):
+        got = gl.splat(Fd)
+    torch.cuda.synchronize()
+    ol = O.Lattice.create(pos, np.full(3, sigma, np.float32))
+    assert ol.n > 2 * 3000 * 1.3              # beyond the first table's reach
+    g2o = _check_structure(gl, ol)
+    P.assert_close(P.rows_in_oracle_order(_host(got), g2o), ol.splat(F)[0], P.TOL_F32, "splat")
+    gl.destroy()
+
+
+def test_create_hierarchy_rejections(L):
+    """Bad arguments return an error and create no handle; an empty cloud
+    gives empty levels."""
+    pos = torch.zeros((10, 3), device="cuda")
+    for levels in (0, 9):
+        with pytest.raises(L.LatticeError) as e:
+            L.Lattice.create_hierarchy(pos, [0.1] * 3, levels)
+        assert e.value.status == -1   # LAT_EINVAL
+    with pytest.raises(L.LatticeError) as e:
+        L.Lattice.create_hierarchy(pos, [0.1, 0.0, 0.1], 2)
+    assert e.value.status == -1   # LAT_EINVAL
+    empty = L.Lattice.create_hierarchy(torch.zeros((0, 3), device="cuda"), [0.1] * 3, 3)
+    assert [g.n for g in empty] == [0, 0, 0] and [g.level for g in empty] == [0, 1, 2]
+    for g in reversed(empty):
+        g.destroy()
+
+
 def test_host_validation_on_gpu(L):
     gl = L.Lattice.create(_dev(_cloud(7, 500)), [0.1] * 3)
     x = torch.zeros((gl.n, 6), device="cuda")
