@@ -37,20 +37,9 @@ constexpr int kScanBlocks = 256;
 constexpr uint64_t kScanReady = 1ull << 32;  // flag of a published range sum
 constexpr int kScanPer = 8;                   // consecutive vertices per thread in a scan tile
 
-// Empty hash table (reference counts 0); zero device counters and scan
-// status words for the build that follows.
-__global__ void __launch_bounds__(kBlock)
-k_clear_table(HashEntry* __restrict__ entries, int64_t cap, uint4* __restrict__ dev_counters,
-              uint64_t* __restrict__ scan_status) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-  for (int64_t e = i; e < cap; e += stride)
-    *reinterpret_cast<uint4*>(&entries[e]) = make_uint4(0xffffffffu, 0xffffffffu, 0u, 0u);
-  if (i == 0) *dev_counters = make_uint4(0u, 0u, 0u, 0u);
-  if (i < kScanBlocks) scan_status[i] = 0ull;
-}
-
-// k_clear_table for several tables at once: blockIdx.y picks the table.
+// Empty hash tables (every key empty, reference counts 0), and zero device
+// counters and scan status words for the builds that follow; several
+// tables in one launch: blockIdx.y picks one.
 struct ClearJobs {
   ClearJob job[kMaxClearJobs];
 };
@@ -657,11 +646,8 @@ inline unsigned blocks_for(int64_t n) { return static_cast<unsigned>((n + kBlock
 }  // namespace
 
 void launch_clear_table(HashEntry* keys, int64_t cap, void* dev_counters, void* scan_work, hipStream_t s) {
-  const int64_t want = (cap + kBlock * 4 - 1) / (kBlock * 4);
-  const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : (want < 8192 ? want : 8192));
-  ScopedKernelTimer tm("fill", s);
-  launch(k_clear_table, dim3(grid), dim3(kBlock), 0, s, keys, cap,
-                     static_cast<uint4*>(dev_counters), static_cast<uint64_t*>(scan_work));
+  const ClearJob job{keys, cap, dev_counters, scan_work};
+  launch_clear_tables(&job, 1, s);
 }
 
 void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,

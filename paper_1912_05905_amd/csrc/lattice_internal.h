@@ -164,6 +164,9 @@ struct RowOrderJob {
   int32_t* rows;        // out: its rows grouped by tap mask within ranges
 };
 constexpr int kMaxRowOrderJobs = 8;
+// Filled by launch_neighbor_table (one job) and launch_coarse_tables (three);
+// the caller keeps n + jobs <= kMaxRowOrderJobs, launching the batch
+// (launch_row_orders) when the next level would not fit.
 struct RowOrderBatch {
   RowOrderJob job[kMaxRowOrderJobs];
   int n = 0;
