@@ -67,10 +67,8 @@ def default_pipelines(wl) -> int:
     """Pipelines the bench runs by default.  A second one helps where one
     cloud's kernels (small levels, a few hundred workgroups) cannot fill the
     GPU.  On the 1M-point clouds they do: a second pipeline gains 2-7% there
-    and doubles every launch's duration.  A training step (gradients given)
-    is bound by the host's issue of its ~50 operators, which a second
-    pipeline only adds to."""
-    return 2 if wl.m < 500_000 and not wl.grads else 1
+    and doubles every launch's duration."""
+    return 2 if wl.m < 500_000 else 1
 
 
 def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mb, steps, warmup, key, pipelines=2):
@@ -339,7 +337,7 @@ def main():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--streams", type=int, default=0,
                     help="pipelines (each with a compute and a build stream) that take the clouds in turn; "
-                         "0: two for forward workloads below 500k points, else one")
+                         "0: two below 500k points, else one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work per CPU-baseline leg")
     ap.add_argument("--report", default=None, help="write a per-family timing report (JSON) here")

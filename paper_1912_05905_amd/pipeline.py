@@ -99,6 +99,15 @@ class GpuPipeline:
                 self._outs[name] = t
         return t
 
+    def _grad(self, name, shape, keep):
+        """Gradient output buffer (float32), kept across steps unless keep."""
+        t = None if keep else self._outs.get(name)
+        if t is None or tuple(t.shape) != tuple(shape):
+            t = torch.empty(shape, dtype=torch.float32, device="cuda")
+            if not keep:
+                self._outs[name] = t
+        return t
+
     def step(self, keep=False, after_op=None):
         """One pass of the pipeline.  Returns (levels, buffers, point outputs).
 
@@ -266,12 +275,43 @@ class GpuPipeline:
                 out = outs[op["out"]] = self._out(op["out"], L.m, Wc.shape[0], keep)
                 check(lib.lattice_deform_slice_classify(L._h, xp, xld, cc, dt, wv.data_ptr(), beta, Wc.data_ptr(),
                                                         bc.data_ptr(), Wc.shape[0], out.data_ptr(), stream))
-            elif kind in ("deform_slice_bwd", "conv_bwd", "splat_bwd"):
-                # backward operators: through the Lattice methods, on views
-                for key in ("x", "src", "y", "dst"):
-                    if key in op:
-                        ptr(op[key])
-                self._backward_op(op, levels, _Buffers(self._store, rows), outs)
+            elif kind == "conv_bwd":
+                lv = op["level"]
+                dst = levels[lv]
+                src = levels[{"conv": lv, "conv_down": lv - 1, "refine": lv + 1}[op["kind"]]]
+                xp, xld = ptr(op["x"])
+                gp, gld = ptr(op["src"])
+                dp, dld = ptr(op["dst"])
+                yp, yld = ptr(op["y"]) if op["relu"] else (None, 0)
+                wp, cout, cin = self._wptr[op["w"]]
+                dW = self._grad(op["out"], (9, cout, cin), keep)
+                db = self._grad("db:" + op["w"], (cout,), keep)
+                check(lib.lattice_conv_backward(dst._h, src._h, xp, xld, cin, wp, cout,
+                                                _lat.LAT_RELU if op["relu"] else 0, yp, yld, gp, gld, dp, dld,
+                                                dW.data_ptr(), db.data_ptr(), stream))
+                outs[op["out"]] = dW.transpose(1, 2)          # taps x Cin x Cout, the workload's layout
+                outs["db:" + op["w"]] = db
+            elif kind == "deform_slice_bwd":
+                L = levels[op["level"]]
+                wv, beta = self.vectors[op["wv"]]
+                xp, xld = ptr(op["x"])
+                dp, dld = ptr(op["dst"])
+                cc = op["x"][2]
+                g = self.grads[op["grad"]]
+                dwv = self._grad(op["out"], (cc,), keep)
+                dbeta = self._grad("dbeta:" + op["wv"], (1,), keep)
+                check(lib.lattice_deform_slice_backward(L._h, xp, xld, cc, wv.data_ptr(), beta, g.data_ptr(),
+                                                        g.stride(0), dp, dld, dwv.data_ptr(), dbeta.data_ptr(),
+                                                        stream))
+                outs[op["out"]], outs["dbeta:" + op["wv"]] = dwv, dbeta
+            elif kind == "splat_bwd":
+                L0 = levels[0]
+                gp, gld = ptr(op["src"])
+                cc = op["src"][2]
+                out = self._grad(op["out"], (L0.m, cc), keep)
+                check(lib.lattice_splat_backward(L0._h, gp, gld, cc, int(bool(op["normalize"])),
+                                                 self._wsum.data_ptr(), out.data_ptr(), stream))
+                outs[op["out"]] = out
             else:
                 raise ValueError(f"unknown op {kind}")
             if after_op is not None:
@@ -280,29 +320,6 @@ class GpuPipeline:
         if keep:
             self._store = {}
         return levels, _Buffers(stores, rows), outs
-
-    def _backward_op(self, op, levels, bufs, outs):
-        def view(spec):
-            name, c0, cc = spec
-            return bufs[name][:, c0:c0 + cc]
-
-        kind = op["op"]
-        if kind == "deform_slice_bwd":
-            wv, beta = self.vectors[op["wv"]]
-            _, dwv, dbeta = levels[op["level"]].deform_slice_backward(
-                view(op["x"]), wv, beta, self.grads[op["grad"]], dx_out=view(op["dst"]))
-            outs[op["out"]], outs["dbeta:" + op["wv"]] = dwv, dbeta
-        elif kind == "conv_bwd":
-            lv = op["level"]
-            src = {"conv": lv, "conv_down": lv - 1, "refine": lv + 1}[op["kind"]]
-            _, dW, db = levels[lv].conv_backward(levels[src], view(op["x"]), self.weights[op["w"]], view(op["src"]),
-                                                 relu=op["relu"], y=view(op["y"]) if op["relu"] else None,
-                                                 dx_out=view(op["dst"]))
-            outs[op["out"]] = dW.transpose(1, 2)          # taps x Cin x Cout, the workload's layout
-            outs["db:" + op["w"]] = db
-        else:
-            outs[op["out"]] = levels[0].splat_backward(view(op["src"]), normalize=bool(op["normalize"]),
-                                                       wsum=self._wsum[:levels[0].n])
 
     def finish_step(self, levels):
         """Release a step's lattices: at once, or (overlap) after the next
