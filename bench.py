@@ -33,7 +33,7 @@ FAMILIES = ["fill", "insert", "scan", "lists", "nbr", "splat", "distribute", "gr
 # the event timing, which names the outermost operator.
 FAMILY_KERNELS = {
     "fill": ["k_clear_table"], "insert": ["k_insert_points"], "scan": ["k_scan("],
-    "lists": ["k_fill_lists"], "nbr": ["k_neighbor_table", "k_coarse_tables", "k_mask_order"],
+    "lists": ["k_fill_lists"], "nbr": ["k_level_tables", "k_mask_order"],
     "deform_bwd": ["k_deform_bwd", "DeformGradRows"],
     "conv_bwd": ["k_conv_wgrad", "k_wgrad_reduce", "k_conv_bwd_prep"], "linear_bwd": ["k_lin_"],
     "splat_bwd": ["k_scale_by_weight_sum"], "groupnorm": ["k_gn_"],

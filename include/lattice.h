@@ -129,8 +129,11 @@ int lattice_coarsen_ex(lattice_t fine, int64_t capacity_hint, int flags, hipStre
  * positions divided by 2).  The results are those of that sequence of
  * calls; the device work is issued in fewer launches and in an order that
  * gives the host every level's vertex count sooner: the levels' tables are
- * cleared in one launch, the inserts run level after level, then the lists
- * and neighbour tables, with the row orders of all tables in one launch.
+ * cleared in one launch, the inserts of all levels run in one launch (each
+ * level elevates the positions and halves them l times, which gives the
+ * same floats as halving the finer level's), then the finest level's lists,
+ * the convolution tables of all levels in one launch and the row orders of
+ * all tables in one launch.
  * out must hold `levels` handles; on an error none is created.  Handles
  * are destroyed coarsest first, as for lattice_coarsen.
  */

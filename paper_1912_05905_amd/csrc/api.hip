@@ -521,24 +521,95 @@ int prepare_build(lattice_s* L, const lattice_s* parent, int64_t cap, hipStream_
   return LAT_OK;
 }
 
-int issue_insert(lattice_s* L, const float* pos, const float* y_src, float y_scale, const float a[3], hipStream_t s) {
-  launch_insert_points(pos, y_src, y_scale, a[0], a[1], a[2], L->m, L->hash(), &L->dc->counter, L->vkeys,
-                       L->vslot, L->slot, L->rank, L->w, L->y, &L->dc->err, L->host_counts_dev, L->stamp,
-                       L->counts_ready, s);
-  L->releases_at_insert = Pool::get().release_count(L->stream);
+// The insert of level L: from the positions (halved `halvings` times after
+// elevation) or from y_src times y_scale.
+InsertJob insert_job(const lattice_s* L, const float* pos, const float* y_src, float y_scale, int halvings,
+                     const float a[3]) {
+  InsertJob j{};
+  j.pos = pos;
+  j.y_in = y_src;
+  j.y_scale = y_scale;
+  j.halvings = halvings;
+  j.a0 = a[0];
+  j.a1 = a[1];
+  j.a2 = a[2];
+  j.h = L->hash();
+  j.counter = &L->dc->counter;
+  j.vkeys = L->vkeys;
+  j.vslot = L->vslot;
+  j.slot_out = L->slot;
+  j.rank_out = L->rank;
+  j.w_out = L->w;
+  j.y_out = L->y;
+  j.err = &L->dc->err;
+  j.host_counts = L->host_counts_dev;
+  j.stamp = L->stamp;
+  j.done = L->counts_ready;
+  return j;
+}
+
+// inserts of n levels of one cloud in one launch (each table cleared on s before)
+int issue_inserts(lattice_s* const* Ls, const InsertJob* jobs, int n, hipStream_t s) {
+  launch_insert_levels(jobs, n, Ls[0]->m, s);
+  for (int i = 0; i < n; ++i) {
+    Ls[i]->releases_at_insert = Pool::get().release_count(Ls[i]->stream);
+    Ls[i]->counts_known = false;
+  }
   HIP_TRY(hipGetLastError());
-  L->counts_known = false;
   return LAT_OK;
+}
+
+int issue_insert(lattice_s* L, const float* pos, const float* y_src, float y_scale, const float a[3], hipStream_t s) {
+  const InsertJob j = insert_job(L, pos, y_src, y_scale, 0, a);
+  return issue_inserts(&L, &j, 1, s);
+}
+
+// the point lists J_v, unless the level builds them on first use
+void issue_lists(lattice_s* L, hipStream_t s) {
+  L->lists_ready = !L->defer_lists;
+  if (!L->defer_lists) {
+    launch_count_scan(L->table, L->vslot, &L->dc->counter, L->offsets, L->scan_work, s);
+    launch_fill_lists(L->hash(), L->slot, L->rank, L->w, L->offsets, L->idx, L->entries, L->entry_w,
+                      L->chunk_first, L->chunk, L->total, s);
+  }
+}
+
+// level L's convolution tables (parent: the finer level, or null)
+TableJob table_job(const lattice_s* L, const lattice_s* parent, int64_t* work) {
+  TableJob j{};
+  j.h = L->hash();
+  j.keys = L->vkeys;
+  j.n_dev = &L->dc->counter;
+  j.nbr = L->nbr;
+  j.ld = L->nmax;
+  *work = L->nmax * kTaps;
+  if (parent) {
+    j.hf = parent->hash();
+    j.fkeys = parent->vkeys;
+    j.nf_dev = &parent->dc->counter;
+    j.down = L->down;
+    j.up = L->up;
+    j.ldf = parent->nmax;
+    *work = (2 * L->nmax + parent->nmax) * kTaps;
+  }
+  return j;
+}
+
+// the row orders of level L's tables, added to b (launched first when b is full)
+void add_row_orders(RowOrderBatch& b, const lattice_s* L, const lattice_s* parent, hipStream_t s) {
+  if (b.n + (parent ? 3 : 1) > kMaxRowOrderJobs) {
+    launch_row_orders(b, nullptr, s);
+    b = RowOrderBatch{};
+  }
+  const int32_t* n_dev = &L->dc->counter;
+  if (parent) b.add(RowOrderJob{L->up, parent->nmax, &parent->dc->counter, L->up_rows}, parent->nmax);
+  b.add(RowOrderJob{L->nbr, L->nmax, n_dev, L->nbr_rows}, L->nmax);
+  if (parent) b.add(RowOrderJob{L->down, L->nmax, n_dev, L->down_rows}, L->nmax);
 }
 
 void issue_tables(lattice_s* L, const lattice_s* parent, hipEvent_t built, hipStream_t s, RowOrderBatch* defer) {
   const int32_t* n_dev = &L->dc->counter;
-  L->lists_ready = !L->defer_lists;
-  if (!L->defer_lists) {
-    launch_count_scan(L->table, L->vslot, n_dev, L->offsets, L->scan_work, s);
-    launch_fill_lists(L->hash(), L->slot, L->rank, L->w, L->offsets, L->idx, L->entries, L->entry_w,
-                      L->chunk_first, L->chunk, L->total, s);
-  }
+  issue_lists(L, s);
   if (parent)
     launch_coarse_tables(L->hash(), parent->hash(), L->vkeys, parent->vkeys, n_dev, &parent->dc->counter, L->nmax,
                          parent->nmax, L->nbr, L->down, L->up, L->up_rows, L->nbr_rows, L->down_rows, built, s,
@@ -973,7 +1044,6 @@ int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float
   for (int j = 0; j < kDim; ++j)
     a[j] = static_cast<float>(sc / (static_cast<double>(sigma_host[j]) *
                                     std::sqrt(static_cast<double>((j + 1) * (j + 2)))));
-  const float a0[kDim] = {0.f, 0.f, 0.f};
   lattice_s* Ls[kMaxClearJobs] = {};
   auto discard = [&](int st) {
     for (int l = levels - 1; l >= 0; --l) {
@@ -1002,25 +1072,27 @@ int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float
     if ((st = prepare_build(L, parent, initial_capacity(L, parent, 0), stream)) != LAT_OK) return discard(st);
   }
   if (m > 0) {
-    // the levels' tables cleared in one launch, the inserts in level order
-    // (a level's insert reads the finer level's elevated positions), then
-    // the lists and tables, their row orders batched
+    // the levels' tables cleared in one launch, the inserts of all levels in
+    // one launch (each level elevates the positions itself), the finest
+    // level's lists, the convolution tables of all levels in one launch and
+    // their row orders batched
     ClearJob jobs[kMaxClearJobs];
     for (int l = 0; l < levels; ++l) jobs[l] = ClearJob{Ls[l]->table, Ls[l]->cap, Ls[l]->dc, Ls[l]->scan_work};
     launch_clear_tables(jobs, levels, stream);
-    for (int l = 0; l < levels; ++l)
-      if ((st = issue_insert(Ls[l], l ? nullptr : pos_dev, l ? Ls[l - 1]->y : nullptr, 0.5f, l ? a0 : a,
-                             stream)) != LAT_OK)
-        return discard(st);
-    RowOrderBatch batch;
+    InsertJob ins[kMaxClearJobs];
+    for (int l = 0; l < levels; ++l) ins[l] = insert_job(Ls[l], pos_dev, nullptr, 1.0f, l, a);
+    if ((st = issue_inserts(Ls, ins, levels, stream)) != LAT_OK) return discard(st);
+    for (int l = 0; l < levels; ++l) issue_lists(Ls[l], stream);  // coarse levels: on first use
+    TableJob tables[kMaxClearJobs];
+    int64_t work_max = 0;
     for (int l = 0; l < levels; ++l) {
-      const int jobs_here = l ? 3 : 1;
-      if (batch.n + jobs_here > kMaxRowOrderJobs) {
-        launch_row_orders(batch, nullptr, stream);
-        batch = RowOrderBatch{};
-      }
-      issue_tables(Ls[l], l ? Ls[l - 1] : nullptr, nullptr, stream, &batch);
+      int64_t work = 0;
+      tables[l] = table_job(Ls[l], l ? Ls[l - 1] : nullptr, &work);
+      work_max = std::max(work_max, work);
     }
+    launch_level_tables(tables, levels, work_max, stream);
+    RowOrderBatch batch;
+    for (int l = 0; l < levels; ++l) add_row_orders(batch, Ls[l], l ? Ls[l - 1] : nullptr, stream);
     launch_row_orders(batch, nullptr, stream);
     if ((st = check_launch("lattice hierarchy build")) != LAT_OK) return discard(st);
   }

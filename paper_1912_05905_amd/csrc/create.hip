@@ -96,13 +96,19 @@ __device__ inline int32_t block_exclusive_sum(int32_t v, int32_t* lds4, int32_t*
 // that vertex's point list, the weights and the elevated position.  Per new
 // vertex: vals[slot] = vertex number, vkeys / vslot by vertex number.
 // The slot's count ends as the number of references of the vertex.
+// Several levels of one cloud go in one launch, blockIdx.y picking the
+// level: a level elevated from the positions and halved l times holds the
+// same floats as one halved from its parent's stored elevated positions, so
+// no level waits for another.
+struct InsertJobs {
+  InsertJob job[kMaxClearJobs];
+};
+
 __global__ void __launch_bounds__(kBlock)
-k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, float y_scale,
-                float a0, float a1, float a2, int64_t m, HashView h, int32_t* counter,
-                uint64_t* __restrict__ vkeys,
-                int32_t* __restrict__ vslot, int4* __restrict__ slot_out, int4* __restrict__ rank_out,
-                float4* __restrict__ w_out, float4* __restrict__ y_out, uint32_t* err,
-                int32_t* __restrict__ host_counts, uint32_t stamp) {
+k_insert_points(InsertJobs jobs, int64_t m) {
+  const InsertJob& J = jobs.job[blockIdx.y];
+  const HashView h = J.h;
+  uint32_t* const err = J.err;
   __shared__ uint64_t lkey[kLdsSlots];
   __shared__ int32_t lcount[kLdsSlots];
   __shared__ int32_t lslot[kLdsSlots];
@@ -123,14 +129,15 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
   bool raised = false;  // this thread set an error bit
   float y[kVerts] = {0.f, 0.f, 0.f, 0.f};
   if (live) {
-    if (pos != nullptr) {
+    if (J.pos != nullptr) {
+      const float* __restrict__ pos = J.pos;
       const float g0 = pos[3 * p + 0], g1 = pos[3 * p + 1], g2 = pos[3 * p + 2];
       if (!isfinite(g0) || !isfinite(g1) || !isfinite(g2)) {
         atomicOr(err, kErrNonFinite);
         raised = true;
         live = false;
       } else {
-        const float t0 = g0 * a0, t1 = g1 * a1, t2 = g2 * a2;
+        const float t0 = g0 * J.a0, t1 = g1 * J.a1, t2 = g2 * J.a2;
         float run = 0.0f;
         const float m3 = 3.0f * t2;
         y[3] = run - m3;
@@ -142,15 +149,18 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
         y[1] = run - m1;
         run = run + t0;
         y[0] = run;
+        for (int l = 0; l < J.halvings; ++l)
+#pragma unroll
+          for (int i = 0; i < kVerts; ++i) y[i] = y[i] * 0.5f;
       }
     } else {
-      const float4 v = y_in[p];
-      y[0] = v.x * y_scale;
-      y[1] = v.y * y_scale;
-      y[2] = v.z * y_scale;
-      y[3] = v.w * y_scale;
+      const float4 v = reinterpret_cast<const float4*>(J.y_in)[p];
+      y[0] = v.x * J.y_scale;
+      y[1] = v.y * J.y_scale;
+      y[2] = v.z * J.y_scale;
+      y[3] = v.w * J.y_scale;
     }
-    if (y_out) y_out[p] = make_float4(y[0], y[1], y[2], y[3]);
+    if (J.y_out) reinterpret_cast<float4*>(J.y_out)[p] = make_float4(y[0], y[1], y[2], y[3]);
   }
   if (live) {
     bool ok = true;
@@ -314,15 +324,16 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
   // workgroup.
   if (tid == 0) {
     const unsigned long long old =
-        __hip_atomic_fetch_add(reinterpret_cast<unsigned long long*>(counter),
+        __hip_atomic_fetch_add(reinterpret_cast<unsigned long long*>(J.counter),
                                (1ull << 32) | static_cast<uint32_t>(nblock), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
     id_base = static_cast<int32_t>(old & 0xffffffffull);
     if ((old >> 32) == gridDim.x - 1) {
+      int32_t* const host_counts = J.host_counts;
       host_counts[0] = id_base + nblock;
       host_counts[1] = static_cast<int32_t>(__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
       __threadfence_system();
-      host_counts[2] = static_cast<int32_t>(stamp);  // the build this readback belongs to
+      host_counts[2] = static_cast<int32_t>(J.stamp);  // the build this readback belongs to
       __threadfence_system();
     }
   }
@@ -336,8 +347,8 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
     }
     if (!(created_mask & (1u << j))) continue;
     h.e[gsl[j]].val = id;
-    vkeys[id] = ukey[j];
-    vslot[id] = gsl[j];
+    J.vkeys[id] = ukey[j];
+    J.vslot[id] = gsl[j];
     ++id;
   }
   __syncthreads();
@@ -350,9 +361,9 @@ k_insert_points(const float* __restrict__ pos, const float4* __restrict__ y_in, 
       so[k] = lsl[k] >= 0 ? lslot[lsl[k]] : -1;
       ro[k] = lsl[k] >= 0 ? lbase[lsl[k]] + lrank[k] : 0;
     }
-    slot_out[p] = make_int4(so[0], so[1], so[2], so[3]);
-    rank_out[p] = make_int4(ro[0], ro[1], ro[2], ro[3]);
-    w_out[p] = make_float4(b[0], b[1], b[2], b[3]);
+    reinterpret_cast<int4*>(J.slot_out)[p] = make_int4(so[0], so[1], so[2], so[3]);
+    reinterpret_cast<int4*>(J.rank_out)[p] = make_int4(ro[0], ro[1], ro[2], ro[3]);
+    reinterpret_cast<float4*>(J.w_out)[p] = make_float4(b[0], b[1], b[2], b[3]);
   }
 
 }
@@ -479,46 +490,39 @@ __device__ inline int32_t up_entry(const HashView& coarse, uint64_t key, int t) 
   return k == kEmptyKey ? -1 : hash_find(coarse, k);
 }
 
-// Same-level table of the finest level, tap-major (nbr[t * ldn + v]).
-__global__ void __launch_bounds__(kBlock)
-k_neighbor_table(HashView h, const uint64_t* __restrict__ vkeys, const int32_t* __restrict__ n_dev,
-                 int32_t* __restrict__ nbr, int64_t ldn) {
-  const int64_t n = *n_dev;
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n * kTaps;
-       i += static_cast<int64_t>(gridDim.x) * kBlock) {
-    const int t = static_cast<int>(i / n);
-    const int64_t v = i - static_cast<int64_t>(t) * n;
-    nbr[static_cast<int64_t>(t) * ldn + v] = t == 0 ? static_cast<int32_t>(v) : same_level_entry(h, vkeys[v], t);
-  }
-}
+// Convolution tables of one or several levels (blockIdx.y picks the level),
+// tap-major (table[t * ld + v]): the same-level table (9 entries per vertex),
+// and for a coarse level its Downsample table (9 per coarse vertex) and the
+// Upsample table from it into the finer level (9 per fine vertex).  Vertex
+// counts come from device memory.
+struct TableJobs {
+  TableJob job[kMaxClearJobs];
+};
 
-// The three tables of a coarse level in one launch: its same-level table
-// and its Downsample table (9 entries per coarse vertex) and the Upsample
-// table from it into the fine level (9 entries per fine vertex).  Both
-// vertex counts come from device memory.
 __global__ void __launch_bounds__(kBlock)
-k_coarse_tables(HashView hc, HashView hf, const uint64_t* __restrict__ ckeys, const uint64_t* __restrict__ fkeys,
-                const int32_t* __restrict__ nc_dev, const int32_t* __restrict__ nf_dev, int32_t* __restrict__ nbr,
-                int32_t* __restrict__ down, int64_t ldc, int32_t* __restrict__ up, int64_t ldf) {
-  const int64_t nc = *nc_dev, nf = *nf_dev;
+k_level_tables(TableJobs jobs) {
+  const TableJob& J = jobs.job[blockIdx.y];
+  const int64_t nc = *J.n_dev;
+  const int64_t nf = J.up ? *J.nf_dev : 0;
   const int64_t per_c = nc * kTaps;
-  const int64_t total = 2 * per_c + nf * kTaps;
+  const int64_t total = J.up ? 2 * per_c + nf * kTaps : per_c;
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < total;
        i += static_cast<int64_t>(gridDim.x) * kBlock) {
     if (i < per_c) {
       const int t = static_cast<int>(i / nc);
       const int64_t v = i - static_cast<int64_t>(t) * nc;
-      nbr[static_cast<int64_t>(t) * ldc + v] = t == 0 ? static_cast<int32_t>(v) : same_level_entry(hc, ckeys[v], t);
+      J.nbr[static_cast<int64_t>(t) * J.ld + v] =
+          t == 0 ? static_cast<int32_t>(v) : same_level_entry(J.h, J.keys[v], t);
     } else if (i < 2 * per_c) {
       const int64_t k = i - per_c;
       const int t = static_cast<int>(k / nc);
       const int64_t v = k - static_cast<int64_t>(t) * nc;
-      down[static_cast<int64_t>(t) * ldc + v] = down_entry(hf, ckeys[v], t);
+      J.down[static_cast<int64_t>(t) * J.ld + v] = down_entry(J.hf, J.keys[v], t);
     } else {
       const int64_t k = i - 2 * per_c;
       const int t = static_cast<int>(k / nf);
       const int64_t v = k - static_cast<int64_t>(t) * nf;
-      up[static_cast<int64_t>(t) * ldf + v] = up_entry(hc, fkeys[v], t);
+      J.up[static_cast<int64_t>(t) * J.ldf + v] = up_entry(J.h, J.fkeys[v], t);
     }
   }
 }
@@ -650,21 +654,17 @@ void launch_clear_table(HashEntry* keys, int64_t cap, void* dev_counters, void* 
   launch_clear_tables(&job, 1, s);
 }
 
-void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
-                          float a2, int64_t m, HashView h, int32_t* counter,
-                          uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
-                          float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, uint32_t stamp,
-                          hipEvent_t done, hipStream_t s) {
-  if (m <= 0) {
-    (void)hipEventRecord(done, s);
-    return;
+void launch_insert_levels(const InsertJob* jobs, int n, int64_t m, hipStream_t s) {
+  if (n <= 0) return;
+  if (m > 0) {
+    InsertJobs all{};
+    for (int i = 0; i < n; ++i) all.job[i] = jobs[i];
+    ScopedKernelTimer tm("insert", s);
+    launch_signal(k_insert_points, dim3(blocks_for(m), n), dim3(kBlock), 0, s, jobs[0].done, all, m);
+  } else {
+    (void)hipEventRecord(jobs[0].done, s);
   }
-  ScopedKernelTimer tm("insert", s);
-  launch_signal(k_insert_points, dim3(blocks_for(m)), dim3(kBlock), 0, s, done, pos,
-                     reinterpret_cast<const float4*>(y_in), y_scale, a0, a1, a2, m, h, counter,
-                     vkeys, vslot, reinterpret_cast<int4*>(slot_out),
-                     reinterpret_cast<int4*>(rank_out), reinterpret_cast<float4*>(w_out),
-                     reinterpret_cast<float4*>(y_out), err, host_counts, stamp);
+  for (int i = 1; i < n; ++i) (void)hipEventRecord(jobs[i].done, s);
 }
 
 int64_t scan_workspace_bytes() { return kScanBlocks * sizeof(uint64_t); }
@@ -694,9 +694,13 @@ inline unsigned stride_grid(int64_t work) {
 void launch_neighbor_table(HashView h, const uint64_t* vkeys, const int32_t* n_dev, int64_t n_max,
                            int32_t* nbr, int64_t ldn, int32_t* nbr_rows, hipStream_t s, RowOrderBatch* defer) {
   if (n_max <= 0) return;
-  ScopedKernelTimer tm("nbr", s);
-  launch(k_neighbor_table, dim3(stride_grid(n_max * kTaps)), dim3(kBlock), 0, s, h, vkeys, n_dev,
-                     nbr, ldn);
+  TableJob j{};
+  j.h = h;
+  j.keys = vkeys;
+  j.n_dev = n_dev;
+  j.nbr = nbr;
+  j.ld = ldn;
+  launch_level_tables(&j, 1, n_max * kTaps, s);
   RowOrderBatch own;
   RowOrderBatch& b = defer ? *defer : own;
   b.add(RowOrderJob{nbr, ldn, n_dev, nbr_rows}, n_max);
@@ -711,9 +715,8 @@ void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse
     if (done) (void)hipEventRecord(done, s);
     return;
   }
-  ScopedKernelTimer tm("nbr", s);
-  launch(k_coarse_tables, dim3(stride_grid((2 * nc_max + nf_max) * kTaps)), dim3(kBlock), 0, s, coarse,
-                     fine, coarse_keys, fine_keys, nc_dev, nf_dev, nbr, down, nc_max, up, nf_max);
+  TableJob j{coarse, fine, coarse_keys, fine_keys, nc_dev, nf_dev, nbr, down, up, nc_max, nf_max};
+  launch_level_tables(&j, 1, (2 * nc_max + nf_max) * kTaps, s);
   // the rows of all three tables grouped by tap mask, in one launch (or in
   // the caller's batch)
   RowOrderBatch own;
@@ -722,6 +725,14 @@ void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse
   b.add(RowOrderJob{nbr, nc_max, nc_dev, nbr_rows}, nc_max);
   b.add(RowOrderJob{down, nc_max, nc_dev, down_rows}, nc_max);
   if (!defer) launch_row_orders(b, done, s);
+}
+
+void launch_level_tables(const TableJob* jobs, int n, int64_t work_max, hipStream_t s) {
+  if (n <= 0 || work_max <= 0) return;
+  TableJobs all{};
+  for (int i = 0; i < n; ++i) all.job[i] = jobs[i];
+  ScopedKernelTimer tm("nbr", s);
+  launch(k_level_tables, dim3(stride_grid(work_max), static_cast<unsigned>(n)), dim3(kBlock), 0, s, all);
 }
 
 void launch_row_orders(const RowOrderBatch& b, hipEvent_t done, hipStream_t s) {

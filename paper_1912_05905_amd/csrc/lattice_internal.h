@@ -157,6 +157,42 @@ struct ClearJob {
   void* scan_work;      // the level's scan status words (zeroed)
 };
 constexpr int kMaxClearJobs = 8;
+// One level's insert.  The elevated positions come from `pos` (m x 3) with
+// the factors a0..a2, then halved `halvings` times (a level that many steps
+// coarser than the finest), or, without `pos`, from y_in times y_scale.
+struct InsertJob {
+  const float* pos;
+  const float* y_in;
+  float y_scale;
+  int halvings;
+  float a0, a1, a2;
+  HashView h;
+  int32_t* counter;
+  uint64_t* vkeys;
+  int32_t* vslot;
+  int32_t* slot_out;
+  int32_t* rank_out;
+  float* w_out;
+  float* y_out;
+  uint32_t* err;
+  int32_t* host_counts;
+  uint32_t stamp;
+  hipEvent_t done;      // recorded once the insert has completed
+};
+// One level's convolution tables: the same-level table, and for a coarse
+// level its Downsample table and the Upsample table into the finer level.
+struct TableJob {
+  HashView h;            // the level's hash table
+  HashView hf;           // the finer level's (coarse levels)
+  const uint64_t* keys;  // the level's vertex keys
+  const uint64_t* fkeys; // the finer level's (coarse levels)
+  const int32_t* n_dev;  // the level's vertex count (device)
+  const int32_t* nf_dev; // the finer level's (coarse levels)
+  int32_t* nbr;          // same-level table, tap-major, row stride ld
+  int32_t* down;         // Downsample table, row stride ld (null for the finest level)
+  int32_t* up;           // Upsample table, row stride ldf (null for the finest level)
+  int64_t ld, ldf;
+};
 struct RowOrderJob {
   const int32_t* nbr;   // tap-major table, row stride ld
   int64_t ld;
@@ -182,11 +218,8 @@ struct RowOrderBatch {
 void launch_clear_table(HashEntry* entries, int64_t cap, void* dev_counters, void* scan_work,
                         hipStream_t s);
 void launch_clear_tables(const ClearJob* jobs, int n, hipStream_t s);
-void launch_insert_points(const float* pos, const float* y_in, float y_scale, float a0, float a1,
-                          float a2, int64_t m, HashView h, int32_t* counter,
-                          uint64_t* vkeys, int32_t* vslot, int32_t* slot_out, int32_t* rank_out,
-                          float* w_out, float* y_out, uint32_t* err, int32_t* host_counts, uint32_t stamp,
-                          hipEvent_t done, hipStream_t s);
+// the inserts of n levels of one cloud of m points in one launch
+void launch_insert_levels(const InsertJob* jobs, int n, int64_t m, hipStream_t s);
 int64_t scan_workspace_bytes();
 void launch_count_scan(const HashEntry* table, const int32_t* vslot, const int32_t* n_dev,
                        int32_t* offsets, void* work, hipStream_t s);
@@ -205,6 +238,9 @@ void launch_coarse_tables(HashView coarse, HashView fine, const uint64_t* coarse
                           hipEvent_t done, hipStream_t s, RowOrderBatch* defer = nullptr);
 // the batch's row orders in one launch (`done`, if given, bound to it)
 void launch_row_orders(const RowOrderBatch& b, hipEvent_t done, hipStream_t s);
+// the tables of n levels in one launch (row orders not included); work_max
+// bounds any job's (row, tap) entries
+void launch_level_tables(const TableJob* jobs, int n, int64_t work_max, hipStream_t s);
 void launch_export_keys(const uint64_t* vkeys, int64_t n, int32_t* out, hipStream_t s);
 // adds to *count the (row, tap) pairs of the first n rows whose entry is >= 0
 void launch_count_taps(const int32_t* tab, int64_t ld, int64_t n, unsigned long long* count, hipStream_t s);

@@ -46,9 +46,14 @@ class GpuPipeline:
     stream) may take steps in turn on compute streams of their own, so that
     consecutive clouds' operators overlap as well."""
 
-    def __init__(self, wl, overlap=False):
+    def __init__(self, wl, overlap=False, hierarchy=True):
         self.wl = wl
         self.overlap = overlap
+        # levels 0..L-1 created by one library call when the workload's
+        # builds are a create followed by coarsenings level by level
+        kinds = [(op["op"], op.get("level")) for op in wl.ops if op["op"] in ("create", "coarsen")]
+        chain = [("create", 0)] + [("coarsen", l) for l in range(1, len(kinds))]
+        self._levels = len(kinds) if hierarchy and kinds == chain else 0
         self._build_stream = torch.cuda.Stream() if overlap else None
         self._pending: list = []      # (levels, operators-done event) of finished steps
         self._ahead = None            # (levels, built event) of the next cloud
@@ -149,6 +154,11 @@ class GpuPipeline:
             return b[0] + c0 * es, b[1]
 
         def build(into, bstream=None):
+            if self._levels:
+                for lv, L in enumerate(Lattice.create_hierarchy(self.pos, self.sigma, self._levels,
+                                                                stream=bstream)):
+                    into[lv] = L
+                return
             for op in wl.ops:
                 if op["op"] == "create":
                     into[0] = Lattice.create(self.pos, self.sigma, stream=bstream)

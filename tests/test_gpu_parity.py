@@ -227,7 +227,8 @@ def _check_down_up(rng, g2o, levels_g, levels_o):
 @pytest.mark.parametrize("cfg,levels", [(2, 3), (4, 3), (4, 1)])
 def test_create_hierarchy(L, O, cfg, levels):
     """lattice_create_hierarchy (one call, tables cleared together, inserts
-    level after level, row orders batched) gives the lattices of create +
+    of all levels in one launch, tables in one launch, row orders batched)
+    gives the lattices of create +
     coarsen: every level bit-exact, the Downsample / Upsample tables through
     the strided and transposed convolutions, and a splat on the coarsest
     level (whose lists are built on first use)."""
