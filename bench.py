@@ -63,12 +63,27 @@ def family_of(kernel_name: str):
     return None
 
 
+def default_layout(wl) -> tuple:
+    """(pipelines, whether they share one build stream) that the bench runs
+    by default, from timings of every workload on MI355X.  More clouds in
+    flight help where one cloud's kernels (small levels, a few hundred
+    workgroups) cannot fill the GPU: the 120k-point LiDAR workloads run
+    three pipelines whose builds share one stream (four streams in all, one
+    per hardware queue).  A training step runs two pipelines with a build
+    stream each (three were slower), and so do the 200k-point rooms, whose
+    kernels are larger (three were slower on the single-level room).  The
+    1M-point clouds run two pipelines on a shared build stream."""
+    if wl.grads:
+        return 2, False
+    if wl.m < 150_000:
+        return 3, True
+    if wl.m < 500_000:
+        return 2, False
+    return 2, True
+
+
 def default_pipelines(wl) -> int:
-    """Pipelines the bench runs by default.  A second one helps where one
-    cloud's kernels (small levels, a few hundred workgroups) cannot fill the
-    GPU.  On the 1M-point clouds they do: a second pipeline gains 2-7% there
-    and doubles every launch's duration."""
-    return 2 if wl.m < 500_000 else 1
+    return default_layout(wl)[0]
 
 
 def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mb, steps, warmup, key, pipelines=2):
@@ -336,8 +351,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--streams", type=int, default=0,
-                    help="pipelines (each with a compute and a build stream) that take the clouds in turn; "
-                         "0: two below 500k points, else one")
+                    help="pipelines (each with a compute stream) that take the clouds in turn; 0: automatic")
+    ap.add_argument("--build", choices=("auto", "own", "shared"), default="auto",
+                    help="a build stream per pipeline (own) or one for all (shared); auto: as --streams 0")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="seconds of oracle work per CPU-baseline leg")
     ap.add_argument("--report", default=None, help="write a per-family timing report (JSON) here")
@@ -383,20 +399,24 @@ def main():
     lattice.lib()
     wl = configs.make(args.config)
     # Consecutive steps overlap.  `streams` pipelines take the clouds in
-    # turn, each with buffers and a build stream of its own: a pipeline
-    # builds its next cloud's lattices one step ahead on its build stream
-    # and runs its operators on its compute stream (the first one on the
-    # current stream), so that the small coarse levels' kernels (a few
-    # hundred workgroups each) and the latency-bound build chains share the
-    # GPU.  Two pipelines use four streams, one per hardware queue of the
-    # HIP runtime's default; a fifth stream would share a queue with another
-    # and serialise behind it.  Every step still does all of its work.
+    # turn, each with buffers of its own: a pipeline builds its next cloud's
+    # lattices one step ahead on a build stream (its own, or one the
+    # pipelines share) and runs its operators on its compute stream (the
+    # first one on the current stream), so that the small coarse levels'
+    # kernels (a few hundred workgroups each) and the latency-bound build
+    # chains share the GPU.  The layouts use at most four streams, one per
+    # hardware queue of the HIP runtime's default; a fifth stream would share
+    # a queue with another and serialise behind it.  Every step still does
+    # all of its work.
     if args.streams < 0:
         print("--streams must be 0 (automatic) or at least 1", file=sys.stderr)
         sys.exit(2)
+    layout = default_layout(wl)
     if args.streams == 0:
-        args.streams = default_pipelines(wl)
-    pipes = [GpuPipeline(wl, overlap=True) for _ in range(args.streams)]
+        args.streams = layout[0]
+    shared = layout[1] if args.build == "auto" else args.build == "shared"
+    build_stream = torch.cuda.Stream() if shared and args.streams > 1 else None
+    pipes = [GpuPipeline(wl, overlap=True, build_stream=build_stream) for _ in range(args.streams)]
     streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(args.streams - 1)]
     issued = [0]   # steps issued so far: step g runs on pipeline / stream g % streams
 
@@ -540,9 +560,10 @@ def main():
                    "distribute_gflop_per_step": mfma_flops["distribute"] / 1e9,
                    "conv_bwd_gflop_per_step": bwd_flops / 1e9,
                    "pipelines": args.streams,
+                   "build_streams": 1 if build_stream is not None else args.streams,
                    "steps_overlap": "pipelines take the clouds in turn, each building its next cloud's "
-                                    "lattices one step ahead on its own build stream while its operators "
-                                    "run on its own compute stream; every step does all of its work"},
+                                    "lattices one step ahead on a build stream while its operators run on "
+                                    "its own compute stream; every step does all of its work"},
         "timing": {"timed_ms": (t1 - t0) * 1e3, "windows": len(windows), "steps_per_window": win,
                    "ms_per_step_median_window": statistics.median(windows),
                    "ms_per_step_min_window": min(windows), "ms_per_step_max_window": max(windows)},

@@ -42,11 +42,12 @@ class GpuPipeline:
     pass of operators).  A step's lattices are destroyed by finish_step() one
     step later, once the build stream is ordered after the step's operators;
     flush() releases what is still held, the hierarchy built ahead
-    included.  Several pipelines (each with its own buffers and build
-    stream) may take steps in turn on compute streams of their own, so that
-    consecutive clouds' operators overlap as well."""
+    included.  Several pipelines (each with its own buffers, and a build
+    stream of its own or one they share, given as build_stream) may take
+    steps in turn on compute streams of their own, so that consecutive
+    clouds' operators overlap as well."""
 
-    def __init__(self, wl, overlap=False, hierarchy=True):
+    def __init__(self, wl, overlap=False, hierarchy=True, build_stream=None):
         self.wl = wl
         self.overlap = overlap
         # levels 0..L-1 created by one library call when the workload's
@@ -54,7 +55,10 @@ class GpuPipeline:
         kinds = [(op["op"], op.get("level")) for op in wl.ops if op["op"] in ("create", "coarsen")]
         chain = [("create", 0)] + [("coarsen", l) for l in range(1, len(kinds))]
         self._levels = len(kinds) if hierarchy and kinds == chain else 0
-        self._build_stream = torch.cuda.Stream() if overlap else None
+        if overlap:
+            self._build_stream = build_stream if build_stream is not None else torch.cuda.Stream()
+        else:
+            self._build_stream = None
         self._pending: list = []      # (levels, operators-done event) of finished steps
         self._ahead = None            # (levels, built event) of the next cloud
         self._events = [torch.cuda.Event() for _ in range(8)] if overlap else []

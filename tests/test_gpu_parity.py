@@ -246,6 +246,23 @@ def test_create_hierarchy(L, O, cfg, levels):
         g.destroy()
 
 
+def test_coarsen_after_hierarchy(L, O):
+    """A level coarsened from the coarsest level of a hierarchy starts from
+    the elevated positions that the one-launch insert stored for it (the
+    finest level's, halved once per level): bit-exact with the oracle's
+    third level."""
+    wl = configs.make(4)
+    gls = L.Lattice.create_hierarchy(_dev(wl.positions), wl.sigma, 2)
+    g2 = gls[1].coarsen()
+    ols = [O.Lattice.create(wl.positions, wl.sigma)]
+    for _ in range(2):
+        ols.append(ols[-1].coarsen())
+    _check_structure(g2, ols[2])
+    g2.destroy()
+    for g in reversed(gls):
+        g.destroy()
+
+
 def test_create_hierarchy_overflow_rebuild(L, O):
     """A hierarchy built in one call from points far apart on the lattice's
     scale: every level's first table overflows (nearly 4 vertices per
@@ -783,20 +800,22 @@ def test_pipeline_overlapped_steps(L, O):
     pipe.flush()
 
 
-def test_pipeline_steps_on_two_streams(L, O):
-    """Two pipelines, each with its own build stream, take steps in turn on
-    two compute streams (the current one and another) with no host
-    synchronisation between steps, as the bench runs them: consecutive
+@pytest.mark.parametrize("K,shared", [(2, False), (3, True)])
+def test_pipeline_steps_on_two_streams(L, O, K, shared):
+    """K pipelines, each with its own build stream or all sharing one, take
+    steps in turn on K compute streams (the current one and others) with no
+    host synchronisation between steps, as the bench runs them: consecutive
     clouds' builds and operators run side by side.  Every step's point
     outputs, copied on its own stream, match the oracle."""
     from paper_1912_05905_amd.pipeline import GpuPipeline
     wl = configs.make(4)
     _, _, oouts = OraclePipeline(wl).run()
-    pipes = [GpuPipeline(wl, overlap=True) for _ in range(2)]
-    streams = [torch.cuda.current_stream(), torch.cuda.Stream()]
+    bs = torch.cuda.Stream() if shared else None
+    pipes = [GpuPipeline(wl, overlap=True, build_stream=bs) for _ in range(K)]
+    streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(K - 1)]
     kept = []
-    for i in range(6):
-        k = i % 2
+    for i in range(2 * K + 2):
+        k = i % K
         with torch.cuda.stream(streams[k]):
             levels, _, outs = pipes[k].step()
             kept.append({name: outs[name].clone() for name in ("slice", "deform")})
