@@ -14,6 +14,7 @@ inside the timed region) and the CPU oracle's throughput on the host cores.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -460,6 +461,13 @@ def main():
     # throughput (median reported)
     win = max(1, args.steps // 20)
     marks = []
+    # Python's cyclic garbage collector is kept out of the timed regions (as
+    # timeit does): a full collection over the interpreter's objects (torch
+    # included) stalls the issuing thread for tens of milliseconds, which
+    # landed in some runs' timed region as +50% on the mean step time
+    gc.collect()
+    gc.freeze()
+    gc.disable()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -492,6 +500,8 @@ def main():
         one_step()
     torch.cuda.synchronize()
     t3 = time.perf_counter()
+    gc.enable()
+    gc.unfreeze()
     fam_timed = {f: lattice.timing_read(f) for f in timed}
     for f in timed:
         lattice.timing_enable(f, False)
@@ -566,7 +576,8 @@ def main():
                                     "its own compute stream; every step does all of its work"},
         "timing": {"timed_ms": (t1 - t0) * 1e3, "windows": len(windows), "steps_per_window": win,
                    "ms_per_step_median_window": statistics.median(windows),
-                   "ms_per_step_min_window": min(windows), "ms_per_step_max_window": max(windows)},
+                   "ms_per_step_min_window": min(windows), "ms_per_step_max_window": max(windows),
+                   "python_gc": "collected and frozen before the timed regions, disabled during them"},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -123,10 +123,16 @@ int lattice_coarsen_ex(lattice_t fine, int64_t capacity_hint, int flags, hipStre
 
 /*
  * A hierarchy of `levels` lattices (1 to 8) in one call, all built on
- * `stream`: out[0] as lattice_create with capacity_hint 0, out[l] as
- * lattice_coarsen_ex(out[l - 1], 0, LAT_ON_STREAM, stream, ...) for
+ * `stream`: out[0] as lattice_create with capacity_hint h[0], out[l] as
+ * lattice_coarsen_ex(out[l - 1], h[l], LAT_ON_STREAM, stream, ...) for
  * l >= 1 (Proposed Operations: each coarser level is the same points with
- * positions divided by 2).  The results are those of that sequence of
+ * positions divided by 2), where h = capacity_hints (`levels` values in
+ * host memory, or all 0 when capacity_hints is null; negative values count
+ * as 0).  A hint sizes its level's hash table as lattice_create's
+ * capacity_hint does (0 = automatic), except that a table that overflows is
+ * rebuilt at the worst-case size (as with hint 0) instead of failing.  A
+ * caller that builds clouds of similar sizes in turn can pass the last
+ * cloud's vertex counts: compact tables stay in the L2 caches.  The results are those of that sequence of
  * calls; the device work is issued in fewer launches and in an order that
  * gives the host every level's vertex count sooner: the levels' tables are
  * cleared in one launch, the inserts of all levels run in one launch (each
@@ -138,7 +144,7 @@ int lattice_coarsen_ex(lattice_t fine, int64_t capacity_hint, int flags, hipStre
  * are destroyed coarsest first, as for lattice_coarsen.
  */
 int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float* sigma_host, int levels,
-                             hipStream_t stream, lattice_t* out);
+                             const int64_t* capacity_hints, hipStream_t stream, lattice_t* out);
 
 /* Release a handle and its device memory (LAT_ELEVEL while it has children). */
 int lattice_destroy(lattice_t L);

@@ -1026,7 +1026,7 @@ int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_ho
 }
 
 int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float* sigma_host, int levels,
-                             hipStream_t stream, lattice_t* out) {
+                             const int64_t* capacity_hints, hipStream_t stream, lattice_t* out) {
   if (!out) return fail(LAT_EINVAL, "out is null");
   if (levels < 1 || levels > kMaxClearJobs)
     return fail(LAT_EINVAL, "levels must be 1 to " + std::to_string(kMaxClearJobs));
@@ -1069,7 +1069,8 @@ int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float
     if (parent) L->parent_generation = parent->generation;
     if (m == 0) continue;
     L->retry_cap = next_pow2(std::max<int64_t>(1024, 8 * m));
-    if ((st = prepare_build(L, parent, initial_capacity(L, parent, 0), stream)) != LAT_OK) return discard(st);
+    const int64_t hint = capacity_hints ? std::max<int64_t>(capacity_hints[l], 0) : 0;
+    if ((st = prepare_build(L, parent, initial_capacity(L, parent, hint), stream)) != LAT_OK) return discard(st);
   }
   if (m > 0) {
     // the levels' tables cleared in one launch, the inserts of all levels in

@@ -33,7 +33,7 @@ SIGNATURES = {
     "lattice_create": (_I32, [_P, _I64, _I32, _P, _I64, _P, C.POINTER(_P)]),
     "lattice_coarsen": (_I32, [_P, _I64, _P, C.POINTER(_P)]),
     "lattice_coarsen_ex": (_I32, [_P, _I64, _I32, _P, C.POINTER(_P)]),
-    "lattice_create_hierarchy": (_I32, [_P, _I64, _I32, _P, _I32, _P, C.POINTER(_P)]),
+    "lattice_create_hierarchy": (_I32, [_P, _I64, _I32, _P, _I32, _P, _P, C.POINTER(_P)]),
     "lattice_destroy": (_I32, [_P]),
     "lattice_num_vertices": (_I32, [_P, C.POINTER(_I64)]),
     "lattice_num_points": (_I32, [_P, C.POINTER(_I64)]),
@@ -181,15 +181,22 @@ class Lattice:
         return cls(h, m=pos.shape[0])
 
     @classmethod
-    def create_hierarchy(cls, pos: torch.Tensor, sigma, levels: int, stream=None) -> list:
+    def create_hierarchy(cls, pos: torch.Tensor, sigma, levels: int, stream=None, capacity_hints=None) -> list:
         """[level 0, level 1, ...]: create then levels - 1 coarsenings, all
-        built on the given (or current) stream in one library call."""
+        built on the given (or current) stream in one library call;
+        capacity_hints: expected vertex counts per level (0 = automatic)."""
         if pos.dtype != torch.float32 or pos.dim() != 2 or not pos.is_contiguous():
             raise ValueError("positions must be a contiguous m x d float32 tensor")
         sig = (C.c_float * pos.shape[1])(*[float(s) for s in sigma])
         hs = (C.c_void_p * max(int(levels), 1))()
+        hints = None
+        if capacity_hints is not None:
+            if len(capacity_hints) != int(levels):
+                raise ValueError("capacity_hints needs one value per level")
+            hints = (C.c_int64 * int(levels))(*[int(h) for h in capacity_hints])
         _check(lib().lattice_create_hierarchy(C.c_void_p(pos.data_ptr()), pos.shape[0], pos.shape[1], sig,
-                                              int(levels), _stream(stream), hs))
+                                              int(levels), C.cast(hints, _P) if hints is not None else None,
+                                              _stream(stream), hs))
         out = [cls(C.c_void_p(hs[0]), m=pos.shape[0])]
         for l in range(1, int(levels)):
             out.append(Lattice(C.c_void_p(hs[l]), parent=out[-1], m=pos.shape[0]))

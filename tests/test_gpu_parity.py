@@ -246,6 +246,25 @@ def test_create_hierarchy(L, O, cfg, levels):
         g.destroy()
 
 
+@pytest.mark.parametrize("hints", ["counts", "small"])
+def test_create_hierarchy_capacity_hints(L, O, hints):
+    """Hash tables sized from capacity hints: the vertex counts of the same
+    cloud (compact tables), or hints far too small, whose tables overflow and
+    are rebuilt; either way every level is bit-exact with the oracle."""
+    wl = configs.make(4)
+    ols = [O.Lattice.create(wl.positions, wl.sigma)]
+    for _ in range(2):
+        ols.append(ols[-1].coarsen())
+    h = [o.n for o in ols] if hints == "counts" else [5, 5, 5]
+    gls = L.Lattice.create_hierarchy(_dev(wl.positions), wl.sigma, 3, capacity_hints=h)
+    g2o = [_check_structure(g, o) for g, o in zip(gls, ols)]
+    _check_down_up(np.random.default_rng(41), g2o, gls, ols)
+    for g in reversed(gls):
+        g.destroy()
+    with pytest.raises(ValueError):
+        L.Lattice.create_hierarchy(_dev(wl.positions), wl.sigma, 3, capacity_hints=[0, 0])
+
+
 def test_coarsen_after_hierarchy(L, O):
     """A level coarsened from the coarsest level of a hierarchy starts from
     the elevated positions that the one-launch insert stored for it (the
