@@ -249,9 +249,12 @@ def algorithmic_bytes(wl, levels, family, pipe=None):
             tot += m * 32 + n * C * u + outs * m * C * 4 + (C * 4 if kind != "slice" else 0)
         return tot or None
     if family == "insert":
-        per_level = m * 12 + m * (16 + 16 + 16)       # positions in, y / slots / weights out
+        # per level: positions in, elevated positions / slots / weights out
+        # (the hierarchy call elevates the positions for every level; a level
+        # coarsened on its own reads its parent's elevated positions instead)
         nlev = len(levels)
-        return per_level + (nlev - 1) * (m * 16 + m * 48)
+        coarse_in = 12 if pipe is not None and getattr(pipe, "_levels", 0) else 16
+        return m * (12 + 48) + (nlev - 1) * m * (coarse_in + 48)
     return None
 
 
