@@ -780,6 +780,37 @@ def test_pipeline_config5_full_size_sampled(L, O):
     GpuPipeline.release(levels)
 
 
+def test_pipeline_config5_bench_layout(L, O):
+    """The 1M-point bf16 U-Net as the bench runs it (two pipelines whose
+    builds share one stream, steps on two compute streams with no host
+    synchronisation between them): every step's point outputs match those of
+    a step issued alone (whose operators the sampled full-size test checks
+    against the oracle), normwise at the bf16 tolerance (the steps build
+    their own lattices, so sums are taken in other orders before bf16
+    rounding)."""
+    from paper_1912_05905_amd.pipeline import GpuPipeline
+    wl = configs.make(5)
+    lv, _, ref = GpuPipeline(wl).step(keep=True)
+    ref = {k: _host(v) for k, v in ref.items()}
+    GpuPipeline.release(lv)
+    assert ref
+    bs = torch.cuda.Stream()
+    pipes = [GpuPipeline(wl, overlap=True, build_stream=bs) for _ in range(2)]
+    streams = [torch.cuda.current_stream(), torch.cuda.Stream()]
+    for i in range(4):
+        k = i % 2
+        with torch.cuda.stream(streams[k]):
+            levels, _, outs = pipes[k].step()
+            got = {n: outs[n].clone() for n in outs}
+            pipes[k].finish_step(levels)
+        torch.cuda.synchronize()
+        assert set(got) == set(ref)
+        for n, t in got.items():
+            P.assert_normwise(_host(t), ref[n], P.TOL_BF16, n)
+    for p in pipes:
+        p.flush()
+
+
 def test_latticenet_bf16_full_size_sampled(L, O):
     """The LatticeNet forward on the 1M-point room in bf16 (workload 10) at
     full size, operator by operator on the GPU's own inputs: the three-level
