@@ -544,13 +544,14 @@ InsertJob insert_job(const lattice_s* L, const float* pos, const float* y_src, f
   j.err = &L->dc->err;
   j.host_counts = L->host_counts_dev;
   j.stamp = L->stamp;
-  j.done = L->counts_ready;
   return j;
 }
 
 // inserts of n levels of one cloud in one launch (each table cleared on s before)
 int issue_inserts(lattice_s* const* Ls, const InsertJob* jobs, int n, hipStream_t s) {
-  launch_insert_levels(jobs, n, Ls[0]->m, s);
+  hipEvent_t done[kMaxLevels];
+  for (int i = 0; i < n; ++i) done[i] = Ls[i]->counts_ready;
+  launch_insert_levels(jobs, done, n, Ls[0]->m, s);
   for (int i = 0; i < n; ++i) {
     Ls[i]->releases_at_insert = Pool::get().release_count(Ls[i]->stream);
     Ls[i]->counts_known = false;
@@ -1028,8 +1029,8 @@ int lattice_create(const float* pos_dev, int64_t m, int d, const float* sigma_ho
 int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float* sigma_host, int levels,
                              const int64_t* capacity_hints, hipStream_t stream, lattice_t* out) {
   if (!out) return fail(LAT_EINVAL, "out is null");
-  if (levels < 1 || levels > kMaxClearJobs)
-    return fail(LAT_EINVAL, "levels must be 1 to " + std::to_string(kMaxClearJobs));
+  if (levels < 1 || levels > kMaxLevels)
+    return fail(LAT_EINVAL, "levels must be 1 to " + std::to_string(kMaxLevels));
   for (int l = 0; l < levels; ++l) out[l] = nullptr;
   if (d != kDim) return fail(LAT_EUNSUPPORTED, "only d = 3 is supported");
   if (m < 0) return fail(LAT_EINVAL, "m < 0");
@@ -1044,7 +1045,7 @@ int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float
   for (int j = 0; j < kDim; ++j)
     a[j] = static_cast<float>(sc / (static_cast<double>(sigma_host[j]) *
                                     std::sqrt(static_cast<double>((j + 1) * (j + 2)))));
-  lattice_s* Ls[kMaxClearJobs] = {};
+  lattice_s* Ls[kMaxLevels] = {};
   auto discard = [&](int st) {
     for (int l = levels - 1; l >= 0; --l) {
       if (!Ls[l]) continue;
@@ -1077,14 +1078,14 @@ int lattice_create_hierarchy(const float* pos_dev, int64_t m, int d, const float
     // one launch (each level elevates the positions itself), the finest
     // level's lists, the convolution tables of all levels in one launch and
     // their row orders batched
-    ClearJob jobs[kMaxClearJobs];
+    ClearJob jobs[kMaxLevels];
     for (int l = 0; l < levels; ++l) jobs[l] = ClearJob{Ls[l]->table, Ls[l]->cap, Ls[l]->dc, Ls[l]->scan_work};
     launch_clear_tables(jobs, levels, stream);
-    InsertJob ins[kMaxClearJobs];
+    InsertJob ins[kMaxLevels];
     for (int l = 0; l < levels; ++l) ins[l] = insert_job(Ls[l], pos_dev, nullptr, 1.0f, l, a);
     if ((st = issue_inserts(Ls, ins, levels, stream)) != LAT_OK) return discard(st);
     for (int l = 0; l < levels; ++l) issue_lists(Ls[l], stream);  // coarse levels: on first use
-    TableJob tables[kMaxClearJobs];
+    TableJob tables[kMaxLevels];
     int64_t work_max = 0;
     for (int l = 0; l < levels; ++l) {
       int64_t work = 0;

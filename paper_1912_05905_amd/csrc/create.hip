@@ -41,7 +41,7 @@ constexpr int kScanPer = 8;                   // consecutive vertices per thread
 // counters and scan status words for the builds that follow; several
 // tables in one launch: blockIdx.y picks one.
 struct ClearJobs {
-  ClearJob job[kMaxClearJobs];
+  ClearJob job[kMaxLevels];
 };
 
 __global__ void __launch_bounds__(kBlock)
@@ -101,7 +101,7 @@ __device__ inline int32_t block_exclusive_sum(int32_t v, int32_t* lds4, int32_t*
 // same floats as one halved from its parent's stored elevated positions, so
 // no level waits for another.
 struct InsertJobs {
-  InsertJob job[kMaxClearJobs];
+  InsertJob job[kMaxLevels];
 };
 
 __global__ void __launch_bounds__(kBlock)
@@ -496,7 +496,7 @@ __device__ inline int32_t up_entry(const HashView& coarse, uint64_t key, int t) 
 // Upsample table from it into the finer level (9 per fine vertex).  Vertex
 // counts come from device memory.
 struct TableJobs {
-  TableJob job[kMaxClearJobs];
+  TableJob job[kMaxLevels];
 };
 
 __global__ void __launch_bounds__(kBlock)
@@ -654,17 +654,17 @@ void launch_clear_table(HashEntry* keys, int64_t cap, void* dev_counters, void* 
   launch_clear_tables(&job, 1, s);
 }
 
-void launch_insert_levels(const InsertJob* jobs, int n, int64_t m, hipStream_t s) {
+void launch_insert_levels(const InsertJob* jobs, const hipEvent_t* done, int n, int64_t m, hipStream_t s) {
   if (n <= 0) return;
   if (m > 0) {
     InsertJobs all{};
     for (int i = 0; i < n; ++i) all.job[i] = jobs[i];
     ScopedKernelTimer tm("insert", s);
-    launch_signal(k_insert_points, dim3(blocks_for(m), n), dim3(kBlock), 0, s, jobs[0].done, all, m);
+    launch_signal(k_insert_points, dim3(blocks_for(m), n), dim3(kBlock), 0, s, done[0], all, m);
   } else {
-    (void)hipEventRecord(jobs[0].done, s);
+    (void)hipEventRecord(done[0], s);
   }
-  for (int i = 1; i < n; ++i) (void)hipEventRecord(jobs[i].done, s);
+  for (int i = 1; i < n; ++i) (void)hipEventRecord(done[i], s);
 }
 
 int64_t scan_workspace_bytes() { return kScanBlocks * sizeof(uint64_t); }

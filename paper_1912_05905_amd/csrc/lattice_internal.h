@@ -156,7 +156,7 @@ struct ClearJob {
   void* dev_counters;   // the level's device counters (zeroed)
   void* scan_work;      // the level's scan status words (zeroed)
 };
-constexpr int kMaxClearJobs = 8;
+constexpr int kMaxLevels = 8;   // levels of one hierarchy call (one launch job each)
 // One level's insert.  The elevated positions come from `pos` (m x 3) with
 // the factors a0..a2, then halved `halvings` times (a level that many steps
 // coarser than the finest), or, without `pos`, from y_in times y_scale.
@@ -177,7 +177,6 @@ struct InsertJob {
   uint32_t* err;
   int32_t* host_counts;
   uint32_t stamp;
-  hipEvent_t done;      // recorded once the insert has completed
 };
 // One level's convolution tables: the same-level table, and for a coarse
 // level its Downsample table and the Upsample table into the finer level.
@@ -218,8 +217,9 @@ struct RowOrderBatch {
 void launch_clear_table(HashEntry* entries, int64_t cap, void* dev_counters, void* scan_work,
                         hipStream_t s);
 void launch_clear_tables(const ClearJob* jobs, int n, hipStream_t s);
-// the inserts of n levels of one cloud of m points in one launch
-void launch_insert_levels(const InsertJob* jobs, int n, int64_t m, hipStream_t s);
+// the inserts of n levels of one cloud of m points in one launch; done[i]
+// is recorded once level i's insert has completed
+void launch_insert_levels(const InsertJob* jobs, const hipEvent_t* done, int n, int64_t m, hipStream_t s);
 int64_t scan_workspace_bytes();
 void launch_count_scan(const HashEntry* table, const int32_t* vslot, const int32_t* n_dev,
                        int32_t* offsets, void* work, hipStream_t s);
