@@ -68,15 +68,17 @@ def default_layout(wl) -> tuple:
     """(pipelines, whether they share one build stream) that the bench runs
     by default, from timings of every workload on MI355X.  More clouds in
     flight help where one cloud's kernels (small levels, a few hundred
-    workgroups) cannot fill the GPU: the 120k-point LiDAR workloads run
-    three pipelines whose builds share one stream (four streams in all, one
-    per hardware queue).  A training step runs two pipelines with a build
-    stream each (three were slower), and so do the 200k-point rooms, whose
-    kernels are larger (three were slower on the single-level room).  The
-    1M-point clouds run two pipelines on a shared build stream."""
+    workgroups) cannot fill the GPU: the 120k-point LiDAR workloads, and
+    the 200k-point room with coarse levels, run three pipelines whose builds
+    share one stream (four streams in all, one per hardware queue).  A
+    training step runs two pipelines with a build stream each (three were
+    slower), and so does the single-level 200k-point room, whose kernels
+    are larger (three were slower there).  The 1M-point clouds run two
+    pipelines on a shared build stream."""
+    levels = 1 + sum(op["op"] == "coarsen" for op in wl.ops)
     if wl.grads:
         return 2, False
-    if wl.m < 150_000:
+    if wl.m < 150_000 or (wl.m < 500_000 and levels > 1):
         return 3, True
     if wl.m < 500_000:
         return 2, False

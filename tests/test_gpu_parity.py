@@ -780,7 +780,7 @@ def test_pipeline_config5_full_size_sampled(L, O):
     GpuPipeline.release(levels)
 
 
-@pytest.mark.parametrize("cfg,K", [(5, 2), (10, 2), (6, 3), (8, 3)])
+@pytest.mark.parametrize("cfg,K", [(5, 2), (10, 2), (6, 3), (8, 3), (9, 3)])
 def test_pipeline_bench_layout(L, O, cfg, K):
     """Workloads as the bench runs them (K pipelines whose builds share one
     stream, steps on K compute streams with no host synchronisation between
