@@ -549,6 +549,9 @@ def main():
     roof["ms_per_step"] = dom_ms_step
     roof["ms_per_launch"] = dom_ms / max(launches, 1)
     roof["timed_region_ms_per_step"] = (t3 - t2) * 1e3 / args.steps
+    roof["launch_context"] = (f"durations of launches that share the GPU with the other {args.streams - 1} "
+                              "pipeline(s)' operators and with the lattice builds, as the step runs them"
+                              if args.streams > 1 else "durations of launches beside the next cloud's build")
     # the HBM-bound operators, each over its own launches in the same region
     hbm = {}
     for f in timed:
