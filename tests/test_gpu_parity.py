@@ -246,16 +246,17 @@ def test_create_hierarchy(L, O, cfg, levels):
         g.destroy()
 
 
-@pytest.mark.parametrize("hints", ["counts", "small"])
+@pytest.mark.parametrize("hints", ["counts", "small", "negative"])
 def test_create_hierarchy_capacity_hints(L, O, hints):
     """Hash tables sized from capacity hints: the vertex counts of the same
-    cloud (compact tables), or hints far too small, whose tables overflow and
-    are rebuilt; either way every level is bit-exact with the oracle."""
+    cloud (compact tables), hints far too small, whose tables overflow and
+    are rebuilt, or negative hints, which count as 0 (automatic); every
+    level is bit-exact with the oracle."""
     wl = configs.make(4)
     ols = [O.Lattice.create(wl.positions, wl.sigma)]
     for _ in range(2):
         ols.append(ols[-1].coarsen())
-    h = [o.n for o in ols] if hints == "counts" else [5, 5, 5]
+    h = {"counts": [o.n for o in ols], "small": [5, 5, 5], "negative": [-7, 0, -1]}[hints]
     gls = L.Lattice.create_hierarchy(_dev(wl.positions), wl.sigma, 3, capacity_hints=h)
     g2o = [_check_structure(g, o) for g, o in zip(gls, ols)]
     _check_down_up(np.random.default_rng(41), g2o, gls, ols)
@@ -335,10 +336,11 @@ def test_create_hierarchy_rejections(L):
     with pytest.raises(L.LatticeError) as e:
         L.Lattice.create_hierarchy(pos, [0.1, 0.0, 0.1], 2)
     assert e.value.status == -1   # LAT_EINVAL
-    empty = L.Lattice.create_hierarchy(torch.zeros((0, 3), device="cuda"), [0.1] * 3, 3)
-    assert [g.n for g in empty] == [0, 0, 0] and [g.level for g in empty] == [0, 1, 2]
-    for g in reversed(empty):
-        g.destroy()
+    for hints in (None, [10, 10, 10]):
+        empty = L.Lattice.create_hierarchy(torch.zeros((0, 3), device="cuda"), [0.1] * 3, 3, capacity_hints=hints)
+        assert [g.n for g in empty] == [0, 0, 0] and [g.level for g in empty] == [0, 1, 2]
+        for g in reversed(empty):
+            g.destroy()
 
 
 def test_host_validation_on_gpu(L):
