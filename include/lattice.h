@@ -132,8 +132,10 @@ int lattice_coarsen_ex(lattice_t fine, int64_t capacity_hint, int flags, hipStre
  * capacity_hint does (0 = automatic), except that a table that overflows is
  * rebuilt at the worst-case size (as with hint 0) instead of failing.  A
  * caller that builds clouds of similar sizes in turn can pass the last
- * cloud's vertex counts: compact tables stay in the L2 caches.  The results are those of that sequence of
- * calls; the device work is issued in fewer launches and in an order that
+ * cloud's vertex counts (smaller tables to clear and probe).  The lattices
+ * are those of that sequence of calls (the vertex sets and simplices do not
+ * depend on the table sizes); the device work is issued in fewer launches
+ * and in an order that
  * gives the host every level's vertex count sooner: the levels' tables are
  * cleared in one launch, the inserts of all levels run in one launch (each
  * level elevates the positions and halves them l times, which gives the
