@@ -514,6 +514,27 @@ def main():
         p.flush()
     launches, dom_ms = fam_timed[dominant]
 
+    # the dominant family once more on one pipeline (its launches beside the
+    # next cloud's build only), for the kernels' position without the other
+    # clouds' operators beside them; not part of the throughput
+    one_ms = None
+    if args.streams > 1:
+        solo = GpuPipeline(wl, overlap=True)
+        n_solo = min(args.steps, 100)
+        for _ in range(5):
+            levels_s, _, _ = solo.step()
+            solo.finish_step(levels_s)
+        torch.cuda.synchronize()
+        lattice.timing_enable(dominant, True)
+        for _ in range(n_solo):
+            levels_s, _, _ = solo.step()
+            solo.finish_step(levels_s)
+        torch.cuda.synchronize()
+        solo_launches, solo_ms = lattice.timing_read(dominant)
+        lattice.timing_enable(dominant, False)
+        solo.flush()
+        one_ms = solo_ms / n_solo
+
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = wl.m / (ms_per_step * 1e-3)
     dom_ms_step = dom_ms / args.steps
@@ -535,6 +556,10 @@ def main():
             roof["occupied_tap_fraction"] = occ_flops / flops
             roof["achieved_occupied"] = occ / 1e12
             roof["frac_occupied"] = occ / peak
+        if one_ms:
+            roof["one_pipeline"] = {"ms_per_step": one_ms, "frac": mfma_flops[dominant] / (one_ms * 1e-3) / peak}
+            if dominant == "conv" and occ_flops:
+                roof["one_pipeline"]["frac_occupied"] = occ_flops / (one_ms * 1e-3) / peak
     else:
         b = bytes_by_fam.get(dominant)
         achieved = (b / (dom_ms_step * 1e-3)) if b else None
