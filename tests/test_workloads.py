@@ -73,3 +73,15 @@ def test_config5_small_variant():
     wl = configs.config5(m=20_000)
     assert wl.dtype == "bf16" and wl.levels == 4
     assert np.array_equal(gen.bf16_bits_to_f32(gen.to_bf16_bits(wl.features)), wl.features)
+
+
+def test_bench_default_layout():
+    """The bench's pipeline layout per workload: three pipelines on one build
+    stream for the 120k-point LiDAR workloads and the multi-level 200k-point
+    LatticeNet, two with a build stream each for the single-level room and
+    the training step, two on one build stream for the 1M-point clouds."""
+    import bench
+    expect = {3: (2, False), 4: (3, True), 5: (2, True), 6: (3, True), 7: (2, False), 8: (3, True),
+              9: (3, True), 10: (2, True)}
+    for cfg, layout in expect.items():
+        assert bench.default_layout(configs.make(cfg)) == layout, cfg
